@@ -1,0 +1,319 @@
+"""Benchmark: UniQuan_F optimisation steps on one MI355X.
+
+A step is one pass of the whole hot path over one batch, for every
+(matrix, k) of the workload:
+    fq_fwd (transform, level table, nearest-level mapping, detransform)
+    -> reconstruction forward GEMM + loss (Et = What X^T - Yt, sum Et^2)
+    -> weight-gradient GEMM (dL/dWhat = 2 Et X)
+    -> fq_bwd (straight-through gradients of s, alpha, z_B)
+    -> SGD update of s, alpha, z_B
+with the mapping schedule of the paper's local and periodic mapping (p = 2:
+local remap on even steps, frozen codes otherwise; the initial full mapping
+is part of set-up).  Inputs are synthetic and resident in HBM before timing.
+
+Output: one JSON line.  ``value`` is the fake-quant fwd+bwd throughput in
+Gweights/s (weights quantized forward and backward per second of quantizer
+kernel time inside the timed steps); the reconstruction GEMM throughput is
+``gemm_tflops``.  Per-kernel averages come from HIP events recorded on the
+stream the kernels run on.  ``roofline`` describes the kernel with the largest
+share of step time; ``cpu_baseline`` times the CPU oracle on a bounded sample.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+PROFILES = os.path.join(ROOT, "profiles")
+CSRC = os.path.join(ROOT, "paper_2506_03781_amd", "csrc")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="attn4096")
+    ap.add_argument("--mode", default="paper", choices=["paper", "full", "local", "frozen"])
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="also run a plain 256 MiB device copy (counter calibration)")
+    return ap.parse_args()
+
+
+def src_hash() -> str:
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(CSRC)):
+        if f.endswith((".hip", ".h")):
+            h.update(open(os.path.join(CSRC, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def fq_bytes_per_weight(k, g, mode, w_bytes=2, what_bytes=2, grad_bytes=2):
+    """Algorithmic HBM bytes per weight: forward and backward quantizer."""
+    grp = (4 * k + 12) / g                      # alpha, z_B, Delta, z_U reads per group
+    fwd = w_bytes + 4 + what_bytes + 1 + (1 if mode != "full" else 0) + grp
+    bwd = grad_bytes + w_bytes + 4 + 1 + 4 + (4 * k + 12) / g   # G, W, s, code, grad_s; group reads+writes
+    return fwd, bwd
+
+
+def schedule(mode, step):
+    from paper_2506_03781_amd import uniquan as uq
+    if mode == "full":
+        return uq.MAP_FULL
+    if mode == "local":
+        return uq.MAP_LOCAL
+    if mode == "frozen":
+        return uq.MAP_FROZEN
+    return uq.MAP_LOCAL if step % 2 == 0 else uq.MAP_FROZEN
+
+
+def load_counters(workload):
+    """HBM traffic per launch from committed rocprofv3 counter runs, if they were
+    taken on the current kernel sources."""
+    path = os.path.join(PROFILES, f"pmc_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    d = json.load(open(path))
+    if d.get("src_hash") != src_hash():
+        return None
+    return d
+
+
+def cpu_baseline(layers_np, mode, budget_s=12.0):
+    """The oracle's fq_fwd + fq_bwd on a bounded row sample of each (matrix, k),
+    numpy restricted to one thread."""
+    from threadpoolctl import threadpool_limits
+    with threadpool_limits(1):
+        return _cpu_baseline(layers_np, mode, budget_s)
+
+
+def _cpu_baseline(layers_np, mode, budget_s):
+    import numpy as np
+    import oracle.uniquan as O
+    omode = {"full": O.MAP_FULL, "local": O.MAP_LOCAL, "frozen": O.MAP_FROZEN}.get(mode, O.MAP_LOCAL)
+    total_w, total_t = 0, 0.0
+    rows_used = []
+    per = budget_s / max(1, len(layers_np))
+    for (W, s, k, g) in layers_np:
+        R, C = W.shape
+        rows = 16
+        spent = 0.0
+        while True:
+            Wr, sr = W[:rows], s[:rows]
+            p = O.init_param_set_a(Wr, sr, k, g)
+            a, z = p["alpha"], p["z_b"]
+            prev = O.fq_fwd(Wr, sr, a, z, k, g)["codes"]
+            Gr = np.random.default_rng(0).standard_normal(Wr.shape).astype(np.float32)
+            t0 = time.perf_counter()
+            f = O.fq_fwd(Wr, sr, a, z, k, g, mode=omode, codes_prev=prev)
+            O.fq_bwd(Wr, sr, a, z, f["codes"], Gr, k, g)
+            dt = time.perf_counter() - t0
+            spent += dt
+            if spent >= per or rows >= R or dt > per / 3:
+                break
+            rows = min(R, rows * 2)
+        total_w += rows * C
+        total_t += dt
+        rows_used.append((rows, C, k))
+    sample = "; ".join(f"{r} rows x {c} cols at k={k}" for r, c, k in rows_used)
+    mname = "local" if mode == "paper" else mode
+    return {"value": total_w / total_t / 1e9, "unit": "Gweights/s", "cores": 1, "kind": "oracle",
+            "sample": f"oracle fq_fwd ({mname} mapping) + fq_bwd on the first rows of each matrix, "
+                      f"numpy on one thread: {sample}; {total_w} weights in {total_t:.2f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); this build has no multi-GPU path.",
+              file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2506_03781_amd import synth
+    from paper_2506_03781_amd import uniquan as uq
+    from paper_2506_03781_amd.layer import QuantLayer
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    uq.lib()
+    wl = synth.WORKLOADS[args.workload]
+    g = wl.group_size
+    layers = []
+    host_np = []
+    for spec in wl.matrices:
+        m = synth.make_matrix(spec, args.seed)
+        wdt = torch.bfloat16 if spec.dtype == "bf16" else torch.float32
+        for k in wl.ks:
+            lay = QuantLayer(m.W, m.X, m.s, k, g, w_dtype=wdt)
+            lay.init_greedy()
+            lay.prepare()
+            lay.fq_fwd(uq.MAP_FULL)        # initial mapping computes every distance
+            layers.append(lay)
+            if not args.no_cpu_baseline and len(host_np) < 2:
+                host_np.append((m.W, m.s, k, g))
+        del m
+    torch.cuda.synchronize()
+
+    phases = ["fq_fwd", "gemm_fwd", "gemm_bwd", "fq_bwd", "sgd"]
+    ev = {}
+
+    def run_step(step, timed):
+        mode = schedule(args.mode, step)
+        for li, lay in enumerate(layers):
+            es = [torch.cuda.Event(enable_timing=True) for _ in range(6)] if timed else None
+            if timed:
+                es[0].record()
+            lay.fq_fwd(mode)
+            if timed:
+                es[1].record()
+            lay.recon(backward=False)
+            if timed:
+                es[2].record()
+            uq.uniquan_layer_grad(lay.T, lay.R, lay.C, lay.Et, lay.Xt, lay.G)
+            if timed:
+                es[3].record()
+            lay.fq_bwd()
+            if timed:
+                es[4].record()
+            lay.sgd()
+            if timed:
+                es[5].record()
+                ev.setdefault(li, []).append(es)
+
+    for s in range(args.warmup):
+        run_step(s, False)
+    if args.calib_copy:
+        src = torch.empty(64 << 20, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        run_step(args.warmup + s, True)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+
+    # per-phase totals (ms per step) and per-launch averages
+    tot = {p: 0.0 for p in phases}
+    per_layer = []
+    for li, lay in enumerate(layers):
+        d = {p: 0.0 for p in phases}
+        for es in ev[li]:
+            for i, p in enumerate(phases):
+                d[p] += es[i].elapsed_time(es[i + 1])
+        for p in phases:
+            d[p] /= args.steps
+            tot[p] += d[p]
+        per_layer.append(d)
+
+    weights = sum(l.R * l.C for l in layers)
+    flops = sum(4.0 * l.T * l.R * l.C for l in layers)
+    fq_ms = tot["fq_fwd"] + tot["fq_bwd"]
+    gemm_ms = tot["gemm_fwd"] + tot["gemm_bwd"]
+    value = weights / (fq_ms * 1e-3) / 1e9
+    gemm_tflops = flops / (gemm_ms * 1e-3) / 1e12
+    mode0 = "local" if args.mode == "paper" else args.mode
+    fq_bytes = 0.0
+    for l in layers:
+        wb = 2 if l.W.dtype == torch.bfloat16 else 4
+        f, b = fq_bytes_per_weight(l.k, l.g, mode0, wb)
+        fq_bytes += (f + b) * l.R * l.C
+    fq_gbs = fq_bytes / (fq_ms * 1e-3) / 1e9
+
+    # per-kernel rooflines (averaged over the layers' launches)
+    def kernel_stats(phase):
+        n = len(layers)
+        dur_ms = tot[phase] / n
+        if phase in ("gemm_fwd", "gemm_bwd"):
+            work = sum(2.0 * l.T * l.R * l.C for l in layers) / n
+            ach = work / (dur_ms * 1e-3) / 1e12
+            return dict(bound="mfma", achieved=ach, peak=MFMA_BF16_PEAK_TFLOPS, unit="TFLOP/s",
+                        frac=ach / MFMA_BF16_PEAK_TFLOPS, avg_ms=dur_ms, algorithmic_flops=work)
+        byt = 0.0
+        for l in layers:
+            wb = 2 if l.W.dtype == torch.bfloat16 else 4
+            f, b = fq_bytes_per_weight(l.k, l.g, mode0, wb)
+            byt += (f if phase == "fq_fwd" else b) * l.R * l.C
+        byt /= n
+        ach = byt / (dur_ms * 1e-3) / 1e9
+        return dict(bound="hbm", achieved=ach, peak=HBM_PEAK_GBS, unit="GB/s", frac=ach / HBM_PEAK_GBS,
+                    avg_ms=dur_ms, algorithmic_bytes=byt)
+
+    ks = {p: kernel_stats(p) for p in ("fq_fwd", "gemm_fwd", "gemm_bwd", "fq_bwd")}
+    dom = max(ks, key=lambda p: ks[p]["avg_ms"])
+    counters = load_counters(args.workload)
+    for p, st in ks.items():
+        tr = None
+        if counters and p in counters.get("kernels", {}):
+            c = counters["kernels"][p]
+            tr = c.get("hbm_bytes_per_launch")
+        st["traffic"] = tr
+    roof = {k2: ks[dom][k2] for k2 in ("bound", "achieved", "peak", "unit", "frac", "traffic")}
+    roof["kernel"] = dom
+
+    # per-mode forward times (after the timed region)
+    by_mode = {}
+    for name, md in (("full", uq.MAP_FULL), ("local", uq.MAP_LOCAL), ("frozen", uq.MAP_FROZEN)):
+        lay = layers[0]
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        lay.fq_fwd(md)
+        a.record()
+        for _ in range(10):
+            lay.fq_fwd(md)
+        b.record()
+        torch.cuda.synchronize()
+        by_mode[name] = a.elapsed_time(b) / 10 * 1e3
+
+    out = {
+        "metric": "fake-quant fwd+bwd Gweights/s (%HBM peak); recon GEMM TFLOP/s (%MFMA)",
+        "value": value,
+        "unit": "Gweights/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "description": wl.description,
+                   "matrices": [[l.R, l.C] for l in layers], "T": layers[0].T, "k": [l.k for l in layers],
+                   "g": g, "mapping": args.mode, "seed": args.seed, "parallelism": "single GPU"},
+        "fq_hbm_gbs": fq_gbs,
+        "fq_frac_hbm": fq_gbs / HBM_PEAK_GBS,
+        "gemm_tflops": gemm_tflops,
+        "gemm_frac_mfma": gemm_tflops / MFMA_BF16_PEAK_TFLOPS,
+        "phase_ms_per_step": tot,
+        "per_layer_phase_ms": per_layer,
+        "kernels": ks,
+        "fq_fwd_us_by_mode": by_mode,
+        "roofline": roof,
+        "counters_src_hash": src_hash(),
+        "precision": "quantizer: fp32 arithmetic on bf16 W / fp32 s, bf16 What and dL/dWhat; "
+                     "GEMMs: bf16 MFMA with fp32 accumulation",
+    }
+    if not args.no_cpu_baseline and host_np:
+        out["cpu_baseline"] = cpu_baseline(host_np, args.mode)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,271 @@
+/*
+ * uniquan.h -- C ABI of the MI355X (gfx950) UniQuan_F fake-quant library.
+ *
+ * UniQuan_F (arXiv 2506.03781) quantizes each group of g weights of a weight
+ * matrix with the unified quantizer of Eq. (3):
+ *     what = D_R( M*_B( T_F(w) ) )
+ * T_F   flexible-mapping transform, Eq. (1):  wbar = w / (Delta * s * s_r) + z_U
+ * M*_B  nearest binary-coding level z_B + sum_i c_i alpha_i, c in {-1,+1}^k
+ *       (Sec. 2.3), with the local and periodic mapping of the appendix
+ *       algorithm "Local and periodic mapping"
+ * D_R   detransform:                          what = Delta * (wtilde - z_U)
+ * and trains Delta, z_U, s, s_r, alpha, z_B by straight-through
+ * backpropagation of the reconstruction loss ||X W^T - X What^T||_F^2
+ * (Algorithm 1), with the gradient filter of the appendix "Implementation
+ * details".  After training, Theorem 1 folds the parameters into plain
+ * binary-coding ones and Eq. (4) extracts the deployable codes.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Memory.   Every pointer is DEVICE memory owned by the caller.  The library
+ *           never allocates, frees or keeps a pointer after returning.
+ * Streams.  `stream` is a hipStream_t passed as void* (NULL = default
+ *           stream).  Calls only enqueue work and return; results are ready
+ *           when the stream reaches them.  Calls on one stream are ordered;
+ *           concurrent calls writing the same buffers race.
+ * Layout.   Weight-shaped arrays are [R x C] row-major (R output channels,
+ *           C input features).  A group is g contiguous weights of one row:
+ *           group id gid = r * (C / g) + c / g, Gn = R * C / g groups.
+ *           Per-group arrays are [Gn]; alpha is [Gn x k] with
+ *           alpha[gid * k + i] = alpha_{i+1}.
+ * Codes.    One byte per weight.  Bits 0..k-1 hold the binary code
+ *           (bit i set <=> c_{i+1} = +1); bit 7 holds the gradient-filter
+ *           mask m (1 = gradient kept).  Bits k..6 are zero on output and
+ *           ignored on input.
+ * Dtypes.   UQ_F32 = IEEE binary32, UQ_BF16 = bfloat16 (uint16 storage).
+ * Sizes.    R, C, T >= 1.  g is a power of two in [8, 512] dividing C.
+ *           1 <= k <= 7.  T (calibration tokens) is a multiple of 8.
+ * Alignment Per-weight arrays, X, Xt, Yt and workspaces: 16 bytes.
+ *           Per-group and per-row arrays: 4 bytes.
+ * Errors.   Every call returns a uq_status.  Arguments are checked on the
+ *           host before any HIP call: UQ_EINVAL for a bad size, pointer,
+ *           alignment or enum, UQ_EUNSUPPORTED for a valid but unsupported
+ *           shape; nothing is enqueued then.  UQ_EHIP reports a failed
+ *           launch.  uniquan_last_error() gives a text for the last failure
+ *           on the calling thread.  Device-data preconditions are NOT
+ *           checked: Delta, s, s_r > 0 and finite; W, X, alpha, z_B, z_U
+ *           finite.
+ * Numerics. Codes and masks are decided in IEEE binary32 with correctly
+ *           rounded division, no contraction and subnormals kept, in the
+ *           operation order stated at each entry point, so they are
+ *           reproducible bit for bit by any IEEE implementation.
+ */
+#ifndef UNIQUAN_H
+#define UNIQUAN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { UQ_OK = 0, UQ_EINVAL = 1, UQ_EUNSUPPORTED = 2, UQ_EHIP = 3 } uq_status;
+typedef enum { UQ_F32 = 0, UQ_BF16 = 1 } uq_dtype;
+typedef enum { UQ_MAP_FULL = 0, UQ_MAP_LOCAL = 1, UQ_MAP_FROZEN = 2 } uq_map_mode;
+
+#define UNIQUAN_ABI_VERSION 1
+
+/* ABI version of the loaded library (UNIQUAN_ABI_VERSION). */
+int uniquan_abi_version(void);
+
+/* Text describing the last non-OK status returned on this thread
+ * (thread-local, valid until the next call on the thread). */
+const char* uniquan_last_error(void);
+
+/*
+ * uniquan_fq_fwd -- quantizer forward Q*_{I_F}, Eq. (3).
+ *
+ * Per group: the 2^k levels q(b) = z_B + (+-alpha_1) + ... + (+-alpha_k)
+ * (sign + iff bit i of b is set), summed left to right in fp32, sorted
+ * ascending (equal values ordered by code).  Per weight:
+ *     den  = (Delta * s_r) * s ;  wbar = (w / den) + z_U          [Eq. (1)]
+ *     FULL   : the nearest sorted level; on equal distance the lower one
+ *     LOCAL  : the nearest of the previous code's sorted position d and its
+ *              neighbours max(d-1,0), min(d+1,2^k-1), lower one on ties
+ *              (appendix algorithm "Local and periodic mapping")
+ *     FROZEN : keep the previous code
+ *     distance = |fl(wbar - q)|;  wtilde = q(code)
+ *     m    = NOT(|fl(wbar - wtilde)| > tau),  tau = min_i |alpha_i|
+ *     what = Delta * (wtilde - z_U)                                [D_R]
+ * The level value is recomputed from the current alpha, z_B on every call;
+ * only the code is kept between calls.
+ *
+ * W       [R*C] w_dtype               in
+ * s       [R*C] fp32 element-wise scales (> 0)                      in
+ * s_r     [R] fp32 row-wise scales, or NULL for 1                   in
+ * delta   [Gn] fp32 (> 0), or NULL for 1                            in
+ * z_u     [Gn] fp32, or NULL for 0                                  in
+ * alpha   [Gn*k] fp32, z_b [Gn] fp32                                in
+ * mode    uq_map_mode
+ * codes   [R*C] uint8: previous codes in (LOCAL, FROZEN), new code|mask out
+ * W_hat   [R*C] w_hat_dtype (bf16 rounds to nearest even)           out
+ */
+uq_status uniquan_fq_fwd(int64_t R, int64_t C, int k, int g,
+                         const void* W, int w_dtype,
+                         const float* s, const float* s_r,
+                         const float* delta, const float* z_u,
+                         const float* alpha, const float* z_b,
+                         int mode, uint8_t* codes,
+                         void* W_hat, int w_hat_dtype,
+                         void* stream);
+
+/*
+ * uniquan_fq_bwd -- straight-through backward of uniquan_fq_fwd with the
+ * gradient filter (appendix "Implementation details": the mapping is
+ * treated as identity, d wtilde / d wbar := m, zero where |wbar - wtilde|
+ * exceeds tau = min alpha).  With G = dL/dWhat and g~ = Delta * G:
+ *     grad_alpha[gid, i] = sum_j g~_j c_{i+1}(code_j)
+ *     grad_z_b[gid]      = sum_j g~_j
+ *     grad_s_j           = -m_j g~_j (wbar_j - z_U) / s_j
+ *     grad_delta[gid]    = sum_j G_j ((wtilde_j - z_U) - m_j (wbar_j - z_U))
+ *     grad_z_u[gid]      = -Delta sum_j (1 - m_j) G_j
+ *     grad_s_r[r]        = -sum_{j in row r} m_j g~_j (wbar_j - z_U) / s_r
+ * Sums over a group and over a row run in a fixed order (bitwise
+ * reproducible run to run).
+ *
+ * W, s, s_r, delta, z_u, alpha, z_b  as for uniquan_fq_fwd           in
+ * codes       [R*C] code|mask bytes written by uniquan_fq_fwd        in
+ * grad_W_hat  [R*C] grad_dtype, dL/dWhat                            in
+ * grad_s      [R*C] fp32                                  out (required)
+ * grad_alpha  [Gn*k] fp32, grad_z_b [Gn] fp32             out (required)
+ * grad_delta, grad_z_u [Gn] fp32; grad_s_r [R] fp32   out, NULL = skipped
+ * group_ws    [Gn] fp32 workspace, required iff grad_s_r != NULL
+ */
+uq_status uniquan_fq_bwd(int64_t R, int64_t C, int k, int g,
+                         const void* W, int w_dtype,
+                         const float* s, const float* s_r,
+                         const float* delta, const float* z_u,
+                         const float* alpha, const float* z_b,
+                         const uint8_t* codes,
+                         const void* grad_W_hat, int grad_dtype,
+                         float* grad_s, float* grad_alpha, float* grad_z_b,
+                         float* grad_delta, float* grad_z_u, float* grad_s_r,
+                         float* group_ws,
+                         void* stream);
+
+/*
+ * uniquan_layer_target -- the fixed reconstruction target of one linear
+ * layer, Y = X W^T (Algorithm 1, output of the unquantized layer), stored
+ * transposed: Yt[r, t] = sum_c W[r, c] X[t, c], fp32 accumulation on bf16
+ * MFMA.  Computed once per layer.
+ *
+ * X  [T*C] bf16;  W [R*C] bf16;  Yt [R*T] fp32 out.
+ */
+uq_status uniquan_layer_target(int64_t T, int64_t R, int64_t C,
+                               const uint16_t* X, const uint16_t* W,
+                               float* Yt, void* stream);
+
+/*
+ * uniquan_transpose_bf16 -- out[c, r] = in[r, c] for a [rows x cols] bf16
+ * matrix (used once per layer to form Xt for the weight-gradient GEMM).
+ * rows and cols are multiples of 8.
+ */
+uq_status uniquan_transpose_bf16(int64_t rows, int64_t cols,
+                                 const uint16_t* in, uint16_t* out, void* stream);
+
+/* Number of fp32 loss partials uniquan_layer_recon needs for (T, R, C). */
+size_t uniquan_recon_ws(int64_t T, int64_t R, int64_t C);
+
+/*
+ * uniquan_layer_recon -- single-layer reconstruction loss of Algorithm 1
+ * (the quantized layer sees the same input, X_hat = X) and its weight
+ * gradient:
+ *     Et[r, t]   = sum_c What[r, c] X[t, c] - Yt[r, t]      (fp32, stored bf16)
+ *     loss       = sum_{r,t} Et[r, t]^2    (squared Frobenius norm, a sum)
+ *     grad_W_hat = 2 Et Xt^T,  i.e. grad[r, c] = 2 sum_t Et[r, t] X[t, c]
+ * Both contractions run on bf16 MFMA with fp32 accumulation.  The loss is
+ * reduced from per-workgroup fp32 partials in fp64 in a fixed order.
+ *
+ * X           [T*C] bf16                                          in
+ * Xt          [C*T] bf16 (transpose of X), NULL => forward only   in
+ * W_hat       [R*C] bf16 (uniquan_fq_fwd output)                  in
+ * Yt          [R*T] fp32 (uniquan_layer_target output)            in
+ * loss        [1] fp32                                            out
+ * Et_ws       [R*T] bf16 workspace; holds Et after the call      out
+ * partials_ws [partials_len] fp32, partials_len >= uniquan_recon_ws()
+ * grad_W_hat  [R*C] grad_dtype, NULL => forward only              out
+ */
+uq_status uniquan_layer_recon(int64_t T, int64_t R, int64_t C,
+                              const uint16_t* X, const uint16_t* Xt,
+                              const uint16_t* W_hat, const float* Yt,
+                              float* loss, uint16_t* Et_ws,
+                              float* partials_ws, size_t partials_len,
+                              void* grad_W_hat, int grad_dtype,
+                              void* stream);
+
+/*
+ * uniquan_layer_grad -- the weight-gradient half of uniquan_layer_recon on
+ * its own: grad_W_hat = 2 Et Xt^T, grad[r, c] = 2 sum_t Et[r, t] X[t, c]
+ * (bf16 MFMA, fp32 accumulation).  For callers that run the forward with
+ * grad_W_hat = NULL and the backward later on the same stream.
+ *
+ * Et [R*T] bf16 (left in Et_ws by uniquan_layer_recon); Xt [C*T] bf16;
+ * grad_W_hat [R*C] grad_dtype out.
+ */
+uq_status uniquan_layer_grad(int64_t T, int64_t R, int64_t C,
+                             const uint16_t* Et, const uint16_t* Xt,
+                             void* grad_W_hat, int grad_dtype, void* stream);
+
+/*
+ * uniquan_fold_to_bcq -- Theorem 1 and Eq. (4): plain binary-coding
+ * parameters that reproduce Delta * (C alpha + z_B - z_U) exactly in real
+ * arithmetic:
+ *     alpha_star = Delta * alpha,  z_star = Delta * (z_B - z_U)    (fp32)
+ * and the deployable codes (bit 7 clear):
+ *     code_src 0: FULL mapping of wbar = T_F(w) against the levels of
+ *                 (alpha, z_B) -- keeps the trained flexible mapping;
+ *     code_src 1: Eq. (4) as printed, FULL mapping of the raw w against
+ *                 the levels of (alpha_star, z_star).
+ * codes_out may be NULL (parameters only).
+ */
+uq_status uniquan_fold_to_bcq(int64_t R, int64_t C, int k, int g,
+                              const void* W, int w_dtype,
+                              const float* s, const float* s_r,
+                              const float* delta, const float* z_u,
+                              const float* alpha, const float* z_b,
+                              float* alpha_star, float* z_star,
+                              uint8_t* codes_out, int code_src,
+                              void* stream);
+
+/*
+ * uniquan_bcq_dequant -- binary-coding reconstruction R_B(C; Theta)
+ * = C alpha + z_B 1_g (Sec. 2.3), the deployed model's weights:
+ *     W_out[j] = z_b[gid] + sum_i (+-alpha[gid, i])   (fp32, left to right)
+ * codes [R*C] uint8 (bit 7 ignored); alpha [Gn*k]; z_b [Gn];
+ * W_out [R*C] out_dtype.
+ */
+uq_status uniquan_bcq_dequant(int64_t R, int64_t C, int k, int g,
+                              const uint8_t* codes, const float* alpha,
+                              const float* z_b, void* W_out, int out_dtype,
+                              void* stream);
+
+/*
+ * uniquan_init_greedy -- greedy binary-coding start of the appendix
+ * algorithm "General alternating update" (its first step): per group,
+ * r = wbar - z_B with wbar = T_F(w) as in uniquan_fq_fwd; then for
+ * i = 1..k: c_i = sign(r) (sign(0) = +1), alpha_i = mean_j |r_j|,
+ * r <- r - alpha_i c_i.  fp32 arithmetic; group sums in a fixed order.
+ *
+ * W, s, s_r, delta, z_u as for uniquan_fq_fwd; z_b [Gn] in;
+ * alpha [Gn*k] fp32 out.
+ */
+uq_status uniquan_init_greedy(int64_t R, int64_t C, int k, int g,
+                              const void* W, int w_dtype,
+                              const float* s, const float* s_r,
+                              const float* delta, const float* z_u,
+                              const float* z_b, float* alpha,
+                              void* stream);
+
+/*
+ * uniquan_sgd -- theta[i] -= lr * grad[i] for i < n (the stochastic
+ * gradient descent update of Algorithm 1, applied per parameter tensor).
+ * theta, grad fp32 [n].
+ */
+uq_status uniquan_sgd(int64_t n, float* theta, const float* grad, float lr, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* UNIQUAN_H */

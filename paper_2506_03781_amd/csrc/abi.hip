@@ -1,0 +1,217 @@
+// C ABI of the library (declared in include/uniquan.h): argument validation
+// on the host, before any HIP call, then the kernel launches.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "../../include/uniquan.h"
+#include "uq_launch.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+uq_status fail(uq_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+#define REQ_PTR(p, al)                                                                   \
+  do {                                                                                   \
+    if ((p) == nullptr) return fail(UQ_EINVAL, "%s: %s must not be NULL", fn, #p);       \
+    if (!aligned((p), (al))) return fail(UQ_EINVAL, "%s: %s must be %d-byte aligned", fn, #p, int(al)); \
+  } while (0)
+#define OPT_PTR(p, al)                                                                   \
+  do {                                                                                   \
+    if ((p) != nullptr && !aligned((p), (al)))                                           \
+      return fail(UQ_EINVAL, "%s: %s must be %d-byte aligned", fn, #p, int(al));         \
+  } while (0)
+
+bool is_dtype(int d) { return d == UQ_F32 || d == UQ_BF16; }
+
+// Shape rules shared by the per-weight entry points.
+uq_status check_quant_shape(const char* fn, int64_t R, int64_t C, int k, int g) {
+  if (R < 1 || C < 1) return fail(UQ_EINVAL, "%s: R=%lld and C=%lld must be >= 1", fn, (long long)R, (long long)C);
+  if (k < 1 || k > 7) return fail(UQ_EINVAL, "%s: k=%d must be in [1, 7]", fn, k);
+  if (g < 8 || (g & (g - 1)) != 0) return fail(UQ_EINVAL, "%s: g=%d must be a power of two >= 8", fn, g);
+  if (g > 512) return fail(UQ_EUNSUPPORTED, "%s: g=%d > 512 is not supported", fn, g);
+  if (C % g != 0) return fail(UQ_EINVAL, "%s: g=%d must divide C=%lld", fn, g, (long long)C);
+  if (R > (int64_t(1) << 40) / C) return fail(UQ_EUNSUPPORTED, "%s: R*C too large", fn);
+  if ((R * C) / g >= (int64_t(1) << 31)) return fail(UQ_EUNSUPPORTED, "%s: more than 2^31 groups", fn);
+  return UQ_OK;
+}
+
+uq_status hip_status(const char* fn, hipError_t e) {
+  if (e == hipSuccess) return UQ_OK;
+  return fail(UQ_EHIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
+}
+
+uq_status check_gemm_dims(const char* fn, int64_t T, int64_t R, int64_t C) {
+  if (T < 1 || R < 1 || C < 1) return fail(UQ_EINVAL, "%s: T, R, C must be >= 1", fn);
+  if (T % 8 != 0) return fail(UQ_EINVAL, "%s: T=%lld must be a multiple of 8", fn, (long long)T);
+  if (C % 8 != 0) return fail(UQ_EINVAL, "%s: C=%lld must be a multiple of 8", fn, (long long)C);
+  const int64_t lim = int64_t(1) << 31;
+  if (T >= lim || R >= lim || C >= lim || T * C >= (int64_t(1) << 40) || R * C >= (int64_t(1) << 40) ||
+      R * T >= (int64_t(1) << 40))
+    return fail(UQ_EUNSUPPORTED, "%s: shape too large", fn);
+  return UQ_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int uniquan_abi_version(void) { return UNIQUAN_ABI_VERSION; }
+
+const char* uniquan_last_error(void) { return g_err; }
+
+uq_status uniquan_fq_fwd(int64_t R, int64_t C, int k, int g, const void* W, int w_dtype, const float* s,
+                         const float* s_r, const float* delta, const float* z_u, const float* alpha,
+                         const float* z_b, int mode, uint8_t* codes, void* W_hat, int w_hat_dtype,
+                         void* stream) {
+  const char* fn = "uniquan_fq_fwd";
+  if (uq_status st = check_quant_shape(fn, R, C, k, g)) return st;
+  if (!is_dtype(w_dtype) || !is_dtype(w_hat_dtype)) return fail(UQ_EINVAL, "%s: bad dtype", fn);
+  if (mode < UQ_MAP_FULL || mode > UQ_MAP_FROZEN) return fail(UQ_EINVAL, "%s: bad mapping mode %d", fn, mode);
+  REQ_PTR(W, 16); REQ_PTR(s, 16); REQ_PTR(alpha, 4); REQ_PTR(z_b, 4); REQ_PTR(codes, 16); REQ_PTR(W_hat, 16);
+  OPT_PTR(s_r, 4); OPT_PTR(delta, 4); OPT_PTR(z_u, 4);
+  uq::FqFwdLaunch p{R, C, k, g, W, w_dtype, s, s_r, delta, z_u, alpha, z_b, mode, codes, W_hat, w_hat_dtype};
+  return hip_status(fn, uq::launch_fq_fwd(p, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uniquan_fq_bwd(int64_t R, int64_t C, int k, int g, const void* W, int w_dtype, const float* s,
+                         const float* s_r, const float* delta, const float* z_u, const float* alpha,
+                         const float* z_b, const uint8_t* codes, const void* grad_W_hat, int grad_dtype,
+                         float* grad_s, float* grad_alpha, float* grad_z_b, float* grad_delta, float* grad_z_u,
+                         float* grad_s_r, float* group_ws, void* stream) {
+  const char* fn = "uniquan_fq_bwd";
+  if (uq_status st = check_quant_shape(fn, R, C, k, g)) return st;
+  if (!is_dtype(w_dtype) || !is_dtype(grad_dtype)) return fail(UQ_EINVAL, "%s: bad dtype", fn);
+  REQ_PTR(W, 16); REQ_PTR(s, 16); REQ_PTR(alpha, 4); REQ_PTR(z_b, 4); REQ_PTR(codes, 16);
+  REQ_PTR(grad_W_hat, 16); REQ_PTR(grad_s, 16); REQ_PTR(grad_alpha, 4); REQ_PTR(grad_z_b, 4);
+  OPT_PTR(s_r, 4); OPT_PTR(delta, 4); OPT_PTR(z_u, 4);
+  OPT_PTR(grad_delta, 4); OPT_PTR(grad_z_u, 4); OPT_PTR(grad_s_r, 4);
+  if (grad_s_r != nullptr) REQ_PTR(group_ws, 4);
+  uq::FqBwdLaunch p{R, C, k, g, W, w_dtype, s, s_r, delta, z_u, alpha, z_b, codes, grad_W_hat, grad_dtype,
+                    grad_s, grad_alpha, grad_z_b, grad_delta, grad_z_u, grad_s_r, group_ws};
+  return hip_status(fn, uq::launch_fq_bwd(p, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uniquan_layer_target(int64_t T, int64_t R, int64_t C, const uint16_t* X, const uint16_t* W, float* Yt,
+                               void* stream) {
+  const char* fn = "uniquan_layer_target";
+  if (uq_status st = check_gemm_dims(fn, T, R, C)) return st;
+  REQ_PTR(X, 16); REQ_PTR(W, 16); REQ_PTR(Yt, 16);
+  uq::GemmLaunch q{W, X, R, T, C, uq::EPI_TARGET, nullptr, Yt, nullptr, 1.0f};
+  return hip_status(fn, uq::launch_gemm(q, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uniquan_transpose_bf16(int64_t rows, int64_t cols, const uint16_t* in, uint16_t* out, void* stream) {
+  const char* fn = "uniquan_transpose_bf16";
+  if (rows < 1 || cols < 1 || rows % 8 || cols % 8)
+    return fail(UQ_EINVAL, "%s: rows, cols must be positive multiples of 8", fn);
+  if (rows >= (int64_t(1) << 31) / 64 * 64 || cols >= (int64_t(1) << 31) / 64 * 64)
+    return fail(UQ_EUNSUPPORTED, "%s: shape too large", fn);
+  REQ_PTR(in, 16); REQ_PTR(out, 16);
+  return hip_status(fn, uq::launch_transpose(rows, cols, in, out, static_cast<hipStream_t>(stream)));
+}
+
+size_t uniquan_recon_ws(int64_t T, int64_t R, int64_t C) {
+  (void)C;
+  if (T < 1 || R < 1) return 0;
+  return uq::gemm_workgroups(R, T, uq::EPI_LOSS);
+}
+
+uq_status uniquan_layer_recon(int64_t T, int64_t R, int64_t C, const uint16_t* X, const uint16_t* Xt,
+                              const uint16_t* W_hat, const float* Yt, float* loss, uint16_t* Et_ws,
+                              float* partials_ws, size_t partials_len, void* grad_W_hat, int grad_dtype,
+                              void* stream) {
+  const char* fn = "uniquan_layer_recon";
+  if (uq_status st = check_gemm_dims(fn, T, R, C)) return st;
+  REQ_PTR(X, 16); REQ_PTR(W_hat, 16); REQ_PTR(Yt, 16); REQ_PTR(loss, 4); REQ_PTR(Et_ws, 16);
+  REQ_PTR(partials_ws, 16);
+  if (partials_len < uniquan_recon_ws(T, R, C))
+    return fail(UQ_EINVAL, "%s: partials_len=%zu < %zu", fn, partials_len, uniquan_recon_ws(T, R, C));
+  if (grad_W_hat != nullptr) {
+    REQ_PTR(Xt, 16);
+    REQ_PTR(grad_W_hat, 16);
+    if (!is_dtype(grad_dtype)) return fail(UQ_EINVAL, "%s: bad dtype", fn);
+  }
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  uq::GemmLaunch f{W_hat, X, R, T, C, uq::EPI_LOSS, Yt, Et_ws, partials_ws, 1.0f};
+  if (uq_status s = hip_status(fn, uq::launch_gemm(f, st))) return s;
+  if (uq_status s = hip_status(fn, uq::launch_reduce_loss(partials_ws, int64_t(uniquan_recon_ws(T, R, C)), loss, st)))
+    return s;
+  if (grad_W_hat == nullptr) return UQ_OK;
+  uq::GemmLaunch b{Et_ws, Xt, R, C, T, grad_dtype == UQ_BF16 ? uq::EPI_GRAD_BF16 : uq::EPI_GRAD_F32,
+                   nullptr, grad_W_hat, nullptr, 2.0f};
+  return hip_status(fn, uq::launch_gemm(b, st));
+}
+
+uq_status uniquan_layer_grad(int64_t T, int64_t R, int64_t C, const uint16_t* Et, const uint16_t* Xt,
+                             void* grad_W_hat, int grad_dtype, void* stream) {
+  const char* fn = "uniquan_layer_grad";
+  if (uq_status st = check_gemm_dims(fn, T, R, C)) return st;
+  REQ_PTR(Et, 16); REQ_PTR(Xt, 16); REQ_PTR(grad_W_hat, 16);
+  if (!is_dtype(grad_dtype)) return fail(UQ_EINVAL, "%s: bad dtype", fn);
+  uq::GemmLaunch b{Et, Xt, R, C, T, grad_dtype == UQ_BF16 ? uq::EPI_GRAD_BF16 : uq::EPI_GRAD_F32,
+                   nullptr, grad_W_hat, nullptr, 2.0f};
+  return hip_status(fn, uq::launch_gemm(b, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uniquan_fold_to_bcq(int64_t R, int64_t C, int k, int g, const void* W, int w_dtype, const float* s,
+                              const float* s_r, const float* delta, const float* z_u, const float* alpha,
+                              const float* z_b, float* alpha_star, float* z_star, uint8_t* codes_out,
+                              int code_src, void* stream) {
+  const char* fn = "uniquan_fold_to_bcq";
+  if (uq_status st = check_quant_shape(fn, R, C, k, g)) return st;
+  if (!is_dtype(w_dtype)) return fail(UQ_EINVAL, "%s: bad dtype", fn);
+  if (code_src != 0 && code_src != 1) return fail(UQ_EINVAL, "%s: code_src must be 0 or 1", fn);
+  REQ_PTR(alpha, 4); REQ_PTR(z_b, 4); REQ_PTR(alpha_star, 4); REQ_PTR(z_star, 4);
+  OPT_PTR(s_r, 4); OPT_PTR(delta, 4); OPT_PTR(z_u, 4);
+  if (codes_out != nullptr) {
+    REQ_PTR(codes_out, 16);
+    REQ_PTR(W, 16);
+    if (code_src == 0) REQ_PTR(s, 16);
+  }
+  uq::FoldLaunch p{R, C, k, g, W, w_dtype, s, s_r, delta, z_u, alpha, z_b, alpha_star, z_star, codes_out, code_src};
+  return hip_status(fn, uq::launch_fold(p, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uniquan_bcq_dequant(int64_t R, int64_t C, int k, int g, const uint8_t* codes, const float* alpha,
+                              const float* z_b, void* W_out, int out_dtype, void* stream) {
+  const char* fn = "uniquan_bcq_dequant";
+  if (uq_status st = check_quant_shape(fn, R, C, k, g)) return st;
+  if (!is_dtype(out_dtype)) return fail(UQ_EINVAL, "%s: bad dtype", fn);
+  REQ_PTR(codes, 16); REQ_PTR(alpha, 4); REQ_PTR(z_b, 4); REQ_PTR(W_out, 16);
+  uq::DequantLaunch p{R, C, k, g, codes, alpha, z_b, W_out, out_dtype};
+  return hip_status(fn, uq::launch_dequant(p, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uniquan_init_greedy(int64_t R, int64_t C, int k, int g, const void* W, int w_dtype, const float* s,
+                              const float* s_r, const float* delta, const float* z_u, const float* z_b,
+                              float* alpha, void* stream) {
+  const char* fn = "uniquan_init_greedy";
+  if (uq_status st = check_quant_shape(fn, R, C, k, g)) return st;
+  if (!is_dtype(w_dtype)) return fail(UQ_EINVAL, "%s: bad dtype", fn);
+  REQ_PTR(W, 16); REQ_PTR(s, 16); REQ_PTR(z_b, 4); REQ_PTR(alpha, 4);
+  OPT_PTR(s_r, 4); OPT_PTR(delta, 4); OPT_PTR(z_u, 4);
+  uq::GreedyLaunch p{R, C, k, g, W, w_dtype, s, s_r, delta, z_u, z_b, alpha};
+  return hip_status(fn, uq::launch_greedy(p, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uniquan_sgd(int64_t n, float* theta, const float* grad, float lr, void* stream) {
+  const char* fn = "uniquan_sgd";
+  if (n < 1) return fail(UQ_EINVAL, "%s: n must be >= 1", fn);
+  REQ_PTR(theta, 4); REQ_PTR(grad, 4);
+  return hip_status(fn, uq::launch_sgd(n, theta, grad, lr, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

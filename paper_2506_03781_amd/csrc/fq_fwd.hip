@@ -1,0 +1,371 @@
+// Quantizer forward Q*_{I_F} (Eq. (3)), the unification-theorem fold
+// (Theorem 1, Eq. (4)), binary-coding dequantization (Sec. 2.3) and the
+// greedy binary-coding start (appendix "General alternating update").
+//
+// Work split: a workgroup of 256 lanes owns one tile of whole groups; each
+// lane streams 8 consecutive weights (16-byte bf16 / 2x16-byte fp32 loads),
+// so a 128-weight group is 16 lanes.  The tile's level tables are built and
+// sorted in LDS once, then every lane maps its 8 weights with an LDS binary
+// search.  HBM-bound: per weight the forward reads W (2 B) and s (4 B) and
+// writes What (2 B) and the code byte (1 B).
+#include "uq_device.h"
+#include "uq_launch.h"
+
+namespace uq {
+
+struct TileGeom {
+  int64_t N;        // R * C
+  int logg;         // g = 1 << logg
+  int logL;         // L = 2^k
+  int k;
+  int gpr;          // groups per row
+  int tile_groups;  // groups per workgroup tile
+};
+
+__device__ __forceinline__ float tau_of(const float* __restrict__ alpha_g, int k) {
+  float t = fabsf(alpha_g[0]);
+  for (int i = 1; i < k; ++i) t = fminf(t, fabsf(alpha_g[i]));
+  return t;
+}
+
+struct FwdArgs {
+  TileGeom t;
+  const void* W;
+  const float* s;
+  const float* s_r;
+  const float* delta;
+  const float* z_u;
+  const float* alpha;
+  const float* z_b;
+  uint8_t* codes;
+  void* W_hat;
+};
+
+template <int WDT, int ODT, int MODE>
+__global__ __launch_bounds__(kThreads) void fq_fwd_kernel(FwdArgs a) {
+  __shared__ LevelTables tab;
+  __shared__ float s_ds[kMaxTileGroups], s_zu[kMaxTileGroups], s_dl[kMaxTileGroups], s_tau[kMaxTileGroups];
+  const TileGeom& g = a.t;
+  const int64_t Gn = g.N >> g.logg;
+  const int64_t gid0 = int64_t(blockIdx.x) * g.tile_groups;
+  const int ng = int(min<int64_t>(g.tile_groups, Gn - gid0));
+  const int lane_w = threadIdx.x * kVec;
+  const bool active = lane_w < (ng << g.logg);
+  const int64_t off = (gid0 << g.logg) + lane_w;
+
+  float w[8], sv[8];
+  uint2 prev = make_uint2(0u, 0u);
+  if (active) {
+    load8<WDT>(a.W, off, w);
+    load8f(a.s, off, sv);
+    if constexpr (MODE != 0) prev = load8u8(a.codes, off);
+  }
+  for (int gl = threadIdx.x; gl < ng; gl += blockDim.x) {
+    const int64_t gid = gid0 + gl;
+    const float dl = a.delta ? a.delta[gid] : 1.0f;
+    const float sr = a.s_r ? a.s_r[uint32_t(gid) / uint32_t(g.gpr)] : 1.0f;
+    s_ds[gl] = dl * sr;
+    s_dl[gl] = dl;
+    s_zu[gl] = a.z_u ? a.z_u[gid] : 0.0f;
+    s_tau[gl] = tau_of(a.alpha + gid * g.k, g.k);
+  }
+  build_tables(tab, a.alpha, a.z_b, gid0, ng, g.k, g.logL);
+  if (!active) return;
+
+  const int gl = lane_w >> g.logg;
+  const int L = 1 << g.logL;
+  const float ds = s_ds[gl], zu = s_zu[gl], dl = s_dl[gl], tau = s_tau[gl];
+  const float* q = tab.qs + (gl << g.logL);
+  const uint8_t* code_of = tab.code_of + (gl << g.logL);
+  const uint8_t* pos_of = tab.pos_of + (gl << g.logL);
+  float out[8];
+  uint32_t cw[2] = {0u, 0u};
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const float den = ds * sv[i];
+    const float wb = w[i] / den + zu;
+    float d;
+    int j;
+    if constexpr (MODE == 0) {
+      j = nearest_full(q, g.logL, wb, d);
+    } else {
+      const int p0 = pos_of[byte_of(prev, i) & uint32_t(L - 1)];
+      if constexpr (MODE == 1) {
+        j = nearest_local(q, L, p0, wb, d);
+      } else {
+        j = p0;
+        d = fabsf(wb - q[j]);
+      }
+    }
+    const float wt = q[j];
+    const uint32_t byte = uint32_t(code_of[j]) | (d > tau ? 0u : 0x80u);
+    cw[i >> 2] |= byte << (8 * (i & 3));
+    out[i] = dl * (wt - zu);
+  }
+  store8<ODT>(a.W_hat, off, out);
+  store8u8(a.codes, off, make_uint2(cw[0], cw[1]));
+}
+
+// ---------------------------------------------------------------------------
+// Fold (Theorem 1): alpha* = Delta alpha, z* = Delta (z_B - z_U); codes by
+// FULL mapping of wbar (code_src 0) or of the raw w against the folded
+// levels (code_src 1, Eq. (4) as printed).
+// ---------------------------------------------------------------------------
+struct FoldArgs {
+  TileGeom t;
+  const void* W;
+  const float* s;
+  const float* s_r;
+  const float* delta;
+  const float* z_u;
+  const float* alpha;
+  const float* z_b;
+  float* alpha_star;
+  float* z_star;
+  uint8_t* codes;
+  int code_src;
+};
+
+template <int WDT>
+__global__ __launch_bounds__(kThreads) void fold_kernel(FoldArgs a) {
+  __shared__ LevelTables tab;
+  __shared__ float s_ds[kMaxTileGroups], s_zu[kMaxTileGroups];
+  __shared__ float s_alpha[kMaxEntries];  // folded alpha (code_src 1)
+  __shared__ float s_zst[kMaxTileGroups];
+  const TileGeom& g = a.t;
+  const int64_t Gn = g.N >> g.logg;
+  const int64_t gid0 = int64_t(blockIdx.x) * g.tile_groups;
+  const int ng = int(min<int64_t>(g.tile_groups, Gn - gid0));
+  const int lane_w = threadIdx.x * kVec;
+  const bool active = a.codes != nullptr && lane_w < (ng << g.logg);
+  const int64_t off = (gid0 << g.logg) + lane_w;
+
+  for (int gl = threadIdx.x; gl < ng; gl += blockDim.x) {
+    const int64_t gid = gid0 + gl;
+    const float dl = a.delta ? a.delta[gid] : 1.0f;
+    const float zu = a.z_u ? a.z_u[gid] : 0.0f;
+    const float sr = a.s_r ? a.s_r[uint32_t(gid) / uint32_t(g.gpr)] : 1.0f;
+    const float zst = dl * (a.z_b[gid] - zu);
+    for (int i = 0; i < g.k; ++i) {
+      const float as = dl * a.alpha[gid * g.k + i];
+      a.alpha_star[gid * g.k + i] = as;
+      if (gl * g.k + i < kMaxEntries) s_alpha[gl * g.k + i] = as;
+    }
+    a.z_star[gid] = zst;
+    s_zst[gl] = zst;
+    s_ds[gl] = dl * sr;
+    s_zu[gl] = zu;
+  }
+  if (a.codes == nullptr) return;  // uniform across the grid
+  __syncthreads();
+  if (a.code_src == 0) {
+    build_tables(tab, a.alpha, a.z_b, gid0, ng, g.k, g.logL);
+  } else {
+    // folded levels from the LDS copies of alpha*, z* (tile_groups * k <= kMaxEntries)
+    const int L = 1 << g.logL;
+    const int n = ng << g.logL;
+    for (int e = threadIdx.x; e < n; e += blockDim.x) {
+      const int gl = e >> g.logL;
+      tab.raw[e] = level_value(s_alpha + gl * g.k, s_zst[gl], g.k, e & (L - 1));
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < n; e += blockDim.x) {
+      const int gl = e >> g.logL;
+      const int b = e & (L - 1);
+      const float* row = tab.raw + (gl << g.logL);
+      const float qv = row[b];
+      int rank = 0;
+      for (int b2 = 0; b2 < L; ++b2) rank += (row[b2] < qv) | ((row[b2] == qv) & (b2 < b));
+      tab.qs[(gl << g.logL) + rank] = qv;
+      tab.code_of[(gl << g.logL) + rank] = uint8_t(b);
+    }
+    __syncthreads();
+  }
+  if (!active) return;
+  const int glw = lane_w >> g.logg;
+  float w[8], sv[8];
+  load8<WDT>(a.W, off, w);
+  if (a.code_src == 0) load8f(a.s, off, sv);
+  const float* q = tab.qs + (glw << g.logL);
+  const uint8_t* code_of = tab.code_of + (glw << g.logL);
+  uint32_t cw[2] = {0u, 0u};
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    float x = w[i];
+    if (a.code_src == 0) {
+      const float den = s_ds[glw] * sv[i];
+      x = x / den + s_zu[glw];
+    }
+    float d;
+    const int j = nearest_full(q, g.logL, x, d);
+    cw[i >> 2] |= uint32_t(code_of[j]) << (8 * (i & 3));
+  }
+  store8u8(a.codes, off, make_uint2(cw[0], cw[1]));
+}
+
+// ---------------------------------------------------------------------------
+// Binary-coding dequantization R_B(C; Theta) = C alpha + z_B 1_g.
+// ---------------------------------------------------------------------------
+struct DequantArgs {
+  TileGeom t;
+  const uint8_t* codes;
+  const float* alpha;
+  const float* z_b;
+  void* W_out;
+};
+
+template <int ODT>
+__global__ __launch_bounds__(kThreads) void dequant_kernel(DequantArgs a) {
+  __shared__ float raw[kMaxEntries];
+  const TileGeom& g = a.t;
+  const int64_t Gn = g.N >> g.logg;
+  const int64_t gid0 = int64_t(blockIdx.x) * g.tile_groups;
+  const int ng = int(min<int64_t>(g.tile_groups, Gn - gid0));
+  const int L = 1 << g.logL;
+  for (int e = threadIdx.x; e < (ng << g.logL); e += blockDim.x) {
+    const int64_t gid = gid0 + (e >> g.logL);
+    raw[e] = level_value(a.alpha + gid * g.k, a.z_b[gid], g.k, e & (L - 1));
+  }
+  __syncthreads();
+  const int lane_w = threadIdx.x * kVec;
+  if (lane_w >= (ng << g.logg)) return;
+  const int64_t off = (gid0 << g.logg) + lane_w;
+  const uint2 cb = load8u8(a.codes, off);
+  const float* row = raw + ((lane_w >> g.logg) << g.logL);
+  float out[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) out[i] = row[byte_of(cb, i) & uint32_t(L - 1)];
+  store8<ODT>(a.W_out, off, out);
+}
+
+// ---------------------------------------------------------------------------
+// Greedy start: per group r = wbar - z_B; for each bit, c = sign(r),
+// alpha = mean |r|, r -= alpha c.  A group of g weights is g/8 lanes of one
+// wavefront; group sums use a fixed xor-butterfly order.
+// ---------------------------------------------------------------------------
+struct GreedyArgs {
+  TileGeom t;
+  const void* W;
+  const float* s;
+  const float* s_r;
+  const float* delta;
+  const float* z_u;
+  const float* z_b;
+  float* alpha;
+};
+
+template <int WDT>
+__global__ __launch_bounds__(kThreads) void greedy_kernel(GreedyArgs a) {
+  const TileGeom& g = a.t;
+  const int64_t chunk = int64_t(blockIdx.x) * kThreads + threadIdx.x;
+  const int64_t off = chunk * kVec;
+  const bool active = off < g.N;
+  const int lpg = 1 << (g.logg - 3);  // lanes per group (<= 64)
+  const int64_t gid = active ? (off >> g.logg) : 0;
+  float r[8];
+  if (active) {
+    float w[8], sv[8];
+    load8<WDT>(a.W, off, w);
+    load8f(a.s, off, sv);
+    const float dl = a.delta ? a.delta[gid] : 1.0f;
+    const float sr = a.s_r ? a.s_r[uint32_t(gid) / uint32_t(g.gpr)] : 1.0f;
+    const float zu = a.z_u ? a.z_u[gid] : 0.0f;
+    const float zb = a.z_b[gid];
+    const float ds = dl * sr;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) r[i] = (w[i] / (ds * sv[i]) + zu) - zb;
+  } else {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) r[i] = 0.0f;
+  }
+  const float inv_g = 1.0f / float(1 << g.logg);  // exact power of two
+  for (int b = 0; b < g.k; ++b) {
+    float acc = 0.0f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc += fabsf(r[i]);
+    for (int m = lpg >> 1; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, 64);
+    const float al = acc * inv_g;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) r[i] = r[i] >= 0.0f ? r[i] - al : r[i] + al;
+    if (active && (threadIdx.x & (lpg - 1)) == 0) a.alpha[gid * g.k + b] = al;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Launchers
+// ---------------------------------------------------------------------------
+static TileGeom make_geom(int64_t R, int64_t C, int k, int g) {
+  TileGeom t;
+  t.N = R * C;
+  t.logg = __builtin_ctz(unsigned(g));
+  t.logL = k;
+  t.k = k;
+  t.gpr = int(C / g);
+  int tg = kTile >> t.logg;
+  const int by_lds = kMaxEntries >> k;
+  if (tg > by_lds) tg = by_lds;
+  if (tg < 1) tg = 1;
+  t.tile_groups = tg;
+  return t;
+}
+
+static unsigned grid_of(const TileGeom& t) {
+  const int64_t Gn = t.N >> t.logg;
+  return unsigned((Gn + t.tile_groups - 1) / t.tile_groups);
+}
+
+hipError_t launch_fq_fwd(const FqFwdLaunch& p, hipStream_t st) {
+  FwdArgs a;
+  a.t = make_geom(p.R, p.C, p.k, p.g);
+  a.W = p.W; a.s = p.s; a.s_r = p.s_r; a.delta = p.delta; a.z_u = p.z_u;
+  a.alpha = p.alpha; a.z_b = p.z_b; a.codes = p.codes; a.W_hat = p.W_hat;
+  const dim3 grid(grid_of(a.t)), block(kThreads);
+#define UQ_FWD(WD, OD, MD) \
+  if (p.w_dtype == WD && p.w_hat_dtype == OD && p.mode == MD) { \
+    hipLaunchKernelGGL((fq_fwd_kernel<WD, OD, MD>), grid, block, 0, st, a); \
+    return hipGetLastError(); }
+  UQ_FWD(BF16, BF16, 0) UQ_FWD(BF16, BF16, 1) UQ_FWD(BF16, BF16, 2)
+  UQ_FWD(BF16, F32, 0) UQ_FWD(BF16, F32, 1) UQ_FWD(BF16, F32, 2)
+  UQ_FWD(F32, BF16, 0) UQ_FWD(F32, BF16, 1) UQ_FWD(F32, BF16, 2)
+  UQ_FWD(F32, F32, 0) UQ_FWD(F32, F32, 1) UQ_FWD(F32, F32, 2)
+#undef UQ_FWD
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_fold(const FoldLaunch& p, hipStream_t st) {
+  FoldArgs a;
+  a.t = make_geom(p.R, p.C, p.k, p.g);
+  // code_src 1 keeps alpha* of a tile in LDS: tile_groups * k entries
+  while (a.t.tile_groups * p.k > kMaxEntries && a.t.tile_groups > 1) a.t.tile_groups >>= 1;
+  a.W = p.W; a.s = p.s; a.s_r = p.s_r; a.delta = p.delta; a.z_u = p.z_u;
+  a.alpha = p.alpha; a.z_b = p.z_b; a.alpha_star = p.alpha_star; a.z_star = p.z_star;
+  a.codes = p.codes; a.code_src = p.code_src;
+  const dim3 grid(grid_of(a.t)), block(kThreads);
+  if (p.w_dtype == BF16) hipLaunchKernelGGL((fold_kernel<BF16>), grid, block, 0, st, a);
+  else hipLaunchKernelGGL((fold_kernel<F32>), grid, block, 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_dequant(const DequantLaunch& p, hipStream_t st) {
+  DequantArgs a;
+  a.t = make_geom(p.R, p.C, p.k, p.g);
+  a.codes = p.codes; a.alpha = p.alpha; a.z_b = p.z_b; a.W_out = p.W_out;
+  const dim3 grid(grid_of(a.t)), block(kThreads);
+  if (p.out_dtype == BF16) hipLaunchKernelGGL((dequant_kernel<BF16>), grid, block, 0, st, a);
+  else hipLaunchKernelGGL((dequant_kernel<F32>), grid, block, 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_greedy(const GreedyLaunch& p, hipStream_t st) {
+  GreedyArgs a;
+  a.t = make_geom(p.R, p.C, p.k, p.g);
+  a.W = p.W; a.s = p.s; a.s_r = p.s_r; a.delta = p.delta; a.z_u = p.z_u;
+  a.z_b = p.z_b; a.alpha = p.alpha;
+  const int64_t chunks = a.t.N / kVec;
+  const dim3 grid(unsigned((chunks + kThreads - 1) / kThreads)), block(kThreads);
+  if (p.w_dtype == BF16) hipLaunchKernelGGL((greedy_kernel<BF16>), grid, block, 0, st, a);
+  else hipLaunchKernelGGL((greedy_kernel<F32>), grid, block, 0, st, a);
+  return hipGetLastError();
+}
+
+}  // namespace uq

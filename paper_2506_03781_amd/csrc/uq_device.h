@@ -1,0 +1,176 @@
+// Device helpers shared by the quantizer kernels (forward, fold, dequant,
+// init): storage conversions, vector loads of 8 consecutive weights, the
+// per-group binary-coding level table kept in LDS and the nearest-level
+// searches.  gfx950 only.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace uq {
+
+constexpr int kThreads = 256;           // threads per quantizer workgroup
+constexpr int kVec = 8;                 // consecutive weights per lane
+constexpr int kTile = kThreads * kVec;  // weights per full tile
+constexpr int kMaxEntries = 2048;       // level-table entries per tile (LDS)
+constexpr int kMaxTileGroups = kTile / 8;
+
+enum DType : int { F32 = 0, BF16 = 1 };
+
+__device__ __forceinline__ float bf16_to_f32(uint32_t h16) { return __uint_as_float(h16 << 16); }
+
+// fp32 -> bf16, round to nearest, ties to even (inputs are finite).
+__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+// 8 consecutive weights starting at element `off` (16-byte aligned).
+template <int DT>
+__device__ __forceinline__ void load8(const void* base, int64_t off, float (&v)[8]) {
+  if constexpr (DT == BF16) {
+    const uint4 q = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(base) + off);
+    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[2 * i] = __uint_as_float(w[i] << 16);
+      v[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+    }
+  } else {
+    const float4* p = reinterpret_cast<const float4*>(static_cast<const float*>(base) + off);
+    const float4 a = p[0], b = p[1];
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+  }
+}
+
+__device__ __forceinline__ void load8f(const float* base, int64_t off, float (&v)[8]) {
+  load8<F32>(base, off, v);
+}
+
+template <int DT>
+__device__ __forceinline__ void store8(void* base, int64_t off, const float (&v)[8]) {
+  if constexpr (DT == BF16) {
+    uint4 q;
+    q.x = f32_to_bf16(v[0]) | (f32_to_bf16(v[1]) << 16);
+    q.y = f32_to_bf16(v[2]) | (f32_to_bf16(v[3]) << 16);
+    q.z = f32_to_bf16(v[4]) | (f32_to_bf16(v[5]) << 16);
+    q.w = f32_to_bf16(v[6]) | (f32_to_bf16(v[7]) << 16);
+    *reinterpret_cast<uint4*>(static_cast<uint16_t*>(base) + off) = q;
+  } else {
+    float4* p = reinterpret_cast<float4*>(static_cast<float*>(base) + off);
+    p[0] = make_float4(v[0], v[1], v[2], v[3]);
+    p[1] = make_float4(v[4], v[5], v[6], v[7]);
+  }
+}
+
+__device__ __forceinline__ void store8f(float* base, int64_t off, const float (&v)[8]) {
+  store8<F32>(base, off, v);
+}
+
+__device__ __forceinline__ uint2 load8u8(const uint8_t* base, int64_t off) {
+  return *reinterpret_cast<const uint2*>(base + off);
+}
+
+__device__ __forceinline__ void store8u8(uint8_t* base, int64_t off, uint2 v) {
+  *reinterpret_cast<uint2*>(base + off) = v;
+}
+
+__device__ __forceinline__ uint32_t byte_of(uint2 v, int i) {
+  return ((i < 4 ? v.x : v.y) >> (8 * (i & 3))) & 0xFFu;
+}
+
+// Level b of a group: z_B + (+-alpha_1) + ... + (+-alpha_k), fp32, left to
+// right; the sign of alpha_{i+1} is + iff bit i of b is set.
+__device__ __forceinline__ float level_value(const float* __restrict__ alpha_g, float zb, int k, int b) {
+  float q = zb;
+  for (int i = 0; i < k; ++i) {
+    const float a = alpha_g[i];
+    q = ((b >> i) & 1) ? q + a : q - a;
+  }
+  return q;
+}
+
+// Per-tile level tables in LDS.  A tile covers `ng` consecutive groups,
+// table of group gl occupies entries [gl*L, (gl+1)*L).
+struct LevelTables {
+  float raw[kMaxEntries];        // q(b), unsorted
+  float qs[kMaxEntries];         // sorted ascending
+  uint8_t code_of[kMaxEntries];  // code at sorted position
+  uint8_t pos_of[kMaxEntries];   // sorted position of code
+};
+
+// Build the sorted tables of groups gid0 .. gid0+ng-1.  All threads of the
+// block take part; ends with a block barrier.  Sort key: (value, code).
+__device__ __forceinline__ void build_tables(LevelTables& t, const float* __restrict__ alpha,
+                                             const float* __restrict__ z_b, int64_t gid0, int ng,
+                                             int k, int logL) {
+  const int L = 1 << logL;
+  const int n = ng << logL;
+  for (int e = threadIdx.x; e < n; e += blockDim.x) {
+    const int gl = e >> logL;
+    const int b = e & (L - 1);
+    const int64_t gid = gid0 + gl;
+    t.raw[e] = level_value(alpha + gid * k, z_b[gid], k, b);
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < n; e += blockDim.x) {
+    const int gl = e >> logL;
+    const int b = e & (L - 1);
+    const float* row = t.raw + (gl << logL);
+    const float q = row[b];
+    int rank = 0;
+    for (int b2 = 0; b2 < L; ++b2) {
+      const float q2 = row[b2];
+      rank += (q2 < q) | ((q2 == q) & (b2 < b));
+    }
+    t.qs[(gl << logL) + rank] = q;
+    t.code_of[(gl << logL) + rank] = uint8_t(b);
+    t.pos_of[(gl << logL) + b] = uint8_t(rank);
+  }
+  __syncthreads();
+}
+
+// Nearest sorted level of x among q[0..L-1] (ascending).  Returns the first
+// position with the smallest |fl(x - q_j)|, i.e. the lower level on ties.
+// Since rounding is monotone, |fl(x - q_j)| is non-increasing up to the last
+// level <= x and non-decreasing after it, so the minimum sits at the bracket
+// {a, b} found by binary search; a run of equal distances ending at a is
+// walked back to its first element (duplicate levels, or levels closer than
+// the distance's ulp).
+__device__ __forceinline__ int nearest_full(const float* __restrict__ q, int logL, float x, float& dist) {
+  int pos = 0;  // number of levels <= x among q[0 .. L-2]
+  for (int step = (1 << logL) >> 1; step >= 1; step >>= 1)
+    pos += (q[pos + step - 1] <= x) ? step : 0;
+  const int a = pos > 0 ? pos - 1 : 0;
+  const int b = pos;
+  const float da = fabsf(x - q[a]);
+  const float db = fabsf(x - q[b]);
+  if (db < da) {
+    dist = db;
+    return b;
+  }
+  int j = a;
+  if (a > 0 && fabsf(x - q[a - 1]) == da) {
+    j = 0;
+    while (j < a && fabsf(x - q[j]) != da) ++j;
+  }
+  dist = da;
+  return j;
+}
+
+// Local mapping: first nearest of {max(d-1,0), d, min(d+1,L-1)}.
+__device__ __forceinline__ int nearest_local(const float* __restrict__ q, int L, int d, float x, float& dist) {
+  const int l = d > 0 ? d - 1 : 0;
+  const int r = d < L - 1 ? d + 1 : L - 1;
+  int best = l;
+  float bd = fabsf(x - q[l]);
+  const float dm = fabsf(x - q[d]);
+  if (dm < bd) { best = d; bd = dm; }
+  const float dr = fabsf(x - q[r]);
+  if (dr < bd) { best = r; bd = dr; }
+  dist = bd;
+  return best;
+}
+
+}  // namespace uq

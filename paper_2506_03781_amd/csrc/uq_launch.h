@@ -1,0 +1,88 @@
+// Internal launch interface between the C-ABI layer (abi.hip) and the
+// kernel files.  Arguments are already validated when these are called.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace uq {
+
+struct FqFwdLaunch {
+  int64_t R, C;
+  int k, g;
+  const void* W; int w_dtype;
+  const float* s; const float* s_r; const float* delta; const float* z_u;
+  const float* alpha; const float* z_b;
+  int mode;
+  uint8_t* codes;
+  void* W_hat; int w_hat_dtype;
+};
+
+struct FqBwdLaunch {
+  int64_t R, C;
+  int k, g;
+  const void* W; int w_dtype;
+  const float* s; const float* s_r; const float* delta; const float* z_u;
+  const float* alpha; const float* z_b;
+  const uint8_t* codes;
+  const void* grad_W_hat; int grad_dtype;
+  float* grad_s; float* grad_alpha; float* grad_z_b;
+  float* grad_delta; float* grad_z_u; float* grad_s_r; float* group_ws;
+};
+
+struct FoldLaunch {
+  int64_t R, C;
+  int k, g;
+  const void* W; int w_dtype;
+  const float* s; const float* s_r; const float* delta; const float* z_u;
+  const float* alpha; const float* z_b;
+  float* alpha_star; float* z_star; uint8_t* codes; int code_src;
+};
+
+struct DequantLaunch {
+  int64_t R, C;
+  int k, g;
+  const uint8_t* codes; const float* alpha; const float* z_b;
+  void* W_out; int out_dtype;
+};
+
+struct GreedyLaunch {
+  int64_t R, C;
+  int k, g;
+  const void* W; int w_dtype;
+  const float* s; const float* s_r; const float* delta; const float* z_u;
+  const float* z_b; float* alpha;
+};
+
+// GEMM epilogues of the reconstruction contractions.
+enum GemmEpi : int {
+  EPI_TARGET = 0,     // out fp32 = acc
+  EPI_LOSS = 1,       // e = acc - Yt; out bf16 = e; partial sum of e^2 per workgroup
+  EPI_GRAD_BF16 = 2,  // out bf16 = scale * acc
+  EPI_GRAD_F32 = 3,   // out fp32 = scale * acc
+};
+
+struct GemmLaunch {
+  // C[M x N] = A[M x K] * B[N x K]^T, bf16 operands with K contiguous.
+  const uint16_t* A; const uint16_t* B;
+  int64_t M, N, K;
+  int epi;
+  const float* Yt;     // EPI_LOSS
+  void* out;
+  float* partials;     // EPI_LOSS, one per workgroup
+  float scale;
+};
+
+hipError_t launch_fq_fwd(const FqFwdLaunch& p, hipStream_t st);
+hipError_t launch_fq_bwd(const FqBwdLaunch& p, hipStream_t st);
+hipError_t launch_fold(const FoldLaunch& p, hipStream_t st);
+hipError_t launch_dequant(const DequantLaunch& p, hipStream_t st);
+hipError_t launch_greedy(const GreedyLaunch& p, hipStream_t st);
+hipError_t launch_gemm(const GemmLaunch& p, hipStream_t st);
+size_t gemm_workgroups(int64_t M, int64_t N, int epi);
+hipError_t launch_reduce_loss(const float* partials, int64_t n, float* loss, hipStream_t st);
+hipError_t launch_transpose(int64_t rows, int64_t cols, const uint16_t* in, uint16_t* out, hipStream_t st);
+hipError_t launch_sgd(int64_t n, float* theta, const float* grad, float lr, hipStream_t st);
+
+}  // namespace uq

@@ -1,0 +1,203 @@
+"""Python binding of libuniquan.so (ctypes).
+
+Argument marshalling only: every function passes torch tensors' device
+pointers, sizes and the current HIP stream to the C entry point of the same
+name and raises ``UniquanError`` on a non-OK status.  All arithmetic runs in
+the library's HIP kernels; there is no fallback path.  The binding also
+checks what the C ABI cannot: that each tensor is a contiguous device tensor
+of the expected dtype with at least the number of elements the call touches.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libuniquan.so")
+HEADER = os.path.join(os.path.dirname(HERE), "include", "uniquan.h")
+
+UQ_OK, UQ_EINVAL, UQ_EUNSUPPORTED, UQ_EHIP = 0, 1, 2, 3
+UQ_F32, UQ_BF16 = 0, 1
+MAP_FULL, MAP_LOCAL, MAP_FROZEN = 0, 1, 2
+
+_STATUS = {UQ_EINVAL: "EINVAL", UQ_EUNSUPPORTED: "EUNSUPPORTED", UQ_EHIP: "EHIP"}
+
+
+class UniquanError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{_STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+_i64, _i32, _vp, _f32 = ctypes.c_int64, ctypes.c_int, ctypes.c_void_p, ctypes.c_float
+_SIGS = {
+    "uniquan_abi_version": ([], _i32),
+    "uniquan_last_error": ([], ctypes.c_char_p),
+    "uniquan_fq_fwd": ([_i64, _i64, _i32, _i32, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _i32, _vp], _i32),
+    "uniquan_fq_bwd": ([_i64, _i64, _i32, _i32, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32,
+                        _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp], _i32),
+    "uniquan_layer_target": ([_i64, _i64, _i64, _vp, _vp, _vp, _vp], _i32),
+    "uniquan_transpose_bf16": ([_i64, _i64, _vp, _vp, _vp], _i32),
+    "uniquan_recon_ws": ([_i64, _i64, _i64], ctypes.c_size_t),
+    "uniquan_layer_recon": ([_i64, _i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp, _i32, _vp], _i32),
+    "uniquan_layer_grad": ([_i64, _i64, _i64, _vp, _vp, _vp, _i32, _vp], _i32),
+    "uniquan_fold_to_bcq": ([_i64, _i64, _i32, _i32, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp], _i32),
+    "uniquan_bcq_dequant": ([_i64, _i64, _i32, _i32, _vp, _vp, _vp, _vp, _i32, _vp], _i32),
+    "uniquan_init_greedy": ([_i64, _i64, _i32, _i32, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp], _i32),
+    "uniquan_sgd": ([_i64, _vp, _vp, _f32, _vp], _i32),
+}
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                               "(python paper_2506_03781_amd/build.py)")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (args, res) in _SIGS.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = res
+        _lib = L
+    return _lib
+
+
+def declared_symbols() -> list:
+    """Entry points declared in include/uniquan.h."""
+    txt = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(uniquan_[a-z0-9_]+)\s*\(", txt)))
+
+
+def last_error() -> str:
+    return lib().uniquan_last_error().decode()
+
+
+def _check(status: int):
+    if status != UQ_OK:
+        raise UniquanError(status, last_error())
+
+
+def _stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return getattr(stream, "cuda_stream", stream)
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return UQ_BF16
+    if t.dtype == torch.float32:
+        return UQ_F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _p(t, n=None, dtypes=None, name="tensor"):
+    """Device pointer of a contiguous tensor with >= n elements (None -> NULL)."""
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtypes is not None and t.dtype not in dtypes:
+        raise TypeError(f"{name} has dtype {t.dtype}, expected one of {dtypes}")
+    if n is not None and t.numel() < n:
+        raise ValueError(f"{name} has {t.numel()} elements, needs {n}")
+    return t.data_ptr()
+
+
+_F = (torch.float32,)
+_W = (torch.float32, torch.bfloat16)
+_B = (torch.bfloat16,)
+_U8 = (torch.uint8,)
+
+
+def uniquan_fq_fwd(R, C, k, g, W, s, s_r, delta, z_u, alpha, z_b, mode, codes, W_hat, stream=None):
+    N, Gn = R * C, R * C // g
+    _check(lib().uniquan_fq_fwd(
+        R, C, k, g, _p(W, N, _W, "W"), _dt(W), _p(s, N, _F, "s"), _p(s_r, R, _F, "s_r"),
+        _p(delta, Gn, _F, "delta"), _p(z_u, Gn, _F, "z_u"), _p(alpha, Gn * k, _F, "alpha"),
+        _p(z_b, Gn, _F, "z_b"), int(mode), _p(codes, N, _U8, "codes"), _p(W_hat, N, _W, "W_hat"),
+        _dt(W_hat), _stream(stream)))
+
+
+def uniquan_fq_bwd(R, C, k, g, W, s, s_r, delta, z_u, alpha, z_b, codes, grad_W_hat,
+                   grad_s, grad_alpha, grad_z_b, grad_delta=None, grad_z_u=None, grad_s_r=None,
+                   group_ws=None, stream=None):
+    N, Gn = R * C, R * C // g
+    _check(lib().uniquan_fq_bwd(
+        R, C, k, g, _p(W, N, _W, "W"), _dt(W), _p(s, N, _F, "s"), _p(s_r, R, _F, "s_r"),
+        _p(delta, Gn, _F, "delta"), _p(z_u, Gn, _F, "z_u"), _p(alpha, Gn * k, _F, "alpha"),
+        _p(z_b, Gn, _F, "z_b"), _p(codes, N, _U8, "codes"), _p(grad_W_hat, N, _W, "grad_W_hat"),
+        _dt(grad_W_hat), _p(grad_s, N, _F, "grad_s"), _p(grad_alpha, Gn * k, _F, "grad_alpha"),
+        _p(grad_z_b, Gn, _F, "grad_z_b"), _p(grad_delta, Gn, _F, "grad_delta"),
+        _p(grad_z_u, Gn, _F, "grad_z_u"), _p(grad_s_r, R, _F, "grad_s_r"),
+        _p(group_ws, Gn, _F, "group_ws"), _stream(stream)))
+
+
+def uniquan_layer_target(T, R, C, X, W, Yt, stream=None):
+    _check(lib().uniquan_layer_target(T, R, C, _p(X, T * C, _B, "X"), _p(W, R * C, _B, "W"),
+                                      _p(Yt, R * T, _F, "Yt"), _stream(stream)))
+
+
+def uniquan_transpose_bf16(rows, cols, x, out, stream=None):
+    _check(lib().uniquan_transpose_bf16(rows, cols, _p(x, rows * cols, _B, "in"),
+                                        _p(out, rows * cols, _B, "out"), _stream(stream)))
+
+
+def uniquan_recon_ws(T, R, C) -> int:
+    return int(lib().uniquan_recon_ws(T, R, C))
+
+
+def uniquan_layer_recon(T, R, C, X, Xt, W_hat, Yt, loss, Et_ws, partials_ws, grad_W_hat=None, stream=None):
+    _check(lib().uniquan_layer_recon(
+        T, R, C, _p(X, T * C, _B, "X"), _p(Xt, T * C, _B, "Xt"), _p(W_hat, R * C, _B, "W_hat"),
+        _p(Yt, R * T, _F, "Yt"), _p(loss, 1, _F, "loss"), _p(Et_ws, R * T, _B, "Et_ws"),
+        _p(partials_ws, uniquan_recon_ws(T, R, C), _F, "partials_ws"),
+        partials_ws.numel() if partials_ws is not None else 0,
+        _p(grad_W_hat, R * C, _W, "grad_W_hat"),
+        _dt(grad_W_hat) if grad_W_hat is not None else UQ_BF16, _stream(stream)))
+
+
+def uniquan_layer_grad(T, R, C, Et, Xt, grad_W_hat, stream=None):
+    _check(lib().uniquan_layer_grad(T, R, C, _p(Et, R * T, _B, "Et"), _p(Xt, T * C, _B, "Xt"),
+                                    _p(grad_W_hat, R * C, _W, "grad_W_hat"), _dt(grad_W_hat), _stream(stream)))
+
+
+def uniquan_fold_to_bcq(R, C, k, g, W, s, s_r, delta, z_u, alpha, z_b, alpha_star, z_star,
+                        codes_out=None, code_src=0, stream=None):
+    N, Gn = R * C, R * C // g
+    _check(lib().uniquan_fold_to_bcq(
+        R, C, k, g, _p(W, N, _W, "W"), _dt(W) if W is not None else UQ_F32, _p(s, N, _F, "s"),
+        _p(s_r, R, _F, "s_r"), _p(delta, Gn, _F, "delta"), _p(z_u, Gn, _F, "z_u"),
+        _p(alpha, Gn * k, _F, "alpha"), _p(z_b, Gn, _F, "z_b"), _p(alpha_star, Gn * k, _F, "alpha_star"),
+        _p(z_star, Gn, _F, "z_star"), _p(codes_out, N, _U8, "codes_out"), int(code_src), _stream(stream)))
+
+
+def uniquan_bcq_dequant(R, C, k, g, codes, alpha, z_b, W_out, stream=None):
+    N, Gn = R * C, R * C // g
+    _check(lib().uniquan_bcq_dequant(R, C, k, g, _p(codes, N, _U8, "codes"), _p(alpha, Gn * k, _F, "alpha"),
+                                     _p(z_b, Gn, _F, "z_b"), _p(W_out, N, _W, "W_out"), _dt(W_out),
+                                     _stream(stream)))
+
+
+def uniquan_init_greedy(R, C, k, g, W, s, s_r, delta, z_u, z_b, alpha, stream=None):
+    N, Gn = R * C, R * C // g
+    _check(lib().uniquan_init_greedy(
+        R, C, k, g, _p(W, N, _W, "W"), _dt(W), _p(s, N, _F, "s"), _p(s_r, R, _F, "s_r"),
+        _p(delta, Gn, _F, "delta"), _p(z_u, Gn, _F, "z_u"), _p(z_b, Gn, _F, "z_b"),
+        _p(alpha, Gn * k, _F, "alpha"), _stream(stream)))
+
+
+def uniquan_sgd(theta, grad, lr, stream=None):
+    n = theta.numel()
+    _check(lib().uniquan_sgd(n, _p(theta, n, _F, "theta"), _p(grad, n, _F, "grad"), float(lr), _stream(stream)))

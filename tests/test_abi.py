@@ -1,0 +1,139 @@
+"""C-ABI checks that need no GPU: the library loads, exports every entry point
+the header declares, and rejects bad arguments on the host before any HIP
+call (so no compute is launched here)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2506_03781_amd import uniquan as uq
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(uq.LIB_PATH):
+        pytest.fail("libuniquan.so is not built; run __graft_entry__.build()")
+    return uq.lib()
+
+
+def test_exports_every_declared_symbol(L):
+    decl = uq.declared_symbols()
+    assert len(decl) >= 12
+    for name in decl:
+        assert hasattr(L, name), name
+    # and the binding wraps each compute entry point under the same name
+    for name in decl:
+        if name not in ("uniquan_abi_version", "uniquan_last_error"):
+            assert hasattr(uq, name), name
+
+
+def test_dynamic_symbol_table_matches_header(L):
+    out = subprocess.run(["nm", "-D", "--defined-only", uq.LIB_PATH], capture_output=True, text=True).stdout
+    exported = set(re.findall(r"\b(uniquan_[a-z0-9_]+)\b", out))
+    assert set(uq.declared_symbols()) <= exported
+
+
+def test_abi_version(L):
+    hdr = open(uq.HEADER).read()
+    ver = int(re.search(r"#define UNIQUAN_ABI_VERSION (\d+)", hdr).group(1))
+    assert L.uniquan_abi_version() == ver
+
+
+FAKE = 1 << 20          # 16-byte aligned non-null "device" address, never dereferenced
+ODD = FAKE + 4          # misaligned for 16-byte arrays
+
+
+def fwd(L, R=4, C=256, k=3, g=128, W=FAKE, wdt=uq.UQ_BF16, s=FAKE, alpha=FAKE, z_b=FAKE, mode=0,
+        codes=FAKE, W_hat=FAKE, odt=uq.UQ_BF16, s_r=None, delta=None, z_u=None):
+    return L.uniquan_fq_fwd(R, C, k, g, W, wdt, s, s_r, delta, z_u, alpha, z_b, mode, codes, W_hat, odt, None)
+
+
+@pytest.mark.parametrize("kw,status,text", [
+    (dict(k=0), uq.UQ_EINVAL, "k=0"),
+    (dict(k=8), uq.UQ_EINVAL, "k=8"),
+    (dict(g=96), uq.UQ_EINVAL, "power of two"),
+    (dict(g=4), uq.UQ_EINVAL, "power of two"),
+    (dict(g=1024, C=2048), uq.UQ_EUNSUPPORTED, "g=1024"),
+    (dict(C=192), uq.UQ_EINVAL, "divide"),
+    (dict(R=0), uq.UQ_EINVAL, "R=0"),
+    (dict(W=None), uq.UQ_EINVAL, "W must not be NULL"),
+    (dict(s=ODD), uq.UQ_EINVAL, "s must be 16-byte aligned"),
+    (dict(codes=None), uq.UQ_EINVAL, "codes"),
+    (dict(mode=3), uq.UQ_EINVAL, "mode"),
+    (dict(wdt=2), uq.UQ_EINVAL, "dtype"),
+    (dict(s_r=FAKE + 2), uq.UQ_EINVAL, "s_r"),
+])
+def test_fq_fwd_validation(L, kw, status, text):
+    assert fwd(L, **kw) == status
+    assert text in uq.last_error()
+
+
+def test_fq_bwd_validation(L):
+    args = [4, 256, 3, 128, FAKE, 1, FAKE, None, None, None, FAKE, FAKE, FAKE, FAKE, 1,
+            FAKE, FAKE, FAKE, None, None, FAKE, None, None]
+    assert L.uniquan_fq_bwd(*args) == uq.UQ_EINVAL          # grad_s_r without group_ws
+    assert "group_ws" in uq.last_error()
+    args2 = list(args)
+    args2[15] = ODD
+    args2[20] = None
+    assert L.uniquan_fq_bwd(*args2) == uq.UQ_EINVAL
+    assert "grad_s" in uq.last_error()
+
+
+def test_recon_validation(L):
+    ws = L.uniquan_recon_ws(64, 256, 256)
+    assert ws >= 1
+    assert L.uniquan_layer_recon(60, 256, 256, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, ws, FAKE, 1, None) \
+        == uq.UQ_EINVAL
+    assert "multiple of 8" in uq.last_error()
+    assert L.uniquan_layer_recon(64, 256, 256, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, ws - 1, FAKE, 1, None) \
+        == uq.UQ_EINVAL
+    assert "partials_len" in uq.last_error()
+    assert L.uniquan_layer_recon(64, 256, 256, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, ws, FAKE, 1, None) \
+        == uq.UQ_EINVAL
+    assert "Xt" in uq.last_error()
+    assert L.uniquan_layer_target(64, 256, 250, FAKE, FAKE, FAKE, None) == uq.UQ_EINVAL
+
+
+def test_other_validation(L):
+    assert L.uniquan_fold_to_bcq(4, 256, 3, 128, FAKE, 1, FAKE, None, None, None, FAKE, FAKE, FAKE, FAKE,
+                                 FAKE, 2, None) == uq.UQ_EINVAL
+    assert L.uniquan_bcq_dequant(4, 256, 3, 128, FAKE, FAKE, FAKE, FAKE, 5, None) == uq.UQ_EINVAL
+    assert L.uniquan_init_greedy(4, 256, 3, 100, FAKE, 1, FAKE, None, None, None, FAKE, FAKE, None) == uq.UQ_EINVAL
+    assert L.uniquan_sgd(0, FAKE, FAKE, ctypes.c_float(0.1), None) == uq.UQ_EINVAL
+    assert L.uniquan_transpose_bf16(12, 16, FAKE, FAKE, None) == uq.UQ_EINVAL
+
+
+def test_error_text_is_thread_local(L):
+    import threading
+    fwd(L, k=0)
+    seen = {}
+
+    def other():
+        seen["t"] = uq.last_error()
+    t = threading.Thread(target=other)
+    t.start()
+    t.join()
+    assert seen["t"] == ""
+    assert "k=0" in uq.last_error()
+
+
+def test_binding_refuses_host_tensors():
+    import torch
+    with pytest.raises(ValueError):
+        uq._p(torch.zeros(4), 4, None, "x")
+
+
+def test_product_never_imports_oracle():
+    """The library's Python side and HIP sources stay independent of oracle/."""
+    pkg = os.path.join(ROOT, "paper_2506_03781_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".h", ".cpp")):
+                txt = open(os.path.join(dirpath, f)).read()
+                assert not re.search(r"^\s*(from|import)\s+oracle", txt, re.M), f
+                assert "oracle/" not in txt, f
