@@ -7,13 +7,15 @@
 // ("NT"), so one kernel template serves them.
 //
 // Tiling: a 256-thread workgroup (4 wavefronts, 2 x 2) computes a BM x BN
-// tile; each wavefront owns (BM/2) x (BN/2) as a grid of 32x32 MFMA blocks
-// with fp32 accumulators.  K advances in steps of 32: the next K-slab is
-// fetched from global memory into registers (16-byte loads) while the MFMAs
-// consume the current slab from LDS.  LDS rows are padded by 16 bytes so
-// the 16-byte fragment reads of 8 consecutive rows hit distinct banks.
-// Workgroups are ordered so that consecutive ones on the same XCD share A
-// row-panels (grouped ordering), which keeps operand panels L2-resident.
+// tile (256x256, 256x128 or 128x128, the largest that still fills the 256
+// compute units); each wavefront owns (BM/2) x (BN/2) as a grid of 32x32 MFMA
+// blocks with fp32 accumulators.  K advances in slabs of 64: the next slab is
+// fetched from global memory into registers (16-byte loads, 8 lanes per
+// 128-byte row segment) while the MFMAs consume the current slab from one of
+// two LDS buffers, so one barrier per slab suffices.  LDS rows are XOR-
+// swizzled instead of padded.  Workgroups are renumbered so that each XCD
+// gets a contiguous run of tiles walked in groups of 8 row-tiles, which keeps
+// the operand panels it needs in its own L2.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -56,19 +58,23 @@ __device__ __forceinline__ void tile_of(int bid, int nb, int tiles_m, int tiles_
   tn = in_group / gsize;
 }
 
+// 16-byte LDS slot of chunk kc (8 bf16 along K) of tile row `row`: rows are
+// 128 bytes (BK = 64) and the chunk index is XOR-swizzled with the row's low
+// three bits, so the 16-byte fragment reads of 8 consecutive rows at one K
+// offset land in 8 distinct bank groups (no padding needed).
+__device__ __forceinline__ int slot(int row, int kc) { return row * 8 + (kc ^ (row & 7)); }
+
 template <int BM, int BN, int EPI>
 __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs p) {
-  constexpr int BK = 32;
-  constexpr int LDK = BK + 8;        // padded row length (elements)
+  constexpr int BK = 64;
   constexpr int WM = BM / 2, WN = BN / 2;
   constexpr int FM = WM / 32, FN = WN / 32;
-  constexpr int CA = BM * BK / 8 / 256;  // 16-byte chunks per thread
-  constexpr int CB = BN * BK / 8 / 256;
+  constexpr int CA = BM * 8 / 256;  // 16-byte chunks per thread and K-slab
+  constexpr int CB = BN * 8 / 256;
   static_assert(CA >= 1 && CB >= 1, "tile too small");
 
-  __shared__ __attribute__((aligned(16))) uint16_t sA[BM * LDK];
-  __shared__ __attribute__((aligned(16))) uint16_t sB[BN * LDK];
-  __shared__ float sred[4];
+  __shared__ uint4 sA[2][BM * 8];
+  __shared__ uint4 sB[2][BN * 8];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -79,33 +85,56 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs p) {
   const int64_t m0 = int64_t(tm) * BM, n0 = int64_t(tn) * BN;
   const int64_t K = p.K;
 
+  // Global -> register staging.  Chunk c of a slab: row c / 8, chunk c % 8,
+  // so 8 consecutive lanes read one 128-byte row segment.
+  const uint16_t* gA[CA];
+  const uint16_t* gB[CB];
+  bool okA[CA], okB[CB];
+#pragma unroll
+  for (int c = 0; c < CA; ++c) {
+    const int idx = tid + c * 256;
+    const int64_t r = m0 + (idx >> 3);
+    okA[c] = r < p.M;
+    gA[c] = p.A + (okA[c] ? r : 0) * K + (idx & 7) * 8;
+  }
+#pragma unroll
+  for (int c = 0; c < CB; ++c) {
+    const int idx = tid + c * 256;
+    const int64_t r = n0 + (idx >> 3);
+    okB[c] = r < p.N;
+    gB[c] = p.B + (okB[c] ? r : 0) * K + (idx & 7) * 8;
+  }
   uint4 ra[CA], rb[CB];
+  const bool interior = (m0 + BM <= p.M) && (n0 + BN <= p.N);
   auto gload = [&](int64_t k0) {
+    if (interior && k0 + BK <= K) {  // uniform: no per-chunk bounds checks
+#pragma unroll
+      for (int c = 0; c < CA; ++c) ra[c] = *reinterpret_cast<const uint4*>(gA[c] + k0);
+#pragma unroll
+      for (int c = 0; c < CB; ++c) rb[c] = *reinterpret_cast<const uint4*>(gB[c] + k0);
+      return;
+    }
 #pragma unroll
     for (int c = 0; c < CA; ++c) {
-      const int idx = tid + c * 256;
-      const int row = idx >> 2, kc = idx & 3;
-      const int64_t gr = m0 + row, gk = k0 + kc * 8;
-      ra[c] = (gr < p.M && gk < K) ? *reinterpret_cast<const uint4*>(p.A + gr * K + gk) : make_uint4(0, 0, 0, 0);
+      const bool ok = okA[c] && (k0 + ((tid + c * 256) & 7) * 8 < K);
+      ra[c] = ok ? *reinterpret_cast<const uint4*>(gA[c] + k0) : make_uint4(0, 0, 0, 0);
     }
 #pragma unroll
     for (int c = 0; c < CB; ++c) {
-      const int idx = tid + c * 256;
-      const int row = idx >> 2, kc = idx & 3;
-      const int64_t gr = n0 + row, gk = k0 + kc * 8;
-      rb[c] = (gr < p.N && gk < K) ? *reinterpret_cast<const uint4*>(p.B + gr * K + gk) : make_uint4(0, 0, 0, 0);
+      const bool ok = okB[c] && (k0 + ((tid + c * 256) & 7) * 8 < K);
+      rb[c] = ok ? *reinterpret_cast<const uint4*>(gB[c] + k0) : make_uint4(0, 0, 0, 0);
     }
   };
-  auto lstore = [&]() {
+  auto lstore = [&](int buf) {
 #pragma unroll
     for (int c = 0; c < CA; ++c) {
       const int idx = tid + c * 256;
-      *reinterpret_cast<uint4*>(&sA[(idx >> 2) * LDK + (idx & 3) * 8]) = ra[c];
+      sA[buf][slot(idx >> 3, idx & 7)] = ra[c];
     }
 #pragma unroll
     for (int c = 0; c < CB; ++c) {
       const int idx = tid + c * 256;
-      *reinterpret_cast<uint4*>(&sB[(idx >> 2) * LDK + (idx & 3) * 8]) = rb[c];
+      sB[buf][slot(idx >> 3, idx & 7)] = rb[c];
     }
   };
 
@@ -117,66 +146,91 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
+  const int lr = lane & 31, lh = lane >> 5;
   const int nk = int((K + BK - 1) / BK);
   gload(0);
-  lstore();
+  lstore(0);
   __syncthreads();
-  const int lrow = lane & 31;
-  const int lk = (lane >> 5) * 8;
   for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
     if (kt + 1 < nk) gload(int64_t(kt + 1) * BK);
-#pragma unroll
-    for (int kk = 0; kk < BK; kk += 16) {
-      bf16x8 af[FM], bfr[FN];
+    const uint4* a_s = sA[buf];
+    const uint4* b_s = sB[buf];
+    // fragments of substep s+1 are read while the MFMAs of substep s run
+    bf16x8 af[2][FM], bfr[2][FN];
+    auto fload = [&](int s, int d) {
+      const int kc = s * 2 + lh;
 #pragma unroll
       for (int i = 0; i < FM; ++i)
-        af[i] = *reinterpret_cast<const bf16x8*>(&sA[(wm * WM + i * 32 + lrow) * LDK + kk + lk]);
+        af[d][i] = __builtin_bit_cast(bf16x8, a_s[(wm * WM + i * 32 + lr) * 8 + (kc ^ (lr & 7))]);
 #pragma unroll
       for (int j = 0; j < FN; ++j)
-        bfr[j] = *reinterpret_cast<const bf16x8*>(&sB[(wn * WN + j * 32 + lrow) * LDK + kk + lk]);
+        bfr[d][j] = __builtin_bit_cast(bf16x8, b_s[(wn * WN + j * 32 + lr) * 8 + (kc ^ (lr & 7))]);
+    };
+    fload(0, 0);
+#pragma unroll
+    for (int s = 0; s < BK / 16; ++s) {
+      if (s + 1 < BK / 16) fload(s + 1, (s + 1) & 1);
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[s & 1][i], bfr[s & 1][j], acc[i][j], 0, 0, 0);
     }
+    if (kt + 1 < nk) lstore(buf ^ 1);
     __syncthreads();
-    if (kt + 1 < nk) {
-      lstore();
-      __syncthreads();
-    }
   }
 
   // Epilogue.  Accumulator register r of lane l holds row
-  // 8*(r/4) + 4*(l/32) + r%4 and column l%32 of its 32x32 block.
+  // 8*(r/4) + 4*(l/32) + r%4 and column l%32 of its 32x32 block.  For the
+  // loss epilogue the 16 target values of a block are loaded in one batch
+  // (16 independent loads in flight) before they are used.
+  const bool full = (m0 + BM <= p.M) && (n0 + BN <= p.N);
   float lsum = 0.0f;
+  const float* __restrict__ Yt = p.Yt;
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
-      const int64_t col = n0 + wn * WN + j * 32 + (lane & 31);
+      const int64_t col = n0 + wn * WN + j * 32 + lr;
+      const int64_t row0 = m0 + wm * WM + i * 32 + 4 * lh;
+      const int64_t base = row0 * p.N + col;
+      bool ok[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int64_t row = m0 + wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        if (row < p.M && col < p.N) {
-          const int64_t o = row * p.N + col;
-          const float v = acc[i][j][r];
-          if constexpr (EPI == EPI_TARGET) {
-            static_cast<float*>(p.out)[o] = v;
-          } else if constexpr (EPI == EPI_LOSS) {
-            const float e = v - p.Yt[o];
-            lsum += e * e;
-            static_cast<uint16_t*>(p.out)[o] = uint16_t(bf16_rne(e));
-          } else if constexpr (EPI == EPI_GRAD_BF16) {
-            static_cast<uint16_t*>(p.out)[o] = uint16_t(bf16_rne(p.scale * v));
-          } else {
-            static_cast<float*>(p.out)[o] = p.scale * v;
-          }
+        const int dr = 8 * (r >> 2) + (r & 3);
+        ok[r] = full || (row0 + dr < p.M && col < p.N);
+      }
+      float y[16];
+      if constexpr (EPI == EPI_LOSS) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int dr = 8 * (r >> 2) + (r & 3);
+          y[r] = ok[r] ? Yt[base + int64_t(dr) * p.N] : 0.0f;
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        if (!ok[r]) continue;
+        const int dr = 8 * (r >> 2) + (r & 3);
+        const int64_t o = base + int64_t(dr) * p.N;
+        const float v = acc[i][j][r];
+        if constexpr (EPI == EPI_TARGET) {
+          static_cast<float*>(p.out)[o] = v;
+        } else if constexpr (EPI == EPI_LOSS) {
+          const float e = v - y[r];
+          lsum += e * e;
+          static_cast<uint16_t*>(p.out)[o] = uint16_t(bf16_rne(e));
+        } else if constexpr (EPI == EPI_GRAD_BF16) {
+          static_cast<uint16_t*>(p.out)[o] = uint16_t(bf16_rne(p.scale * v));
+        } else {
+          static_cast<float*>(p.out)[o] = p.scale * v;
         }
       }
     }
   }
   if constexpr (EPI == EPI_LOSS) {
+    __shared__ float sred[4];
     for (int msk = 32; msk >= 1; msk >>= 1) lsum += __shfl_xor(lsum, msk, 64);
     if (lane == 0) sred[wave] = lsum;
     __syncthreads();
@@ -189,12 +243,22 @@ static int tiles(int64_t M, int64_t N) {
   return int(((M + BM - 1) / BM) * ((N + BN - 1) / BN));
 }
 
-// Large 256x256 tiles halve the LDS and L2 traffic per flop; they are used
-// when they still give at least one workgroup per compute unit.
-static bool use_big(int64_t M, int64_t N) { return tiles<256, 256>(M, N) >= 256; }
+// Tile shape: the largest of 256x256, 256x128, 128x128 that still gives at
+// least one workgroup per compute unit (larger tiles move fewer operand
+// bytes per flop through L2 and LDS).
+enum TileShape { T256x256, T256x128, T128x128 };
+static TileShape pick(int64_t M, int64_t N) {
+  if (tiles<256, 256>(M, N) >= 256) return T256x256;
+  if (tiles<256, 128>(M, N) >= 256) return T256x128;
+  return T128x128;
+}
 
 size_t gemm_workgroups(int64_t M, int64_t N, int /*epi*/) {
-  return use_big(M, N) ? size_t(tiles<256, 256>(M, N)) : size_t(tiles<128, 128>(M, N));
+  switch (pick(M, N)) {
+    case T256x256: return size_t(tiles<256, 256>(M, N));
+    case T256x128: return size_t(tiles<256, 128>(M, N));
+    default: return size_t(tiles<128, 128>(M, N));
+  }
 }
 
 template <int BM, int BN>
@@ -215,7 +279,11 @@ static hipError_t launch_bm(const GemmLaunch& q, hipStream_t st) {
 }
 
 hipError_t launch_gemm(const GemmLaunch& q, hipStream_t st) {
-  return use_big(q.M, q.N) ? launch_bm<256, 256>(q, st) : launch_bm<128, 128>(q, st);
+  switch (pick(q.M, q.N)) {
+    case T256x256: return launch_bm<256, 256>(q, st);
+    case T256x128: return launch_bm<256, 128>(q, st);
+    default: return launch_bm<128, 128>(q, st);
+  }
 }
 
 // Deterministic loss: fixed strided fp64 partial sums, then a fixed tree.
