@@ -28,6 +28,32 @@ __device__ __forceinline__ float tau_of(const float* __restrict__ alpha_g, int k
   return t;
 }
 
+// Raw storage of 8 weights as loaded (bf16 kept packed until use).
+template <int DT> struct Raw8;
+template <> struct Raw8<BF16> {
+  uint4 q;
+  __device__ __forceinline__ void load(const void* base, int64_t off) {
+    q = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(base) + off);
+  }
+  __device__ __forceinline__ float get(int i) const {
+    const uint32_t w = i < 2 ? q.x : i < 4 ? q.y : i < 6 ? q.z : q.w;
+    return (i & 1) ? __uint_as_float(w & 0xFFFF0000u) : __uint_as_float(w << 16);
+  }
+};
+template <> struct Raw8<F32> {
+  float4 a, b;
+  __device__ __forceinline__ void load(const void* base, int64_t off) {
+    const float4* p = reinterpret_cast<const float4*>(static_cast<const float*>(base) + off);
+    a = p[0];
+    b = p[1];
+  }
+  __device__ __forceinline__ float get(int i) const {
+    const float4& v = i < 4 ? a : b;
+    const int j = i & 3;
+    return j == 0 ? v.x : j == 1 ? v.y : j == 2 ? v.z : v.w;
+  }
+};
+
 struct FwdArgs {
   TileGeom t;
   const void* W;
@@ -41,24 +67,45 @@ struct FwdArgs {
   void* W_hat;
 };
 
-template <int WDT, int ODT, int MODE>
+// Dynamic LDS of a quantizer tile: the level tables plus four per-group
+// fp32 arrays.
+static size_t tile_lds_bytes(const TileGeom& t) {
+  const size_t e = size_t(t.tile_groups) << t.logL;
+  return ((e * 10 + 15) & ~size_t(15)) + 16 * size_t(t.tile_groups);
+}
+
+// CH chunks of 8 weights per lane (chunk c of the tile = lane c % 256,
+// slot c / 256): all loads of the tile are issued before the level tables
+// are built, so CH * 20 KB per workgroup are in flight while the tables are
+// sorted.
+template <int WDT, int ODT, int MODE, int CH>
 __global__ __launch_bounds__(kThreads) void fq_fwd_kernel(FwdArgs a) {
-  __shared__ LevelTables tab;
-  __shared__ float s_ds[kMaxTileGroups], s_zu[kMaxTileGroups], s_dl[kMaxTileGroups], s_tau[kMaxTileGroups];
+  extern __shared__ __attribute__((aligned(16))) char smem[];
   const TileGeom& g = a.t;
+  LevelTables tab;
+  float* s_ds = reinterpret_cast<float*>(carve_tables(tab, smem, g.tile_groups << g.logL));
+  float* s_zu = s_ds + g.tile_groups;
+  float* s_dl = s_zu + g.tile_groups;
+  float* s_tau = s_dl + g.tile_groups;
   const int64_t Gn = g.N >> g.logg;
   const int64_t gid0 = int64_t(blockIdx.x) * g.tile_groups;
   const int ng = int(min<int64_t>(g.tile_groups, Gn - gid0));
-  const int lane_w = threadIdx.x * kVec;
-  const bool active = lane_w < (ng << g.logg);
-  const int64_t off = (gid0 << g.logg) + lane_w;
+  const int nw = ng << g.logg;
+  const int64_t base = gid0 << g.logg;
 
-  float w[8], sv[8];
-  uint2 prev = make_uint2(0u, 0u);
-  if (active) {
-    load8<WDT>(a.W, off, w);
-    load8f(a.s, off, sv);
-    if constexpr (MODE != 0) prev = load8u8(a.codes, off);
+  Raw8<WDT> w[CH];
+  float4 s0[CH], s1[CH];
+  uint2 prev[CH];
+#pragma unroll
+  for (int j = 0; j < CH; ++j) {
+    const int lw = (threadIdx.x + j * kThreads) * kVec;
+    if (lw < nw) {
+      w[j].load(a.W, base + lw);
+      const float4* sp = reinterpret_cast<const float4*>(a.s + base + lw);
+      s0[j] = sp[0];
+      s1[j] = sp[1];
+      if constexpr (MODE != 0) prev[j] = load8u8(a.codes, base + lw);
+    }
   }
   for (int gl = threadIdx.x; gl < ng; gl += blockDim.x) {
     const int64_t gid = gid0 + gl;
@@ -70,40 +117,45 @@ __global__ __launch_bounds__(kThreads) void fq_fwd_kernel(FwdArgs a) {
     s_tau[gl] = tau_of(a.alpha + gid * g.k, g.k);
   }
   build_tables(tab, a.alpha, a.z_b, gid0, ng, g.k, g.logL);
-  if (!active) return;
 
-  const int gl = lane_w >> g.logg;
   const int L = 1 << g.logL;
-  const float ds = s_ds[gl], zu = s_zu[gl], dl = s_dl[gl], tau = s_tau[gl];
-  const float* q = tab.qs + (gl << g.logL);
-  const uint8_t* code_of = tab.code_of + (gl << g.logL);
-  const uint8_t* pos_of = tab.pos_of + (gl << g.logL);
-  float out[8];
-  uint32_t cw[2] = {0u, 0u};
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const float den = ds * sv[i];
-    const float wb = w[i] / den + zu;
-    float d;
-    int j;
-    if constexpr (MODE == 0) {
-      j = nearest_full(q, g.logL, wb, d);
-    } else {
-      const int p0 = pos_of[byte_of(prev, i) & uint32_t(L - 1)];
-      if constexpr (MODE == 1) {
-        j = nearest_local(q, L, p0, wb, d);
+  for (int j = 0; j < CH; ++j) {
+    const int lw = (threadIdx.x + j * kThreads) * kVec;
+    if (lw >= nw) continue;
+    const int gl = lw >> g.logg;
+    const float ds = s_ds[gl], zu = s_zu[gl], dl = s_dl[gl], tau = s_tau[gl];
+    const float* q = tab.qs + (gl << g.logL);
+    const uint8_t* code_of = tab.code_of + (gl << g.logL);
+    const uint8_t* pos_of = tab.pos_of + (gl << g.logL);
+    const float sv[8] = {s0[j].x, s0[j].y, s0[j].z, s0[j].w, s1[j].x, s1[j].y, s1[j].z, s1[j].w};
+    float out[8];
+    uint32_t cw[2] = {0u, 0u};
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float den = ds * sv[i];
+      const float wb = w[j].get(i) / den + zu;
+      float d;
+      int jj;
+      if constexpr (MODE == 0) {
+        jj = nearest_full(q, g.logL, wb, d);
       } else {
-        j = p0;
-        d = fabsf(wb - q[j]);
+        const int p0 = pos_of[byte_of(prev[j], i) & uint32_t(L - 1)];
+        if constexpr (MODE == 1) {
+          jj = nearest_local(q, L, p0, wb, d);
+        } else {
+          jj = p0;
+          d = fabsf(wb - q[jj]);
+        }
       }
+      const float wt = q[jj];
+      const uint32_t byte = uint32_t(code_of[jj]) | (d > tau ? 0u : 0x80u);
+      cw[i >> 2] |= byte << (8 * (i & 3));
+      out[i] = dl * (wt - zu);
     }
-    const float wt = q[j];
-    const uint32_t byte = uint32_t(code_of[j]) | (d > tau ? 0u : 0x80u);
-    cw[i >> 2] |= byte << (8 * (i & 3));
-    out[i] = dl * (wt - zu);
+    store8<ODT>(a.W_hat, base + lw, out);
+    store8u8(a.codes, base + lw, make_uint2(cw[0], cw[1]));
   }
-  store8<ODT>(a.W_hat, off, out);
-  store8u8(a.codes, off, make_uint2(cw[0], cw[1]));
 }
 
 // ---------------------------------------------------------------------------
@@ -126,18 +178,24 @@ struct FoldArgs {
   int code_src;
 };
 
+// LDS: tables, per-group (Delta s_r, z_U, z*) and the tile's alpha* (k per group)
+static size_t fold_lds_bytes(const TileGeom& t) {
+  return tile_lds_bytes(t) + 4 * size_t(t.tile_groups) * size_t(t.k);
+}
+
 template <int WDT>
 __global__ __launch_bounds__(kThreads) void fold_kernel(FoldArgs a) {
-  __shared__ LevelTables tab;
-  __shared__ float s_ds[kMaxTileGroups], s_zu[kMaxTileGroups];
-  __shared__ float s_alpha[kMaxEntries];  // folded alpha (code_src 1)
-  __shared__ float s_zst[kMaxTileGroups];
+  extern __shared__ __attribute__((aligned(16))) char smem[];
   const TileGeom& g = a.t;
+  LevelTables tab;
+  float* s_ds = reinterpret_cast<float*>(carve_tables(tab, smem, g.tile_groups << g.logL));
+  float* s_zu = s_ds + g.tile_groups;
+  float* s_zst = s_zu + g.tile_groups;
+  float* s_alpha = s_zst + 2 * g.tile_groups;  // tile_groups * k entries
   const int64_t Gn = g.N >> g.logg;
   const int64_t gid0 = int64_t(blockIdx.x) * g.tile_groups;
   const int ng = int(min<int64_t>(g.tile_groups, Gn - gid0));
   const int lane_w = threadIdx.x * kVec;
-  const bool active = a.codes != nullptr && lane_w < (ng << g.logg);
   const int64_t off = (gid0 << g.logg) + lane_w;
 
   for (int gl = threadIdx.x; gl < ng; gl += blockDim.x) {
@@ -149,7 +207,7 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(FoldArgs a) {
     for (int i = 0; i < g.k; ++i) {
       const float as = dl * a.alpha[gid * g.k + i];
       a.alpha_star[gid * g.k + i] = as;
-      if (gl * g.k + i < kMaxEntries) s_alpha[gl * g.k + i] = as;
+      s_alpha[gl * g.k + i] = as;
     }
     a.z_star[gid] = zst;
     s_zst[gl] = zst;
@@ -161,27 +219,15 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(FoldArgs a) {
   if (a.code_src == 0) {
     build_tables(tab, a.alpha, a.z_b, gid0, ng, g.k, g.logL);
   } else {
-    // folded levels from the LDS copies of alpha*, z* (tile_groups * k <= kMaxEntries)
     const int L = 1 << g.logL;
-    const int n = ng << g.logL;
-    for (int e = threadIdx.x; e < n; e += blockDim.x) {
+    for (int e = threadIdx.x; e < (ng << g.logL); e += blockDim.x) {
       const int gl = e >> g.logL;
       tab.raw[e] = level_value(s_alpha + gl * g.k, s_zst[gl], g.k, e & (L - 1));
     }
     __syncthreads();
-    for (int e = threadIdx.x; e < n; e += blockDim.x) {
-      const int gl = e >> g.logL;
-      const int b = e & (L - 1);
-      const float* row = tab.raw + (gl << g.logL);
-      const float qv = row[b];
-      int rank = 0;
-      for (int b2 = 0; b2 < L; ++b2) rank += (row[b2] < qv) | ((row[b2] == qv) & (b2 < b));
-      tab.qs[(gl << g.logL) + rank] = qv;
-      tab.code_of[(gl << g.logL) + rank] = uint8_t(b);
-    }
-    __syncthreads();
+    sort_tables(tab, ng, g.logL);
   }
-  if (!active) return;
+  if (lane_w >= (ng << g.logg)) return;
   const int glw = lane_w >> g.logg;
   float w[8], sv[8];
   load8<WDT>(a.W, off, w);
@@ -216,7 +262,8 @@ struct DequantArgs {
 
 template <int ODT>
 __global__ __launch_bounds__(kThreads) void dequant_kernel(DequantArgs a) {
-  __shared__ float raw[kMaxEntries];
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  float* raw = reinterpret_cast<float*>(smem);
   const TileGeom& g = a.t;
   const int64_t Gn = g.N >> g.logg;
   const int64_t gid0 = int64_t(blockIdx.x) * g.tile_groups;
@@ -294,14 +341,16 @@ __global__ __launch_bounds__(kThreads) void greedy_kernel(GreedyArgs a) {
 // ---------------------------------------------------------------------------
 // Launchers
 // ---------------------------------------------------------------------------
-static TileGeom make_geom(int64_t R, int64_t C, int k, int g) {
+// Tile of `chunks` x 2048 weights, capped so the level tables stay within
+// kMaxEntries entries.
+static TileGeom make_geom(int64_t R, int64_t C, int k, int g, int chunks) {
   TileGeom t;
   t.N = R * C;
   t.logg = __builtin_ctz(unsigned(g));
   t.logL = k;
   t.k = k;
   t.gpr = int(C / g);
-  int tg = kTile >> t.logg;
+  int tg = (chunks * kTile) >> t.logg;
   const int by_lds = kMaxEntries >> k;
   if (tg > by_lds) tg = by_lds;
   if (tg < 1) tg = 1;
@@ -314,15 +363,27 @@ static unsigned grid_of(const TileGeom& t) {
   return unsigned((Gn + t.tile_groups - 1) / t.tile_groups);
 }
 
+// Four chunks per lane once there are enough weights to keep every compute
+// unit busy with several 8192-weight tiles; one chunk below that.
+static int fwd_chunks(int64_t N) { return N >= (int64_t(1) << 22) ? 4 : 1; }
+
+template <int WD, int OD, int MD>
+static void launch_fwd_ch(const FwdArgs& a, int ch, hipStream_t st) {
+  const dim3 grid(grid_of(a.t)), block(kThreads);
+  const size_t lds = tile_lds_bytes(a.t);
+  if (ch == 4) hipLaunchKernelGGL((fq_fwd_kernel<WD, OD, MD, 4>), grid, block, lds, st, a);
+  else hipLaunchKernelGGL((fq_fwd_kernel<WD, OD, MD, 1>), grid, block, lds, st, a);
+}
+
 hipError_t launch_fq_fwd(const FqFwdLaunch& p, hipStream_t st) {
   FwdArgs a;
-  a.t = make_geom(p.R, p.C, p.k, p.g);
+  const int ch = fwd_chunks(p.R * p.C);
+  a.t = make_geom(p.R, p.C, p.k, p.g, ch);
   a.W = p.W; a.s = p.s; a.s_r = p.s_r; a.delta = p.delta; a.z_u = p.z_u;
   a.alpha = p.alpha; a.z_b = p.z_b; a.codes = p.codes; a.W_hat = p.W_hat;
-  const dim3 grid(grid_of(a.t)), block(kThreads);
 #define UQ_FWD(WD, OD, MD) \
   if (p.w_dtype == WD && p.w_hat_dtype == OD && p.mode == MD) { \
-    hipLaunchKernelGGL((fq_fwd_kernel<WD, OD, MD>), grid, block, 0, st, a); \
+    launch_fwd_ch<WD, OD, MD>(a, ch, st); \
     return hipGetLastError(); }
   UQ_FWD(BF16, BF16, 0) UQ_FWD(BF16, BF16, 1) UQ_FWD(BF16, BF16, 2)
   UQ_FWD(BF16, F32, 0) UQ_FWD(BF16, F32, 1) UQ_FWD(BF16, F32, 2)
@@ -334,31 +395,31 @@ hipError_t launch_fq_fwd(const FqFwdLaunch& p, hipStream_t st) {
 
 hipError_t launch_fold(const FoldLaunch& p, hipStream_t st) {
   FoldArgs a;
-  a.t = make_geom(p.R, p.C, p.k, p.g);
-  // code_src 1 keeps alpha* of a tile in LDS: tile_groups * k entries
-  while (a.t.tile_groups * p.k > kMaxEntries && a.t.tile_groups > 1) a.t.tile_groups >>= 1;
+  a.t = make_geom(p.R, p.C, p.k, p.g, 1);
   a.W = p.W; a.s = p.s; a.s_r = p.s_r; a.delta = p.delta; a.z_u = p.z_u;
   a.alpha = p.alpha; a.z_b = p.z_b; a.alpha_star = p.alpha_star; a.z_star = p.z_star;
   a.codes = p.codes; a.code_src = p.code_src;
   const dim3 grid(grid_of(a.t)), block(kThreads);
-  if (p.w_dtype == BF16) hipLaunchKernelGGL((fold_kernel<BF16>), grid, block, 0, st, a);
-  else hipLaunchKernelGGL((fold_kernel<F32>), grid, block, 0, st, a);
+  const size_t lds = fold_lds_bytes(a.t);
+  if (p.w_dtype == BF16) hipLaunchKernelGGL((fold_kernel<BF16>), grid, block, lds, st, a);
+  else hipLaunchKernelGGL((fold_kernel<F32>), grid, block, lds, st, a);
   return hipGetLastError();
 }
 
 hipError_t launch_dequant(const DequantLaunch& p, hipStream_t st) {
   DequantArgs a;
-  a.t = make_geom(p.R, p.C, p.k, p.g);
+  a.t = make_geom(p.R, p.C, p.k, p.g, 1);
   a.codes = p.codes; a.alpha = p.alpha; a.z_b = p.z_b; a.W_out = p.W_out;
   const dim3 grid(grid_of(a.t)), block(kThreads);
-  if (p.out_dtype == BF16) hipLaunchKernelGGL((dequant_kernel<BF16>), grid, block, 0, st, a);
-  else hipLaunchKernelGGL((dequant_kernel<F32>), grid, block, 0, st, a);
+  const size_t lds = 4 * (size_t(a.t.tile_groups) << a.t.logL);
+  if (p.out_dtype == BF16) hipLaunchKernelGGL((dequant_kernel<BF16>), grid, block, lds, st, a);
+  else hipLaunchKernelGGL((dequant_kernel<F32>), grid, block, lds, st, a);
   return hipGetLastError();
 }
 
 hipError_t launch_greedy(const GreedyLaunch& p, hipStream_t st) {
   GreedyArgs a;
-  a.t = make_geom(p.R, p.C, p.k, p.g);
+  a.t = make_geom(p.R, p.C, p.k, p.g, 1);
   a.W = p.W; a.s = p.s; a.s_r = p.s_r; a.delta = p.delta; a.z_u = p.z_u;
   a.z_b = p.z_b; a.alpha = p.alpha;
   const int64_t chunks = a.t.N / kVec;

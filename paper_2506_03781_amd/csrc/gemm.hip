@@ -64,6 +64,84 @@ __device__ __forceinline__ void tile_of(int bid, int nb, int tiles_m, int tiles_
 // offset land in 8 distinct bank groups (no padding needed).
 __device__ __forceinline__ int slot(int row, int kc) { return row * 8 + (kc ^ (row & 7)); }
 
+// Store an accumulator tile with the requested epilogue, staged through LDS
+// one 32-row strip at a time.  Accumulator register r of lane l of a 32x32
+// MFMA block holds row 8*(r/4) + 4*(l/32) + r%4 and column l%32; each wave
+// writes its strip (32 x WN fp32) to its own LDS region, then reads it back
+// as rows of float4 so that the target is loaded and the output stored as
+// contiguous 16-byte / 8-byte vectors.  `scratch` must hold 4 * 32 * WN
+// floats and may alias the operand stages (all waves are past their last
+// operand read when this is called).
+template <int BM, int BN, int EPI, int FM = BM / 64, int FN = BN / 64>
+__device__ __forceinline__ void epilogue(const GemmArgs& p, f32x16 (&acc)[FM][FN], int64_t m0, int64_t n0,
+                                         int wm, int wn, int lane, int wave, int tid, float* scratch) {
+  constexpr int WM = BM / 2, WN = BN / 2;
+  constexpr int Q = WN / 4;            // float4 per strip row
+  constexpr int ITER = 32 * Q / 64;    // float4 per lane per strip
+  const int lr = lane & 31, lh = lane >> 5;
+  float* strip = scratch + wave * 32 * WN;
+  const bool full = (m0 + BM <= p.M) && (n0 + BN <= p.N);
+  const float* __restrict__ Yt = p.Yt;
+  float lsum = 0.0f;
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        strip[(8 * (r >> 2) + 4 * lh + (r & 3)) * WN + j * 32 + lr] = acc[i][j][r];
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): the strip is written (own wave only)
+    __builtin_amdgcn_wave_barrier();
+    const int64_t row_base = m0 + wm * WM + i * 32;
+    const int64_t col_base = n0 + wn * WN;
+    float4 y[ITER];
+    if constexpr (EPI == EPI_LOSS) {
+#pragma unroll
+      for (int it = 0; it < ITER; ++it) {
+        const int idx = lane + it * 64;
+        const int64_t row = row_base + idx / Q, col = col_base + (idx % Q) * 4;
+        const bool ok = full || (row < p.M && col < p.N);  // N % 4 == 0 for this epilogue
+        y[it] = ok ? *reinterpret_cast<const float4*>(Yt + row * p.N + col) : make_float4(0, 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int it = 0; it < ITER; ++it) {
+      const int idx = lane + it * 64;
+      const int64_t row = row_base + idx / Q, col = col_base + (idx % Q) * 4;
+      const float4 v = *reinterpret_cast<const float4*>(&strip[(idx / Q) * WN + (idx % Q) * 4]);
+      if (!(full || (row < p.M && col < p.N))) continue;
+      const int64_t o = row * p.N + col;
+      if constexpr (EPI == EPI_TARGET) {
+        *reinterpret_cast<float4*>(static_cast<float*>(p.out) + o) = v;
+      } else if constexpr (EPI == EPI_LOSS) {
+        const float e0 = v.x - y[it].x, e1 = v.y - y[it].y, e2 = v.z - y[it].z, e3 = v.w - y[it].w;
+        lsum += e0 * e0;
+        lsum += e1 * e1;
+        lsum += e2 * e2;
+        lsum += e3 * e3;
+        *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.out) + o) =
+            make_uint2(bf16_rne(e0) | (bf16_rne(e1) << 16), bf16_rne(e2) | (bf16_rne(e3) << 16));
+      } else if constexpr (EPI == EPI_GRAD_BF16) {
+        *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.out) + o) =
+            make_uint2(bf16_rne(p.scale * v.x) | (bf16_rne(p.scale * v.y) << 16),
+                       bf16_rne(p.scale * v.z) | (bf16_rne(p.scale * v.w) << 16));
+      } else {
+        *reinterpret_cast<float4*>(static_cast<float*>(p.out) + o) =
+            make_float4(p.scale * v.x, p.scale * v.y, p.scale * v.z, p.scale * v.w);
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // strip reads done before the next strip overwrites it
+    __builtin_amdgcn_wave_barrier();
+  }
+  if constexpr (EPI == EPI_LOSS) {
+    __shared__ float sred[4];
+    for (int msk = 32; msk >= 1; msk >>= 1) lsum += __shfl_xor(lsum, msk, 64);
+    if (lane == 0) sred[wave] = lsum;
+    __syncthreads();
+    if (tid == 0) p.partials[blockIdx.x] = (sred[0] + sred[1]) + (sred[2] + sred[3]);
+  }
+}
+
 template <int BM, int BN, int EPI>
 __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs p) {
   constexpr int BK = 64;
@@ -73,8 +151,9 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs p) {
   constexpr int CB = BN * 8 / 256;
   static_assert(CA >= 1 && CB >= 1, "tile too small");
 
-  __shared__ uint4 sA[2][BM * 8];
-  __shared__ uint4 sB[2][BN * 8];
+  __shared__ uint4 smem[2 * (BM + BN) * 8];
+  uint4 (*sA)[BM * 8] = reinterpret_cast<uint4 (*)[BM * 8]>(smem);
+  uint4 (*sB)[BN * 8] = reinterpret_cast<uint4 (*)[BN * 8]>(smem + 2 * BM * 8);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -181,61 +260,158 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs p) {
     __syncthreads();
   }
 
-  // Epilogue.  Accumulator register r of lane l holds row
-  // 8*(r/4) + 4*(l/32) + r%4 and column l%32 of its 32x32 block.  For the
-  // loss epilogue the 16 target values of a block are loaded in one batch
-  // (16 independent loads in flight) before they are used.
-  const bool full = (m0 + BM <= p.M) && (n0 + BN <= p.N);
-  float lsum = 0.0f;
-  const float* __restrict__ Yt = p.Yt;
+  epilogue<BM, BN, EPI>(p, acc, m0, n0, wm, wn, lane, wave, tid, reinterpret_cast<float*>(smem));
+}
+
+// ---------------------------------------------------------------------------
+// Pipelined variant for K % 32 == 0: operands go straight from global memory
+// into a ring of S LDS stages (gfx950 global_load_lds_dwordx4, no register
+// staging), two stages ahead of the MFMAs; workgroup barriers carry no
+// memory fence (each wave waits only for its own loads of the stage it is
+// about to read, with an exact vmcnt), and the fragments of the next
+// 16-deep substep are read while the MFMAs of the current one run.
+// A stage holds BK = 32 of K: rows of 64 bytes, four 16-byte chunks per row,
+// chunk position kc ^ ((row >> 1) & 3) so that 8 consecutive rows read at
+// one K offset hit 8 distinct bank groups.  Rows past M or N are loaded from
+// row M-1 / N-1 (valid addresses) and masked at the store.
+// ---------------------------------------------------------------------------
+typedef __attribute__((address_space(3))) void lds_void;
+typedef const __attribute__((address_space(1))) void glb_void;
+
+template <int VM>
+__device__ __forceinline__ void wait_vmcnt() {
+  // s_waitcnt fields: vmcnt[3:0] and [15:14], expcnt[6:4], lgkmcnt[11:8]
+  __builtin_amdgcn_s_waitcnt((VM & 0xF) | ((VM >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+template <int BM, int BN, int EPI, int S, int IL>
+__global__ __launch_bounds__(256) void gemm_pipe_kernel(GemmArgs p) {
+  constexpr int BK = 32;
+  constexpr int WM = BM / 2, WN = BN / 2;
+  constexpr int FM = WM / 32, FN = WN / 32;
+  constexpr int ABLK = BM / 16, BBLK = BN / 16;      // 1 KB blocks (16 rows) per stage
+  constexpr int PER_WAVE = (ABLK + BBLK) / 4;         // load instructions per wave and stage
+  static_assert((ABLK + BBLK) % 4 == 0, "stage blocks must split over 4 waves");
+
+  __shared__ uint4 smem[S * (BM + BN) * 4];
+  uint4 (*sA)[BM * 4] = reinterpret_cast<uint4 (*)[BM * 4]>(smem);
+  uint4 (*sB)[BN * 4] = reinterpret_cast<uint4 (*)[BN * 4]>(smem + S * BM * 4);
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  int tm, tn;
+  tile_of(blockIdx.x, gridDim.x, p.tiles_m, p.tiles_n, tm, tn);
+  const int64_t m0 = int64_t(tm) * BM, n0 = int64_t(tn) * BN;
+  const int64_t K = p.K;
+
+  // This lane's source for each of the wave's load instructions.  Lane l
+  // fills LDS slot l of a 1 KB block: row 16*blk + l/4, slot l%4, which holds
+  // chunk (l%4) ^ ((row>>1)&3) of that row.
+  const uint16_t* src[PER_WAVE];
+  int dst_off[PER_WAVE];
+  bool isA[PER_WAVE];
 #pragma unroll
-  for (int i = 0; i < FM; ++i) {
+  for (int q = 0; q < PER_WAVE; ++q) {
+    const int blk = wave * PER_WAVE + q;
+    const bool a = blk < ABLK;
+    const int b = a ? blk : blk - ABLK;
+    const int row = b * 16 + (lane >> 2);
+    const int kc = (lane & 3) ^ ((row >> 1) & 3);
+    isA[q] = a;
+    const int64_t gr = a ? min(m0 + row, p.M - 1) : min(n0 + row, p.N - 1);
+    src[q] = (a ? p.A : p.B) + gr * K + kc * 8;
+    dst_off[q] = b * 64;
+  }
+  auto issue = [&](int stage, int64_t k0) {
+#pragma unroll
+    for (int q = 0; q < PER_WAVE; ++q) {
+      uint4* dst = isA[q] ? &sA[stage][dst_off[q]] : &sB[stage][dst_off[q]];
+      __builtin_amdgcn_global_load_lds((glb_void*)(src[q] + k0), (lds_void*)dst, 16, 0, 0);
+    }
+  };
+
+  f32x16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  const int lr = lane & 31, lh = lane >> 5;
+  int offA[2][FM], offB[2][FN];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int kc = s * 2 + lh;
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int row = wm * WM + i * 32 + lr;
+      offA[s][i] = row * 4 + (kc ^ ((row >> 1) & 3));
+    }
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
-      const int64_t col = n0 + wn * WN + j * 32 + lr;
-      const int64_t row0 = m0 + wm * WM + i * 32 + 4 * lh;
-      const int64_t base = row0 * p.N + col;
-      bool ok[16];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int dr = 8 * (r >> 2) + (r & 3);
-        ok[r] = full || (row0 + dr < p.M && col < p.N);
-      }
-      float y[16];
-      if constexpr (EPI == EPI_LOSS) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int dr = 8 * (r >> 2) + (r & 3);
-          y[r] = ok[r] ? Yt[base + int64_t(dr) * p.N] : 0.0f;
-        }
-      }
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        if (!ok[r]) continue;
-        const int dr = 8 * (r >> 2) + (r & 3);
-        const int64_t o = base + int64_t(dr) * p.N;
-        const float v = acc[i][j][r];
-        if constexpr (EPI == EPI_TARGET) {
-          static_cast<float*>(p.out)[o] = v;
-        } else if constexpr (EPI == EPI_LOSS) {
-          const float e = v - y[r];
-          lsum += e * e;
-          static_cast<uint16_t*>(p.out)[o] = uint16_t(bf16_rne(e));
-        } else if constexpr (EPI == EPI_GRAD_BF16) {
-          static_cast<uint16_t*>(p.out)[o] = uint16_t(bf16_rne(p.scale * v));
-        } else {
-          static_cast<float*>(p.out)[o] = p.scale * v;
-        }
-      }
+      const int row = wn * WN + j * 32 + lr;
+      offB[s][j] = row * 4 + (kc ^ ((row >> 1) & 3));
     }
   }
-  if constexpr (EPI == EPI_LOSS) {
-    __shared__ float sred[4];
-    for (int msk = 32; msk >= 1; msk >>= 1) lsum += __shfl_xor(lsum, msk, 64);
-    if (lane == 0) sred[wave] = lsum;
-    __syncthreads();
-    if (tid == 0) p.partials[blockIdx.x] = (sred[0] + sred[1]) + (sred[2] + sred[3]);
+  bf16x8 a0[FM], b0[FN], a1[FM], b1[FN];
+  auto rd = [&](int st, int s, bf16x8 (&af)[FM], bf16x8 (&bfr)[FN]) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i) af[i] = __builtin_bit_cast(bf16x8, sA[st][offA[s][i]]);
+#pragma unroll
+    for (int j = 0; j < FN; ++j) bfr[j] = __builtin_bit_cast(bf16x8, sB[st][offB[s][j]]);
+  };
+  auto mma = [&](const bf16x8 (&af)[FM], const bf16x8 (&bfr)[FN]) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+  };
+  auto interleave = [&]() {
+    if constexpr (IL) {
+#pragma unroll
+      for (int q = 0; q < FM + FN; ++q) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                      // one LDS read
+        __builtin_amdgcn_sched_group_barrier(0x008, (FM * FN) / (FM + FN), 0);  // then MFMAs
+      }
+    }
+  };
+
+  const int nk = int(K / BK);
+#pragma unroll
+  for (int s = 0; s < S - 1; ++s)
+    if (s < nk) issue(s, int64_t(s) * BK);
+  if (nk >= S - 1) wait_vmcnt<(S - 2) * PER_WAVE>();
+  else wait_vmcnt<0>();
+  __builtin_amdgcn_s_barrier();
+  rd(0, 0, a0, b0);
+  for (int kt = 0; kt < nk; ++kt) {
+    const int st = kt % S;
+    __builtin_amdgcn_sched_barrier(0);
+    rd(st, 1, a1, b1);  // substep 1 of stage kt while substep 0 multiplies
+    mma(a0, b0);
+    interleave();
+    __builtin_amdgcn_sched_barrier(0);
+    if (kt + 1 < nk) {
+      // stage kt+1 must be resident; loads of later stages may stay in flight
+      const int later = min(nk - 1, kt + S - 2) - (kt + 1);
+      if (later >= S - 3) wait_vmcnt<(S - 3) * PER_WAVE>();
+      else if (later == 1) wait_vmcnt<PER_WAVE>();
+      else wait_vmcnt<0>();
+      __builtin_amdgcn_s_barrier();
+      // the stage overwritten here was last read before this barrier
+      if (kt + S - 1 < nk) issue((kt + S - 1) % S, int64_t(kt + S - 1) * BK);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    rd((kt + 1) % S, 0, a0, b0);  // substep 0 of stage kt+1 (unused after the last stage)
+    mma(a1, b1);
+    interleave();
   }
+  __syncthreads();  // every wave is past its last operand read: the stages become epilogue scratch
+  epilogue<BM, BN, EPI>(p, acc, m0, n0, wm, wn, lane, wave, tid, reinterpret_cast<float*>(smem));
 }
 
 template <int BM, int BN>
@@ -261,6 +437,15 @@ size_t gemm_workgroups(int64_t M, int64_t N, int /*epi*/) {
   }
 }
 
+// Pipelined kernel when K is a multiple of its 32-deep stages; the
+// register-staged kernel (any K that is a multiple of 8) otherwise.
+template <int BM, int BN, int EPI>
+static void launch_epi(const GemmArgs& a, dim3 grid, hipStream_t st) {
+  constexpr int IL = (BM == 256 && BN == 256) ? 0 : 1;
+  if (a.K % 32 == 0) hipLaunchKernelGGL((gemm_pipe_kernel<BM, BN, EPI, 4, IL>), grid, dim3(256), 0, st, a);
+  else hipLaunchKernelGGL((gemm_nt_kernel<BM, BN, EPI>), grid, dim3(256), 0, st, a);
+}
+
 template <int BM, int BN>
 static hipError_t launch_bm(const GemmLaunch& q, hipStream_t st) {
   GemmArgs a;
@@ -268,12 +453,12 @@ static hipError_t launch_bm(const GemmLaunch& q, hipStream_t st) {
   a.Yt = q.Yt; a.out = q.out; a.partials = q.partials; a.scale = q.scale;
   a.tiles_m = int((q.M + BM - 1) / BM);
   a.tiles_n = int((q.N + BN - 1) / BN);
-  const dim3 grid(unsigned(a.tiles_m * a.tiles_n)), block(256);
+  const dim3 grid(unsigned(a.tiles_m * a.tiles_n));
   switch (q.epi) {
-    case EPI_TARGET: hipLaunchKernelGGL((gemm_nt_kernel<BM, BN, EPI_TARGET>), grid, block, 0, st, a); break;
-    case EPI_LOSS: hipLaunchKernelGGL((gemm_nt_kernel<BM, BN, EPI_LOSS>), grid, block, 0, st, a); break;
-    case EPI_GRAD_BF16: hipLaunchKernelGGL((gemm_nt_kernel<BM, BN, EPI_GRAD_BF16>), grid, block, 0, st, a); break;
-    default: hipLaunchKernelGGL((gemm_nt_kernel<BM, BN, EPI_GRAD_F32>), grid, block, 0, st, a); break;
+    case EPI_TARGET: launch_epi<BM, BN, EPI_TARGET>(a, grid, st); break;
+    case EPI_LOSS: launch_epi<BM, BN, EPI_LOSS>(a, grid, st); break;
+    case EPI_GRAD_BF16: launch_epi<BM, BN, EPI_GRAD_BF16>(a, grid, st); break;
+    default: launch_epi<BM, BN, EPI_GRAD_F32>(a, grid, st); break;
   }
   return hipGetLastError();
 }

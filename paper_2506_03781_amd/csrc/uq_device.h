@@ -13,7 +13,6 @@ constexpr int kThreads = 256;           // threads per quantizer workgroup
 constexpr int kVec = 8;                 // consecutive weights per lane
 constexpr int kTile = kThreads * kVec;  // weights per full tile
 constexpr int kMaxEntries = 2048;       // level-table entries per tile (LDS)
-constexpr int kMaxTileGroups = kTile / 8;
 
 enum DType : int { F32 = 0, BF16 = 1 };
 
@@ -91,29 +90,31 @@ __device__ __forceinline__ float level_value(const float* __restrict__ alpha_g, 
   return q;
 }
 
-// Per-tile level tables in LDS.  A tile covers `ng` consecutive groups,
-// table of group gl occupies entries [gl*L, (gl+1)*L).
+// Per-tile level tables in LDS.  A tile covers `ng` consecutive groups; the
+// table of group gl occupies entries [gl*L, (gl+1)*L) of each array.
 struct LevelTables {
-  float raw[kMaxEntries];        // q(b), unsorted
-  float qs[kMaxEntries];         // sorted ascending
-  uint8_t code_of[kMaxEntries];  // code at sorted position
-  uint8_t pos_of[kMaxEntries];   // sorted position of code
+  float* raw;         // q(b), unsorted
+  float* qs;          // sorted ascending
+  uint8_t* code_of;   // code at sorted position
+  uint8_t* pos_of;    // sorted position of code
 };
 
-// Build the sorted tables of groups gid0 .. gid0+ng-1.  All threads of the
-// block take part; ends with a block barrier.  Sort key: (value, code).
-__device__ __forceinline__ void build_tables(LevelTables& t, const float* __restrict__ alpha,
-                                             const float* __restrict__ z_b, int64_t gid0, int ng,
-                                             int k, int logL) {
+// Carve the tables for `entries` levels out of dynamic LDS starting at p;
+// returns the first byte after them (16-byte aligned).
+__device__ __forceinline__ char* carve_tables(LevelTables& t, char* p, int entries) {
+  t.raw = reinterpret_cast<float*>(p);
+  t.qs = t.raw + entries;
+  t.code_of = reinterpret_cast<uint8_t*>(t.qs + entries);
+  t.pos_of = t.code_of + entries;
+  return p + ((size_t(entries) * 10 + 15) & ~size_t(15));
+}
+
+// Rank every raw level of the tile's groups (sort key (value, code)) and
+// scatter into the sorted arrays.  Callers have filled t.raw and issued a
+// barrier; ends with a barrier.
+__device__ __forceinline__ void sort_tables(LevelTables& t, int ng, int logL) {
   const int L = 1 << logL;
   const int n = ng << logL;
-  for (int e = threadIdx.x; e < n; e += blockDim.x) {
-    const int gl = e >> logL;
-    const int b = e & (L - 1);
-    const int64_t gid = gid0 + gl;
-    t.raw[e] = level_value(alpha + gid * k, z_b[gid], k, b);
-  }
-  __syncthreads();
   for (int e = threadIdx.x; e < n; e += blockDim.x) {
     const int gl = e >> logL;
     const int b = e & (L - 1);
@@ -129,6 +130,23 @@ __device__ __forceinline__ void build_tables(LevelTables& t, const float* __rest
     t.pos_of[(gl << logL) + b] = uint8_t(rank);
   }
   __syncthreads();
+}
+
+// Build the sorted tables of groups gid0 .. gid0+ng-1 from alpha and z_b.
+// All threads of the block take part; ends with a block barrier.
+__device__ __forceinline__ void build_tables(LevelTables& t, const float* __restrict__ alpha,
+                                             const float* __restrict__ z_b, int64_t gid0, int ng,
+                                             int k, int logL) {
+  const int L = 1 << logL;
+  const int n = ng << logL;
+  for (int e = threadIdx.x; e < n; e += blockDim.x) {
+    const int gl = e >> logL;
+    const int b = e & (L - 1);
+    const int64_t gid = gid0 + gl;
+    t.raw[e] = level_value(alpha + gid * k, z_b[gid], k, b);
+  }
+  __syncthreads();
+  sort_tables(t, ng, logL);
 }
 
 // Nearest sorted level of x among q[0..L-1] (ascending).  Returns the first

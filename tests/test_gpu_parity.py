@@ -142,6 +142,21 @@ def test_fwd_local_and_frozen(k):
     check_fwd(m.W, s1, p1, k, g, uq.MAP_LOCAL, prev)
 
 
+@pytest.mark.parametrize("k", [3, 4])
+def test_fwd_four_chunks_ragged(k):
+    """>= 4M weights: four 8-weight chunks per lane, 8192-weight tiles, the
+    last tile holding a single row."""
+    m = small_matrix(1031, 4096, 10)
+    g = 128
+    p = params(m.W, m.s, k, g, "A")
+    check_fwd(m.W, m.s, p, k, g)
+    prev = synth.random_codes(1031, 4096, k, 11)
+    p1 = dict(p)
+    p1["alpha"] = synth.perturb(p["alpha"], 0.05, 10, 5)
+    check_fwd(m.W, m.s, p1, k, g, uq.MAP_LOCAL, prev)
+    check_fwd(m.W, m.s, p1, k, g, uq.MAP_FROZEN, prev)
+
+
 def test_fwd_adversarial():
     """Midpoint ties, duplicate and zero scales, huge values, constant groups."""
     k, g = 3, 8
