@@ -145,6 +145,32 @@ uq_status uniquan_fq_bwd(int64_t R, int64_t C, int k, int g,
                          void* stream);
 
 /*
+ * uniquan_fq_bwd_sgd -- uniquan_fq_bwd (required gradients only) fused with
+ * the stochastic gradient descent update of Algorithm 1 for the trained
+ * parameters, in place and in the same pass over the weights:
+ *     s     <- s     - lr_f * grad_s          (Theta_F learning rate)
+ *     alpha <- alpha - lr_b * grad_alpha      (Theta_B learning rate)
+ *     z_b   <- z_b   - lr_b * grad_z_b
+ * Gradients are those of the parameters before the update; they are also
+ * written to grad_s, grad_alpha, grad_z_b unless those are NULL (a caller
+ * that only steps the parameters saves the 4 B per weight of grad_s).  Each
+ * update is the fp32
+ * expression theta - lr * grad, as uniquan_sgd computes it, so the result
+ * equals uniquan_fq_bwd followed by three uniquan_sgd calls bit for bit.
+ * Arguments as for uniquan_fq_bwd; s, alpha, z_b are in/out.
+ */
+uq_status uniquan_fq_bwd_sgd(int64_t R, int64_t C, int k, int g,
+                             const void* W, int w_dtype,
+                             float* s, const float* s_r,
+                             const float* delta, const float* z_u,
+                             float* alpha, float* z_b,
+                             const uint8_t* codes,
+                             const void* grad_W_hat, int grad_dtype,
+                             float* grad_s, float* grad_alpha, float* grad_z_b,
+                             float lr_f, float lr_b,
+                             void* stream);
+
+/*
  * uniquan_layer_target -- the fixed reconstruction target of one linear
  * layer, Y = X W^T (Algorithm 1, output of the unquantized layer), stored
  * transposed: Yt[r, t] = sum_c W[r, c] X[t, c], fp32 accumulation on bf16

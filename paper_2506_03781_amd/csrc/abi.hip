@@ -100,7 +100,22 @@ uq_status uniquan_fq_bwd(int64_t R, int64_t C, int k, int g, const void* W, int 
   OPT_PTR(grad_delta, 4); OPT_PTR(grad_z_u, 4); OPT_PTR(grad_s_r, 4);
   if (grad_s_r != nullptr) REQ_PTR(group_ws, 4);
   uq::FqBwdLaunch p{R, C, k, g, W, w_dtype, s, s_r, delta, z_u, alpha, z_b, codes, grad_W_hat, grad_dtype,
-                    grad_s, grad_alpha, grad_z_b, grad_delta, grad_z_u, grad_s_r, group_ws};
+                    grad_s, grad_alpha, grad_z_b, grad_delta, grad_z_u, grad_s_r, group_ws, 0, 0.0f, 0.0f};
+  return hip_status(fn, uq::launch_fq_bwd(p, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uniquan_fq_bwd_sgd(int64_t R, int64_t C, int k, int g, const void* W, int w_dtype, float* s,
+                             const float* s_r, const float* delta, const float* z_u, float* alpha, float* z_b,
+                             const uint8_t* codes, const void* grad_W_hat, int grad_dtype, float* grad_s,
+                             float* grad_alpha, float* grad_z_b, float lr_f, float lr_b, void* stream) {
+  const char* fn = "uniquan_fq_bwd_sgd";
+  if (uq_status st = check_quant_shape(fn, R, C, k, g)) return st;
+  if (!is_dtype(w_dtype) || !is_dtype(grad_dtype)) return fail(UQ_EINVAL, "%s: bad dtype", fn);
+  REQ_PTR(W, 16); REQ_PTR(s, 16); REQ_PTR(alpha, 4); REQ_PTR(z_b, 4); REQ_PTR(codes, 16);
+  REQ_PTR(grad_W_hat, 16); OPT_PTR(grad_s, 16); OPT_PTR(grad_alpha, 4); OPT_PTR(grad_z_b, 4);
+  OPT_PTR(s_r, 4); OPT_PTR(delta, 4); OPT_PTR(z_u, 4);
+  uq::FqBwdLaunch p{R, C, k, g, W, w_dtype, s, s_r, delta, z_u, alpha, z_b, codes, grad_W_hat, grad_dtype,
+                    grad_s, grad_alpha, grad_z_b, nullptr, nullptr, nullptr, nullptr, 1, lr_f, lr_b};
   return hip_status(fn, uq::launch_fq_bwd(p, static_cast<hipStream_t>(stream)));
 }
 

@@ -31,6 +31,9 @@ struct BwdArgs {
   float* grad_delta;
   float* grad_z_u;
   float* group_ws;
+  // in-place SGD (update != 0): s -= lr_f grad_s; alpha, z_b -= lr_b grad
+  int update;
+  float lr_f, lr_b;
 };
 
 template <int WDT, int GDT, int K>
@@ -86,7 +89,13 @@ __global__ __launch_bounds__(kThreads) void fq_bwd_kernel(BwdArgs a) {
       if (want_zu && !m) GZ += g;
       if (want_sr && m) P += g * x;
     }
-    store8f(a.grad_s, off, gs);
+    if (a.grad_s) store8f(a.grad_s, off, gs);
+    if (a.update) {
+      float sn[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) sn[i] = sv[i] - a.lr_f * gs[i];
+      store8f(const_cast<float*>(a.s), off, sn);
+    }
   }
   // group reduction over lpg lanes (lpg is a power of two <= 64)
   for (int msk = lpg >> 1; msk >= 1; msk >>= 1) {
@@ -98,9 +107,20 @@ __global__ __launch_bounds__(kThreads) void fq_bwd_kernel(BwdArgs a) {
     if (want_sr) P += __shfl_xor(P, msk, 64);
   }
   if (active && (threadIdx.x & (lpg - 1)) == 0) {
-    a.grad_z_b[gid] = dl * S;
+    const float gzb = dl * S;
+    if (a.grad_z_b) a.grad_z_b[gid] = gzb;
+    if (a.grad_alpha) {
 #pragma unroll
-    for (int b = 0; b < K; ++b) a.grad_alpha[gid * K + b] = dl * Sa[b];
+      for (int b = 0; b < K; ++b) a.grad_alpha[gid * K + b] = dl * Sa[b];
+    }
+    if (a.update) {
+      // every lane of the group read alpha / z_b before the butterfly above
+      float* alpha = const_cast<float*>(a.alpha);
+      float* z_b = const_cast<float*>(a.z_b);
+#pragma unroll
+      for (int b = 0; b < K; ++b) alpha[gid * K + b] = alpha[gid * K + b] - a.lr_b * (dl * Sa[b]);
+      z_b[gid] = z_b[gid] - a.lr_b * gzb;
+    }
     if (want_delta) a.grad_delta[gid] = GD;
     if (want_zu) a.grad_z_u[gid] = -dl * GZ;
     if (want_sr) a.group_ws[gid] = -dl * P;
@@ -140,6 +160,9 @@ hipError_t launch_fq_bwd(const FqBwdLaunch& p, hipStream_t st) {
   a.grad_s = p.grad_s; a.grad_alpha = p.grad_alpha; a.grad_z_b = p.grad_z_b;
   a.grad_delta = p.grad_delta; a.grad_z_u = p.grad_z_u;
   a.group_ws = p.grad_s_r ? p.group_ws : nullptr;
+  a.update = p.update;
+  a.lr_f = p.lr_f;
+  a.lr_b = p.lr_b;
   const int64_t chunks = a.N / kVec;
   const dim3 grid(unsigned((chunks + kThreads - 1) / kThreads));
   if (p.w_dtype == BF16 && p.grad_dtype == BF16) launch_k<BF16, BF16>(a, p.k, grid, st);

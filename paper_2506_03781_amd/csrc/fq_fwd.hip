@@ -74,40 +74,87 @@ static size_t tile_lds_bytes(const TileGeom& t) {
   return ((e * 10 + 15) & ~size_t(15)) + 16 * size_t(t.tile_groups);
 }
 
-// CH chunks of 8 weights per lane (chunk c of the tile = lane c % 256,
-// slot c / 256): all loads of the tile are issued before the level tables
-// are built, so CH * 20 KB per workgroup are in flight while the tables are
-// sorted.
-template <int WDT, int ODT, int MODE, int CH>
+// Forward kernel.  Each wavefront owns 512 consecutive weights (8 per lane;
+// groups never straddle waves since g divides 512) and keeps the level
+// tables of its 512/g groups in a private LDS region, so the table build
+// needs only wave-local ordering and no workgroup barrier.  The lane issues
+// its W, s (and code) loads first; while they are in flight the wave builds
+// its tables: one lane per level computes q(b), then ranks it among the
+// group's levels by counting (sort key (value, code)).
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+  __builtin_amdgcn_wave_barrier();
+}
+
+template <int LOGL>
+__device__ __forceinline__ int nearest_full_k(const float* __restrict__ q, float x, float& dist) {
+  constexpr int L = 1 << LOGL;
+  int pos = 0;  // number of levels <= x among q[0 .. L-2]
+#pragma unroll
+  for (int step = L >> 1; step >= 1; step >>= 1) pos += (q[pos + step - 1] <= x) ? step : 0;
+  const int a = pos > 0 ? pos - 1 : 0;
+  const int b = pos;
+  const float da = fabsf(x - q[a]);
+  const float db = fabsf(x - q[b]);
+  if (db < da) {
+    dist = db;
+    return b;
+  }
+  int j = a;
+  if (a > 0 && fabsf(x - q[a - 1]) == da) {  // run of equal distances: take its first element
+    j = 0;
+    while (j < a && fabsf(x - q[j]) != da) ++j;
+  }
+  dist = da;
+  return j;
+}
+
+// Per-wave LDS bytes: tables of (512/g) groups of 2^k levels + 4 floats per group.
+__host__ __device__ inline size_t wave_lds_bytes(int logg, int k) {
+  const size_t groups = size_t(512) >> logg;
+  const size_t e = groups << k;
+  return ((e * 10 + 15) & ~size_t(15)) + 16 * groups;
+}
+
+template <int WDT, int ODT, int MODE, int LOGL>
 __global__ __launch_bounds__(kThreads) void fq_fwd_kernel(FwdArgs a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
+  constexpr int L = 1 << LOGL;
   const TileGeom& g = a.t;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int gw = 512 >> g.logg;                     // groups per wave (g divides 512)
+  const int ew = gw << LOGL;                        // table entries per wave
+  char* mine = smem + size_t(wave) * wave_lds_bytes(g.logg, LOGL);
   LevelTables tab;
-  float* s_ds = reinterpret_cast<float*>(carve_tables(tab, smem, g.tile_groups << g.logL));
-  float* s_zu = s_ds + g.tile_groups;
-  float* s_dl = s_zu + g.tile_groups;
-  float* s_tau = s_dl + g.tile_groups;
-  const int64_t Gn = g.N >> g.logg;
-  const int64_t gid0 = int64_t(blockIdx.x) * g.tile_groups;
-  const int ng = int(min<int64_t>(g.tile_groups, Gn - gid0));
-  const int nw = ng << g.logg;
-  const int64_t base = gid0 << g.logg;
+  float* s_ds = reinterpret_cast<float*>(carve_tables(tab, mine, ew));
+  float* s_zu = s_ds + gw;
+  float* s_dl = s_zu + gw;
+  float* s_tau = s_dl + gw;
+  const int64_t wbase = (int64_t(blockIdx.x) * (blockDim.x >> 6) + wave) * 512;  // first weight of this wave
+  if (wbase >= g.N) return;                                       // whole wave past the end
+  const int nvalid = int(min<int64_t>(512, g.N - wbase));        // a multiple of g (and of 8)
+  const bool active = lane * kVec < nvalid;
+  const int gv = nvalid >> g.logg;                                // valid groups of this wave
+  const int ev = gv << LOGL;                                      // valid table entries
+  const int64_t off = wbase + lane * kVec;
+  const int64_t gid0 = wbase >> g.logg;
 
-  Raw8<WDT> w[CH];
-  float4 s0[CH], s1[CH];
-  uint2 prev[CH];
-#pragma unroll
-  for (int j = 0; j < CH; ++j) {
-    const int lw = (threadIdx.x + j * kThreads) * kVec;
-    if (lw < nw) {
-      w[j].load(a.W, base + lw);
-      const float4* sp = reinterpret_cast<const float4*>(a.s + base + lw);
-      s0[j] = sp[0];
-      s1[j] = sp[1];
-      if constexpr (MODE != 0) prev[j] = load8u8(a.codes, base + lw);
-    }
+  Raw8<WDT> w;
+  float4 s0 = make_float4(0, 0, 0, 0), s1 = s0;
+  uint2 prev = make_uint2(0u, 0u);
+  if (active) {
+    w.load(a.W, off);
+    const float4* sp = reinterpret_cast<const float4*>(a.s + off);
+    s0 = sp[0];
+    s1 = sp[1];
+    if constexpr (MODE != 0) prev = load8u8(a.codes, off);
   }
-  for (int gl = threadIdx.x; gl < ng; gl += blockDim.x) {
+
+  for (int e = lane; e < ev; e += 64) {
+    const int gl = e >> LOGL;
+    tab.raw[e] = level_value(a.alpha + (gid0 + gl) * g.k, a.z_b[gid0 + gl], g.k, e & (L - 1));
+  }
+  for (int gl = lane; gl < gv; gl += 64) {
     const int64_t gid = gid0 + gl;
     const float dl = a.delta ? a.delta[gid] : 1.0f;
     const float sr = a.s_r ? a.s_r[uint32_t(gid) / uint32_t(g.gpr)] : 1.0f;
@@ -116,46 +163,57 @@ __global__ __launch_bounds__(kThreads) void fq_fwd_kernel(FwdArgs a) {
     s_zu[gl] = a.z_u ? a.z_u[gid] : 0.0f;
     s_tau[gl] = tau_of(a.alpha + gid * g.k, g.k);
   }
-  build_tables(tab, a.alpha, a.z_b, gid0, ng, g.k, g.logL);
-
-  const int L = 1 << g.logL;
+  wave_lds_sync();
+  for (int e = lane; e < ev; e += 64) {
+    const int gl = e >> LOGL;
+    const int b = e & (L - 1);
+    const float* row = tab.raw + (gl << LOGL);
+    const float q = row[b];
+    int rank = 0;
 #pragma unroll
-  for (int j = 0; j < CH; ++j) {
-    const int lw = (threadIdx.x + j * kThreads) * kVec;
-    if (lw >= nw) continue;
-    const int gl = lw >> g.logg;
-    const float ds = s_ds[gl], zu = s_zu[gl], dl = s_dl[gl], tau = s_tau[gl];
-    const float* q = tab.qs + (gl << g.logL);
-    const uint8_t* code_of = tab.code_of + (gl << g.logL);
-    const uint8_t* pos_of = tab.pos_of + (gl << g.logL);
-    const float sv[8] = {s0[j].x, s0[j].y, s0[j].z, s0[j].w, s1[j].x, s1[j].y, s1[j].z, s1[j].w};
-    float out[8];
-    uint32_t cw[2] = {0u, 0u};
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const float den = ds * sv[i];
-      const float wb = w[j].get(i) / den + zu;
-      float d;
-      int jj;
-      if constexpr (MODE == 0) {
-        jj = nearest_full(q, g.logL, wb, d);
-      } else {
-        const int p0 = pos_of[byte_of(prev[j], i) & uint32_t(L - 1)];
-        if constexpr (MODE == 1) {
-          jj = nearest_local(q, L, p0, wb, d);
-        } else {
-          jj = p0;
-          d = fabsf(wb - q[jj]);
-        }
-      }
-      const float wt = q[jj];
-      const uint32_t byte = uint32_t(code_of[jj]) | (d > tau ? 0u : 0x80u);
-      cw[i >> 2] |= byte << (8 * (i & 3));
-      out[i] = dl * (wt - zu);
+    for (int b2 = 0; b2 < L; ++b2) {
+      const float q2 = row[b2];
+      rank += (q2 < q) | ((q2 == q) & (b2 < b));
     }
-    store8<ODT>(a.W_hat, base + lw, out);
-    store8u8(a.codes, base + lw, make_uint2(cw[0], cw[1]));
+    tab.qs[(gl << LOGL) + rank] = q;
+    tab.code_of[(gl << LOGL) + rank] = uint8_t(b);
+    tab.pos_of[(gl << LOGL) + b] = uint8_t(rank);
   }
+  wave_lds_sync();
+  if (!active) return;
+
+  const int gl = (lane * kVec) >> g.logg;
+  const float ds = s_ds[gl], zu = s_zu[gl], dl = s_dl[gl], tau = s_tau[gl];
+  const float* q = tab.qs + (gl << LOGL);
+  const uint8_t* code_of = tab.code_of + (gl << LOGL);
+  const uint8_t* pos_of = tab.pos_of + (gl << LOGL);
+  const float sv[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+  float out[8];
+  uint32_t cw[2] = {0u, 0u};
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const float den = ds * sv[i];
+    const float wb = w.get(i) / den + zu;
+    float d;
+    int jj;
+    if constexpr (MODE == 0) {
+      jj = nearest_full_k<LOGL>(q, wb, d);
+    } else {
+      const int p0 = pos_of[byte_of(prev, i) & uint32_t(L - 1)];
+      if constexpr (MODE == 1) {
+        jj = nearest_local(q, L, p0, wb, d);
+      } else {
+        jj = p0;
+        d = fabsf(wb - q[jj]);
+      }
+    }
+    const float wt = q[jj];
+    const uint32_t byte = uint32_t(code_of[jj]) | (d > tau ? 0u : 0x80u);
+    cw[i >> 2] |= byte << (8 * (i & 3));
+    out[i] = dl * (wt - zu);
+  }
+  store8<ODT>(a.W_hat, off, out);
+  store8u8(a.codes, off, make_uint2(cw[0], cw[1]));
 }
 
 // ---------------------------------------------------------------------------
@@ -363,28 +421,49 @@ static unsigned grid_of(const TileGeom& t) {
   return unsigned((Gn + t.tile_groups - 1) / t.tile_groups);
 }
 
-// Four chunks per lane once there are enough weights to keep every compute
-// unit busy with several 8192-weight tiles; one chunk below that.
-static int fwd_chunks(int64_t N) { return N >= (int64_t(1) << 22) ? 4 : 1; }
+// Waves per workgroup: up to 4, as many as fit 64 KB of dynamic LDS; a
+// single wave above that (tiny groups with many levels) opts in to the
+// larger LDS of gfx950.
+static int fwd_waves_per_block(size_t wave_bytes) {
+  int wpb = int(65536 / wave_bytes);
+  return wpb < 1 ? 1 : wpb > 4 ? 4 : wpb;
+}
+
+template <typename Kern>
+static hipError_t launch_fwd_kern(Kern kern, const FwdArgs& a, size_t wave_bytes, hipStream_t st) {
+  const int wpb = fwd_waves_per_block(wave_bytes);
+  const size_t lds = size_t(wpb) * wave_bytes;
+  if (lds > 65536) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+    if (e != hipSuccess) return e;
+  }
+  const int64_t waves = (a.t.N + 511) / 512;
+  hipLaunchKernelGGL(kern, dim3(unsigned((waves + wpb - 1) / wpb)), dim3(64 * wpb), lds, st, a);
+  return hipGetLastError();
+}
 
 template <int WD, int OD, int MD>
-static void launch_fwd_ch(const FwdArgs& a, int ch, hipStream_t st) {
-  const dim3 grid(grid_of(a.t)), block(kThreads);
-  const size_t lds = tile_lds_bytes(a.t);
-  if (ch == 4) hipLaunchKernelGGL((fq_fwd_kernel<WD, OD, MD, 4>), grid, block, lds, st, a);
-  else hipLaunchKernelGGL((fq_fwd_kernel<WD, OD, MD, 1>), grid, block, lds, st, a);
+static hipError_t launch_fwd_k(const FwdArgs& a, int k, hipStream_t st) {
+  const size_t wb = wave_lds_bytes(a.t.logg, k);
+  switch (k) {
+    case 1: return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, 1>, a, wb, st);
+    case 2: return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, 2>, a, wb, st);
+    case 3: return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, 3>, a, wb, st);
+    case 4: return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, 4>, a, wb, st);
+    case 5: return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, 5>, a, wb, st);
+    case 6: return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, 6>, a, wb, st);
+    default: return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, 7>, a, wb, st);
+  }
 }
 
 hipError_t launch_fq_fwd(const FqFwdLaunch& p, hipStream_t st) {
   FwdArgs a;
-  const int ch = fwd_chunks(p.R * p.C);
-  a.t = make_geom(p.R, p.C, p.k, p.g, ch);
+  a.t = make_geom(p.R, p.C, p.k, p.g, 1);
   a.W = p.W; a.s = p.s; a.s_r = p.s_r; a.delta = p.delta; a.z_u = p.z_u;
   a.alpha = p.alpha; a.z_b = p.z_b; a.codes = p.codes; a.W_hat = p.W_hat;
 #define UQ_FWD(WD, OD, MD) \
-  if (p.w_dtype == WD && p.w_hat_dtype == OD && p.mode == MD) { \
-    launch_fwd_ch<WD, OD, MD>(a, ch, st); \
-    return hipGetLastError(); }
+  if (p.w_dtype == WD && p.w_hat_dtype == OD && p.mode == MD) return launch_fwd_k<WD, OD, MD>(a, p.k, st);
   UQ_FWD(BF16, BF16, 0) UQ_FWD(BF16, BF16, 1) UQ_FWD(BF16, BF16, 2)
   UQ_FWD(BF16, F32, 0) UQ_FWD(BF16, F32, 1) UQ_FWD(BF16, F32, 2)
   UQ_FWD(F32, BF16, 0) UQ_FWD(F32, BF16, 1) UQ_FWD(F32, BF16, 2)

@@ -37,9 +37,13 @@ struct GemmArgs {
   int tiles_m, tiles_n;
 };
 
-__device__ __forceinline__ uint32_t bf16_rne(float f) {
-  uint32_t u = __float_as_uint(f);
-  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+// Two fp32 values -> packed bf16 pair (lo in bits 0..15), round to nearest
+// even: one v_cvt_pk_bf16_f32 on gfx950.
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  const f32x2 f = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2));
 }
 
 // Map a linear workgroup id to (tile_m, tile_n).  Hardware dispatches
@@ -120,11 +124,10 @@ __device__ __forceinline__ void epilogue(const GemmArgs& p, f32x16 (&acc)[FM][FN
         lsum += e2 * e2;
         lsum += e3 * e3;
         *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.out) + o) =
-            make_uint2(bf16_rne(e0) | (bf16_rne(e1) << 16), bf16_rne(e2) | (bf16_rne(e3) << 16));
+            make_uint2(pack_bf16x2(e0, e1), pack_bf16x2(e2, e3));
       } else if constexpr (EPI == EPI_GRAD_BF16) {
         *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.out) + o) =
-            make_uint2(bf16_rne(p.scale * v.x) | (bf16_rne(p.scale * v.y) << 16),
-                       bf16_rne(p.scale * v.z) | (bf16_rne(p.scale * v.w) << 16));
+            make_uint2(pack_bf16x2(p.scale * v.x, p.scale * v.y), pack_bf16x2(p.scale * v.z, p.scale * v.w));
       } else {
         *reinterpret_cast<float4*>(static_cast<float*>(p.out) + o) =
             make_float4(p.scale * v.x, p.scale * v.y, p.scale * v.z, p.scale * v.w);

@@ -18,10 +18,13 @@ enum DType : int { F32 = 0, BF16 = 1 };
 
 __device__ __forceinline__ float bf16_to_f32(uint32_t h16) { return __uint_as_float(h16 << 16); }
 
-// fp32 -> bf16, round to nearest, ties to even (inputs are finite).
-__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+// Two fp32 values -> packed bf16 pair (lo in bits 0..15), round to nearest
+// even: one v_cvt_pk_bf16_f32 on gfx950.
+typedef __bf16 uq_bf16x2 __attribute__((ext_vector_type(2)));
+typedef float uq_f32x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  const uq_f32x2 f = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, uq_bf16x2));
 }
 
 // 8 consecutive weights starting at element `off` (16-byte aligned).
@@ -51,10 +54,10 @@ template <int DT>
 __device__ __forceinline__ void store8(void* base, int64_t off, const float (&v)[8]) {
   if constexpr (DT == BF16) {
     uint4 q;
-    q.x = f32_to_bf16(v[0]) | (f32_to_bf16(v[1]) << 16);
-    q.y = f32_to_bf16(v[2]) | (f32_to_bf16(v[3]) << 16);
-    q.z = f32_to_bf16(v[4]) | (f32_to_bf16(v[5]) << 16);
-    q.w = f32_to_bf16(v[6]) | (f32_to_bf16(v[7]) << 16);
+    q.x = pack_bf16x2(v[0], v[1]);
+    q.y = pack_bf16x2(v[2], v[3]);
+    q.z = pack_bf16x2(v[4], v[5]);
+    q.w = pack_bf16x2(v[6], v[7]);
     *reinterpret_cast<uint4*>(static_cast<uint16_t*>(base) + off) = q;
   } else {
     float4* p = reinterpret_cast<float4*>(static_cast<float*>(base) + off);

@@ -29,6 +29,8 @@ struct FqBwdLaunch {
   const void* grad_W_hat; int grad_dtype;
   float* grad_s; float* grad_alpha; float* grad_z_b;
   float* grad_delta; float* grad_z_u; float* grad_s_r; float* group_ws;
+  int update;            // uniquan_fq_bwd_sgd: apply SGD in place
+  float lr_f, lr_b;
 };
 
 struct FoldLaunch {

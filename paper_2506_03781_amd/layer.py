@@ -75,6 +75,13 @@ class QuantLayer:
                           self.alpha, self.z_b, self.codes, self.G, self.grad_s, self.grad_alpha,
                           self.grad_z_b)
 
+    def fq_bwd_sgd(self, lr_f=0.005, lr_b=0.0005, keep_grads=False):
+        """Backward with the SGD update of s, alpha, z_B fused into the same pass
+        (gradients stored only with keep_grads)."""
+        gs, ga, gz = (self.grad_s, self.grad_alpha, self.grad_z_b) if keep_grads else (None, None, None)
+        uq.uniquan_fq_bwd_sgd(self.R, self.C, self.k, self.g, self.W, self.s, self.s_r, self.delta,
+                              self.z_u, self.alpha, self.z_b, self.codes, self.G, gs, ga, gz, lr_f, lr_b)
+
     def sgd(self, lr_f=0.005, lr_b=0.0005):
         """Plain SGD with the paper's learning rates (Theta_F: s; Theta_B: alpha, z_B)."""
         uq.uniquan_sgd(self.s, self.grad_s, lr_f)
@@ -84,9 +91,10 @@ class QuantLayer:
     def step(self, mode=uq.MAP_FULL, update=True):
         self.fq_fwd(mode)
         self.recon(True)
-        self.fq_bwd()
         if update:
-            self.sgd()
+            self.fq_bwd_sgd()
+        else:
+            self.fq_bwd()
 
     def fold(self, code_src=0):
         a = torch.empty(self.Gn * self.k, dtype=torch.float32, device=self.W.device)

@@ -39,6 +39,8 @@ _SIGS = {
     "uniquan_fq_fwd": ([_i64, _i64, _i32, _i32, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _i32, _vp], _i32),
     "uniquan_fq_bwd": ([_i64, _i64, _i32, _i32, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32,
                         _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp], _i32),
+    "uniquan_fq_bwd_sgd": ([_i64, _i64, _i32, _i32, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32,
+                            _vp, _vp, _vp, _f32, _f32, _vp], _i32),
     "uniquan_layer_target": ([_i64, _i64, _i64, _vp, _vp, _vp, _vp], _i32),
     "uniquan_transpose_bf16": ([_i64, _i64, _vp, _vp, _vp], _i32),
     "uniquan_recon_ws": ([_i64, _i64, _i64], ctypes.c_size_t),
@@ -142,6 +144,17 @@ def uniquan_fq_bwd(R, C, k, g, W, s, s_r, delta, z_u, alpha, z_b, codes, grad_W_
         _p(grad_z_b, Gn, _F, "grad_z_b"), _p(grad_delta, Gn, _F, "grad_delta"),
         _p(grad_z_u, Gn, _F, "grad_z_u"), _p(grad_s_r, R, _F, "grad_s_r"),
         _p(group_ws, Gn, _F, "group_ws"), _stream(stream)))
+
+
+def uniquan_fq_bwd_sgd(R, C, k, g, W, s, s_r, delta, z_u, alpha, z_b, codes, grad_W_hat,
+                       grad_s, grad_alpha, grad_z_b, lr_f, lr_b, stream=None):
+    N, Gn = R * C, R * C // g
+    _check(lib().uniquan_fq_bwd_sgd(
+        R, C, k, g, _p(W, N, _W, "W"), _dt(W), _p(s, N, _F, "s"), _p(s_r, R, _F, "s_r"),
+        _p(delta, Gn, _F, "delta"), _p(z_u, Gn, _F, "z_u"), _p(alpha, Gn * k, _F, "alpha"),
+        _p(z_b, Gn, _F, "z_b"), _p(codes, N, _U8, "codes"), _p(grad_W_hat, N, _W, "grad_W_hat"),
+        _dt(grad_W_hat), _p(grad_s, N, _F, "grad_s"), _p(grad_alpha, Gn * k, _F, "grad_alpha"),
+        _p(grad_z_b, Gn, _F, "grad_z_b"), float(lr_f), float(lr_b), _stream(stream)))
 
 
 def uniquan_layer_target(T, R, C, X, W, Yt, stream=None):

@@ -232,6 +232,49 @@ def test_bwd(gdt, k):
         assert torch.equal(o2[n], out[n]), n
 
 
+@pytest.mark.parametrize("k", [3, 4])
+def test_bwd_sgd_fused(k):
+    """Fused backward + SGD equals the backward followed by three SGD calls,
+    bit for bit, and the fp64 oracle's SGD step within tolerance."""
+    m = small_matrix(40, 512, 12)
+    g = 128
+    p = params(m.W, m.s, k, g, "B")
+    ref = O.fq_fwd(m.W, m.s, p["alpha"], p["z_b"], k, g, p["s_r"], p["delta"], p["z_u"])
+    G = synth.round_to_bf16(np.random.default_rng(3).standard_normal(m.W.shape).astype(F32))
+    R, C = m.W.shape
+    Gn = R * C // g
+    lr_f, lr_b = 0.005, 0.0005
+    common = (dev(m.W, torch.bfloat16),)
+    # unfused
+    s1, a1, z1 = dev(m.s), dev(p["alpha"].reshape(-1)), dev(p["z_b"])
+    gs1, ga1, gz1 = (torch.empty(R * C, device=DEV), torch.empty(Gn * k, device=DEV), torch.empty(Gn, device=DEV))
+    uq.uniquan_fq_bwd(R, C, k, g, common[0], s1, dev(p["s_r"]), dev(p["delta"]), dev(p["z_u"]), a1, z1,
+                      dev(ref["codes"], torch.uint8), dev(G, torch.bfloat16), gs1, ga1, gz1)
+    for th, gr, lr in ((s1, gs1, lr_f), (a1, ga1, lr_b), (z1, gz1, lr_b)):
+        uq.uniquan_sgd(th, gr, lr)
+    # fused, with and without gradient outputs
+    for keep in (True, False):
+        s2, a2, z2 = dev(m.s), dev(p["alpha"].reshape(-1)), dev(p["z_b"])
+        gs2, ga2, gz2 = ((torch.empty(R * C, device=DEV), torch.empty(Gn * k, device=DEV), torch.empty(Gn, device=DEV))
+                         if keep else (None, None, None))
+        uq.uniquan_fq_bwd_sgd(R, C, k, g, common[0], s2, dev(p["s_r"]), dev(p["delta"]), dev(p["z_u"]), a2, z2,
+                              dev(ref["codes"], torch.uint8), dev(G, torch.bfloat16), gs2, ga2, gz2, lr_f, lr_b)
+        torch.cuda.synchronize()
+        for x, y in ((s1, s2), (a1, a2), (z1, z2)):
+            assert torch.equal(x, y)
+        if keep:
+            for x, y in ((gs1, gs2), (ga1, ga2), (gz1, gz2)):
+                assert torch.equal(x, y)
+    bw = O.fq_bwd(m.W, m.s, p["alpha"], p["z_b"], ref["codes"], G, k, g, p["s_r"], p["delta"], p["z_u"])
+    s_ref = O.sgd_step(m.s, bw["grad_s"], lr_f)
+    a_ref = O.sgd_step(p["alpha"], bw["grad_alpha"], lr_b)
+    z_ref = O.sgd_step(p["z_b"], bw["grad_z_b"], lr_b)
+    # the update itself is tiny relative to the parameters: compare the step
+    close(host(s2).reshape(R, C) - m.s, s_ref - m.s, what="s step")
+    close(host(a2).reshape(Gn, k) - p["alpha"], a_ref - p["alpha"], tol=2e-2, what="alpha step")
+    close(host(z2) - p["z_b"], z_ref - p["z_b"], tol=2e-2, what="z_b step")
+
+
 @pytest.mark.parametrize("g", [8, 32, 512])
 def test_bwd_group_sizes(g):
     m = small_matrix(8, 1024, 7)
