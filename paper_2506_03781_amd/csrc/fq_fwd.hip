@@ -109,24 +109,34 @@ __device__ __forceinline__ int nearest_full_k(const float* __restrict__ q, float
   return j;
 }
 
-// Per-wave LDS bytes: tables of (512/g) groups of 2^k levels + 4 floats per group.
-__host__ __device__ inline size_t wave_lds_bytes(int logg, int k) {
+// Per-wave LDS bytes: the level tables of (512/g) groups of 2^k levels,
+// optionally the local-mapping neighbour table (16 B per level), and 4
+// floats per group.
+__host__ __device__ inline size_t wave_lds_bytes(int logg, int k, bool nbt) {
   const size_t groups = size_t(512) >> logg;
   const size_t e = groups << k;
-  return ((e * 10 + 15) & ~size_t(15)) + 16 * groups;
+  return ((e * 10 + 15) & ~size_t(15)) + (nbt ? 16 * e : 0) + 16 * groups;
 }
 
+// Neighbour tables for the local mapping are kept when they fit (16 B per
+// level, at most 4096 levels per wave).
+static bool use_neighbour_table(int logg, int k) { return ((size_t(512) >> logg) << k) <= 4096; }
+
 template <int WDT, int ODT, int MODE, int LOGL>
-__global__ __launch_bounds__(kThreads) void fq_fwd_kernel(FwdArgs a) {
+__global__ __launch_bounds__(kThreads) void fq_fwd_kernel(FwdArgs a, int nbt) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   constexpr int L = 1 << LOGL;
   const TileGeom& g = a.t;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int gw = 512 >> g.logg;                     // groups per wave (g divides 512)
   const int ew = gw << LOGL;                        // table entries per wave
-  char* mine = smem + size_t(wave) * wave_lds_bytes(g.logg, LOGL);
+  const bool has_nb = MODE == 1 && nbt;
+  char* mine = smem + size_t(wave) * wave_lds_bytes(g.logg, LOGL, has_nb);
   LevelTables tab;
-  float* s_ds = reinterpret_cast<float*>(carve_tables(tab, mine, ew));
+  char* p = carve_tables(tab, mine, ew);
+  float4* nb = reinterpret_cast<float4*>(p);        // [ew] (q_l, q_d, q_r, codes l|d<<8|r<<16)
+  if (has_nb) p += 16 * size_t(ew);
+  float* s_ds = reinterpret_cast<float*>(p);
   float* s_zu = s_ds + gw;
   float* s_dl = s_zu + gw;
   float* s_tau = s_dl + gw;
@@ -150,6 +160,7 @@ __global__ __launch_bounds__(kThreads) void fq_fwd_kernel(FwdArgs a) {
     if constexpr (MODE != 0) prev = load8u8(a.codes, off);
   }
 
+  // raw levels by code, and the per-group parameters
   for (int e = lane; e < ev; e += 64) {
     const int gl = e >> LOGL;
     tab.raw[e] = level_value(a.alpha + (gid0 + gl) * g.k, a.z_b[gid0 + gl], g.k, e & (L - 1));
@@ -164,27 +175,45 @@ __global__ __launch_bounds__(kThreads) void fq_fwd_kernel(FwdArgs a) {
     s_tau[gl] = tau_of(a.alpha + gid * g.k, g.k);
   }
   wave_lds_sync();
-  for (int e = lane; e < ev; e += 64) {
-    const int gl = e >> LOGL;
-    const int b = e & (L - 1);
-    const float* row = tab.raw + (gl << LOGL);
-    const float q = row[b];
-    int rank = 0;
+  if constexpr (MODE != 2) {
+    // sorted order: rank of each level by counting, key (value, code)
+    for (int e = lane; e < ev; e += 64) {
+      const int gl = e >> LOGL;
+      const int b = e & (L - 1);
+      const float* row = tab.raw + (gl << LOGL);
+      const float q = row[b];
+      int rank = 0;
 #pragma unroll
-    for (int b2 = 0; b2 < L; ++b2) {
-      const float q2 = row[b2];
-      rank += (q2 < q) | ((q2 == q) & (b2 < b));
+      for (int b2 = 0; b2 < L; ++b2) {
+        const float q2 = row[b2];
+        rank += (q2 < q) | ((q2 == q) & (b2 < b));
+      }
+      tab.qs[(gl << LOGL) + rank] = q;
+      tab.code_of[(gl << LOGL) + rank] = uint8_t(b);
+      tab.pos_of[(gl << LOGL) + b] = uint8_t(rank);
     }
-    tab.qs[(gl << LOGL) + rank] = q;
-    tab.code_of[(gl << LOGL) + rank] = uint8_t(b);
-    tab.pos_of[(gl << LOGL) + b] = uint8_t(rank);
+    wave_lds_sync();
   }
-  wave_lds_sync();
+  if (has_nb) {
+    // per code: the levels at sorted positions d-1, d, d+1 (clipped) and their codes
+    for (int e = lane; e < ev; e += 64) {
+      const int base = e & ~(L - 1);
+      const int d = tab.pos_of[e];
+      const int l = d > 0 ? d - 1 : 0;
+      const int r = d < L - 1 ? d + 1 : L - 1;
+      const uint32_t codes = uint32_t(tab.code_of[base + l]) | (uint32_t(tab.code_of[base + d]) << 8) |
+                             (uint32_t(tab.code_of[base + r]) << 16);
+      nb[e] = make_float4(tab.qs[base + l], tab.qs[base + d], tab.qs[base + r], __uint_as_float(codes));
+    }
+    wave_lds_sync();
+  }
   if (!active) return;
 
   const int gl = (lane * kVec) >> g.logg;
   const float ds = s_ds[gl], zu = s_zu[gl], dl = s_dl[gl], tau = s_tau[gl];
   const float* q = tab.qs + (gl << LOGL);
+  const float* qraw = tab.raw + (gl << LOGL);
+  const float4* nbg = nb + (gl << LOGL);
   const uint8_t* code_of = tab.code_of + (gl << LOGL);
   const uint8_t* pos_of = tab.pos_of + (gl << LOGL);
   const float sv[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
@@ -194,21 +223,38 @@ __global__ __launch_bounds__(kThreads) void fq_fwd_kernel(FwdArgs a) {
   for (int i = 0; i < 8; ++i) {
     const float den = ds * sv[i];
     const float wb = w.get(i) / den + zu;
-    float d;
-    int jj;
+    float d, wt;
+    uint32_t code;
     if constexpr (MODE == 0) {
-      jj = nearest_full_k<LOGL>(q, wb, d);
+      const int jj = nearest_full_k<LOGL>(q, wb, d);
+      wt = q[jj];
+      code = code_of[jj];
+    } else if constexpr (MODE == 2) {
+      code = byte_of(prev, i) & uint32_t(L - 1);
+      wt = qraw[code];
+      d = fabsf(wb - wt);
     } else {
-      const int p0 = pos_of[byte_of(prev, i) & uint32_t(L - 1)];
-      if constexpr (MODE == 1) {
-        jj = nearest_local(q, L, p0, wb, d);
+      const uint32_t c0 = byte_of(prev, i) & uint32_t(L - 1);
+      if (has_nb) {
+        // first nearest of (d-1, d, d+1) in ascending order
+        const float4 e4 = nbg[c0];
+        const uint32_t cs = __float_as_uint(e4.w);
+        float bd = fabsf(wb - e4.x);
+        wt = e4.x;
+        uint32_t sh = 0;
+        const float dm = fabsf(wb - e4.y);
+        if (dm < bd) { bd = dm; wt = e4.y; sh = 8; }
+        const float dr = fabsf(wb - e4.z);
+        if (dr < bd) { bd = dr; wt = e4.z; sh = 16; }
+        d = bd;
+        code = (cs >> sh) & 0xFFu;
       } else {
-        jj = p0;
-        d = fabsf(wb - q[jj]);
+        const int jj = nearest_local(q, L, pos_of[c0], wb, d);
+        wt = q[jj];
+        code = code_of[jj];
       }
     }
-    const float wt = q[jj];
-    const uint32_t byte = uint32_t(code_of[jj]) | (d > tau ? 0u : 0x80u);
+    const uint32_t byte = code | (d > tau ? 0u : 0x80u);
     cw[i >> 2] |= byte << (8 * (i & 3));
     out[i] = dl * (wt - zu);
   }
@@ -430,7 +476,7 @@ static int fwd_waves_per_block(size_t wave_bytes) {
 }
 
 template <typename Kern>
-static hipError_t launch_fwd_kern(Kern kern, const FwdArgs& a, size_t wave_bytes, hipStream_t st) {
+static hipError_t launch_fwd_kern(Kern kern, const FwdArgs& a, size_t wave_bytes, int nbt, hipStream_t st) {
   const int wpb = fwd_waves_per_block(wave_bytes);
   const size_t lds = size_t(wpb) * wave_bytes;
   if (lds > 65536) {
@@ -439,21 +485,22 @@ static hipError_t launch_fwd_kern(Kern kern, const FwdArgs& a, size_t wave_bytes
     if (e != hipSuccess) return e;
   }
   const int64_t waves = (a.t.N + 511) / 512;
-  hipLaunchKernelGGL(kern, dim3(unsigned((waves + wpb - 1) / wpb)), dim3(64 * wpb), lds, st, a);
+  hipLaunchKernelGGL(kern, dim3(unsigned((waves + wpb - 1) / wpb)), dim3(64 * wpb), lds, st, a, nbt);
   return hipGetLastError();
 }
 
 template <int WD, int OD, int MD>
 static hipError_t launch_fwd_k(const FwdArgs& a, int k, hipStream_t st) {
-  const size_t wb = wave_lds_bytes(a.t.logg, k);
+  const int nbt = (MD == 1 && use_neighbour_table(a.t.logg, k)) ? 1 : 0;
+  const size_t wb = wave_lds_bytes(a.t.logg, k, nbt != 0);
   switch (k) {
-    case 1: return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, 1>, a, wb, st);
-    case 2: return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, 2>, a, wb, st);
-    case 3: return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, 3>, a, wb, st);
-    case 4: return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, 4>, a, wb, st);
-    case 5: return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, 5>, a, wb, st);
-    case 6: return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, 6>, a, wb, st);
-    default: return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, 7>, a, wb, st);
+    case 1: return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, 1>, a, wb, nbt, st);
+    case 2: return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, 2>, a, wb, nbt, st);
+    case 3: return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, 3>, a, wb, nbt, st);
+    case 4: return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, 4>, a, wb, nbt, st);
+    case 5: return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, 5>, a, wb, nbt, st);
+    case 6: return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, 6>, a, wb, nbt, st);
+    default: return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, 7>, a, wb, nbt, st);
   }
 }
 
