@@ -284,6 +284,44 @@ uq_status uniquan_init_greedy(int64_t R, int64_t C, int k, int g,
                               void* stream);
 
 /*
+ * uniquan_init_unified -- unified initialisation of Theta_{I_F} (Sec. 3
+ * "Unified initialization"; appendix algorithms "Unified Initialization" and
+ * "General alternating update"; appendix "Details of clipping strategies").
+ *
+ * Per group (w = its g weights, w_m / w_M their min / max, L1 = 2^k - 1):
+ *   for j = 1..grid_G, gamma = j / grid_G (fp32 division):
+ *     Delta' = (gamma (w_M - w_m)) / L1, or 1 if that is not > 0;
+ *     z'_U   = -(w_m / Delta')              clip 0, fixed minimum
+ *              L1 - (w_M / Delta')          clip 1, fixed maximum
+ *              -((gamma w_m) / Delta')      clip 2, balanced
+ *     wbar   = (w / Delta') + z'_U          (T_F with s = 1, s_r = 1)
+ *     z_B = L1 / 2; greedy start on wbar - z_B (as uniquan_init_greedy);
+ *     alt_T rounds of: alpha <- (C^T C)^{-1} C^T (wbar - z_B);
+ *                      C <- nearest level's code of each wbar (FULL rule);
+ *                      z_B <- mean(wbar - C alpha) when grid_G == 1;
+ *     e' = ||w - what||^2, what = the fp32 output of uniquan_fq_fwd (FULL);
+ *   keep the first candidate, then any with strictly smaller e'.
+ * Fixed fp32 evaluation order: group sums are pairwise with adjacent pairing;
+ * the inverse of C^T C is exact (integer adjugate over the determinant), its
+ * product with C^T (wbar - z_B) formed in fp64 and rounded to fp32; a singular
+ * C^T C keeps the previous alpha.  Results are bit-reproducible.
+ *
+ * W [R*C] w_dtype (16-byte aligned).  Out (fp32, caller-owned): delta, z_u,
+ * z_b [Gn], alpha [Gn*k].  Optional out (NULL = skipped): codes [R*C] uint8,
+ * the kept candidate's FULL-mapping codes (bit 7 clear; 8-byte aligned);
+ * err [Gn], its e'; s [R*C] and s_r [R] filled with 1.
+ * Limits: 1 <= k <= 4 (UQ_EUNSUPPORTED above), g a power of two in 8..512,
+ * 1 <= grid_G <= 4096, 0 <= alt_T <= 10000, clip in {0, 1, 2} (UQ_EINVAL).
+ * Preconditions (not checked): finite weights whose squares are finite.
+ */
+uq_status uniquan_init_unified(int64_t R, int64_t C, int k, int g,
+                               const void* W, int w_dtype,
+                               int grid_G, int alt_T, int clip,
+                               float* delta, float* z_u, float* alpha, float* z_b,
+                               uint8_t* codes, float* err, float* s, float* s_r,
+                               void* stream);
+
+/*
  * uniquan_sgd -- theta[i] -= lr * grad[i] for i < n (the stochastic
  * gradient descent update of Algorithm 1, applied per parameter tensor).
  * theta, grad fp32 [n].

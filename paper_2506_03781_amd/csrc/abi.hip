@@ -222,6 +222,23 @@ uq_status uniquan_init_greedy(int64_t R, int64_t C, int k, int g, const void* W,
   return hip_status(fn, uq::launch_greedy(p, static_cast<hipStream_t>(stream)));
 }
 
+uq_status uniquan_init_unified(int64_t R, int64_t C, int k, int g, const void* W, int w_dtype, int grid_G,
+                               int alt_T, int clip, float* delta, float* z_u, float* alpha, float* z_b,
+                               uint8_t* codes, float* err, float* s, float* s_r, void* stream) {
+  const char* fn = "uniquan_init_unified";
+  if (uq_status st = check_quant_shape(fn, R, C, k, g)) return st;
+  if (k > 4) return fail(UQ_EUNSUPPORTED, "%s: k = %d, supported 1..4", fn, k);
+  if (!is_dtype(w_dtype)) return fail(UQ_EINVAL, "%s: bad dtype", fn);
+  if (grid_G < 1 || grid_G > 4096) return fail(UQ_EINVAL, "%s: grid_G = %d, must be in 1..4096", fn, grid_G);
+  if (alt_T < 0 || alt_T > 10000) return fail(UQ_EINVAL, "%s: alt_T = %d, must be in 0..10000", fn, alt_T);
+  if (clip < 0 || clip > 2) return fail(UQ_EINVAL, "%s: clip = %d, must be 0, 1 or 2", fn, clip);
+  REQ_PTR(W, 16); REQ_PTR(delta, 4); REQ_PTR(z_u, 4); REQ_PTR(alpha, 4); REQ_PTR(z_b, 4);
+  OPT_PTR(codes, 8); OPT_PTR(err, 4); OPT_PTR(s, 16); OPT_PTR(s_r, 4);
+  uq::InitUnifiedLaunch p{R, C, k, g, W, w_dtype, grid_G, alt_T, clip,
+                          delta, z_u, alpha, z_b, codes, err, s, s_r};
+  return hip_status(fn, uq::launch_init_unified(p, static_cast<hipStream_t>(stream)));
+}
+
 uq_status uniquan_sgd(int64_t n, float* theta, const float* grad, float lr, void* stream) {
   const char* fn = "uniquan_sgd";
   if (n < 1) return fail(UQ_EINVAL, "%s: n must be >= 1", fn);

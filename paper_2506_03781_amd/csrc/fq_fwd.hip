@@ -74,41 +74,6 @@ static size_t tile_lds_bytes(const TileGeom& t) {
   return ((e * 10 + 15) & ~size_t(15)) + 16 * size_t(t.tile_groups);
 }
 
-// Forward kernel.  Each wavefront owns 512 consecutive weights (8 per lane;
-// groups never straddle waves since g divides 512) and keeps the level
-// tables of its 512/g groups in a private LDS region, so the table build
-// needs only wave-local ordering and no workgroup barrier.  The lane issues
-// its W, s (and code) loads first; while they are in flight the wave builds
-// its tables: one lane per level computes q(b), then ranks it among the
-// group's levels by counting (sort key (value, code)).
-__device__ __forceinline__ void wave_lds_sync() {
-  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
-  __builtin_amdgcn_wave_barrier();
-}
-
-template <int LOGL>
-__device__ __forceinline__ int nearest_full_k(const float* __restrict__ q, float x, float& dist) {
-  constexpr int L = 1 << LOGL;
-  int pos = 0;  // number of levels <= x among q[0 .. L-2]
-#pragma unroll
-  for (int step = L >> 1; step >= 1; step >>= 1) pos += (q[pos + step - 1] <= x) ? step : 0;
-  const int a = pos > 0 ? pos - 1 : 0;
-  const int b = pos;
-  const float da = fabsf(x - q[a]);
-  const float db = fabsf(x - q[b]);
-  if (db < da) {
-    dist = db;
-    return b;
-  }
-  int j = a;
-  if (a > 0 && fabsf(x - q[a - 1]) == da) {  // run of equal distances: take its first element
-    j = 0;
-    while (j < a && fabsf(x - q[j]) != da) ++j;
-  }
-  dist = da;
-  return j;
-}
-
 // Per-wave LDS bytes: the level tables of (512/g) groups of 2^k levels,
 // optionally the local-mapping neighbour table (16 B per level), and 4
 // floats per group.
@@ -122,6 +87,13 @@ __host__ __device__ inline size_t wave_lds_bytes(int logg, int k, bool nbt) {
 // level, at most 4096 levels per wave).
 static bool use_neighbour_table(int logg, int k) { return ((size_t(512) >> logg) << k) <= 4096; }
 
+// Forward kernel.  Each wavefront owns 512 consecutive weights (8 per lane;
+// groups never straddle waves since g divides 512) and keeps the level
+// tables of its 512/g groups in a private LDS region, so the table build
+// needs only wave-local ordering and no workgroup barrier.  The lane issues
+// its W, s (and code) loads first; while they are in flight the wave builds
+// its tables: one lane per level computes q(b), then ranks it among the
+// group's levels by counting (sort key (value, code)).
 template <int WDT, int ODT, int MODE, int LOGL>
 __global__ __launch_bounds__(kThreads) void fq_fwd_kernel(FwdArgs a, int nbt) {
   extern __shared__ __attribute__((aligned(16))) char smem[];

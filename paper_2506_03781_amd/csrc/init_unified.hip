@@ -1,0 +1,370 @@
+// Unified initialisation of UniQuan_F's parameters (Sec. 3 "Unified
+// initialization"; appendix algorithms "Unified Initialization" and "General
+// alternating update"; appendix "Details of clipping strategies").
+//
+// Per group of g weights: a grid search over gamma = j/G of candidate
+// (Delta', z'_U) from a clipping strategy; for each, wbar = T_F(w) with
+// s = s_r = 1, the general alternating update (greedy start, then T rounds of
+// least-squares alpha, nearest codes and, with a one-point grid, the mean
+// shift z_B), and the error ||w - Q*(w)||^2; the first smallest error wins.
+//
+// Mapping: each lane holds 8 consecutive weights, a group is g/8 adjacent
+// lanes, a wavefront 512 weights.  Everything stays in registers except each
+// group's 2^k-level table (LDS, wave-private).  The arithmetic follows one
+// fixed order so that every code and every scale is reproducible:
+//   * group sums are pairwise with adjacent pairing: a lane's 8 values as
+//     ((v0+v1)+(v2+v3))+((v4+v5)+(v6+v7)), then xor-butterflies over lane
+//     distance 1, 2, 4, ... (each step adds the sibling subtree);
+//   * C^T C holds integers; its inverse is exact: alpha_a =
+//     fp32( fp64(sum_b adj_ab v_b) / det ) with the integer adjugate, where
+//     every product adj_ab v_b is exact in fp64 (|adj| < 2^30, v is fp32);
+//     det = 0 keeps the previous alpha;
+//   * nearest level: first minimum of |fl(wbar - q)| over the ascending table
+//     (the forward's rule), a constant group takes Delta' = 1.
+// ALU-bound: the weights are read once and stay in registers for all G * T
+// rounds.
+#include "uq_device.h"
+#include "uq_launch.h"
+
+namespace uq {
+
+struct InitArgs {
+  int64_t N;
+  int logg, gpr, G, T, clip;
+  const void* W;
+  float* delta;
+  float* z_u;
+  float* alpha;
+  float* z_b;
+  uint8_t* codes;
+  float* err;
+  float* s;
+  float* s_r;
+};
+
+// Pairwise sum over a group: the lane's 8 values, then lane distances 1, 2, ...
+__device__ __forceinline__ float group_sum(const float (&v)[8], int lpg) {
+  float t = ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
+  for (int m = 1; m < lpg; m <<= 1) t = t + __shfl_xor(t, m, 64);
+  return t;
+}
+
+__device__ __forceinline__ int group_isum(int t, int lpg) {
+  for (int m = 1; m < lpg; m <<= 1) t += __shfl_xor(t, m, 64);
+  return t;
+}
+
+// Signed minors of C^T C.  M is symmetric with |M_ab| <= g <= 512.
+__device__ __forceinline__ int det2(int a, int b, int c, int d) { return a * d - b * c; }
+
+template <int K>
+__device__ __forceinline__ int cofactor(const int (&M)[K][K], int r, int c) {
+  // (-1)^(r+c) det(M without row r and column c); r, c are compile-time after
+  // unrolling, so the index maps resolve statically.
+  int S[3][3];
+#pragma unroll
+  for (int i = 0, ii = 0; i < K; ++i) {
+    if (i == r) continue;
+#pragma unroll
+    for (int j = 0, jj = 0; j < K; ++j) {
+      if (j == c) continue;
+      S[ii][jj] = M[i][j];
+      ++jj;
+    }
+    ++ii;
+  }
+  int d;
+  if constexpr (K == 2) {
+    d = S[0][0];
+  } else if constexpr (K == 3) {
+    d = det2(S[0][0], S[0][1], S[1][0], S[1][1]);
+  } else {
+    d = S[0][0] * det2(S[1][1], S[1][2], S[2][1], S[2][2]) -
+        S[0][1] * det2(S[1][0], S[1][2], S[2][0], S[2][2]) +
+        S[0][2] * det2(S[1][0], S[1][1], S[2][0], S[2][1]);
+  }
+  return ((r + c) & 1) ? -d : d;
+}
+
+// alpha = (C^T C)^{-1} v with the exact inverse adj / det; unchanged if det = 0.
+template <int K>
+__device__ __forceinline__ void solve_alpha(const int (&M)[K][K], const float (&v)[K], float (&al)[K]) {
+  int adj[K][K];
+  if constexpr (K == 1) {
+    adj[0][0] = 1;
+  } else {
+#pragma unroll
+    for (int a = 0; a < K; ++a)
+#pragma unroll
+      for (int b = 0; b < K; ++b) adj[a][b] = cofactor<K>(M, b, a);
+  }
+  double det = 0.0;  // Laplace along row 0; exact (|terms| < 2^40)
+#pragma unroll
+  for (int b = 0; b < K; ++b) det = det + double(M[0][b]) * double(adj[b][0]);
+  if (det == 0.0) return;
+#pragma unroll
+  for (int a = 0; a < K; ++a) {
+    double S = double(adj[a][0]) * double(v[0]);
+#pragma unroll
+    for (int b = 1; b < K; ++b) S = S + double(adj[a][b]) * double(v[b]);
+    al[a] = float(S / det);
+  }
+}
+
+// Ascending level table of the lane's group in LDS (raw, sorted, code_of).
+// jl = lane index within the group.
+template <int K>
+__device__ __forceinline__ void build_table(float* raw, float* qs, uint8_t* cof, const float (&al)[K], float zb,
+                                            int jl, int lpg) {
+  constexpr int L = 1 << K;
+  for (int b = jl; b < L; b += lpg) {
+    float q = zb;
+#pragma unroll
+    for (int i = 0; i < K; ++i) q = ((b >> i) & 1) ? q + al[i] : q - al[i];
+    raw[b] = q;
+  }
+  wave_lds_sync();
+  for (int b = jl; b < L; b += lpg) {
+    const float q = raw[b];
+    int rank = 0;
+#pragma unroll
+    for (int b2 = 0; b2 < L; ++b2) {
+      const float q2 = raw[b2];
+      rank += (q2 < q) | ((q2 == q) & (b2 < b));
+    }
+    qs[rank] = q;
+    cof[rank] = uint8_t(b);
+  }
+  wave_lds_sync();
+}
+
+__host__ __device__ inline size_t init_wave_lds_bytes(int logg, int k) {
+  const size_t e = (size_t(512) >> logg) << k;  // levels per wave
+  return (e * 9 + 15) & ~size_t(15);
+}
+
+template <int WDT, int K>
+__global__ __launch_bounds__(kThreads) void init_unified_kernel(InitArgs a) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  constexpr int L = 1 << K;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int lpg = 1 << (a.logg - 3);
+  const int jl = lane & (lpg - 1);
+  const int64_t wave_off = (int64_t(blockIdx.x) * (kThreads / 64) + wave) * 512;
+  if (wave_off >= a.N) return;  // whole wavefront past the end (no block barriers below)
+  const int64_t off = wave_off + lane * 8;
+  const bool active = off < a.N;
+  const int64_t gid = active ? (off >> a.logg) : 0;
+
+  // This group's table in the wave's LDS region.
+  char* wbase = smem + size_t(wave) * init_wave_lds_bytes(a.logg, K);
+  const int gl = lane / lpg;  // group index within the wave
+  const int gpw = 64 / lpg;
+  float* raw = reinterpret_cast<float*>(wbase) + gl * L;
+  float* qs = reinterpret_cast<float*>(wbase) + (gpw + gl) * L;
+  uint8_t* cof = reinterpret_cast<uint8_t*>(wbase) + size_t(2 * gpw * L) * 4 + gl * L;
+
+  float w[8];
+  if (active) {
+    load8<WDT>(a.W, off, w);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) w[i] = 0.0f;
+  }
+  float wm = w[0], wM = w[0];
+#pragma unroll
+  for (int i = 1; i < 8; ++i) {
+    wm = fminf(wm, w[i]);
+    wM = fmaxf(wM, w[i]);
+  }
+  for (int m = 1; m < lpg; m <<= 1) {
+    wm = fminf(wm, __shfl_xor(wm, m, 64));
+    wM = fmaxf(wM, __shfl_xor(wM, m, 64));
+  }
+
+  const float L1 = float(L - 1);
+  const float zb0 = L1 * 0.5f;
+  const float inv_g = 1.0f / float(1 << a.logg);  // exact power of two
+  const int g = 1 << a.logg;
+
+  float best_d = 1.0f, best_zu = 0.0f, best_zb = zb0, best_e = 0.0f, best_al[K];
+  uint32_t best_c0 = 0, best_c1 = 0;
+#pragma unroll
+  for (int b = 0; b < K; ++b) best_al[b] = 0.0f;
+
+  for (int j = 1; j <= a.G; ++j) {
+    const float gamma = float(j) / float(a.G);
+    float dl = (gamma * (wM - wm)) / L1;
+    if (!(dl > 0.0f)) dl = 1.0f;
+    float zu;
+    if (a.clip == 0) zu = -(wm / dl);
+    else if (a.clip == 1) zu = L1 - (wM / dl);
+    else zu = -((gamma * wm) / dl);
+
+    float wbar[8], x[8];
+    float zb = zb0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      wbar[i] = (w[i] / dl) + zu;
+      x[i] = wbar[i] - zb;
+    }
+
+    // Greedy start: one bit at a time.
+    float al[K];
+    int code[8];
+    {
+      float r[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        r[i] = x[i];
+        code[i] = 0;
+      }
+#pragma unroll
+      for (int b = 0; b < K; ++b) {
+        float ab[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) ab[i] = fabsf(r[i]);
+        const float ai = group_sum(ab, lpg) * inv_g;
+        al[b] = ai;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const bool plus = r[i] >= 0.0f;
+          code[i] |= int(plus) << b;
+          r[i] = plus ? r[i] - ai : r[i] + ai;
+        }
+      }
+    }
+
+    for (int t = 0; t < a.T; ++t) {
+      // alpha <- (C^T C)^{-1} C^T (wbar - z_B)
+      float v[K];
+#pragma unroll
+      for (int b = 0; b < K; ++b) {
+        float sx[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) sx[i] = ((code[i] >> b) & 1) ? x[i] : -x[i];
+        v[b] = group_sum(sx, lpg);
+      }
+      int M[K][K];
+      {
+        int mb[K];  // bit b of every weight's code as an 8-bit mask
+#pragma unroll
+        for (int b = 0; b < K; ++b) {
+          int m = 0;
+#pragma unroll
+          for (int i = 0; i < 8; ++i) m |= ((code[i] >> b) & 1) << i;
+          mb[b] = m;
+        }
+#pragma unroll
+        for (int p = 0; p < K; ++p) {
+          M[p][p] = g;
+#pragma unroll
+          for (int q = p + 1; q < K; ++q) {
+            const int dis = group_isum(__builtin_popcount(mb[p] ^ mb[q]), lpg);
+            M[p][q] = g - 2 * dis;
+            M[q][p] = M[p][q];
+          }
+        }
+      }
+      solve_alpha<K>(M, v, al);
+
+      // C <- nearest level's code
+      build_table<K>(raw, qs, cof, al, zb, jl, lpg);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        float dist;
+        code[i] = cof[nearest_full_k<K>(qs, wbar[i], dist)];
+      }
+
+      // z_B <- mean(wbar - C alpha), only with a one-point grid
+      if (a.G == 1) {
+        float dd[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          float ca = 0.0f;
+#pragma unroll
+          for (int b = 0; b < K; ++b) ca = ((code[i] >> b) & 1) ? ca + al[b] : ca - al[b];
+          dd[i] = wbar[i] - ca;
+        }
+        zb = group_sum(dd, lpg) * inv_g;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) x[i] = wbar[i] - zb;
+      }
+    }
+
+    // Candidate error ||w - Q*(w)||^2 with the forward's FULL mapping.
+    build_table<K>(raw, qs, cof, al, zb, jl, lpg);
+    float e2[8];
+    uint32_t c0 = 0, c1 = 0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      float dist;
+      const int pos = nearest_full_k<K>(qs, wbar[i], dist);
+      const uint32_t cb = cof[pos];
+      if (i < 4) c0 |= cb << (8 * i);
+      else c1 |= cb << (8 * (i - 4));
+      const float what = dl * (qs[pos] - zu);
+      const float d = w[i] - what;
+      e2[i] = d * d;
+    }
+    const float e = group_sum(e2, lpg);
+    if (j == 1 || e < best_e) {
+      best_e = e;
+      best_d = dl;
+      best_zu = zu;
+      best_zb = zb;
+#pragma unroll
+      for (int b = 0; b < K; ++b) best_al[b] = al[b];
+      best_c0 = c0;
+      best_c1 = c1;
+    }
+  }
+
+  if (!active) return;
+  if (a.codes) store8u8(a.codes, off, make_uint2(best_c0, best_c1));
+  if (a.s) {
+    const float one[8] = {1.0f, 1.0f, 1.0f, 1.0f, 1.0f, 1.0f, 1.0f, 1.0f};
+    store8f(a.s, off, one);
+  }
+  if (jl == 0) {
+    a.delta[gid] = best_d;
+    a.z_u[gid] = best_zu;
+    a.z_b[gid] = best_zb;
+#pragma unroll
+    for (int b = 0; b < K; ++b) a.alpha[gid * K + b] = best_al[b];
+    if (a.err) a.err[gid] = best_e;
+    if (a.s_r && (gid % a.gpr) == 0) a.s_r[gid / a.gpr] = 1.0f;
+  }
+}
+
+template <int WDT>
+static hipError_t launch_init_k(const InitArgs& a, int k, dim3 grid, size_t lds, hipStream_t st) {
+  switch (k) {
+    case 1: hipLaunchKernelGGL((init_unified_kernel<WDT, 1>), grid, dim3(kThreads), lds, st, a); break;
+    case 2: hipLaunchKernelGGL((init_unified_kernel<WDT, 2>), grid, dim3(kThreads), lds, st, a); break;
+    case 3: hipLaunchKernelGGL((init_unified_kernel<WDT, 3>), grid, dim3(kThreads), lds, st, a); break;
+    default: hipLaunchKernelGGL((init_unified_kernel<WDT, 4>), grid, dim3(kThreads), lds, st, a); break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_init_unified(const InitUnifiedLaunch& p, hipStream_t st) {
+  InitArgs a;
+  a.N = p.R * p.C;
+  a.logg = __builtin_ctz(unsigned(p.g));
+  a.gpr = int(p.C / p.g);
+  a.G = p.grid_G;
+  a.T = p.alt_T;
+  a.clip = p.clip;
+  a.W = p.W;
+  a.delta = p.delta; a.z_u = p.z_u; a.alpha = p.alpha; a.z_b = p.z_b;
+  a.codes = p.codes; a.err = p.err; a.s = p.s; a.s_r = p.s_r;
+  const int64_t waves = (a.N + 511) / 512;
+  const dim3 grid(unsigned((waves + 3) / 4));
+  const size_t lds = 4 * init_wave_lds_bytes(a.logg, p.k);
+  if (p.w_dtype == BF16) return launch_init_k<BF16>(a, p.k, grid, lds, st);
+  return launch_init_k<F32>(a, p.k, grid, lds, st);
+}
+
+}  // namespace uq

@@ -194,4 +194,36 @@ __device__ __forceinline__ int nearest_local(const float* __restrict__ q, int L,
   return best;
 }
 
+// Makes a wavefront's earlier LDS writes visible to its later LDS reads from
+// other lanes: LDS executes one wavefront's instructions in order, so waiting
+// for its own outstanding LDS operations is enough (no workgroup barrier).
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+  __builtin_amdgcn_wave_barrier();
+}
+
+// nearest_full with the table size fixed at compile time (unrolled search).
+template <int LOGL>
+__device__ __forceinline__ int nearest_full_k(const float* __restrict__ q, float x, float& dist) {
+  constexpr int L = 1 << LOGL;
+  int pos = 0;  // number of levels <= x among q[0 .. L-2]
+#pragma unroll
+  for (int step = L >> 1; step >= 1; step >>= 1) pos += (q[pos + step - 1] <= x) ? step : 0;
+  const int a = pos > 0 ? pos - 1 : 0;
+  const int b = pos;
+  const float da = fabsf(x - q[a]);
+  const float db = fabsf(x - q[b]);
+  if (db < da) {
+    dist = db;
+    return b;
+  }
+  int j = a;
+  if (a > 0 && fabsf(x - q[a - 1]) == da) {  // run of equal distances: take its first element
+    j = 0;
+    while (j < a && fabsf(x - q[j]) != da) ++j;
+  }
+  dist = da;
+  return j;
+}
+
 }  // namespace uq

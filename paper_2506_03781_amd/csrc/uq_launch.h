@@ -57,6 +57,15 @@ struct GreedyLaunch {
   const float* z_b; float* alpha;
 };
 
+struct InitUnifiedLaunch {
+  int64_t R, C;
+  int k, g;
+  const void* W; int w_dtype;
+  int grid_G, alt_T, clip;
+  float* delta; float* z_u; float* alpha; float* z_b;
+  uint8_t* codes; float* err; float* s; float* s_r;
+};
+
 // GEMM epilogues of the reconstruction contractions.
 enum GemmEpi : int {
   EPI_TARGET = 0,     // out fp32 = acc
@@ -81,6 +90,7 @@ hipError_t launch_fq_bwd(const FqBwdLaunch& p, hipStream_t st);
 hipError_t launch_fold(const FoldLaunch& p, hipStream_t st);
 hipError_t launch_dequant(const DequantLaunch& p, hipStream_t st);
 hipError_t launch_greedy(const GreedyLaunch& p, hipStream_t st);
+hipError_t launch_init_unified(const InitUnifiedLaunch& p, hipStream_t st);
 hipError_t launch_gemm(const GemmLaunch& p, hipStream_t st);
 size_t gemm_workgroups(int64_t M, int64_t N, int epi);
 hipError_t launch_reduce_loss(const float* partials, int64_t n, float* loss, hipStream_t st);

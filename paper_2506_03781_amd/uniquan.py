@@ -49,6 +49,8 @@ _SIGS = {
     "uniquan_fold_to_bcq": ([_i64, _i64, _i32, _i32, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp], _i32),
     "uniquan_bcq_dequant": ([_i64, _i64, _i32, _i32, _vp, _vp, _vp, _vp, _i32, _vp], _i32),
     "uniquan_init_greedy": ([_i64, _i64, _i32, _i32, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp], _i32),
+    "uniquan_init_unified": ([_i64, _i64, _i32, _i32, _vp, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp,
+                              _vp, _vp, _vp, _vp, _vp], _i32),
     "uniquan_sgd": ([_i64, _vp, _vp, _f32, _vp], _i32),
 }
 
@@ -209,6 +211,16 @@ def uniquan_init_greedy(R, C, k, g, W, s, s_r, delta, z_u, z_b, alpha, stream=No
         R, C, k, g, _p(W, N, _W, "W"), _dt(W), _p(s, N, _F, "s"), _p(s_r, R, _F, "s_r"),
         _p(delta, Gn, _F, "delta"), _p(z_u, Gn, _F, "z_u"), _p(z_b, Gn, _F, "z_b"),
         _p(alpha, Gn * k, _F, "alpha"), _stream(stream)))
+
+
+def uniquan_init_unified(R, C, k, g, W, grid_G, alt_T, clip, delta, z_u, alpha, z_b,
+                         codes=None, err=None, s=None, s_r=None, stream=None):
+    N, Gn = R * C, R * C // g
+    _check(lib().uniquan_init_unified(
+        R, C, k, g, _p(W, N, _W, "W"), _dt(W), int(grid_G), int(alt_T), int(clip),
+        _p(delta, Gn, _F, "delta"), _p(z_u, Gn, _F, "z_u"), _p(alpha, Gn * k, _F, "alpha"),
+        _p(z_b, Gn, _F, "z_b"), _p(codes, N, _U8, "codes"), _p(err, Gn, _F, "err"),
+        _p(s, N, _F, "s"), _p(s_r, R, _F, "s_r"), _stream(stream)))
 
 
 def uniquan_sgd(theta, grad, lr, stream=None):

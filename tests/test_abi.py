@@ -105,6 +105,26 @@ def test_other_validation(L):
     assert L.uniquan_bcq_dequant(4, 256, 3, 128, FAKE, FAKE, FAKE, FAKE, 5, None) == uq.UQ_EINVAL
     assert L.uniquan_init_greedy(4, 256, 3, 100, FAKE, 1, FAKE, None, None, None, FAKE, FAKE, None) == uq.UQ_EINVAL
     assert L.uniquan_sgd(0, FAKE, FAKE, ctypes.c_float(0.1), None) == uq.UQ_EINVAL
+
+
+@pytest.mark.parametrize("kw,status,text", [
+    (dict(k=5), uq.UQ_EUNSUPPORTED, "k = 5"),
+    (dict(G=0), uq.UQ_EINVAL, "grid_G"),
+    (dict(G=4097), uq.UQ_EINVAL, "grid_G"),
+    (dict(T=-1), uq.UQ_EINVAL, "alt_T"),
+    (dict(clip=3), uq.UQ_EINVAL, "clip"),
+    (dict(g=100), uq.UQ_EINVAL, "g=100"),
+    (dict(alpha=None), uq.UQ_EINVAL, "alpha"),
+    (dict(codes=FAKE + 4), uq.UQ_EINVAL, "codes"),
+    (dict(W=ODD), uq.UQ_EINVAL, "W"),
+])
+def test_init_unified_validation(L, kw, status, text):
+    a = dict(k=3, g=128, G=30, T=15, clip=0, W=FAKE, alpha=FAKE, codes=None)
+    a.update(kw)
+    st = L.uniquan_init_unified(4, 256, a["k"], a["g"], a["W"], 1, a["G"], a["T"], a["clip"],
+                                FAKE, FAKE, a["alpha"], FAKE, a["codes"], None, None, None, None)
+    assert st == status
+    assert text in uq.last_error()
     assert L.uniquan_transpose_bf16(12, 16, FAKE, FAKE, None) == uq.UQ_EINVAL
 
 
