@@ -10,6 +10,10 @@ A step is one pass of the whole hot path over one batch, for every
 with the mapping schedule of the paper's local and periodic mapping (p = 2:
 local remap on even steps, frozen codes otherwise; the initial full mapping
 is part of set-up).  Inputs are synthetic and resident in HBM before timing.
+Set-up initialises every layer with the unified initialisation (grid search
+over clipping ranges with the general alternating update, G = 30, T = 15 by
+default); its kernel time is reported under ``init`` with an ALU roofline and
+its own CPU-oracle baseline, outside the timed steps.
 
 Output: one JSON line.  ``value`` is the fake-quant fwd+bwd throughput in
 Gweights/s (weights quantized forward and backward per second of quantizer
@@ -35,6 +39,9 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+# Plain 32-bit VALU operations per second: the 157.3 TFLOP/s fp32 vector peak
+# (256 CUs x 128 FMA lanes per clock x 2.4 GHz) counts an FMA as 2 flops.
+VALU_PEAK_TOPS = 157.3 / 2
 PROFILES = os.path.join(ROOT, "profiles")
 CSRC = os.path.join(ROOT, "paper_2506_03781_amd", "csrc")
 
@@ -48,6 +55,11 @@ def parse():
     ap.add_argument("--mode", default="paper", choices=["paper", "full", "local", "frozen"])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--init", default="unified", choices=["unified", "greedy"],
+                    help="parameter initialisation (set-up, timed separately from the steps)")
+    ap.add_argument("--init-grid", type=int, default=30, help="grid points G of the unified init")
+    ap.add_argument("--init-rounds", type=int, default=15, help="alternating rounds T of the unified init")
+    ap.add_argument("--init-clip", type=int, default=0, help="0 fixed min, 1 fixed max, 2 balanced")
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run a plain 256 MiB device copy (counter calibration)")
     return ap.parse_args()
@@ -68,6 +80,40 @@ def fq_bytes_per_weight(k, g, mode, w_bytes=2, what_bytes=2, grad_bytes=2):
     # dL/dWhat, W, s, code in; s out; per group Delta, z_U in, alpha, z_B in and out
     bwd = grad_bytes + w_bytes + 4 + 1 + 4 + (8 + 2 * (4 * k + 4)) / g
     return fwd, bwd
+
+
+def init_ops_per_weight(k, G, T):
+    """Algorithmic VALU operations per weight of the unified initialisation:
+    per grid point the transform (2) and shifted copy (1), the greedy start
+    (4 per bit: |r|, sum, sign test, residual update), per alternating round
+    the signed sums (2k), the C^T C counts (k(k-1)/2), the nearest-level search
+    (k compares, 2 distances, 2 |.|, 1 compare) and with a one-point grid the
+    shift update (k + 3), and the candidate error (search k + 5, detransform 2,
+    difference, square, sum)."""
+    rnd = 2 * k + k * (k - 1) // 2 + (k + 5) + ((k + 3) if G == 1 else 0)
+    per_point = 3 + 4 * k + T * rnd + (k + 5) + 5
+    return G * per_point
+
+
+def cpu_baseline_init(W, k, g, G, T, clip, budget_s=3.0):
+    """The oracle's unified initialisation on the first groups of a matrix,
+    numpy restricted to one thread."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+    import oracle.unified_init as UI
+    Wg = np.asarray(W, np.float32).reshape(-1, g)
+    n = 2
+    with threadpool_limits(1):
+        while True:
+            t0 = time.perf_counter()
+            UI.unified_init(Wg[:n], k, g, G=G, T=T, clip=clip)
+            dt = time.perf_counter() - t0
+            if dt >= budget_s / 3 or n * 2 > Wg.shape[0]:
+                break
+            n *= 2
+    return {"value": n * g / dt / 1e9, "unit": "Gweights/s", "cores": 1, "kind": "oracle",
+            "sample": f"oracle unified_init (G={G}, T={T}, k={k}) on the first {n} groups of "
+                      f"{g} weights, numpy on one thread: {dt:.2f} s"}
 
 
 def schedule(mode, step):
@@ -156,12 +202,26 @@ def main():
     g = wl.group_size
     layers = []
     host_np = []
+    init_ms = []
+    init_np = None
     for spec in wl.matrices:
         m = synth.make_matrix(spec, args.seed)
         wdt = torch.bfloat16 if spec.dtype == "bf16" else torch.float32
         for k in wl.ks:
             lay = QuantLayer(m.W, m.X, m.s, k, g, w_dtype=wdt)
-            lay.init_greedy()
+            if args.init == "unified":
+                if not layers:
+                    lay.init_unified(args.init_grid, args.init_rounds, args.init_clip)  # first-launch warm-up
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                lay.init_unified(args.init_grid, args.init_rounds, args.init_clip)
+                e1.record()
+                e1.synchronize()
+                init_ms.append(e0.elapsed_time(e1))
+                if init_np is None and not args.no_cpu_baseline:
+                    init_np = (m.W, k, g)
+            else:
+                lay.init_greedy()
             lay.prepare()
             lay.fq_fwd(uq.MAP_FULL)        # initial mapping computes every distance
             layers.append(lay)
@@ -308,6 +368,20 @@ def main():
         "precision": "quantizer: fp32 arithmetic on bf16 W / fp32 s, bf16 What and dL/dWhat; "
                      "GEMMs: bf16 MFMA with fp32 accumulation",
     }
+    if init_ms:
+        iw = sum(l.R * l.C for l in layers)
+        ops = sum(init_ops_per_weight(l.k, args.init_grid, args.init_rounds) * l.R * l.C for l in layers)
+        isec = sum(init_ms) * 1e-3
+        ach = ops / isec / 1e12
+        out["init"] = {
+            "method": "unified", "grid_G": args.init_grid, "alt_T": args.init_rounds, "clip": args.init_clip,
+            "ms_per_layer": init_ms, "ms_total": sum(init_ms), "gweights_per_s": iw / isec / 1e9,
+            "roofline": {"bound": "alu", "achieved": ach, "peak": VALU_PEAK_TOPS, "unit": "Tops/s",
+                         "frac": ach / VALU_PEAK_TOPS, "algorithmic_ops": ops},
+        }
+        if init_np is not None:
+            out["init"]["cpu_baseline"] = cpu_baseline_init(*init_np, args.init_grid, args.init_rounds,
+                                                            args.init_clip)
     if not args.no_cpu_baseline and host_np:
         out["cpu_baseline"] = cpu_baseline(host_np, args.mode)
     print(json.dumps(out), flush=True)

@@ -17,7 +17,8 @@
 //     distance 1, 2, 4, ... (each step adds the sibling subtree);
 //   * C^T C holds integers; its inverse is exact: alpha_a =
 //     fp32( fp64(sum_b adj_ab v_b) / det ) with the integer adjugate, where
-//     every product adj_ab v_b is exact in fp64 (|adj| < 2^30, v is fp32);
+//     every product adj_ab v_b is exact in fp64 (C^T C and its adjugate are
+//     positive semidefinite, so |adj_ab| <= g^3 <= 2^27, and v is fp32);
 //     det = 0 keeps the previous alpha;
 //   * nearest level: first minimum of |fl(wbar - q)| over the ascending table
 //     (the forward's rule), a constant group takes Delta' = 1.
@@ -42,20 +43,59 @@ struct InitArgs {
   float* s_r;
 };
 
+// Value of the lane whose subtree is the sibling of this lane's at butterfly
+// level M (lane distance M).  Levels 1 and 2 pair lanes by xor (quad_perm);
+// from level 4 on every lane of a subtree holds the same partial sum, so the
+// mirror patterns (lane i <-> 7-i within 8, 15-i within 16) reach the sibling
+// subtree as xor would, without going through LDS.
+template <int M>
+__device__ __forceinline__ int sibling(int v) {
+  if constexpr (M == 1) return __builtin_amdgcn_mov_dpp(v, 0xB1, 0xF, 0xF, false);   // quad_perm [1,0,3,2]
+  else if constexpr (M == 2) return __builtin_amdgcn_mov_dpp(v, 0x4E, 0xF, 0xF, false);  // quad_perm [2,3,0,1]
+  else if constexpr (M == 4) return __builtin_amdgcn_mov_dpp(v, 0x141, 0xF, 0xF, false); // row_half_mirror
+  else if constexpr (M == 8) return __builtin_amdgcn_mov_dpp(v, 0x140, 0xF, 0xF, false); // row_mirror
+  else if constexpr (M == 16) return __builtin_amdgcn_ds_swizzle(v, 0x401F);             // lane ^ 16
+  else return __shfl_xor(v, 32, 64);
+}
+
+template <int M>
+__device__ __forceinline__ float sibling(float v) {
+  return __builtin_bit_cast(float, sibling<M>(__builtin_bit_cast(int, v)));
+}
+
+// Butterfly over the LPG lanes of a group (sum, min or max).
+template <int LPG, typename T, typename Op>
+__device__ __forceinline__ T group_reduce(T t, Op op) {
+  if constexpr (LPG >= 2) t = op(t, sibling<1>(t));
+  if constexpr (LPG >= 4) t = op(t, sibling<2>(t));
+  if constexpr (LPG >= 8) t = op(t, sibling<4>(t));
+  if constexpr (LPG >= 16) t = op(t, sibling<8>(t));
+  if constexpr (LPG >= 32) t = op(t, sibling<16>(t));
+  if constexpr (LPG >= 64) t = op(t, sibling<32>(t));
+  return t;
+}
+
+struct AddF { __device__ float operator()(float a, float b) const { return a + b; } };
+struct AddI { __device__ int operator()(int a, int b) const { return a + b; } };
+struct MinF { __device__ float operator()(float a, float b) const { return fminf(a, b); } };
+struct MaxF { __device__ float operator()(float a, float b) const { return fmaxf(a, b); } };
+
 // Pairwise sum over a group: the lane's 8 values, then lane distances 1, 2, ...
-__device__ __forceinline__ float group_sum(const float (&v)[8], int lpg) {
-  float t = ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
-  for (int m = 1; m < lpg; m <<= 1) t = t + __shfl_xor(t, m, 64);
-  return t;
+// (IEEE addition is commutative, so both lanes of a pair hold the same sum).
+template <int LPG>
+__device__ __forceinline__ float group_sum(const float (&v)[8]) {
+  const float t = ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
+  return group_reduce<LPG>(t, AddF());
 }
 
-__device__ __forceinline__ int group_isum(int t, int lpg) {
-  for (int m = 1; m < lpg; m <<= 1) t += __shfl_xor(t, m, 64);
-  return t;
+__device__ __forceinline__ uint32_t pack4(int c0, int c1, int c2, int c3) {
+  return uint32_t(c0) | (uint32_t(c1) << 8) | (uint32_t(c2) << 16) | (uint32_t(c3) << 24);
 }
 
-// Signed minors of C^T C.  M is symmetric with |M_ab| <= g <= 512.
-__device__ __forceinline__ int det2(int a, int b, int c, int d) { return a * d - b * c; }
+// Signed minors of C^T C.  M is symmetric with |M_ab| <= g <= 512, so every
+// factor fits 24 bits (2x2 minors < 2^19) and every product 32 bits: the
+// full-rate 24-bit multiply is exact here.
+__device__ __forceinline__ int det2(int a, int b, int c, int d) { return __mul24(a, d) - __mul24(b, c); }
 
 template <int K>
 __device__ __forceinline__ int cofactor(const int (&M)[K][K], int r, int c) {
@@ -79,9 +119,9 @@ __device__ __forceinline__ int cofactor(const int (&M)[K][K], int r, int c) {
   } else if constexpr (K == 3) {
     d = det2(S[0][0], S[0][1], S[1][0], S[1][1]);
   } else {
-    d = S[0][0] * det2(S[1][1], S[1][2], S[2][1], S[2][2]) -
-        S[0][1] * det2(S[1][0], S[1][2], S[2][0], S[2][2]) +
-        S[0][2] * det2(S[1][0], S[1][1], S[2][0], S[2][1]);
+    d = __mul24(S[0][0], det2(S[1][1], S[1][2], S[2][1], S[2][2])) -
+        __mul24(S[0][1], det2(S[1][0], S[1][2], S[2][0], S[2][2])) +
+        __mul24(S[0][2], det2(S[1][0], S[1][1], S[2][0], S[2][1]));
   }
   return ((r + c) & 1) ? -d : d;
 }
@@ -96,17 +136,23 @@ __device__ __forceinline__ void solve_alpha(const int (&M)[K][K], const float (&
 #pragma unroll
     for (int a = 0; a < K; ++a)
 #pragma unroll
-      for (int b = 0; b < K; ++b) adj[a][b] = cofactor<K>(M, b, a);
+      for (int b = a; b < K; ++b) {
+        adj[a][b] = cofactor<K>(M, b, a);  // adj of a symmetric matrix is symmetric
+        adj[b][a] = adj[a][b];
+      }
   }
-  double det = 0.0;  // Laplace along row 0; exact (|terms| < 2^40)
+  // Laplace along row 0; exact (|terms| < 2^40).  Every product below is
+  // exact in fp64, so fma(p, q, S) equals S + p*q rounded once, as in the
+  // ascending-b sum it implements.
+  double det = 0.0;
 #pragma unroll
-  for (int b = 0; b < K; ++b) det = det + double(M[0][b]) * double(adj[b][0]);
+  for (int b = 0; b < K; ++b) det = __builtin_fma(double(M[0][b]), double(adj[b][0]), det);
   if (det == 0.0) return;
 #pragma unroll
   for (int a = 0; a < K; ++a) {
     double S = double(adj[a][0]) * double(v[0]);
 #pragma unroll
-    for (int b = 1; b < K; ++b) S = S + double(adj[a][b]) * double(v[b]);
+    for (int b = 1; b < K; ++b) S = __builtin_fma(double(adj[a][b]), double(v[b]), S);
     al[a] = float(S / det);
   }
 }
@@ -143,22 +189,22 @@ __host__ __device__ inline size_t init_wave_lds_bytes(int logg, int k) {
   return (e * 9 + 15) & ~size_t(15);
 }
 
-template <int WDT, int K>
+template <int WDT, int K, int LOGG>
 __global__ __launch_bounds__(kThreads) void init_unified_kernel(InitArgs a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   constexpr int L = 1 << K;
+  constexpr int lpg = 1 << (LOGG - 3);  // lanes per group
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int lpg = 1 << (a.logg - 3);
   const int jl = lane & (lpg - 1);
   const int64_t wave_off = (int64_t(blockIdx.x) * (kThreads / 64) + wave) * 512;
   if (wave_off >= a.N) return;  // whole wavefront past the end (no block barriers below)
   const int64_t off = wave_off + lane * 8;
   const bool active = off < a.N;
-  const int64_t gid = active ? (off >> a.logg) : 0;
+  const int64_t gid = active ? (off >> LOGG) : 0;
 
   // This group's table in the wave's LDS region.
-  char* wbase = smem + size_t(wave) * init_wave_lds_bytes(a.logg, K);
+  char* wbase = smem + size_t(wave) * init_wave_lds_bytes(LOGG, K);
   const int gl = lane / lpg;  // group index within the wave
   const int gpw = 64 / lpg;
   float* raw = reinterpret_cast<float*>(wbase) + gl * L;
@@ -178,15 +224,13 @@ __global__ __launch_bounds__(kThreads) void init_unified_kernel(InitArgs a) {
     wm = fminf(wm, w[i]);
     wM = fmaxf(wM, w[i]);
   }
-  for (int m = 1; m < lpg; m <<= 1) {
-    wm = fminf(wm, __shfl_xor(wm, m, 64));
-    wM = fmaxf(wM, __shfl_xor(wM, m, 64));
-  }
+  wm = group_reduce<lpg>(wm, MinF());
+  wM = group_reduce<lpg>(wM, MaxF());
 
   const float L1 = float(L - 1);
   const float zb0 = L1 * 0.5f;
-  const float inv_g = 1.0f / float(1 << a.logg);  // exact power of two
-  const int g = 1 << a.logg;
+  constexpr float inv_g = 1.0f / float(1 << LOGG);  // exact power of two
+  constexpr int g = 1 << LOGG;
 
   float best_d = 1.0f, best_zu = 0.0f, best_zb = zb0, best_e = 0.0f, best_al[K];
   uint32_t best_c0 = 0, best_c1 = 0;
@@ -225,7 +269,7 @@ __global__ __launch_bounds__(kThreads) void init_unified_kernel(InitArgs a) {
         float ab[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) ab[i] = fabsf(r[i]);
-        const float ai = group_sum(ab, lpg) * inv_g;
+        const float ai = group_sum<lpg>(ab) * inv_g;
         al[b] = ai;
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
@@ -236,6 +280,9 @@ __global__ __launch_bounds__(kThreads) void init_unified_kernel(InitArgs a) {
       }
     }
 
+    // Codes packed 4 per word: the C^T C counts and the fixed-point test use them.
+    uint32_t cw0 = pack4(code[0], code[1], code[2], code[3]);
+    uint32_t cw1 = pack4(code[4], code[5], code[6], code[7]);
     for (int t = 0; t < a.T; ++t) {
       // alpha <- (C^T C)^{-1} C^T (wbar - z_B)
       float v[K];
@@ -244,25 +291,24 @@ __global__ __launch_bounds__(kThreads) void init_unified_kernel(InitArgs a) {
         float sx[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) sx[i] = ((code[i] >> b) & 1) ? x[i] : -x[i];
-        v[b] = group_sum(sx, lpg);
+        v[b] = group_sum<lpg>(sx);
       }
       int M[K][K];
       {
-        int mb[K];  // bit b of every weight's code as an 8-bit mask
+        // bit b of the lane's 8 codes, one bit per byte
+        uint32_t p0[K], p1[K];
 #pragma unroll
         for (int b = 0; b < K; ++b) {
-          int m = 0;
-#pragma unroll
-          for (int i = 0; i < 8; ++i) m |= ((code[i] >> b) & 1) << i;
-          mb[b] = m;
+          p0[b] = (cw0 >> b) & 0x01010101u;
+          p1[b] = (cw1 >> b) & 0x01010101u;
         }
 #pragma unroll
         for (int p = 0; p < K; ++p) {
           M[p][p] = g;
 #pragma unroll
           for (int q = p + 1; q < K; ++q) {
-            const int dis = group_isum(__builtin_popcount(mb[p] ^ mb[q]), lpg);
-            M[p][q] = g - 2 * dis;
+            const int dis = __builtin_popcount(p0[p] ^ p0[q]) + __builtin_popcount(p1[p] ^ p1[q]);
+            M[p][q] = g - 2 * group_reduce<lpg>(dis, AddI());
             M[q][p] = M[p][q];
           }
         }
@@ -276,8 +322,11 @@ __global__ __launch_bounds__(kThreads) void init_unified_kernel(InitArgs a) {
         float dist;
         code[i] = cof[nearest_full_k<K>(qs, wbar[i], dist)];
       }
+      const uint32_t nw0 = pack4(code[0], code[1], code[2], code[3]);
+      const uint32_t nw1 = pack4(code[4], code[5], code[6], code[7]);
 
       // z_B <- mean(wbar - C alpha), only with a one-point grid
+      const float zb_prev = zb;
       if (a.G == 1) {
         float dd[8];
 #pragma unroll
@@ -287,10 +336,18 @@ __global__ __launch_bounds__(kThreads) void init_unified_kernel(InitArgs a) {
           for (int b = 0; b < K; ++b) ca = ((code[i] >> b) & 1) ? ca + al[b] : ca - al[b];
           dd[i] = wbar[i] - ca;
         }
-        zb = group_sum(dd, lpg) * inv_g;
+        zb = group_sum<lpg>(dd) * inv_g;
 #pragma unroll
         for (int i = 0; i < 8; ++i) x[i] = wbar[i] - zb;
       }
+
+      // Unchanged codes and shift make this state a fixed point of the round
+      // (the round is a deterministic function of C, z_B and, for a singular
+      // C^T C, alpha), so the remaining rounds would reproduce it exactly.
+      const bool same = (nw0 == cw0) & (nw1 == cw1) & (zb == zb_prev);
+      cw0 = nw0;
+      cw1 = nw1;
+      if (__all(same || !active)) break;
     }
 
     // Candidate error ||w - Q*(w)||^2 with the forward's FULL mapping.
@@ -308,7 +365,7 @@ __global__ __launch_bounds__(kThreads) void init_unified_kernel(InitArgs a) {
       const float d = w[i] - what;
       e2[i] = d * d;
     }
-    const float e = group_sum(e2, lpg);
+    const float e = group_sum<lpg>(e2);
     if (j == 1 || e < best_e) {
       best_e = e;
       best_d = dl;
@@ -338,13 +395,26 @@ __global__ __launch_bounds__(kThreads) void init_unified_kernel(InitArgs a) {
   }
 }
 
+template <int WDT, int K>
+static void launch_init_g(const InitArgs& a, dim3 grid, size_t lds, hipStream_t st) {
+  switch (a.logg) {
+    case 3: hipLaunchKernelGGL((init_unified_kernel<WDT, K, 3>), grid, dim3(kThreads), lds, st, a); break;
+    case 4: hipLaunchKernelGGL((init_unified_kernel<WDT, K, 4>), grid, dim3(kThreads), lds, st, a); break;
+    case 5: hipLaunchKernelGGL((init_unified_kernel<WDT, K, 5>), grid, dim3(kThreads), lds, st, a); break;
+    case 6: hipLaunchKernelGGL((init_unified_kernel<WDT, K, 6>), grid, dim3(kThreads), lds, st, a); break;
+    case 7: hipLaunchKernelGGL((init_unified_kernel<WDT, K, 7>), grid, dim3(kThreads), lds, st, a); break;
+    case 8: hipLaunchKernelGGL((init_unified_kernel<WDT, K, 8>), grid, dim3(kThreads), lds, st, a); break;
+    default: hipLaunchKernelGGL((init_unified_kernel<WDT, K, 9>), grid, dim3(kThreads), lds, st, a); break;
+  }
+}
+
 template <int WDT>
 static hipError_t launch_init_k(const InitArgs& a, int k, dim3 grid, size_t lds, hipStream_t st) {
   switch (k) {
-    case 1: hipLaunchKernelGGL((init_unified_kernel<WDT, 1>), grid, dim3(kThreads), lds, st, a); break;
-    case 2: hipLaunchKernelGGL((init_unified_kernel<WDT, 2>), grid, dim3(kThreads), lds, st, a); break;
-    case 3: hipLaunchKernelGGL((init_unified_kernel<WDT, 3>), grid, dim3(kThreads), lds, st, a); break;
-    default: hipLaunchKernelGGL((init_unified_kernel<WDT, 4>), grid, dim3(kThreads), lds, st, a); break;
+    case 1: launch_init_g<WDT, 1>(a, grid, lds, st); break;
+    case 2: launch_init_g<WDT, 2>(a, grid, lds, st); break;
+    case 3: launch_init_g<WDT, 3>(a, grid, lds, st); break;
+    default: launch_init_g<WDT, 4>(a, grid, lds, st); break;
   }
   return hipGetLastError();
 }

@@ -20,8 +20,9 @@ def to_dev(a: np.ndarray, dtype=torch.float32, device="cuda") -> torch.Tensor:
 class QuantLayer:
     """Device tensors of one matrix: W [R, C], X [T, C] and Theta_{I_F}.
 
-    Delta, z_U, s_r, z_B are set by the caller (e.g. identity uniform part and
-    z_B = 0); alpha comes from ``init_greedy``.
+    Theta_{I_F} comes from ``init_unified`` (the paper's initialisation), or
+    Delta, z_U, s_r, z_B are set by the caller and alpha comes from
+    ``init_greedy``.
     """
 
     def __init__(self, W, X, s, k, g, w_dtype=torch.bfloat16, device="cuda",
@@ -52,6 +53,13 @@ class QuantLayer:
         self.grad_s = torch.empty(R, C, dtype=torch.float32, device=dev)
         self.grad_alpha = torch.empty(Gn * k, dtype=torch.float32, device=dev)
         self.grad_z_b = torch.empty(Gn, dtype=torch.float32, device=dev)
+
+    def init_unified(self, grid_G=30, alt_T=15, clip=0, err=None):
+        """Unified initialisation of Delta, z_U, alpha, z_B (and s = 1, s_r = 1)
+        from W; the codes of the kept candidate go to ``codes``."""
+        uq.uniquan_init_unified(self.R, self.C, self.k, self.g, self.W, grid_G, alt_T, clip,
+                                self.delta, self.z_u, self.alpha, self.z_b, self.codes, err,
+                                self.s, self.s_r)
 
     def init_greedy(self):
         uq.uniquan_init_greedy(self.R, self.C, self.k, self.g, self.W, self.s, self.s_r, self.delta,
