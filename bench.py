@@ -2,8 +2,10 @@
 
 A step is one pass of the whole hot path over one batch, for every
 (matrix, k) of the workload:
-    fq_fwd (transform, level table, nearest-level mapping, detransform)
-    -> reconstruction forward GEMM + loss (Et = What X^T - Yt, sum Et^2)
+    fq_fwd (transform, level table, nearest-level mapping, detransform; it
+            stores the residual What - W)
+    -> reconstruction forward GEMM + loss (Et = (What - W) X^T, sum Et^2; the
+       same error as What X^T - X W^T without the stored fp32 target)
     -> weight-gradient GEMM (dL/dWhat = 2 Et X)
     -> fq_bwd fused with the SGD update (straight-through gradients of s,
        alpha, z_B applied in place in the same pass)
@@ -60,6 +62,8 @@ def parse():
     ap.add_argument("--init-grid", type=int, default=30, help="grid points G of the unified init")
     ap.add_argument("--init-rounds", type=int, default=15, help="alternating rounds T of the unified init")
     ap.add_argument("--init-clip", type=int, default=0, help="0 fixed min, 1 fixed max, 2 balanced")
+    ap.add_argument("--target", action="store_true",
+                    help="loss against a stored fp32 target Y = X W^T instead of the residual form")
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run a plain 256 MiB device copy (counter calibration)")
     return ap.parse_args()
@@ -208,7 +212,7 @@ def main():
         m = synth.make_matrix(spec, args.seed)
         wdt = torch.bfloat16 if spec.dtype == "bf16" else torch.float32
         for k in wl.ks:
-            lay = QuantLayer(m.W, m.X, m.s, k, g, w_dtype=wdt)
+            lay = QuantLayer(m.W, m.X, m.s, k, g, w_dtype=wdt, residual=not args.target)
             if args.init == "unified":
                 if not layers:
                     lay.init_unified(args.init_grid, args.init_rounds, args.init_clip)  # first-launch warm-up
@@ -354,7 +358,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": args.workload, "description": wl.description,
                    "matrices": [[l.R, l.C] for l in layers], "T": layers[0].T, "k": [l.k for l in layers],
-                   "g": g, "mapping": args.mode, "seed": args.seed, "parallelism": "single GPU"},
+                   "g": g, "mapping": args.mode, "seed": args.seed, "parallelism": "single GPU",
+                   "loss_form": "target" if args.target else "residual"},
         "fq_hbm_gbs": fq_gbs,
         "fq_frac_hbm": fq_gbs / HBM_PEAK_GBS,
         "gemm_tflops": gemm_tflops,

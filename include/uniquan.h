@@ -111,6 +111,27 @@ uq_status uniquan_fq_fwd(int64_t R, int64_t C, int k, int g,
                          void* stream);
 
 /*
+ * uniquan_fq_fwd_residual -- uniquan_fq_fwd with the reconstruction residual
+ * in place of the quantized weight:
+ *     R_out[j] = fl(what[j] - w[j])   (what as uniquan_fq_fwd computes it in
+ *                                      fp32; then rounded to r_dtype, RNE)
+ * For one linear layer the reconstruction error is X What^T - X W^T =
+ * X (What - W)^T (Algorithm 1's loss with X_hat = X), so feeding R_out to
+ * uniquan_layer_recon with Yt = NULL gives the loss without the fp32 target,
+ * and the small residual keeps more bits in bf16 than What does.  The
+ * gradient with respect to What is unchanged.  Arguments, codes and errors
+ * as for uniquan_fq_fwd; R_out [R*C] r_dtype out.
+ */
+uq_status uniquan_fq_fwd_residual(int64_t R, int64_t C, int k, int g,
+                                  const void* W, int w_dtype,
+                                  const float* s, const float* s_r,
+                                  const float* delta, const float* z_u,
+                                  const float* alpha, const float* z_b,
+                                  int mode, uint8_t* codes,
+                                  void* R_out, int r_dtype,
+                                  void* stream);
+
+/*
  * uniquan_fq_bwd -- straight-through backward of uniquan_fq_fwd with the
  * gradient filter (appendix "Implementation details": the mapping is
  * treated as identity, d wtilde / d wbar := m, zero where |wbar - wtilde|
@@ -206,7 +227,9 @@ size_t uniquan_recon_ws(int64_t T, int64_t R, int64_t C);
  * X           [T*C] bf16                                          in
  * Xt          [C*T] bf16 (transpose of X), NULL => forward only   in
  * W_hat       [R*C] bf16 (uniquan_fq_fwd output)                  in
- * Yt          [R*T] fp32 (uniquan_layer_target output)            in
+ * Yt          [R*T] fp32 (uniquan_layer_target output), or NULL:  in
+ *             then W_hat holds the residual What - W
+ *             (uniquan_fq_fwd_residual) and Et = W_hat X^T
  * loss        [1] fp32                                            out
  * Et_ws       [R*T] bf16 workspace; holds Et after the call      out
  * partials_ws [partials_len] fp32, partials_len >= uniquan_recon_ws()

@@ -298,6 +298,20 @@ def recon(X, W_hat, Y):
 # ----------------------------------------------------------------------------
 # Unification theorem (Theorem 1 and its proof) and the code search, Eq. (4).
 # ----------------------------------------------------------------------------
+def residual_f32(what32, W):
+    """Reconstruction residual What - W in fp32 (one rounding), [R, C]."""
+    return (np.asarray(what32, F32) - np.asarray(W, F32)).astype(F32)
+
+
+def recon_residual(X, Rw):
+    """Single-layer reconstruction from the residual Rw = What - W:
+    E = X Rw^T (which equals X What^T - X W^T), loss = sum E^2,
+    dL/dWhat = 2 E^T X; fp64.  Returns (E [T, R], loss, grad [R, C])."""
+    X = np.asarray(X, F64)
+    E = X @ np.asarray(Rw, F64).T
+    return E, float(np.sum(E * E)), 2.0 * E.T @ X
+
+
 def fold_params_f32(alpha, z_b, k, delta=None, z_u=None):
     """alpha* = Delta * alpha, z*_B = Delta * (z_B - z_U), each a fp32 product."""
     alpha = np.asarray(alpha, F32).reshape(-1, k)

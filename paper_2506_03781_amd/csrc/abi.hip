@@ -72,18 +72,33 @@ int uniquan_abi_version(void) { return UNIQUAN_ABI_VERSION; }
 
 const char* uniquan_last_error(void) { return g_err; }
 
-uq_status uniquan_fq_fwd(int64_t R, int64_t C, int k, int g, const void* W, int w_dtype, const float* s,
-                         const float* s_r, const float* delta, const float* z_u, const float* alpha,
-                         const float* z_b, int mode, uint8_t* codes, void* W_hat, int w_hat_dtype,
-                         void* stream) {
-  const char* fn = "uniquan_fq_fwd";
+static uq_status fq_fwd_common(const char* fn, int64_t R, int64_t C, int k, int g, const void* W, int w_dtype,
+                               const float* s, const float* s_r, const float* delta, const float* z_u,
+                               const float* alpha, const float* z_b, int mode, uint8_t* codes, void* W_hat,
+                               int w_hat_dtype, int resid, void* stream) {
   if (uq_status st = check_quant_shape(fn, R, C, k, g)) return st;
   if (!is_dtype(w_dtype) || !is_dtype(w_hat_dtype)) return fail(UQ_EINVAL, "%s: bad dtype", fn);
   if (mode < UQ_MAP_FULL || mode > UQ_MAP_FROZEN) return fail(UQ_EINVAL, "%s: bad mapping mode %d", fn, mode);
   REQ_PTR(W, 16); REQ_PTR(s, 16); REQ_PTR(alpha, 4); REQ_PTR(z_b, 4); REQ_PTR(codes, 16); REQ_PTR(W_hat, 16);
   OPT_PTR(s_r, 4); OPT_PTR(delta, 4); OPT_PTR(z_u, 4);
-  uq::FqFwdLaunch p{R, C, k, g, W, w_dtype, s, s_r, delta, z_u, alpha, z_b, mode, codes, W_hat, w_hat_dtype};
+  uq::FqFwdLaunch p{R, C, k, g, W, w_dtype, s, s_r, delta, z_u, alpha, z_b, mode, codes, W_hat, w_hat_dtype, resid};
   return hip_status(fn, uq::launch_fq_fwd(p, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uniquan_fq_fwd(int64_t R, int64_t C, int k, int g, const void* W, int w_dtype, const float* s,
+                         const float* s_r, const float* delta, const float* z_u, const float* alpha,
+                         const float* z_b, int mode, uint8_t* codes, void* W_hat, int w_hat_dtype,
+                         void* stream) {
+  return fq_fwd_common("uniquan_fq_fwd", R, C, k, g, W, w_dtype, s, s_r, delta, z_u, alpha, z_b, mode, codes,
+                       W_hat, w_hat_dtype, 0, stream);
+}
+
+uq_status uniquan_fq_fwd_residual(int64_t R, int64_t C, int k, int g, const void* W, int w_dtype, const float* s,
+                                  const float* s_r, const float* delta, const float* z_u, const float* alpha,
+                                  const float* z_b, int mode, uint8_t* codes, void* R_out, int r_dtype,
+                                  void* stream) {
+  return fq_fwd_common("uniquan_fq_fwd_residual", R, C, k, g, W, w_dtype, s, s_r, delta, z_u, alpha, z_b, mode,
+                       codes, R_out, r_dtype, 1, stream);
 }
 
 uq_status uniquan_fq_bwd(int64_t R, int64_t C, int k, int g, const void* W, int w_dtype, const float* s,
@@ -150,7 +165,7 @@ uq_status uniquan_layer_recon(int64_t T, int64_t R, int64_t C, const uint16_t* X
                               void* stream) {
   const char* fn = "uniquan_layer_recon";
   if (uq_status st = check_gemm_dims(fn, T, R, C)) return st;
-  REQ_PTR(X, 16); REQ_PTR(W_hat, 16); REQ_PTR(Yt, 16); REQ_PTR(loss, 4); REQ_PTR(Et_ws, 16);
+  REQ_PTR(X, 16); REQ_PTR(W_hat, 16); OPT_PTR(Yt, 16); REQ_PTR(loss, 4); REQ_PTR(Et_ws, 16);
   REQ_PTR(partials_ws, 16);
   if (partials_len < uniquan_recon_ws(T, R, C))
     return fail(UQ_EINVAL, "%s: partials_len=%zu < %zu", fn, partials_len, uniquan_recon_ws(T, R, C));

@@ -65,6 +65,7 @@ struct FwdArgs {
   const float* z_b;
   uint8_t* codes;
   void* W_hat;
+  int resid;  // 1: store What - W (the reconstruction residual) instead of What
 };
 
 // Dynamic LDS of a quantizer tile: the level tables plus four per-group
@@ -74,11 +75,11 @@ static size_t tile_lds_bytes(const TileGeom& t) {
   return ((e * 10 + 15) & ~size_t(15)) + 16 * size_t(t.tile_groups);
 }
 
-// Per-wave LDS bytes: the level tables of (512/g) groups of 2^k levels,
+// Per-wave LDS bytes: the level tables of (512 ch / g) groups of 2^k levels,
 // optionally the local-mapping neighbour table (16 B per level), and 4
 // floats per group.
-__host__ __device__ inline size_t wave_lds_bytes(int logg, int k, bool nbt) {
-  const size_t groups = size_t(512) >> logg;
+__host__ __device__ inline size_t wave_lds_bytes(int logg, int k, bool nbt, int ch = 1) {
+  const size_t groups = (size_t(512) * ch) >> logg;
   const size_t e = groups << k;
   return ((e * 10 + 15) & ~size_t(15)) + (nbt ? 16 * e : 0) + 16 * groups;
 }
@@ -87,23 +88,25 @@ __host__ __device__ inline size_t wave_lds_bytes(int logg, int k, bool nbt) {
 // level, at most 4096 levels per wave).
 static bool use_neighbour_table(int logg, int k) { return ((size_t(512) >> logg) << k) <= 4096; }
 
-// Forward kernel.  Each wavefront owns 512 consecutive weights (8 per lane;
-// groups never straddle waves since g divides 512) and keeps the level
-// tables of its 512/g groups in a private LDS region, so the table build
-// needs only wave-local ordering and no workgroup barrier.  The lane issues
-// its W, s (and code) loads first; while they are in flight the wave builds
-// its tables: one lane per level computes q(b), then ranks it among the
-// group's levels by counting (sort key (value, code)).
-template <int WDT, int ODT, int MODE, int LOGL>
+// Forward kernel.  Each wavefront owns CH chunks of 512 consecutive weights
+// (8 per lane per chunk; groups never straddle chunks since g divides 512)
+// and keeps the level tables of their groups in a private LDS region, so
+// table building needs only wave-local ordering and no workgroup barrier.
+// The lane issues the W, s (and code) loads of all its chunks first, so a
+// wavefront keeps CH x 3.5 KB in flight; while they are in flight the wave
+// builds its tables: one lane per level computes q(b), then ranks it among
+// the group's levels by counting (sort key (value, code)).
+template <int WDT, int ODT, int MODE, int LOGL, int CH>
 __global__ __launch_bounds__(kThreads) void fq_fwd_kernel(FwdArgs a, int nbt) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   constexpr int L = 1 << LOGL;
+  constexpr int WPW = 512 * CH;                     // weights per wave
   const TileGeom& g = a.t;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int gw = 512 >> g.logg;                     // groups per wave (g divides 512)
+  const int gw = WPW >> g.logg;                     // groups per wave (g divides 512)
   const int ew = gw << LOGL;                        // table entries per wave
   const bool has_nb = MODE == 1 && nbt;
-  char* mine = smem + size_t(wave) * wave_lds_bytes(g.logg, LOGL, has_nb);
+  char* mine = smem + size_t(wave) * wave_lds_bytes(g.logg, LOGL, has_nb, CH);
   LevelTables tab;
   char* p = carve_tables(tab, mine, ew);
   float4* nb = reinterpret_cast<float4*>(p);        // [ew] (q_l, q_d, q_r, codes l|d<<8|r<<16)
@@ -112,24 +115,30 @@ __global__ __launch_bounds__(kThreads) void fq_fwd_kernel(FwdArgs a, int nbt) {
   float* s_zu = s_ds + gw;
   float* s_dl = s_zu + gw;
   float* s_tau = s_dl + gw;
-  const int64_t wbase = (int64_t(blockIdx.x) * (blockDim.x >> 6) + wave) * 512;  // first weight of this wave
+  const int64_t wbase = (int64_t(blockIdx.x) * (blockDim.x >> 6) + wave) * WPW;  // first weight of this wave
   if (wbase >= g.N) return;                                       // whole wave past the end
-  const int nvalid = int(min<int64_t>(512, g.N - wbase));        // a multiple of g (and of 8)
-  const bool active = lane * kVec < nvalid;
+  const int nvalid = int(min<int64_t>(WPW, g.N - wbase));        // a multiple of g (and of 8)
   const int gv = nvalid >> g.logg;                                // valid groups of this wave
   const int ev = gv << LOGL;                                      // valid table entries
-  const int64_t off = wbase + lane * kVec;
   const int64_t gid0 = wbase >> g.logg;
 
-  Raw8<WDT> w;
-  float4 s0 = make_float4(0, 0, 0, 0), s1 = s0;
-  uint2 prev = make_uint2(0u, 0u);
-  if (active) {
-    w.load(a.W, off);
-    const float4* sp = reinterpret_cast<const float4*>(a.s + off);
-    s0 = sp[0];
-    s1 = sp[1];
-    if constexpr (MODE != 0) prev = load8u8(a.codes, off);
+  Raw8<WDT> w[CH];
+  float4 s0[CH], s1[CH];
+  uint2 prev[CH];
+#pragma unroll
+  for (int h = 0; h < CH; ++h) {
+    const int lo = h * 512 + lane * kVec;  // this lane's first weight of chunk h, within the wave
+    s0[h] = make_float4(0, 0, 0, 0);
+    s1[h] = s0[h];
+    prev[h] = make_uint2(0u, 0u);
+    if (lo < nvalid) {
+      const int64_t off = wbase + lo;
+      w[h].load(a.W, off);
+      const float4* sp = reinterpret_cast<const float4*>(a.s + off);
+      s0[h] = sp[0];
+      s1[h] = sp[1];
+      if constexpr (MODE != 0) prev[h] = load8u8(a.codes, off);
+    }
   }
 
   // raw levels by code, and the per-group parameters
@@ -179,59 +188,65 @@ __global__ __launch_bounds__(kThreads) void fq_fwd_kernel(FwdArgs a, int nbt) {
     }
     wave_lds_sync();
   }
-  if (!active) return;
 
-  const int gl = (lane * kVec) >> g.logg;
-  const float ds = s_ds[gl], zu = s_zu[gl], dl = s_dl[gl], tau = s_tau[gl];
-  const float* q = tab.qs + (gl << LOGL);
-  const float* qraw = tab.raw + (gl << LOGL);
-  const float4* nbg = nb + (gl << LOGL);
-  const uint8_t* code_of = tab.code_of + (gl << LOGL);
-  const uint8_t* pos_of = tab.pos_of + (gl << LOGL);
-  const float sv[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
-  float out[8];
-  uint32_t cw[2] = {0u, 0u};
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const float den = ds * sv[i];
-    const float wb = w.get(i) / den + zu;
-    float d, wt;
-    uint32_t code;
-    if constexpr (MODE == 0) {
-      const int jj = nearest_full_k<LOGL>(q, wb, d);
-      wt = q[jj];
-      code = code_of[jj];
-    } else if constexpr (MODE == 2) {
-      code = byte_of(prev, i) & uint32_t(L - 1);
-      wt = qraw[code];
-      d = fabsf(wb - wt);
-    } else {
-      const uint32_t c0 = byte_of(prev, i) & uint32_t(L - 1);
-      if (has_nb) {
-        // first nearest of (d-1, d, d+1) in ascending order
-        const float4 e4 = nbg[c0];
-        const uint32_t cs = __float_as_uint(e4.w);
-        float bd = fabsf(wb - e4.x);
-        wt = e4.x;
-        uint32_t sh = 0;
-        const float dm = fabsf(wb - e4.y);
-        if (dm < bd) { bd = dm; wt = e4.y; sh = 8; }
-        const float dr = fabsf(wb - e4.z);
-        if (dr < bd) { bd = dr; wt = e4.z; sh = 16; }
-        d = bd;
-        code = (cs >> sh) & 0xFFu;
-      } else {
-        const int jj = nearest_local(q, L, pos_of[c0], wb, d);
+  for (int h = 0; h < CH; ++h) {
+    const int lo = h * 512 + lane * kVec;
+    if (lo >= nvalid) break;  // later chunks start further out
+    const int64_t off = wbase + lo;
+    const int gl = lo >> g.logg;
+    const float ds = s_ds[gl], zu = s_zu[gl], dl = s_dl[gl], tau = s_tau[gl];
+    const float* q = tab.qs + (gl << LOGL);
+    const float* qraw = tab.raw + (gl << LOGL);
+    const float4* nbg = nb + (gl << LOGL);
+    const uint8_t* code_of = tab.code_of + (gl << LOGL);
+    const uint8_t* pos_of = tab.pos_of + (gl << LOGL);
+    const float sv[8] = {s0[h].x, s0[h].y, s0[h].z, s0[h].w, s1[h].x, s1[h].y, s1[h].z, s1[h].w};
+    float out[8];
+    uint32_t cw[2] = {0u, 0u};
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float den = ds * sv[i];
+      const float wb = w[h].get(i) / den + zu;
+      float d, wt;
+      uint32_t code;
+      if constexpr (MODE == 0) {
+        const int jj = nearest_full_k<LOGL>(q, wb, d);
         wt = q[jj];
         code = code_of[jj];
+      } else if constexpr (MODE == 2) {
+        code = byte_of(prev[h], i) & uint32_t(L - 1);
+        wt = qraw[code];
+        d = fabsf(wb - wt);
+      } else {
+        const uint32_t c0 = byte_of(prev[h], i) & uint32_t(L - 1);
+        if (has_nb) {
+          // first nearest of (d-1, d, d+1) in ascending order
+          const float4 e4 = nbg[c0];
+          const uint32_t cs = __float_as_uint(e4.w);
+          float bd = fabsf(wb - e4.x);
+          wt = e4.x;
+          uint32_t sh = 0;
+          const float dm = fabsf(wb - e4.y);
+          if (dm < bd) { bd = dm; wt = e4.y; sh = 8; }
+          const float dr = fabsf(wb - e4.z);
+          if (dr < bd) { bd = dr; wt = e4.z; sh = 16; }
+          d = bd;
+          code = (cs >> sh) & 0xFFu;
+        } else {
+          const int jj = nearest_local(q, L, pos_of[c0], wb, d);
+          wt = q[jj];
+          code = code_of[jj];
+        }
       }
+      const uint32_t byte = code | (d > tau ? 0u : 0x80u);
+      cw[i >> 2] |= byte << (8 * (i & 3));
+      out[i] = dl * (wt - zu);
+      if (a.resid) out[i] = out[i] - w[h].get(i);
     }
-    const uint32_t byte = code | (d > tau ? 0u : 0x80u);
-    cw[i >> 2] |= byte << (8 * (i & 3));
-    out[i] = dl * (wt - zu);
+    store8<ODT>(a.W_hat, off, out);
+    store8u8(a.codes, off, make_uint2(cw[0], cw[1]));
   }
-  store8<ODT>(a.W_hat, off, out);
-  store8u8(a.codes, off, make_uint2(cw[0], cw[1]));
 }
 
 // ---------------------------------------------------------------------------
@@ -448,7 +463,7 @@ static int fwd_waves_per_block(size_t wave_bytes) {
 }
 
 template <typename Kern>
-static hipError_t launch_fwd_kern(Kern kern, const FwdArgs& a, size_t wave_bytes, int nbt, hipStream_t st) {
+static hipError_t launch_fwd_kern(Kern kern, const FwdArgs& a, size_t wave_bytes, int nbt, int ch, hipStream_t st) {
   const int wpb = fwd_waves_per_block(wave_bytes);
   const size_t lds = size_t(wpb) * wave_bytes;
   if (lds > 65536) {
@@ -456,23 +471,38 @@ static hipError_t launch_fwd_kern(Kern kern, const FwdArgs& a, size_t wave_bytes
                                              hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
     if (e != hipSuccess) return e;
   }
-  const int64_t waves = (a.t.N + 511) / 512;
+  const int64_t per_wave = 512 * int64_t(ch);
+  const int64_t waves = (a.t.N + per_wave - 1) / per_wave;
   hipLaunchKernelGGL(kern, dim3(unsigned((waves + wpb - 1) / wpb)), dim3(64 * wpb), lds, st, a, nbt);
   return hipGetLastError();
+}
+
+// Chunks per wavefront: two (twice the loads in flight) for the bf16 step path
+// with k <= 4 when the doubled tables stay small; one otherwise.
+template <int LOGL, int WD, int OD>
+static constexpr bool two_chunks_ok() { return WD == BF16 && OD == BF16 && LOGL <= 4; }
+
+template <int WD, int OD, int MD, int LOGL>
+static hipError_t launch_fwd_l(const FwdArgs& a, int nbt, hipStream_t st) {
+  if constexpr (two_chunks_ok<LOGL, WD, OD>()) {
+    const size_t wb2 = wave_lds_bytes(a.t.logg, LOGL, nbt != 0, 2);
+    if (wb2 <= 16384) return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, LOGL, 2>, a, wb2, nbt, 2, st);
+  }
+  return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, LOGL, 1>, a, wave_lds_bytes(a.t.logg, LOGL, nbt != 0, 1), nbt,
+                         1, st);
 }
 
 template <int WD, int OD, int MD>
 static hipError_t launch_fwd_k(const FwdArgs& a, int k, hipStream_t st) {
   const int nbt = (MD == 1 && use_neighbour_table(a.t.logg, k)) ? 1 : 0;
-  const size_t wb = wave_lds_bytes(a.t.logg, k, nbt != 0);
   switch (k) {
-    case 1: return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, 1>, a, wb, nbt, st);
-    case 2: return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, 2>, a, wb, nbt, st);
-    case 3: return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, 3>, a, wb, nbt, st);
-    case 4: return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, 4>, a, wb, nbt, st);
-    case 5: return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, 5>, a, wb, nbt, st);
-    case 6: return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, 6>, a, wb, nbt, st);
-    default: return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, 7>, a, wb, nbt, st);
+    case 1: return launch_fwd_l<WD, OD, MD, 1>(a, nbt, st);
+    case 2: return launch_fwd_l<WD, OD, MD, 2>(a, nbt, st);
+    case 3: return launch_fwd_l<WD, OD, MD, 3>(a, nbt, st);
+    case 4: return launch_fwd_l<WD, OD, MD, 4>(a, nbt, st);
+    case 5: return launch_fwd_l<WD, OD, MD, 5>(a, nbt, st);
+    case 6: return launch_fwd_l<WD, OD, MD, 6>(a, nbt, st);
+    default: return launch_fwd_l<WD, OD, MD, 7>(a, nbt, st);
   }
 }
 
@@ -481,6 +511,7 @@ hipError_t launch_fq_fwd(const FqFwdLaunch& p, hipStream_t st) {
   a.t = make_geom(p.R, p.C, p.k, p.g, 1);
   a.W = p.W; a.s = p.s; a.s_r = p.s_r; a.delta = p.delta; a.z_u = p.z_u;
   a.alpha = p.alpha; a.z_b = p.z_b; a.codes = p.codes; a.W_hat = p.W_hat;
+  a.resid = p.resid;
 #define UQ_FWD(WD, OD, MD) \
   if (p.w_dtype == WD && p.w_hat_dtype == OD && p.mode == MD) return launch_fwd_k<WD, OD, MD>(a, p.k, st);
   UQ_FWD(BF16, BF16, 0) UQ_FWD(BF16, BF16, 1) UQ_FWD(BF16, BF16, 2)

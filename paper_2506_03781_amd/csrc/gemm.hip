@@ -100,11 +100,12 @@ __device__ __forceinline__ void epilogue(const GemmArgs& p, f32x16 (&acc)[FM][FN
     const int64_t col_base = n0 + wn * WN;
     float4 y[ITER];
     if constexpr (EPI == EPI_LOSS) {
+      // no target: the A operand already holds the residual What - W
 #pragma unroll
       for (int it = 0; it < ITER; ++it) {
         const int idx = lane + it * 64;
         const int64_t row = row_base + idx / Q, col = col_base + (idx % Q) * 4;
-        const bool ok = full || (row < p.M && col < p.N);  // N % 4 == 0 for this epilogue
+        const bool ok = Yt != nullptr && (full || (row < p.M && col < p.N));  // N % 4 == 0 here
         y[it] = ok ? *reinterpret_cast<const float4*>(Yt + row * p.N + col) : make_float4(0, 0, 0, 0);
       }
     }

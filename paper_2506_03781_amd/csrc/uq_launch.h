@@ -17,6 +17,7 @@ struct FqFwdLaunch {
   int mode;
   uint8_t* codes;
   void* W_hat; int w_hat_dtype;
+  int resid;  // store What - W instead of What
 };
 
 struct FqBwdLaunch {

@@ -26,9 +26,11 @@ class QuantLayer:
     """
 
     def __init__(self, W, X, s, k, g, w_dtype=torch.bfloat16, device="cuda",
-                 delta=None, z_u=None, s_r=None, z_b=None, grad_dtype=torch.bfloat16):
+                 delta=None, z_u=None, s_r=None, z_b=None, grad_dtype=torch.bfloat16, residual=False):
         R, C = W.shape
         T = X.shape[0]
+        # residual: W_hat holds What - W and the loss needs no target (Yt unused)
+        self.residual = residual
         self.R, self.C, self.T, self.k, self.g = R, C, T, k, g
         Gn = R * C // g
         self.Gn = Gn
@@ -45,7 +47,7 @@ class QuantLayer:
         self.codes = torch.zeros(R * C, dtype=torch.uint8, device=dev)
         self.W_hat = torch.empty(R, C, dtype=torch.bfloat16, device=dev)
         self.Xt = torch.empty(C, T, dtype=torch.bfloat16, device=dev)
-        self.Yt = torch.empty(R, T, dtype=torch.float32, device=dev)
+        self.Yt = None if residual else torch.empty(R, T, dtype=torch.float32, device=dev)
         self.Et = torch.empty(R, T, dtype=torch.bfloat16, device=dev)
         self.partials = torch.empty(max(1, uq.uniquan_recon_ws(T, R, C)), dtype=torch.float32, device=dev)
         self.loss = torch.zeros(1, dtype=torch.float32, device=dev)
@@ -66,13 +68,16 @@ class QuantLayer:
                                self.z_u, self.z_b, self.alpha)
 
     def prepare(self):
-        """Fixed target Yt = W X^T and Xt, once per layer."""
-        uq.uniquan_layer_target(self.T, self.R, self.C, self.X, self.W_bf16, self.Yt)
+        """Xt and (without the residual form) the fixed target Yt = W X^T, once
+        per layer."""
+        if self.Yt is not None:
+            uq.uniquan_layer_target(self.T, self.R, self.C, self.X, self.W_bf16, self.Yt)
         uq.uniquan_transpose_bf16(self.T, self.C, self.X, self.Xt)
 
     def fq_fwd(self, mode=uq.MAP_FULL):
-        uq.uniquan_fq_fwd(self.R, self.C, self.k, self.g, self.W, self.s, self.s_r, self.delta, self.z_u,
-                          self.alpha, self.z_b, mode, self.codes, self.W_hat)
+        fn = uq.uniquan_fq_fwd_residual if self.residual else uq.uniquan_fq_fwd
+        fn(self.R, self.C, self.k, self.g, self.W, self.s, self.s_r, self.delta, self.z_u,
+           self.alpha, self.z_b, mode, self.codes, self.W_hat)
 
     def recon(self, backward=True):
         uq.uniquan_layer_recon(self.T, self.R, self.C, self.X, self.Xt, self.W_hat, self.Yt, self.loss,

@@ -37,6 +37,8 @@ _SIGS = {
     "uniquan_abi_version": ([], _i32),
     "uniquan_last_error": ([], ctypes.c_char_p),
     "uniquan_fq_fwd": ([_i64, _i64, _i32, _i32, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _i32, _vp], _i32),
+    "uniquan_fq_fwd_residual": ([_i64, _i64, _i32, _i32, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _i32,
+                                 _vp], _i32),
     "uniquan_fq_bwd": ([_i64, _i64, _i32, _i32, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32,
                         _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp], _i32),
     "uniquan_fq_bwd_sgd": ([_i64, _i64, _i32, _i32, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32,
@@ -132,6 +134,15 @@ def uniquan_fq_fwd(R, C, k, g, W, s, s_r, delta, z_u, alpha, z_b, mode, codes, W
         _p(delta, Gn, _F, "delta"), _p(z_u, Gn, _F, "z_u"), _p(alpha, Gn * k, _F, "alpha"),
         _p(z_b, Gn, _F, "z_b"), int(mode), _p(codes, N, _U8, "codes"), _p(W_hat, N, _W, "W_hat"),
         _dt(W_hat), _stream(stream)))
+
+
+def uniquan_fq_fwd_residual(R, C, k, g, W, s, s_r, delta, z_u, alpha, z_b, mode, codes, R_out, stream=None):
+    N, Gn = R * C, R * C // g
+    _check(lib().uniquan_fq_fwd_residual(
+        R, C, k, g, _p(W, N, _W, "W"), _dt(W), _p(s, N, _F, "s"), _p(s_r, R, _F, "s_r"),
+        _p(delta, Gn, _F, "delta"), _p(z_u, Gn, _F, "z_u"), _p(alpha, Gn * k, _F, "alpha"),
+        _p(z_b, Gn, _F, "z_b"), int(mode), _p(codes, N, _U8, "codes"), _p(R_out, N, _W, "R_out"),
+        _dt(R_out), _stream(stream)))
 
 
 def uniquan_fq_bwd(R, C, k, g, W, s, s_r, delta, z_u, alpha, z_b, codes, grad_W_hat,

@@ -503,7 +503,9 @@ def test_full_size_attn4096(attn4096, k):
     Yt_rows = host(lay.Yt)[rows]
     E_rows = Xb @ what.astype(np.float64).T - Yt_rows.T.astype(np.float64)
     close(host(lay.Et)[rows], E_rows.T, what="E rows")
-    G_rows = 2.0 * E_rows.T @ Xb
+    # the weight-gradient GEMM consumes Et as stored (bf16): round the
+    # oracle's own E the same way before forming 2 E^T X
+    G_rows = 2.0 * O.bf16_rne(E_rows.astype(F32)).astype(np.float64).T @ Xb
     Gd = host(lay.G)
     close(Gd[rows], G_rows, what="grad_W_hat rows")
     What_all = host(lay.W_hat).astype(np.float64)
@@ -515,3 +517,95 @@ def test_full_size_attn4096(attn4096, k):
     close(host(lay.grad_s).reshape(R, C)[rows], bw["grad_s"], what="grad_s rows")
     close(host(lay.grad_alpha).reshape(-1, k)[gidx], bw["grad_alpha"], what="grad_alpha rows")
     close(host(lay.grad_z_b)[gidx], bw["grad_z_b"], what="grad_z_b rows")
+
+
+# ---------------------------------------------------------------------------
+# Residual form: the quantizer writes What - W and the loss GEMM runs without
+# the fp32 target (E = X (What - W)^T).
+# ---------------------------------------------------------------------------
+def gpu_fwd_residual(W, s, p, k, g, mode, codes_prev, wdt, odt):
+    R, C = W.shape
+    codes = dev(codes_prev if codes_prev is not None else np.zeros((R, C), np.uint8), torch.uint8).reshape(-1)
+    Rout = torch.empty(R * C, dtype=odt, device=DEV)
+    uq.uniquan_fq_fwd_residual(R, C, k, g, dev(W, wdt), dev(s), dev(p["s_r"]), dev(p["delta"]), dev(p["z_u"]),
+                               dev(p["alpha"].reshape(-1)), dev(p["z_b"]), mode, codes, Rout)
+    torch.cuda.synchronize()
+    return host(codes).reshape(R, C), host(Rout).reshape(R, C)
+
+
+@pytest.mark.parametrize("mode", [uq.MAP_FULL, uq.MAP_LOCAL, uq.MAP_FROZEN])
+@pytest.mark.parametrize("wdt", [torch.bfloat16, torch.float32])
+def test_fwd_residual(mode, wdt):
+    m = small_matrix(37, 384, 21)
+    k, g = 4, 128
+    W = m.W if wdt == torch.bfloat16 else (m.W + 1e-4 * np.random.default_rng(3).standard_normal(m.W.shape)).astype(F32)
+    p = params(W, m.s, k, g, "B")
+    prev = synth.random_codes(37, 384, k, 22) if mode != uq.MAP_FULL else None
+    ref = O.fq_fwd(W, m.s, p["alpha"], p["z_b"], k, g, p["s_r"], p["delta"], p["z_u"], mode, prev)
+    res32 = O.residual_f32(ref["what32"], W)
+    codes, r32 = gpu_fwd_residual(W, m.s, p, k, g, mode, prev, wdt, torch.float32)
+    assert np.array_equal(codes, ref["codes"])
+    assert np.array_equal(r32.view(np.uint32), res32.view(np.uint32))
+    codes_b, rb = gpu_fwd_residual(W, m.s, p, k, g, mode, prev, wdt, torch.bfloat16)
+    assert np.array_equal(codes_b, ref["codes"])
+    assert np.array_equal(rb, O.bf16_rne(res32))
+
+
+@pytest.mark.parametrize("T,R,C", [(64, 256, 256), (200, 300, 264), (136, 1000, 136), (4096, 4096, 128)])
+def test_recon_residual(T, R, C):
+    rs = np.random.default_rng(T + 7 * R + C)
+    X = synth.round_to_bf16(rs.standard_normal((T, C)).astype(F32))
+    Rw = synth.round_to_bf16((0.002 * rs.standard_normal((R, C))).astype(F32))
+    Xd = dev(X, torch.bfloat16)
+    Xt = torch.empty(C, T, dtype=torch.bfloat16, device=DEV)
+    uq.uniquan_transpose_bf16(T, C, Xd, Xt)
+    Et = torch.empty(R, T, dtype=torch.bfloat16, device=DEV)
+    part = torch.empty(uq.uniquan_recon_ws(T, R, C), device=DEV)
+    loss = torch.zeros(1, device=DEV)
+    G = torch.empty(R, C, dtype=torch.bfloat16, device=DEV)
+    uq.uniquan_layer_recon(T, R, C, Xd, Xt, dev(Rw, torch.bfloat16), None, loss, Et, part, G)
+    torch.cuda.synchronize()
+    E, L, G64 = O.recon_residual(X, Rw)
+    assert abs(float(loss.item()) - L) <= 1e-2 * L
+    close(host(Et), E.T, what="E")
+    close(host(G), G64, what="grad_W_hat")
+
+
+def test_full_size_attn4096_residual(attn4096):
+    """The step path the bench times: residual forward (LOCAL after FULL),
+    target-free loss GEMM, weight gradient, on the 4096 x 4096 / 2048-token
+    layer; sampled rows against the oracle, the whole loss in fp64."""
+    from paper_2506_03781_amd.layer import QuantLayer
+    m = attn4096
+    k, g = 4, 128
+    R, C, T = m.R, m.C, m.T
+    lay = QuantLayer(m.W, m.X, m.s, k, g, residual=True)
+    lay.init_unified(grid_G=2, alt_T=3, clip=0)
+    lay.prepare()
+    lay.fq_fwd(uq.MAP_FULL)
+    prev = host(lay.codes).reshape(R, C).copy()
+    lay.fq_fwd(uq.MAP_LOCAL)
+    lay.recon(True)
+    torch.cuda.synchronize()
+    rows = np.sort(np.random.default_rng(5).choice(R, 12, replace=False))
+    gpr = C // g
+    gidx = (rows[:, None] * gpr + np.arange(gpr)[None, :]).reshape(-1)
+    alpha = host(lay.alpha).reshape(-1, k)[gidx]
+    z_b, delta, z_u = host(lay.z_b)[gidx], host(lay.delta)[gidx], host(lay.z_u)[gidx]
+    s_rows = host(lay.s).reshape(R, C)[rows]
+    Wr = m.W[rows]
+    ref = O.fq_fwd(Wr, s_rows, alpha, z_b, k, g, None, delta, z_u, uq.MAP_LOCAL, prev[rows])
+    assert np.array_equal(host(lay.codes).reshape(R, C)[rows], ref["codes"])
+    res_b = O.bf16_rne(O.residual_f32(ref["what32"], Wr))
+    assert np.array_equal(host(lay.W_hat)[rows], res_b)
+    Xb = m.X.astype(np.float64)
+    E_rows = Xb @ res_b.astype(np.float64).T
+    close(host(lay.Et)[rows], E_rows.T, what="E rows")
+    # the weight-gradient GEMM consumes Et as stored (bf16): round the
+    # oracle's own E the same way before forming 2 E^T X
+    Eb = O.bf16_rne(E_rows.astype(F32)).astype(np.float64)
+    close(host(lay.G)[rows], 2.0 * Eb.T @ Xb, what="grad rows")
+    Rall = host(lay.W_hat).astype(np.float64)
+    E_all = Xb @ Rall.T
+    L = float(np.sum(E_all * E_all))
+    assert abs(float(lay.loss.item()) - L) <= 1e-2 * L

@@ -361,6 +361,14 @@ def pin_idempotence_and_recon():
     W2 = Wh.astype(np.float64).copy(); W2[1, 3] -= h
     fdv = (U.recon(X, W1, Y)[1] - U.recon(X, W2, Y)[1]) / (2 * h)
     assert abs(fdv - Gr[1, 3]) < 1e-6 * max(1, abs(fdv))
+    # The residual form: X (What - W)^T is the same error, loss and gradient.
+    Rw = U.residual_f32(Wh, W)
+    assert np.array_equal(Rw.astype(np.float64), Wh.astype(np.float64) - W.astype(np.float64))  # exact here
+    E2, L2, G2 = U.recon_residual(X, Rw)
+    assert np.max(np.abs(E2 - E)) <= 1e-12 * max(1.0, np.abs(E).max())
+    assert abs(L2 - L) <= 1e-9 * L
+    assert np.max(np.abs(G2 - Gr)) <= 1e-12 * max(1.0, np.abs(Gr).max())
+    assert not np.any(U.residual_f32(out["what32"], W))   # exactly quantizable W: zero residual
 
 
 def test_p7_idempotence_and_recon():
@@ -582,6 +590,18 @@ def _mut_bf16_trunc(x):                     # truncation instead of round-to-nea
 
 
 MUTATIONS += [("levels_f64", _mut_levels64), ("bf16_rne", _mut_bf16_trunc)]
+
+
+def _mut_residual(what32, W):               # sign of the residual flipped
+    return (np.asarray(W, F32) - np.asarray(what32, F32)).astype(F32)
+
+
+def _mut_recon_residual(X, Rw):             # missing factor 2 in the gradient
+    E, L, G = U._orig_recon_residual(X, Rw)
+    return E, L, 0.5 * G
+
+
+MUTATIONS += [("residual_f32", _mut_residual), ("recon_residual", _mut_recon_residual)]
 
 
 @pytest.mark.parametrize("name,fn", MUTATIONS, ids=[f"{m[0]}-{m[1].__name__}" for m in MUTATIONS])
