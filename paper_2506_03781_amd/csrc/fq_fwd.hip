@@ -28,6 +28,24 @@ __device__ __forceinline__ float tau_of(const float* __restrict__ alpha_g, int k
   return t;
 }
 
+// The same two quantities with k fixed at compile time (unrolled, one base
+// address for the k loads).
+template <int K>
+__device__ __forceinline__ float tau_k(const float* __restrict__ alpha_g) {
+  float t = fabsf(alpha_g[0]);
+#pragma unroll
+  for (int i = 1; i < K; ++i) t = fminf(t, fabsf(alpha_g[i]));
+  return t;
+}
+
+template <int K>
+__device__ __forceinline__ float level_value_k(const float* __restrict__ alpha_g, float zb, int b) {
+  float q = zb;
+#pragma unroll
+  for (int i = 0; i < K; ++i) q = ((b >> i) & 1) ? q + alpha_g[i] : q - alpha_g[i];
+  return q;
+}
+
 // Raw storage of 8 weights as loaded (bf16 kept packed until use).
 template <int DT> struct Raw8;
 template <> struct Raw8<BF16> {
@@ -81,7 +99,16 @@ static size_t tile_lds_bytes(const TileGeom& t) {
 __host__ __device__ inline size_t wave_lds_bytes(int logg, int k, bool nbt, int ch = 1) {
   const size_t groups = (size_t(512) * ch) >> logg;
   const size_t e = groups << k;
-  return ((e * 10 + 15) & ~size_t(15)) + (nbt ? 16 * e : 0) + 16 * groups;
+  return ((e * 10 + 15) & ~size_t(15)) + (nbt ? 16 * e : 0) + 16 * groups + (k <= 4 ? 8 * e : 0);
+}
+
+// Sort key of level b with value q: the value's bits mapped to an unsigned
+// integer of the same order (-0 folded onto +0 first), then the code, so one
+// 64-bit compare orders by (value, code).
+__device__ __forceinline__ uint64_t level_key(float q, int b) {
+  const uint32_t u = __float_as_uint(q + 0.0f);
+  const uint32_t ord = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return (uint64_t(ord) << 8) | uint64_t(b);
 }
 
 // Neighbour tables for the local mapping are kept when they fit (16 B per
@@ -96,16 +123,19 @@ static bool use_neighbour_table(int logg, int k) { return ((size_t(512) >> logg)
 // wavefront keeps CH x 3.5 KB in flight; while they are in flight the wave
 // builds its tables: one lane per level computes q(b), then ranks it among
 // the group's levels by counting (sort key (value, code)).
+// MODE: 0 FULL, 1 LOCAL by search, 2 FROZEN, 3 LOCAL through the neighbour
+// table (the LOCAL variant used whenever the table fits).
 template <int WDT, int ODT, int MODE, int LOGL, int CH>
-__global__ __launch_bounds__(kThreads) void fq_fwd_kernel(FwdArgs a, int nbt) {
+__global__ __launch_bounds__(kThreads) void fq_fwd_kernel(FwdArgs a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   constexpr int L = 1 << LOGL;
   constexpr int WPW = 512 * CH;                     // weights per wave
+  constexpr bool has_nb = MODE == 3;
+  constexpr bool keyed = LOGL <= 4;                 // rank by 64-bit keys
   const TileGeom& g = a.t;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int gw = WPW >> g.logg;                     // groups per wave (g divides 512)
   const int ew = gw << LOGL;                        // table entries per wave
-  const bool has_nb = MODE == 1 && nbt;
   char* mine = smem + size_t(wave) * wave_lds_bytes(g.logg, LOGL, has_nb, CH);
   LevelTables tab;
   char* p = carve_tables(tab, mine, ew);
@@ -115,6 +145,7 @@ __global__ __launch_bounds__(kThreads) void fq_fwd_kernel(FwdArgs a, int nbt) {
   float* s_zu = s_ds + gw;
   float* s_dl = s_zu + gw;
   float* s_tau = s_dl + gw;
+  uint64_t* keys = reinterpret_cast<uint64_t*>(s_tau + gw);  // [ew] when keyed; 16-byte aligned (16 gw bytes above)
   const int64_t wbase = (int64_t(blockIdx.x) * (blockDim.x >> 6) + wave) * WPW;  // first weight of this wave
   if (wbase >= g.N) return;                                       // whole wave past the end
   const int nvalid = int(min<int64_t>(WPW, g.N - wbase));        // a multiple of g (and of 8)
@@ -141,10 +172,12 @@ __global__ __launch_bounds__(kThreads) void fq_fwd_kernel(FwdArgs a, int nbt) {
     }
   }
 
-  // raw levels by code, and the per-group parameters
+  // raw levels by code (and their sort keys), and the per-group parameters
   for (int e = lane; e < ev; e += 64) {
     const int gl = e >> LOGL;
-    tab.raw[e] = level_value(a.alpha + (gid0 + gl) * g.k, a.z_b[gid0 + gl], g.k, e & (L - 1));
+    const float q = level_value_k<LOGL>(a.alpha + (gid0 + gl) * LOGL, a.z_b[gid0 + gl], e & (L - 1));
+    tab.raw[e] = q;
+    if constexpr (keyed && MODE != 2) keys[e] = level_key(q, e & (L - 1));
   }
   for (int gl = lane; gl < gv; gl += 64) {
     const int64_t gid = gid0 + gl;
@@ -153,7 +186,7 @@ __global__ __launch_bounds__(kThreads) void fq_fwd_kernel(FwdArgs a, int nbt) {
     s_ds[gl] = dl * sr;
     s_dl[gl] = dl;
     s_zu[gl] = a.z_u ? a.z_u[gid] : 0.0f;
-    s_tau[gl] = tau_of(a.alpha + gid * g.k, g.k);
+    s_tau[gl] = tau_k<LOGL>(a.alpha + gid * LOGL);
   }
   wave_lds_sync();
   if constexpr (MODE != 2) {
@@ -164,10 +197,17 @@ __global__ __launch_bounds__(kThreads) void fq_fwd_kernel(FwdArgs a, int nbt) {
       const float* row = tab.raw + (gl << LOGL);
       const float q = row[b];
       int rank = 0;
+      if constexpr (keyed) {
+        const uint64_t* krow = keys + (gl << LOGL);
+        const uint64_t kb = krow[b];
 #pragma unroll
-      for (int b2 = 0; b2 < L; ++b2) {
-        const float q2 = row[b2];
-        rank += (q2 < q) | ((q2 == q) & (b2 < b));
+        for (int b2 = 0; b2 < L; ++b2) rank += krow[b2] < kb;
+      } else {
+#pragma unroll
+        for (int b2 = 0; b2 < L; ++b2) {
+          const float q2 = row[b2];
+          rank += (q2 < q) | ((q2 == q) & (b2 < b));
+        }
       }
       tab.qs[(gl << LOGL) + rank] = q;
       tab.code_of[(gl << LOGL) + rank] = uint8_t(b);
@@ -220,7 +260,7 @@ __global__ __launch_bounds__(kThreads) void fq_fwd_kernel(FwdArgs a, int nbt) {
         d = fabsf(wb - wt);
       } else {
         const uint32_t c0 = byte_of(prev[h], i) & uint32_t(L - 1);
-        if (has_nb) {
+        if constexpr (has_nb) {
           // first nearest of (d-1, d, d+1) in ascending order
           const float4 e4 = nbg[c0];
           const uint32_t cs = __float_as_uint(e4.w);
@@ -463,7 +503,7 @@ static int fwd_waves_per_block(size_t wave_bytes) {
 }
 
 template <typename Kern>
-static hipError_t launch_fwd_kern(Kern kern, const FwdArgs& a, size_t wave_bytes, int nbt, int ch, hipStream_t st) {
+static hipError_t launch_fwd_kern(Kern kern, const FwdArgs& a, size_t wave_bytes, int ch, hipStream_t st) {
   const int wpb = fwd_waves_per_block(wave_bytes);
   const size_t lds = size_t(wpb) * wave_bytes;
   if (lds > 65536) {
@@ -473,37 +513,46 @@ static hipError_t launch_fwd_kern(Kern kern, const FwdArgs& a, size_t wave_bytes
   }
   const int64_t per_wave = 512 * int64_t(ch);
   const int64_t waves = (a.t.N + per_wave - 1) / per_wave;
-  hipLaunchKernelGGL(kern, dim3(unsigned((waves + wpb - 1) / wpb)), dim3(64 * wpb), lds, st, a, nbt);
+  hipLaunchKernelGGL(kern, dim3(unsigned((waves + wpb - 1) / wpb)), dim3(64 * wpb), lds, st, a);
   return hipGetLastError();
 }
 
 // Chunks per wavefront: two (twice the loads in flight) for the bf16 step path
-// with k <= 4 when the doubled tables stay small; one otherwise.
-template <int LOGL, int WD, int OD>
-static constexpr bool two_chunks_ok() { return WD == BF16 && OD == BF16 && LOGL <= 4; }
+// (LOCAL and FROZEN mapping, k <= 4) when the doubled tables stay small; one
+// otherwise (FULL mapping holds more registers per weight, so one chunk keeps
+// more wavefronts resident).
+template <int LOGL, int WD, int OD, int MD>
+static constexpr bool two_chunks_ok() { return WD == BF16 && OD == BF16 && LOGL <= 4 && MD != 0; }
 
 template <int WD, int OD, int MD, int LOGL>
-static hipError_t launch_fwd_l(const FwdArgs& a, int nbt, hipStream_t st) {
-  if constexpr (two_chunks_ok<LOGL, WD, OD>()) {
-    const size_t wb2 = wave_lds_bytes(a.t.logg, LOGL, nbt != 0, 2);
-    if (wb2 <= 16384) return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, LOGL, 2>, a, wb2, nbt, 2, st);
+static hipError_t launch_fwd_l(const FwdArgs& a, hipStream_t st) {
+  constexpr bool nbt = MD == 3;
+  if constexpr (two_chunks_ok<LOGL, WD, OD, MD>()) {
+    const size_t wb2 = wave_lds_bytes(a.t.logg, LOGL, nbt, 2);
+    if (wb2 <= 16384) return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, LOGL, 2>, a, wb2, 2, st);
   }
-  return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, LOGL, 1>, a, wave_lds_bytes(a.t.logg, LOGL, nbt != 0, 1), nbt,
-                         1, st);
+  return launch_fwd_kern(fq_fwd_kernel<WD, OD, MD, LOGL, 1>, a, wave_lds_bytes(a.t.logg, LOGL, nbt, 1), 1, st);
+}
+
+template <int WD, int OD, int MD>
+static hipError_t launch_fwd_m(const FwdArgs& a, int k, hipStream_t st) {
+  switch (k) {
+    case 1: return launch_fwd_l<WD, OD, MD, 1>(a, st);
+    case 2: return launch_fwd_l<WD, OD, MD, 2>(a, st);
+    case 3: return launch_fwd_l<WD, OD, MD, 3>(a, st);
+    case 4: return launch_fwd_l<WD, OD, MD, 4>(a, st);
+    case 5: return launch_fwd_l<WD, OD, MD, 5>(a, st);
+    case 6: return launch_fwd_l<WD, OD, MD, 6>(a, st);
+    default: return launch_fwd_l<WD, OD, MD, 7>(a, st);
+  }
 }
 
 template <int WD, int OD, int MD>
 static hipError_t launch_fwd_k(const FwdArgs& a, int k, hipStream_t st) {
-  const int nbt = (MD == 1 && use_neighbour_table(a.t.logg, k)) ? 1 : 0;
-  switch (k) {
-    case 1: return launch_fwd_l<WD, OD, MD, 1>(a, nbt, st);
-    case 2: return launch_fwd_l<WD, OD, MD, 2>(a, nbt, st);
-    case 3: return launch_fwd_l<WD, OD, MD, 3>(a, nbt, st);
-    case 4: return launch_fwd_l<WD, OD, MD, 4>(a, nbt, st);
-    case 5: return launch_fwd_l<WD, OD, MD, 5>(a, nbt, st);
-    case 6: return launch_fwd_l<WD, OD, MD, 6>(a, nbt, st);
-    default: return launch_fwd_l<WD, OD, MD, 7>(a, nbt, st);
+  if constexpr (MD == 1) {
+    if (use_neighbour_table(a.t.logg, k)) return launch_fwd_m<WD, OD, 3>(a, k, st);
   }
+  return launch_fwd_m<WD, OD, MD>(a, k, st);
 }
 
 hipError_t launch_fq_fwd(const FqFwdLaunch& p, hipStream_t st) {
