@@ -41,9 +41,11 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
-# Plain 32-bit VALU operations per second: the 157.3 TFLOP/s fp32 vector peak
-# (256 CUs x 128 FMA lanes per clock x 2.4 GHz) counts an FMA as 2 flops.
-VALU_PEAK_TOPS = 157.3 / 2
+# Plain (unpacked) 32-bit VALU operations per second: 256 CUs x 4 SIMDs x 16
+# lanes x 2.4 GHz.  The 157.3 TFLOP/s fp32 vector peak counts a packed FMA as
+# 4 flops; a timed chain of independent v_add_f32 / v_fma_f32 reaches 37 T of
+# these lane-operations per second, so 39.3 T is the issue limit.
+VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
 PROFILES = os.path.join(ROOT, "profiles")
 CSRC = os.path.join(ROOT, "paper_2506_03781_amd", "csrc")
 
