@@ -345,6 +345,28 @@ def main():
         torch.cuda.synchronize()
         by_mode[name] = a.elapsed_time(b) / 10 * 1e3
 
+    # the same steps with the backward quantizer fused into the weight-gradient
+    # GEMM's epilogue (after the timed region; not part of `value`)
+    fused = None
+    if all(l.k <= 4 and l.g <= 128 and l.T % 32 == 0 for l in layers):
+        fev = []
+        for s_ in range(args.steps + 2):
+            mode = schedule(args.mode, args.warmup + args.steps + s_)
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+            e[0].record()
+            for lay in layers:
+                lay.fq_fwd(mode)
+                lay.recon(backward=False)
+                lay.grad_ste_sgd()
+            e[1].record()
+            if s_ >= 2:
+                fev.append(e)
+        torch.cuda.synchronize()
+        fused_ms = sum(a.elapsed_time(b) for a, b in fev) / len(fev)
+        fused = {"ms_per_step": fused_ms, "unfused_ms_per_step_events": sum(tot.values()),
+                 "note": "fq_fwd -> loss GEMM -> weight-gradient GEMM with the straight-through backward "
+                         "and SGD update in its epilogue (dL/dWhat never written)"}
+
     out = {
         "metric": "fake-quant fwd+bwd Gweights/s (%HBM peak); recon GEMM TFLOP/s (%MFMA)",
         "value": value,
@@ -371,6 +393,7 @@ def main():
         "kernels": ks,
         "fq_fwd_us_by_mode": by_mode,
         "roofline": roof,
+        "fused_bwd_step": fused,
         "counters_src_hash": src_hash(),
         "precision": "quantizer: fp32 arithmetic on bf16 W / fp32 s, bf16 What and dL/dWhat; "
                      "GEMMs: bf16 MFMA with fp32 accumulation",

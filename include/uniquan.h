@@ -257,6 +257,38 @@ uq_status uniquan_layer_grad(int64_t T, int64_t R, int64_t C,
                              void* grad_W_hat, int grad_dtype, void* stream);
 
 /*
+ * uniquan_layer_grad_ste_sgd -- the weight-gradient GEMM of
+ * uniquan_layer_grad with the straight-through backward and the SGD update
+ * of uniquan_fq_bwd_sgd run in its epilogue (Algorithm 1's backward and
+ * update lines; appendix "Implementation details" for the filter).  The
+ * gradient dL/dWhat = 2 Et Xt^T never leaves the chip: each 256 x 256 tile
+ * applies, to the fp32 accumulators,
+ *     grad_s = -m Delta G (wbar - z_U) / s,  s -= lr_f grad_s
+ *     grad_alpha_i = Delta sum_g sigma_i G,  alpha -= lr_b grad_alpha
+ *     grad_z_B = Delta sum_g G,              z_B -= lr_b grad_z_B
+ * with the mask m from bit 7 of the code byte (as uniquan_fq_bwd), group
+ * sums over g/8 lanes in a fixed butterfly order.  Differs from the
+ * unfused path only in using the fp32 gradient instead of its bf16 copy.
+ *
+ * Et [R*T] bf16, Xt [C*T] bf16 (as uniquan_layer_grad); W, s (in/out),
+ * s_r, delta, z_u, alpha (in/out), z_b (in/out), codes as for
+ * uniquan_fq_bwd_sgd; grad_s [R*C], grad_alpha [Gn*k], grad_z_b [Gn]:
+ * optional copies of the gradients (NULL = not stored).
+ * Limits: 1 <= k <= 4, g <= 128, T % 32 == 0 (UQ_EUNSUPPORTED otherwise),
+ * plus the shape rules of uniquan_fq_fwd and uniquan_layer_grad.
+ */
+uq_status uniquan_layer_grad_ste_sgd(int64_t T, int64_t R, int64_t C, int k, int g,
+                                     const uint16_t* Et, const uint16_t* Xt,
+                                     const void* W, int w_dtype,
+                                     float* s, const float* s_r,
+                                     const float* delta, const float* z_u,
+                                     float* alpha, float* z_b,
+                                     const uint8_t* codes,
+                                     float lr_f, float lr_b,
+                                     float* grad_s, float* grad_alpha, float* grad_z_b,
+                                     void* stream);
+
+/*
  * uniquan_fold_to_bcq -- Theorem 1 and Eq. (4): plain binary-coding
  * parameters that reproduce Delta * (C alpha + z_B - z_U) exactly in real
  * arithmetic:

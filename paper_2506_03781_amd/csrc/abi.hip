@@ -196,6 +196,28 @@ uq_status uniquan_layer_grad(int64_t T, int64_t R, int64_t C, const uint16_t* Et
   return hip_status(fn, uq::launch_gemm(b, static_cast<hipStream_t>(stream)));
 }
 
+uq_status uniquan_layer_grad_ste_sgd(int64_t T, int64_t R, int64_t C, int k, int g, const uint16_t* Et,
+                                     const uint16_t* Xt, const void* W, int w_dtype, float* s, const float* s_r,
+                                     const float* delta, const float* z_u, float* alpha, float* z_b,
+                                     const uint8_t* codes, float lr_f, float lr_b, float* grad_s,
+                                     float* grad_alpha, float* grad_z_b, void* stream) {
+  const char* fn = "uniquan_layer_grad_ste_sgd";
+  if (uq_status st = check_gemm_dims(fn, T, R, C)) return st;
+  if (uq_status st = check_quant_shape(fn, R, C, k, g)) return st;
+  if (k > 4) return fail(UQ_EUNSUPPORTED, "%s: k = %d, supported 1..4", fn, k);
+  if (g > 128) return fail(UQ_EUNSUPPORTED, "%s: g = %d, supported up to 128", fn, g);
+  if (T % 32 != 0) return fail(UQ_EUNSUPPORTED, "%s: T = %lld, must be a multiple of 32", fn, (long long)T);
+  if (!is_dtype(w_dtype)) return fail(UQ_EINVAL, "%s: bad dtype", fn);
+  REQ_PTR(Et, 16); REQ_PTR(Xt, 16); REQ_PTR(W, 16); REQ_PTR(s, 16); REQ_PTR(alpha, 4); REQ_PTR(z_b, 4);
+  REQ_PTR(codes, 16);
+  OPT_PTR(s_r, 4); OPT_PTR(delta, 4); OPT_PTR(z_u, 4); OPT_PTR(grad_s, 16); OPT_PTR(grad_alpha, 4);
+  OPT_PTR(grad_z_b, 4);
+  uq::GemmLaunch b{Et, Xt, R, C, T, uq::EPI_STE, nullptr, nullptr, nullptr, 2.0f};
+  b.ste = uq::SteParams{W, w_dtype == UQ_BF16 ? 1 : 0, s, s_r, delta, z_u, alpha, z_b, codes,
+                        __builtin_ctz(unsigned(g)), int(C / g), lr_f, lr_b, grad_s, grad_alpha, grad_z_b};
+  return hip_status(fn, uq::launch_gemm_ste(b, k, static_cast<hipStream_t>(stream)));
+}
+
 uq_status uniquan_fold_to_bcq(int64_t R, int64_t C, int k, int g, const void* W, int w_dtype, const float* s,
                               const float* s_r, const float* delta, const float* z_u, const float* alpha,
                               const float* z_b, float* alpha_star, float* z_star, uint8_t* codes_out,

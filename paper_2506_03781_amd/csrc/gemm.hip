@@ -1,21 +1,24 @@
 // Reconstruction contractions on bf16 MFMA (gfx950 v_mfma_f32_32x32x16_bf16)
 // with fused epilogues:
-//   target   Yt = W X^T                    (once per layer)
-//   forward  Et = What X^T - Yt, sum Et^2   (loss partials per workgroup)
-//   backward G  = 2 Et Xt^T                 (weight gradient)
-// All three are C[M x N] = A[M x K] B[N x K]^T with both operands K-contiguous
+//   target   Yt = W X^T                       (once per layer)
+//   forward  Et = What X^T [- Yt], sum Et^2    (loss partials per workgroup;
+//                                               no target in the residual form)
+//   backward G  = 2 Et Xt^T                    (weight gradient, bf16 or fp32),
+//            or the straight-through backward + SGD update applied to G in
+//            the epilogue (G never stored)
+// All are C[M x N] = A[M x K] B[N x K]^T with both operands K-contiguous
 // ("NT"), so one kernel template serves them.
 //
 // Tiling: a 256-thread workgroup (4 wavefronts, 2 x 2) computes a BM x BN
 // tile (256x256, 256x128 or 128x128, the largest that still fills the 256
 // compute units); each wavefront owns (BM/2) x (BN/2) as a grid of 32x32 MFMA
-// blocks with fp32 accumulators.  K advances in slabs of 64: the next slab is
-// fetched from global memory into registers (16-byte loads, 8 lanes per
-// 128-byte row segment) while the MFMAs consume the current slab from one of
-// two LDS buffers, so one barrier per slab suffices.  LDS rows are XOR-
-// swizzled instead of padded.  Workgroups are renumbered so that each XCD
-// gets a contiguous run of tiles walked in groups of 8 row-tiles, which keeps
-// the operand panels it needs in its own L2.
+// blocks with fp32 accumulators.  The main kernel streams K in 32-wide
+// slices through a 4-stage LDS ring filled by global_load_lds_dwordx4 (direct
+// to LDS, XOR-swizzled rows) with explicit vmcnt waits and s_barrier; a
+// register-staged variant with 64-wide double-buffered slabs serves K not
+// divisible by 32.  Workgroups are renumbered so that each XCD gets a
+// contiguous run of tiles walked in groups of 8 row-tiles, which keeps the
+// operand panels it needs in its own L2.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -35,6 +38,7 @@ struct GemmArgs {
   float* partials;
   float scale;
   int tiles_m, tiles_n;
+  SteParams ste;
 };
 
 // Two fp32 values -> packed bf16 pair (lo in bits 0..15), round to nearest
@@ -76,6 +80,123 @@ __device__ __forceinline__ int slot(int row, int kc) { return row * 8 + (kc ^ (r
 // contiguous 16-byte / 8-byte vectors.  `scratch` must hold 4 * 32 * WN
 // floats and may alias the operand stages (all waves are past their last
 // operand read when this is called).
+// Straight-through backward of one strip (32 rows x 128 columns of the
+// wave's tile, staged in LDS as fp32 acc) with the SGD update, the same
+// arithmetic as the standalone backward kernel: lane l takes 8 consecutive
+// columns of row 4 it + l / 16, a group of g columns is g / 8 adjacent lanes,
+// and the group sums use the same fixed xor-butterfly.
+template <int KB>
+__device__ __forceinline__ void ste_strip(const GemmArgs& p, const float* strip, int64_t row_base, int64_t col_base,
+                                          int lane) {
+  const SteParams& q = p.ste;
+  const int lpg = 1 << (q.logg - 3);
+  constexpr int NB = 8;  // row-iterations whose loads are in flight together
+#pragma unroll 1
+  for (int it0 = 0; it0 < 8; it0 += NB) {
+    uint4 wq[NB];
+    float4 s0[NB], s1[NB];
+    uint2 cb[NB];
+    float dlv[NB], srv[NB];
+    bool act[NB];
+    int64_t off[NB];
+    // loads of NB row-iterations first (the epilogue has few wavefronts per
+    // CU, so bytes in flight per lane decide the memory phase's speed)
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const int lrow = (it0 + j) * 4 + (lane >> 4);
+      const int64_t row = row_base + lrow, col = col_base + (lane & 15) * 8;
+      act[j] = row < p.M && col < p.N;
+      off[j] = row * p.N + col;
+      wq[j] = make_uint4(0, 0, 0, 0);
+      s0[j] = make_float4(1, 1, 1, 1);
+      s1[j] = s0[j];
+      cb[j] = make_uint2(0, 0);
+      dlv[j] = 1.0f;
+      srv[j] = 1.0f;
+      if (act[j]) {
+        // bf16 weights travel with this batch; fp32 weights are read at use
+        if (q.w_bf16) wq[j] = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(q.W) + off[j]);
+        const float4* sp = reinterpret_cast<const float4*>(q.s + off[j]);
+        s0[j] = sp[0];
+        s1[j] = sp[1];
+        cb[j] = *reinterpret_cast<const uint2*>(q.codes + off[j]);
+        const int64_t gid = off[j] >> q.logg;
+        dlv[j] = q.delta ? q.delta[gid] : 1.0f;
+        srv[j] = q.s_r ? q.s_r[row] : 1.0f;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const int lrow = (it0 + j) * 4 + (lane >> 4);
+      const int c8 = (lane & 15) * 8;
+      const int64_t gid = act[j] ? (off[j] >> q.logg) : 0;
+      float S = 0.0f, Sa[KB];
+#pragma unroll
+      for (int b = 0; b < KB; ++b) Sa[b] = 0.0f;
+      const float dl = dlv[j];
+      if (act[j]) {
+        float G[8], w[8];
+        const float4 g0 = *reinterpret_cast<const float4*>(strip + lrow * 128 + c8);
+        const float4 g1 = *reinterpret_cast<const float4*>(strip + lrow * 128 + c8 + 4);
+        G[0] = p.scale * g0.x; G[1] = p.scale * g0.y; G[2] = p.scale * g0.z; G[3] = p.scale * g0.w;
+        G[4] = p.scale * g1.x; G[5] = p.scale * g1.y; G[6] = p.scale * g1.z; G[7] = p.scale * g1.w;
+        if (q.w_bf16) {
+          const uint32_t wv[4] = {wq[j].x, wq[j].y, wq[j].z, wq[j].w};
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            w[2 * i] = __uint_as_float(wv[i] << 16);
+            w[2 * i + 1] = __uint_as_float(wv[i] & 0xFFFF0000u);
+          }
+        } else {
+          const float4* wp = reinterpret_cast<const float4*>(static_cast<const float*>(q.W) + off[j]);
+          const float4 a = wp[0], b = wp[1];
+          w[0] = a.x; w[1] = a.y; w[2] = a.z; w[3] = a.w; w[4] = b.x; w[5] = b.y; w[6] = b.z; w[7] = b.w;
+        }
+        const float sv[8] = {s0[j].x, s0[j].y, s0[j].z, s0[j].w, s1[j].x, s1[j].y, s1[j].z, s1[j].w};
+        const float ds = dl * srv[j];
+        float gs[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const uint32_t byte = ((i < 4 ? cb[j].x : cb[j].y) >> (8 * (i & 3))) & 0xFFu;
+          const bool m = (byte & 0x80u) != 0u;
+          const float g = G[i];
+          S += g;
+#pragma unroll
+          for (int b = 0; b < KB; ++b) Sa[b] += ((byte >> b) & 1u) ? g : -g;
+          const float x = w[i] * __builtin_amdgcn_rcpf(ds * sv[i]);
+          gs[i] = m ? -(dl * g) * x * __builtin_amdgcn_rcpf(sv[i]) : 0.0f;
+        }
+        if (q.grad_s) {
+          float4* gp = reinterpret_cast<float4*>(q.grad_s + off[j]);
+          gp[0] = make_float4(gs[0], gs[1], gs[2], gs[3]);
+          gp[1] = make_float4(gs[4], gs[5], gs[6], gs[7]);
+        }
+        float4* sp = reinterpret_cast<float4*>(q.s + off[j]);
+        sp[0] = make_float4(sv[0] - q.lr_f * gs[0], sv[1] - q.lr_f * gs[1], sv[2] - q.lr_f * gs[2],
+                            sv[3] - q.lr_f * gs[3]);
+        sp[1] = make_float4(sv[4] - q.lr_f * gs[4], sv[5] - q.lr_f * gs[5], sv[6] - q.lr_f * gs[6],
+                            sv[7] - q.lr_f * gs[7]);
+      }
+      for (int msk = lpg >> 1; msk >= 1; msk >>= 1) {
+        S += __shfl_xor(S, msk, 64);
+#pragma unroll
+        for (int b = 0; b < KB; ++b) Sa[b] += __shfl_xor(Sa[b], msk, 64);
+      }
+      if (act[j] && (lane & (lpg - 1)) == 0) {
+        const float gzb = dl * S;
+#pragma unroll
+        for (int b = 0; b < KB; ++b) {
+          const float ga = dl * Sa[b];
+          if (q.grad_alpha) q.grad_alpha[gid * KB + b] = ga;
+          q.alpha[gid * KB + b] = q.alpha[gid * KB + b] - q.lr_b * ga;
+        }
+        if (q.grad_z_b) q.grad_z_b[gid] = gzb;
+        q.z_b[gid] = q.z_b[gid] - q.lr_b * gzb;
+      }
+    }
+  }
+}
+
 template <int BM, int BN, int EPI, int FM = BM / 64, int FN = BN / 64>
 __device__ __forceinline__ void epilogue(const GemmArgs& p, f32x16 (&acc)[FM][FN], int64_t m0, int64_t n0,
                                          int wm, int wn, int lane, int wave, int tid, float* scratch) {
@@ -98,6 +219,13 @@ __device__ __forceinline__ void epilogue(const GemmArgs& p, f32x16 (&acc)[FM][FN
     __builtin_amdgcn_wave_barrier();
     const int64_t row_base = m0 + wm * WM + i * 32;
     const int64_t col_base = n0 + wn * WN;
+    if constexpr (EPI >= EPI_STE) {
+      static_assert(WN == 128, "the fused backward needs 128-column wave tiles");
+      ste_strip<EPI - EPI_STE>(p, strip, row_base, col_base, lane);
+      __builtin_amdgcn_s_waitcnt(0xC07F);  // strip reads done before the next strip overwrites it
+      __builtin_amdgcn_wave_barrier();
+      continue;
+    }
     float4 y[ITER];
     if constexpr (EPI == EPI_LOSS) {
       // no target: the A operand already holds the residual What - W
@@ -129,7 +257,7 @@ __device__ __forceinline__ void epilogue(const GemmArgs& p, f32x16 (&acc)[FM][FN
       } else if constexpr (EPI == EPI_GRAD_BF16) {
         *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.out) + o) =
             make_uint2(pack_bf16x2(p.scale * v.x, p.scale * v.y), pack_bf16x2(p.scale * v.z, p.scale * v.w));
-      } else {
+      } else if constexpr (EPI == EPI_GRAD_F32) {
         *reinterpret_cast<float4*>(static_cast<float*>(p.out) + o) =
             make_float4(p.scale * v.x, p.scale * v.y, p.scale * v.z, p.scale * v.w);
       }
@@ -463,6 +591,25 @@ static hipError_t launch_bm(const GemmLaunch& q, hipStream_t st) {
     case EPI_LOSS: launch_epi<BM, BN, EPI_LOSS>(a, grid, st); break;
     case EPI_GRAD_BF16: launch_epi<BM, BN, EPI_GRAD_BF16>(a, grid, st); break;
     default: launch_epi<BM, BN, EPI_GRAD_F32>(a, grid, st); break;
+  }
+  return hipGetLastError();
+}
+
+// Weight-gradient GEMM with the fused straight-through backward: 256 x 256
+// tiles (128-column wave tiles hold whole groups for g <= 128), K % 32 == 0.
+hipError_t launch_gemm_ste(const GemmLaunch& q, int k, hipStream_t st) {
+  GemmArgs a;
+  a.A = q.A; a.B = q.B; a.M = q.M; a.N = q.N; a.K = q.K;
+  a.Yt = nullptr; a.out = nullptr; a.partials = nullptr; a.scale = q.scale;
+  a.ste = q.ste;
+  a.tiles_m = int((q.M + 255) / 256);
+  a.tiles_n = int((q.N + 255) / 256);
+  const dim3 grid(unsigned(a.tiles_m * a.tiles_n));
+  switch (k) {
+    case 1: hipLaunchKernelGGL((gemm_pipe_kernel<256, 256, EPI_STE + 1, 4, 0>), grid, dim3(256), 0, st, a); break;
+    case 2: hipLaunchKernelGGL((gemm_pipe_kernel<256, 256, EPI_STE + 2, 4, 0>), grid, dim3(256), 0, st, a); break;
+    case 3: hipLaunchKernelGGL((gemm_pipe_kernel<256, 256, EPI_STE + 3, 4, 0>), grid, dim3(256), 0, st, a); break;
+    default: hipLaunchKernelGGL((gemm_pipe_kernel<256, 256, EPI_STE + 4, 4, 0>), grid, dim3(256), 0, st, a); break;
   }
   return hipGetLastError();
 }

@@ -68,10 +68,22 @@ struct InitUnifiedLaunch {
 };
 
 // GEMM epilogues of the reconstruction contractions.
+// Straight-through backward with the SGD update, run in the weight-gradient
+// GEMM's epilogue on the fp32 gradient tile (see uniquan_layer_grad_ste_sgd).
+struct SteParams {
+  const void* W; int w_bf16;
+  float* s; const float* s_r; const float* delta; const float* z_u;
+  float* alpha; float* z_b; const uint8_t* codes;
+  int logg, gpr;
+  float lr_f, lr_b;
+  float* grad_s; float* grad_alpha; float* grad_z_b;  // optional copies of the gradients
+};
+
 enum GemmEpi : int {
   EPI_TARGET = 0,     // out fp32 = acc
   EPI_LOSS = 1,       // e = acc - Yt; out bf16 = e; partial sum of e^2 per workgroup
   EPI_GRAD_BF16 = 2,  // out bf16 = scale * acc
+  EPI_STE = 16,       // EPI_STE + k: scale * acc is dL/dWhat; straight-through backward + SGD in place
   EPI_GRAD_F32 = 3,   // out fp32 = scale * acc
 };
 
@@ -84,6 +96,7 @@ struct GemmLaunch {
   void* out;
   float* partials;     // EPI_LOSS, one per workgroup
   float scale;
+  SteParams ste;       // EPI_STE
 };
 
 hipError_t launch_fq_fwd(const FqFwdLaunch& p, hipStream_t st);
@@ -93,6 +106,7 @@ hipError_t launch_dequant(const DequantLaunch& p, hipStream_t st);
 hipError_t launch_greedy(const GreedyLaunch& p, hipStream_t st);
 hipError_t launch_init_unified(const InitUnifiedLaunch& p, hipStream_t st);
 hipError_t launch_gemm(const GemmLaunch& p, hipStream_t st);
+hipError_t launch_gemm_ste(const GemmLaunch& p, int k, hipStream_t st);
 size_t gemm_workgroups(int64_t M, int64_t N, int epi);
 hipError_t launch_reduce_loss(const float* partials, int64_t n, float* loss, hipStream_t st);
 hipError_t launch_transpose(int64_t rows, int64_t cols, const uint16_t* in, uint16_t* out, hipStream_t st);

@@ -88,6 +88,13 @@ class QuantLayer:
                           self.alpha, self.z_b, self.codes, self.G, self.grad_s, self.grad_alpha,
                           self.grad_z_b)
 
+    def grad_ste_sgd(self, lr_f=0.005, lr_b=0.0005):
+        """Weight-gradient GEMM with the straight-through backward and the SGD
+        update in its epilogue (dL/dWhat stays on chip); needs Et from recon."""
+        uq.uniquan_layer_grad_ste_sgd(self.T, self.R, self.C, self.k, self.g, self.Et, self.Xt, self.W, self.s,
+                                      self.s_r, self.delta, self.z_u, self.alpha, self.z_b, self.codes,
+                                      lr_f, lr_b)
+
     def fq_bwd_sgd(self, lr_f=0.005, lr_b=0.0005, keep_grads=False):
         """Backward with the SGD update of s, alpha, z_B fused into the same pass
         (gradients stored only with keep_grads)."""

@@ -48,6 +48,8 @@ _SIGS = {
     "uniquan_recon_ws": ([_i64, _i64, _i64], ctypes.c_size_t),
     "uniquan_layer_recon": ([_i64, _i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp, _i32, _vp], _i32),
     "uniquan_layer_grad": ([_i64, _i64, _i64, _vp, _vp, _vp, _i32, _vp], _i32),
+    "uniquan_layer_grad_ste_sgd": ([_i64, _i64, _i64, _i32, _i32, _vp, _vp, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp,
+                                    _vp, _f32, _f32, _vp, _vp, _vp, _vp], _i32),
     "uniquan_fold_to_bcq": ([_i64, _i64, _i32, _i32, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp], _i32),
     "uniquan_bcq_dequant": ([_i64, _i64, _i32, _i32, _vp, _vp, _vp, _vp, _i32, _vp], _i32),
     "uniquan_init_greedy": ([_i64, _i64, _i32, _i32, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp], _i32),
@@ -197,6 +199,17 @@ def uniquan_layer_recon(T, R, C, X, Xt, W_hat, Yt, loss, Et_ws, partials_ws, gra
 def uniquan_layer_grad(T, R, C, Et, Xt, grad_W_hat, stream=None):
     _check(lib().uniquan_layer_grad(T, R, C, _p(Et, R * T, _B, "Et"), _p(Xt, T * C, _B, "Xt"),
                                     _p(grad_W_hat, R * C, _W, "grad_W_hat"), _dt(grad_W_hat), _stream(stream)))
+
+
+def uniquan_layer_grad_ste_sgd(T, R, C, k, g, Et, Xt, W, s, s_r, delta, z_u, alpha, z_b, codes, lr_f, lr_b,
+                               grad_s=None, grad_alpha=None, grad_z_b=None, stream=None):
+    N, Gn = R * C, R * C // g
+    _check(lib().uniquan_layer_grad_ste_sgd(
+        T, R, C, k, g, _p(Et, R * T, _B, "Et"), _p(Xt, T * C, _B, "Xt"), _p(W, N, _W, "W"), _dt(W),
+        _p(s, N, _F, "s"), _p(s_r, R, _F, "s_r"), _p(delta, Gn, _F, "delta"), _p(z_u, Gn, _F, "z_u"),
+        _p(alpha, Gn * k, _F, "alpha"), _p(z_b, Gn, _F, "z_b"), _p(codes, N, _U8, "codes"),
+        float(lr_f), float(lr_b), _p(grad_s, N, _F, "grad_s"), _p(grad_alpha, Gn * k, _F, "grad_alpha"),
+        _p(grad_z_b, Gn, _F, "grad_z_b"), _stream(stream)))
 
 
 def uniquan_fold_to_bcq(R, C, k, g, W, s, s_r, delta, z_u, alpha, z_b, alpha_star, z_star,

@@ -107,6 +107,18 @@ def test_other_validation(L):
     assert L.uniquan_sgd(0, FAKE, FAKE, ctypes.c_float(0.1), None) == uq.UQ_EINVAL
 
 
+def test_layer_grad_ste_sgd_validation(L):
+    def call(T=64, k=3, g=128, codes=FAKE):
+        return L.uniquan_layer_grad_ste_sgd(T, 64, 256, k, g, FAKE, FAKE, FAKE, 1, FAKE, None, None, None,
+                                            FAKE, FAKE, codes, ctypes.c_float(0.1), ctypes.c_float(0.1),
+                                            None, None, None, None)
+    assert call(k=5) == uq.UQ_EUNSUPPORTED
+    assert call(g=256) == uq.UQ_EUNSUPPORTED
+    assert call(T=48) == uq.UQ_EUNSUPPORTED
+    assert call(T=60) == uq.UQ_EINVAL
+    assert call(codes=None) == uq.UQ_EINVAL
+
+
 @pytest.mark.parametrize("kw,status,text", [
     (dict(k=5), uq.UQ_EUNSUPPORTED, "k = 5"),
     (dict(G=0), uq.UQ_EINVAL, "grid_G"),
