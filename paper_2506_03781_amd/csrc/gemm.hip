@@ -72,14 +72,6 @@ __device__ __forceinline__ void tile_of(int bid, int nb, int tiles_m, int tiles_
 // offset land in 8 distinct bank groups (no padding needed).
 __device__ __forceinline__ int slot(int row, int kc) { return row * 8 + (kc ^ (row & 7)); }
 
-// Store an accumulator tile with the requested epilogue, staged through LDS
-// one 32-row strip at a time.  Accumulator register r of lane l of a 32x32
-// MFMA block holds row 8*(r/4) + 4*(l/32) + r%4 and column l%32; each wave
-// writes its strip (32 x WN fp32) to its own LDS region, then reads it back
-// as rows of float4 so that the target is loaded and the output stored as
-// contiguous 16-byte / 8-byte vectors.  `scratch` must hold 4 * 32 * WN
-// floats and may alias the operand stages (all waves are past their last
-// operand read when this is called).
 // Straight-through backward of one strip (32 rows x 128 columns of the
 // wave's tile, staged in LDS as fp32 acc) with the SGD update, the same
 // arithmetic as the standalone backward kernel: lane l takes 8 consecutive
@@ -197,6 +189,14 @@ __device__ __forceinline__ void ste_strip(const GemmArgs& p, const float* strip,
   }
 }
 
+// Store an accumulator tile with the requested epilogue, staged through LDS
+// one 32-row strip at a time.  Accumulator register r of lane l of a 32x32
+// MFMA block holds row 8*(r/4) + 4*(l/32) + r%4 and column l%32; each wave
+// writes its strip (32 x WN fp32) to its own LDS region, then reads it back
+// as rows of float4 so that the target is loaded and the output stored as
+// contiguous 16-byte / 8-byte vectors.  `scratch` must hold 4 * 32 * WN
+// floats and may alias the operand stages (all waves are past their last
+// operand read when this is called).
 template <int BM, int BN, int EPI, int FM = BM / 64, int FN = BN / 64>
 __device__ __forceinline__ void epilogue(const GemmArgs& p, f32x16 (&acc)[FM][FN], int64_t m0, int64_t n0,
                                          int wm, int wn, int lane, int wave, int tid, float* scratch) {

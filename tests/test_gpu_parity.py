@@ -315,7 +315,10 @@ def run_recon(X, Wh, Yt_np, with_grad=True, gdt=torch.bfloat16):
     return float(loss.item()), host(Et), (host(G) if with_grad else None), host(Xt)
 
 
-@pytest.mark.parametrize("T,R,C", [(64, 256, 256), (200, 300, 264), (512, 640, 768), (8, 8, 8), (136, 1000, 136)])
+# (2000, 4000, 192): 256 x 128 tiles with ragged rows and columns and three
+# 64-deep K stages (the double-buffered 64-deep kernel)
+@pytest.mark.parametrize("T,R,C", [(64, 256, 256), (200, 300, 264), (512, 640, 768), (8, 8, 8), (136, 1000, 136),
+                                   (2000, 4000, 192)])
 def test_recon(T, R, C):
     rs = np.random.default_rng(T + R + C)
     X = synth.round_to_bf16(rs.standard_normal((T, C)).astype(F32))
@@ -560,7 +563,8 @@ def test_fwd_residual(mode, wdt):
     assert np.array_equal(rb, O.bf16_rne(res32))
 
 
-@pytest.mark.parametrize("T,R,C", [(64, 256, 256), (200, 300, 264), (136, 1000, 136), (4096, 4096, 128)])
+@pytest.mark.parametrize("T,R,C", [(64, 256, 256), (200, 300, 264), (136, 1000, 136), (4096, 4096, 128),
+                                   (2000, 4000, 192)])
 def test_recon_residual(T, R, C):
     rs = np.random.default_rng(T + 7 * R + C)
     X = synth.round_to_bf16(rs.standard_normal((T, C)).astype(F32))
