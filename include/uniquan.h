@@ -322,6 +322,49 @@ uq_status uniquan_bcq_dequant(int64_t R, int64_t C, int k, int g,
                               void* stream);
 
 /*
+ * Deployment form of a folded layer and its inference product (the single
+ * binary-coding step R_B(C; Theta*) that Theorem 1 leaves; storage as in the
+ * appendix "Memory usage": g k + 16 (k + 1) bits per group).
+ *
+ * Layout (rows are the fastest index of every array):
+ *   planes  uint32 [k][C/128][R][4]: word m of quad q of row r in plane i
+ *           has bit j = bit i of the code of column 128 q + 32 m + j
+ *           (1 <=> c_{i+1} = +1);
+ *   alpha16 IEEE binary16 [k][C/g][R]: alpha*_{i+1} of group (r, j);
+ *   z16     IEEE binary16 [C/g][R]:    z*_B of group (r, j).
+ * Shape rules: 1 <= k <= 4, C % 128 == 0, g % 128 == 0, C % g == 0
+ * (UQ_EUNSUPPORTED otherwise).
+ */
+
+/*
+ * uniquan_bcq_pack -- the stored form from uniquan_fold_to_bcq's outputs:
+ * codes [R*C] uint8 (bits 0..k-1 used, 16-byte aligned), alpha_star [Gn*k],
+ * z_star [Gn] fp32 (rounded to binary16, to nearest even).  planes
+ * (16-byte aligned) R*C*k/8 bytes, alpha16 Gn*k and z16 Gn halves out.
+ */
+uq_status uniquan_bcq_pack(int64_t R, int64_t C, int k, int g,
+                           const uint8_t* codes, const float* alpha_star,
+                           const float* z_star, uint32_t* planes,
+                           uint16_t* alpha16, uint16_t* z16, void* stream);
+
+/*
+ * uniquan_bcq_matmul -- Y = X What^T for a batch of T <= 8 activation rows,
+ * What[r][c] = z* + sum_i alpha*_i sigma_i(r, c) from the stored form:
+ * X [T*C] bf16 (8-byte aligned), Y [T*R] fp32 out.  Per group the kernel
+ * uses sum_c sigma_i x_c = 2 P_i - S (S: the group's activation sum, P_i:
+ * the sum over columns whose bit i is set), P_i from 16-entry subset-sum
+ * tables of 4 activations; fp32 accumulation, deterministic order.
+ * partials_ws [partials_len] fp32 workspace of at least
+ * uniquan_bcq_matmul_ws(T, R, C) floats (0: may be NULL).
+ */
+size_t uniquan_bcq_matmul_ws(int T, int64_t R, int64_t C);
+uq_status uniquan_bcq_matmul(int T, int64_t R, int64_t C, int k, int g,
+                             const uint16_t* X, const uint32_t* planes,
+                             const uint16_t* alpha16, const uint16_t* z16,
+                             float* Y, float* partials_ws, size_t partials_len,
+                             void* stream);
+
+/*
  * uniquan_init_greedy -- greedy binary-coding start of the appendix
  * algorithm "General alternating update" (its first step): per group,
  * r = wbar - z_B with wbar = T_F(w) as in uniquan_fq_fwd; then for

@@ -276,6 +276,53 @@ uq_status uniquan_init_unified(int64_t R, int64_t C, int k, int g, const void* W
   return hip_status(fn, uq::launch_init_unified(p, static_cast<hipStream_t>(stream)));
 }
 
+// Shape rules of the deployment form: 16-byte plane words cover 128 columns
+// and each word lies inside one group.
+static uq_status check_bcq_shape(const char* fn, int64_t R, int64_t C, int k, int g) {
+  if (R < 1 || C < 1) return fail(UQ_EINVAL, "%s: R=%lld and C=%lld must be >= 1", fn, (long long)R, (long long)C);
+  if (k < 1 || k > 4) return fail(UQ_EUNSUPPORTED, "%s: k=%d, supported 1..4", fn, k);
+  if (C % 128 != 0) return fail(UQ_EUNSUPPORTED, "%s: C=%lld must be a multiple of 128", fn, (long long)C);
+  if (g < 128 || g % 128 != 0) return fail(UQ_EUNSUPPORTED, "%s: g=%d must be a multiple of 128", fn, g);
+  if (C % g != 0) return fail(UQ_EINVAL, "%s: g=%d must divide C=%lld", fn, g, (long long)C);
+  if (R >= (int64_t(1) << 31) || R > (int64_t(1) << 40) / C)
+    return fail(UQ_EUNSUPPORTED, "%s: R*C too large", fn);
+  return UQ_OK;
+}
+
+uq_status uniquan_bcq_pack(int64_t R, int64_t C, int k, int g, const uint8_t* codes, const float* alpha_star,
+                           const float* z_star, uint32_t* planes, uint16_t* alpha16, uint16_t* z16,
+                           void* stream) {
+  const char* fn = "uniquan_bcq_pack";
+  if (uq_status st = check_bcq_shape(fn, R, C, k, g)) return st;
+  REQ_PTR(codes, 16); REQ_PTR(alpha_star, 4); REQ_PTR(z_star, 4);
+  REQ_PTR(planes, 16); REQ_PTR(alpha16, 2); REQ_PTR(z16, 2);
+  uq::BcqPackLaunch p{R, C, k, g, codes, alpha_star, z_star, planes, alpha16, z16};
+  return hip_status(fn, uq::launch_bcq_pack(p, static_cast<hipStream_t>(stream)));
+}
+
+size_t uniquan_bcq_matmul_ws(int T, int64_t R, int64_t C) {
+  if (T < 1 || R < 1 || C < 128) return 0;
+  const int64_t slabs = uq::bcq_slabs(R, C / 128 * 128);
+  return slabs > 1 ? size_t(slabs) * size_t(T) * size_t(R) : 0;
+}
+
+uq_status uniquan_bcq_matmul(int T, int64_t R, int64_t C, int k, int g, const uint16_t* X, const uint32_t* planes,
+                             const uint16_t* alpha16, const uint16_t* z16, float* Y, float* partials_ws,
+                             size_t partials_len, void* stream) {
+  const char* fn = "uniquan_bcq_matmul";
+  if (uq_status st = check_bcq_shape(fn, R, C, k, g)) return st;
+  if (T < 1 || T > 8) return fail(UQ_EUNSUPPORTED, "%s: T=%d, supported 1..8", fn, T);
+  REQ_PTR(X, 8); REQ_PTR(planes, 16); REQ_PTR(alpha16, 2); REQ_PTR(z16, 2); REQ_PTR(Y, 4);
+  const size_t need = uniquan_bcq_matmul_ws(T, R, C);
+  if (need > 0) {
+    REQ_PTR(partials_ws, 4);
+    if (partials_len < need)
+      return fail(UQ_EINVAL, "%s: partials_len=%zu, need %zu floats (uniquan_bcq_matmul_ws)", fn, partials_len, need);
+  }
+  uq::BcqMatmulLaunch p{T, R, C, k, g, X, planes, alpha16, z16, Y, partials_ws};
+  return hip_status(fn, uq::launch_bcq_matmul(p, static_cast<hipStream_t>(stream)));
+}
+
 uq_status uniquan_sgd(int64_t n, float* theta, const float* grad, float lr, void* stream) {
   const char* fn = "uniquan_sgd";
   if (n < 1) return fail(UQ_EINVAL, "%s: n must be >= 1", fn);

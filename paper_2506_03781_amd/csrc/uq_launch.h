@@ -99,6 +99,21 @@ struct GemmLaunch {
   SteParams ste;       // EPI_STE
 };
 
+// Deployment form (bit-planes + binary16 Theta*_B) and its product.
+struct BcqPackLaunch {
+  int64_t R, C;
+  int k, g;
+  const uint8_t* codes; const float* alpha_star; const float* z_star;
+  uint32_t* planes; uint16_t* alpha16; uint16_t* z16;
+};
+struct BcqMatmulLaunch {
+  int T;
+  int64_t R, C;
+  int k, g;
+  const uint16_t* X; const uint32_t* planes; const uint16_t* alpha16; const uint16_t* z16;
+  float* Y; float* partials;
+};
+
 hipError_t launch_fq_fwd(const FqFwdLaunch& p, hipStream_t st);
 hipError_t launch_fq_bwd(const FqBwdLaunch& p, hipStream_t st);
 hipError_t launch_fold(const FoldLaunch& p, hipStream_t st);
@@ -111,5 +126,8 @@ size_t gemm_workgroups(int64_t M, int64_t N, int epi);
 hipError_t launch_reduce_loss(const float* partials, int64_t n, float* loss, hipStream_t st);
 hipError_t launch_transpose(int64_t rows, int64_t cols, const uint16_t* in, uint16_t* out, hipStream_t st);
 hipError_t launch_sgd(int64_t n, float* theta, const float* grad, float lr, hipStream_t st);
+hipError_t launch_bcq_pack(const BcqPackLaunch& p, hipStream_t st);
+hipError_t launch_bcq_matmul(const BcqMatmulLaunch& p, hipStream_t st);
+int64_t bcq_slabs(int64_t R, int64_t C);
 
 }  // namespace uq

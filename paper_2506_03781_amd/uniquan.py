@@ -56,6 +56,10 @@ _SIGS = {
     "uniquan_init_unified": ([_i64, _i64, _i32, _i32, _vp, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp,
                               _vp, _vp, _vp, _vp, _vp], _i32),
     "uniquan_sgd": ([_i64, _vp, _vp, _f32, _vp], _i32),
+    "uniquan_bcq_pack": ([_i64, _i64, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp], _i32),
+    "uniquan_bcq_matmul_ws": ([_i32, _i64, _i64], ctypes.c_size_t),
+    "uniquan_bcq_matmul": ([_i32, _i64, _i64, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp],
+                           _i32),
 }
 
 _lib = None
@@ -127,6 +131,8 @@ _F = (torch.float32,)
 _W = (torch.float32, torch.bfloat16)
 _B = (torch.bfloat16,)
 _U8 = (torch.uint8,)
+_H = (torch.float16,)
+_U32 = (torch.int32, torch.uint32)  # bit-plane words (bits only)
 
 
 def uniquan_fq_fwd(R, C, k, g, W, s, s_r, delta, z_u, alpha, z_b, mode, codes, W_hat, stream=None):
@@ -250,3 +256,28 @@ def uniquan_init_unified(R, C, k, g, W, grid_G, alt_T, clip, delta, z_u, alpha, 
 def uniquan_sgd(theta, grad, lr, stream=None):
     n = theta.numel()
     _check(lib().uniquan_sgd(n, _p(theta, n, _F, "theta"), _p(grad, n, _F, "grad"), float(lr), _stream(stream)))
+
+
+def uniquan_bcq_pack(R, C, k, g, codes, alpha_star, z_star, planes, alpha16, z16, stream=None):
+    """Stored form from the fold: planes (R*C*k/32 32-bit words), alpha16
+    (Gn*k) and z16 (Gn) binary16 out."""
+    N, Gn = R * C, R * C // g
+    _check(lib().uniquan_bcq_pack(
+        R, C, k, g, _p(codes, N, _U8, "codes"), _p(alpha_star, Gn * k, _F, "alpha_star"),
+        _p(z_star, Gn, _F, "z_star"), _p(planes, N * k // 32, _U32, "planes"),
+        _p(alpha16, Gn * k, _H, "alpha16"), _p(z16, Gn, _H, "z16"), _stream(stream)))
+
+
+def uniquan_bcq_matmul_ws(T, R, C) -> int:
+    return int(lib().uniquan_bcq_matmul_ws(T, R, C))
+
+
+def uniquan_bcq_matmul(T, R, C, k, g, X, planes, alpha16, z16, Y, partials_ws=None, stream=None):
+    """Y [T, R] fp32 = X [T, C] (bf16) times the stored layer's What^T."""
+    N, Gn = R * C, R * C // g
+    need = uniquan_bcq_matmul_ws(T, R, C)
+    _check(lib().uniquan_bcq_matmul(
+        T, R, C, k, g, _p(X, T * C, _B, "X"), _p(planes, N * k // 32, _U32, "planes"),
+        _p(alpha16, Gn * k, _H, "alpha16"), _p(z16, Gn, _H, "z16"), _p(Y, T * R, _F, "Y"),
+        _p(partials_ws, need, _F, "partials_ws") if need else _p(partials_ws, None, _F, "partials_ws"),
+        partials_ws.numel() if partials_ws is not None else 0, _stream(stream)))

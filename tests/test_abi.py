@@ -140,6 +140,39 @@ def test_init_unified_validation(L, kw, status, text):
     assert L.uniquan_transpose_bf16(12, 16, FAKE, FAKE, None) == uq.UQ_EINVAL
 
 
+def bcq_mm(L, T=1, R=256, C=512, k=3, g=128, X=FAKE, planes=FAKE, a16=FAKE, z16=FAKE, Y=FAKE, ws=FAKE,
+           ws_len=1 << 30):
+    return L.uniquan_bcq_matmul(T, R, C, k, g, X, planes, a16, z16, Y, ws, ws_len, None)
+
+
+@pytest.mark.parametrize("kw,status,text", [
+    (dict(k=5), uq.UQ_EUNSUPPORTED, "k=5"),
+    (dict(C=320), uq.UQ_EUNSUPPORTED, "multiple of 128"),
+    (dict(g=64), uq.UQ_EUNSUPPORTED, "g=64"),
+    (dict(g=384), uq.UQ_EINVAL, "divide"),
+    (dict(T=9), uq.UQ_EUNSUPPORTED, "T=9"),
+    (dict(T=0), uq.UQ_EUNSUPPORTED, "T=0"),
+    (dict(planes=ODD), uq.UQ_EINVAL, "planes"),
+    (dict(X=None), uq.UQ_EINVAL, "X"),
+    (dict(ws_len=3), uq.UQ_EINVAL, "partials_len"),
+])
+def test_bcq_matmul_validation(L, kw, status, text):
+    assert bcq_mm(L, **kw) == status
+    assert text in uq.last_error()
+
+
+def test_bcq_pack_validation(L):
+    assert L.uniquan_bcq_pack(4, 256, 5, 128, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == uq.UQ_EUNSUPPORTED
+    assert L.uniquan_bcq_pack(4, 200, 2, 128, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == uq.UQ_EUNSUPPORTED
+    assert L.uniquan_bcq_pack(4, 256, 2, 128, FAKE, FAKE, FAKE, ODD, FAKE, FAKE, None) == uq.UQ_EINVAL
+    assert "planes" in uq.last_error()
+    assert L.uniquan_bcq_pack(0, 256, 2, 128, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == uq.UQ_EINVAL
+    # workspace: one partial row set per column slab, none for a single slab
+    assert uq.uniquan_bcq_matmul_ws(1, 4096, 4096) == 32 * 4096
+    assert uq.uniquan_bcq_matmul_ws(2, 28672, 8192) == 16 * 2 * 28672
+    assert uq.uniquan_bcq_matmul_ws(1, 100, 128) == 0
+
+
 def test_error_text_is_thread_local(L):
     import threading
     fwd(L, k=0)
