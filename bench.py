@@ -188,6 +188,53 @@ def _cpu_baseline(layers_np, mode, budget_s):
                       f"numpy on one thread: {sample}; {total_w} weights in {total_t:.2f} s"}
 
 
+def bcq_inference(layers, batches=(1, 8), target_bytes=512 << 20):
+    """The deployed layer after the timed steps: fold (Theorem 1) -> stored
+    form -> Y = X What^T for a batch of T activation rows.  Copies of the
+    stored form are rotated so that the bytes touched between two reads of one
+    copy exceed the 256 MB last-level cache (cold-cache decode, as one token's
+    pass over a model reads each layer once)."""
+    import torch
+
+    from paper_2506_03781_amd import uniquan as uq
+    res = []
+    for lay in layers:
+        R, C, k, g = lay.R, lay.C, lay.k, lay.g
+        if C % 128 or g % 128 or k > 4:
+            continue
+        a, z, c = lay.fold()
+        Gn = R * C // g
+        per_copy = R * C * k // 8 + 2 * (k + 1) * Gn
+        n_copy = int(min(64, max(2, -(-target_bytes // per_copy))))
+        copies = []
+        for _ in range(n_copy):
+            st = (torch.empty(R * C * k // 32, dtype=torch.int32, device="cuda"),
+                  torch.empty(Gn * k, dtype=torch.float16, device="cuda"),
+                  torch.empty(Gn, dtype=torch.float16, device="cuda"))
+            uq.uniquan_bcq_pack(R, C, k, g, c, a, z, *st)
+            copies.append(st)
+        for T in batches:
+            X = lay.X[:T].contiguous()
+            Y = torch.empty(T, R, device="cuda")
+            ws = torch.empty(max(1, uq.uniquan_bcq_matmul_ws(T, R, C)), device="cuda")
+            for i in range(3):
+                uq.uniquan_bcq_matmul(T, R, C, k, g, X, *copies[i % n_copy], Y, ws)
+            n_it = max(20, 2 * n_copy)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for i in range(n_it):
+                uq.uniquan_bcq_matmul(T, R, C, k, g, X, *copies[i % n_copy], Y, ws)
+            e1.record()
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) / n_it * 1e3
+            byt = per_copy + 2 * T * C + 4 * T * R
+            gbs = byt / (us * 1e-6) / 1e9
+            res.append({"R": R, "C": C, "k": k, "g": g, "T": T, "us_per_call": us, "algorithmic_bytes": byt,
+                        "achieved_gbs": gbs, "frac_hbm": gbs / HBM_PEAK_GBS, "copies_rotated": n_copy})
+        del copies
+    return res
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -367,6 +414,8 @@ def main():
                  "note": "fq_fwd -> loss GEMM -> weight-gradient GEMM with the straight-through backward "
                          "and SGD update in its epilogue (dL/dWhat never written)"}
 
+    bcq = bcq_inference(layers)
+
     out = {
         "metric": "fake-quant fwd+bwd Gweights/s (%HBM peak); recon GEMM TFLOP/s (%MFMA)",
         "value": value,
@@ -394,6 +443,9 @@ def main():
         "fq_fwd_us_by_mode": by_mode,
         "roofline": roof,
         "fused_bwd_step": fused,
+        "bcq_inference": {"per_call": bcq,
+                          "note": "deployed layer (fold -> bit-planes + binary16 Theta*_B): Y = X What^T for T "
+                                  "activation rows; bytes = planes + parameters + X + Y"},
         "counters_src_hash": src_hash(),
         "precision": "quantizer: fp32 arithmetic on bf16 W / fp32 s, bf16 What and dL/dWhat; "
                      "GEMMs: bf16 MFMA with fp32 accumulation",

@@ -100,88 +100,152 @@ struct BcqArgs {
   int g, qps;
 };
 
+// One v_bfe_u32 (the compiler otherwise splits a field extract of a masked
+// word into a shift and an and).
+template <int OFF>
+__device__ __forceinline__ uint32_t byte_field(uint32_t w) {
+  uint32_t r;
+  asm volatile("v_bfe_u32 %0, %1, %2, 8" : "=v"(r) : "v"(w), "i"(OFF));
+  return r;
+}
+
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float(uint32_t(h) << 16); }
 __device__ __forceinline__ float f16_to_f32(uint16_t h) { return float(__builtin_bit_cast(_Float16, h)); }
 
 // Workgroup (bx, by): rows 256 bx .. 256 bx + 255 (one per lane), column
-// quads qps by .. qps by + qps - 1.  LDS: T tables of qps * 32 nibbles x 16
-// subset sums, then the T x qps quad sums.
-template <int K, int T>
+// quads QPS by .. QPS by + QPS - 1.  LDS: T tables of QPS * 32 nibbles x 16
+// subset sums, then the T x QPS quad sums (activation sums S of the quads).
+template <int K, int T, int QPS>
 __global__ __launch_bounds__(256) void bcq_matmul_kernel(BcqArgs a) {
-  extern __shared__ float lut[];
+  constexpr int PER_T = QPS * 512;  // floats per batch row's tables
+  __shared__ __attribute__((aligned(16))) float lut[T * PER_T + T * QPS];
   const int tid = threadIdx.x;
-  const int qps = a.qps;
-  const int64_t q0 = int64_t(blockIdx.y) * qps;
-  const int nqs = int(min<int64_t>(qps, a.nq - q0));
-  const int per_t = qps * 512;  // floats per batch row's tables
-  float* S = lut + T * per_t;
-
-  // tables: entry v of nibble n is the sum, in ascending bit order, of the
-  // activations of columns 4 n + b of the slab with bit b of v set
-  const int per_t_used = nqs * 512;
-  for (int e = tid; e < T * per_t_used; e += 256) {
-    const int t = e / per_t_used, rem = e - t * per_t_used;
-    const int n = rem >> 4, v = rem & 15;
-    const uint2 xv = *reinterpret_cast<const uint2*>(a.X + int64_t(t) * a.C + q0 * 128 + 4 * n);
-    const float x[4] = {bf16_to_f32(uint16_t(xv.x)), bf16_to_f32(uint16_t(xv.x >> 16)),
-                        bf16_to_f32(uint16_t(xv.y)), bf16_to_f32(uint16_t(xv.y >> 16))};
-    float s = 0.0f;
-#pragma unroll
-    for (int b = 0; b < 4; ++b)
-      if ((v >> b) & 1) s += x[b];
-    lut[t * per_t + rem] = s;
-  }
-  __syncthreads();
-  // quad sums: the 32 nibble totals (entry 15) of the quad, ascending
-  for (int e = tid; e < T * nqs; e += 256) {
-    const int t = e / nqs, qq = e - t * nqs;
-    float s = 0.0f;
-    for (int n = 0; n < 32; ++n) s += lut[t * per_t + (qq * 32 + n) * 16 + 15];
-    S[t * qps + qq] = s;
-  }
-  __syncthreads();
-
+  const int64_t q0 = int64_t(blockIdx.y) * QPS;
+  const int nqs = int(min<int64_t>(QPS, a.nq - q0));
+  float* S = lut + T * PER_T;
   const int64_t r = int64_t(blockIdx.x) * 256 + tid;
-  if (r >= a.R) return;  // no barrier follows
+  const bool live = r < a.R;
+
+  // The activations this thread turns into tables (nibble tables e = tid +
+  // 256 u of the T x nqs x 32 in the slab) are loaded first, then this lane's
+  // plane words and parameters for the whole slab: loads complete in issue
+  // order, so the table build waits only for the activations while the
+  // plane loads stay in flight.
+  constexpr int NT = (T * QPS * 32 + 255) / 256;  // nibble tables per thread (upper bound)
+  constexpr int LOG_FULL = QPS == 4 ? 7 : QPS == 2 ? 6 : 5;  // log2(QPS * 32)
+  const bool full = nqs == QPS;
+  const int n_tab = T * nqs * 32;
+  const uint16_t* xs = a.X + q0 * 128;
+  uint2 xv[NT];
+  // loads are unconditional (indices clamped into range) so that no branch
+  // splits the load sequence; clamped values are never used
+#pragma unroll
+  for (int u = 0; u < NT; ++u) {
+    const int e = min(tid + 256 * u, n_tab - 1);
+    const int t = full ? (e >> LOG_FULL) : e / (nqs * 32);
+    const int n = e - t * (nqs * 32);
+    xv[u] = *reinterpret_cast<const uint2*>(xs + int64_t(t) * a.C + 4 * n);
+  }
+  asm volatile("" ::: "memory");  // keep the activation loads ahead of the plane loads
+  // plane i of quad q for row r at planes[(i nq + q) R + r]; parameters of
+  // group column j at [(i gpr + j) R + r]; quad q lies in group q / qpg
+  const int64_t R = a.R;
+  const int64_t pstride = a.nq * R, astride = a.gpr * R;
+  const int64_t rc = live ? r : R - 1;
+  const u32x4* pp = a.planes + q0 * R + rc;
+  const uint32_t qpg = uint32_t(a.g) >> 7;
+  const uint32_t j0 = uint32_t(q0) / qpg, rem0 = uint32_t(q0) - j0 * qpg;
+  u32x4 pw[QPS][K];
+  float al[QPS][K], zz[QPS];
+#pragma unroll
+  for (int qq = 0; qq < QPS; ++qq) {
+    const int qc = min(qq, nqs - 1);
+    const int64_t j = int64_t(j0 + (rem0 + uint32_t(qc)) / qpg);
+    const uint16_t* ap = a.alpha16 + j * R + rc;
+#pragma unroll
+    for (int i = 0; i < K; ++i) {
+      pw[qq][i] = pp[qc * R + i * pstride];
+      al[qq][i] = f16_to_f32(ap[i * astride]);
+    }
+    zz[qq] = f16_to_f32(a.z16[j * R + rc]);
+  }
+
+  // table of nibble n: entry v is the sum of the activations of columns
+  // 4 n + b with bit b of v set, in ascending bit order (built by doubling:
+  // entries 2^b .. 2^(b+1) - 1 are entries 0 .. 2^b - 1 plus x_b)
+#pragma unroll
+  for (int u = 0; u < NT; ++u) {
+    // threads past the last table repeat it (identical values, same place)
+    const int e = min(tid + 256 * u, n_tab - 1);
+    {
+      const int t = full ? (e >> LOG_FULL) : e / (nqs * 32);
+      const int n = e - t * (nqs * 32);
+      const float x0 = bf16_to_f32(uint16_t(xv[u].x)), x1 = bf16_to_f32(uint16_t(xv[u].x >> 16));
+      const float x2 = bf16_to_f32(uint16_t(xv[u].y)), x3 = bf16_to_f32(uint16_t(xv[u].y >> 16));
+      float L[16];
+      L[0] = 0.0f;
+      L[1] = x0;
+      L[2] = x1;
+      L[3] = x0 + x1;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) L[4 + v] = L[v] + x2;
+#pragma unroll
+      for (int v = 0; v < 8; ++v) L[8 + v] = L[v] + x3;
+      float4* dst = reinterpret_cast<float4*>(lut + t * PER_T + n * 16);
+#pragma unroll
+      for (int v = 0; v < 4; ++v) dst[v] = make_float4(L[4 * v], L[4 * v + 1], L[4 * v + 2], L[4 * v + 3]);
+      // quad sum: the 32 nibble totals of a quad sit in 32 adjacent lanes
+      // (tables are numbered quad-major and 256 u is a multiple of 32);
+      // fixed xor-butterfly, written by the quad's first lane
+      float tot = L[15];
+#pragma unroll
+      for (int msk = 16; msk >= 1; msk >>= 1) tot += __shfl_xor(tot, msk, 64);
+      if ((tid & 31) == 0 && tid + 256 * u < n_tab) S[t * QPS + (n >> 5)] = tot;
+    }
+  }
+  __syncthreads();
+  if (!live) return;  // no barrier follows
+
+  const char* lb = reinterpret_cast<const char*>(lut);
   float acc[T];
 #pragma unroll
   for (int t = 0; t < T; ++t) acc[t] = 0.0f;
-  for (int qq = 0; qq < nqs; ++qq) {
-    const int64_t q = q0 + qq;
-    const int64_t j = (q * 128) / a.g;  // group column of this quad
-    u32x4 pw[K];
-    float al[K];
 #pragma unroll
-    for (int i = 0; i < K; ++i) {
-      pw[i] = a.planes[(int64_t(i) * a.nq + q) * a.R + r];
-      al[i] = f16_to_f32(a.alpha16[(int64_t(i) * a.gpr + j) * a.R + r]);
-    }
-    const float z = f16_to_f32(a.z16[j * a.R + r]);
+  for (int qq = 0; qq < QPS; ++qq) {
+    if (qq >= nqs) break;
     float asum = 0.0f;
 #pragma unroll
-    for (int i = 0; i < K; ++i) asum += al[i];
-    const float* base = lut + qq * 512;
+    for (int i = 0; i < K; ++i) asum += al[qq][i];
 #pragma unroll
     for (int i = 0; i < K; ++i) {
       float P[T];
 #pragma unroll
       for (int t = 0; t < T; ++t) P[t] = 0.0f;
-      const uint32_t wv[4] = {pw[i].x, pw[i].y, pw[i].z, pw[i].w};
 #pragma unroll
-      for (int m = 0; m < 4; ++m)
+      for (int m = 0; m < 4; ++m) {
+        // byte offsets of the table entries: the even nibbles of the word
+        // shifted to bits 8 n + 2 .. 8 n + 5, the odd ones likewise, so one
+        // field extract gives 4 v for each nibble
+        const uint32_t ev = (pw[qq][i][m] << 2) & 0x3C3C3C3Cu;
+        const uint32_t od = (pw[qq][i][m] >> 2) & 0x3C3C3C3Cu;
+        const uint32_t boff[8] = {byte_field<0>(ev), byte_field<0>(od), byte_field<8>(ev), byte_field<8>(od),
+                                  byte_field<16>(ev), byte_field<16>(od), byte_field<24>(ev),
+                                  byte_field<24>(od)};
 #pragma unroll
         for (int nib = 0; nib < 8; ++nib) {
-          const int v = int((wv[m] >> (4 * nib)) & 15u);
+          const int row0 = ((qq * 32 + m * 8 + nib) * 16) * 4;  // byte offset of the nibble's table
 #pragma unroll
-          for (int t = 0; t < T; ++t) P[t] += base[t * per_t + (m * 8 + nib) * 16 + v];
+          for (int t = 0; t < T; ++t)
+            P[t] += *reinterpret_cast<const float*>(lb + boff[nib] + (row0 + t * PER_T * 4));
         }
-      const float a2 = 2.0f * al[i];
+      }
+      const float a2 = 2.0f * al[qq][i];
 #pragma unroll
       for (int t = 0; t < T; ++t) acc[t] += a2 * P[t];
     }
-    const float zc = z - asum;
+    const float zc = zz[qq] - asum;
 #pragma unroll
-    for (int t = 0; t < T; ++t) acc[t] += zc * S[t * qps + qq];
+    for (int t = 0; t < T; ++t) acc[t] += zc * S[t * QPS + qq];
   }
   float* out = a.out + int64_t(blockIdx.y) * T * a.R;
 #pragma unroll
@@ -193,8 +257,17 @@ __global__ __launch_bounds__(256) void bcq_reduce_kernel(const float* __restrict
                                                          int64_t n, int slabs) {
   const int64_t idx = int64_t(blockIdx.x) * 256 + threadIdx.x;
   if (idx >= n) return;
+  // up to 32 independent loads in flight (one memory round trip for most
+  // shapes), added in slab order
   float s = 0.0f;
-  for (int b = 0; b < slabs; ++b) s += part[int64_t(b) * n + idx];
+  for (int b0 = 0; b0 < slabs; b0 += 32) {
+    float v[32];
+#pragma unroll
+    for (int j = 0; j < 32; ++j) v[j] = b0 + j < slabs ? part[int64_t(b0 + j) * n + idx] : 0.0f;
+#pragma unroll
+    for (int j = 0; j < 32; ++j)
+      if (b0 + j < slabs) s += v[j];
+  }
   Y[idx] = s;
 }
 
@@ -211,25 +284,29 @@ int64_t bcq_slabs(int64_t R, int64_t C) {
   return (C / 128 + qps - 1) / qps;
 }
 
+template <int K, int T, int QPS>
+static void launch_mm(const BcqArgs& a, dim3 grid, hipStream_t st) {
+  hipLaunchKernelGGL((bcq_matmul_kernel<K, T, QPS>), grid, dim3(256), 0, st, a);
+}
+
 template <int K, int T>
-static void launch_mm(const BcqArgs& a, dim3 grid, size_t lds, hipStream_t st) {
-  if (lds > 65536)
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(bcq_matmul_kernel<K, T>),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
-  hipLaunchKernelGGL((bcq_matmul_kernel<K, T>), grid, dim3(256), lds, st, a);
+static void launch_mm_q(const BcqArgs& a, dim3 grid, hipStream_t st) {
+  if (a.qps == 4) launch_mm<K, T, 4>(a, grid, st);
+  else if (a.qps == 2) launch_mm<K, T, 2>(a, grid, st);
+  else launch_mm<K, T, 1>(a, grid, st);
 }
 
 template <int K>
-static void launch_mm_t(const BcqArgs& a, int T, dim3 grid, size_t lds, hipStream_t st) {
+static void launch_mm_t(const BcqArgs& a, int T, dim3 grid, hipStream_t st) {
   switch (T) {
-    case 1: launch_mm<K, 1>(a, grid, lds, st); break;
-    case 2: launch_mm<K, 2>(a, grid, lds, st); break;
-    case 3: launch_mm<K, 3>(a, grid, lds, st); break;
-    case 4: launch_mm<K, 4>(a, grid, lds, st); break;
-    case 5: launch_mm<K, 5>(a, grid, lds, st); break;
-    case 6: launch_mm<K, 6>(a, grid, lds, st); break;
-    case 7: launch_mm<K, 7>(a, grid, lds, st); break;
-    default: launch_mm<K, 8>(a, grid, lds, st); break;
+    case 1: launch_mm_q<K, 1>(a, grid, st); break;
+    case 2: launch_mm_q<K, 2>(a, grid, st); break;
+    case 3: launch_mm_q<K, 3>(a, grid, st); break;
+    case 4: launch_mm_q<K, 4>(a, grid, st); break;
+    case 5: launch_mm_q<K, 5>(a, grid, st); break;
+    case 6: launch_mm_q<K, 6>(a, grid, st); break;
+    case 7: launch_mm_q<K, 7>(a, grid, st); break;
+    default: launch_mm_q<K, 8>(a, grid, st); break;
   }
 }
 
@@ -248,12 +325,11 @@ hipError_t launch_bcq_matmul(const BcqMatmulLaunch& p, hipStream_t st) {
   const int64_t slabs = (a.nq + a.qps - 1) / a.qps;
   a.out = slabs == 1 ? p.Y : p.partials;
   const dim3 grid(unsigned((p.R + 255) / 256), unsigned(slabs));
-  const size_t lds = (size_t(p.T) * a.qps * 512 + size_t(p.T) * a.qps) * sizeof(float);
   switch (p.k) {
-    case 1: launch_mm_t<1>(a, p.T, grid, lds, st); break;
-    case 2: launch_mm_t<2>(a, p.T, grid, lds, st); break;
-    case 3: launch_mm_t<3>(a, p.T, grid, lds, st); break;
-    default: launch_mm_t<4>(a, p.T, grid, lds, st); break;
+    case 1: launch_mm_t<1>(a, p.T, grid, st); break;
+    case 2: launch_mm_t<2>(a, p.T, grid, st); break;
+    case 3: launch_mm_t<3>(a, p.T, grid, st); break;
+    default: launch_mm_t<4>(a, p.T, grid, st); break;
   }
   if (slabs > 1) {
     const int64_t n = int64_t(p.T) * p.R;
