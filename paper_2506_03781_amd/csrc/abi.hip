@@ -57,6 +57,8 @@ uq_status check_gemm_dims(const char* fn, int64_t T, int64_t R, int64_t C) {
   if (T < 1 || R < 1 || C < 1) return fail(UQ_EINVAL, "%s: T, R, C must be >= 1", fn);
   if (T % 8 != 0) return fail(UQ_EINVAL, "%s: T=%lld must be a multiple of 8", fn, (long long)T);
   if (C % 8 != 0) return fail(UQ_EINVAL, "%s: C=%lld must be a multiple of 8", fn, (long long)C);
+  if (T >= (int64_t(1) << 26) || C >= (int64_t(1) << 26))
+    return fail(UQ_EUNSUPPORTED, "%s: T and C must be < 2^26", fn);
   const int64_t lim = int64_t(1) << 31;
   if (T >= lim || R >= lim || C >= lim || T * C >= (int64_t(1) << 40) || R * C >= (int64_t(1) << 40) ||
       R * T >= (int64_t(1) << 40))

@@ -226,28 +226,33 @@ __device__ __forceinline__ void epilogue(const GemmArgs& p, f32x16 (&acc)[FM][FN
       __builtin_amdgcn_wave_barrier();
       continue;
     }
+    // the strip's first element once in 64 bits; element offsets in 32 bits
+    // (N < 2^26 is checked on the host)
+    const int64_t base = row_base * p.N + col_base;
+    const int ldn = int(p.N);
     float4 y[ITER];
-    if constexpr (EPI == EPI_LOSS) {
-      // no target: the A operand already holds the residual What - W
+    if constexpr (EPI == EPI_LOSS) {  // stored target
 #pragma unroll
       for (int it = 0; it < ITER; ++it) {
-        const int idx = lane + it * 64;
-        const int64_t row = row_base + idx / Q, col = col_base + (idx % Q) * 4;
-        const bool ok = Yt != nullptr && (full || (row < p.M && col < p.N));  // N % 4 == 0 here
-        y[it] = ok ? *reinterpret_cast<const float4*>(Yt + row * p.N + col) : make_float4(0, 0, 0, 0);
+        const int idx = lane + it * 64, rr = idx / Q, cc = (idx % Q) * 4;
+        const bool ok = full || (row_base + rr < p.M && col_base + cc < p.N);  // N % 4 == 0 here
+        y[it] = ok ? *reinterpret_cast<const float4*>(Yt + base + rr * ldn + cc) : make_float4(0, 0, 0, 0);
       }
     }
-#pragma unroll
-    for (int it = 0; it < ITER; ++it) {
-      const int idx = lane + it * 64;
-      const int64_t row = row_base + idx / Q, col = col_base + (idx % Q) * 4;
-      const float4 v = *reinterpret_cast<const float4*>(&strip[(idx / Q) * WN + (idx % Q) * 4]);
-      if (!(full || (row < p.M && col < p.N))) continue;
-      const int64_t o = row * p.N + col;
+    auto put = [&](int it) {
+      const int idx = lane + it * 64, rr = idx / Q, cc = (idx % Q) * 4;
+      const float4 v = *reinterpret_cast<const float4*>(&strip[rr * WN + cc]);
+      const int64_t o = base + rr * ldn + cc;
       if constexpr (EPI == EPI_TARGET) {
         *reinterpret_cast<float4*>(static_cast<float*>(p.out) + o) = v;
-      } else if constexpr (EPI == EPI_LOSS) {
-        const float e0 = v.x - y[it].x, e1 = v.y - y[it].y, e2 = v.z - y[it].z, e3 = v.w - y[it].w;
+      } else if constexpr (EPI == EPI_LOSS || EPI == EPI_LOSS_RES) {
+        float e0 = v.x, e1 = v.y, e2 = v.z, e3 = v.w;
+        if constexpr (EPI == EPI_LOSS) {
+          e0 = v.x - y[it].x;
+          e1 = v.y - y[it].y;
+          e2 = v.z - y[it].z;
+          e3 = v.w - y[it].w;
+        }
         lsum += e0 * e0;
         lsum += e1 * e1;
         lsum += e2 * e2;
@@ -261,11 +266,21 @@ __device__ __forceinline__ void epilogue(const GemmArgs& p, f32x16 (&acc)[FM][FN
         *reinterpret_cast<float4*>(static_cast<float*>(p.out) + o) =
             make_float4(p.scale * v.x, p.scale * v.y, p.scale * v.z, p.scale * v.w);
       }
+    };
+    if (full) {  // uniform: interior tiles store without per-element checks
+#pragma unroll
+      for (int it = 0; it < ITER; ++it) put(it);
+    } else {
+#pragma unroll
+      for (int it = 0; it < ITER; ++it) {
+        const int idx = lane + it * 64;
+        if (row_base + idx / Q < p.M && col_base + (idx % Q) * 4 < p.N) put(it);
+      }
     }
     __builtin_amdgcn_s_waitcnt(0xC07F);  // strip reads done before the next strip overwrites it
     __builtin_amdgcn_wave_barrier();
   }
-  if constexpr (EPI == EPI_LOSS) {
+  if constexpr (EPI == EPI_LOSS || EPI == EPI_LOSS_RES) {
     __shared__ float sred[4];
     for (int msk = 32; msk >= 1; msk >>= 1) lsum += __shfl_xor(lsum, msk, 64);
     if (lane == 0) sred[wave] = lsum;
@@ -588,7 +603,10 @@ static hipError_t launch_bm(const GemmLaunch& q, hipStream_t st) {
   const dim3 grid(unsigned(a.tiles_m * a.tiles_n));
   switch (q.epi) {
     case EPI_TARGET: launch_epi<BM, BN, EPI_TARGET>(a, grid, st); break;
-    case EPI_LOSS: launch_epi<BM, BN, EPI_LOSS>(a, grid, st); break;
+    case EPI_LOSS:
+      if (a.Yt != nullptr) launch_epi<BM, BN, EPI_LOSS>(a, grid, st);
+      else launch_epi<BM, BN, EPI_LOSS_RES>(a, grid, st);
+      break;
     case EPI_GRAD_BF16: launch_epi<BM, BN, EPI_GRAD_BF16>(a, grid, st); break;
     default: launch_epi<BM, BN, EPI_GRAD_F32>(a, grid, st); break;
   }
@@ -622,19 +640,17 @@ hipError_t launch_gemm(const GemmLaunch& q, hipStream_t st) {
   }
 }
 
-// Deterministic loss: fixed strided fp64 partial sums, then a fixed tree.
+// Deterministic loss: fixed strided fp64 partial sums, a fixed xor butterfly
+// within each wavefront, then the four wavefront totals in order.
 __global__ __launch_bounds__(256) void reduce_loss_kernel(const float* __restrict__ partials, int64_t n,
                                                           float* __restrict__ loss) {
-  __shared__ double sm[256];
+  __shared__ double sm[4];
   double acc = 0.0;
   for (int64_t i = threadIdx.x; i < n; i += 256) acc += double(partials[i]);
-  sm[threadIdx.x] = acc;
+  for (int msk = 32; msk >= 1; msk >>= 1) acc += __shfl_xor(acc, msk, 64);
+  if ((threadIdx.x & 63) == 0) sm[threadIdx.x >> 6] = acc;
   __syncthreads();
-  for (int w = 128; w >= 1; w >>= 1) {
-    if (threadIdx.x < w) sm[threadIdx.x] += sm[threadIdx.x + w];
-    __syncthreads();
-  }
-  if (threadIdx.x == 0) loss[0] = float(sm[0]);
+  if (threadIdx.x == 0) loss[0] = float((sm[0] + sm[1]) + (sm[2] + sm[3]));
 }
 
 hipError_t launch_reduce_loss(const float* partials, int64_t n, float* loss, hipStream_t st) {

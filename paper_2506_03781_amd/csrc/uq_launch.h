@@ -85,6 +85,7 @@ enum GemmEpi : int {
   EPI_GRAD_BF16 = 2,  // out bf16 = scale * acc
   EPI_STE = 16,       // EPI_STE + k: scale * acc is dL/dWhat; straight-through backward + SGD in place
   EPI_GRAD_F32 = 3,   // out fp32 = scale * acc
+  EPI_LOSS_RES = 4,   // EPI_LOSS without a target (A holds What - W); chosen when Yt is NULL
 };
 
 struct GemmLaunch {
