@@ -53,10 +53,13 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 // Map a linear workgroup id to (tile_m, tile_n).  Hardware dispatches
 // workgroup i to XCD i % 8; renumber so that each XCD receives a contiguous
 // run of logical tiles, then walk logical tiles in groups of GM row-tiles.
+// An XCD's run of tiles then covers GM row-tiles and (run / GM) column-tiles,
+// whose operand panels it pulls into its L2: GM balances the two panel sizes
+// (BM and BN rows of K), 4 for 256 x 128 tiles, 8 otherwise.
+template <int GM>
 __device__ __forceinline__ void tile_of(int bid, int nb, int tiles_m, int tiles_n, int& tm, int& tn) {
   int logical = bid;
   if ((nb & 7) == 0) logical = (bid & 7) * (nb >> 3) + (bid >> 3);
-  constexpr int GM = 8;
   const int per_group = GM * tiles_n;
   const int group = logical / per_group;
   const int first_m = group * GM;
@@ -307,7 +310,7 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs p) {
   const int wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   int tm, tn;
-  tile_of(blockIdx.x, gridDim.x, p.tiles_m, p.tiles_n, tm, tn);
+  tile_of<(BM == 256 && BN == 128) ? 4 : 8>(blockIdx.x, gridDim.x, p.tiles_m, p.tiles_n, tm, tn);
   const int64_t m0 = int64_t(tm) * BM, n0 = int64_t(tn) * BN;
   const int64_t K = p.K;
 
@@ -449,7 +452,7 @@ __global__ __launch_bounds__(256) void gemm_pipe_kernel(GemmArgs p) {
   const int wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   int tm, tn;
-  tile_of(blockIdx.x, gridDim.x, p.tiles_m, p.tiles_n, tm, tn);
+  tile_of<(BM == 256 && BN == 128) ? 4 : 8>(blockIdx.x, gridDim.x, p.tiles_m, p.tiles_n, tm, tn);
   const int64_t m0 = int64_t(tm) * BM, n0 = int64_t(tn) * BN;
   const int64_t K = p.K;
 
