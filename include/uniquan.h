@@ -332,8 +332,8 @@ uq_status uniquan_bcq_dequant(int64_t R, int64_t C, int k, int g,
  *           (1 <=> c_{i+1} = +1);
  *   alpha16 IEEE binary16 [k][C/g][R]: alpha*_{i+1} of group (r, j);
  *   z16     IEEE binary16 [C/g][R]:    z*_B of group (r, j).
- * Shape rules: 1 <= k <= 4, C % 128 == 0, g % 128 == 0, C % g == 0
- * (UQ_EUNSUPPORTED otherwise).
+ * Shape rules: 1 <= k <= 4, C % 128 == 0, C <= 2^22, g % 128 == 0,
+ * C % g == 0 (UQ_EUNSUPPORTED otherwise; UQ_EINVAL if g does not divide C).
  */
 
 /*

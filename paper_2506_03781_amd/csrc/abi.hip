@@ -284,6 +284,8 @@ static uq_status check_bcq_shape(const char* fn, int64_t R, int64_t C, int k, in
   if (R < 1 || C < 1) return fail(UQ_EINVAL, "%s: R=%lld and C=%lld must be >= 1", fn, (long long)R, (long long)C);
   if (k < 1 || k > 4) return fail(UQ_EUNSUPPORTED, "%s: k=%d, supported 1..4", fn, k);
   if (C % 128 != 0) return fail(UQ_EUNSUPPORTED, "%s: C=%lld must be a multiple of 128", fn, (long long)C);
+  // column slabs form the grid's second dimension (at most 65535)
+  if (C > (int64_t(1) << 22)) return fail(UQ_EUNSUPPORTED, "%s: C=%lld > 2^22 is not supported", fn, (long long)C);
   if (g < 128 || g % 128 != 0) return fail(UQ_EUNSUPPORTED, "%s: g=%d must be a multiple of 128", fn, g);
   if (C % g != 0) return fail(UQ_EINVAL, "%s: g=%d must divide C=%lld", fn, g, (long long)C);
   if (R >= (int64_t(1) << 31) || R > (int64_t(1) << 40) / C)

@@ -148,6 +148,7 @@ def bcq_mm(L, T=1, R=256, C=512, k=3, g=128, X=FAKE, planes=FAKE, a16=FAKE, z16=
 @pytest.mark.parametrize("kw,status,text", [
     (dict(k=5), uq.UQ_EUNSUPPORTED, "k=5"),
     (dict(C=320), uq.UQ_EUNSUPPORTED, "multiple of 128"),
+    (dict(C=(1 << 22) + 128, R=2), uq.UQ_EUNSUPPORTED, "2^22"),
     (dict(g=64), uq.UQ_EUNSUPPORTED, "g=64"),
     (dict(g=384), uq.UQ_EINVAL, "divide"),
     (dict(T=9), uq.UQ_EUNSUPPORTED, "T=9"),
