@@ -66,6 +66,8 @@ def parse():
     ap.add_argument("--init-clip", type=int, default=0, help="0 fixed min, 1 fixed max, 2 balanced")
     ap.add_argument("--target", action="store_true",
                     help="loss against a stored fp32 target Y = X W^T instead of the residual form")
+    ap.add_argument("--no-block", action="store_true",
+                    help="skip the block-level step on the 7B MLP module (gate/up/down 11008x4096, 4096 tokens)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run a plain 256 MiB device copy (counter calibration)")
     return ap.parse_args()
@@ -233,6 +235,84 @@ def bcq_inference(layers, batches=(1, 8), target_bytes=512 << 20):
                         "achieved_gbs": gbs, "frac_hbm": gbs / HBM_PEAK_GBS, "copies_rotated": n_copy})
         del copies
     return res
+
+
+def block_mlp(seed, k=3, steps=10, warmup=2):
+    """Block-level reconstruction of a 7B MLP module (Algorithm 1 with the
+    SiLU-gated gate/up/down as f): per step the three fake-quant forwards,
+    the module's forward on What, the loss, backpropagation to all three
+    matrices and the straight-through backward with the SGD update.  Seven
+    GEMMs of 2 T C I flops each carry the step."""
+    import torch
+
+    from paper_2506_03781_amd import synth
+    from paper_2506_03781_amd import uniquan as uq
+    from paper_2506_03781_amd.block import MLPBlock, QuantMatrix
+    wl = synth.WORKLOADS["mlp7b"]
+    g = wl.group_size
+    qs, X = [], None
+    for spec in wl.matrices:
+        m = synth.make_matrix(spec, seed)
+        if X is None:
+            X = m.X
+        q = QuantMatrix(m.W, m.s, k, g)
+        q.init_unified()
+        qs.append(q)
+        del m
+    blk = MLPBlock(X, *qs)
+    blk.prepare()
+    T, C, I = blk.T, blk.C, blk.I
+    # SGD on L / L0, the loss relative to its value at the initialisation (one
+    # step with zero learning rates measures L0): the sum's gradients grow
+    # with the block's size and output scale, the relative loss's do not
+    blk.step(uq.MAP_FULL, 0.0, 0.0)
+    l0 = float(blk.loss.item())
+    lr_f, lr_b = 0.005 / l0, 0.0005 / l0
+    rel = []
+    for i in range(warmup):
+        blk.step(uq.MAP_FULL if i == 0 else uq.MAP_LOCAL, lr_f, lr_b)
+        rel.append(float(blk.loss.item()) / l0)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        blk.step(uq.MAP_LOCAL, lr_f, lr_b)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    # one instrumented step for the split between phases
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+    ev[0].record()
+    for q in qs:
+        q.fq_fwd(uq.MAP_LOCAL)
+    ev[1].record()
+    blk._forward_h(qs[0].W_hat, qs[1].W_hat)
+    uq.uniquan_layer_recon(T, C, I, blk.H, blk.Ht, qs[2].W_hat, blk.Yt_ref, blk.loss, blk.Et, blk.partials, qs[2].G)
+    ev[2].record()
+    uq.uniquan_transpose_bf16(C, T, blk.Et, blk.E)
+    uq.uniquan_transpose_bf16(C, I, qs[2].W_hat, blk.WdT)
+    uq.uniquan_gemm_nt(I, T, C, blk.WdT, blk.E, blk.dHt, 2.0)
+    uq.uniquan_silu_mul_bwd(blk.dHt, blk.Gt, blk.Ut, blk.dGt, blk.dUt)
+    uq.uniquan_gemm_nt(I, C, T, blk.dGt, blk.Xt, qs[0].G)
+    uq.uniquan_gemm_nt(I, C, T, blk.dUt, blk.Xt, qs[1].G)
+    ev[3].record()
+    for q in qs:
+        q.fq_bwd_sgd(lr_f, lr_b)
+    ev[4].record()
+    torch.cuda.synchronize()
+    phases = dict(zip(("fq_fwd", "forward_loss_dWd", "backprop_dWg_dWu", "ste_sgd"),
+                      (ev[i].elapsed_time(ev[i + 1]) for i in range(4))))
+    flops = 7 * 2.0 * T * C * I
+    tf = flops / (ms * 1e-3) / 1e12
+    n_w = 3 * C * I
+    return {"T": T, "C": C, "I": I, "k": k, "g": g, "steps": steps, "ms_per_step": ms,
+            "gweights_per_s": n_w / (ms * 1e-3) / 1e9, "gemm_flops_per_step": flops,
+            "tflops_effective": tf, "frac_mfma": tf / MFMA_BF16_PEAK_TFLOPS, "phase_ms": phases,
+            "loss_init": l0, "rel_loss_warmup": rel, "rel_loss_last": float(blk.loss.item()) / l0,
+            "optimiser": "SGD on L / L_init (learning rates 0.005 / 0.0005 divided by the initial loss)",
+            "note": "whole step over the three matrices (fake-quant fwd, module forward on What, loss, "
+                    "backpropagation, straight-through backward + SGD); flops count the seven GEMMs only"}
+
 
 
 def main():
@@ -415,6 +495,7 @@ def main():
                          "and SGD update in its epilogue (dL/dWhat never written)"}
 
     bcq = bcq_inference(layers)
+    blk = None if args.no_block else block_mlp(args.seed)
 
     out = {
         "metric": "fake-quant fwd+bwd Gweights/s (%HBM peak); recon GEMM TFLOP/s (%MFMA)",
@@ -446,6 +527,7 @@ def main():
         "bcq_inference": {"per_call": bcq,
                           "note": "deployed layer (fold -> bit-planes + binary16 Theta*_B): Y = X What^T for T "
                                   "activation rows; bytes = planes + parameters + X + Y"},
+        "block_mlp": blk,
         "counters_src_hash": src_hash(),
         "precision": "quantizer: fp32 arithmetic on bf16 W / fp32 s, bf16 What and dL/dWhat; "
                      "GEMMs: bf16 MFMA with fp32 accumulation",

@@ -322,6 +322,42 @@ uq_status uniquan_bcq_dequant(int64_t R, int64_t C, int k, int g,
                               void* stream);
 
 /*
+ * Block-level reconstruction of a Transformer block's MLP module
+ * (Algorithm 1 with f = the SiLU-gated MLP G = X W_g^T, U = X W_u^T,
+ * H = silu(G) * U, Y = H W_d^T; the loss is ||Y(X; W) - Y(X; What)||_F^2).
+ * The block step is composed from uniquan_fq_fwd / uniquan_fq_bwd_sgd per
+ * matrix, uniquan_layer_target / uniquan_layer_recon for the output and
+ * the down matrix's gradient, uniquan_transpose_bf16, and the three calls
+ * below.
+ */
+
+/*
+ * uniquan_gemm_nt -- out[M x N] = scale * A[M x K] B[N x K]^T, bf16 operands
+ * with K contiguous (16-byte aligned), fp32 accumulation, out bf16 (RNE) or
+ * fp32 row-major.  N and K multiples of 8, N < 2^26.
+ */
+uq_status uniquan_gemm_nt(int64_t M, int64_t N, int64_t K, const uint16_t* A,
+                          const uint16_t* B, void* out, int out_dtype,
+                          float scale, void* stream);
+
+/*
+ * uniquan_silu_mul_fwd -- H[i] = silu(G[i]) * U[i], i < n (bf16 in and out,
+ * fp32 arithmetic, silu(x) = x / (1 + exp(-x))); n a multiple of 8,
+ * pointers 16-byte aligned.
+ */
+uq_status uniquan_silu_mul_fwd(int64_t n, const uint16_t* G, const uint16_t* U,
+                               uint16_t* H, void* stream);
+
+/*
+ * uniquan_silu_mul_bwd -- dG[i] = dH[i] U[i] silu'(G[i]),
+ * dU[i] = dH[i] silu(G[i]) (bf16 in and out, fp32 arithmetic,
+ * silu'(x) = sigma(x) (1 + x (1 - sigma(x)))); n a multiple of 8.
+ */
+uq_status uniquan_silu_mul_bwd(int64_t n, const uint16_t* dH, const uint16_t* G,
+                               const uint16_t* U, uint16_t* dG, uint16_t* dU,
+                               void* stream);
+
+/*
  * Deployment form of a folded layer and its inference product (the single
  * binary-coding step R_B(C; Theta*) that Theorem 1 leaves; storage as in the
  * appendix "Memory usage": g k + 16 (k + 1) bits per group).

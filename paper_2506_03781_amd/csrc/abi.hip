@@ -327,6 +327,37 @@ uq_status uniquan_bcq_matmul(int T, int64_t R, int64_t C, int k, int g, const ui
   return hip_status(fn, uq::launch_bcq_matmul(p, static_cast<hipStream_t>(stream)));
 }
 
+uq_status uniquan_gemm_nt(int64_t M, int64_t N, int64_t K, const uint16_t* A, const uint16_t* B, void* out,
+                          int out_dtype, float scale, void* stream) {
+  const char* fn = "uniquan_gemm_nt";
+  if (M < 1 || N < 1 || K < 1) return fail(UQ_EINVAL, "%s: M, N, K must be >= 1", fn);
+  if (N % 8 != 0 || K % 8 != 0) return fail(UQ_EINVAL, "%s: N=%lld and K=%lld must be multiples of 8", fn,
+                                            (long long)N, (long long)K);
+  if (N >= (int64_t(1) << 26) || K >= (int64_t(1) << 31) || M >= (int64_t(1) << 31) ||
+      M * K >= (int64_t(1) << 40) || N * K >= (int64_t(1) << 40) || M * N >= (int64_t(1) << 40))
+    return fail(UQ_EUNSUPPORTED, "%s: shape too large", fn);
+  if (!is_dtype(out_dtype)) return fail(UQ_EINVAL, "%s: bad dtype", fn);
+  REQ_PTR(A, 16); REQ_PTR(B, 16); REQ_PTR(out, 16);
+  uq::GemmLaunch g{A, B, M, N, K, out_dtype == UQ_BF16 ? uq::EPI_GRAD_BF16 : uq::EPI_GRAD_F32, nullptr, out, nullptr,
+                   scale};
+  return hip_status(fn, uq::launch_gemm(g, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uniquan_silu_mul_fwd(int64_t n, const uint16_t* G, const uint16_t* U, uint16_t* H, void* stream) {
+  const char* fn = "uniquan_silu_mul_fwd";
+  if (n < 8 || n % 8 != 0) return fail(UQ_EINVAL, "%s: n=%lld must be a positive multiple of 8", fn, (long long)n);
+  REQ_PTR(G, 16); REQ_PTR(U, 16); REQ_PTR(H, 16);
+  return hip_status(fn, uq::launch_silu_mul_fwd(n, G, U, H, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uniquan_silu_mul_bwd(int64_t n, const uint16_t* dH, const uint16_t* G, const uint16_t* U, uint16_t* dG,
+                               uint16_t* dU, void* stream) {
+  const char* fn = "uniquan_silu_mul_bwd";
+  if (n < 8 || n % 8 != 0) return fail(UQ_EINVAL, "%s: n=%lld must be a positive multiple of 8", fn, (long long)n);
+  REQ_PTR(dH, 16); REQ_PTR(G, 16); REQ_PTR(U, 16); REQ_PTR(dG, 16); REQ_PTR(dU, 16);
+  return hip_status(fn, uq::launch_silu_mul_bwd(n, dH, G, U, dG, dU, static_cast<hipStream_t>(stream)));
+}
+
 uq_status uniquan_sgd(int64_t n, float* theta, const float* grad, float lr, void* stream) {
   const char* fn = "uniquan_sgd";
   if (n < 1) return fail(UQ_EINVAL, "%s: n must be >= 1", fn);

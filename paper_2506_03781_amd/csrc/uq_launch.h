@@ -128,6 +128,9 @@ hipError_t launch_reduce_loss(const float* partials, int64_t n, float* loss, hip
 hipError_t launch_transpose(int64_t rows, int64_t cols, const uint16_t* in, uint16_t* out, hipStream_t st);
 hipError_t launch_sgd(int64_t n, float* theta, const float* grad, float lr, hipStream_t st);
 hipError_t launch_bcq_pack(const BcqPackLaunch& p, hipStream_t st);
+hipError_t launch_silu_mul_fwd(int64_t n, const uint16_t* G, const uint16_t* U, uint16_t* H, hipStream_t st);
+hipError_t launch_silu_mul_bwd(int64_t n, const uint16_t* dH, const uint16_t* G, const uint16_t* U, uint16_t* dG,
+                               uint16_t* dU, hipStream_t st);
 hipError_t launch_bcq_matmul(const BcqMatmulLaunch& p, hipStream_t st);
 int64_t bcq_slabs(int64_t R, int64_t C);
 

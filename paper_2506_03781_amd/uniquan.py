@@ -57,6 +57,9 @@ _SIGS = {
                               _vp, _vp, _vp, _vp, _vp], _i32),
     "uniquan_sgd": ([_i64, _vp, _vp, _f32, _vp], _i32),
     "uniquan_bcq_pack": ([_i64, _i64, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp], _i32),
+    "uniquan_gemm_nt": ([_i64, _i64, _i64, _vp, _vp, _vp, _i32, _f32, _vp], _i32),
+    "uniquan_silu_mul_fwd": ([_i64, _vp, _vp, _vp, _vp], _i32),
+    "uniquan_silu_mul_bwd": ([_i64, _vp, _vp, _vp, _vp, _vp, _vp], _i32),
     "uniquan_bcq_matmul_ws": ([_i32, _i64, _i64], ctypes.c_size_t),
     "uniquan_bcq_matmul": ([_i32, _i64, _i64, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp],
                            _i32),
@@ -281,3 +284,20 @@ def uniquan_bcq_matmul(T, R, C, k, g, X, planes, alpha16, z16, Y, partials_ws=No
         _p(alpha16, Gn * k, _H, "alpha16"), _p(z16, Gn, _H, "z16"), _p(Y, T * R, _F, "Y"),
         _p(partials_ws, need, _F, "partials_ws") if need else _p(partials_ws, None, _F, "partials_ws"),
         partials_ws.numel() if partials_ws is not None else 0, _stream(stream)))
+
+
+def uniquan_gemm_nt(M, N, K, A, B, out, scale=1.0, stream=None):
+    """out [M, N] = scale * A [M, K] B [N, K]^T (bf16 operands; out bf16 or fp32)."""
+    _check(lib().uniquan_gemm_nt(M, N, K, _p(A, M * K, _B, "A"), _p(B, N * K, _B, "B"),
+                                 _p(out, M * N, _W, "out"), _dt(out), float(scale), _stream(stream)))
+
+
+def uniquan_silu_mul_fwd(G, U, H, stream=None):
+    n = G.numel()
+    _check(lib().uniquan_silu_mul_fwd(n, _p(G, n, _B, "G"), _p(U, n, _B, "U"), _p(H, n, _B, "H"), _stream(stream)))
+
+
+def uniquan_silu_mul_bwd(dH, G, U, dG, dU, stream=None):
+    n = G.numel()
+    _check(lib().uniquan_silu_mul_bwd(n, _p(dH, n, _B, "dH"), _p(G, n, _B, "G"), _p(U, n, _B, "U"),
+                                      _p(dG, n, _B, "dG"), _p(dU, n, _B, "dU"), _stream(stream)))

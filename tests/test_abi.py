@@ -174,6 +174,22 @@ def test_bcq_pack_validation(L):
     assert uq.uniquan_bcq_matmul_ws(1, 100, 128) == 0
 
 
+def test_block_entry_validation(L):
+    F = uq.UQ_F32
+    assert L.uniquan_gemm_nt(0, 8, 8, FAKE, FAKE, FAKE, F, 1.0, None) == uq.UQ_EINVAL
+    assert L.uniquan_gemm_nt(4, 12, 8, FAKE, FAKE, FAKE, F, 1.0, None) == uq.UQ_EINVAL
+    assert "N=12" in uq.last_error()
+    assert L.uniquan_gemm_nt(4, 8, 20, FAKE, FAKE, FAKE, F, 1.0, None) == uq.UQ_EINVAL
+    assert L.uniquan_gemm_nt(4, 1 << 26, 8, FAKE, FAKE, FAKE, F, 1.0, None) == uq.UQ_EUNSUPPORTED
+    assert L.uniquan_gemm_nt(4, 8, 8, ODD, FAKE, FAKE, F, 1.0, None) == uq.UQ_EINVAL
+    assert L.uniquan_gemm_nt(4, 8, 8, FAKE, FAKE, FAKE, 7, 1.0, None) == uq.UQ_EINVAL
+    assert L.uniquan_silu_mul_fwd(12, FAKE, FAKE, FAKE, None) == uq.UQ_EINVAL
+    assert L.uniquan_silu_mul_fwd(0, FAKE, FAKE, FAKE, None) == uq.UQ_EINVAL
+    assert L.uniquan_silu_mul_fwd(16, FAKE, None, FAKE, None) == uq.UQ_EINVAL
+    assert L.uniquan_silu_mul_bwd(16, FAKE, FAKE, FAKE, ODD, FAKE, None) == uq.UQ_EINVAL
+    assert L.uniquan_silu_mul_bwd(20, FAKE, FAKE, FAKE, FAKE, FAKE, None) == uq.UQ_EINVAL
+
+
 def test_error_text_is_thread_local(L):
     import threading
     fwd(L, k=0)
