@@ -434,7 +434,7 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((VM & 0xF) | ((VM >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
-template <int BM, int BN, int EPI, int S, int IL>
+template <int BM, int BN, int EPI, int S>
 __global__ __launch_bounds__(256) void gemm_pipe_kernel(GemmArgs p) {
   constexpr int BK = 32;
   constexpr int WM = BM / 2, WN = BN / 2;
@@ -520,14 +520,20 @@ __global__ __launch_bounds__(256) void gemm_pipe_kernel(GemmArgs p) {
       for (int j = 0; j < FN; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
   };
+  // Each substep: one MFMA, half of the next substep's fragment reads, one
+  // MFMA, the other half, then the remaining MFMAs.  An MFMA leads, so the
+  // LDS wait in front of it covers only fragments read a whole substep
+  // earlier (with LDS-DMA loads in flight the compiler can only wait for
+  // every outstanding LDS read, so a read issued first would be waited for
+  // too), and the last read is followed by FM*FN - 2 MFMAs before its data
+  // is needed.
   auto interleave = [&]() {
-    if constexpr (IL) {
-#pragma unroll
-      for (int q = 0; q < FM + FN; ++q) {
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                      // one LDS read
-        __builtin_amdgcn_sched_group_barrier(0x008, (FM * FN) / (FM + FN), 0);  // then MFMAs
-      }
-    }
+    constexpr int R0 = (FM + FN) / 2;
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);             // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x100, R0, 0);            // LDS reads
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);             // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x100, FM + FN - R0, 0);  // LDS reads
+    __builtin_amdgcn_sched_group_barrier(0x008, FM * FN - 2, 0);   // MFMAs
   };
 
   const int nk = int(K / BK);
@@ -538,7 +544,28 @@ __global__ __launch_bounds__(256) void gemm_pipe_kernel(GemmArgs p) {
   else wait_vmcnt<0>();
   __builtin_amdgcn_s_barrier();
   rd(0, 0, a0, b0);
-  for (int kt = 0; kt < nk; ++kt) {
+  int kt = 0;
+  // Steady state: every iteration issues stage kt+S-1 and waits with the same
+  // count, so the body has no branches and the compiler's LDS wait before the
+  // first MFMA of each substep covers only the fragments it reads (with
+  // branches its merged state forced a wait for every outstanding LDS read).
+  for (; kt + S - 1 < nk; ++kt) {
+    const int st = kt % S;
+    __builtin_amdgcn_sched_barrier(0);
+    rd(st, 1, a1, b1);
+    mma(a0, b0);
+    interleave();
+    __builtin_amdgcn_sched_barrier(0);
+    wait_vmcnt<(S - 3) * PER_WAVE>();  // stage kt+1 resident, kt+2..kt+S-2 may be in flight
+    __builtin_amdgcn_s_barrier();
+    issue((kt + S - 1) % S, int64_t(kt + S - 1) * BK);
+    __builtin_amdgcn_sched_barrier(0);
+    rd((kt + 1) % S, 0, a0, b0);
+    mma(a1, b1);
+    interleave();
+  }
+  // the last S-1 stages: nothing left to issue, the waits shrink to zero
+  for (; kt < nk; ++kt) {
     const int st = kt % S;
     __builtin_amdgcn_sched_barrier(0);
     rd(st, 1, a1, b1);  // substep 1 of stage kt while substep 0 multiplies
@@ -591,8 +618,7 @@ size_t gemm_workgroups(int64_t M, int64_t N, int /*epi*/) {
 // register-staged kernel (any K that is a multiple of 8) otherwise.
 template <int BM, int BN, int EPI>
 static void launch_epi(const GemmArgs& a, dim3 grid, hipStream_t st) {
-  constexpr int IL = (BM == 256 && BN == 256) ? 0 : 1;
-  if (a.K % 32 == 0) hipLaunchKernelGGL((gemm_pipe_kernel<BM, BN, EPI, 4, IL>), grid, dim3(256), 0, st, a);
+  if (a.K % 32 == 0) hipLaunchKernelGGL((gemm_pipe_kernel<BM, BN, EPI, 4>), grid, dim3(256), 0, st, a);
   else hipLaunchKernelGGL((gemm_nt_kernel<BM, BN, EPI>), grid, dim3(256), 0, st, a);
 }
 
@@ -627,10 +653,10 @@ hipError_t launch_gemm_ste(const GemmLaunch& q, int k, hipStream_t st) {
   a.tiles_n = int((q.N + 255) / 256);
   const dim3 grid(unsigned(a.tiles_m * a.tiles_n));
   switch (k) {
-    case 1: hipLaunchKernelGGL((gemm_pipe_kernel<256, 256, EPI_STE + 1, 4, 0>), grid, dim3(256), 0, st, a); break;
-    case 2: hipLaunchKernelGGL((gemm_pipe_kernel<256, 256, EPI_STE + 2, 4, 0>), grid, dim3(256), 0, st, a); break;
-    case 3: hipLaunchKernelGGL((gemm_pipe_kernel<256, 256, EPI_STE + 3, 4, 0>), grid, dim3(256), 0, st, a); break;
-    default: hipLaunchKernelGGL((gemm_pipe_kernel<256, 256, EPI_STE + 4, 4, 0>), grid, dim3(256), 0, st, a); break;
+    case 1: hipLaunchKernelGGL((gemm_pipe_kernel<256, 256, EPI_STE + 1, 4>), grid, dim3(256), 0, st, a); break;
+    case 2: hipLaunchKernelGGL((gemm_pipe_kernel<256, 256, EPI_STE + 2, 4>), grid, dim3(256), 0, st, a); break;
+    case 3: hipLaunchKernelGGL((gemm_pipe_kernel<256, 256, EPI_STE + 3, 4>), grid, dim3(256), 0, st, a); break;
+    default: hipLaunchKernelGGL((gemm_pipe_kernel<256, 256, EPI_STE + 4, 4>), grid, dim3(256), 0, st, a); break;
   }
   return hipGetLastError();
 }
