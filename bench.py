@@ -29,6 +29,7 @@ Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
 from __future__ import annotations
 
 import argparse
+import ctypes
 import hashlib
 import json
 import os
@@ -50,11 +51,62 @@ PROFILES = os.path.join(ROOT, "profiles")
 CSRC = os.path.join(ROOT, "paper_2506_03781_amd", "csrc")
 
 
+_HIP = None
+HIP_EVENT_DISABLE_SYSTEM_FENCE = 0x20000000
+
+
+class TimingEvent:
+    """A HIP timing event created with hipEventDisableSystemFence, recorded on
+    torch's current stream.  A default event writes back and invalidates the
+    caches when it completes: a few microseconds of idle GPU per event and
+    the next kernel starts on cold caches, both counted in the phase it
+    brackets.  These events skip that fence; they are read only after a
+    device-wide synchronisation, so their timestamps are complete.  The HIP
+    runtime is the one torch already loaded (one runtime per process)."""
+
+    def __init__(self):
+        global _HIP
+        import torch
+        if _HIP is None:
+            torch.zeros(1, device="cuda")
+            path = next(l.split()[-1] for l in open("/proc/self/maps") if "libamdhip64" in l)
+            h = ctypes.CDLL(path)
+            h.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+            h.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+            h.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+            h.hipEventDestroy.argtypes = [ctypes.c_void_p]
+            _HIP = h
+        self._torch = torch
+        self.ev = ctypes.c_void_p()
+        rc = _HIP.hipEventCreateWithFlags(ctypes.byref(self.ev), HIP_EVENT_DISABLE_SYSTEM_FENCE)
+        if rc != 0:
+            raise RuntimeError(f"hipEventCreateWithFlags failed ({rc})")
+
+    def record(self):
+        rc = _HIP.hipEventRecord(self.ev, ctypes.c_void_p(self._torch.cuda.current_stream().cuda_stream))
+        if rc != 0:
+            raise RuntimeError(f"hipEventRecord failed ({rc})")
+
+    def elapsed_time(self, end) -> float:
+        """Milliseconds from this event to ``end`` (call after a device synchronisation)."""
+        ms = ctypes.c_float()
+        rc = _HIP.hipEventElapsedTime(ctypes.byref(ms), self.ev, end.ev)
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed ({rc})")
+        return ms.value
+
+    def __del__(self):
+        if _HIP is not None and self.ev:
+            _HIP.hipEventDestroy(self.ev)
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=50)
+    # the first few dozen steps after the set-up kernels run slower (the GEMMs
+    # by up to 15%) before the timing settles
+    ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--workload", default="attn4096")
     ap.add_argument("--mode", default="paper", choices=["paper", "full", "local", "frozen"])
     ap.add_argument("--seed", type=int, default=0)
@@ -222,7 +274,7 @@ def bcq_inference(layers, batches=(1, 8), target_bytes=512 << 20):
             for i in range(3):
                 uq.uniquan_bcq_matmul(T, R, C, k, g, X, *copies[i % n_copy], Y, ws)
             n_it = max(20, 2 * n_copy)
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0, e1 = TimingEvent(), TimingEvent()
             e0.record()
             for i in range(n_it):
                 uq.uniquan_bcq_matmul(T, R, C, k, g, X, *copies[i % n_copy], Y, ws)
@@ -272,16 +324,18 @@ def block_mlp(seed, k=3, steps=10, warmup=2):
     for i in range(warmup):
         blk.step(uq.MAP_FULL if i == 0 else uq.MAP_LOCAL, lr_f, lr_b)
         rel.append(float(blk.loss.item()) / l0)
+    # the LOCAL step's launches, recorded once (that run is one more step)
+    step_local = uq.record(blk.step, uq.MAP_LOCAL, lr_f, lr_b)
     torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0, e1 = TimingEvent(), TimingEvent()
     e0.record()
     for _ in range(steps):
-        blk.step(uq.MAP_LOCAL, lr_f, lr_b)
+        step_local()
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / steps
     # one instrumented step for the split between phases
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+    ev = [TimingEvent() for _ in range(5)]
     ev[0].record()
     for q in qs:
         q.fq_fwd(uq.MAP_LOCAL)
@@ -345,11 +399,11 @@ def main():
             if args.init == "unified":
                 if not layers:
                     lay.init_unified(args.init_grid, args.init_rounds, args.init_clip)  # first-launch warm-up
-                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0, e1 = TimingEvent(), TimingEvent()
                 e0.record()
                 lay.init_unified(args.init_grid, args.init_rounds, args.init_clip)
                 e1.record()
-                e1.synchronize()
+                torch.cuda.synchronize()
                 init_ms.append(e0.elapsed_time(e1))
                 if init_np is None and not args.no_cpu_baseline:
                     init_np = (m.W, k, g)
@@ -365,27 +419,40 @@ def main():
 
     phases = ["fq_fwd", "gemm_fwd", "gemm_bwd", "fq_bwd"]
     ev = {}
+    # Each phase's launches are recorded through the checked wrappers the
+    # first time it runs (a warm-up step) and replayed afterwards, so the
+    # host enqueues a phase in a few microseconds and the stream stays ahead
+    # of the GPU; the timing events are created before the timed steps.
+    launches = {}
+
+    def phase(li, lay, name, mode, fn, *a):
+        key = (li, name, mode)
+        if key in launches:
+            launches[key]()
+        else:
+            launches[key] = uq.record(fn, *a)
 
     def run_step(step, timed):
         mode = schedule(args.mode, step)
         for li, lay in enumerate(layers):
-            es = [torch.cuda.Event(enable_timing=True) for _ in range(5)] if timed else None
+            es = ev_pool.pop() if timed else None
             if timed:
                 es[0].record()
-            lay.fq_fwd(mode)
+            phase(li, lay, "fq_fwd", mode, lay.fq_fwd, mode)
             if timed:
                 es[1].record()
-            lay.recon(backward=False)
+            phase(li, lay, "gemm_fwd", 0, lay.recon, False)
             if timed:
                 es[2].record()
-            uq.uniquan_layer_grad(lay.T, lay.R, lay.C, lay.Et, lay.Xt, lay.G)
+            phase(li, lay, "gemm_bwd", 0, uq.uniquan_layer_grad, lay.T, lay.R, lay.C, lay.Et, lay.Xt, lay.G)
             if timed:
                 es[3].record()
-            lay.fq_bwd_sgd()
+            phase(li, lay, "fq_bwd", 0, lay.fq_bwd_sgd)
             if timed:
                 es[4].record()
                 ev.setdefault(li, []).append(es)
 
+    ev_pool = [[TimingEvent() for _ in range(5)] for _ in range(args.steps * len(layers))]
     for s in range(args.warmup):
         run_step(s, False)
     if args.calib_copy:
@@ -463,7 +530,7 @@ def main():
     by_mode = {}
     for name, md in (("full", uq.MAP_FULL), ("local", uq.MAP_LOCAL), ("frozen", uq.MAP_FROZEN)):
         lay = layers[0]
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a, b = TimingEvent(), TimingEvent()
         lay.fq_fwd(md)
         a.record()
         for _ in range(10):
@@ -479,7 +546,7 @@ def main():
         fev = []
         for s_ in range(args.steps + 2):
             mode = schedule(args.mode, args.warmup + args.steps + s_)
-            e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+            e = [TimingEvent() for _ in range(2)]
             e[0].record()
             for lay in layers:
                 lay.fq_fwd(mode)

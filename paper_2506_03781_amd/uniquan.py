@@ -66,10 +66,10 @@ _SIGS = {
 }
 
 _lib = None
+_recorder = None
 
 
-def lib() -> ctypes.CDLL:
-    """The loaded library; raises if it has not been built."""
+def _load() -> ctypes.CDLL:
     global _lib
     if _lib is None:
         if not os.path.exists(LIB_PATH):
@@ -82,6 +82,71 @@ def lib() -> ctypes.CDLL:
             fn.restype = res
         _lib = L
     return _lib
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library; raises if it has not been built."""
+    L = _load()
+    return L if _recorder is None else _recorder
+
+
+def _is_launch(name: str) -> bool:
+    """Entry points that enqueue work: status result, stream as last argument."""
+    sig = _SIGS.get(name)
+    return sig is not None and sig[1] is _i32 and len(sig[0]) > 0 and sig[0][-1] is _vp
+
+
+class _Recorder:
+    """Stands in for the library while ``record`` runs: every launch entry
+    point is called as usual and its marshalled arguments are kept."""
+
+    def __init__(self, real):
+        self.real, self.calls = real, []
+
+    def __getattr__(self, name):
+        fn = getattr(self.real, name)
+        if not _is_launch(name):
+            return fn
+
+        def call(*args):
+            self.calls.append((fn, args))
+            return fn(*args)
+        return call
+
+
+class Launches:
+    """Entry-point calls recorded once through the checked wrappers and
+    replayed with the same marshalled arguments (pointers, sizes, scalars) on
+    the stream given to the call: the per-tensor checks run once, at
+    recording.  The tensors behind the recorded pointers must stay alive and
+    keep their storage; a status other than UQ_OK still raises."""
+
+    def __init__(self, calls):
+        self.calls = calls
+
+    def __len__(self):
+        return len(self.calls)
+
+    def __call__(self, stream=None):
+        st = _stream(stream)
+        for fn, args in self.calls:
+            status = fn(*args[:-1], st)
+            if status != UQ_OK:
+                raise UniquanError(status, last_error())
+
+
+def record(fn, *args, **kwargs) -> Launches:
+    """Run ``fn(*args, **kwargs)`` once (it executes normally) and return its
+    launches for replay.  Not thread-safe: one recording at a time."""
+    global _recorder
+    if _recorder is not None:
+        raise RuntimeError("record() does not nest")
+    _recorder = _Recorder(_load())
+    try:
+        fn(*args, **kwargs)
+        return Launches(_recorder.calls)
+    finally:
+        _recorder = None
 
 
 def declared_symbols() -> list:

@@ -219,3 +219,26 @@ def test_product_never_imports_oracle():
                 txt = open(os.path.join(dirpath, f)).read()
                 assert not re.search(r"^\s*(from|import)\s+oracle", txt, re.M), f
                 assert "oracle/" not in txt, f
+
+
+def test_recorder_classifies_launches(L):
+    launches = {n for n in uq._SIGS if uq._is_launch(n)}
+    assert "uniquan_fq_fwd" in launches and "uniquan_gemm_nt" in launches and "uniquan_bcq_matmul" in launches
+    for n in ("uniquan_abi_version", "uniquan_last_error", "uniquan_recon_ws", "uniquan_bcq_matmul_ws"):
+        assert n not in launches
+    assert len(launches) == len(uq._SIGS) - 4
+
+
+def test_replay_raises_on_error_status(L):
+    bad = uq.Launches([(L.uniquan_sgd, (0, FAKE, FAKE, 0.1, None))])
+    assert len(bad) == 1
+    with pytest.raises(uq.UniquanError, match="n must be"):
+        bad(stream=0)
+
+
+def test_record_propagates_and_resets(L):
+    def failing():
+        uq._check(uq.lib().uniquan_sgd(0, FAKE, FAKE, 0.1, None))
+    with pytest.raises(uq.UniquanError):
+        uq.record(failing)
+    assert uq._recorder is None and uq.lib() is uq._load()
