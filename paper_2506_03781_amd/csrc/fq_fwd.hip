@@ -119,10 +119,12 @@ static bool use_neighbour_table(int logg, int k) { return ((size_t(512) >> logg)
 // (8 per lane per chunk; groups never straddle chunks since g divides 512)
 // and keeps the level tables of their groups in a private LDS region, so
 // table building needs only wave-local ordering and no workgroup barrier.
-// The lane issues the W, s (and code) loads of all its chunks first, so a
-// wavefront keeps CH x 3.5 KB in flight; while they are in flight the wave
-// builds its tables: one lane per level computes q(b), then ranks it among
-// the group's levels by counting (sort key (value, code)).
+// The wave builds its tables first (one lane per level computes q(b), then
+// ranks it among the group's levels by counting, sort key (value, code)) and
+// only then issues the W, s (and code) loads of all its chunks, CH x 3.5 KB
+// in flight: a wave's loads complete in issue order, so parameter loads
+// issued behind the chunk loads kept the table build waiting for the whole
+// chunk, while other wavefronts' chunk loads cover this one's table build.
 // MODE: 0 FULL, 1 LOCAL by search, 2 FROZEN, 3 LOCAL through the neighbour
 // table (the LOCAL variant used whenever the table fits).
 template <int WDT, int ODT, int MODE, int LOGL, int CH>
@@ -156,22 +158,6 @@ __global__ __launch_bounds__(kThreads) void fq_fwd_kernel(FwdArgs a) {
   Raw8<WDT> w[CH];
   float4 s0[CH], s1[CH];
   uint2 prev[CH];
-#pragma unroll
-  for (int h = 0; h < CH; ++h) {
-    const int lo = h * 512 + lane * kVec;  // this lane's first weight of chunk h, within the wave
-    s0[h] = make_float4(0, 0, 0, 0);
-    s1[h] = s0[h];
-    prev[h] = make_uint2(0u, 0u);
-    if (lo < nvalid) {
-      const int64_t off = wbase + lo;
-      w[h].load(a.W, off);
-      const float4* sp = reinterpret_cast<const float4*>(a.s + off);
-      s0[h] = sp[0];
-      s1[h] = sp[1];
-      if constexpr (MODE != 0) prev[h] = load8u8(a.codes, off);
-    }
-  }
-
   // raw levels by code (and their sort keys), and the per-group parameters
   for (int e = lane; e < ev; e += 64) {
     const int gl = e >> LOGL;
@@ -227,6 +213,22 @@ __global__ __launch_bounds__(kThreads) void fq_fwd_kernel(FwdArgs a) {
       nb[e] = make_float4(tab.qs[base + l], tab.qs[base + d], tab.qs[base + r], __uint_as_float(codes));
     }
     wave_lds_sync();
+  }
+
+#pragma unroll
+  for (int h = 0; h < CH; ++h) {
+    const int lo = h * 512 + lane * kVec;  // this lane's first weight of chunk h, within the wave
+    s0[h] = make_float4(0, 0, 0, 0);
+    s1[h] = s0[h];
+    prev[h] = make_uint2(0u, 0u);
+    if (lo < nvalid) {
+      const int64_t off = wbase + lo;
+      w[h].load(a.W, off);
+      const float4* sp = reinterpret_cast<const float4*>(a.s + off);
+      s0[h] = sp[0];
+      s1[h] = sp[1];
+      if constexpr (MODE != 0) prev[h] = load8u8(a.codes, off);
+    }
   }
 
 #pragma unroll
