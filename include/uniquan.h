@@ -358,6 +358,103 @@ uq_status uniquan_silu_mul_bwd(int64_t n, const uint16_t* dH, const uint16_t* G,
                                void* stream);
 
 /*
+ * Block-level reconstruction of a whole Transformer block (Algorithm 1; the
+ * block is one multi-head attention module and one MLP module, appendix
+ * "Units in LLMs"; the loss ||f(X; W) - f(X_hat; What)||_F^2 of the appendix
+ * "Error Types").  Pre-norm block: Z1 = RMSNorm(X; g1); Q, K rotary-embedded
+ * (pairs (i, i + d/2), angle p 1e4^(-2i/d) at position p of the sequence),
+ * causal softmax attention per sequence and head; R = X + O W_o^T;
+ * Z2 = RMSNorm(R; g2); Y = R + MLP(Z2).  RMSNorm(x; g) = x / sqrt(mean(x^2)
+ * + 1e-5) g over the C hidden features.  Layouts: token-major [T, C];
+ * head-major [H, T, d] (T = n_seq L tokens, one [L, d] block per sequence
+ * and head); scores [H n_seq, L, L].  The step is composed from the calls
+ * below, uniquan_gemm_nt(_batched), uniquan_silu_mul_*, uniquan_transpose_*
+ * and the quantizer entry points; every pointer is a device pointer owned by
+ * the caller, errors are reported before any launch.
+ */
+
+/*
+ * uniquan_gemm_nt_batched -- for b < batch:
+ * out_b[M x N] = scale * A_b[M x K] B_b[N x K]^T with A_b = A + b stride_a,
+ * B_b = B + b stride_b (elements; 0 repeats an operand), out_b = out +
+ * b stride_out (elements of out_dtype, >= M N).  Shape rules as
+ * uniquan_gemm_nt; strides multiples of 8; batch <= 65535.
+ */
+uq_status uniquan_gemm_nt_batched(int64_t M, int64_t N, int64_t K, int64_t batch,
+                                  const uint16_t* A, int64_t stride_a,
+                                  const uint16_t* B, int64_t stride_b, void* out,
+                                  int64_t stride_out, int out_dtype, float scale,
+                                  void* stream);
+
+/*
+ * uniquan_add_rmsnorm -- per row t < T of [T, C] (fp32): v = X + A (A may be
+ * NULL), R = v (written when A is given; R may be NULL otherwise),
+ * rinv[t] = 1 / sqrt(mean(v^2) + 1e-5), Z = bf16((v rinv) gamma).
+ * C a multiple of 8.
+ */
+uq_status uniquan_add_rmsnorm(int64_t T, int64_t C, const float* X,
+                              const float* A, const float* gamma, float* R,
+                              uint16_t* Z, float* rinv, void* stream);
+
+/*
+ * uniquan_rmsnorm_bwd -- backward of Z = (X rinv) gamma plus a residual
+ * gradient: with g = gamma (dZa + dZb) (dZb may be NULL),
+ * dR = escale E + rinv g - X rinv^3 sum(g X) / C per row; E (bf16) may be
+ * NULL.  dR is written in bf16, and in fp32 to dRf when given.
+ */
+uq_status uniquan_rmsnorm_bwd(int64_t T, int64_t C, const float* dZa,
+                              const float* dZb, const float* X,
+                              const float* gamma, const float* rinv,
+                              const uint16_t* E, float escale, uint16_t* dR,
+                              float* dRf, void* stream);
+
+/*
+ * uniquan_rope_split -- token-major in [T, H d] (UQ_F32 or UQ_BF16) to
+ * head-major bf16 out [H, T, d]; with rotate != 0 each pair (i, i + d/2) of
+ * token t is rotated by angle (t mod L) 1e4^(-2i/d).  d even, L divides T.
+ * uniquan_rope_merge -- the inverse layout change (head-major in, token-
+ * major bf16 out), rotating by minus the angle when rotate != 0.
+ */
+uq_status uniquan_rope_split(int64_t T, int H, int d, int L, const void* in,
+                             int in_dtype, int rotate, uint16_t* out,
+                             void* stream);
+uq_status uniquan_rope_merge(int64_t T, int H, int d, int L, const void* in,
+                             int in_dtype, int rotate, uint16_t* out,
+                             void* stream);
+
+/*
+ * uniquan_softmax_causal -- for each row r < rows of S [rows, L] (fp32, row
+ * i = r mod L of an [L, L] score block): P[r, j] = softmax over j <= i of
+ * S[r, j], 0 for j > i (bf16).  rows a multiple of L.
+ * uniquan_softmax_causal_bwd -- dS = P (dP - sum_j P dP) per row (bf16 out;
+ * dP fp32, P bf16 as written by the forward).
+ */
+uq_status uniquan_softmax_causal(int64_t rows, int L, const float* S,
+                                 uint16_t* P, void* stream);
+uq_status uniquan_softmax_causal_bwd(int64_t rows, int L, const float* dP,
+                                     const uint16_t* P, uint16_t* dS,
+                                     void* stream);
+
+/*
+ * uniquan_transpose_bf16_batched -- out_b = in_b^T for batch matrices
+ * [R, C] stored back to back (bf16).
+ */
+uq_status uniquan_transpose_bf16_batched(int64_t batch, int64_t R, int64_t C,
+                                         const uint16_t* in, uint16_t* out,
+                                         void* stream);
+
+/*
+ * uniquan_block_loss -- E = (R + M) - Yref element-wise (fp32 in, bf16 out)
+ * and loss[0] = sum of the unrounded E^2 (per-block fp32 partials summed in
+ * fp64 in a fixed order).  partials holds uniquan_block_loss_ws() floats
+ * (partials_len gives its size).
+ */
+size_t uniquan_block_loss_ws(void);
+uq_status uniquan_block_loss(int64_t n, const float* R, const float* M,
+                             const float* Yref, uint16_t* E, float* partials,
+                             size_t partials_len, float* loss, void* stream);
+
+/*
  * Deployment form of a folded layer and its inference product (the single
  * binary-coding step R_B(C; Theta*) that Theorem 1 leaves; storage as in the
  * appendix "Memory usage": g k + 16 (k + 1) bits per group).

@@ -13,7 +13,8 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libuniquan.so")
-SOURCES = ["abi.hip", "fq_fwd.hip", "fq_bwd.hip", "gemm.hip", "init_unified.hip", "bcq_deploy.hip", "block_mlp.hip"]
+SOURCES = ["abi.hip", "fq_fwd.hip", "fq_bwd.hip", "gemm.hip", "init_unified.hip", "bcq_deploy.hip", "block_mlp.hip",
+           "block_attn.hip"]
 
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

@@ -358,6 +358,125 @@ uq_status uniquan_silu_mul_bwd(int64_t n, const uint16_t* dH, const uint16_t* G,
   return hip_status(fn, uq::launch_silu_mul_bwd(n, dH, G, U, dG, dU, static_cast<hipStream_t>(stream)));
 }
 
+uq_status uniquan_gemm_nt_batched(int64_t M, int64_t N, int64_t K, int64_t batch, const uint16_t* A, int64_t stride_a,
+                                  const uint16_t* B, int64_t stride_b, void* out, int64_t stride_out, int out_dtype,
+                                  float scale, void* stream) {
+  const char* fn = "uniquan_gemm_nt_batched";
+  if (M < 1 || N < 1 || K < 1) return fail(UQ_EINVAL, "%s: M, N, K must be >= 1", fn);
+  if (batch < 1 || batch > 65535) return fail(UQ_EINVAL, "%s: batch=%lld must be in 1..65535", fn, (long long)batch);
+  if (N % 8 != 0 || K % 8 != 0) return fail(UQ_EINVAL, "%s: N=%lld and K=%lld must be multiples of 8", fn,
+                                            (long long)N, (long long)K);
+  if (N >= (int64_t(1) << 26) || K >= (int64_t(1) << 31) || M >= (int64_t(1) << 31) ||
+      M * K >= (int64_t(1) << 40) || N * K >= (int64_t(1) << 40) || M * N >= (int64_t(1) << 40))
+    return fail(UQ_EUNSUPPORTED, "%s: shape too large", fn);
+  if (!is_dtype(out_dtype)) return fail(UQ_EINVAL, "%s: bad dtype", fn);
+  if (stride_a < 0 || stride_b < 0 || stride_a % 8 != 0 || stride_b % 8 != 0)
+    return fail(UQ_EINVAL, "%s: operand strides must be non-negative multiples of 8", fn);
+  if (stride_out < M * N || stride_out % 8 != 0)
+    return fail(UQ_EINVAL, "%s: stride_out=%lld must be a multiple of 8 and >= M*N", fn, (long long)stride_out);
+  if ((batch - 1) * stride_out >= (int64_t(1) << 40)) return fail(UQ_EUNSUPPORTED, "%s: batch span too large", fn);
+  REQ_PTR(A, 16); REQ_PTR(B, 16); REQ_PTR(out, 16);
+  uq::GemmLaunch g{A, B, M, N, K, out_dtype == UQ_BF16 ? uq::EPI_GRAD_BF16 : uq::EPI_GRAD_F32, nullptr, out, nullptr,
+                   scale};
+  g.batch = batch;
+  g.bsa = stride_a;
+  g.bsb = stride_b;
+  g.bso = stride_out * (out_dtype == UQ_BF16 ? 2 : 4);
+  return hip_status(fn, uq::launch_gemm(g, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uniquan_add_rmsnorm(int64_t T, int64_t C, const float* X, const float* A, const float* gamma, float* R,
+                              uint16_t* Z, float* rinv, void* stream) {
+  const char* fn = "uniquan_add_rmsnorm";
+  if (T < 1 || C < 8 || C % 8 != 0) return fail(UQ_EINVAL, "%s: T >= 1 and C a positive multiple of 8 required", fn);
+  if (A != nullptr && R == nullptr) return fail(UQ_EINVAL, "%s: R must be given with A", fn);
+  REQ_PTR(X, 4); REQ_PTR(gamma, 4); REQ_PTR(Z, 2); REQ_PTR(rinv, 4);
+  if (A && !aligned(A, 4)) return fail(UQ_EINVAL, "%s: A must be 4-byte aligned", fn);
+  if (R && !aligned(R, 4)) return fail(UQ_EINVAL, "%s: R must be 4-byte aligned", fn);
+  return hip_status(fn, uq::launch_add_rmsnorm(T, C, X, A, gamma, R, Z, rinv, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uniquan_rmsnorm_bwd(int64_t T, int64_t C, const float* dZa, const float* dZb, const float* X,
+                              const float* gamma, const float* rinv, const uint16_t* E, float escale, uint16_t* dR,
+                              float* dRf, void* stream) {
+  const char* fn = "uniquan_rmsnorm_bwd";
+  if (T < 1 || C < 8 || C % 8 != 0) return fail(UQ_EINVAL, "%s: T >= 1 and C a positive multiple of 8 required", fn);
+  REQ_PTR(dZa, 4); REQ_PTR(X, 4); REQ_PTR(gamma, 4); REQ_PTR(rinv, 4); REQ_PTR(dR, 2);
+  if (dZb && !aligned(dZb, 4)) return fail(UQ_EINVAL, "%s: dZb must be 4-byte aligned", fn);
+  if (E && !aligned(E, 2)) return fail(UQ_EINVAL, "%s: E must be 2-byte aligned", fn);
+  if (dRf && !aligned(dRf, 4)) return fail(UQ_EINVAL, "%s: dRf must be 4-byte aligned", fn);
+  return hip_status(fn, uq::launch_rmsnorm_bwd(T, C, dZa, dZb, X, gamma, rinv, E, escale, dR, dRf,
+                                               static_cast<hipStream_t>(stream)));
+}
+
+static uq_status check_heads(const char* fn, int64_t T, int H, int d, int L, int in_dtype) {
+  if (T < 1 || H < 1 || d < 2 || d % 2 != 0 || L < 1 || T % L != 0)
+    return fail(UQ_EINVAL, "%s: need T >= 1, H >= 1, even d >= 2 and L dividing T", fn);
+  if (T * H * d >= (int64_t(1) << 40) || L >= (1 << 24)) return fail(UQ_EUNSUPPORTED, "%s: shape too large", fn);
+  if (!is_dtype(in_dtype)) return fail(UQ_EINVAL, "%s: bad dtype", fn);
+  return UQ_OK;
+}
+
+uq_status uniquan_rope_split(int64_t T, int H, int d, int L, const void* in, int in_dtype, int rotate, uint16_t* out,
+                             void* stream) {
+  const char* fn = "uniquan_rope_split";
+  const uq_status c = check_heads(fn, T, H, d, L, in_dtype);
+  if (c != UQ_OK) return c;
+  REQ_PTR(in, in_dtype == UQ_F32 ? 4 : 2); REQ_PTR(out, 2);
+  return hip_status(fn, uq::launch_rope_split(T, H, d, L, in, in_dtype == UQ_F32, rotate != 0, out,
+                                              static_cast<hipStream_t>(stream)));
+}
+
+uq_status uniquan_rope_merge(int64_t T, int H, int d, int L, const void* in, int in_dtype, int rotate, uint16_t* out,
+                             void* stream) {
+  const char* fn = "uniquan_rope_merge";
+  const uq_status c = check_heads(fn, T, H, d, L, in_dtype);
+  if (c != UQ_OK) return c;
+  REQ_PTR(in, in_dtype == UQ_F32 ? 4 : 2); REQ_PTR(out, 2);
+  return hip_status(fn, uq::launch_rope_merge(T, H, d, L, in, in_dtype == UQ_F32, rotate != 0, out,
+                                              static_cast<hipStream_t>(stream)));
+}
+
+uq_status uniquan_softmax_causal(int64_t rows, int L, const float* S, uint16_t* P, void* stream) {
+  const char* fn = "uniquan_softmax_causal";
+  if (L < 1 || rows < 1 || rows % L != 0) return fail(UQ_EINVAL, "%s: rows must be a positive multiple of L", fn);
+  if (rows * L >= (int64_t(1) << 40)) return fail(UQ_EUNSUPPORTED, "%s: shape too large", fn);
+  REQ_PTR(S, 4); REQ_PTR(P, 2);
+  return hip_status(fn, uq::launch_softmax_causal(rows, L, S, P, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uniquan_softmax_causal_bwd(int64_t rows, int L, const float* dP, const uint16_t* P, uint16_t* dS,
+                                     void* stream) {
+  const char* fn = "uniquan_softmax_causal_bwd";
+  if (L < 1 || rows < 1 || rows % L != 0) return fail(UQ_EINVAL, "%s: rows must be a positive multiple of L", fn);
+  if (rows * L >= (int64_t(1) << 40)) return fail(UQ_EUNSUPPORTED, "%s: shape too large", fn);
+  REQ_PTR(dP, 4); REQ_PTR(P, 2); REQ_PTR(dS, 2);
+  return hip_status(fn, uq::launch_softmax_bwd(rows, L, dP, P, dS, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uniquan_transpose_bf16_batched(int64_t batch, int64_t R, int64_t C, const uint16_t* in, uint16_t* out,
+                                         void* stream) {
+  const char* fn = "uniquan_transpose_bf16_batched";
+  if (batch < 1 || batch > 65535 || R < 1 || C < 1)
+    return fail(UQ_EINVAL, "%s: need 1 <= batch <= 65535 and R, C >= 1", fn);
+  if (batch * R * C >= (int64_t(1) << 40) || ((R + 63) / 64) * ((C + 63) / 64) >= (int64_t(1) << 31))
+    return fail(UQ_EUNSUPPORTED, "%s: shape too large", fn);
+  REQ_PTR(in, 2); REQ_PTR(out, 2);
+  return hip_status(fn, uq::launch_transpose_batched(batch, R, C, in, out, static_cast<hipStream_t>(stream)));
+}
+
+size_t uniquan_block_loss_ws(void) { return uq::block_loss_ws(); }
+
+uq_status uniquan_block_loss(int64_t n, const float* R, const float* M, const float* Yref, uint16_t* E,
+                             float* partials, size_t partials_len, float* loss, void* stream) {
+  const char* fn = "uniquan_block_loss";
+  if (n < 1) return fail(UQ_EINVAL, "%s: n must be >= 1", fn);
+  if (partials_len < uq::block_loss_ws())
+    return fail(UQ_EINVAL, "%s: partials has %zu floats, needs %zu", fn, partials_len, uq::block_loss_ws());
+  REQ_PTR(R, 4); REQ_PTR(M, 4); REQ_PTR(Yref, 4); REQ_PTR(E, 2); REQ_PTR(partials, 4); REQ_PTR(loss, 4);
+  return hip_status(fn, uq::launch_block_loss(n, R, M, Yref, E, partials, loss, static_cast<hipStream_t>(stream)));
+}
+
 uq_status uniquan_sgd(int64_t n, float* theta, const float* grad, float lr, void* stream) {
   const char* fn = "uniquan_sgd";
   if (n < 1) return fail(UQ_EINVAL, "%s: n must be >= 1", fn);

@@ -39,7 +39,20 @@ struct GemmArgs {
   float scale;
   int tiles_m, tiles_n;
   SteParams ste;
+  // strided batch (gridDim.y > 1): element offsets of A and B and byte
+  // offset of out per batch
+  int64_t bsa, bsb, bso;
 };
+
+// Operands and output of batch blockIdx.y.
+__device__ __forceinline__ void select_batch(GemmArgs& p) {
+  if (gridDim.y > 1) {
+    const int64_t b = blockIdx.y;
+    p.A += b * p.bsa;
+    p.B += b * p.bsb;
+    p.out = static_cast<char*>(p.out) + b * p.bso;
+  }
+}
 
 // Two fp32 values -> packed bf16 pair (lo in bits 0..15), round to nearest
 // even: one v_cvt_pk_bf16_f32 on gfx950.
@@ -294,6 +307,7 @@ __device__ __forceinline__ void epilogue(const GemmArgs& p, f32x16 (&acc)[FM][FN
 
 template <int BM, int BN, int EPI>
 __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs p) {
+  select_batch(p);
   constexpr int BK = 64;
   constexpr int WM = BM / 2, WN = BN / 2;
   constexpr int FM = WM / 32, FN = WN / 32;
@@ -436,6 +450,7 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 template <int BM, int BN, int EPI, int S>
 __global__ __launch_bounds__(256) void gemm_pipe_kernel(GemmArgs p) {
+  select_batch(p);
   constexpr int BK = 32;
   constexpr int WM = BM / 2, WN = BN / 2;
   constexpr int FM = WM / 32, FN = WN / 32;
@@ -600,9 +615,10 @@ static int tiles(int64_t M, int64_t N) {
 // least one workgroup per compute unit (larger tiles move fewer operand
 // bytes per flop through L2 and LDS).
 enum TileShape { T256x256, T256x128, T128x128 };
-static TileShape pick(int64_t M, int64_t N) {
-  if (tiles<256, 256>(M, N) >= 256) return T256x256;
-  if (tiles<256, 128>(M, N) >= 256) return T256x128;
+static TileShape pick(int64_t M, int64_t N, int64_t batch = 1) {
+  const int64_t nb = batch > 1 ? batch : 1;
+  if (tiles<256, 256>(M, N) * nb >= 256) return T256x256;
+  if (tiles<256, 128>(M, N) * nb >= 256) return T256x128;
   return T128x128;
 }
 
@@ -627,9 +643,10 @@ static hipError_t launch_bm(const GemmLaunch& q, hipStream_t st) {
   GemmArgs a;
   a.A = q.A; a.B = q.B; a.M = q.M; a.N = q.N; a.K = q.K;
   a.Yt = q.Yt; a.out = q.out; a.partials = q.partials; a.scale = q.scale;
+  a.bsa = q.bsa; a.bsb = q.bsb; a.bso = q.bso;
   a.tiles_m = int((q.M + BM - 1) / BM);
   a.tiles_n = int((q.N + BN - 1) / BN);
-  const dim3 grid(unsigned(a.tiles_m * a.tiles_n));
+  const dim3 grid(unsigned(a.tiles_m * a.tiles_n), unsigned(q.batch > 1 ? q.batch : 1));
   switch (q.epi) {
     case EPI_TARGET: launch_epi<BM, BN, EPI_TARGET>(a, grid, st); break;
     case EPI_LOSS:
@@ -649,6 +666,7 @@ hipError_t launch_gemm_ste(const GemmLaunch& q, int k, hipStream_t st) {
   a.A = q.A; a.B = q.B; a.M = q.M; a.N = q.N; a.K = q.K;
   a.Yt = nullptr; a.out = nullptr; a.partials = nullptr; a.scale = q.scale;
   a.ste = q.ste;
+  a.bsa = a.bsb = a.bso = 0;
   a.tiles_m = int((q.M + 255) / 256);
   a.tiles_n = int((q.N + 255) / 256);
   const dim3 grid(unsigned(a.tiles_m * a.tiles_n));
@@ -662,7 +680,7 @@ hipError_t launch_gemm_ste(const GemmLaunch& q, int k, hipStream_t st) {
 }
 
 hipError_t launch_gemm(const GemmLaunch& q, hipStream_t st) {
-  switch (pick(q.M, q.N)) {
+  switch (pick(q.M, q.N, q.batch)) {
     case T256x256: return launch_bm<256, 256>(q, st);
     case T256x128: return launch_bm<256, 128>(q, st);
     default: return launch_bm<128, 128>(q, st);

@@ -98,6 +98,9 @@ struct GemmLaunch {
   float* partials;     // EPI_LOSS, one per workgroup
   float scale;
   SteParams ste;       // EPI_STE
+  // strided batch (EPI_GRAD_*): batch > 1 products, operands and output of
+  // batch b at A + b bsa, B + b bsb (elements), out + b bso (bytes)
+  int64_t batch, bsa, bsb, bso;
 };
 
 // Deployment form (bit-planes + binary16 Theta*_B) and its product.
@@ -128,6 +131,22 @@ hipError_t launch_reduce_loss(const float* partials, int64_t n, float* loss, hip
 hipError_t launch_transpose(int64_t rows, int64_t cols, const uint16_t* in, uint16_t* out, hipStream_t st);
 hipError_t launch_sgd(int64_t n, float* theta, const float* grad, float lr, hipStream_t st);
 hipError_t launch_bcq_pack(const BcqPackLaunch& p, hipStream_t st);
+hipError_t launch_add_rmsnorm(int64_t T, int64_t C, const float* X, const float* A, const float* gamma, float* R,
+                              uint16_t* Z, float* rinv, hipStream_t st);
+hipError_t launch_rmsnorm_bwd(int64_t T, int64_t C, const float* dZa, const float* dZb, const float* X,
+                              const float* gamma, const float* rinv, const uint16_t* E, float escale, uint16_t* dR,
+                              float* dRf, hipStream_t st);
+hipError_t launch_rope_split(int64_t T, int H, int d, int L, const void* in, int in_f32, int rotate, uint16_t* out,
+                             hipStream_t st);
+hipError_t launch_rope_merge(int64_t T, int H, int d, int L, const void* in, int in_f32, int rotate, uint16_t* out,
+                             hipStream_t st);
+hipError_t launch_softmax_causal(int64_t rows, int L, const float* S, uint16_t* P, hipStream_t st);
+hipError_t launch_softmax_bwd(int64_t rows, int L, const float* dP, const uint16_t* P, uint16_t* dS, hipStream_t st);
+hipError_t launch_transpose_batched(int64_t B, int64_t R, int64_t C, const uint16_t* in, uint16_t* out,
+                                    hipStream_t st);
+size_t block_loss_ws();
+hipError_t launch_block_loss(int64_t n, const float* Rres, const float* M, const float* Yref, uint16_t* E,
+                             float* partials, float* loss, hipStream_t st);
 hipError_t launch_silu_mul_fwd(int64_t n, const uint16_t* G, const uint16_t* U, uint16_t* H, hipStream_t st);
 hipError_t launch_silu_mul_bwd(int64_t n, const uint16_t* dH, const uint16_t* G, const uint16_t* U, uint16_t* dG,
                                uint16_t* dU, hipStream_t st);

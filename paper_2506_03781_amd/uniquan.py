@@ -60,6 +60,16 @@ _SIGS = {
     "uniquan_gemm_nt": ([_i64, _i64, _i64, _vp, _vp, _vp, _i32, _f32, _vp], _i32),
     "uniquan_silu_mul_fwd": ([_i64, _vp, _vp, _vp, _vp], _i32),
     "uniquan_silu_mul_bwd": ([_i64, _vp, _vp, _vp, _vp, _vp, _vp], _i32),
+    "uniquan_gemm_nt_batched": ([_i64, _i64, _i64, _i64, _vp, _i64, _vp, _i64, _vp, _i64, _i32, _f32, _vp], _i32),
+    "uniquan_add_rmsnorm": ([_i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp], _i32),
+    "uniquan_rmsnorm_bwd": ([_i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _f32, _vp, _vp, _vp], _i32),
+    "uniquan_rope_split": ([_i64, _i32, _i32, _i32, _vp, _i32, _i32, _vp, _vp], _i32),
+    "uniquan_rope_merge": ([_i64, _i32, _i32, _i32, _vp, _i32, _i32, _vp, _vp], _i32),
+    "uniquan_softmax_causal": ([_i64, _i32, _vp, _vp, _vp], _i32),
+    "uniquan_softmax_causal_bwd": ([_i64, _i32, _vp, _vp, _vp, _vp], _i32),
+    "uniquan_transpose_bf16_batched": ([_i64, _i64, _i64, _vp, _vp, _vp], _i32),
+    "uniquan_block_loss_ws": ([], ctypes.c_size_t),
+    "uniquan_block_loss": ([_i64, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp, _vp], _i32),
     "uniquan_bcq_matmul_ws": ([_i32, _i64, _i64], ctypes.c_size_t),
     "uniquan_bcq_matmul": ([_i32, _i64, _i64, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp],
                            _i32),
@@ -366,3 +376,66 @@ def uniquan_silu_mul_bwd(dH, G, U, dG, dU, stream=None):
     n = G.numel()
     _check(lib().uniquan_silu_mul_bwd(n, _p(dH, n, _B, "dH"), _p(G, n, _B, "G"), _p(U, n, _B, "U"),
                                       _p(dG, n, _B, "dG"), _p(dU, n, _B, "dU"), _stream(stream)))
+
+
+def uniquan_gemm_nt_batched(M, N, K, batch, A, stride_a, B, stride_b, out, stride_out, scale=1.0, stream=None):
+    """out_b = scale * A_b B_b^T for b < batch (strides in elements; 0 repeats an operand)."""
+    na = (batch - 1) * stride_a + M * K
+    nb = (batch - 1) * stride_b + N * K
+    no = (batch - 1) * stride_out + M * N
+    _check(lib().uniquan_gemm_nt_batched(M, N, K, batch, _p(A, na, _B, "A"), stride_a, _p(B, nb, _B, "B"), stride_b,
+                                         _p(out, no, _W, "out"), stride_out, _dt(out), float(scale), _stream(stream)))
+
+
+def uniquan_add_rmsnorm(T, C, X, A, gamma, R, Z, rinv, stream=None):
+    n = T * C
+    _check(lib().uniquan_add_rmsnorm(T, C, _p(X, n, _F, "X"), _p(A, n, _F, "A"), _p(gamma, C, _F, "gamma"),
+                                     _p(R, n, _F, "R"), _p(Z, n, _B, "Z"), _p(rinv, T, _F, "rinv"), _stream(stream)))
+
+
+def uniquan_rmsnorm_bwd(T, C, dZa, dZb, X, gamma, rinv, E, escale, dR, dRf=None, stream=None):
+    n = T * C
+    _check(lib().uniquan_rmsnorm_bwd(T, C, _p(dZa, n, _F, "dZa"), _p(dZb, n, _F, "dZb"), _p(X, n, _F, "X"),
+                                     _p(gamma, C, _F, "gamma"), _p(rinv, T, _F, "rinv"), _p(E, n, _B, "E"),
+                                     float(escale), _p(dR, n, _B, "dR"), _p(dRf, n, _F, "dRf"), _stream(stream)))
+
+
+def uniquan_rope_split(T, H, d, L, x, out, rotate=True, stream=None):
+    """Token-major x [T, H d] (fp32 or bf16) -> head-major bf16 out [H, T, d]."""
+    n = T * H * d
+    _check(lib().uniquan_rope_split(T, H, d, L, _p(x, n, _W, "in"), _dt(x), int(bool(rotate)),
+                                    _p(out, n, _B, "out"), _stream(stream)))
+
+
+def uniquan_rope_merge(T, H, d, L, x, out, rotate=True, stream=None):
+    """Head-major x [H, T, d] (fp32 or bf16) -> token-major bf16 out [T, H d]."""
+    n = T * H * d
+    _check(lib().uniquan_rope_merge(T, H, d, L, _p(x, n, _W, "in"), _dt(x), int(bool(rotate)),
+                                    _p(out, n, _B, "out"), _stream(stream)))
+
+
+def uniquan_softmax_causal(rows, L, S, P, stream=None):
+    n = rows * L
+    _check(lib().uniquan_softmax_causal(rows, L, _p(S, n, _F, "S"), _p(P, n, _B, "P"), _stream(stream)))
+
+
+def uniquan_softmax_causal_bwd(rows, L, dP, P, dS, stream=None):
+    n = rows * L
+    _check(lib().uniquan_softmax_causal_bwd(rows, L, _p(dP, n, _F, "dP"), _p(P, n, _B, "P"), _p(dS, n, _B, "dS"),
+                                            _stream(stream)))
+
+
+def uniquan_transpose_bf16_batched(batch, R, C, x, out, stream=None):
+    n = batch * R * C
+    _check(lib().uniquan_transpose_bf16_batched(batch, R, C, _p(x, n, _B, "in"), _p(out, n, _B, "out"),
+                                                _stream(stream)))
+
+
+def uniquan_block_loss_ws():
+    return int(lib().uniquan_block_loss_ws())
+
+
+def uniquan_block_loss(n, R, M, Yref, E, partials, loss, stream=None):
+    _check(lib().uniquan_block_loss(n, _p(R, n, _F, "R"), _p(M, n, _F, "M"), _p(Yref, n, _F, "Yref"),
+                                    _p(E, n, _B, "E"), _p(partials, None, _F, "partials"), partials.numel(),
+                                    _p(loss, 1, _F, "loss"), _stream(stream)))

@@ -224,9 +224,8 @@ def test_product_never_imports_oracle():
 def test_recorder_classifies_launches(L):
     launches = {n for n in uq._SIGS if uq._is_launch(n)}
     assert "uniquan_fq_fwd" in launches and "uniquan_gemm_nt" in launches and "uniquan_bcq_matmul" in launches
-    for n in ("uniquan_abi_version", "uniquan_last_error", "uniquan_recon_ws", "uniquan_bcq_matmul_ws"):
-        assert n not in launches
-    assert len(launches) == len(uq._SIGS) - 4
+    others = {n for n in uq._SIGS if n not in launches}
+    assert others == {"uniquan_abi_version", "uniquan_last_error"} | {n for n in uq._SIGS if n.endswith("_ws")}
 
 
 def test_replay_raises_on_error_status(L):
@@ -242,3 +241,29 @@ def test_record_propagates_and_resets(L):
     with pytest.raises(uq.UniquanError):
         uq.record(failing)
     assert uq._recorder is None and uq.lib() is uq._load()
+
+
+def test_decoder_entry_validation(L):
+    B, F = uq.UQ_BF16, uq.UQ_F32
+    g = L.uniquan_gemm_nt_batched
+    assert g(8, 8, 8, 0, FAKE, 64, FAKE, 64, FAKE, 64, F, 1.0, None) == uq.UQ_EINVAL
+    assert g(8, 8, 8, 70000, FAKE, 64, FAKE, 64, FAKE, 64, F, 1.0, None) == uq.UQ_EINVAL
+    assert g(8, 8, 8, 2, FAKE, 64, FAKE, 64, FAKE, 32, F, 1.0, None) == uq.UQ_EINVAL
+    assert "stride_out" in uq.last_error()
+    assert g(8, 8, 8, 2, FAKE, 4, FAKE, 64, FAKE, 64, F, 1.0, None) == uq.UQ_EINVAL
+    assert g(8, 12, 8, 2, FAKE, 64, FAKE, 96, FAKE, 96, F, 1.0, None) == uq.UQ_EINVAL
+    assert g(8, 8, 8, 2, ODD, 64, FAKE, 64, FAKE, 64, F, 1.0, None) == uq.UQ_EINVAL
+    assert L.uniquan_add_rmsnorm(4, 12, FAKE, None, FAKE, None, FAKE, FAKE, None) == uq.UQ_EINVAL
+    assert L.uniquan_add_rmsnorm(4, 16, FAKE, FAKE, FAKE, None, FAKE, FAKE, None) == uq.UQ_EINVAL
+    assert "R must be given" in uq.last_error()
+    assert L.uniquan_rmsnorm_bwd(4, 16, None, None, FAKE, FAKE, FAKE, None, 2.0, FAKE, None, None) == uq.UQ_EINVAL
+    assert L.uniquan_rope_split(6, 2, 4, 4, FAKE, F, 1, FAKE, None) == uq.UQ_EINVAL       # L does not divide T
+    assert L.uniquan_rope_split(6, 2, 3, 3, FAKE, F, 1, FAKE, None) == uq.UQ_EINVAL       # odd d
+    assert L.uniquan_rope_merge(6, 2, 4, 3, FAKE, 9, 1, FAKE, None) == uq.UQ_EINVAL       # bad dtype
+    assert L.uniquan_softmax_causal(10, 4, FAKE, FAKE, None) == uq.UQ_EINVAL
+    assert L.uniquan_softmax_causal_bwd(8, 4, FAKE, None, FAKE, None) == uq.UQ_EINVAL
+    assert L.uniquan_transpose_bf16_batched(0, 4, 4, FAKE, FAKE, None) == uq.UQ_EINVAL
+    ws = uq.uniquan_block_loss_ws()
+    assert ws >= 1
+    assert L.uniquan_block_loss(16, FAKE, FAKE, FAKE, FAKE, FAKE, ws - 1, FAKE, None) == uq.UQ_EINVAL
+    assert L.uniquan_block_loss(0, FAKE, FAKE, FAKE, FAKE, FAKE, ws, FAKE, None) == uq.UQ_EINVAL

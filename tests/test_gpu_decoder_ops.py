@@ -1,0 +1,189 @@
+"""GPU parity of the decoder-block operations (csrc/block_attn.hip and the
+strided-batch GEMM) against oracle/block_decoder.py and plain definitions,
+on seeded inputs generated here (never from device output).  Bars: layout
+moves and fp32 adds bit-exact; bf16 outputs within one rounding (2^-8
+relative) of the fp64 value plus the fp32 arithmetic before it; fp32 outputs
+within 1e-5 of the row's scale."""
+import numpy as np
+import pytest
+import torch
+
+import oracle.block_decoder as D
+import oracle.uniquan as O
+from paper_2506_03781_amd import uniquan as uq
+
+pytestmark = pytest.mark.gpu
+F32 = np.float32
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    uq.lib()
+    torch.cuda.set_device(0)
+
+
+def dev(a, dtype):
+    return torch.from_numpy(np.ascontiguousarray(np.asarray(a, F32))).to("cuda").to(dtype).contiguous()
+
+
+def host(t):
+    return (t.float() if t.dtype == torch.bfloat16 else t).cpu().numpy().astype(np.float64)
+
+
+def bfr(a):
+    return O.bf16_rne(np.asarray(a, F32)).astype(np.float64)
+
+
+def within_bf16(x, ref, floor=0.0, what="", rel=1e-5):
+    """One bf16 rounding (2^-8 relative) on top of fp32 arithmetic (rel)."""
+    err = np.abs(x - ref)
+    lim = (2.0 ** -8 + rel) * np.abs(ref) + floor + 1e-30
+    assert np.all(err <= lim), (what, float(np.max(err / lim)))
+
+
+@pytest.mark.parametrize("M,N,K,batch,sa,sb", [(64, 64, 32, 5, 1, 1), (200, 264, 128, 3, 1, 0),
+                                              (2048 // 4, 512, 128, 8, 1, 1), (256, 256, 96, 4, 1, 1)])
+def test_gemm_nt_batched(M, N, K, batch, sa, sb):
+    rs = np.random.default_rng(M + N + K + batch)
+    A = bfr(rs.standard_normal((batch, M, K)))
+    B = bfr(rs.standard_normal((batch, N, K)))
+    if sb == 0:
+        B[1:] = B[0]
+    dA, dB = dev(A, torch.bfloat16), dev(B if sb else B[:1], torch.bfloat16)
+    out = torch.empty(batch, M, N, device="cuda")
+    uq.uniquan_gemm_nt_batched(M, N, K, batch, dA, M * K, dB, N * K * sb, out, M * N, 0.5)
+    single = torch.empty(M, N, device="cuda")
+    torch.cuda.synchronize()
+    got = host(out)
+    for b in range(batch):
+        ref = 0.5 * A[b] @ B[b].T
+        mag = 0.5 * np.abs(A[b]) @ np.abs(B[b]).T
+        assert np.all(np.abs(got[b] - ref) <= 1e-5 * mag), b
+        uq.uniquan_gemm_nt(M, N, K, dA[b], dB[b if sb else 0], single, 0.5)
+        torch.cuda.synchronize()
+        assert np.array_equal(host(single), got[b]), b   # the batch is the same kernel on each slice
+
+
+@pytest.mark.parametrize("T,C", [(5, 8), (37, 264), (64, 4096)])
+def test_add_rmsnorm(T, C):
+    rs = np.random.default_rng(T * C)
+    X = rs.standard_normal((T, C)).astype(F32)
+    A = (0.5 * rs.standard_normal((T, C))).astype(F32)
+    g = (1.0 + 0.2 * rs.standard_normal(C)).astype(F32)
+    R, Z, r = torch.empty(T, C, device="cuda"), torch.empty(T, C, dtype=torch.bfloat16, device="cuda"), \
+        torch.empty(T, device="cuda")
+    uq.uniquan_add_rmsnorm(T, C, dev(X, torch.float32), dev(A, torch.float32), dev(g, torch.float32), R, Z, r)
+    torch.cuda.synchronize()
+    v = (X + A).astype(F32)
+    assert np.array_equal(host(R), v.astype(np.float64))
+    zref, rref = D.rmsnorm(v.astype(np.float64), g.astype(np.float64))
+    assert np.allclose(host(r), rref[:, 0], rtol=1e-5)
+    within_bf16(host(Z), zref, 1e-6 * np.abs(zref).max(), "Z")
+    Z2, r2 = torch.empty_like(Z), torch.empty_like(r)
+    uq.uniquan_add_rmsnorm(T, C, dev(X, torch.float32), None, dev(g, torch.float32), None, Z2, r2)
+    torch.cuda.synchronize()
+    zref2, _ = D.rmsnorm(X.astype(np.float64), g.astype(np.float64))
+    within_bf16(host(Z2), zref2, 1e-6 * np.abs(zref2).max(), "Z without A")
+
+
+@pytest.mark.parametrize("T,C", [(7, 16), (33, 512)])
+def test_rmsnorm_bwd(T, C):
+    rs = np.random.default_rng(T + C)
+    X = rs.standard_normal((T, C))
+    g = 1.0 + 0.2 * rs.standard_normal(C)
+    dZa, dZb = rs.standard_normal((T, C)), rs.standard_normal((T, C))
+    E = bfr(rs.standard_normal((T, C)))
+    _, rref = D.rmsnorm(X, g)
+    r32 = rref[:, 0].astype(F32)
+    dR = torch.empty(T, C, dtype=torch.bfloat16, device="cuda")
+    dRf = torch.empty(T, C, device="cuda")
+    uq.uniquan_rmsnorm_bwd(T, C, dev(dZa, torch.float32), dev(dZb, torch.float32), dev(X, torch.float32),
+                           dev(g, torch.float32), dev(r32, torch.float32), dev(E, torch.bfloat16), 2.0, dR, dRf)
+    torch.cuda.synchronize()
+    ref = 2.0 * E + D.rmsnorm_bwd(dZa.astype(F32).astype(np.float64) + dZb.astype(F32).astype(np.float64),
+                                  X.astype(F32).astype(np.float64), g.astype(F32).astype(np.float64),
+                                  r32.astype(np.float64)[:, None])
+    scale = np.max(np.abs(ref), axis=1, keepdims=True)
+    assert np.all(np.abs(host(dRf) - ref) <= 1e-5 * scale)
+    within_bf16(host(dR), ref, 1e-5 * scale, "dR")
+
+
+@pytest.mark.parametrize("n_seq,L,H,d", [(2, 5, 3, 8), (2, 64, 4, 128)])
+def test_rope_split_merge(n_seq, L, H, d):
+    T, C = n_seq * L, H * d
+    rs = np.random.default_rng(L * H)
+    x = rs.standard_normal((T, C)).astype(F32)
+    out = torch.empty(H, T, d, dtype=torch.bfloat16, device="cuda")
+    uq.uniquan_rope_split(T, H, d, L, dev(x, torch.float32), out, rotate=True)
+    torch.cuda.synchronize()
+    ang = D.rope_angles(L, d)
+    ref = D.rope(D.split_heads(x.astype(np.float64), n_seq, H), ang)     # [n_seq, H, L, d]
+    ref_hm = ref.transpose(1, 0, 2, 3).reshape(H, T, d)
+    within_bf16(host(out), ref_hm, 2e-6 * np.abs(ref_hm).max(), "rope split")
+    # inverse rotation on fp32 head-major input, merged back to token-major
+    y = rs.standard_normal((H, T, d)).astype(F32)
+    back = torch.empty(T, C, dtype=torch.bfloat16, device="cuda")
+    uq.uniquan_rope_merge(T, H, d, L, dev(y, torch.float32), back, rotate=True)
+    torch.cuda.synchronize()
+    yin = y.astype(np.float64).reshape(H, n_seq, L, d).transpose(1, 0, 2, 3)
+    ref_back = D.merge_heads(D.rope(yin, ang, inverse=True))
+    within_bf16(host(back), ref_back, 2e-6 * np.abs(ref_back).max(), "rope merge")
+    # no rotation: pure layout moves of bf16 data, bit-exact round trip
+    xb = bfr(x)
+    hm = torch.empty(H, T, d, dtype=torch.bfloat16, device="cuda")
+    tm = torch.empty(T, C, dtype=torch.bfloat16, device="cuda")
+    uq.uniquan_rope_split(T, H, d, L, dev(xb, torch.bfloat16), hm, rotate=False)
+    uq.uniquan_rope_merge(T, H, d, L, hm, tm, rotate=False)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(hm), xb.reshape(T, H, d).transpose(1, 0, 2))
+    assert np.array_equal(host(tm), xb)
+
+
+@pytest.mark.parametrize("B,L", [(3, 7), (4, 130), (2, 2048)])
+def test_softmax_causal(B, L):
+    rs = np.random.default_rng(B * L)
+    S = (3.0 * rs.standard_normal((B, L, L))).astype(F32)
+    P = torch.empty(B, L, L, dtype=torch.bfloat16, device="cuda")
+    uq.uniquan_softmax_causal(B * L, L, dev(S, torch.float32), P)
+    torch.cuda.synchronize()
+    ref = D.causal_softmax(S.astype(np.float64))
+    got = host(P)
+    assert np.all(got[:, np.triu_indices(L, 1)[0], np.triu_indices(L, 1)[1]] == 0.0)
+    within_bf16(got, ref, 1e-6, "P")
+    # backward on a probability matrix and upstream gradient generated here
+    Pin = bfr(ref)
+    dP = rs.standard_normal((B, L, L)).astype(F32)
+    dS = torch.empty_like(P)
+    uq.uniquan_softmax_causal_bwd(B * L, L, dev(dP, torch.float32), dev(Pin, torch.bfloat16), dS)
+    torch.cuda.synchronize()
+    mask = np.tril(np.ones((L, L)))
+    dpm = dP.astype(np.float64) * mask
+    ref_ds = Pin * (dpm - np.sum(Pin * dpm, axis=-1, keepdims=True))
+    # the fp32 row dot product errs by ~1e-5 of the row's largest |dP|; dS carries it times P
+    scale = np.max(np.abs(dpm), axis=-1, keepdims=True)
+    within_bf16(host(dS), ref_ds, 1e-5 * scale * Pin + 1e-7, "dS")
+
+
+@pytest.mark.parametrize("B,R,C", [(1, 5, 7), (3, 64, 130), (2, 300, 64)])
+def test_transpose_batched(B, R, C):
+    x = bfr(np.random.default_rng(R * C).standard_normal((B, R, C)))
+    out = torch.empty(B, C, R, dtype=torch.bfloat16, device="cuda")
+    uq.uniquan_transpose_bf16_batched(B, R, C, dev(x, torch.bfloat16), out)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(out), x.transpose(0, 2, 1))
+
+
+@pytest.mark.parametrize("n", [8, 1000, 3 * 2 ** 20 + 24])
+def test_block_loss(n):
+    rs = np.random.default_rng(n)
+    R, M, Y = (rs.standard_normal(n).astype(F32) for _ in range(3))
+    E = torch.empty(n, dtype=torch.bfloat16, device="cuda")
+    part = torch.empty(uq.uniquan_block_loss_ws(), device="cuda")
+    loss = torch.zeros(1, device="cuda")
+    uq.uniquan_block_loss(n, dev(R, torch.float32), dev(M, torch.float32), dev(Y, torch.float32), E, part, loss)
+    torch.cuda.synchronize()
+    e = ((R + M) - Y).astype(F32)
+    assert np.array_equal(host(E), bfr(e))
+    ref = float(np.sum(e.astype(np.float64) ** 2))
+    assert abs(float(loss.item()) - ref) <= 1e-5 * ref
