@@ -123,3 +123,164 @@ class MLPBlock:
         self.forward_backward(mode)
         for q in (self.gate, self.up, self.down):
             q.fq_bwd_sgd(lr_f, lr_b, keep_grads)
+
+
+class DecoderBlock:
+    """One whole Transformer block (Algorithm 1 with f = one multi-head
+    attention module and one MLP module): pre-norm, rotary causal attention
+    over n_seq sequences of L = T / n_seq tokens with H heads of d = C / H,
+    and the SiLU-gated MLP.  The seven matrices are QuantMatrix objects
+    (q, k, v, o [C, C]; g, u [I, C]; d [C, I]); g1, g2 are the norms'
+    weights (not trained).
+
+    ``prepare(X)`` computes the full-precision block's output on the
+    full-precision input X (the target); ``set_input(Xhat)`` gives the
+    quantized block its input (the output of the preceding quantized blocks;
+    X itself for the first block).  ``step`` is one reconstruction step on
+    the quantized block: fake-quant, forward on What, the loss, the
+    backpropagation to all seven matrices, and the straight-through backward
+    with the SGD update.  ``output()`` is the quantized block's output on
+    its input, the next block's Xhat.
+    """
+
+    NAMES = ("q", "k", "v", "o", "g", "u", "d")
+
+    def __init__(self, mats: dict, g1, g2, T, n_seq, H, device="cuda"):
+        q, gm = mats["q"], mats["g"]
+        C, I = q.C, gm.R
+        assert C % H == 0 and T % n_seq == 0
+        self.mats, self.T, self.C, self.I, self.H, self.n_seq = mats, T, C, I, H, n_seq
+        self.d, self.L = C // H, T // n_seq
+        self.B = H * n_seq
+        T, L, d, B = self.T, self.L, self.d, self.B
+        f32 = dict(dtype=torch.float32, device=device)
+        b16 = dict(dtype=torch.bfloat16, device=device)
+        e = torch.empty
+        self.g1 = to_dev(g1, torch.float32, device)
+        self.g2 = to_dev(g2, torch.float32, device)
+        self.Xhat, self.Yref, self.A32, self.R, self.M32, self.Yhat = (e(T, C, **f32) for _ in range(6))
+        self.Qf, self.Kf, self.dZa, self.dZb = (e(T, C, **f32) for _ in range(4))
+        self.r1, self.r2 = e(T, **f32), e(T, **f32)
+        (self.Z1, self.Vb, self.O, self.Z2, self.E, self.dA, self.dO, self.dQ, self.dK,
+         self.dV) = (e(T, C, **b16) for _ in range(10))
+        (self.Z1t, self.Ot, self.Z2t, self.Et, self.dAt, self.dQt, self.dKt,
+         self.dVt) = (e(C, T, **b16) for _ in range(8))
+        self.Qh, self.Kh, self.Vh, self.Oh, self.dOh, self.dVh = (e(B, L, d, **b16) for _ in range(6))
+        self.Qt, self.Kt, self.Vt, self.dOt = (e(B, d, L, **b16) for _ in range(4))
+        self.dQr, self.dKr = e(B, L, d, **f32), e(B, L, d, **f32)
+        self.S, self.dP = e(B, L, L, **f32), e(B, L, L, **f32)
+        self.P, self.Pt, self.dS, self.dSt = (e(B, L, L, **b16) for _ in range(4))
+        self.Gt, self.Ut, self.Ht, self.dHt, self.dGt, self.dUt = (e(I, T, **b16) for _ in range(6))
+        self.Hm, self.dG, self.dU = (e(T, I, **b16) for _ in range(3))
+        self.WdT = e(I, C, **b16)
+        self.WgT, self.WuT = e(C, I, **b16), e(C, I, **b16)
+        self.WoT = e(C, C, **b16)
+        self.partials = e(uq.uniquan_block_loss_ws(), **f32)
+        self.loss = torch.zeros(1, **f32)
+        self._rinv_tmp = e(T, **f32)
+        self._z_tmp = e(T, C, **b16)
+
+    # ---- forward on weights W (dict of bf16 [R, C] tensors) and fp32 input X
+    def _forward(self, W, X):
+        T, C, I, H, d, L, B = self.T, self.C, self.I, self.H, self.d, self.L, self.B
+        sc = 1.0 / float(d) ** 0.5
+        uq.uniquan_add_rmsnorm(T, C, X, None, self.g1, None, self.Z1, self.r1)
+        uq.uniquan_gemm_nt(T, C, C, self.Z1, W["q"], self.Qf)
+        uq.uniquan_gemm_nt(T, C, C, self.Z1, W["k"], self.Kf)
+        uq.uniquan_gemm_nt(T, C, C, self.Z1, W["v"], self.Vb)
+        uq.uniquan_rope_split(T, H, d, L, self.Qf, self.Qh, rotate=True)
+        uq.uniquan_rope_split(T, H, d, L, self.Kf, self.Kh, rotate=True)
+        uq.uniquan_rope_split(T, H, d, L, self.Vb, self.Vh, rotate=False)
+        uq.uniquan_gemm_nt_batched(L, L, d, B, self.Qh, L * d, self.Kh, L * d, self.S, L * L, sc)
+        uq.uniquan_softmax_causal(B * L, L, self.S, self.P)
+        uq.uniquan_transpose_bf16_batched(B, L, d, self.Vh, self.Vt)
+        uq.uniquan_gemm_nt_batched(L, d, L, B, self.P, L * L, self.Vt, d * L, self.Oh, L * d)
+        uq.uniquan_rope_merge(T, H, d, L, self.Oh, self.O, rotate=False)
+        uq.uniquan_gemm_nt(T, C, C, self.O, W["o"], self.A32)
+        uq.uniquan_add_rmsnorm(T, C, X, self.A32, self.g2, self.R, self.Z2, self.r2)
+        uq.uniquan_gemm_nt(I, T, C, W["g"], self.Z2, self.Gt)
+        uq.uniquan_gemm_nt(I, T, C, W["u"], self.Z2, self.Ut)
+        uq.uniquan_silu_mul_fwd(self.Gt, self.Ut, self.Ht)
+        uq.uniquan_transpose_bf16(I, T, self.Ht, self.Hm)
+        uq.uniquan_gemm_nt(T, C, I, self.Hm, W["d"], self.M32)
+
+    def _sum_out(self, out):
+        """out = R + M (fp32), through the residual-add path of the norm kernel."""
+        uq.uniquan_add_rmsnorm(self.T, self.C, self.R, self.M32, self.g2, out, self._z_tmp, self._rinv_tmp)
+
+    def prepare(self, X):
+        """Target: the full-precision block's output on the full-precision input X [T, C]."""
+        Xd = X if isinstance(X, torch.Tensor) else to_dev(X, torch.float32)
+        self._forward({n: m.W for n, m in self.mats.items()}, Xd.float().contiguous())
+        self._sum_out(self.Yref)
+
+    def set_input(self, Xhat):
+        Xd = Xhat if isinstance(Xhat, torch.Tensor) else to_dev(Xhat, torch.float32)
+        self.Xhat.copy_(Xd.float())
+
+    def forward_backward(self, mode):
+        T, C, I, H, d, L, B = self.T, self.C, self.I, self.H, self.d, self.L, self.B
+        sc = 1.0 / float(d) ** 0.5
+        m = self.mats
+        for q in m.values():
+            q.fq_fwd(mode)
+        Wh = {n: q.W_hat for n, q in m.items()}
+        self._forward(Wh, self.Xhat)
+        uq.uniquan_block_loss(T * C, self.R, self.M32, self.Yref, self.E, self.partials, self.loss)
+        # MLP module (dY = 2 E)
+        uq.uniquan_transpose_bf16(T, C, self.E, self.Et)
+        uq.uniquan_gemm_nt(C, I, T, self.Et, self.Ht, m["d"].G, 2.0)
+        uq.uniquan_transpose_bf16(C, I, Wh["d"], self.WdT)
+        uq.uniquan_gemm_nt(I, T, C, self.WdT, self.E, self.dHt, 2.0)
+        uq.uniquan_silu_mul_bwd(self.dHt, self.Gt, self.Ut, self.dGt, self.dUt)
+        uq.uniquan_transpose_bf16(T, C, self.Z2, self.Z2t)
+        uq.uniquan_gemm_nt(I, C, T, self.dGt, self.Z2t, m["g"].G)
+        uq.uniquan_gemm_nt(I, C, T, self.dUt, self.Z2t, m["u"].G)
+        uq.uniquan_transpose_bf16(I, T, self.dGt, self.dG)
+        uq.uniquan_transpose_bf16(I, T, self.dUt, self.dU)
+        uq.uniquan_transpose_bf16(I, C, Wh["g"], self.WgT)
+        uq.uniquan_transpose_bf16(I, C, Wh["u"], self.WuT)
+        uq.uniquan_gemm_nt(T, C, I, self.dG, self.WgT, self.dZa)
+        uq.uniquan_gemm_nt(T, C, I, self.dU, self.WuT, self.dZb)
+        # second norm and residual: dR = 2 E + RMSNorm backward
+        uq.uniquan_rmsnorm_bwd(T, C, self.dZa, self.dZb, self.R, self.g2, self.r2, self.E, 2.0, self.dA)
+        # attention module
+        uq.uniquan_transpose_bf16(T, C, self.dA, self.dAt)
+        uq.uniquan_transpose_bf16(T, C, self.O, self.Ot)
+        uq.uniquan_gemm_nt(C, C, T, self.dAt, self.Ot, m["o"].G)
+        uq.uniquan_transpose_bf16(C, C, Wh["o"], self.WoT)
+        uq.uniquan_gemm_nt(T, C, C, self.dA, self.WoT, self.dO)
+        uq.uniquan_rope_split(T, H, d, L, self.dO, self.dOh, rotate=False)
+        uq.uniquan_gemm_nt_batched(L, L, d, B, self.dOh, L * d, self.Vh, L * d, self.dP, L * L)
+        uq.uniquan_softmax_causal_bwd(B * L, L, self.dP, self.P, self.dS)
+        uq.uniquan_transpose_bf16_batched(B, L, d, self.Kh, self.Kt)
+        uq.uniquan_gemm_nt_batched(L, d, L, B, self.dS, L * L, self.Kt, d * L, self.dQr, L * d, sc)
+        uq.uniquan_transpose_bf16_batched(B, L, L, self.dS, self.dSt)
+        uq.uniquan_transpose_bf16_batched(B, L, d, self.Qh, self.Qt)
+        uq.uniquan_gemm_nt_batched(L, d, L, B, self.dSt, L * L, self.Qt, d * L, self.dKr, L * d, sc)
+        uq.uniquan_transpose_bf16_batched(B, L, L, self.P, self.Pt)
+        uq.uniquan_transpose_bf16_batched(B, L, d, self.dOh, self.dOt)
+        uq.uniquan_gemm_nt_batched(L, d, L, B, self.Pt, L * L, self.dOt, d * L, self.dVh, L * d)
+        uq.uniquan_rope_merge(T, H, d, L, self.dQr, self.dQ, rotate=True)
+        uq.uniquan_rope_merge(T, H, d, L, self.dKr, self.dK, rotate=True)
+        uq.uniquan_rope_merge(T, H, d, L, self.dVh, self.dV, rotate=False)
+        uq.uniquan_transpose_bf16(T, C, self.Z1, self.Z1t)
+        for g, src, dst in (("q", self.dQ, self.dQt), ("k", self.dK, self.dKt), ("v", self.dV, self.dVt)):
+            uq.uniquan_transpose_bf16(T, C, src, dst)
+            uq.uniquan_gemm_nt(C, C, T, dst, self.Z1t, m[g].G)
+
+    def step(self, mode=uq.MAP_FULL, lr_f=0.005, lr_b=0.0005, keep_grads=False):
+        self.forward_backward(mode)
+        for q in self.mats.values():
+            q.fq_bwd_sgd(lr_f, lr_b, keep_grads)
+
+    def output(self):
+        """The quantized block's output on its input (fp32 [T, C]): the next
+        block's Xhat.  The weights are the finished quantization's, i.e. the
+        canonical FULL mapping with the current parameters (what the fold of
+        Theorem 1 stores), so this ends the block's optimisation."""
+        for q in self.mats.values():
+            q.fq_fwd(uq.MAP_FULL)
+        self._forward({n: q.W_hat for n, q in self.mats.items()}, self.Xhat)
+        self._sum_out(self.Yhat)
+        return self.Yhat

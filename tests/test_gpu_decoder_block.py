@@ -1,0 +1,161 @@
+"""GPU parity of block-level reconstruction for a whole Transformer block
+(paper_2506_03781_amd/block.py DecoderBlock) against
+oracle/block_decoder.py.
+
+Seeded inputs: the seven matrices from the generator's 7B block recipe at a
+small shape (C = 256 in 2 heads of 128, I = 384, two sequences of 64
+tokens), norm weights 1 + 0.1 N(0, 1), quantizer parameters from the
+oracle's fixed-minimum clipping with a greedy start.  The oracle evaluates
+the block in fp64 with the device's bf16 storage points and never sees
+device output.  Bars: codes bit-exact per matrix; the loss within 1e-2;
+dL/dWhat of all seven matrices within 1e-2 normwise.  Per element the bar is
+0.1 of max(|x|, rms): the residual E = Yhat - Y_ref is a small difference of
+large values and each side rounds its bf16 intermediates (and its target)
+independently, so single elements of E, and of the gradients summed from
+them, differ by several percent where the attention is sharp; the
+per-element check still catches a misplaced or transposed gradient.  The chained test gives the second block the first
+quantized block's output as its input (Algorithm 1 run from the bottom
+block up), each side computing that input itself.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle.block_decoder as D
+import oracle.uniquan as O
+from paper_2506_03781_amd import synth
+from paper_2506_03781_amd import uniquan as uq
+from paper_2506_03781_amd.block import DecoderBlock, QuantMatrix
+
+pytestmark = pytest.mark.gpu
+
+F32 = np.float32
+N_SEQ, L, C, H, I, K, G = 2, 64, 256, 2, 384, 3, 128
+T = N_SEQ * L
+SHAPES = {"q": (C, C), "k": (C, C), "v": (C, C), "o": (C, C), "g": (I, C), "u": (I, C), "d": (C, I)}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    uq.lib()
+    torch.cuda.set_device(0)
+
+
+def host(t):
+    return (t.float() if t.dtype == torch.bfloat16 else t).cpu().numpy().astype(np.float64)
+
+
+def close(x, ref, tol=1e-2, elem=0.1, what=""):
+    x, ref = np.asarray(x, np.float64), np.asarray(ref, np.float64)
+    nrm = np.linalg.norm(ref)
+    assert np.linalg.norm(x - ref) <= tol * max(nrm, 1e-30), f"{what}: normwise {np.linalg.norm(x - ref) / nrm}"
+    rms = np.sqrt(np.mean(ref * ref))
+    ratio = np.abs(x - ref) / np.maximum(np.abs(ref), rms)
+    assert np.all(ratio <= elem), f"{what}: {(ratio > elem).sum()} of {ratio.size} elements, worst {ratio.max():.3g}"
+
+
+def make_block(seed, qk_scale=1.0):
+    specs = synth.WORKLOADS["block7b"].matrices
+    mats, X = {}, None
+    for name, spec in zip(SHAPES, specs):
+        R_, C_ = SHAPES[name]
+        m = synth.make_matrix(synth.scaled(spec, R=R_, C=C_, T=T), seed)
+        if X is None:
+            X = m.X.astype(F32)
+        W = m.W
+        if name in ("q", "k") and qk_scale != 1.0:       # sharper attention: scores of order 1-10
+            W = O.bf16_rne((np.asarray(W, F32) * F32(qk_scale)).astype(F32))
+        mats[name] = (W, m.s, O.init_param_set_b(W, m.s, K, G))
+    rs = np.random.default_rng(seed + 1000)
+    g1 = (1.0 + 0.1 * rs.standard_normal(C)).astype(F32)
+    g2 = (1.0 + 0.1 * rs.standard_normal(C)).astype(F32)
+    return X, mats, g1, g2
+
+
+def device_block(mats, g1, g2):
+    qs = {n: QuantMatrix(W, s, K, G, p["delta"], p["z_u"], p["s_r"], p["z_b"], p["alpha"])
+          for n, (W, s, p) in mats.items()}
+    return DecoderBlock(qs, g1, g2, T, N_SEQ, H), qs
+
+
+def oracle_what(mats, mode=O.MAP_FULL):
+    out = {}
+    for n, (W, s, p) in mats.items():
+        out[n] = O.fq_fwd(W, s, p["alpha"], p["z_b"], K, G, p["s_r"], p["delta"], p["z_u"], mode, None)
+    return out
+
+
+def wfp(mats):
+    return {n: np.asarray(W, np.float64) for n, (W, _, _) in mats.items()}
+
+
+@pytest.mark.parametrize("qk_scale", [1.0, 6.0])
+def test_decoder_block_step(qk_scale):
+    X, mats, g1, g2 = make_block(3, qk_scale)
+    blk, qs = device_block(mats, g1, g2)
+    blk.prepare(X)
+    blk.set_input(X)
+    blk.forward_backward(uq.MAP_FULL)
+    torch.cuda.synchronize()
+
+    f = oracle_what(mats)
+    for n in mats:
+        assert np.array_equal(host(qs[n].codes).reshape(SHAPES[n]).astype(np.uint8), f[n]["codes"]), f"{n} codes"
+    Y_ref = D.decoder_forward(X, wfp(mats), g1, g2, N_SEQ, H, store=O.bf16_rne)["Y"]
+    assert np.allclose(host(blk.Yref), Y_ref, rtol=2e-2, atol=2e-2 * np.abs(Y_ref).max())
+    st = D.decoder_step(X, Y_ref, {n: f[n]["what_bf16"] for n in mats}, g1, g2, N_SEQ, H, store=O.bf16_rne)
+    if qk_scale > 1.0:   # the attention is far from uniform
+        assert np.mean(np.max(st["P"][..., 8:, :], axis=-1)) > 0.3
+    loss = float(blk.loss.item())
+    assert abs(loss - st["loss"]) <= 1e-2 * st["loss"], (loss, st["loss"])
+    for n in mats:
+        close(host(qs[n].G), st["grads"][n], what=f"dL/dWhat_{n}")
+
+
+def test_decoder_blocks_chained():
+    """Block 2 runs on the quantized block 1's output (Xhat) against the
+    full-precision block 1's output (X), as in the bottom-up order."""
+    X, m1, g1a, g2a = make_block(5)
+    _, m2, g1b, g2b = make_block(6)
+    b1, _ = device_block(m1, g1a, g2a)
+    b1.prepare(X)
+    b1.set_input(X)
+    xhat2 = b1.output().clone()
+    x2 = b1.Yref.clone()
+    b2, q2 = device_block(m2, g1b, g2b)
+    b2.prepare(x2)
+    b2.set_input(xhat2)
+    b2.forward_backward(uq.MAP_FULL)
+    torch.cuda.synchronize()
+
+    f1 = oracle_what(m1)
+    x2_o = D.decoder_forward(X, wfp(m1), g1a, g2a, N_SEQ, H, store=O.bf16_rne)["Y"]
+    xhat2_o = D.decoder_forward(X, {n: f1[n]["what_bf16"] for n in m1}, g1a, g2a, N_SEQ, H, store=O.bf16_rne)["Y"]
+    close(host(xhat2), xhat2_o, tol=1e-3, elem=2e-2, what="Xhat of block 2")
+    assert not np.allclose(xhat2_o, x2_o)          # the quantized path's input differs from the full-precision one
+    f2 = oracle_what(m2)
+    Y2_ref = D.decoder_forward(x2_o, wfp(m2), g1b, g2b, N_SEQ, H, store=O.bf16_rne)["Y"]
+    st = D.decoder_step(xhat2_o, Y2_ref, {n: f2[n]["what_bf16"] for n in m2}, g1b, g2b, N_SEQ, H,
+                        store=O.bf16_rne)
+    assert abs(float(b2.loss.item()) - st["loss"]) <= 1e-2 * st["loss"]
+    for n in m2:
+        close(host(q2[n].G), st["grads"][n], what=f"block 2 dL/dWhat_{n}")
+
+
+def test_decoder_block_step_updates():
+    """A FULL step then LOCAL steps with the SGD update: the loss stays finite
+    and the straight-through backward of every matrix ran (parameters moved)."""
+    X, mats, g1, g2 = make_block(8)
+    blk, qs = device_block(mats, g1, g2)
+    blk.prepare(X)
+    blk.set_input(X)
+    s0 = {n: q.s.clone() for n, q in qs.items()}
+    losses = []
+    for i, mode in enumerate((uq.MAP_FULL, uq.MAP_LOCAL, uq.MAP_LOCAL)):
+        blk.step(mode, 1e-4, 1e-5)
+        losses.append(float(blk.loss.item()))
+    torch.cuda.synchronize()
+    assert all(np.isfinite(losses)) and losses[0] > 0
+    for n, q in qs.items():
+        assert not torch.equal(q.s, s0[n]), n
