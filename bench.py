@@ -118,7 +118,7 @@ def parse():
     ap.add_argument("--target", action="store_true",
                     help="loss against a stored fp32 target Y = X W^T instead of the residual form")
     ap.add_argument("--no-block", action="store_true",
-                    help="skip the block-level step on the 7B MLP module (gate/up/down 11008x4096, 4096 tokens)")
+                    help="skip the block-level step on a 7B decoder block (8192 tokens, 32 heads, I = 11008)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run a plain 256 MiB device copy (counter calibration)")
     return ap.parse_args()
@@ -288,34 +288,40 @@ def bcq_inference(layers, batches=(1, 8), target_bytes=512 << 20):
     return res
 
 
-def block_mlp(seed, k=3, steps=10, warmup=2):
-    """Block-level reconstruction of a 7B MLP module (Algorithm 1 with the
-    SiLU-gated gate/up/down as f): per step the three fake-quant forwards,
-    the module's forward on What, the loss, backpropagation to all three
-    matrices and the straight-through backward with the SGD update.  Seven
-    GEMMs of 2 T C I flops each carry the step."""
+def block_decoder(seed, k=3, steps=5, warmup=2):
+    """Block-level reconstruction of a 7B decoder block (Algorithm 1 with f =
+    one rotary causal attention module and one SiLU-gated MLP module): per
+    step the seven fake-quant forwards, the block's forward on What, the
+    loss, backpropagation to all seven matrices and the straight-through
+    backward with the SGD update.  8192 tokens as 4 sequences of 2048,
+    C = 4096 in 32 heads of 128, I = 11008."""
+    import numpy as np
     import torch
 
     from paper_2506_03781_amd import synth
     from paper_2506_03781_amd import uniquan as uq
-    from paper_2506_03781_amd.block import MLPBlock, QuantMatrix
-    wl = synth.WORKLOADS["mlp7b"]
+    from paper_2506_03781_amd.block import DecoderBlock, QuantMatrix
+    wl = synth.WORKLOADS["block7b"]
     g = wl.group_size
-    qs, X = [], None
-    for spec in wl.matrices:
-        m = synth.make_matrix(spec, seed)
+    n_seq, H = 4, 32
+    mats, X = {}, None
+    for name, spec in zip(DecoderBlock.NAMES, wl.matrices):
+        # only the first matrix's activations are used; the weights do not depend on T
+        m = synth.make_matrix(spec if X is None else synth.scaled(spec, T=8), seed)
         if X is None:
             X = m.X
         q = QuantMatrix(m.W, m.s, k, g)
         q.init_unified()
-        qs.append(q)
+        mats[name] = q
         del m
-    blk = MLPBlock(X, *qs)
-    blk.prepare()
-    T, C, I = blk.T, blk.C, blk.I
-    # SGD on L / L0, the loss relative to its value at the initialisation (one
-    # step with zero learning rates measures L0): the sum's gradients grow
-    # with the block's size and output scale, the relative loss's do not
+    rs = np.random.default_rng(seed + 1000)
+    C = mats["q"].C
+    g1 = (1.0 + 0.1 * rs.standard_normal(C)).astype(np.float32)
+    g2 = (1.0 + 0.1 * rs.standard_normal(C)).astype(np.float32)
+    blk = DecoderBlock(mats, g1, g2, X.shape[0], n_seq, H)
+    blk.prepare(X)
+    blk.set_input(X)
+    # SGD on L / L0 (one step with zero learning rates measures L0)
     blk.step(uq.MAP_FULL, 0.0, 0.0)
     l0 = float(blk.loss.item())
     lr_f, lr_b = 0.005 / l0, 0.0005 / l0
@@ -323,7 +329,6 @@ def block_mlp(seed, k=3, steps=10, warmup=2):
     for i in range(warmup):
         blk.step(uq.MAP_FULL if i == 0 else uq.MAP_LOCAL, lr_f, lr_b)
         rel.append(float(blk.loss.item()) / l0)
-    # the LOCAL step's launches, recorded once (that run is one more step)
     step_local = uq.record(blk.step, uq.MAP_LOCAL, lr_f, lr_b)
     torch.cuda.synchronize()
     e0, e1 = TimingEvent(), TimingEvent()
@@ -334,39 +339,34 @@ def block_mlp(seed, k=3, steps=10, warmup=2):
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / steps
     # one instrumented step for the split between phases
-    ev = [TimingEvent() for _ in range(5)]
+    ev = [TimingEvent() for _ in range(6)]
     ev[0].record()
-    for q in qs:
-        q.fq_fwd(uq.MAP_LOCAL)
+    blk.quantize(uq.MAP_LOCAL)
     ev[1].record()
-    blk._forward_h(qs[0].W_hat, qs[1].W_hat)
-    uq.uniquan_layer_recon(T, C, I, blk.H, blk.Ht, qs[2].W_hat, blk.Yt_ref, blk.loss, blk.Et, blk.partials, qs[2].G)
+    blk.forward()
     ev[2].record()
-    uq.uniquan_transpose_bf16(C, T, blk.Et, blk.E)
-    uq.uniquan_transpose_bf16(C, I, qs[2].W_hat, blk.WdT)
-    uq.uniquan_gemm_nt(I, T, C, blk.WdT, blk.E, blk.dHt, 2.0)
-    uq.uniquan_silu_mul_bwd(blk.dHt, blk.Gt, blk.Ut, blk.dGt, blk.dUt)
-    uq.uniquan_gemm_nt(I, C, T, blk.dGt, blk.Xt, qs[0].G)
-    uq.uniquan_gemm_nt(I, C, T, blk.dUt, blk.Xt, qs[1].G)
+    blk.compute_loss()
     ev[3].record()
-    for q in qs:
-        q.fq_bwd_sgd(lr_f, lr_b)
+    blk.backward()
     ev[4].record()
+    blk.update(lr_f, lr_b)
+    ev[5].record()
     torch.cuda.synchronize()
-    phases = dict(zip(("fq_fwd", "forward_loss_dWd", "backprop_dWg_dWu", "ste_sgd"),
-                      (ev[i].elapsed_time(ev[i + 1]) for i in range(4))))
-    flops = 7 * 2.0 * T * C * I
+    phases = dict(zip(("fq_fwd", "forward", "loss", "backward", "ste_sgd"),
+                      (ev[i].elapsed_time(ev[i + 1]) for i in range(5))))
+    flops = blk.flops_per_step()
     tf = flops / (ms * 1e-3) / 1e12
-    n_w = 3 * C * I
-    return {"T": T, "C": C, "I": I, "k": k, "g": g, "steps": steps, "ms_per_step": ms,
-            "gweights_per_s": n_w / (ms * 1e-3) / 1e9, "gemm_flops_per_step": flops,
-            "tflops_effective": tf, "frac_mfma": tf / MFMA_BF16_PEAK_TFLOPS, "phase_ms": phases,
-            "loss_init": l0, "rel_loss_warmup": rel, "rel_loss_last": float(blk.loss.item()) / l0,
+    n_w = sum(q.R * q.C for q in mats.values())
+    last = float(blk.loss.item()) / l0
+    return {"T": blk.T, "C": blk.C, "I": blk.I, "heads": H, "seq_len": blk.L, "n_seq": n_seq, "k": k, "g": g,
+            "steps": steps, "ms_per_step": ms, "gweights_per_s": n_w / (ms * 1e-3) / 1e9,
+            "gemm_flops_per_step": flops, "tflops_effective": tf, "frac_mfma": tf / MFMA_BF16_PEAK_TFLOPS,
+            "phase_ms": phases, "loss_init": l0, "rel_loss_warmup": rel, "rel_loss_last": last,
+            "state_finite": bool(math.isfinite(last)),
             "optimiser": "SGD on L / L_init (learning rates 0.005 / 0.0005 divided by the initial loss)",
-            "note": "whole step over the three matrices (fake-quant fwd, module forward on What, loss, "
-                    "backpropagation, straight-through backward + SGD); flops count the seven GEMMs only"}
-
-
+            "note": "whole step over the seven matrices (fake-quant fwd, block forward on What with the "
+                    "quantized input, loss, backpropagation, straight-through backward + SGD); flops count "
+                    "the GEMMs only"}
 
 def main():
     args = parse()
@@ -571,7 +571,7 @@ def main():
                          "and SGD update in its epilogue (dL/dWhat never written)"}
 
     bcq = bcq_inference(layers)
-    blk = None if args.no_block else block_mlp(args.seed)
+    blk = None if args.no_block else block_decoder(args.seed)
 
     out = {
         "metric": "fake-quant fwd+bwd Gweights/s (%HBM peak); recon GEMM TFLOP/s (%MFMA)",
@@ -606,7 +606,7 @@ def main():
         "bcq_inference": {"per_call": bcq,
                           "note": "deployed layer (fold -> bit-planes + binary16 Theta*_B): Y = X What^T for T "
                                   "activation rows; bytes = planes + parameters + X + Y"},
-        "block_mlp": blk,
+        "block_decoder": blk,
         "counters_src_hash": src_hash(),
         "precision": "quantizer: fp32 arithmetic on bf16 W / fp32 s, bf16 What and dL/dWhat; "
                      "GEMMs: bf16 MFMA with fp32 accumulation",

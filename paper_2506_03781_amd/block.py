@@ -218,15 +218,31 @@ class DecoderBlock:
         Xd = Xhat if isinstance(Xhat, torch.Tensor) else to_dev(Xhat, torch.float32)
         self.Xhat.copy_(Xd.float())
 
+    def quantize(self, mode):
+        for q in self.mats.values():
+            q.fq_fwd(mode)
+
+    def forward(self):
+        """The quantized block on Xhat with the current What."""
+        self._forward({n: q.W_hat for n, q in self.mats.items()}, self.Xhat)
+
+    def compute_loss(self):
+        uq.uniquan_block_loss(self.T * self.C, self.R, self.M32, self.Yref, self.E, self.partials, self.loss)
+
     def forward_backward(self, mode):
+        """Quantize, forward, loss and dL/dWhat of all seven matrices (left
+        in each QuantMatrix.G)."""
+        self.quantize(mode)
+        self.forward()
+        self.compute_loss()
+        self.backward()
+
+    def backward(self):
+        """Backpropagation from E to dL/dWhat of the seven matrices."""
         T, C, I, H, d, L, B = self.T, self.C, self.I, self.H, self.d, self.L, self.B
         sc = 1.0 / float(d) ** 0.5
         m = self.mats
-        for q in m.values():
-            q.fq_fwd(mode)
         Wh = {n: q.W_hat for n, q in m.items()}
-        self._forward(Wh, self.Xhat)
-        uq.uniquan_block_loss(T * C, self.R, self.M32, self.Yref, self.E, self.partials, self.loss)
         # MLP module (dY = 2 E)
         uq.uniquan_transpose_bf16(T, C, self.E, self.Et)
         uq.uniquan_gemm_nt(C, I, T, self.Et, self.Ht, m["d"].G, 2.0)
@@ -269,10 +285,23 @@ class DecoderBlock:
             uq.uniquan_transpose_bf16(T, C, src, dst)
             uq.uniquan_gemm_nt(C, C, T, dst, self.Z1t, m[g].G)
 
-    def step(self, mode=uq.MAP_FULL, lr_f=0.005, lr_b=0.0005, keep_grads=False):
-        self.forward_backward(mode)
+    def update(self, lr_f=0.005, lr_b=0.0005, keep_grads=False):
+        """Straight-through backward with the SGD update of every matrix."""
         for q in self.mats.values():
             q.fq_bwd_sgd(lr_f, lr_b, keep_grads)
+
+    def step(self, mode=uq.MAP_FULL, lr_f=0.005, lr_b=0.0005, keep_grads=False):
+        self.forward_backward(mode)
+        self.update(lr_f, lr_b, keep_grads)
+
+    def flops_per_step(self):
+        """GEMM flops of one step: the seven projections forward and their
+        weight gradients, the input gradients through the MLP and the output
+        projection, and the attention products forward and backward."""
+        T, C, I, L, d, B = self.T, self.C, self.I, self.L, self.d, self.B
+        lin = 2.0 * T * C * C * 4 + 2.0 * T * C * I * 3
+        attn = 2.0 * B * L * L * d
+        return 2 * lin + 3 * (2.0 * T * C * I) + 2.0 * T * C * C + 6 * attn
 
     def output(self):
         """The quantized block's output on its input (fp32 [T, C]): the next
