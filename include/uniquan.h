@@ -390,7 +390,7 @@ uq_status uniquan_gemm_nt_batched(int64_t M, int64_t N, int64_t K, int64_t batch
  * uniquan_add_rmsnorm -- per row t < T of [T, C] (fp32): v = X + A (A may be
  * NULL), R = v (written when A is given; R may be NULL otherwise),
  * rinv[t] = 1 / sqrt(mean(v^2) + 1e-5), Z = bf16((v rinv) gamma).
- * C a multiple of 8.
+ * C a multiple of 8; fp32 arrays 16-byte aligned, Z 8-byte aligned.
  */
 uq_status uniquan_add_rmsnorm(int64_t T, int64_t C, const float* X,
                               const float* A, const float* gamma, float* R,
@@ -400,7 +400,8 @@ uq_status uniquan_add_rmsnorm(int64_t T, int64_t C, const float* X,
  * uniquan_rmsnorm_bwd -- backward of Z = (X rinv) gamma plus a residual
  * gradient: with g = gamma (dZa + dZb) (dZb may be NULL),
  * dR = escale E + rinv g - X rinv^3 sum(g X) / C per row; E (bf16) may be
- * NULL.  dR is written in bf16, and in fp32 to dRf when given.
+ * NULL.  dR is written in bf16, and in fp32 to dRf when given.  fp32 arrays
+ * 16-byte aligned, E and dR 8-byte aligned.
  */
 uq_status uniquan_rmsnorm_bwd(int64_t T, int64_t C, const float* dZa,
                               const float* dZb, const float* X,
@@ -437,7 +438,7 @@ uq_status uniquan_softmax_causal_bwd(int64_t rows, int L, const float* dP,
 
 /*
  * uniquan_transpose_bf16_batched -- out_b = in_b^T for batch matrices
- * [R, C] stored back to back (bf16).
+ * [R, C] stored back to back (bf16; in and out 8-byte aligned).
  */
 uq_status uniquan_transpose_bf16_batched(int64_t batch, int64_t R, int64_t C,
                                          const uint16_t* in, uint16_t* out,

@@ -390,9 +390,9 @@ uq_status uniquan_add_rmsnorm(int64_t T, int64_t C, const float* X, const float*
   const char* fn = "uniquan_add_rmsnorm";
   if (T < 1 || C < 8 || C % 8 != 0) return fail(UQ_EINVAL, "%s: T >= 1 and C a positive multiple of 8 required", fn);
   if (A != nullptr && R == nullptr) return fail(UQ_EINVAL, "%s: R must be given with A", fn);
-  REQ_PTR(X, 4); REQ_PTR(gamma, 4); REQ_PTR(Z, 2); REQ_PTR(rinv, 4);
-  if (A && !aligned(A, 4)) return fail(UQ_EINVAL, "%s: A must be 4-byte aligned", fn);
-  if (R && !aligned(R, 4)) return fail(UQ_EINVAL, "%s: R must be 4-byte aligned", fn);
+  REQ_PTR(X, 16); REQ_PTR(gamma, 16); REQ_PTR(Z, 8); REQ_PTR(rinv, 4);
+  if (A && !aligned(A, 16)) return fail(UQ_EINVAL, "%s: A must be 16-byte aligned", fn);
+  if (R && !aligned(R, 16)) return fail(UQ_EINVAL, "%s: R must be 16-byte aligned", fn);
   return hip_status(fn, uq::launch_add_rmsnorm(T, C, X, A, gamma, R, Z, rinv, static_cast<hipStream_t>(stream)));
 }
 
@@ -401,10 +401,10 @@ uq_status uniquan_rmsnorm_bwd(int64_t T, int64_t C, const float* dZa, const floa
                               float* dRf, void* stream) {
   const char* fn = "uniquan_rmsnorm_bwd";
   if (T < 1 || C < 8 || C % 8 != 0) return fail(UQ_EINVAL, "%s: T >= 1 and C a positive multiple of 8 required", fn);
-  REQ_PTR(dZa, 4); REQ_PTR(X, 4); REQ_PTR(gamma, 4); REQ_PTR(rinv, 4); REQ_PTR(dR, 2);
-  if (dZb && !aligned(dZb, 4)) return fail(UQ_EINVAL, "%s: dZb must be 4-byte aligned", fn);
-  if (E && !aligned(E, 2)) return fail(UQ_EINVAL, "%s: E must be 2-byte aligned", fn);
-  if (dRf && !aligned(dRf, 4)) return fail(UQ_EINVAL, "%s: dRf must be 4-byte aligned", fn);
+  REQ_PTR(dZa, 16); REQ_PTR(X, 16); REQ_PTR(gamma, 16); REQ_PTR(rinv, 4); REQ_PTR(dR, 8);
+  if (dZb && !aligned(dZb, 16)) return fail(UQ_EINVAL, "%s: dZb must be 16-byte aligned", fn);
+  if (E && !aligned(E, 8)) return fail(UQ_EINVAL, "%s: E must be 8-byte aligned", fn);
+  if (dRf && !aligned(dRf, 16)) return fail(UQ_EINVAL, "%s: dRf must be 16-byte aligned", fn);
   return hip_status(fn, uq::launch_rmsnorm_bwd(T, C, dZa, dZb, X, gamma, rinv, E, escale, dR, dRf,
                                                static_cast<hipStream_t>(stream)));
 }
@@ -461,7 +461,7 @@ uq_status uniquan_transpose_bf16_batched(int64_t batch, int64_t R, int64_t C, co
     return fail(UQ_EINVAL, "%s: need 1 <= batch <= 65535 and R, C >= 1", fn);
   if (batch * R * C >= (int64_t(1) << 40) || ((R + 63) / 64) * ((C + 63) / 64) >= (int64_t(1) << 31))
     return fail(UQ_EUNSUPPORTED, "%s: shape too large", fn);
-  REQ_PTR(in, 2); REQ_PTR(out, 2);
+  REQ_PTR(in, 8); REQ_PTR(out, 8);
   return hip_status(fn, uq::launch_transpose_batched(batch, R, C, in, out, static_cast<hipStream_t>(stream)));
 }
 

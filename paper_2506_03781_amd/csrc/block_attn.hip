@@ -40,7 +40,8 @@ __device__ __forceinline__ float rope_angle(int p, int i, int d) {
 }  // namespace
 
 // One wavefront per row: R = X + A (A optional), r = 1 / sqrt(mean(R^2) + eps),
-// Z = bf16((R r) gamma).  C is a multiple of 8.
+// Z = bf16((R r) gamma).  C is a multiple of 8; lane l takes the four
+// consecutive columns 4 l + 256 j, so each load covers 1 KB of the row.
 __global__ __launch_bounds__(256) void add_rmsnorm_kernel(int64_t T, int64_t C, const float* __restrict__ X,
                                                           const float* __restrict__ A, const float* __restrict__ gamma,
                                                           float* __restrict__ R, uint16_t* __restrict__ Z,
@@ -48,31 +49,45 @@ __global__ __launch_bounds__(256) void add_rmsnorm_kernel(int64_t T, int64_t C, 
   const int lane = threadIdx.x & 63;
   const int64_t row = int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6);
   if (row >= T) return;
-  const float* x = X + row * C;
-  const float* a = A ? A + row * C : nullptr;
+  const float4* x = reinterpret_cast<const float4*>(X + row * C);
+  const float4* a = A ? reinterpret_cast<const float4*>(A + row * C) : nullptr;
+  const int64_t n4 = C / 4;
   float ss = 0.0f;
-  for (int64_t c = int64_t(lane) * 8; c < C; c += 512) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const float v = a ? x[c + i] + a[c + i] : x[c + i];
-      ss += v * v;
+#pragma unroll 4
+  for (int64_t c = lane; c < n4; c += 64) {
+    float4 v = x[c];
+    if (a) {
+      const float4 w = a[c];
+      v.x += w.x; v.y += w.y; v.z += w.z; v.w += w.w;
     }
+    ss += v.x * v.x;
+    ss += v.y * v.y;
+    ss += v.z * v.z;
+    ss += v.w * v.w;
   }
   ss = wave_sum(ss);
   const float r = 1.0f / sqrtf(ss / float(C) + 1e-5f);
   if (lane == 0) rinv[row] = r;
-  for (int64_t c = int64_t(lane) * 8; c < C; c += 512) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const float v = a ? x[c + i] + a[c + i] : x[c + i];
-      if (R) R[row * C + c + i] = v;
-      Z[row * C + c + i] = to_bf((v * r) * gamma[c + i]);
+  const float4* g4 = reinterpret_cast<const float4*>(gamma);
+  float4* R4 = R ? reinterpret_cast<float4*>(R + row * C) : nullptr;
+  uint2* Z2 = reinterpret_cast<uint2*>(Z + row * C);
+#pragma unroll 4
+  for (int64_t c = lane; c < n4; c += 64) {
+    float4 v = x[c];
+    if (a) {
+      const float4 w = a[c];
+      v.x += w.x; v.y += w.y; v.z += w.z; v.w += w.w;
     }
+    if (R4) R4[c] = v;
+    const float4 g = g4[c];
+    Z2[c] = make_uint2(uint32_t(to_bf((v.x * r) * g.x)) | (uint32_t(to_bf((v.y * r) * g.y)) << 16),
+                       uint32_t(to_bf((v.z * r) * g.z)) | (uint32_t(to_bf((v.w * r) * g.w)) << 16));
   }
 }
 
 // One wavefront per row: dR = escale * E + r g - x r^3 sum(g x) / C with
 // g = gamma (dZa + dZb); writes dR in bf16 (and in fp32 when dRf is given).
+// Same lane layout as the forward (four consecutive columns per access).
 __global__ __launch_bounds__(256) void rmsnorm_bwd_kernel(int64_t T, int64_t C, const float* __restrict__ dZa,
                                                           const float* __restrict__ dZb,
                                                           const float* __restrict__ Xin,
@@ -84,26 +99,51 @@ __global__ __launch_bounds__(256) void rmsnorm_bwd_kernel(int64_t T, int64_t C, 
   const int64_t row = int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6);
   if (row >= T) return;
   const int64_t base = row * C;
-  float dot = 0.0f;
-  for (int64_t c = int64_t(lane) * 8; c < C; c += 512) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const float dz = dZb ? dZa[base + c + i] + dZb[base + c + i] : dZa[base + c + i];
-      dot += (gamma[c + i] * dz) * Xin[base + c + i];
+  const int64_t n4 = C / 4;
+  const float4* za = reinterpret_cast<const float4*>(dZa + base);
+  const float4* zb = dZb ? reinterpret_cast<const float4*>(dZb + base) : nullptr;
+  const float4* x4 = reinterpret_cast<const float4*>(Xin + base);
+  const float4* g4 = reinterpret_cast<const float4*>(gamma);
+  auto gdz = [&](int64_t c) {
+    float4 z = za[c];
+    if (zb) {
+      const float4 w = zb[c];
+      z.x += w.x; z.y += w.y; z.z += w.z; z.w += w.w;
     }
+    const float4 g = g4[c];
+    return make_float4(g.x * z.x, g.y * z.y, g.z * z.z, g.w * z.w);
+  };
+  float dot = 0.0f;
+#pragma unroll 4
+  for (int64_t c = lane; c < n4; c += 64) {
+    const float4 g = gdz(c);
+    const float4 v = x4[c];
+    dot += g.x * v.x;
+    dot += g.y * v.y;
+    dot += g.z * v.z;
+    dot += g.w * v.w;
   }
   dot = wave_sum(dot);
   const float r = rinv[row];
   const float k3 = (r * r * r) * (dot / float(C));
-  for (int64_t c = int64_t(lane) * 8; c < C; c += 512) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const float dz = dZb ? dZa[base + c + i] + dZb[base + c + i] : dZa[base + c + i];
-      float v = r * (gamma[c + i] * dz) - Xin[base + c + i] * k3;
-      if (E) v += escale * bf(E[base + c + i]);
-      dR[base + c + i] = to_bf(v);
-      if (dRf) dRf[base + c + i] = v;
+  const uint2* e2 = E ? reinterpret_cast<const uint2*>(E + base) : nullptr;
+  uint2* d2 = reinterpret_cast<uint2*>(dR + base);
+  float4* df = dRf ? reinterpret_cast<float4*>(dRf + base) : nullptr;
+#pragma unroll 4
+  for (int64_t c = lane; c < n4; c += 64) {
+    const float4 g = gdz(c);
+    const float4 v = x4[c];
+    float o[4] = {r * g.x - v.x * k3, r * g.y - v.y * k3, r * g.z - v.z * k3, r * g.w - v.w * k3};
+    if (e2) {
+      const uint2 e = e2[c];
+      o[0] += escale * bf(uint16_t(e.x & 0xFFFFu));
+      o[1] += escale * bf(uint16_t(e.x >> 16));
+      o[2] += escale * bf(uint16_t(e.y & 0xFFFFu));
+      o[3] += escale * bf(uint16_t(e.y >> 16));
     }
+    d2[c] = make_uint2(uint32_t(to_bf(o[0])) | (uint32_t(to_bf(o[1])) << 16),
+                       uint32_t(to_bf(o[2])) | (uint32_t(to_bf(o[3])) << 16));
+    if (df) df[c] = make_float4(o[0], o[1], o[2], o[3]);
   }
 }
 
@@ -174,7 +214,10 @@ __global__ __launch_bounds__(256) void rope_merge_kernel(int64_t T, int H, int d
 }
 
 // One wavefront per score row i of one [L, L] block: P[i, j] = softmax over
-// j <= i of S[i, j], 0 for j > i (bf16).
+// j <= i of S[i, j], 0 for j > i (bf16).  Rows of up to 2048 are held in
+// registers (NPL = 32 values per lane, one read of S); longer rows take three
+// passes over S.
+template <int NPL>
 __global__ __launch_bounds__(256) void softmax_causal_kernel(int64_t rows, int L, const float* __restrict__ S,
                                                              uint16_t* __restrict__ P) {
   const int lane = threadIdx.x & 63;
@@ -183,18 +226,44 @@ __global__ __launch_bounds__(256) void softmax_causal_kernel(int64_t rows, int L
   const int i = int(row % L);
   const float* s = S + row * L;
   uint16_t* p = P + row * L;
-  float m = -INFINITY;
-  for (int j = lane; j <= i; j += 64) m = fmaxf(m, s[j]);
-  m = wave_max(m);
-  float sum = 0.0f;
-  for (int j = lane; j <= i; j += 64) sum += expf(s[j] - m);
-  sum = wave_sum(sum);
-  const float inv = 1.0f / sum;
-  for (int j = lane; j < L; j += 64) p[j] = j <= i ? to_bf(expf(s[j] - m) * inv) : uint16_t(0);
+  if constexpr (NPL > 0) {
+    float v[NPL];
+    float m = -INFINITY;
+#pragma unroll
+    for (int k = 0; k < NPL; ++k) {
+      const int j = lane + 64 * k;
+      v[k] = j <= i ? s[j] : -INFINITY;
+      m = fmaxf(m, v[k]);
+    }
+    m = wave_max(m);
+    float sum = 0.0f;
+#pragma unroll
+    for (int k = 0; k < NPL; ++k) {
+      v[k] = lane + 64 * k <= i ? expf(v[k] - m) : 0.0f;
+      sum += v[k];
+    }
+    sum = wave_sum(sum);
+    const float inv = 1.0f / sum;
+#pragma unroll
+    for (int k = 0; k < NPL; ++k) {
+      const int j = lane + 64 * k;
+      if (j < L) p[j] = j <= i ? to_bf(v[k] * inv) : uint16_t(0);
+    }
+  } else {
+    float m = -INFINITY;
+    for (int j = lane; j <= i; j += 64) m = fmaxf(m, s[j]);
+    m = wave_max(m);
+    float sum = 0.0f;
+    for (int j = lane; j <= i; j += 64) sum += expf(s[j] - m);
+    sum = wave_sum(sum);
+    const float inv = 1.0f / sum;
+    for (int j = lane; j < L; j += 64) p[j] = j <= i ? to_bf(expf(s[j] - m) * inv) : uint16_t(0);
+  }
 }
 
 // dS[i, j] = P[i, j] (dP[i, j] - sum_j' P[i, j'] dP[i, j']) (bf16), one
-// wavefront per row.
+// wavefront per row; rows of up to 2048 in registers as in the forward.
+template <int NPL>
 __global__ __launch_bounds__(256) void softmax_bwd_kernel(int64_t rows, int L, const float* __restrict__ dP,
                                                           const uint16_t* __restrict__ P, uint16_t* __restrict__ dS) {
   const int lane = threadIdx.x & 63;
@@ -203,28 +272,66 @@ __global__ __launch_bounds__(256) void softmax_bwd_kernel(int64_t rows, int L, c
   const int i = int(row % L);
   const float* dp = dP + row * L;
   const uint16_t* p = P + row * L;
-  float dot = 0.0f;
-  for (int j = lane; j <= i; j += 64) dot += bf(p[j]) * dp[j];
-  dot = wave_sum(dot);
-  for (int j = lane; j < L; j += 64) dS[row * L + j] = j <= i ? to_bf(bf(p[j]) * (dp[j] - dot)) : uint16_t(0);
+  if constexpr (NPL > 0) {
+    float pv[NPL], dv[NPL];
+    float dot = 0.0f;
+#pragma unroll
+    for (int k = 0; k < NPL; ++k) {
+      const int j = lane + 64 * k;
+      pv[k] = j <= i ? bf(p[j]) : 0.0f;
+      dv[k] = j <= i ? dp[j] : 0.0f;
+      dot += pv[k] * dv[k];
+    }
+    dot = wave_sum(dot);
+#pragma unroll
+    for (int k = 0; k < NPL; ++k) {
+      const int j = lane + 64 * k;
+      if (j < L) dS[row * L + j] = j <= i ? to_bf(pv[k] * (dv[k] - dot)) : uint16_t(0);
+    }
+  } else {
+    float dot = 0.0f;
+    for (int j = lane; j <= i; j += 64) dot += bf(p[j]) * dp[j];
+    dot = wave_sum(dot);
+    for (int j = lane; j < L; j += 64) dS[row * L + j] = j <= i ? to_bf(bf(p[j]) * (dp[j] - dot)) : uint16_t(0);
+  }
 }
 
-// out[b] = in[b]^T for B matrices [R, C] (bf16), 64 x 64 tiles through LDS.
+// out[b] = in[b]^T for B matrices [R, C] (bf16): 64 x 64 tiles through LDS,
+// 8-byte accesses on both sides (four columns per lane and access).
 __global__ __launch_bounds__(256) void transpose_batched_kernel(int64_t R, int64_t C, const uint16_t* __restrict__ in,
                                                                 uint16_t* __restrict__ out) {
-  __shared__ uint16_t tile[64][66];
+  __shared__ uint16_t tile[64][68];
   const int64_t tiles_c = (C + 63) / 64;
   const int64_t r0 = (int64_t(blockIdx.x) / tiles_c) * 64, c0 = (int64_t(blockIdx.x) % tiles_c) * 64;
   const int64_t boff = int64_t(blockIdx.y) * R * C;
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-  for (int y = ty; y < 64; y += 4) {
-    const int64_t r = r0 + y, c = c0 + tx;
-    tile[y][tx] = (r < R && c < C) ? in[boff + r * C + c] : uint16_t(0);
+  const int q = threadIdx.x & 15, y0 = threadIdx.x >> 4;  // column group, first row
+  const bool vec = (C % 4 == 0) && (R % 4 == 0);
+  for (int y = y0; y < 64; y += 16) {
+    const int64_t r = r0 + y, c = c0 + 4 * q;
+    if (vec && r < R && c + 3 < C) {
+      const uint2 v = *reinterpret_cast<const uint2*>(in + boff + r * C + c);
+      tile[y][4 * q] = uint16_t(v.x & 0xFFFFu);
+      tile[y][4 * q + 1] = uint16_t(v.x >> 16);
+      tile[y][4 * q + 2] = uint16_t(v.y & 0xFFFFu);
+      tile[y][4 * q + 3] = uint16_t(v.y >> 16);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) tile[y][4 * q + e] = (r < R && c + e < C) ? in[boff + r * C + c + e] : uint16_t(0);
+    }
   }
   __syncthreads();
-  for (int y = ty; y < 64; y += 4) {
-    const int64_t c = c0 + y, r = r0 + tx;
-    if (c < C && r < R) out[boff + c * R + r] = tile[tx][y];
+  for (int y = y0; y < 64; y += 16) {
+    const int64_t c = c0 + y, r = r0 + 4 * q;  // output row c, columns r .. r+3
+    if (c >= C) continue;
+    if (vec && r + 3 < R) {
+      const uint2 v = make_uint2(uint32_t(tile[4 * q][y]) | (uint32_t(tile[4 * q + 1][y]) << 16),
+                                 uint32_t(tile[4 * q + 2][y]) | (uint32_t(tile[4 * q + 3][y]) << 16));
+      *reinterpret_cast<uint2*>(out + boff + c * R + r) = v;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (r + e < R) out[boff + c * R + r + e] = tile[4 * q + e][y];
+    }
   }
 }
 
@@ -295,12 +402,16 @@ hipError_t launch_rope_merge(int64_t T, int H, int d, int L, const void* in, int
 }
 
 hipError_t launch_softmax_causal(int64_t rows, int L, const float* S, uint16_t* P, hipStream_t st) {
-  hipLaunchKernelGGL(softmax_causal_kernel, dim3(unsigned((rows + 3) / 4)), dim3(256), 0, st, rows, L, S, P);
+  const dim3 grid(unsigned((rows + 3) / 4));
+  if (L <= 2048) hipLaunchKernelGGL(softmax_causal_kernel<32>, grid, dim3(256), 0, st, rows, L, S, P);
+  else hipLaunchKernelGGL(softmax_causal_kernel<0>, grid, dim3(256), 0, st, rows, L, S, P);
   return hipGetLastError();
 }
 
 hipError_t launch_softmax_bwd(int64_t rows, int L, const float* dP, const uint16_t* P, uint16_t* dS, hipStream_t st) {
-  hipLaunchKernelGGL(softmax_bwd_kernel, dim3(unsigned((rows + 3) / 4)), dim3(256), 0, st, rows, L, dP, P, dS);
+  const dim3 grid(unsigned((rows + 3) / 4));
+  if (L <= 2048) hipLaunchKernelGGL(softmax_bwd_kernel<32>, grid, dim3(256), 0, st, rows, L, dP, P, dS);
+  else hipLaunchKernelGGL(softmax_bwd_kernel<0>, grid, dim3(256), 0, st, rows, L, dP, P, dS);
   return hipGetLastError();
 }
 

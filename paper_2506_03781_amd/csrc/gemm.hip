@@ -617,8 +617,9 @@ static int tiles(int64_t M, int64_t N) {
 enum TileShape { T256x256, T256x128, T128x128 };
 static TileShape pick(int64_t M, int64_t N, int64_t batch = 1) {
   const int64_t nb = batch > 1 ? batch : 1;
-  if (tiles<256, 256>(M, N) * nb >= 256) return T256x256;
-  if (tiles<256, 128>(M, N) * nb >= 256) return T256x128;
+  // a 256-wide side only where the matrix is wider than 128 (no half-empty tiles)
+  if (M > 128 && N > 128 && tiles<256, 256>(M, N) * nb >= 256) return T256x256;
+  if (M > 128 && tiles<256, 128>(M, N) * nb >= 256) return T256x128;
   return T128x128;
 }
 

@@ -140,7 +140,7 @@ def test_rope_split_merge(n_seq, L, H, d):
     assert np.array_equal(host(tm), xb)
 
 
-@pytest.mark.parametrize("B,L", [(3, 7), (4, 130), (2, 2048)])
+@pytest.mark.parametrize("B,L", [(3, 7), (4, 130), (2, 2048), (1, 2100)])   # 2100: rows past the register path
 def test_softmax_causal(B, L):
     rs = np.random.default_rng(B * L)
     S = (3.0 * rs.standard_normal((B, L, L))).astype(F32)
@@ -165,7 +165,7 @@ def test_softmax_causal(B, L):
     within_bf16(host(dS), ref_ds, 1e-5 * scale * Pin + 1e-7, "dS")
 
 
-@pytest.mark.parametrize("B,R,C", [(1, 5, 7), (3, 64, 130), (2, 300, 64)])
+@pytest.mark.parametrize("B,R,C", [(1, 5, 7), (3, 64, 130), (2, 300, 64), (3, 68, 132), (2, 2048, 128)])
 def test_transpose_batched(B, R, C):
     x = bfr(np.random.default_rng(R * C).standard_normal((B, R, C)))
     out = torch.empty(B, C, R, dtype=torch.bfloat16, device="cuda")
