@@ -379,12 +379,21 @@ uq_status uniquan_silu_mul_bwd(int64_t n, const uint16_t* dH, const uint16_t* G,
  * B_b = B + b stride_b (elements; 0 repeats an operand), out_b = out +
  * b stride_out (elements of out_dtype, >= M N).  Shape rules as
  * uniquan_gemm_nt; strides multiples of 8; batch <= 65535.
+ * causal (the attention's square [L, L] operands, K % 32 == 0):
+ *   0  the full product;
+ *   1  M == N: tiles entirely above the diagonal (all columns > all rows)
+ *      are skipped and their outputs left unwritten (the causal softmax
+ *      reads only j <= i);
+ *   2  M == K: A is zero above the diagonal; the K loop of a row tile ends
+ *      at the tile's last row (the result equals the full product);
+ *   3  M == K: A is zero below the diagonal; the K loop of a row tile starts
+ *      at its first row (the result equals the full product).
  */
 uq_status uniquan_gemm_nt_batched(int64_t M, int64_t N, int64_t K, int64_t batch,
                                   const uint16_t* A, int64_t stride_a,
                                   const uint16_t* B, int64_t stride_b, void* out,
                                   int64_t stride_out, int out_dtype, float scale,
-                                  void* stream);
+                                  int causal, void* stream);
 
 /*
  * uniquan_add_rmsnorm -- per row t < T of [T, C] (fp32): v = X + A (A may be

@@ -191,10 +191,10 @@ class DecoderBlock:
         uq.uniquan_rope_split(T, H, d, L, self.Qf, self.Qh, rotate=True)
         uq.uniquan_rope_split(T, H, d, L, self.Kf, self.Kh, rotate=True)
         uq.uniquan_rope_split(T, H, d, L, self.Vb, self.Vh, rotate=False)
-        uq.uniquan_gemm_nt_batched(L, L, d, B, self.Qh, L * d, self.Kh, L * d, self.S, L * L, sc)
+        uq.uniquan_gemm_nt_batched(L, L, d, B, self.Qh, L * d, self.Kh, L * d, self.S, L * L, sc, causal=1)
         uq.uniquan_softmax_causal(B * L, L, self.S, self.P)
         uq.uniquan_transpose_bf16_batched(B, L, d, self.Vh, self.Vt)
-        uq.uniquan_gemm_nt_batched(L, d, L, B, self.P, L * L, self.Vt, d * L, self.Oh, L * d)
+        uq.uniquan_gemm_nt_batched(L, d, L, B, self.P, L * L, self.Vt, d * L, self.Oh, L * d, causal=2)
         uq.uniquan_rope_merge(T, H, d, L, self.Oh, self.O, rotate=False)
         uq.uniquan_gemm_nt(T, C, C, self.O, W["o"], self.A32)
         uq.uniquan_add_rmsnorm(T, C, X, self.A32, self.g2, self.R, self.Z2, self.r2)
@@ -267,16 +267,16 @@ class DecoderBlock:
         uq.uniquan_transpose_bf16(C, C, Wh["o"], self.WoT)
         uq.uniquan_gemm_nt(T, C, C, self.dA, self.WoT, self.dO)
         uq.uniquan_rope_split(T, H, d, L, self.dO, self.dOh, rotate=False)
-        uq.uniquan_gemm_nt_batched(L, L, d, B, self.dOh, L * d, self.Vh, L * d, self.dP, L * L)
+        uq.uniquan_gemm_nt_batched(L, L, d, B, self.dOh, L * d, self.Vh, L * d, self.dP, L * L, causal=1)
         uq.uniquan_softmax_causal_bwd(B * L, L, self.dP, self.P, self.dS)
         uq.uniquan_transpose_bf16_batched(B, L, d, self.Kh, self.Kt)
-        uq.uniquan_gemm_nt_batched(L, d, L, B, self.dS, L * L, self.Kt, d * L, self.dQr, L * d, sc)
+        uq.uniquan_gemm_nt_batched(L, d, L, B, self.dS, L * L, self.Kt, d * L, self.dQr, L * d, sc, causal=2)
         uq.uniquan_transpose_bf16_batched(B, L, L, self.dS, self.dSt)
         uq.uniquan_transpose_bf16_batched(B, L, d, self.Qh, self.Qt)
-        uq.uniquan_gemm_nt_batched(L, d, L, B, self.dSt, L * L, self.Qt, d * L, self.dKr, L * d, sc)
+        uq.uniquan_gemm_nt_batched(L, d, L, B, self.dSt, L * L, self.Qt, d * L, self.dKr, L * d, sc, causal=3)
         uq.uniquan_transpose_bf16_batched(B, L, L, self.P, self.Pt)
         uq.uniquan_transpose_bf16_batched(B, L, d, self.dOh, self.dOt)
-        uq.uniquan_gemm_nt_batched(L, d, L, B, self.Pt, L * L, self.dOt, d * L, self.dVh, L * d)
+        uq.uniquan_gemm_nt_batched(L, d, L, B, self.Pt, L * L, self.dOt, d * L, self.dVh, L * d, causal=3)
         uq.uniquan_rope_merge(T, H, d, L, self.dQr, self.dQ, rotate=True)
         uq.uniquan_rope_merge(T, H, d, L, self.dKr, self.dK, rotate=True)
         uq.uniquan_rope_merge(T, H, d, L, self.dVh, self.dV, rotate=False)
@@ -297,10 +297,12 @@ class DecoderBlock:
     def flops_per_step(self):
         """GEMM flops of one step: the seven projections forward and their
         weight gradients, the input gradients through the MLP and the output
-        projection, and the attention products forward and backward."""
+        projection, and the attention products forward and backward (the
+        causal half of each [L, L] product that is never computed is not
+        counted)."""
         T, C, I, L, d, B = self.T, self.C, self.I, self.L, self.d, self.B
         lin = 2.0 * T * C * C * 4 + 2.0 * T * C * I * 3
-        attn = 2.0 * B * L * L * d
+        attn = 2.0 * B * (L * (L + 1) / 2) * d
         return 2 * lin + 3 * (2.0 * T * C * I) + 2.0 * T * C * C + 6 * attn
 
     def output(self):

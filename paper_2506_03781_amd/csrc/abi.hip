@@ -360,7 +360,7 @@ uq_status uniquan_silu_mul_bwd(int64_t n, const uint16_t* dH, const uint16_t* G,
 
 uq_status uniquan_gemm_nt_batched(int64_t M, int64_t N, int64_t K, int64_t batch, const uint16_t* A, int64_t stride_a,
                                   const uint16_t* B, int64_t stride_b, void* out, int64_t stride_out, int out_dtype,
-                                  float scale, void* stream) {
+                                  float scale, int causal, void* stream) {
   const char* fn = "uniquan_gemm_nt_batched";
   if (M < 1 || N < 1 || K < 1) return fail(UQ_EINVAL, "%s: M, N, K must be >= 1", fn);
   if (batch < 1 || batch > 65535) return fail(UQ_EINVAL, "%s: batch=%lld must be in 1..65535", fn, (long long)batch);
@@ -375,6 +375,10 @@ uq_status uniquan_gemm_nt_batched(int64_t M, int64_t N, int64_t K, int64_t batch
   if (stride_out < M * N || stride_out % 8 != 0)
     return fail(UQ_EINVAL, "%s: stride_out=%lld must be a multiple of 8 and >= M*N", fn, (long long)stride_out);
   if ((batch - 1) * stride_out >= (int64_t(1) << 40)) return fail(UQ_EUNSUPPORTED, "%s: batch span too large", fn);
+  if (causal < 0 || causal > 3) return fail(UQ_EINVAL, "%s: causal=%d must be 0..3", fn, causal);
+  if (causal != 0 && K % 32 != 0) return fail(UQ_EINVAL, "%s: causal modes need K %% 32 == 0", fn);
+  if (causal == 1 && M != N) return fail(UQ_EINVAL, "%s: causal mode 1 needs M == N", fn);
+  if ((causal == 2 || causal == 3) && M != K) return fail(UQ_EINVAL, "%s: causal modes 2 and 3 need M == K", fn);
   REQ_PTR(A, 16); REQ_PTR(B, 16); REQ_PTR(out, 16);
   uq::GemmLaunch g{A, B, M, N, K, out_dtype == UQ_BF16 ? uq::EPI_GRAD_BF16 : uq::EPI_GRAD_F32, nullptr, out, nullptr,
                    scale};
@@ -382,6 +386,7 @@ uq_status uniquan_gemm_nt_batched(int64_t M, int64_t N, int64_t K, int64_t batch
   g.bsa = stride_a;
   g.bsb = stride_b;
   g.bso = stride_out * (out_dtype == UQ_BF16 ? 2 : 4);
+  g.causal = causal;
   return hip_status(fn, uq::launch_gemm(g, static_cast<hipStream_t>(stream)));
 }
 

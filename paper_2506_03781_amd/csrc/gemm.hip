@@ -42,6 +42,11 @@ struct GemmArgs {
   // strided batch (gridDim.y > 1): element offsets of A and B and byte
   // offset of out per batch
   int64_t bsa, bsb, bso;
+  // causal structure of square [L, L] products (attention): 1 skips tiles
+  // entirely above the diagonal (their outputs are not written), 2 ends the
+  // K loop at the row tile's end (A zero above the diagonal), 3 starts it at
+  // the row tile's start (A zero below the diagonal)
+  int causal;
 };
 
 // Operands and output of batch blockIdx.y.
@@ -470,6 +475,9 @@ __global__ __launch_bounds__(256) void gemm_pipe_kernel(GemmArgs p) {
   tile_of<(BM == 256 && BN == 128) ? 4 : 8>(blockIdx.x, gridDim.x, p.tiles_m, p.tiles_n, tm, tn);
   const int64_t m0 = int64_t(tm) * BM, n0 = int64_t(tn) * BN;
   const int64_t K = p.K;
+  if (p.causal == 1 && n0 >= m0 + BM) return;  // whole tile above the diagonal (uniform per workgroup)
+  const int64_t kb = p.causal == 3 ? m0 : 0;
+  const int64_t ke = p.causal == 2 ? min(K, m0 + BM) : K;
 
   // This lane's source for each of the wave's load instructions.  Lane l
   // fills LDS slot l of a 1 KB block: row 16*blk + l/4, slot l%4, which holds
@@ -486,7 +494,7 @@ __global__ __launch_bounds__(256) void gemm_pipe_kernel(GemmArgs p) {
     const int kc = (lane & 3) ^ ((row >> 1) & 3);
     isA[q] = a;
     const int64_t gr = a ? min(m0 + row, p.M - 1) : min(n0 + row, p.N - 1);
-    src[q] = (a ? p.A : p.B) + gr * K + kc * 8;
+    src[q] = (a ? p.A : p.B) + gr * K + kb + kc * 8;
     dst_off[q] = b * 64;
   }
   auto issue = [&](int stage, int64_t k0) {
@@ -551,7 +559,7 @@ __global__ __launch_bounds__(256) void gemm_pipe_kernel(GemmArgs p) {
     __builtin_amdgcn_sched_group_barrier(0x008, FM * FN - 2, 0);   // MFMAs
   };
 
-  const int nk = int(K / BK);
+  const int nk = int((ke - kb) / BK);
 #pragma unroll
   for (int s = 0; s < S - 1; ++s)
     if (s < nk) issue(s, int64_t(s) * BK);
@@ -645,6 +653,7 @@ static hipError_t launch_bm(const GemmLaunch& q, hipStream_t st) {
   a.A = q.A; a.B = q.B; a.M = q.M; a.N = q.N; a.K = q.K;
   a.Yt = q.Yt; a.out = q.out; a.partials = q.partials; a.scale = q.scale;
   a.bsa = q.bsa; a.bsb = q.bsb; a.bso = q.bso;
+  a.causal = q.causal;
   a.tiles_m = int((q.M + BM - 1) / BM);
   a.tiles_n = int((q.N + BN - 1) / BN);
   const dim3 grid(unsigned(a.tiles_m * a.tiles_n), unsigned(q.batch > 1 ? q.batch : 1));
@@ -668,6 +677,7 @@ hipError_t launch_gemm_ste(const GemmLaunch& q, int k, hipStream_t st) {
   a.Yt = nullptr; a.out = nullptr; a.partials = nullptr; a.scale = q.scale;
   a.ste = q.ste;
   a.bsa = a.bsb = a.bso = 0;
+  a.causal = 0;
   a.tiles_m = int((q.M + 255) / 256);
   a.tiles_n = int((q.N + 255) / 256);
   const dim3 grid(unsigned(a.tiles_m * a.tiles_n));

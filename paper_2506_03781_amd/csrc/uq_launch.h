@@ -101,6 +101,7 @@ struct GemmLaunch {
   // strided batch (EPI_GRAD_*): batch > 1 products, operands and output of
   // batch b at A + b bsa, B + b bsb (elements), out + b bso (bytes)
   int64_t batch, bsa, bsb, bso;
+  int causal;  // 0, or the causal mode of square attention products (see gemm.hip)
 };
 
 // Deployment form (bit-planes + binary16 Theta*_B) and its product.

@@ -60,7 +60,8 @@ _SIGS = {
     "uniquan_gemm_nt": ([_i64, _i64, _i64, _vp, _vp, _vp, _i32, _f32, _vp], _i32),
     "uniquan_silu_mul_fwd": ([_i64, _vp, _vp, _vp, _vp], _i32),
     "uniquan_silu_mul_bwd": ([_i64, _vp, _vp, _vp, _vp, _vp, _vp], _i32),
-    "uniquan_gemm_nt_batched": ([_i64, _i64, _i64, _i64, _vp, _i64, _vp, _i64, _vp, _i64, _i32, _f32, _vp], _i32),
+    "uniquan_gemm_nt_batched": ([_i64, _i64, _i64, _i64, _vp, _i64, _vp, _i64, _vp, _i64, _i32, _f32, _i32, _vp],
+                                _i32),
     "uniquan_add_rmsnorm": ([_i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp], _i32),
     "uniquan_rmsnorm_bwd": ([_i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _f32, _vp, _vp, _vp], _i32),
     "uniquan_rope_split": ([_i64, _i32, _i32, _i32, _vp, _i32, _i32, _vp, _vp], _i32),
@@ -378,13 +379,16 @@ def uniquan_silu_mul_bwd(dH, G, U, dG, dU, stream=None):
                                       _p(dG, n, _B, "dG"), _p(dU, n, _B, "dU"), _stream(stream)))
 
 
-def uniquan_gemm_nt_batched(M, N, K, batch, A, stride_a, B, stride_b, out, stride_out, scale=1.0, stream=None):
-    """out_b = scale * A_b B_b^T for b < batch (strides in elements; 0 repeats an operand)."""
+def uniquan_gemm_nt_batched(M, N, K, batch, A, stride_a, B, stride_b, out, stride_out, scale=1.0, causal=0,
+                            stream=None):
+    """out_b = scale * A_b B_b^T for b < batch (strides in elements; 0 repeats an operand);
+    causal 1/2/3 as declared in the header."""
     na = (batch - 1) * stride_a + M * K
     nb = (batch - 1) * stride_b + N * K
     no = (batch - 1) * stride_out + M * N
     _check(lib().uniquan_gemm_nt_batched(M, N, K, batch, _p(A, na, _B, "A"), stride_a, _p(B, nb, _B, "B"), stride_b,
-                                         _p(out, no, _W, "out"), stride_out, _dt(out), float(scale), _stream(stream)))
+                                         _p(out, no, _W, "out"), stride_out, _dt(out), float(scale), int(causal),
+                                         _stream(stream)))
 
 
 def uniquan_add_rmsnorm(T, C, X, A, gamma, R, Z, rinv, stream=None):

@@ -246,13 +246,17 @@ def test_record_propagates_and_resets(L):
 def test_decoder_entry_validation(L):
     B, F = uq.UQ_BF16, uq.UQ_F32
     g = L.uniquan_gemm_nt_batched
-    assert g(8, 8, 8, 0, FAKE, 64, FAKE, 64, FAKE, 64, F, 1.0, None) == uq.UQ_EINVAL
-    assert g(8, 8, 8, 70000, FAKE, 64, FAKE, 64, FAKE, 64, F, 1.0, None) == uq.UQ_EINVAL
-    assert g(8, 8, 8, 2, FAKE, 64, FAKE, 64, FAKE, 32, F, 1.0, None) == uq.UQ_EINVAL
+    assert g(8, 8, 8, 0, FAKE, 64, FAKE, 64, FAKE, 64, F, 1.0, 0, None) == uq.UQ_EINVAL
+    assert g(8, 8, 8, 70000, FAKE, 64, FAKE, 64, FAKE, 64, F, 1.0, 0, None) == uq.UQ_EINVAL
+    assert g(8, 8, 8, 2, FAKE, 64, FAKE, 64, FAKE, 32, F, 1.0, 0, None) == uq.UQ_EINVAL
     assert "stride_out" in uq.last_error()
-    assert g(8, 8, 8, 2, FAKE, 4, FAKE, 64, FAKE, 64, F, 1.0, None) == uq.UQ_EINVAL
-    assert g(8, 12, 8, 2, FAKE, 64, FAKE, 96, FAKE, 96, F, 1.0, None) == uq.UQ_EINVAL
-    assert g(8, 8, 8, 2, ODD, 64, FAKE, 64, FAKE, 64, F, 1.0, None) == uq.UQ_EINVAL
+    assert g(8, 8, 8, 2, FAKE, 4, FAKE, 64, FAKE, 64, F, 1.0, 0, None) == uq.UQ_EINVAL
+    assert g(8, 12, 8, 2, FAKE, 64, FAKE, 96, FAKE, 96, F, 1.0, 0, None) == uq.UQ_EINVAL
+    assert g(8, 8, 8, 2, ODD, 64, FAKE, 64, FAKE, 64, F, 1.0, 0, None) == uq.UQ_EINVAL
+    assert g(64, 64, 64, 2, FAKE, 4096, FAKE, 4096, FAKE, 4096, F, 1.0, 4, None) == uq.UQ_EINVAL
+    assert g(64, 64, 40, 2, FAKE, 2560, FAKE, 2560, FAKE, 4096, F, 1.0, 1, None) == uq.UQ_EINVAL   # K % 32
+    assert g(64, 32, 64, 2, FAKE, 4096, FAKE, 2048, FAKE, 2048, F, 1.0, 1, None) == uq.UQ_EINVAL   # M != N
+    assert g(64, 32, 32, 2, FAKE, 2048, FAKE, 1024, FAKE, 2048, F, 1.0, 2, None) == uq.UQ_EINVAL   # M != K
     assert L.uniquan_add_rmsnorm(4, 12, FAKE, None, FAKE, None, FAKE, FAKE, None) == uq.UQ_EINVAL
     assert L.uniquan_add_rmsnorm(4, 16, FAKE, FAKE, FAKE, None, FAKE, FAKE, None) == uq.UQ_EINVAL
     assert "R must be given" in uq.last_error()

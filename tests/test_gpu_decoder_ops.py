@@ -187,3 +187,32 @@ def test_block_loss(n):
     assert np.array_equal(host(E), bfr(e))
     ref = float(np.sum(e.astype(np.float64) ** 2))
     assert abs(float(loss.item()) - ref) <= 1e-5 * ref
+
+
+@pytest.mark.parametrize("L,N,batch", [(96, 64, 3), (256, 128, 2), (2048, 128, 2)])
+def test_gemm_nt_batched_causal(L, N, batch):
+    """Causal modes against the full product: mode 1 on j <= i; modes 2 and 3
+    (operands zero above / below the diagonal) bit-identical everywhere."""
+    rs = np.random.default_rng(L + N)
+    full32 = lambda M_, N_, K_, a, b, o, causal: uq.uniquan_gemm_nt_batched(  # noqa: E731
+        M_, N_, K_, batch, a, M_ * K_, b, N_ * K_, o, M_ * N_, 1.0, causal)
+    # mode 1: scores, M == N == L, K = 128
+    Q = torch.from_numpy(bfr(rs.standard_normal((batch, L, 128))).astype(F32)).to("cuda").to(torch.bfloat16)
+    Kt = torch.from_numpy(bfr(rs.standard_normal((batch, L, 128))).astype(F32)).to("cuda").to(torch.bfloat16)
+    S0 = torch.zeros(batch, L, L, device="cuda")
+    S1 = torch.full((batch, L, L), 7.0, device="cuda")
+    full32(L, L, 128, Q, Kt, S0, 0)
+    full32(L, L, 128, Q, Kt, S1, 1)
+    torch.cuda.synchronize()
+    low = np.tril(np.ones((L, L), dtype=bool))
+    assert np.array_equal(host(S1)[:, low], host(S0)[:, low])
+    # modes 2 and 3: A [L, L] triangular, B [N, L]
+    Bm = torch.from_numpy(bfr(rs.standard_normal((batch, N, L))).astype(F32)).to("cuda").to(torch.bfloat16)
+    for mode, tri in ((2, np.tril), (3, np.triu)):
+        A = torch.from_numpy(tri(bfr(rs.standard_normal((batch, L, L)))).astype(F32)).to("cuda").to(torch.bfloat16)
+        O0 = torch.zeros(batch, L, N, device="cuda")
+        O1 = torch.full((batch, L, N), 7.0, device="cuda")
+        full32(L, N, L, A, Bm, O0, 0)
+        full32(L, N, L, A, Bm, O1, mode)
+        torch.cuda.synchronize()
+        assert np.array_equal(host(O1), host(O0)), mode
