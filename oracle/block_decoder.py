@@ -13,8 +13,11 @@ This oracle takes the standard pre-norm form of those models (the readings
 are listed with the design notes):
 
     Z1 = RMSNorm(X; g1)
-    Q = RoPE(Z1 W_q^T), K = RoPE(Z1 W_k^T), V = Z1 W_v^T     (H heads of d = C / H)
-    P = causal softmax(Q_h K_h^T / sqrt(d)) per sequence and head
+    Q = RoPE(Z1 W_q^T)  (H heads of d = C / H),
+    K = RoPE(Z1 W_k^T), V = Z1 W_v^T  (H_kv heads of d; query head h uses
+    key/value head h // (H / H_kv): grouped-query attention, the form of
+    the Mistral and Llama-3 blocks; H_kv = H is multi-head attention)
+    P = causal softmax(Q_h K_kv(h)^T / sqrt(d)) per sequence and head
     O = concat_h(P V_h),  A = O W_o^T,  R = X + A
     Z2 = RMSNorm(R; g2),  Y = R + silu(Z2 W_g^T) * (Z2 W_u^T) W_d^T
 
@@ -100,22 +103,26 @@ def causal_softmax(S):
     return e / np.sum(e, axis=-1, keepdims=True)
 
 
-def decoder_forward(X, W, g1, g2, n_seq, H, store=_ident):
+def decoder_forward(X, W, g1, g2, n_seq, H, store=_ident, n_kv=None):
     """All intermediates of the block on input X [T, C] with weights
-    W = dict(q, k, v, o [C, C], g, u [I, C], d [C, I])."""
+    W = dict(q, o [C, C], k, v [n_kv d, C], g, u [I, C], d [C, I])
+    (n_kv key/value heads, H by default)."""
     X = np.asarray(X, F64)
     T, C = X.shape
     d = C // H
+    n_kv = H if n_kv is None else n_kv
+    grp = H // n_kv                      # query heads per key/value head
     ang = rope_angles(T // n_seq, d)
     Wf = {n: np.asarray(w, F64) for n, w in W.items()}
     Z1r, r1 = rmsnorm(X, g1)
     Z1 = store(Z1r)
     Qh = store(rope(split_heads(Z1 @ Wf["q"].T, n_seq, H), ang))
-    Kh = store(rope(split_heads(Z1 @ Wf["k"].T, n_seq, H), ang))
-    Vh = store(split_heads(Z1 @ Wf["v"].T, n_seq, H))
-    S = Qh @ np.swapaxes(Kh, -1, -2) / np.sqrt(d)
+    Kh = store(rope(split_heads(Z1 @ Wf["k"].T, n_seq, n_kv), ang))
+    Vh = store(split_heads(Z1 @ Wf["v"].T, n_seq, n_kv))
+    Kx, Vx = np.repeat(Kh, grp, axis=1), np.repeat(Vh, grp, axis=1)   # head h reads key/value head h // grp
+    S = Qh @ np.swapaxes(Kx, -1, -2) / np.sqrt(d)
     P = store(causal_softmax(S))
-    O = store(merge_heads(P @ Vh))
+    O = store(merge_heads(P @ Vx))
     A = O @ Wf["o"].T
     R = X + A
     Z2r, r2 = rmsnorm(R, g2)
@@ -124,15 +131,16 @@ def decoder_forward(X, W, g1, g2, n_seq, H, store=_ident):
     U = store(Z2 @ Wf["u"].T)
     Hm = store(silu(G) * U)
     Y = R + Hm @ Wf["d"].T
-    return dict(Z1=Z1, r1=r1, Qh=Qh, Kh=Kh, Vh=Vh, S=S, P=P, O=O, A=A, R=R, Z2=Z2, r2=r2, G=G, U=U, H=Hm, Y=Y,
-                ang=ang)
+    return dict(Z1=Z1, r1=r1, Qh=Qh, Kh=Kh, Vh=Vh, Kx=Kx, Vx=Vx, S=S, P=P, O=O, A=A, R=R, Z2=Z2, r2=r2, G=G, U=U,
+                H=Hm, Y=Y, ang=ang, n_kv=n_kv)
 
 
-def decoder_step(Xhat, Y_ref, W, g1, g2, n_seq, H, store=_ident):
+def decoder_step(Xhat, Y_ref, W, g1, g2, n_seq, H, store=_ident, n_kv=None):
     """Loss ||Y(Xhat; W) - Y_ref||_F^2 and its gradient for each of the seven
     matrices (Algorithm 1's backpropagation; the input and the norm weights
     are not trained)."""
-    f = decoder_forward(Xhat, W, g1, g2, n_seq, H, store)
+    f = decoder_forward(Xhat, W, g1, g2, n_seq, H, store, n_kv)
+    grp = H // f["n_kv"]
     Wf = {n: np.asarray(w, F64) for n, w in W.items()}
     T, C = f["R"].shape
     d = C // H
@@ -153,13 +161,17 @@ def decoder_step(Xhat, Y_ref, W, g1, g2, n_seq, H, store=_ident):
     dA = store(dR)
     go = dA.T @ f["O"]
     dOh = split_heads(store(dA @ Wf["o"]), n_seq, H)
-    dP = dOh @ np.swapaxes(f["Vh"], -1, -2)
+    dP = dOh @ np.swapaxes(f["Vx"], -1, -2)
     dS = store(f["P"] * (dP - np.sum(dP * f["P"], axis=-1, keepdims=True)))
-    dQh = dS @ f["Kh"] / np.sqrt(d)
-    dKh = np.swapaxes(dS, -1, -2) @ f["Qh"] / np.sqrt(d)
-    dVh = store(np.swapaxes(f["P"], -1, -2) @ dOh)
+    dQh = dS @ f["Kx"] / np.sqrt(d)
+
+    def group_sum(x):  # per query head -> per key/value head
+        n, Hq, L, dd = x.shape
+        return x.reshape(n, Hq // grp, grp, L, dd).sum(axis=2)
+    dKh = group_sum(np.swapaxes(dS, -1, -2) @ f["Qh"] / np.sqrt(d))
+    dVh = group_sum(np.swapaxes(f["P"], -1, -2) @ dOh)
     dQ = store(merge_heads(rope(dQh, f["ang"], inverse=True)))
     dK = store(merge_heads(rope(dKh, f["ang"], inverse=True)))
-    dV = merge_heads(dVh)
+    dV = store(merge_heads(dVh))
     grads = dict(q=dQ.T @ f["Z1"], k=dK.T @ f["Z1"], v=dV.T @ f["Z1"], o=go, g=gg, u=gu, d=gd)
     return dict(loss=loss, E=E, grads=grads, dR=dR, dZ2=dZ2, dS=dS, dQ=dQ, dK=dK, dV=dV, **f)

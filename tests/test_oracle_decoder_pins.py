@@ -18,12 +18,13 @@ import oracle.uniquan as U
 F64 = np.float64
 
 
-def tiny(seed, n_seq=2, L=3, C=8, H=2, I=12, scale=0.6):
+def tiny(seed, n_seq=2, L=3, C=8, H=2, I=12, scale=0.6, n_kv=None):
     rs = np.random.default_rng(seed)
     T = n_seq * L
+    Ckv = C // H * (H if n_kv is None else n_kv)
     X = rs.standard_normal((T, C))
     W = {n: rs.standard_normal(sh) * scale for n, sh in
-         (("q", (C, C)), ("k", (C, C)), ("v", (C, C)), ("o", (C, C)), ("g", (I, C)), ("u", (I, C)), ("d", (C, I)))}
+         (("q", (C, C)), ("k", (Ckv, C)), ("v", (Ckv, C)), ("o", (C, C)), ("g", (I, C)), ("u", (I, C)), ("d", (C, I)))}
     g1 = 1.0 + 0.2 * rs.standard_normal(C)
     g2 = 1.0 + 0.2 * rs.standard_normal(C)
     Y_ref = rs.standard_normal((T, C))
@@ -144,20 +145,23 @@ def pin_forward_loops():
 
 
 def pin_gradients_finite_differences():
-    X, W, g1, g2, Y_ref, n_seq, H = tiny(4)
-    st = D.decoder_step(X, Y_ref, W, g1, g2, n_seq, H)
-    h = 1e-6
-    for name in W:
-        num = np.zeros_like(W[name])
-        for idx in np.ndindex(W[name].shape):
-            Wp = {n: w.copy() for n, w in W.items()}
-            Wm = {n: w.copy() for n, w in W.items()}
-            Wp[name][idx] += h
-            Wm[name][idx] -= h
-            num[idx] = (D.decoder_step(X, Y_ref, Wp, g1, g2, n_seq, H)["loss"]
-                        - D.decoder_step(X, Y_ref, Wm, g1, g2, n_seq, H)["loss"]) / (2 * h)
-        scale = max(1.0, np.max(np.abs(num)))
-        assert np.allclose(st["grads"][name], num, rtol=1e-5, atol=1e-6 * scale), (name, np.max(np.abs(st["grads"][name] - num)))
+    # multi-head (2 heads) and grouped-query (4 query heads sharing 2 key/value heads)
+    for kw in (dict(H=2), dict(H=4, n_kv=2)):
+        X, W, g1, g2, Y_ref, n_seq, H = tiny(4, **kw)
+        nkv = kw.get("n_kv")
+        st = D.decoder_step(X, Y_ref, W, g1, g2, n_seq, H, n_kv=nkv)
+        h = 1e-6
+        for name in W:
+            num = np.zeros_like(W[name])
+            for idx in np.ndindex(W[name].shape):
+                Wp = {n: w.copy() for n, w in W.items()}
+                Wm = {n: w.copy() for n, w in W.items()}
+                Wp[name][idx] += h
+                Wm[name][idx] -= h
+                num[idx] = (D.decoder_step(X, Y_ref, Wp, g1, g2, n_seq, H, n_kv=nkv)["loss"]
+                            - D.decoder_step(X, Y_ref, Wm, g1, g2, n_seq, H, n_kv=nkv)["loss"]) / (2 * h)
+            scale = max(1.0, np.max(np.abs(num)))
+            assert np.allclose(st["grads"][name], num, rtol=1e-5, atol=1e-6 * scale), (kw, name)
 
 
 def pin_zero_loss():
@@ -188,8 +192,28 @@ def pin_reduces_to_mlp():
     assert np.allclose(f["Y"], X + M.mlp_forward(z, W["g"], W["u"], W["d"])["Y"], rtol=1e-13, atol=1e-13)
 
 
+def pin_grouped_heads():
+    """Grouped-query attention equals multi-head attention whose key/value
+    projections repeat each shared head's rows for every query head of its
+    group; with as many key/value heads as query heads it is multi-head."""
+    X, W, g1, g2, Y_ref, n_seq, H = tiny(9, C=16, H=4, n_kv=2)
+    d, G = 16 // 4, 2
+    Wm = dict(W)
+    for n in ("k", "v"):
+        Wm[n] = np.concatenate([W[n][kv * d:(kv + 1) * d] for kv in range(2) for _ in range(G)], axis=0)
+    a = D.decoder_forward(X, W, g1, g2, n_seq, H, n_kv=2)["Y"]
+    b = D.decoder_forward(X, Wm, g1, g2, n_seq, H)["Y"]
+    assert np.allclose(a, b, rtol=1e-12, atol=1e-12)
+    st_g = D.decoder_step(X, Y_ref, W, g1, g2, n_seq, H, n_kv=2)
+    st_m = D.decoder_step(X, Y_ref, Wm, g1, g2, n_seq, H)
+    for n in ("k", "v"):   # the shared head's gradient is the sum over its group's copies
+        summed = sum(st_m["grads"][n].reshape(2, G, d, 16)[:, g] for g in range(G)).reshape(2 * d, 16)
+        assert np.allclose(st_g["grads"][n], summed, rtol=1e-10, atol=1e-12), n
+    assert np.allclose(D.decoder_forward(X, Wm, g1, g2, n_seq, H, n_kv=4)["Y"], b)
+
+
 PINS = [pin_rmsnorm, pin_rope, pin_causal_softmax, pin_forward_loops, pin_gradients_finite_differences,
-        pin_zero_loss, pin_store_hook, pin_reduces_to_mlp]
+        pin_zero_loss, pin_store_hook, pin_reduces_to_mlp, pin_grouped_heads]
 
 
 @pytest.mark.parametrize("pin", PINS, ids=[p.__name__ for p in PINS])
