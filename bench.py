@@ -119,6 +119,8 @@ def parse():
                     help="loss against a stored fp32 target Y = X W^T instead of the residual form")
     ap.add_argument("--no-block", action="store_true",
                     help="skip the block-level step on a 7B decoder block (8192 tokens, 32 heads, I = 11008)")
+    ap.add_argument("--block-kv", type=int, default=None,
+                    help="key/value heads of the decoder block (default 32, multi-head; 8 for grouped-query)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run a plain 256 MiB device copy (counter calibration)")
     return ap.parse_args()
@@ -288,13 +290,14 @@ def bcq_inference(layers, batches=(1, 8), target_bytes=512 << 20):
     return res
 
 
-def block_decoder(seed, k=3, steps=5, warmup=2):
+def block_decoder(seed, k=3, steps=5, warmup=2, n_kv=None):
     """Block-level reconstruction of a 7B decoder block (Algorithm 1 with f =
     one rotary causal attention module and one SiLU-gated MLP module): per
     step the seven fake-quant forwards, the block's forward on What, the
     loss, backpropagation to all seven matrices and the straight-through
     backward with the SGD update.  8192 tokens as 4 sequences of 2048,
-    C = 4096 in 32 heads of 128, I = 11008."""
+    C = 4096 in 32 heads of 128, I = 11008; n_kv key/value heads (32 by
+    default; 8 gives the grouped-query form with k, v of [1024, 4096])."""
     import numpy as np
     import torch
 
@@ -304,10 +307,14 @@ def block_decoder(seed, k=3, steps=5, warmup=2):
     wl = synth.WORKLOADS["block7b"]
     g = wl.group_size
     n_seq, H = 4, 32
+    n_kv = H if n_kv is None else n_kv
     mats, X = {}, None
     for name, spec in zip(DecoderBlock.NAMES, wl.matrices):
         # only the first matrix's activations are used; the weights do not depend on T
-        m = synth.make_matrix(spec if X is None else synth.scaled(spec, T=8), seed)
+        sc = synth.scaled(spec, T=8) if X is not None else spec
+        if name in ("k", "v"):
+            sc = synth.scaled(sc, R=spec.R * n_kv // H)
+        m = synth.make_matrix(sc, seed)
         if X is None:
             X = m.X
         q = QuantMatrix(m.W, m.s, k, g)
@@ -318,7 +325,7 @@ def block_decoder(seed, k=3, steps=5, warmup=2):
     C = mats["q"].C
     g1 = (1.0 + 0.1 * rs.standard_normal(C)).astype(np.float32)
     g2 = (1.0 + 0.1 * rs.standard_normal(C)).astype(np.float32)
-    blk = DecoderBlock(mats, g1, g2, X.shape[0], n_seq, H)
+    blk = DecoderBlock(mats, g1, g2, X.shape[0], n_seq, H, n_kv=n_kv)
     blk.prepare(X)
     blk.set_input(X)
     # SGD on L / L0 (one step with zero learning rates measures L0)
@@ -358,7 +365,7 @@ def block_decoder(seed, k=3, steps=5, warmup=2):
     tf = flops / (ms * 1e-3) / 1e12
     n_w = sum(q.R * q.C for q in mats.values())
     last = float(blk.loss.item()) / l0
-    return {"T": blk.T, "C": blk.C, "I": blk.I, "heads": H, "seq_len": blk.L, "n_seq": n_seq, "k": k, "g": g,
+    return {"T": blk.T, "C": blk.C, "I": blk.I, "heads": H, "kv_heads": n_kv, "seq_len": blk.L, "n_seq": n_seq, "k": k, "g": g,
             "steps": steps, "ms_per_step": ms, "gweights_per_s": n_w / (ms * 1e-3) / 1e9,
             "gemm_flops_per_step": flops, "tflops_effective": tf, "frac_mfma": tf / MFMA_BF16_PEAK_TFLOPS,
             "phase_ms": phases, "loss_init": l0, "rel_loss_warmup": rel, "rel_loss_last": last,
@@ -571,7 +578,7 @@ def main():
                          "and SGD update in its epilogue (dL/dWhat never written)"}
 
     bcq = bcq_inference(layers)
-    blk = None if args.no_block else block_decoder(args.seed)
+    blk = None if args.no_block else block_decoder(args.seed, n_kv=args.block_kv)
 
     out = {
         "metric": "fake-quant fwd+bwd Gweights/s (%HBM peak); recon GEMM TFLOP/s (%MFMA)",

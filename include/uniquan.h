@@ -422,15 +422,21 @@ uq_status uniquan_rmsnorm_bwd(int64_t T, int64_t C, const float* dZa,
  * uniquan_rope_split -- token-major in [T, H d] (UQ_F32 or UQ_BF16) to
  * head-major bf16 out [H, T, d]; with rotate != 0 each pair (i, i + d/2) of
  * token t is rotated by angle (t mod L) 1e4^(-2i/d).  d even, L divides T.
- * uniquan_rope_merge -- the inverse layout change (head-major in, token-
- * major bf16 out), rotating by minus the angle when rotate != 0.
+ * group (dividing H; 1 for the plain order) stores head h at slot
+ * (h mod group) (H / group) + h / group: for grouped-query attention with
+ * group query heads per key/value head, the query heads at one position of
+ * their groups become contiguous in key/value head order.
+ * uniquan_rope_merge -- the inverse layout change (head-major in with the
+ * same slot order, token-major bf16 out), rotating by minus the angle when
+ * rotate != 0; the input holds nsum stacked [H, T, d] partials that are
+ * summed first (the gradient of a shared key/value head, nsum = group size).
  */
-uq_status uniquan_rope_split(int64_t T, int H, int d, int L, const void* in,
-                             int in_dtype, int rotate, uint16_t* out,
-                             void* stream);
-uq_status uniquan_rope_merge(int64_t T, int H, int d, int L, const void* in,
-                             int in_dtype, int rotate, uint16_t* out,
-                             void* stream);
+uq_status uniquan_rope_split(int64_t T, int H, int d, int L, int group,
+                             const void* in, int in_dtype, int rotate,
+                             uint16_t* out, void* stream);
+uq_status uniquan_rope_merge(int64_t T, int H, int d, int L, int group,
+                             int nsum, const void* in, int in_dtype, int rotate,
+                             uint16_t* out, void* stream);
 
 /*
  * uniquan_softmax_causal -- for each row r < rows of S [rows, L] (fp32, row

@@ -128,10 +128,12 @@ class MLPBlock:
 class DecoderBlock:
     """One whole Transformer block (Algorithm 1 with f = one multi-head
     attention module and one MLP module): pre-norm, rotary causal attention
-    over n_seq sequences of L = T / n_seq tokens with H heads of d = C / H,
-    and the SiLU-gated MLP.  The seven matrices are QuantMatrix objects
-    (q, k, v, o [C, C]; g, u [I, C]; d [C, I]); g1, g2 are the norms'
-    weights (not trained).
+    over n_seq sequences of L = T / n_seq tokens with H query heads of
+    d = C / H and n_kv key/value heads (grouped-query attention, each shared
+    by H / n_kv query heads; n_kv = H by default), and the SiLU-gated MLP.
+    The seven matrices are QuantMatrix objects (q, o [C, C]; k, v
+    [n_kv d, C]; g, u [I, C]; d [C, I]); g1, g2 are the norms' weights (not
+    trained).
 
     ``prepare(X)`` computes the full-precision block's output on the
     full-precision input X (the target); ``set_input(Xhat)`` gives the
@@ -145,29 +147,39 @@ class DecoderBlock:
 
     NAMES = ("q", "k", "v", "o", "g", "u", "d")
 
-    def __init__(self, mats: dict, g1, g2, T, n_seq, H, device="cuda"):
+    def __init__(self, mats: dict, g1, g2, T, n_seq, H, n_kv=None, device="cuda"):
         q, gm = mats["q"], mats["g"]
         C, I = q.C, gm.R
-        assert C % H == 0 and T % n_seq == 0
+        n_kv = H if n_kv is None else n_kv
+        assert C % H == 0 and T % n_seq == 0 and H % n_kv == 0
         self.mats, self.T, self.C, self.I, self.H, self.n_seq = mats, T, C, I, H, n_seq
         self.d, self.L = C // H, T // n_seq
+        self.Hkv, self.grp = n_kv, H // n_kv
+        self.Ckv = n_kv * self.d
+        assert mats["k"].R == self.Ckv and mats["v"].R == self.Ckv
         self.B = H * n_seq
-        T, L, d, B = self.T, self.L, self.d, self.B
+        self.Bkv = n_kv * n_seq
+        T, L, d, B, Ckv, Bkv = self.T, self.L, self.d, self.B, self.Ckv, self.Bkv
         f32 = dict(dtype=torch.float32, device=device)
         b16 = dict(dtype=torch.bfloat16, device=device)
         e = torch.empty
         self.g1 = to_dev(g1, torch.float32, device)
         self.g2 = to_dev(g2, torch.float32, device)
         self.Xhat, self.Yref, self.A32, self.R, self.M32, self.Yhat = (e(T, C, **f32) for _ in range(6))
-        self.Qf, self.Kf, self.dZa, self.dZb = (e(T, C, **f32) for _ in range(4))
+        self.Qf, self.dZa, self.dZb = (e(T, C, **f32) for _ in range(3))
+        self.Kf = e(T, Ckv, **f32)
         self.r1, self.r2 = e(T, **f32), e(T, **f32)
-        (self.Z1, self.Vb, self.O, self.Z2, self.E, self.dA, self.dO, self.dQ, self.dK,
-         self.dV) = (e(T, C, **b16) for _ in range(10))
-        (self.Z1t, self.Ot, self.Z2t, self.Et, self.dAt, self.dQt, self.dKt,
-         self.dVt) = (e(C, T, **b16) for _ in range(8))
-        self.Qh, self.Kh, self.Vh, self.Oh, self.dOh, self.dVh = (e(B, L, d, **b16) for _ in range(6))
-        self.Qt, self.Kt, self.Vt, self.dOt = (e(B, d, L, **b16) for _ in range(4))
-        self.dQr, self.dKr = e(B, L, d, **f32), e(B, L, d, **f32)
+        (self.Z1, self.O, self.Z2, self.E, self.dA, self.dO, self.dQ) = (e(T, C, **b16) for _ in range(7))
+        self.Vb, self.dK, self.dV = (e(T, Ckv, **b16) for _ in range(3))
+        (self.Z1t, self.Ot, self.Z2t, self.Et, self.dAt, self.dQt) = (e(C, T, **b16) for _ in range(6))
+        self.dKt, self.dVt = e(Ckv, T, **b16), e(Ckv, T, **b16)
+        # query heads in grouped slot order (see uniquan_rope_split), key/value heads plain
+        self.Qh, self.Oh, self.dOh = (e(B, L, d, **b16) for _ in range(3))
+        self.Kh, self.Vh = e(Bkv, L, d, **b16), e(Bkv, L, d, **b16)
+        self.Qt, self.dOt = e(B, d, L, **b16), e(B, d, L, **b16)
+        self.Kt, self.Vt = e(Bkv, d, L, **b16), e(Bkv, d, L, **b16)
+        # dQ per query head; dK, dV per query head = grp stacked partials per key/value head
+        self.dQr, self.dKp, self.dVp = (e(B, L, d, **f32) for _ in range(3))
         self.S, self.dP = e(B, L, L, **f32), e(B, L, L, **f32)
         self.P, self.Pt, self.dS, self.dSt = (e(B, L, L, **b16) for _ in range(4))
         self.Gt, self.Ut, self.Ht, self.dHt, self.dGt, self.dUt = (e(I, T, **b16) for _ in range(6))
@@ -185,17 +197,22 @@ class DecoderBlock:
         T, C, I, H, d, L, B = self.T, self.C, self.I, self.H, self.d, self.L, self.B
         sc = 1.0 / float(d) ** 0.5
         uq.uniquan_add_rmsnorm(T, C, X, None, self.g1, None, self.Z1, self.r1)
+        Hkv, Ckv, Bkv, grp = self.Hkv, self.Ckv, self.Bkv, self.grp
         uq.uniquan_gemm_nt(T, C, C, self.Z1, W["q"], self.Qf)
-        uq.uniquan_gemm_nt(T, C, C, self.Z1, W["k"], self.Kf)
-        uq.uniquan_gemm_nt(T, C, C, self.Z1, W["v"], self.Vb)
-        uq.uniquan_rope_split(T, H, d, L, self.Qf, self.Qh, rotate=True)
-        uq.uniquan_rope_split(T, H, d, L, self.Kf, self.Kh, rotate=True)
-        uq.uniquan_rope_split(T, H, d, L, self.Vb, self.Vh, rotate=False)
-        uq.uniquan_gemm_nt_batched(L, L, d, B, self.Qh, L * d, self.Kh, L * d, self.S, L * L, sc, causal=1)
+        uq.uniquan_gemm_nt(T, Ckv, C, self.Z1, W["k"], self.Kf)
+        uq.uniquan_gemm_nt(T, Ckv, C, self.Z1, W["v"], self.Vb)
+        uq.uniquan_rope_split(T, H, d, L, self.Qf, self.Qh, rotate=True, group=grp)
+        uq.uniquan_rope_split(T, Hkv, d, L, self.Kf, self.Kh, rotate=True)
+        uq.uniquan_rope_split(T, Hkv, d, L, self.Vb, self.Vh, rotate=False)
+        uq.uniquan_transpose_bf16_batched(Bkv, L, d, self.Vh, self.Vt)
+        for g in range(grp):   # query heads at group position g against every key/value head
+            uq.uniquan_gemm_nt_batched(L, L, d, Bkv, self._q(self.Qh, g, L * d), L * d, self.Kh, L * d,
+                                       self._q(self.S, g, L * L), L * L, sc, causal=1)
         uq.uniquan_softmax_causal(B * L, L, self.S, self.P)
-        uq.uniquan_transpose_bf16_batched(B, L, d, self.Vh, self.Vt)
-        uq.uniquan_gemm_nt_batched(L, d, L, B, self.P, L * L, self.Vt, d * L, self.Oh, L * d, causal=2)
-        uq.uniquan_rope_merge(T, H, d, L, self.Oh, self.O, rotate=False)
+        for g in range(grp):
+            uq.uniquan_gemm_nt_batched(L, d, L, Bkv, self._q(self.P, g, L * L), L * L, self.Vt, d * L,
+                                       self._q(self.Oh, g, L * d), L * d, causal=2)
+        uq.uniquan_rope_merge(T, H, d, L, self.Oh, self.O, rotate=False, group=grp)
         uq.uniquan_gemm_nt(T, C, C, self.O, W["o"], self.A32)
         uq.uniquan_add_rmsnorm(T, C, X, self.A32, self.g2, self.R, self.Z2, self.r2)
         uq.uniquan_gemm_nt(I, T, C, W["g"], self.Z2, self.Gt)
@@ -203,6 +220,11 @@ class DecoderBlock:
         uq.uniquan_silu_mul_fwd(self.Gt, self.Ut, self.Ht)
         uq.uniquan_transpose_bf16(I, T, self.Ht, self.Hm)
         uq.uniquan_gemm_nt(T, C, I, self.Hm, W["d"], self.M32)
+
+    def _q(self, x, g, per):
+        """Batches of group position g of a query-head buffer (grp blocks of Bkv batches of `per` elements)."""
+        n = self.Bkv * per
+        return x.view(-1)[g * n:(g + 1) * n]
 
     def _sum_out(self, out):
         """out = R + M (fp32), through the residual-add path of the norm kernel."""
@@ -266,24 +288,35 @@ class DecoderBlock:
         uq.uniquan_gemm_nt(C, C, T, self.dAt, self.Ot, m["o"].G)
         uq.uniquan_transpose_bf16(C, C, Wh["o"], self.WoT)
         uq.uniquan_gemm_nt(T, C, C, self.dA, self.WoT, self.dO)
-        uq.uniquan_rope_split(T, H, d, L, self.dO, self.dOh, rotate=False)
-        uq.uniquan_gemm_nt_batched(L, L, d, B, self.dOh, L * d, self.Vh, L * d, self.dP, L * L, causal=1)
+        Hkv, Ckv, Bkv, grp = self.Hkv, self.Ckv, self.Bkv, self.grp
+        q = self._q
+        uq.uniquan_rope_split(T, H, d, L, self.dO, self.dOh, rotate=False, group=grp)
+        for g in range(grp):
+            uq.uniquan_gemm_nt_batched(L, L, d, Bkv, q(self.dOh, g, L * d), L * d, self.Vh, L * d,
+                                       q(self.dP, g, L * L), L * L, causal=1)
         uq.uniquan_softmax_causal_bwd(B * L, L, self.dP, self.P, self.dS)
-        uq.uniquan_transpose_bf16_batched(B, L, d, self.Kh, self.Kt)
-        uq.uniquan_gemm_nt_batched(L, d, L, B, self.dS, L * L, self.Kt, d * L, self.dQr, L * d, sc, causal=2)
+        uq.uniquan_transpose_bf16_batched(Bkv, L, d, self.Kh, self.Kt)
         uq.uniquan_transpose_bf16_batched(B, L, L, self.dS, self.dSt)
         uq.uniquan_transpose_bf16_batched(B, L, d, self.Qh, self.Qt)
-        uq.uniquan_gemm_nt_batched(L, d, L, B, self.dSt, L * L, self.Qt, d * L, self.dKr, L * d, sc, causal=3)
         uq.uniquan_transpose_bf16_batched(B, L, L, self.P, self.Pt)
         uq.uniquan_transpose_bf16_batched(B, L, d, self.dOh, self.dOt)
-        uq.uniquan_gemm_nt_batched(L, d, L, B, self.Pt, L * L, self.dOt, d * L, self.dVh, L * d, causal=3)
-        uq.uniquan_rope_merge(T, H, d, L, self.dQr, self.dQ, rotate=True)
-        uq.uniquan_rope_merge(T, H, d, L, self.dKr, self.dK, rotate=True)
-        uq.uniquan_rope_merge(T, H, d, L, self.dVh, self.dV, rotate=False)
+        for g in range(grp):
+            uq.uniquan_gemm_nt_batched(L, d, L, Bkv, q(self.dS, g, L * L), L * L, self.Kt, d * L,
+                                       q(self.dQr, g, L * d), L * d, sc, causal=2)
+            # partial g of each shared key/value head's gradient
+            uq.uniquan_gemm_nt_batched(L, d, L, Bkv, q(self.dSt, g, L * L), L * L, q(self.Qt, g, d * L), d * L,
+                                       q(self.dKp, g, L * d), L * d, sc, causal=3)
+            uq.uniquan_gemm_nt_batched(L, d, L, Bkv, q(self.Pt, g, L * L), L * L, q(self.dOt, g, d * L), d * L,
+                                       q(self.dVp, g, L * d), L * d, causal=3)
+        uq.uniquan_rope_merge(T, H, d, L, self.dQr, self.dQ, rotate=True, group=grp)
+        uq.uniquan_rope_merge(T, Hkv, d, L, self.dKp, self.dK, rotate=True, nsum=grp)
+        uq.uniquan_rope_merge(T, Hkv, d, L, self.dVp, self.dV, rotate=False, nsum=grp)
         uq.uniquan_transpose_bf16(T, C, self.Z1, self.Z1t)
-        for g, src, dst in (("q", self.dQ, self.dQt), ("k", self.dK, self.dKt), ("v", self.dV, self.dVt)):
-            uq.uniquan_transpose_bf16(T, C, src, dst)
-            uq.uniquan_gemm_nt(C, C, T, dst, self.Z1t, m[g].G)
+        uq.uniquan_transpose_bf16(T, C, self.dQ, self.dQt)
+        uq.uniquan_gemm_nt(C, C, T, self.dQt, self.Z1t, m["q"].G)
+        for g, src, dst in (("k", self.dK, self.dKt), ("v", self.dV, self.dVt)):
+            uq.uniquan_transpose_bf16(T, Ckv, src, dst)
+            uq.uniquan_gemm_nt(Ckv, C, T, dst, self.Z1t, m[g].G)
 
     def update(self, lr_f=0.005, lr_b=0.0005, keep_grads=False):
         """Straight-through backward with the SGD update of every matrix."""
@@ -301,7 +334,7 @@ class DecoderBlock:
         causal half of each [L, L] product that is never computed is not
         counted)."""
         T, C, I, L, d, B = self.T, self.C, self.I, self.L, self.d, self.B
-        lin = 2.0 * T * C * C * 4 + 2.0 * T * C * I * 3
+        lin = 2.0 * T * C * C * 2 + 2.0 * T * self.Ckv * C * 2 + 2.0 * T * C * I * 3
         attn = 2.0 * B * (L * (L + 1) / 2) * d
         return 2 * lin + 3 * (2.0 * T * C * I) + 2.0 * T * C * C + 6 * attn
 

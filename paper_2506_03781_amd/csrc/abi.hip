@@ -422,23 +422,27 @@ static uq_status check_heads(const char* fn, int64_t T, int H, int d, int L, int
   return UQ_OK;
 }
 
-uq_status uniquan_rope_split(int64_t T, int H, int d, int L, const void* in, int in_dtype, int rotate, uint16_t* out,
-                             void* stream) {
+uq_status uniquan_rope_split(int64_t T, int H, int d, int L, int group, const void* in, int in_dtype, int rotate,
+                             uint16_t* out, void* stream) {
   const char* fn = "uniquan_rope_split";
   const uq_status c = check_heads(fn, T, H, d, L, in_dtype);
   if (c != UQ_OK) return c;
+  if (group < 1 || H % group != 0) return fail(UQ_EINVAL, "%s: group=%d must divide H=%d", fn, group, H);
   REQ_PTR(in, in_dtype == UQ_F32 ? 4 : 2); REQ_PTR(out, 2);
-  return hip_status(fn, uq::launch_rope_split(T, H, d, L, in, in_dtype == UQ_F32, rotate != 0, out,
+  return hip_status(fn, uq::launch_rope_split(T, H, d, L, group, in, in_dtype == UQ_F32, rotate != 0, out,
                                               static_cast<hipStream_t>(stream)));
 }
 
-uq_status uniquan_rope_merge(int64_t T, int H, int d, int L, const void* in, int in_dtype, int rotate, uint16_t* out,
-                             void* stream) {
+uq_status uniquan_rope_merge(int64_t T, int H, int d, int L, int group, int nsum, const void* in, int in_dtype,
+                             int rotate, uint16_t* out, void* stream) {
   const char* fn = "uniquan_rope_merge";
   const uq_status c = check_heads(fn, T, H, d, L, in_dtype);
   if (c != UQ_OK) return c;
+  if (group < 1 || H % group != 0) return fail(UQ_EINVAL, "%s: group=%d must divide H=%d", fn, group, H);
+  if (nsum < 1 || nsum > 256 || nsum * T * H * d >= (int64_t(1) << 40))
+    return fail(UQ_EINVAL, "%s: nsum=%d must be in 1..256", fn, nsum);
   REQ_PTR(in, in_dtype == UQ_F32 ? 4 : 2); REQ_PTR(out, 2);
-  return hip_status(fn, uq::launch_rope_merge(T, H, d, L, in, in_dtype == UQ_F32, rotate != 0, out,
+  return hip_status(fn, uq::launch_rope_merge(T, H, d, L, group, nsum, in, in_dtype == UQ_F32, rotate != 0, out,
                                               static_cast<hipStream_t>(stream)));
 }
 

@@ -147,11 +147,19 @@ __global__ __launch_bounds__(256) void rmsnorm_bwd_kernel(int64_t T, int64_t C, 
   }
 }
 
-// Token-major [T, C] (fp32 or bf16) -> head-major bf16 [H, T, d], rotating
-// pairs (i, i + d/2) by the position's angle when ROT.  One thread per pair.
+// Head h of a grouped layout (perm heads sharing a key/value head) is stored
+// at slot (h mod perm) (H / perm) + h / perm: the heads at one position of
+// their groups are contiguous, in key/value head order.
+__device__ __forceinline__ int head_slot(int h, int H, int perm) {
+  return perm > 1 ? (h % perm) * (H / perm) + h / perm : h;
+}
+
+// Token-major [T, C] (fp32 or bf16) -> head-major bf16 [H, T, d] (head h at
+// head_slot(h)), rotating pairs (i, i + d/2) by the position's angle when
+// ROT.  One thread per pair.
 template <bool IN_F32, bool ROT>
-__global__ __launch_bounds__(256) void rope_split_kernel(int64_t T, int H, int d, int L, const void* __restrict__ in,
-                                                         uint16_t* __restrict__ out) {
+__global__ __launch_bounds__(256) void rope_split_kernel(int64_t T, int H, int d, int L, int perm,
+                                                         const void* __restrict__ in, uint16_t* __restrict__ out) {
   const int hd = d >> 1;
   const int64_t n = T * H * hd;
   const int64_t idx = int64_t(blockIdx.x) * 256 + threadIdx.x;
@@ -175,16 +183,18 @@ __global__ __launch_bounds__(256) void rope_split_kernel(int64_t T, int H, int d
     y1 = x1 * c - x2 * s;
     y2 = x2 * c + x1 * s;
   }
-  const int64_t dst = (int64_t(h) * T + t) * d + i;
+  const int64_t dst = (int64_t(head_slot(h, H, perm)) * T + t) * d + i;
   out[dst] = to_bf(y1);
   out[dst + hd] = to_bf(y2);
 }
 
-// Head-major [H, T, d] (fp32 or bf16) -> token-major bf16 [T, C], rotating
-// by minus the position's angle when ROT (the inverse rotation).
+// Head-major [nsum, H, T, d] (fp32 or bf16; head h at head_slot(h)) ->
+// token-major bf16 [T, C]: the nsum stacked partials are summed (the
+// gradient of a key/value head shared by a group), then rotated by minus
+// the position's angle when ROT (the inverse rotation).
 template <bool IN_F32, bool ROT>
-__global__ __launch_bounds__(256) void rope_merge_kernel(int64_t T, int H, int d, int L, const void* __restrict__ in,
-                                                         uint16_t* __restrict__ out) {
+__global__ __launch_bounds__(256) void rope_merge_kernel(int64_t T, int H, int d, int L, int perm, int nsum,
+                                                         const void* __restrict__ in, uint16_t* __restrict__ out) {
   const int hd = d >> 1;
   const int64_t n = T * H * hd;
   const int64_t idx = int64_t(blockIdx.x) * 256 + threadIdx.x;
@@ -192,14 +202,18 @@ __global__ __launch_bounds__(256) void rope_merge_kernel(int64_t T, int H, int d
   const int i = int(idx % hd);
   const int h = int((idx / hd) % H);
   const int64_t t = idx / (int64_t(hd) * H);
-  const int64_t src = (int64_t(h) * T + t) * d + i;
-  float x1, x2;
-  if (IN_F32) {
-    x1 = static_cast<const float*>(in)[src];
-    x2 = static_cast<const float*>(in)[src + hd];
-  } else {
-    x1 = bf(static_cast<const uint16_t*>(in)[src]);
-    x2 = bf(static_cast<const uint16_t*>(in)[src + hd]);
+  const int64_t src0 = (int64_t(head_slot(h, H, perm)) * T + t) * d + i;
+  const int64_t pstride = int64_t(H) * T * d;
+  float x1 = 0.0f, x2 = 0.0f;
+  for (int q = 0; q < nsum; ++q) {
+    const int64_t src = src0 + q * pstride;
+    if (IN_F32) {
+      x1 += static_cast<const float*>(in)[src];
+      x2 += static_cast<const float*>(in)[src + hd];
+    } else {
+      x1 += bf(static_cast<const uint16_t*>(in)[src]);
+      x2 += bf(static_cast<const uint16_t*>(in)[src + hd]);
+    }
   }
   float y1 = x1, y2 = x2;
   if (ROT) {
@@ -381,23 +395,30 @@ hipError_t launch_rmsnorm_bwd(int64_t T, int64_t C, const float* dZa, const floa
   return hipGetLastError();
 }
 
-hipError_t launch_rope_split(int64_t T, int H, int d, int L, const void* in, int in_f32, int rotate, uint16_t* out,
-                             hipStream_t st) {
+hipError_t launch_rope_split(int64_t T, int H, int d, int L, int perm, const void* in, int in_f32, int rotate,
+                             uint16_t* out, hipStream_t st) {
   const dim3 grid(unsigned((T * H * (d / 2) + 255) / 256));
-  if (in_f32 && rotate) hipLaunchKernelGGL((rope_split_kernel<true, true>), grid, dim3(256), 0, st, T, H, d, L, in, out);
-  else if (in_f32) hipLaunchKernelGGL((rope_split_kernel<true, false>), grid, dim3(256), 0, st, T, H, d, L, in, out);
-  else if (rotate) hipLaunchKernelGGL((rope_split_kernel<false, true>), grid, dim3(256), 0, st, T, H, d, L, in, out);
-  else hipLaunchKernelGGL((rope_split_kernel<false, false>), grid, dim3(256), 0, st, T, H, d, L, in, out);
+  if (in_f32 && rotate)
+    hipLaunchKernelGGL((rope_split_kernel<true, true>), grid, dim3(256), 0, st, T, H, d, L, perm, in, out);
+  else if (in_f32)
+    hipLaunchKernelGGL((rope_split_kernel<true, false>), grid, dim3(256), 0, st, T, H, d, L, perm, in, out);
+  else if (rotate)
+    hipLaunchKernelGGL((rope_split_kernel<false, true>), grid, dim3(256), 0, st, T, H, d, L, perm, in, out);
+  else hipLaunchKernelGGL((rope_split_kernel<false, false>), grid, dim3(256), 0, st, T, H, d, L, perm, in, out);
   return hipGetLastError();
 }
 
-hipError_t launch_rope_merge(int64_t T, int H, int d, int L, const void* in, int in_f32, int rotate, uint16_t* out,
-                             hipStream_t st) {
+hipError_t launch_rope_merge(int64_t T, int H, int d, int L, int perm, int nsum, const void* in, int in_f32,
+                             int rotate, uint16_t* out, hipStream_t st) {
   const dim3 grid(unsigned((T * H * (d / 2) + 255) / 256));
-  if (in_f32 && rotate) hipLaunchKernelGGL((rope_merge_kernel<true, true>), grid, dim3(256), 0, st, T, H, d, L, in, out);
-  else if (in_f32) hipLaunchKernelGGL((rope_merge_kernel<true, false>), grid, dim3(256), 0, st, T, H, d, L, in, out);
-  else if (rotate) hipLaunchKernelGGL((rope_merge_kernel<false, true>), grid, dim3(256), 0, st, T, H, d, L, in, out);
-  else hipLaunchKernelGGL((rope_merge_kernel<false, false>), grid, dim3(256), 0, st, T, H, d, L, in, out);
+  if (in_f32 && rotate)
+    hipLaunchKernelGGL((rope_merge_kernel<true, true>), grid, dim3(256), 0, st, T, H, d, L, perm, nsum, in, out);
+  else if (in_f32)
+    hipLaunchKernelGGL((rope_merge_kernel<true, false>), grid, dim3(256), 0, st, T, H, d, L, perm, nsum, in, out);
+  else if (rotate)
+    hipLaunchKernelGGL((rope_merge_kernel<false, true>), grid, dim3(256), 0, st, T, H, d, L, perm, nsum, in, out);
+  else
+    hipLaunchKernelGGL((rope_merge_kernel<false, false>), grid, dim3(256), 0, st, T, H, d, L, perm, nsum, in, out);
   return hipGetLastError();
 }
 

@@ -64,8 +64,8 @@ _SIGS = {
                                 _i32),
     "uniquan_add_rmsnorm": ([_i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp], _i32),
     "uniquan_rmsnorm_bwd": ([_i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _f32, _vp, _vp, _vp], _i32),
-    "uniquan_rope_split": ([_i64, _i32, _i32, _i32, _vp, _i32, _i32, _vp, _vp], _i32),
-    "uniquan_rope_merge": ([_i64, _i32, _i32, _i32, _vp, _i32, _i32, _vp, _vp], _i32),
+    "uniquan_rope_split": ([_i64, _i32, _i32, _i32, _i32, _vp, _i32, _i32, _vp, _vp], _i32),
+    "uniquan_rope_merge": ([_i64, _i32, _i32, _i32, _i32, _i32, _vp, _i32, _i32, _vp, _vp], _i32),
     "uniquan_softmax_causal": ([_i64, _i32, _vp, _vp, _vp], _i32),
     "uniquan_softmax_causal_bwd": ([_i64, _i32, _vp, _vp, _vp, _vp], _i32),
     "uniquan_transpose_bf16_batched": ([_i64, _i64, _i64, _vp, _vp, _vp], _i32),
@@ -404,18 +404,18 @@ def uniquan_rmsnorm_bwd(T, C, dZa, dZb, X, gamma, rinv, E, escale, dR, dRf=None,
                                      float(escale), _p(dR, n, _B, "dR"), _p(dRf, n, _F, "dRf"), _stream(stream)))
 
 
-def uniquan_rope_split(T, H, d, L, x, out, rotate=True, stream=None):
-    """Token-major x [T, H d] (fp32 or bf16) -> head-major bf16 out [H, T, d]."""
+def uniquan_rope_split(T, H, d, L, x, out, rotate=True, group=1, stream=None):
+    """Token-major x [T, H d] (fp32 or bf16) -> head-major bf16 out [H, T, d] (grouped slot order when group > 1)."""
     n = T * H * d
-    _check(lib().uniquan_rope_split(T, H, d, L, _p(x, n, _W, "in"), _dt(x), int(bool(rotate)),
+    _check(lib().uniquan_rope_split(T, H, d, L, int(group), _p(x, n, _W, "in"), _dt(x), int(bool(rotate)),
                                     _p(out, n, _B, "out"), _stream(stream)))
 
 
-def uniquan_rope_merge(T, H, d, L, x, out, rotate=True, stream=None):
-    """Head-major x [H, T, d] (fp32 or bf16) -> token-major bf16 out [T, H d]."""
+def uniquan_rope_merge(T, H, d, L, x, out, rotate=True, group=1, nsum=1, stream=None):
+    """Head-major x [nsum, H, T, d] (fp32 or bf16) -> token-major bf16 out [T, H d], partials summed."""
     n = T * H * d
-    _check(lib().uniquan_rope_merge(T, H, d, L, _p(x, n, _W, "in"), _dt(x), int(bool(rotate)),
-                                    _p(out, n, _B, "out"), _stream(stream)))
+    _check(lib().uniquan_rope_merge(T, H, d, L, int(group), int(nsum), _p(x, n * nsum, _W, "in"), _dt(x),
+                                    int(bool(rotate)), _p(out, n, _B, "out"), _stream(stream)))
 
 
 def uniquan_softmax_causal(rows, L, S, P, stream=None):

@@ -13,7 +13,14 @@ dL/dWhat of all seven matrices within 1e-2 normwise.  Per element the bar is
 large values and each side rounds its bf16 intermediates (and its target)
 independently, so single elements of E, and of the gradients summed from
 them, differ by several percent where the attention is sharp; the
-per-element check still catches a misplaced or transposed gradient.  The chained test gives the second block the first
+per-element check still catches a misplaced or transposed gradient.  The
+grouped-query cases use C = 512 in 4 query heads of 128 sharing 2 or 1
+key/value heads (k, v of [n_kv 128, 512]); their per-element bar is 0.3:
+there the oracle's own bf16-storage gradients differ from its exact ones
+by 7% normwise and up to 2-4 rms in single elements of dL/dWhat_q, so one
+rounding decision taken the other way at a storage point moves isolated
+elements by a fifth of rms, while a misplaced row, column or head still
+fails the normwise 1e-2.  The chained test gives the second block the first
 quantized block's output as its input (Algorithm 1 run from the bottom
 block up), each side computing that input itself.
 """
@@ -55,11 +62,17 @@ def close(x, ref, tol=1e-2, elem=0.1, what=""):
     assert np.all(ratio <= elem), f"{what}: {(ratio > elem).sum()} of {ratio.size} elements, worst {ratio.max():.3g}"
 
 
-def make_block(seed, qk_scale=1.0):
+def shapes_for(C_, I_, n_kv_d):
+    return {"q": (C_, C_), "k": (n_kv_d, C_), "v": (n_kv_d, C_), "o": (C_, C_), "g": (I_, C_), "u": (I_, C_),
+            "d": (C_, I_)}
+
+
+def make_block(seed, qk_scale=1.0, shapes=SHAPES):
     specs = synth.WORKLOADS["block7b"].matrices
     mats, X = {}, None
-    for name, spec in zip(SHAPES, specs):
-        R_, C_ = SHAPES[name]
+    C = shapes["q"][1]
+    for name, spec in zip(shapes, specs):
+        R_, C_ = shapes[name]
         m = synth.make_matrix(synth.scaled(spec, R=R_, C=C_, T=T), seed)
         if X is None:
             X = m.X.astype(F32)
@@ -73,10 +86,10 @@ def make_block(seed, qk_scale=1.0):
     return X, mats, g1, g2
 
 
-def device_block(mats, g1, g2):
+def device_block(mats, g1, g2, H_=H, n_kv=None):
     qs = {n: QuantMatrix(W, s, K, G, p["delta"], p["z_u"], p["s_r"], p["z_b"], p["alpha"])
           for n, (W, s, p) in mats.items()}
-    return DecoderBlock(qs, g1, g2, T, N_SEQ, H), qs
+    return DecoderBlock(qs, g1, g2, T, N_SEQ, H_, n_kv=n_kv), qs
 
 
 def oracle_what(mats, mode=O.MAP_FULL):
@@ -159,3 +172,29 @@ def test_decoder_block_step_updates():
     assert all(np.isfinite(losses)) and losses[0] > 0
     for n, q in qs.items():
         assert not torch.equal(q.s, s0[n]), n
+
+
+@pytest.mark.parametrize("n_kv,qk_scale", [(2, 1.0), (2, 6.0), (1, 1.0)])
+def test_decoder_block_grouped_query(n_kv, qk_scale):
+    """Grouped-query attention: 4 query heads over n_kv key/value heads; the
+    gradients of the shared k and v matrices sum over each group."""
+    Hq, Cq, Iq = 4, 512, 384
+    shapes = shapes_for(Cq, Iq, n_kv * (Cq // Hq))
+    X, mats, g1, g2 = make_block(11 + n_kv, qk_scale, shapes)
+    blk, qs = device_block(mats, g1, g2, Hq, n_kv)
+    blk.prepare(X)
+    blk.set_input(X)
+    blk.forward_backward(uq.MAP_FULL)
+    torch.cuda.synchronize()
+
+    f = oracle_what(mats)
+    for n in mats:
+        assert np.array_equal(host(qs[n].codes).reshape(shapes[n]).astype(np.uint8), f[n]["codes"]), f"{n} codes"
+    Y_ref = D.decoder_forward(X, wfp(mats), g1, g2, N_SEQ, Hq, store=O.bf16_rne, n_kv=n_kv)["Y"]
+    assert np.allclose(host(blk.Yref), Y_ref, rtol=2e-2, atol=2e-2 * np.abs(Y_ref).max())
+    st = D.decoder_step(X, Y_ref, {n: f[n]["what_bf16"] for n in mats}, g1, g2, N_SEQ, Hq, store=O.bf16_rne,
+                        n_kv=n_kv)
+    loss = float(blk.loss.item())
+    assert abs(loss - st["loss"]) <= 1e-2 * st["loss"], (loss, st["loss"])
+    for n in mats:
+        close(host(qs[n].G), st["grads"][n], elem=0.3, what=f"dL/dWhat_{n}")

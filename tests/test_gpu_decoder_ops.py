@@ -216,3 +216,30 @@ def test_gemm_nt_batched_causal(L, N, batch):
         full32(L, N, L, A, Bm, O1, mode)
         torch.cuda.synchronize()
         assert np.array_equal(host(O1), host(O0)), mode
+
+
+@pytest.mark.parametrize("n_seq,L,H,G,nsum", [(2, 8, 4, 2, 2), (2, 64, 8, 4, 4)])
+def test_rope_grouped_slots_and_partial_sums(n_seq, L, H, G, nsum):
+    """Grouped slot order (head h at (h mod G) (H / G) + h / G) and the merge
+    of nsum stacked partials with the inverse rotation."""
+    d = 16 if L == 8 else 128
+    T, C = n_seq * L, H * d
+    rs = np.random.default_rng(H * G)
+    slot = [(h % G) * (H // G) + h // G for h in range(H)]
+    xb = bfr(rs.standard_normal((T, C)))
+    hm = torch.empty(H, T, d, dtype=torch.bfloat16, device="cuda")
+    uq.uniquan_rope_split(T, H, d, L, dev(xb, torch.bfloat16), hm, rotate=False, group=G)
+    torch.cuda.synchronize()
+    got = host(hm)
+    for h in range(H):
+        assert np.array_equal(got[slot[h]], xb[:, h * d:(h + 1) * d]), h
+    # merge: sum of nsum partials, unpermute, inverse rotation
+    y = rs.standard_normal((nsum, H, T, d)).astype(F32)
+    out = torch.empty(T, C, dtype=torch.bfloat16, device="cuda")
+    uq.uniquan_rope_merge(T, H, d, L, dev(y, torch.float32), out, rotate=True, group=G, nsum=nsum)
+    torch.cuda.synchronize()
+    ysum = y.astype(np.float64).sum(axis=0)                       # [H(slot), T, d]
+    yh = np.stack([ysum[slot[h]] for h in range(H)])              # [H(head), T, d]
+    yin = yh.reshape(H, n_seq, L, d).transpose(1, 0, 2, 3)
+    ref = D.merge_heads(D.rope(yin, D.rope_angles(L, d), inverse=True))
+    within_bf16(host(out), ref, 4e-6 * np.abs(ref).max(), "grouped merge")
