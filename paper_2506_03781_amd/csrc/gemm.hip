@@ -98,12 +98,11 @@ __device__ __forceinline__ int slot(int row, int kc) { return row * 8 + (kc ^ (r
 // arithmetic as the standalone backward kernel: lane l takes 8 consecutive
 // columns of row 4 it + l / 16, a group of g columns is g / 8 adjacent lanes,
 // and the group sums use the same fixed xor-butterfly.
-template <int KB>
+template <int KB, int NB>
 __device__ __forceinline__ void ste_strip(const GemmArgs& p, const float* strip, int64_t row_base, int64_t col_base,
                                           int lane) {
   const SteParams& q = p.ste;
   const int lpg = 1 << (q.logg - 3);
-  constexpr int NB = 8;  // row-iterations whose loads are in flight together
 #pragma unroll 1
   for (int it0 = 0; it0 < 8; it0 += NB) {
     uint4 wq[NB];
@@ -242,7 +241,9 @@ __device__ __forceinline__ void epilogue(const GemmArgs& p, f32x16 (&acc)[FM][FN
     const int64_t col_base = n0 + wn * WN;
     if constexpr (EPI >= EPI_STE) {
       static_assert(WN == 128, "the fused backward needs 128-column wave tiles");
-      ste_strip<EPI - EPI_STE>(p, strip, row_base, col_base, lane);
+      // row-iterations whose loads are in flight together: 8 with one workgroup
+      // per CU, 2 where two share a CU (their wavefronts keep loads in flight)
+      ste_strip<EPI - EPI_STE, (BM == 128 ? 2 : 8)>(p, strip, row_base, col_base, lane);
       __builtin_amdgcn_s_waitcnt(0xC07F);  // strip reads done before the next strip overwrites it
       __builtin_amdgcn_wave_barrier();
       continue;
@@ -453,8 +454,9 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((VM & 0xF) | ((VM >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
-template <int BM, int BN, int EPI, int S>
-__global__ __launch_bounds__(256) void gemm_pipe_kernel(GemmArgs p) {
+// OCC: workgroups per CU the kernel is built for (register budget 512 / OCC).
+template <int BM, int BN, int EPI, int S, int OCC = 1>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(OCC))) void gemm_pipe_kernel(GemmArgs p) {
   select_batch(p);
   constexpr int BK = 32;
   constexpr int WM = BM / 2, WN = BN / 2;
@@ -669,8 +671,10 @@ static hipError_t launch_bm(const GemmLaunch& q, hipStream_t st) {
   return hipGetLastError();
 }
 
-// Weight-gradient GEMM with the fused straight-through backward: 256 x 256
-// tiles (128-column wave tiles hold whole groups for g <= 128), K % 32 == 0.
+// Weight-gradient GEMM with the fused straight-through backward: 128 x 256
+// tiles two per CU where the shape gives at least 512 of them, 256 x 256
+// otherwise; both have 128-column wave tiles, which hold whole groups for
+// g <= 128.  K % 32 == 0.
 hipError_t launch_gemm_ste(const GemmLaunch& q, int k, hipStream_t st) {
   GemmArgs a;
   a.A = q.A; a.B = q.B; a.M = q.M; a.N = q.N; a.K = q.K;
@@ -678,6 +682,21 @@ hipError_t launch_gemm_ste(const GemmLaunch& q, int k, hipStream_t st) {
   a.ste = q.ste;
   a.bsa = a.bsb = a.bso = 0;
   a.causal = 0;
+  // 128 x 256 tiles with a 3-stage ring (72 KB of LDS, at most 256 registers)
+  // where they give two workgroups per CU: one workgroup's epilogue then
+  // runs beside the other's main loop and memory phase
+  if (tiles<128, 256>(q.M, q.N) >= 512) {
+    a.tiles_m = int((q.M + 127) / 128);
+    a.tiles_n = int((q.N + 255) / 256);
+    const dim3 grid(unsigned(a.tiles_m * a.tiles_n));
+    switch (k) {
+      case 1: hipLaunchKernelGGL((gemm_pipe_kernel<128, 256, EPI_STE + 1, 3, 2>), grid, dim3(256), 0, st, a); break;
+      case 2: hipLaunchKernelGGL((gemm_pipe_kernel<128, 256, EPI_STE + 2, 3, 2>), grid, dim3(256), 0, st, a); break;
+      case 3: hipLaunchKernelGGL((gemm_pipe_kernel<128, 256, EPI_STE + 3, 3, 2>), grid, dim3(256), 0, st, a); break;
+      default: hipLaunchKernelGGL((gemm_pipe_kernel<128, 256, EPI_STE + 4, 3, 2>), grid, dim3(256), 0, st, a); break;
+    }
+    return hipGetLastError();
+  }
   a.tiles_m = int((q.M + 255) / 256);
   a.tiles_n = int((q.N + 255) / 256);
   const dim3 grid(unsigned(a.tiles_m * a.tiles_n));

@@ -131,6 +131,31 @@ def test_fused_bwd_rejects_unsupported():
         assert e.value.status == status
 
 
+def sampled_rows_check(R, C, T, k, g, seed, rows):
+    m, p, codes, Et = case(R, C, T, k, g, seed, forward_codes=False)
+    lr_f, lr_b = 0.005, 0.0005
+    got = run_fused(m, p, codes, Et, k, g, lr_f, lr_b)
+    gpr = C // g
+    gidx = (rows[:, None] * gpr + np.arange(gpr)[None, :]).reshape(-1)
+    Xb = synth.round_to_bf16(m.X).astype(np.float64)
+    G = 2.0 * Et[rows].astype(np.float64) @ Xb
+    bw = O.fq_bwd(m.W[rows], m.s[rows], p["alpha"][gidx], p["z_b"][gidx], codes[rows], G, k, g,
+                  p["s_r"][rows], p["delta"][gidx], p["z_u"][gidx])
+    close(got["grad_s"][rows], bw["grad_s"], what="grad_s rows")
+    close(got["grad_alpha"][gidx], bw["grad_alpha"], what="grad_alpha rows")
+    close(got["z_b"][gidx].astype(np.float64) - p["z_b"][gidx], -lr_b * bw["grad_z_b"], what="z_b step rows")
+    close(got["s"][rows].astype(np.float64) - m.s[rows], -lr_f * bw["grad_s"], what="s step rows")
+
+
+def test_fused_bwd_two_per_cu_ragged():
+    """4100 x 3968 weights (33 x 16 tiles of 128 x 256, the last row tile 4
+    rows deep and the last column tile half wide): the two-workgroups-per-CU
+    launch with partial tiles; sampled rows, including the last ones."""
+    R, C = 4100, 3968
+    rows = np.array([0, 1, 127, 128, 2049, 4095, 4096, 4099])
+    sampled_rows_check(R, C, 256, 3, 128, 37, rows)
+
+
 def test_fused_bwd_full_size_attn4096():
     """4096 x 4096 weights, 2048 tokens, k = 4: the launch the fused step
     uses; sampled rows against the oracle."""
