@@ -579,6 +579,8 @@ def main():
 
     bcq = bcq_inference(layers)
     blk = None if args.no_block else block_decoder(args.seed, n_kv=args.block_kv)
+    # the same block with grouped-query attention (8 key/value heads, as in Mistral 7B and Llama-3 8B)
+    blk_gqa = None if (args.no_block or args.block_kv is not None) else block_decoder(args.seed, n_kv=8)
 
     out = {
         "metric": "fake-quant fwd+bwd Gweights/s (%HBM peak); recon GEMM TFLOP/s (%MFMA)",
@@ -614,6 +616,7 @@ def main():
                           "note": "deployed layer (fold -> bit-planes + binary16 Theta*_B): Y = X What^T for T "
                                   "activation rows; bytes = planes + parameters + X + Y"},
         "block_decoder": blk,
+        "block_decoder_gqa": blk_gqa,
         "counters_src_hash": src_hash(),
         "precision": "quantizer: fp32 arithmetic on bf16 W / fp32 s, bf16 What and dL/dWhat; "
                      "GEMMs: bf16 MFMA with fp32 accumulation",
