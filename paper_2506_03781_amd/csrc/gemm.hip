@@ -217,10 +217,10 @@ __device__ __forceinline__ void ste_strip(const GemmArgs& p, const float* strip,
 // contiguous 16-byte / 8-byte vectors.  `scratch` must hold 4 * 32 * WN
 // floats and may alias the operand stages (all waves are past their last
 // operand read when this is called).
-template <int BM, int BN, int EPI, int FM = BM / 64, int FN = BN / 64>
+template <int BM, int BN, int EPI, int WM = BM / 2, int WN = BN / 2, int NW = 4, int FM = WM / 32,
+          int FN = WN / 32>
 __device__ __forceinline__ void epilogue(const GemmArgs& p, f32x16 (&acc)[FM][FN], int64_t m0, int64_t n0,
                                          int wm, int wn, int lane, int wave, int tid, float* scratch) {
-  constexpr int WM = BM / 2, WN = BN / 2;
   constexpr int Q = WN / 4;            // float4 per strip row
   constexpr int ITER = 32 * Q / 64;    // float4 per lane per strip
   const int lr = lane & 31, lh = lane >> 5;
@@ -303,11 +303,19 @@ __device__ __forceinline__ void epilogue(const GemmArgs& p, f32x16 (&acc)[FM][FN
     __builtin_amdgcn_wave_barrier();
   }
   if constexpr (EPI == EPI_LOSS || EPI == EPI_LOSS_RES) {
-    __shared__ float sred[4];
+    __shared__ float sred[NW];
     for (int msk = 32; msk >= 1; msk >>= 1) lsum += __shfl_xor(lsum, msk, 64);
     if (lane == 0) sred[wave] = lsum;
     __syncthreads();
-    if (tid == 0) p.partials[blockIdx.x] = (sred[0] + sred[1]) + (sred[2] + sred[3]);
+    if (tid == 0) {
+      float t;
+      if constexpr (NW == 4) {
+        t = (sred[0] + sred[1]) + (sred[2] + sred[3]);
+      } else {
+        t = ((sred[0] + sred[1]) + (sred[2] + sred[3])) + ((sred[4] + sred[5]) + (sred[6] + sred[7]));
+      }
+      p.partials[blockIdx.x] = t;
+    }
   }
 }
 
@@ -616,6 +624,140 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(OCC))) void
   epilogue<BM, BN, EPI>(p, acc, m0, n0, wm, wn, lane, wave, tid, reinterpret_cast<float*>(smem));
 }
 
+// ---------------------------------------------------------------------------
+// Ping-pong main loop for single products with K % 32 == 0 and 256 x 256 or
+// 256 x 128 tiles.  Eight wavefronts in two groups of four, one wavefront of
+// each group per SIMD.  The groups alternate between an MFMA phase on
+// fragments held in registers and a memory phase (the next stage's
+// fragments from LDS, this wavefront's share of the copy of stage k+3),
+// separated by workgroup barriers and offset by one phase: group 1 passes
+// one barrier before the loop and group 0 one after it, so both pass the
+// same number.  While one group's MFMAs run, the other group's LDS reads and
+// copies proceed on the same SIMDs.  Stage rows are 64 bytes; chunk kc of
+// row r sits at kc ^ ((r >> 2) & 3), so the 16 rows a quarter-wavefront reads
+// at one K offset fall in 16 distinct bank groups.  Copies past the last
+// stage reload it into a slot no phase reads again, so every iteration
+// issues and waits the same; rows past M or N are loaded from row M-1 / N-1
+// and masked at the store.
+// ---------------------------------------------------------------------------
+template <int BM, int BN, int EPI>
+__global__ __launch_bounds__(512) void gemm_pp_kernel(GemmArgs p) {
+  constexpr int S = 4, BK = 32;
+  constexpr int WAVES_M = BN == 256 ? 2 : 4, WAVES_N = 8 / WAVES_M;
+  constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N, FM = WM / 32, FN = WN / 32;
+  constexpr int ABLK = BM / 16, BBLK = BN / 16, PW = (ABLK + BBLK) / 8;  // 1 KB copies per wave and stage
+  static_assert((ABLK + BBLK) % 8 == 0, "stage blocks must split over 8 waves");
+
+  __shared__ uint4 smem[S * (BM + BN) * 4];
+  uint4 (*sA)[BM * 4] = reinterpret_cast<uint4 (*)[BM * 4]>(smem);
+  uint4 (*sB)[BN * 4] = reinterpret_cast<uint4 (*)[BN * 4]>(smem + S * BM * 4);
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int grp = wave >> 2, qw = wave & 3;
+  // 256 x 256: rows by qw / 2, columns by (qw % 2, group); 256 x 128: rows by qw, columns by group
+  const int wm = WAVES_M == 2 ? (qw >> 1) : qw;
+  const int wn = WAVES_M == 2 ? ((qw & 1) * 2 + grp) : grp;
+  int tm, tn;
+  tile_of<(BM == 256 && BN == 128) ? 4 : 8>(blockIdx.x, gridDim.x, p.tiles_m, p.tiles_n, tm, tn);
+  const int64_t m0 = int64_t(tm) * BM, n0 = int64_t(tn) * BN;
+  const int64_t K = p.K;
+
+  // Lane l of a copy fills LDS slot l of a 1 KB block: row 16 blk + l / 4,
+  // slot l % 4, which holds chunk (l % 4) ^ ((row >> 2) & 3) of that row.
+  const uint16_t* src[PW];
+  int dst_off[PW];
+  bool isA[PW];
+#pragma unroll
+  for (int j = 0; j < PW; ++j) {
+    const int blk = wave * PW + j;
+    const bool a = blk < ABLK;
+    const int b = a ? blk : blk - ABLK;
+    const int row = b * 16 + (lane >> 2);
+    const int kc = (lane & 3) ^ ((row >> 2) & 3);
+    isA[j] = a;
+    const int64_t gr = a ? min(m0 + row, p.M - 1) : min(n0 + row, p.N - 1);
+    src[j] = (a ? p.A : p.B) + gr * K + kc * 8;
+    dst_off[j] = b * 64;
+  }
+  const int nk = int(K / BK);
+  auto issue = [&](int stage, int kstage) {
+    const int64_t k0 = int64_t(min(kstage, nk - 1)) * BK;
+#pragma unroll
+    for (int j = 0; j < PW; ++j) {
+      uint4* dst = isA[j] ? &sA[stage][dst_off[j]] : &sB[stage][dst_off[j]];
+      __builtin_amdgcn_global_load_lds((glb_void*)(src[j] + k0), (lds_void*)dst, 16, 0, 0);
+    }
+  };
+
+  f32x16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  const int lr = lane & 31, lh = lane >> 5;
+  int offA[2][FM], offB[2][FN];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int kc = s * 2 + lh;
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int row = wm * WM + i * 32 + lr;
+      offA[s][i] = row * 4 + (kc ^ ((row >> 2) & 3));
+    }
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int row = wn * WN + j * 32 + lr;
+      offB[s][j] = row * 4 + (kc ^ ((row >> 2) & 3));
+    }
+  }
+  bf16x8 af[2][FM], bfr[2][FN];
+  auto rd = [&](int st) {
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+#pragma unroll
+      for (int i = 0; i < FM; ++i) af[s][i] = __builtin_bit_cast(bf16x8, sA[st][offA[s][i]]);
+#pragma unroll
+      for (int j = 0; j < FN; ++j) bfr[s][j] = __builtin_bit_cast(bf16x8, sB[st][offB[s][j]]);
+    }
+  };
+
+#pragma unroll
+  for (int s = 0; s < S - 1; ++s) issue(s, s);
+  wait_vmcnt<(S - 2) * PW>();  // this wavefront's share of stage 0
+  __builtin_amdgcn_s_barrier();
+  if (grp == 1) __builtin_amdgcn_s_barrier();
+  for (int k = 0; k < nk; ++k) {
+    // memory phase: fragments of stage k, copy of stage k+3 into the slot
+    // stage k-1 used (both groups finished reading it a phase ago)
+    __builtin_amdgcn_sched_barrier(0);
+    rd(k % S);
+    issue((k + S - 1) % S, k + S - 1);
+    wait_vmcnt<(S - 2) * PW>();            // this wavefront's share of stage k+1
+    __builtin_amdgcn_s_waitcnt(0xC07F);    // lgkmcnt(0): fragments in registers
+    __builtin_amdgcn_s_barrier();
+    // MFMA phase
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[s][i], bfr[s][j], acc[i][j], 0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_barrier();
+  }
+  if (grp == 0) __builtin_amdgcn_s_barrier();
+  wait_vmcnt<0>();   // the reloads past the end have landed
+  __syncthreads();   // every wave is past its last operand read: the stages become epilogue scratch
+  epilogue<BM, BN, EPI, WM, WN, 8>(p, acc, m0, n0, wm, wn, lane, wave, tid, reinterpret_cast<float*>(smem));
+}
+
 template <int BM, int BN>
 static int tiles(int64_t M, int64_t N) {
   return int(((M + BM - 1) / BM) * ((N + BN - 1) / BN));
@@ -641,10 +783,18 @@ size_t gemm_workgroups(int64_t M, int64_t N, int /*epi*/) {
   }
 }
 
-// Pipelined kernel when K is a multiple of its 32-deep stages; the
-// register-staged kernel (any K that is a multiple of 8) otherwise.
+// Single products with K a multiple of 32 on 256-row tiles: the ping-pong
+// kernel; other products with K a multiple of 32 (batched, causal, 128-row
+// tiles): the pipelined kernel; the register-staged kernel (any K that is a
+// multiple of 8) otherwise.
 template <int BM, int BN, int EPI>
 static void launch_epi(const GemmArgs& a, dim3 grid, hipStream_t st) {
+  if constexpr (BM == 256 && (BN == 256 || BN == 128)) {
+    if (a.K % 32 == 0 && grid.y == 1 && a.causal == 0) {
+      hipLaunchKernelGGL((gemm_pp_kernel<BM, BN, EPI>), grid, dim3(512), 0, st, a);
+      return;
+    }
+  }
   if (a.K % 32 == 0) hipLaunchKernelGGL((gemm_pipe_kernel<BM, BN, EPI, 4>), grid, dim3(256), 0, st, a);
   else hipLaunchKernelGGL((gemm_nt_kernel<BM, BN, EPI>), grid, dim3(256), 0, st, a);
 }
