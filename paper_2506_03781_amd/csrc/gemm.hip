@@ -241,9 +241,9 @@ __device__ __forceinline__ void epilogue(const GemmArgs& p, f32x16 (&acc)[FM][FN
     const int64_t col_base = n0 + wn * WN;
     if constexpr (EPI >= EPI_STE) {
       static_assert(WN == 128, "the fused backward needs 128-column wave tiles");
-      // row-iterations whose loads are in flight together: 8 with one workgroup
-      // per CU, 2 where two share a CU (their wavefronts keep loads in flight)
-      ste_strip<EPI - EPI_STE, (BM == 128 ? 2 : 8)>(p, strip, row_base, col_base, lane);
+      // row-iterations whose loads are in flight together: 8 with four
+      // wavefronts per workgroup, 2 with eight (they keep loads in flight)
+      ste_strip<EPI - EPI_STE, (NW == 8 ? 2 : 8)>(p, strip, row_base, col_base, lane);
       __builtin_amdgcn_s_waitcnt(0xC07F);  // strip reads done before the next strip overwrites it
       __builtin_amdgcn_wave_barrier();
       continue;
@@ -462,9 +462,8 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((VM & 0xF) | ((VM >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
-// OCC: workgroups per CU the kernel is built for (register budget 512 / OCC).
-template <int BM, int BN, int EPI, int S, int OCC = 1>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(OCC))) void gemm_pipe_kernel(GemmArgs p) {
+template <int BM, int BN, int EPI, int S>
+__global__ __launch_bounds__(256) void gemm_pipe_kernel(GemmArgs p) {
   select_batch(p);
   constexpr int BK = 32;
   constexpr int WM = BM / 2, WN = BN / 2;
@@ -640,10 +639,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(OCC))) void
 // issues and waits the same; rows past M or N are loaded from row M-1 / N-1
 // and masked at the store.
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int EPI>
+template <int BM, int BN, int EPI, int WAVES_M = (BN == 256 ? 2 : 4)>
 __global__ __launch_bounds__(512) void gemm_pp_kernel(GemmArgs p) {
   constexpr int S = 4, BK = 32;
-  constexpr int WAVES_M = BN == 256 ? 2 : 4, WAVES_N = 8 / WAVES_M;
+  constexpr int WAVES_N = 8 / WAVES_M;
   constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N, FM = WM / 32, FN = WN / 32;
   constexpr int ABLK = BM / 16, BBLK = BN / 16, PW = (ABLK + BBLK) / 8;  // 1 KB copies per wave and stage
   static_assert((ABLK + BBLK) % 8 == 0, "stage blocks must split over 8 waves");
@@ -656,7 +655,7 @@ __global__ __launch_bounds__(512) void gemm_pp_kernel(GemmArgs p) {
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int grp = wave >> 2, qw = wave & 3;
-  // 256 x 256: rows by qw / 2, columns by (qw % 2, group); 256 x 128: rows by qw, columns by group
+  // 2 x 4 wave grid: rows by qw / 2, columns by (qw % 2, group); 4 x 2: rows by qw, columns by group
   const int wm = WAVES_M == 2 ? (qw >> 1) : qw;
   const int wn = WAVES_M == 2 ? ((qw & 1) * 2 + grp) : grp;
   int tm, tn;
@@ -821,10 +820,10 @@ static hipError_t launch_bm(const GemmLaunch& q, hipStream_t st) {
   return hipGetLastError();
 }
 
-// Weight-gradient GEMM with the fused straight-through backward: 128 x 256
-// tiles two per CU where the shape gives at least 512 of them, 256 x 256
-// otherwise; both have 128-column wave tiles, which hold whole groups for
-// g <= 128.  K % 32 == 0.
+// Weight-gradient GEMM with the fused straight-through backward: 256 x 256
+// tiles, on the ping-pong kernel where there are at least 256 of them and on
+// the pipelined kernel otherwise; both use 128-column wave tiles, which hold
+// whole groups for g <= 128.  K % 32 == 0.
 hipError_t launch_gemm_ste(const GemmLaunch& q, int k, hipStream_t st) {
   GemmArgs a;
   a.A = q.A; a.B = q.B; a.M = q.M; a.N = q.N; a.K = q.K;
@@ -832,18 +831,18 @@ hipError_t launch_gemm_ste(const GemmLaunch& q, int k, hipStream_t st) {
   a.ste = q.ste;
   a.bsa = a.bsb = a.bso = 0;
   a.causal = 0;
-  // 128 x 256 tiles with a 3-stage ring (72 KB of LDS, at most 256 registers)
-  // where they give two workgroups per CU: one workgroup's epilogue then
-  // runs beside the other's main loop and memory phase
-  if (tiles<128, 256>(q.M, q.N) >= 512) {
-    a.tiles_m = int((q.M + 127) / 128);
+  // ping-pong kernel (4 x 2 wave grid: 64 x 128 wave tiles) where the shape
+  // gives at least one 256 x 256 tile per CU: the epilogue's memory phase then
+  // runs on eight wavefronts per CU
+  if (tiles<256, 256>(q.M, q.N) >= 256) {
+    a.tiles_m = int((q.M + 255) / 256);
     a.tiles_n = int((q.N + 255) / 256);
     const dim3 grid(unsigned(a.tiles_m * a.tiles_n));
     switch (k) {
-      case 1: hipLaunchKernelGGL((gemm_pipe_kernel<128, 256, EPI_STE + 1, 3, 2>), grid, dim3(256), 0, st, a); break;
-      case 2: hipLaunchKernelGGL((gemm_pipe_kernel<128, 256, EPI_STE + 2, 3, 2>), grid, dim3(256), 0, st, a); break;
-      case 3: hipLaunchKernelGGL((gemm_pipe_kernel<128, 256, EPI_STE + 3, 3, 2>), grid, dim3(256), 0, st, a); break;
-      default: hipLaunchKernelGGL((gemm_pipe_kernel<128, 256, EPI_STE + 4, 3, 2>), grid, dim3(256), 0, st, a); break;
+      case 1: hipLaunchKernelGGL((gemm_pp_kernel<256, 256, EPI_STE + 1, 4>), grid, dim3(512), 0, st, a); break;
+      case 2: hipLaunchKernelGGL((gemm_pp_kernel<256, 256, EPI_STE + 2, 4>), grid, dim3(512), 0, st, a); break;
+      case 3: hipLaunchKernelGGL((gemm_pp_kernel<256, 256, EPI_STE + 3, 4>), grid, dim3(512), 0, st, a); break;
+      default: hipLaunchKernelGGL((gemm_pp_kernel<256, 256, EPI_STE + 4, 4>), grid, dim3(512), 0, st, a); break;
     }
     return hipGetLastError();
   }

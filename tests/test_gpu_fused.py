@@ -147,9 +147,9 @@ def sampled_rows_check(R, C, T, k, g, seed, rows):
     close(got["s"][rows].astype(np.float64) - m.s[rows], -lr_f * bw["grad_s"], what="s step rows")
 
 
-def test_fused_bwd_two_per_cu_ragged():
-    """4100 x 3968 weights (33 x 16 tiles of 128 x 256, the last row tile 4
-    rows deep and the last column tile half wide): the two-workgroups-per-CU
+def test_fused_bwd_large_ragged():
+    """4100 x 3968 weights (17 x 16 tiles of 256 x 256, the last row tile 4
+    rows deep and the last column tile half wide): the eight-wavefront
     launch with partial tiles; sampled rows, including the last ones."""
     R, C = 4100, 3968
     rows = np.array([0, 1, 127, 128, 2049, 4095, 4096, 4099])
