@@ -624,32 +624,43 @@ __global__ __launch_bounds__(256) void gemm_pipe_kernel(GemmArgs p) {
 }
 
 // ---------------------------------------------------------------------------
-// Ping-pong main loop for single products with K % 32 == 0 and 256 x 256 or
-// 256 x 128 tiles.  Eight wavefronts in two groups of four, one wavefront of
-// each group per SIMD.  The groups alternate between an MFMA phase on
-// fragments held in registers and a memory phase (the next stage's
-// fragments from LDS, this wavefront's share of the copy of stage k+3),
-// separated by workgroup barriers and offset by one phase: group 1 passes
-// one barrier before the loop and group 0 one after it, so both pass the
-// same number.  While one group's MFMAs run, the other group's LDS reads and
-// copies proceed on the same SIMDs.  Stage rows are 64 bytes; chunk kc of
-// row r sits at kc ^ ((r >> 2) & 3), so the 16 rows a quarter-wavefront reads
-// at one K offset fall in 16 distinct bank groups.  Copies past the last
-// stage reload it into a slot no phase reads again, so every iteration
-// issues and waits the same; rows past M or N are loaded from row M-1 / N-1
-// and masked at the store.
+// Ping-pong main loop for single products on 256 x 256 or 256 x 128 tiles.
+// Eight wavefronts in two groups of four, one wavefront of each group per
+// SIMD.  The groups alternate between an MFMA phase on fragments held in
+// registers and a memory phase (the next stage's fragments from LDS, this
+// wavefront's share of the copy of stage k+S-1, the wait for its share of
+// stage k+1), separated by workgroup barriers and offset by one phase: group
+// 1 passes one barrier before the loop and group 0 one after it, so both
+// pass the same number, and no stage is overwritten while either group may
+// still read it.  While one group's MFMAs run, the other group's LDS reads
+// and copies proceed on the same SIMDs.  Stages are BK = 32 deep (64-byte
+// rows, 4-stage ring) or 64 deep (128-byte rows, 3-stage ring: twice the
+// MFMAs per phase for the 64 x 64 wave tiles of 256 x 128).  Chunk kc of row
+// r sits at kc ^ ((r >> 2) & 3) (BK 32) or kc ^ ((r >> 1) & 7) (BK 64), so
+// the 16 rows a quarter-wavefront reads at one K offset fall in 16 distinct
+// bank groups.  Copies past the last stage reload it into a slot no phase
+// reads again, so every iteration issues and waits the same; rows past M or N
+// are loaded from row M-1 / N-1 and masked at the store.
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int EPI, int WAVES_M = (BN == 256 ? 2 : 4)>
+template <int BK>
+__device__ __forceinline__ int pp_chunk(int row, int kc) {
+  return BK == 64 ? (kc ^ ((row >> 1) & 7)) : (kc ^ ((row >> 2) & 3));
+}
+
+template <int BM, int BN, int EPI, int WAVES_M = (BN == 256 ? 2 : 4), int BK = 32>
 __global__ __launch_bounds__(512) void gemm_pp_kernel(GemmArgs p) {
-  constexpr int S = 4, BK = 32;
+  constexpr int S = BK == 64 ? 3 : 4;
+  constexpr int CPR = BK / 8;        // 16-byte chunks per stage row
+  constexpr int RPB = 64 / CPR;      // stage rows per 1 KB copy
+  constexpr int NS = BK / 16;        // MFMA substeps per stage
   constexpr int WAVES_N = 8 / WAVES_M;
   constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N, FM = WM / 32, FN = WN / 32;
-  constexpr int ABLK = BM / 16, BBLK = BN / 16, PW = (ABLK + BBLK) / 8;  // 1 KB copies per wave and stage
+  constexpr int ABLK = BM / RPB, BBLK = BN / RPB, PW = (ABLK + BBLK) / 8;  // 1 KB copies per wave and stage
   static_assert((ABLK + BBLK) % 8 == 0, "stage blocks must split over 8 waves");
 
-  __shared__ uint4 smem[S * (BM + BN) * 4];
-  uint4 (*sA)[BM * 4] = reinterpret_cast<uint4 (*)[BM * 4]>(smem);
-  uint4 (*sB)[BN * 4] = reinterpret_cast<uint4 (*)[BN * 4]>(smem + S * BM * 4);
+  __shared__ uint4 smem[S * (BM + BN) * CPR];
+  uint4 (*sA)[BM * CPR] = reinterpret_cast<uint4 (*)[BM * CPR]>(smem);
+  uint4 (*sB)[BN * CPR] = reinterpret_cast<uint4 (*)[BN * CPR]>(smem + S * BM * CPR);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -663,8 +674,8 @@ __global__ __launch_bounds__(512) void gemm_pp_kernel(GemmArgs p) {
   const int64_t m0 = int64_t(tm) * BM, n0 = int64_t(tn) * BN;
   const int64_t K = p.K;
 
-  // Lane l of a copy fills LDS slot l of a 1 KB block: row 16 blk + l / 4,
-  // slot l % 4, which holds chunk (l % 4) ^ ((row >> 2) & 3) of that row.
+  // Lane l of a copy fills LDS slot l of a 1 KB block: row RPB blk + l / CPR,
+  // slot l % CPR, which holds chunk pp_chunk(row, l % CPR) of that row.
   const uint16_t* src[PW];
   int dst_off[PW];
   bool isA[PW];
@@ -673,8 +684,8 @@ __global__ __launch_bounds__(512) void gemm_pp_kernel(GemmArgs p) {
     const int blk = wave * PW + j;
     const bool a = blk < ABLK;
     const int b = a ? blk : blk - ABLK;
-    const int row = b * 16 + (lane >> 2);
-    const int kc = (lane & 3) ^ ((row >> 2) & 3);
+    const int row = b * RPB + lane / CPR;
+    const int kc = pp_chunk<BK>(row, lane % CPR);
     isA[j] = a;
     const int64_t gr = a ? min(m0 + row, p.M - 1) : min(n0 + row, p.N - 1);
     src[j] = (a ? p.A : p.B) + gr * K + kc * 8;
@@ -699,25 +710,25 @@ __global__ __launch_bounds__(512) void gemm_pp_kernel(GemmArgs p) {
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
   const int lr = lane & 31, lh = lane >> 5;
-  int offA[2][FM], offB[2][FN];
+  int offA[NS][FM], offB[NS][FN];
 #pragma unroll
-  for (int s = 0; s < 2; ++s) {
+  for (int s = 0; s < NS; ++s) {
     const int kc = s * 2 + lh;
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
       const int row = wm * WM + i * 32 + lr;
-      offA[s][i] = row * 4 + (kc ^ ((row >> 2) & 3));
+      offA[s][i] = row * CPR + pp_chunk<BK>(row, kc);
     }
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
       const int row = wn * WN + j * 32 + lr;
-      offB[s][j] = row * 4 + (kc ^ ((row >> 2) & 3));
+      offB[s][j] = row * CPR + pp_chunk<BK>(row, kc);
     }
   }
-  bf16x8 af[2][FM], bfr[2][FN];
+  bf16x8 af[NS][FM], bfr[NS][FN];
   auto rd = [&](int st) {
 #pragma unroll
-    for (int s = 0; s < 2; ++s) {
+    for (int s = 0; s < NS; ++s) {
 #pragma unroll
       for (int i = 0; i < FM; ++i) af[s][i] = __builtin_bit_cast(bf16x8, sA[st][offA[s][i]]);
 #pragma unroll
@@ -731,7 +742,7 @@ __global__ __launch_bounds__(512) void gemm_pp_kernel(GemmArgs p) {
   __builtin_amdgcn_s_barrier();
   if (grp == 1) __builtin_amdgcn_s_barrier();
   for (int k = 0; k < nk; ++k) {
-    // memory phase: fragments of stage k, copy of stage k+3 into the slot
+    // memory phase: fragments of stage k, copy of stage k+S-1 into the slot
     // stage k-1 used (both groups finished reading it a phase ago)
     __builtin_amdgcn_sched_barrier(0);
     rd(k % S);
@@ -742,7 +753,7 @@ __global__ __launch_bounds__(512) void gemm_pp_kernel(GemmArgs p) {
     // MFMA phase
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int s = 0; s < 2; ++s)
+    for (int s = 0; s < NS; ++s)
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -790,6 +801,13 @@ template <int BM, int BN, int EPI>
 static void launch_epi(const GemmArgs& a, dim3 grid, hipStream_t st) {
   if constexpr (BM == 256 && (BN == 256 || BN == 128)) {
     if (a.K % 32 == 0 && grid.y == 1 && a.causal == 0) {
+      // 64-deep stages where 256 x 128 tiles allow them (three fit in LDS)
+      if constexpr (BN == 128) {
+        if (a.K % 64 == 0) {
+          hipLaunchKernelGGL((gemm_pp_kernel<BM, BN, EPI, 4, 64>), grid, dim3(512), 0, st, a);
+          return;
+        }
+      }
       hipLaunchKernelGGL((gemm_pp_kernel<BM, BN, EPI>), grid, dim3(512), 0, st, a);
       return;
     }

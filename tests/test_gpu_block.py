@@ -170,10 +170,11 @@ def test_silu_mul_kernels(n):
         assert np.all(err <= 2.0 ** -8 * np.abs(ref) + floor + 1e-38), (name, np.max(err / (np.abs(ref) + 1e-30)))
 
 
-# (4100, 2104, 512) and (4100, 4104, 256): the ping-pong kernel's 256 x 128 and
-# 256 x 256 tiles, ragged in both dimensions
+# (4100, 2104, 512), (4100, 2104, 480) and (4100, 4104, 256): the ping-pong
+# kernel's 256 x 128 tiles with 64-deep and 32-deep stages and its 256 x 256
+# tiles, ragged in both dimensions
 @pytest.mark.parametrize("M,N,K", [(1, 8, 8), (200, 264, 136), (512, 384, 1024), (1000, 2056, 72),
-                                   (4100, 2104, 512), (4100, 4104, 256)])
+                                   (4100, 2104, 512), (4100, 2104, 480), (4100, 4104, 256)])
 def test_gemm_nt(M, N, K):
     """out = scale A B^T against fp64 on the same bf16 operands: fp32 output
     within 1e-5 of the row's absolute sum (accumulation order), bf16 output
