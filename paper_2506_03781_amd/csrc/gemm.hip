@@ -649,6 +649,7 @@ __device__ __forceinline__ int pp_chunk(int row, int kc) {
 
 template <int BM, int BN, int EPI, int WAVES_M = (BN == 256 ? 2 : 4), int BK = 32>
 __global__ __launch_bounds__(512) void gemm_pp_kernel(GemmArgs p) {
+  select_batch(p);
   constexpr int S = BK == 64 ? 3 : 4;
   constexpr int CPR = BK / 8;        // 16-byte chunks per stage row
   constexpr int RPB = 64 / CPR;      // stage rows per 1 KB copy
@@ -673,6 +674,10 @@ __global__ __launch_bounds__(512) void gemm_pp_kernel(GemmArgs p) {
   tile_of<(BM == 256 && BN == 128) ? 4 : 8>(blockIdx.x, gridDim.x, p.tiles_m, p.tiles_n, tm, tn);
   const int64_t m0 = int64_t(tm) * BM, n0 = int64_t(tn) * BN;
   const int64_t K = p.K;
+  // causal structure (uniform per workgroup, before any barrier)
+  if (p.causal == 1 && n0 >= m0 + BM) return;
+  const int64_t kb = p.causal == 3 ? m0 : 0;
+  const int64_t ke = p.causal == 2 ? min(K, m0 + BM) : K;
 
   // Lane l of a copy fills LDS slot l of a 1 KB block: row RPB blk + l / CPR,
   // slot l % CPR, which holds chunk pp_chunk(row, l % CPR) of that row.
@@ -688,10 +693,10 @@ __global__ __launch_bounds__(512) void gemm_pp_kernel(GemmArgs p) {
     const int kc = pp_chunk<BK>(row, lane % CPR);
     isA[j] = a;
     const int64_t gr = a ? min(m0 + row, p.M - 1) : min(n0 + row, p.N - 1);
-    src[j] = (a ? p.A : p.B) + gr * K + kc * 8;
+    src[j] = (a ? p.A : p.B) + gr * K + kb + kc * 8;
     dst_off[j] = b * 64;
   }
-  const int nk = int(K / BK);
+  const int nk = int((ke - kb) / BK);
   auto issue = [&](int stage, int kstage) {
     const int64_t k0 = int64_t(min(kstage, nk - 1)) * BK;
 #pragma unroll
@@ -793,14 +798,13 @@ size_t gemm_workgroups(int64_t M, int64_t N, int /*epi*/) {
   }
 }
 
-// Single products with K a multiple of 32 on 256-row tiles: the ping-pong
-// kernel; other products with K a multiple of 32 (batched, causal, 128-row
-// tiles): the pipelined kernel; the register-staged kernel (any K that is a
-// multiple of 8) otherwise.
+// Products with K a multiple of 32 on 256-row tiles (single, batched or
+// causal): the ping-pong kernel; on 128-row tiles: the pipelined kernel; the
+// register-staged kernel (any K that is a multiple of 8) otherwise.
 template <int BM, int BN, int EPI>
 static void launch_epi(const GemmArgs& a, dim3 grid, hipStream_t st) {
   if constexpr (BM == 256 && (BN == 256 || BN == 128)) {
-    if (a.K % 32 == 0 && grid.y == 1 && a.causal == 0) {
+    if (a.K % 32 == 0) {
       // 64-deep stages where 256 x 128 tiles allow them (three fit in LDS)
       if constexpr (BN == 128) {
         if (a.K % 64 == 0) {
