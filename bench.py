@@ -17,14 +17,22 @@ over clipping ranges with the general alternating update, G = 30, T = 15 by
 default); its kernel time is reported under ``init`` with an ALU roofline and
 its own CPU-oracle baseline, outside the timed steps.
 
-Output: one JSON line.  ``value`` is the fake-quant fwd+bwd throughput in
-Gweights/s (weights quantized forward and backward per second of quantizer
-kernel time inside the timed steps); the reconstruction GEMM throughput is
-``gemm_tflops``.  Per-kernel averages come from HIP events recorded on the
-stream the kernels run on.  ``roofline`` describes the kernel with the largest
-share of step time; ``cpu_baseline`` times the CPU oracle on a bounded sample.
+Output: one JSON line.  The headline workload is the 70B MLP slice
+(``mlp70b``: gate/up 28672x8192 and down 8192x28672, 4096 tokens, k = 2 and
+3), the largest single-GPU configuration.  ``value`` is the fake-quant
+fwd+bwd throughput in Gweights/s (weights quantized forward and backward per
+second of quantizer kernel time inside the timed steps); the reconstruction
+GEMM throughput is ``gemm_tflops``.  Per-kernel averages come from HIP events
+recorded on the stream the kernels run on.  ``roofline`` describes the kernel
+with the largest share of step time; ``ceilings`` holds the streaming and
+MFMA rates this GPU reaches (measured in the same run) and each headline
+fraction against them; ``workloads`` holds the other configurations (the
+4096x4096 projection, the 7B MLP, the 7B block's seven matrices over 100
+timed steps) as sub-records; ``cpu_baseline`` times the CPU oracle on a
+bounded sample on all host cores.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+       python bench.py --summarize-profiles WORKLOAD   (CPU: profiles/ from rocprofv3 CSVs)
 """
 from __future__ import annotations
 
@@ -106,7 +114,15 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=50)
-    ap.add_argument("--workload", default="attn4096")
+    ap.add_argument("--workload", default="mlp70b")
+    ap.add_argument("--sub-workloads", default="attn4096,mlp7b,block7b",
+                    help="comma-separated workloads reported as sub-records ('' for none)")
+    ap.add_argument("--sub-steps", type=int, default=20, help="timed steps of each sub-record")
+    ap.add_argument("--block7b-steps", type=int, default=100,
+                    help="timed steps of the 7B block's seven matrices (the configuration times 100)")
+    ap.add_argument("--no-ceilings", action="store_true", help="skip the streaming and MFMA ceiling probes")
+    ap.add_argument("--summarize-profiles", default=None, metavar="WORKLOAD",
+                    help="(no GPU) write profiles/ summaries from the rocprofv3 CSVs under gpurun_out/")
     ap.add_argument("--mode", default="paper", choices=["paper", "full", "local", "frozen"])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -141,6 +157,14 @@ def fq_bytes_per_weight(k, g, mode, w_bytes=2, what_bytes=2, grad_bytes=2):
     # dL/dWhat, W, s, code in; s out; per group Delta, z_U in, alpha, z_B in and out
     bwd = grad_bytes + w_bytes + 4 + 1 + 4 + (8 + 2 * (4 * k + 4)) / g
     return fwd, bwd
+
+
+def fq_read_write_bytes(k, g, mode, w_bytes=2, what_bytes=2, grad_bytes=2):
+    """The read and written parts of fq_bytes_per_weight (forward + backward)."""
+    rd = (w_bytes + 4 + (1 if mode != "full" else 0) + (4 * k + 12) / g
+          + grad_bytes + w_bytes + 4 + 1 + (8 + 4 * k + 4) / g)
+    wr = what_bytes + 1 + 4 + (4 * k + 4) / g
+    return rd, wr
 
 
 def init_ops_per_weight(k, G, T):
@@ -200,47 +224,130 @@ def load_counters(workload):
     return d
 
 
-def cpu_baseline(layers_np, mode, budget_s=12.0):
-    """The oracle's fq_fwd + fq_bwd on a bounded row sample of each (matrix, k),
-    numpy restricted to one thread."""
+def host_cores() -> int:
+    return len(os.sched_getaffinity(0))
+
+
+def cpu_baseline(layers_np, X, mode, budget_s=20.0):
+    """The oracle on a bounded row sample of the headline workload's first
+    (matrix, k) layers, on the host cores of this machine: fq_fwd + fq_bwd
+    (the metric's unit; vectorised numpy, effectively one thread), the
+    reconstruction loss and weight gradient (fp64 matmuls, BLAS on every
+    core) and the fold.  Rows double until each part has used its share of
+    the budget."""
     from threadpoolctl import threadpool_limits
-    with threadpool_limits(1):
-        return _cpu_baseline(layers_np, mode, budget_s)
+    cores = host_cores()
+    with threadpool_limits(cores):
+        return _cpu_baseline(layers_np, X, mode, budget_s, cores)
 
 
-def _cpu_baseline(layers_np, mode, budget_s):
+def _timed_rows(fn, R, per, rows=8):
+    """Run fn(rows) with rows doubling until it takes >= per / 3 (or all rows)."""
+    while True:
+        t0 = time.perf_counter()
+        fn(rows)
+        dt = time.perf_counter() - t0
+        if dt >= per / 3 or rows >= R:
+            return rows, dt
+        rows = min(R, rows * 2)
+
+
+def _cpu_baseline(layers_np, X, mode, budget_s, cores):
     import numpy as np
     import oracle.uniquan as O
     omode = {"full": O.MAP_FULL, "local": O.MAP_LOCAL, "frozen": O.MAP_FROZEN}.get(mode, O.MAP_LOCAL)
-    total_w, total_t = 0, 0.0
-    rows_used = []
-    per = budget_s / max(1, len(layers_np))
+    per = budget_s / (3 * max(1, len(layers_np)))
+    fq_w = fq_t = rc_f = rc_t = fo_w = fo_t = 0.0
+    parts = []
+    Xb = np.asarray(X, np.float32)
+    T = Xb.shape[0]
     for (W, s, k, g) in layers_np:
         R, C = W.shape
-        rows = 16
-        spent = 0.0
-        while True:
-            Wr, sr = W[:rows], s[:rows]
-            p = O.init_param_set_a(Wr, sr, k, g)
-            a, z = p["alpha"], p["z_b"]
-            prev = O.fq_fwd(Wr, sr, a, z, k, g)["codes"]
+        cache = {}
+
+        def params(rows):
+            if rows not in cache:
+                Wr, sr = W[:rows], s[:rows]
+                p = O.init_param_set_a(Wr, sr, k, g)
+                prev = O.fq_fwd(Wr, sr, p["alpha"], p["z_b"], k, g)["codes"]
+                cache.clear()
+                cache[rows] = (Wr, sr, p["alpha"], p["z_b"], prev)
+            return cache[rows]
+
+        def fq(rows):
+            Wr, sr, a, z, prev = params(rows)
             Gr = np.random.default_rng(0).standard_normal(Wr.shape).astype(np.float32)
             t0 = time.perf_counter()
             f = O.fq_fwd(Wr, sr, a, z, k, g, mode=omode, codes_prev=prev)
             O.fq_bwd(Wr, sr, a, z, f["codes"], Gr, k, g)
-            dt = time.perf_counter() - t0
-            spent += dt
-            if spent >= per or rows >= R or dt > per / 3:
+            return time.perf_counter() - t0
+
+        # fq: time only the oracle calls (parameter set-up excluded)
+        rows = 8
+        while True:
+            dt = fq(rows)
+            if dt >= per / 3 or rows >= R:
                 break
             rows = min(R, rows * 2)
-        total_w += rows * C
-        total_t += dt
-        rows_used.append((rows, C, k))
-    sample = "; ".join(f"{r} rows x {c} cols at k={k}" for r, c, k in rows_used)
-    mname = "local" if mode == "paper" else mode
-    return {"value": total_w / total_t / 1e9, "unit": "Gweights/s", "cores": 1, "kind": "oracle",
-            "sample": f"oracle fq_fwd ({mname} mapping) + fq_bwd on the first rows of each matrix, "
-                      f"numpy on one thread: {sample}; {total_w} weights in {total_t:.2f} s"}
+        fq_w += rows * C
+        fq_t += dt
+        Wr, sr, a, z, _ = params(rows)
+        Rw = O.residual_f32(O.fq_fwd(Wr, sr, a, z, k, g)["what32"], Wr)
+        rr, dt2 = _timed_rows(lambda n: O.recon_residual(Xb, Rw[:n]), rows, per)
+        rc_f += 4.0 * T * rr * C
+        rc_t += dt2
+        fr, dt3 = _timed_rows(lambda n: O.fold(Wr[:n], sr[:n], a[: n * C // g], z[: n * C // g], k, g), rows, per)
+        fo_w += fr * C
+        fo_t += dt3
+        parts.append(f"{rows} rows x {C} cols at k={k} (recon on {rr} rows x {T} tokens, fold on {fr} rows)")
+    return {"value": fq_w / fq_t / 1e9, "unit": "Gweights/s", "cores": cores, "kind": "oracle",
+            "sample": "oracle fq_fwd (" + ("local" if mode == "paper" else mode) + " mapping) + fq_bwd, "
+                      "recon (fp64 matmuls) and fold on the first rows of the headline layers: "
+                      + "; ".join(parts) + f"; fq {int(fq_w)} weights in {fq_t:.2f} s",
+            "threads": {"fq": "vectorised numpy (one thread)", "recon": f"BLAS on {cores} threads",
+                        "fold": "vectorised numpy (one thread)"},
+            "recon_tflops": rc_f / rc_t / 1e12 if rc_t else None,
+            "fold_gweights_per_s": fo_w / fo_t / 1e9 if fo_t else None,
+            "seconds": {"fq": fq_t, "recon": rc_t, "fold": fo_t}}
+
+
+def ceilings(n_bytes=1 << 30, reps=5):
+    """What this GPU reaches: 16-byte nontemporal streaming read, write and
+    copy over n_bytes buffers (best of reps launches, each launch timed by
+    HIP events) and independent MFMA chains on registers."""
+    import torch
+
+    from paper_2506_03781_amd import uniquan as uq
+    sink = torch.empty(uq.uniquan_probe_sink_len(), dtype=torch.int32, device="cuda")
+    src = torch.ones(n_bytes // 4, dtype=torch.int32, device="cuda")
+    dst = torch.empty_like(src)
+    out = {}
+    for name, op, moved in (("read", 0, n_bytes), ("write", 1, n_bytes), ("copy", 2, 2 * n_bytes)):
+        best = None
+        for _ in range(reps + 1):
+            a, b = TimingEvent(), TimingEvent()
+            a.record()
+            uq.uniquan_probe_stream(op, n_bytes, src, dst, sink)
+            b.record()
+            torch.cuda.synchronize()
+            ms = a.elapsed_time(b)
+            best = ms if best is None else min(best, ms)
+        out[f"{name}_gbs"] = moved / (best * 1e-3) / 1e9
+    iters = 2000
+    best = None
+    for _ in range(reps + 1):
+        a, b = TimingEvent(), TimingEvent()
+        a.record()
+        uq.uniquan_probe_mfma(iters, sink)
+        b.record()
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b)
+        best = ms if best is None else min(best, ms)
+    out["mfma_bf16_tflops"] = uq.uniquan_probe_mfma_flops(iters) / (best * 1e-3) / 1e12
+    out["note"] = (f"streaming probes over {n_bytes >> 20} MiB buffers (best of {reps + 1}); "
+                   "MFMA probe: 8 independent v_mfma_f32_32x32x16_bf16 chains per wavefront, 4096 wavefronts")
+    del src, dst, sink
+    return out
 
 
 def bcq_inference(layers, batches=(1, 8), target_bytes=512 << 20):
@@ -375,30 +482,126 @@ def block_decoder(seed, k=3, steps=5, warmup=2, n_kv=None):
                     "quantized input, loss, backpropagation, straight-through backward + SGD); flops count "
                     "the GEMMs only"}
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); this build has no multi-GPU path.",
-              file=sys.stderr)
-        sys.exit(2)
-    import numpy as np
+# Kernel-name patterns of the step's four phases in rocprofv3 output.
+PHASE_PATTERNS = {
+    "fq_fwd": r"fq_fwd_kernel<1, 1, [23], ",
+    "gemm_fwd": r"gemm_pp_kernel<256, \d+, [14], ",
+    "gemm_bwd": r"gemm_pp_kernel<256, 256, 2, ",
+    "fq_bwd": r"fq_bwd_kernel<1, 1, ",
+}
+
+
+def summarize_profiles(workload, steps, warmup, out_dir=PROFILES, run_dir=os.path.join(ROOT, "gpurun_out")):
+    """Write profiles/uniquan_kernels_<workload>.md and pmc_<workload>.json from
+    the CSVs of three rocprofv3 runs of this script (commands in the summary):
+    a kernel trace with statistics, then FETCH_SIZE and WRITE_SIZE counter
+    runs.  Counters are scaled by what they read for a plain 256 MiB device
+    copy (run by --calib-copy in the counter runs)."""
+    import csv
+    import collections
+    import re
+    from paper_2506_03781_amd import synth
+    wl = synth.WORKLOADS[workload]
+    n_layers = len(wl.matrices) * len(wl.ks)
+    pdir = os.path.join(run_dir, f"prof_{workload}")
+    stats = list(csv.DictReader(open(os.path.join(pdir, "trace_kernel_stats.csv"))))
+    trace = list(csv.DictReader(open(os.path.join(pdir, "trace_kernel_trace.csv"))))
+
+    def counters(path):
+        d = collections.defaultdict(list)
+        for r in csv.DictReader(open(path)):
+            d[r["Kernel_Name"]].append(float(r["Counter_Value"]))
+        return d
+
+    fetch = counters(os.path.join(run_dir, f"pmc_fetch_{workload}", "fetch_counter_collection.csv"))
+    write = counters(os.path.join(run_dir, f"pmc_write_{workload}", "write_counter_collection.csv"))
+    kib_copy = 256 * 1024
+    cf = [v for k, vs in fetch.items() if "copyBuffer" in k for v in vs if v > kib_copy / 4]
+    cw = [v for k, vs in write.items() if "copyBuffer" in k for v in vs if v > kib_copy / 4]
+    fscale = kib_copy / (sum(cf) / len(cf))
+    wscale = kib_copy / (sum(cw) / len(cw))
+
+    def mean_kib(d, pat):
+        vals = [v for k, vs in d.items() if re.search(pat, k) for v in vs]
+        return sum(vals) / len(vals), len(vals)
+
+    kern = {}
+    for ph, pat in PHASE_PATTERNS.items():
+        f, nf = mean_kib(fetch, pat)
+        w, nw = mean_kib(write, pat)
+        kern[ph] = {"pattern": pat, "fetch_kib_raw": f, "write_kib_raw": w, "dispatches": [nf, nw],
+                    "hbm_bytes_per_launch": (f * fscale + w * wscale) * 1024}
+    win = {}
+    for ph, pat in list(PHASE_PATTERNS.items()) + [("loss_reduce", r"reduce_loss_kernel")]:
+        d = sorted((int(r["Start_Timestamp"]), int(r["End_Timestamp"])) for r in trace
+                   if re.search(pat, r["Kernel_Name"]))
+        sel = d[warmup * n_layers:(warmup + steps) * n_layers]
+        win[ph] = (len(sel), sum(e - b for b, e in sel) / max(1, len(sel)) / 1e3)
+    js = {"workload": workload, "src_hash": src_hash(), "fetch_scale": fscale, "write_scale": wscale,
+          "calibration": "plain 256 MiB device copy (torch copy_ -> __amd_rocclr_copyBuffer): FETCH_SIZE and "
+                         "WRITE_SIZE scaled so that it reads and writes 262144 KiB",
+          "kernels": kern, "trace_timed_avg_us": {ph: v[1] for ph, v in win.items()}}
+    json.dump(js, open(os.path.join(out_dir, f"pmc_{workload}.json"), "w"), indent=1)
+    cmd_common = f"--workload {workload} --no-cpu-baseline --no-block --no-ceilings --sub-workloads ''"
+    lines = [f"# rocprofv3 summary: UniQuan_F step kernels, workload `{workload}`", "",
+             f"Workload: {wl.description}; bench.py step (unified initialisation G = 30, T = 15 at set-up, "
+             "residual loss form, LOCAL/FROZEN mapping alternating); MI355X.", "",
+             "Commands (run from the repository root on the GPU box; the summary is then written on the CPU "
+             f"with `python bench.py --summarize-profiles {workload} --steps {steps} --warmup {warmup}`):", "",
+             "```",
+             f"rocprofv3 --kernel-trace --stats -f csv -d gpurun_out/prof_{workload} -o trace -- "
+             f"python3 bench.py --steps {steps} --warmup {warmup} {cmd_common}",
+             f"rocprofv3 --pmc FETCH_SIZE -f csv -d gpurun_out/pmc_fetch_{workload} -o fetch -- "
+             f"python3 bench.py --steps 2 --warmup 1 {cmd_common} --calib-copy",
+             f"rocprofv3 --pmc WRITE_SIZE -f csv -d gpurun_out/pmc_write_{workload} -o write -- "
+             f"python3 bench.py --steps 2 --warmup 1 {cmd_common} --calib-copy",
+             "```", "", f"Kernel sources hash (bench.src_hash): `{src_hash()}`", "",
+             f"## Timed steps only ({steps} steps after {warmup} warm-up steps, {n_layers} layers)", "",
+             "Per-dispatch durations from the trace (`trace_kernel_trace.csv`), each phase kernel's dispatches in "
+             "time order after the warm-up steps.  The bench's per-phase HIP events bracket a phase: gemm_fwd "
+             "is the loss GEMM plus its loss reduction.", "",
+             "| Phase | Kernel pattern | Dispatches | Average (us) |", "|---|---|---|---|"]
+    for ph, (n, avg) in win.items():
+        lines.append(f"| {ph} | `{PHASE_PATTERNS.get(ph, 'reduce_loss_kernel')}` | {n} | {avg:.1f} |")
+    lines += ["", "## HBM traffic per launch (`--pmc FETCH_SIZE`, `--pmc WRITE_SIZE`)", "",
+              f"Calibration on a plain 256 MiB device copy: FETCH_SIZE x {fscale:.3f}, WRITE_SIZE x {wscale:.3f}.",
+              "", "| Phase | Kernel pattern | FETCH_SIZE raw (KiB) | WRITE_SIZE (KiB) | HBM bytes / launch (scaled) |",
+              "|---|---|---|---|---|"]
+    for ph, k in kern.items():
+        lines.append(f"| {ph} | `{k['pattern']}` | {k['fetch_kib_raw']:.0f} | {k['write_kib_raw']:.0f} | "
+                     f"{k['hbm_bytes_per_launch'] / 1e6:.1f} MB |")
+    lines += ["", "## Kernel trace statistics (`--kernel-trace --stats`, whole run)", "",
+              "| Kernel | Calls | Average (us) | Min (us) | Max (us) | Share of GPU time |", "|---|---|---|---|---|---|"]
+    for r in stats:
+        n = r["Name"]
+        if "uq::" not in n:
+            continue
+        n = re.sub(r"\(uq::\w+\)", "", n).replace("void ", "")
+        lines.append(f"| `{n[:90]}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
+                     f"{float(r['MinNs']) / 1e3:.1f} | {float(r['MaxNs']) / 1e3:.1f} | {float(r['Percentage']):.1f}% |")
+    open(os.path.join(out_dir, f"uniquan_kernels_{workload}.md"), "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def progress(msg):
+    """One progress line on stderr (stdout carries only the JSON line)."""
+    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+
+
+def build_layers(wl, args, want_cpu):
+    """Device state of every (matrix, k) of a workload: synthetic data,
+    unified initialisation (timed), the initial FULL mapping and L0."""
     import torch
 
     from paper_2506_03781_amd import synth
     from paper_2506_03781_amd import uniquan as uq
     from paper_2506_03781_amd.layer import QuantLayer
-
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
-    torch.cuda.set_device(0)
-    uq.lib()
-    wl = synth.WORKLOADS[args.workload]
     g = wl.group_size
-    layers = []
-    host_np = []
-    init_ms = []
-    init_np = None
+    layers, host_np, init_ms = [], [], []
+    init_np, X_np = None, None
     for spec in wl.matrices:
         m = synth.make_matrix(spec, args.seed)
+        progress(f"{wl.name}: {spec.name} {spec.R}x{spec.C} generated")
         wdt = torch.bfloat16 if spec.dtype == "bf16" else torch.float32
         for k in wl.ks:
             lay = QuantLayer(m.W, m.X, m.s, k, g, w_dtype=wdt, residual=not args.target)
@@ -411,8 +614,8 @@ def main():
                 e1.record()
                 torch.cuda.synchronize()
                 init_ms.append(e0.elapsed_time(e1))
-                if init_np is None and not args.no_cpu_baseline:
-                    init_np = (m.W, k, g)
+                if init_np is None and want_cpu:
+                    init_np = (m.W[:64].copy(), k, g)
             else:
                 lay.init_greedy()
             lay.prepare()
@@ -424,118 +627,201 @@ def main():
             lay.l0 = float(lay.loss.item())
             lay.lr = (0.005 / lay.l0, 0.0005 / lay.l0)
             layers.append(lay)
-            if not args.no_cpu_baseline and len(host_np) < 2:
-                host_np.append((m.W, m.s, k, g))
+            if want_cpu and len(host_np) < 2:
+                nr = min(m.R, 4096)
+                host_np.append((m.W[:nr].copy(), m.s[:nr].copy(), k, g))
+                if X_np is None:
+                    X_np = m.X.copy()
         del m
     torch.cuda.synchronize()
+    return layers, init_ms, host_np, init_np, X_np
 
-    phases = ["fq_fwd", "gemm_fwd", "gemm_bwd", "fq_bwd"]
-    ev = {}
-    # Each phase's launches are recorded through the checked wrappers the
-    # first time it runs (a warm-up step) and replayed afterwards, so the
-    # host enqueues a phase in a few microseconds and the stream stays ahead
-    # of the GPU; the timing events are created before the timed steps.
-    launches = {}
 
-    def phase(li, lay, name, mode, fn, *a):
+PHASES = ["fq_fwd", "gemm_fwd", "gemm_bwd", "fq_bwd"]
+
+
+class StepRunner:
+    """The timed steps of a list of layers.  Each phase's launches are
+    recorded through the checked wrappers the first time it runs (a warm-up
+    step) and replayed afterwards, so the host enqueues a phase in a few
+    microseconds and the stream stays ahead of the GPU; the timing events are
+    created before the timed steps."""
+
+    def __init__(self, layers, mode):
+        self.layers, self.mode = layers, mode
+        self.launches = {}
+
+    def phase(self, li, name, mode, fn, *a):
+        from paper_2506_03781_amd import uniquan as uq
         key = (li, name, mode)
-        if key in launches:
-            launches[key]()
+        if key in self.launches:
+            self.launches[key]()
         else:
-            launches[key] = uq.record(fn, *a)
+            self.launches[key] = uq.record(fn, *a)
 
-    def run_step(step, timed):
-        mode = schedule(args.mode, step)
-        for li, lay in enumerate(layers):
-            es = ev_pool.pop() if timed else None
-            if timed:
+    def step(self, step, evs=None):
+        from paper_2506_03781_amd import uniquan as uq
+        mode = schedule(self.mode, step)
+        for li, lay in enumerate(self.layers):
+            es = evs[li] if evs is not None else None
+            if es:
                 es[0].record()
-            phase(li, lay, "fq_fwd", mode, lay.fq_fwd, mode)
-            if timed:
+            self.phase(li, "fq_fwd", mode, lay.fq_fwd, mode)
+            if es:
                 es[1].record()
-            phase(li, lay, "gemm_fwd", 0, lay.recon, False)
-            if timed:
+            self.phase(li, "gemm_fwd", 0, lay.recon, False)
+            if es:
                 es[2].record()
-            phase(li, lay, "gemm_bwd", 0, uq.uniquan_layer_grad, lay.T, lay.R, lay.C, lay.Et, lay.Xt, lay.G)
-            if timed:
+            self.phase(li, "gemm_bwd", 0, uq.uniquan_layer_grad, lay.T, lay.R, lay.C, lay.Et, lay.Xt, lay.G)
+            if es:
                 es[3].record()
-            phase(li, lay, "fq_bwd", 0, lay.fq_bwd_sgd, *lay.lr)
-            if timed:
+            self.phase(li, "fq_bwd", 0, lay.fq_bwd_sgd, *lay.lr)
+            if es:
                 es[4].record()
-                ev.setdefault(li, []).append(es)
 
-    ev_pool = [[TimingEvent() for _ in range(5)] for _ in range(args.steps * len(layers))]
-    for s in range(args.warmup):
-        run_step(s, False)
-    if args.calib_copy:
-        src = torch.empty(64 << 20, dtype=torch.float32, device="cuda")
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for s in range(args.steps):
-        run_step(args.warmup + s, True)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ms_per_step = (t1 - t0) * 1e3 / args.steps
-    rel_loss = [float(lay.loss.item()) / lay.l0 for lay in layers]
-    finite = all(math.isfinite(r) for r in rel_loss) and all(bool(torch.isfinite(lay.s).all()) for lay in layers)
+    def run(self, steps, warmup):
+        """warmup untimed steps, then `steps` timed ones; per-phase HIP events."""
+        import torch
+        pool = [[[TimingEvent() for _ in range(5)] for _ in self.layers] for _ in range(steps)]
+        for s_ in range(warmup):
+            self.step(s_)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for s_ in range(steps):
+            self.step(warmup + s_, pool[s_])
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        tot = {p: 0.0 for p in PHASES}
+        per_layer = []
+        for li in range(len(self.layers)):
+            d = {p: 0.0 for p in PHASES}
+            for es_step in pool:
+                es = es_step[li]
+                for i, p in enumerate(PHASES):
+                    d[p] += es[i].elapsed_time(es[i + 1])
+            for p in PHASES:
+                d[p] /= steps
+                tot[p] += d[p]
+            per_layer.append(d)
+        self.next_step = warmup + steps
+        return {"ms_per_step": (t1 - t0) * 1e3 / steps, "wall_s": t1 - t0, "tot": tot, "per_layer": per_layer}
 
-    # per-phase totals (ms per step) and per-launch averages
-    tot = {p: 0.0 for p in phases}
-    per_layer = []
-    for li, lay in enumerate(layers):
-        d = {p: 0.0 for p in phases}
-        for es in ev[li]:
-            for i, p in enumerate(phases):
-                d[p] += es[i].elapsed_time(es[i + 1])
-        for p in phases:
-            d[p] /= args.steps
-            tot[p] += d[p]
-        per_layer.append(d)
 
+def layer_kernel_stats(layers, tot, mode0):
+    """Per-phase achieved rates, averaged over the layers' launches."""
+    import torch
+    n = len(layers)
+    out = {}
+    for ph in PHASES:
+        dur_ms = tot[ph] / n
+        if ph in ("gemm_fwd", "gemm_bwd"):
+            work = sum(2.0 * l.T * l.R * l.C for l in layers) / n
+            ach = work / (dur_ms * 1e-3) / 1e12
+            out[ph] = dict(bound="mfma", achieved=ach, peak=MFMA_BF16_PEAK_TFLOPS, unit="TFLOP/s",
+                           frac=ach / MFMA_BF16_PEAK_TFLOPS, avg_ms=dur_ms, algorithmic_flops=work)
+            continue
+        byt = 0.0
+        for l in layers:
+            wb = 2 if l.W.dtype == torch.bfloat16 else 4
+            f, b = fq_bytes_per_weight(l.k, l.g, mode0, wb)
+            byt += (f if ph == "fq_fwd" else b) * l.R * l.C
+        byt /= n
+        ach = byt / (dur_ms * 1e-3) / 1e9
+        out[ph] = dict(bound="hbm", achieved=ach, peak=HBM_PEAK_GBS, unit="GB/s", frac=ach / HBM_PEAK_GBS,
+                       avg_ms=dur_ms, algorithmic_bytes=byt)
+    return out
+
+
+def step_summary(layers, res, mode0):
+    import torch
+    tot = res["tot"]
     weights = sum(l.R * l.C for l in layers)
     flops = sum(4.0 * l.T * l.R * l.C for l in layers)
     fq_ms = tot["fq_fwd"] + tot["fq_bwd"]
     gemm_ms = tot["gemm_fwd"] + tot["gemm_bwd"]
-    value = weights / (fq_ms * 1e-3) / 1e9
-    gemm_tflops = flops / (gemm_ms * 1e-3) / 1e12
-    mode0 = "local" if args.mode == "paper" else args.mode
     fq_bytes = 0.0
     for l in layers:
         wb = 2 if l.W.dtype == torch.bfloat16 else 4
         f, b = fq_bytes_per_weight(l.k, l.g, mode0, wb)
         fq_bytes += (f + b) * l.R * l.C
     fq_gbs = fq_bytes / (fq_ms * 1e-3) / 1e9
+    gemm_tflops = flops / (gemm_ms * 1e-3) / 1e12
+    rel = [float(l.loss.item()) / l.l0 for l in layers]
+    finite = all(math.isfinite(r) for r in rel) and all(bool(torch.isfinite(l.s).all()) for l in layers)
+    return {"value": weights / (fq_ms * 1e-3) / 1e9, "fq_hbm_gbs": fq_gbs, "fq_frac_hbm": fq_gbs / HBM_PEAK_GBS,
+            "gemm_tflops": gemm_tflops, "gemm_frac_mfma": gemm_tflops / MFMA_BF16_PEAK_TFLOPS,
+            "rel_loss": rel, "finite": finite}
 
-    # per-kernel rooflines (averaged over the layers' launches)
-    def kernel_stats(phase):
-        n = len(layers)
-        dur_ms = tot[phase] / n
-        if phase in ("gemm_fwd", "gemm_bwd"):
-            work = sum(2.0 * l.T * l.R * l.C for l in layers) / n
-            ach = work / (dur_ms * 1e-3) / 1e12
-            return dict(bound="mfma", achieved=ach, peak=MFMA_BF16_PEAK_TFLOPS, unit="TFLOP/s",
-                        frac=ach / MFMA_BF16_PEAK_TFLOPS, avg_ms=dur_ms, algorithmic_flops=work)
-        byt = 0.0
-        for l in layers:
-            wb = 2 if l.W.dtype == torch.bfloat16 else 4
-            f, b = fq_bytes_per_weight(l.k, l.g, mode0, wb)
-            byt += (f if phase == "fq_fwd" else b) * l.R * l.C
-        byt /= n
-        ach = byt / (dur_ms * 1e-3) / 1e9
-        return dict(bound="hbm", achieved=ach, peak=HBM_PEAK_GBS, unit="GB/s", frac=ach / HBM_PEAK_GBS,
-                    avg_ms=dur_ms, algorithmic_bytes=byt)
 
-    ks = {p: kernel_stats(p) for p in ("fq_fwd", "gemm_fwd", "gemm_bwd", "fq_bwd")}
+def sub_record(name, args, steps, warmup):
+    """A compact record of another configuration: the same step, kernels and
+    method as the headline; only the sizes differ."""
+    import torch
+
+    from paper_2506_03781_amd import synth
+    wl = synth.WORKLOADS[name]
+    layers, init_ms, _, _, _ = build_layers(wl, args, False)
+    mode0 = "local" if args.mode == "paper" else args.mode
+    res = StepRunner(layers, args.mode).run(steps, warmup)
+    sm = step_summary(layers, res, mode0)
+    ks = layer_kernel_stats(layers, res["tot"], mode0)
+    rec = {"description": wl.description, "matrices": [[l.R, l.C] for l in layers], "T": layers[0].T,
+           "k": [l.k for l in layers], "g": wl.group_size, "steps": steps, "warmup": warmup,
+           "ms_per_step": res["ms_per_step"], "timed_s": res["wall_s"],
+           "value": sm["value"], "unit": "Gweights/s", "fq_frac_hbm": sm["fq_frac_hbm"],
+           "gemm_tflops": sm["gemm_tflops"], "gemm_frac_mfma": sm["gemm_frac_mfma"],
+           "phase_ms_per_step": res["tot"],
+           "kernels": {p: {"avg_ms": v["avg_ms"], "achieved": v["achieved"], "unit": v["unit"], "frac": v["frac"]}
+                       for p, v in ks.items()},
+           "init_ms_total": sum(init_ms), "rel_loss_after_timed_steps": sm["rel_loss"],
+           "state_finite": sm["finite"]}
+    del layers
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return rec
+
+
+def main():
+    args = parse()
+    if args.summarize_profiles:
+        summarize_profiles(args.summarize_profiles, args.steps, args.warmup)
+        return
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); this build has no multi-GPU path.",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2506_03781_amd import synth
+    from paper_2506_03781_amd import uniquan as uq
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    uq.lib()
+    wl = synth.WORKLOADS[args.workload]
+    g = wl.group_size
+    want_cpu = not args.no_cpu_baseline
+    layers, init_ms, host_np, init_np, X_np = build_layers(wl, args, want_cpu)
+    mode0 = "local" if args.mode == "paper" else args.mode
+
+    runner = StepRunner(layers, args.mode)
+    if args.calib_copy:
+        src = torch.empty(64 << 20, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        del src, dst
+    res = runner.run(args.steps, args.warmup)
+    progress(f"{args.workload}: {args.steps} timed steps, {res['ms_per_step']:.3f} ms per step")
+    tot, per_layer = res["tot"], res["per_layer"]
+    sm = step_summary(layers, res, mode0)
+    ks = layer_kernel_stats(layers, tot, mode0)
     dom = max(ks, key=lambda p: ks[p]["avg_ms"])
     counters = load_counters(args.workload)
     for p, st in ks.items():
         tr = None
         if counters and p in counters.get("kernels", {}):
-            c = counters["kernels"][p]
-            tr = c.get("hbm_bytes_per_launch")
+            tr = counters["kernels"][p].get("hbm_bytes_per_launch")
         st["traffic"] = tr
     roof = {k2: ks[dom][k2] for k2 in ("bound", "achieved", "peak", "unit", "frac", "traffic")}
     roof["kernel"] = dom
@@ -557,39 +843,38 @@ def main():
     # GEMM's epilogue (after the timed region; not part of `value`)
     fused = None
     if all(l.k <= 4 and l.g <= 128 and l.T % 32 == 0 for l in layers):
+        nfs = min(args.steps, 10)
         fev = []
-        fpool = [[TimingEvent() for _ in range(2)] for _ in range(args.steps)]
-        for s_ in range(args.steps + 2):
-            mode = schedule(args.mode, args.warmup + args.steps + s_)
+        fpool = [[TimingEvent() for _ in range(2)] for _ in range(nfs)]
+        for s_ in range(nfs + 2):
+            mode = schedule(args.mode, runner.next_step + s_)
             e = fpool.pop() if s_ >= 2 else None
             if e:
                 e[0].record()
             for li, lay in enumerate(layers):
-                phase(li, lay, "fq_fwd", mode, lay.fq_fwd, mode)
-                phase(li, lay, "gemm_fwd", 0, lay.recon, False)
-                phase(li, lay, "ste_sgd", 0, lay.grad_ste_sgd, *lay.lr)
+                runner.phase(li, "fq_fwd", mode, lay.fq_fwd, mode)
+                runner.phase(li, "gemm_fwd", 0, lay.recon, False)
+                runner.phase(li, "ste_sgd", 0, lay.grad_ste_sgd, *lay.lr)
             if e:
                 e[1].record()
                 fev.append(e)
         torch.cuda.synchronize()
         fused_ms = sum(a.elapsed_time(b) for a, b in fev) / len(fev)
-        fused = {"ms_per_step": fused_ms, "unfused_ms_per_step_events": sum(tot.values()),
+        fused = {"ms_per_step": fused_ms, "unfused_ms_per_step_events": sum(tot.values()), "steps": nfs,
                  "note": "fq_fwd -> loss GEMM -> weight-gradient GEMM with the straight-through backward "
                          "and SGD update in its epilogue (dL/dWhat never written)"}
 
     bcq = bcq_inference(layers)
-    blk = None if args.no_block else block_decoder(args.seed, n_kv=args.block_kv)
-    # the same block with grouped-query attention (8 key/value heads, as in Mistral 7B and Llama-3 8B)
-    blk_gqa = None if (args.no_block or args.block_kv is not None) else block_decoder(args.seed, n_kv=8)
-
+    progress("per-mode, fused and deployment legs done")
+    rel_loss, finite = sm["rel_loss"], sm["finite"]
     out = {
         "metric": "fake-quant fwd+bwd Gweights/s (%HBM peak); recon GEMM TFLOP/s (%MFMA)",
-        "value": value,
+        "value": sm["value"],
         "unit": "Gweights/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms_per_step,
+        "ms_per_step": res["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -599,10 +884,10 @@ def main():
                    "matrices": [[l.R, l.C] for l in layers], "T": layers[0].T, "k": [l.k for l in layers],
                    "g": g, "mapping": args.mode, "seed": args.seed, "parallelism": "single GPU",
                    "loss_form": "target" if args.target else "residual"},
-        "fq_hbm_gbs": fq_gbs,
-        "fq_frac_hbm": fq_gbs / HBM_PEAK_GBS,
-        "gemm_tflops": gemm_tflops,
-        "gemm_frac_mfma": gemm_tflops / MFMA_BF16_PEAK_TFLOPS,
+        "fq_hbm_gbs": sm["fq_hbm_gbs"],
+        "fq_frac_hbm": sm["fq_frac_hbm"],
+        "gemm_tflops": sm["gemm_tflops"],
+        "gemm_frac_mfma": sm["gemm_frac_mfma"],
         "phase_ms_per_step": tot,
         "per_layer_phase_ms": per_layer,
         "kernels": ks,
@@ -615,8 +900,6 @@ def main():
         "bcq_inference": {"per_call": bcq,
                           "note": "deployed layer (fold -> bit-planes + binary16 Theta*_B): Y = X What^T for T "
                                   "activation rows; bytes = planes + parameters + X + Y"},
-        "block_decoder": blk,
-        "block_decoder_gqa": blk_gqa,
         "counters_src_hash": src_hash(),
         "precision": "quantizer: fp32 arithmetic on bf16 W / fp32 s, bf16 What and dL/dWhat; "
                      "GEMMs: bf16 MFMA with fp32 accumulation",
@@ -632,11 +915,58 @@ def main():
             "roofline": {"bound": "alu", "achieved": ach, "peak": VALU_PEAK_TOPS, "unit": "Tops/s",
                          "frac": ach / VALU_PEAK_TOPS, "algorithmic_ops": ops},
         }
-        if init_np is not None:
-            out["init"]["cpu_baseline"] = cpu_baseline_init(*init_np, args.init_grid, args.init_rounds,
-                                                            args.init_clip)
-    if not args.no_cpu_baseline and host_np:
-        out["cpu_baseline"] = cpu_baseline(host_np, args.mode)
+    fq_mix = [0.0, 0.0]
+    for l in layers:
+        wb = 2 if l.W.dtype == torch.bfloat16 else 4
+        r_, w_ = fq_read_write_bytes(l.k, l.g, mode0, wb)
+        fq_mix[0] += r_ * l.R * l.C
+        fq_mix[1] += w_ * l.R * l.C
+    del layers, runner
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+    if not args.no_ceilings:
+        ce = ceilings()
+        progress(f"ceilings: {json.dumps({k: round(v, 1) for k, v in ce.items() if k != 'note'})}")
+        out["ceilings"] = ce
+        ach_fq = sm["fq_hbm_gbs"]
+        # the quantizer kernels read more than they write: the ceiling of
+        # their mix is time = read bytes / read rate + written bytes / write rate
+        rd, wr = fq_mix
+        mix = (rd + wr) / (rd / ce["read_gbs"] + wr / ce["write_gbs"])
+        out["ceilings"]["fq_mix_ceiling_gbs"] = mix
+        out["ceilings"]["fq_frac_of_mix_ceiling"] = ach_fq / mix
+        out["ceilings"]["fq_frac_of_copy"] = ach_fq / ce["copy_gbs"]
+        out["ceilings"]["fq_frac_of_read"] = ach_fq / ce["read_gbs"]
+        out["ceilings"]["gemm_frac_of_mfma_probe"] = sm["gemm_tflops"] / ce["mfma_bf16_tflops"]
+        out["ceilings"]["roofline_frac_of_measured"] = roof["achieved"] / (
+            ce["mfma_bf16_tflops"] if roof["bound"] == "mfma" else ce["copy_gbs"])
+
+    subs = [w for w in args.sub_workloads.split(",") if w and w != args.workload]
+    if subs:
+        out["workloads"] = {}
+        for w in subs:
+            n_steps = args.block7b_steps if w == "block7b" else args.sub_steps
+            out["workloads"][w] = sub_record(w, args, n_steps, min(args.warmup, 5))
+            progress(f"sub-record {w}: {out['workloads'][w]['ms_per_step']:.3f} ms per step")
+        if "block7b" in out["workloads"]:
+            out["workloads"]["block7b"]["note"] = (
+                f"the 7B block's seven matrices (q, k, v, o, gate, up, down), each a single-layer step; "
+                f"{args.block7b_steps} optimisation steps timed")
+
+    if not args.no_block:
+        out["block_decoder"] = block_decoder(args.seed, n_kv=args.block_kv)
+        progress(f"decoder block: {out['block_decoder']['ms_per_step']:.2f} ms per step")
+        # the same block with grouped-query attention (8 key/value heads, as in Mistral 7B and Llama-3 8B)
+        if args.block_kv is None:
+            out["block_decoder_gqa"] = block_decoder(args.seed, n_kv=8)
+
+    if init_np is not None:
+        out["init"]["cpu_baseline"] = cpu_baseline_init(*init_np, args.init_grid, args.init_rounds,
+                                                        args.init_clip)
+    if want_cpu and host_np:
+        progress("cpu baseline (oracle on the host cores)")
+        out["cpu_baseline"] = cpu_baseline(host_np, X_np, args.mode)
     print(json.dumps(out), flush=True)
 
 

@@ -575,6 +575,26 @@ uq_status uniquan_init_unified(int64_t R, int64_t C, int k, int g,
  */
 uq_status uniquan_sgd(int64_t n, float* theta, const float* grad, float lr, void* stream);
 
+/*
+ * Measurement probes (not part of the method): the streaming HBM rates and
+ * the bf16 MFMA issue rate this GPU reaches, reported next to the nominal
+ * peaks.  sink [uniquan_probe_sink_len()] uint32/fp32 receives one word per
+ * lane (so that nothing is optimised away); its contents are meaningless.
+ *
+ * uniquan_probe_stream -- op 0 reads n_bytes of src, op 1 writes n_bytes of
+ * dst, op 2 copies n_bytes from src to dst; 16-byte nontemporal accesses in a
+ * grid-stride loop.  n_bytes a positive multiple of 16; src, dst 16-byte
+ * aligned device memory (the unused one may be NULL).
+ * uniquan_probe_mfma -- iters rounds of independent v_mfma_f32_32x32x16_bf16
+ * chains on register operands over the whole GPU; the work done is
+ * uniquan_probe_mfma_flops(iters) floating-point operations.
+ */
+size_t uniquan_probe_sink_len(void);
+double uniquan_probe_mfma_flops(int iters);
+uq_status uniquan_probe_stream(int op, int64_t n_bytes, const void* src, void* dst,
+                               uint32_t* sink, void* stream);
+uq_status uniquan_probe_mfma(int iters, float* sink, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -2,12 +2,16 @@
 // (Theorem 1, Eq. (4)), binary-coding dequantization (Sec. 2.3) and the
 // greedy binary-coding start (appendix "General alternating update").
 //
-// Work split: a workgroup of 256 lanes owns one tile of whole groups; each
-// lane streams 8 consecutive weights (16-byte bf16 / 2x16-byte fp32 loads),
-// so a 128-weight group is 16 lanes.  The tile's level tables are built and
-// sorted in LDS once, then every lane maps its 8 weights with an LDS binary
-// search.  HBM-bound: per weight the forward reads W (2 B) and s (4 B) and
-// writes What (2 B) and the code byte (1 B).
+// Work split of the forward: each wavefront owns 512 consecutive weights
+// (8 per lane, 16-byte bf16 / 2 x 16-byte fp32 loads; g divides 512, so a
+// group never straddles wavefronts and a 128-weight group is 16 lanes) and
+// builds the sorted level tables of its own groups in a private LDS region,
+// with wave-local ordering only; every lane then maps its 8 weights by an LDS
+// binary search (FULL), a neighbour-table lookup (LOCAL) or the stored code
+// (FROZEN).  The fold, dequantization and greedy kernels work on tiles of
+// whole groups per workgroup with workgroup-wide tables.  HBM-bound: per
+// weight the forward reads W (2 B) and s (4 B) and writes What (2 B) and the
+// code byte (1 B).
 #include "uq_device.h"
 #include "uq_launch.h"
 

@@ -9,16 +9,21 @@
 // All are C[M x N] = A[M x K] B[N x K]^T with both operands K-contiguous
 // ("NT"), so one kernel template serves them.
 //
-// Tiling: a 256-thread workgroup (4 wavefronts, 2 x 2) computes a BM x BN
-// tile (256x256, 256x128 or 128x128, the largest that still fills the 256
-// compute units); each wavefront owns (BM/2) x (BN/2) as a grid of 32x32 MFMA
-// blocks with fp32 accumulators.  The main kernel streams K in 32-wide
-// slices through a 4-stage LDS ring filled by global_load_lds_dwordx4 (direct
-// to LDS, XOR-swizzled rows) with explicit vmcnt waits and s_barrier; a
-// register-staged variant with 64-wide double-buffered slabs serves K not
-// divisible by 32.  Workgroups are renumbered so that each XCD gets a
-// contiguous run of tiles walked in groups of 8 row-tiles, which keeps the
-// operand panels it needs in its own L2.
+// Kernels (all bf16 MFMA v_mfma_f32_32x32x16_bf16, fp32 accumulation):
+//   gemm_pp_kernel    the main one, for K % 32 == 0 on 256 x 256 and 256 x 128
+//                     tiles: eight wavefronts in two groups that alternate
+//                     ("ping-pong") between an MFMA phase and a memory phase
+//                     (LDS fragment reads, global_load_lds copies into a ring
+//                     of 32- or 64-deep stages, exact vmcnt waits, barriers);
+//   gemm_pipe_kernel  four wavefronts, the same direct-to-LDS stage ring, for
+//                     128 x 128 tiles (shapes too small to fill the GPU with
+//                     256-row tiles);
+//   gemm_nt_kernel    register-staged, 64-deep double-buffered slabs, for K
+//                     not a multiple of 32.
+// The tile is the largest of 256x256, 256x128, 128x128 that still gives a
+// workgroup per compute unit.  Workgroups are renumbered so that each XCD
+// gets a contiguous run of tiles walked in groups of row-tiles, which keeps
+// the operand panels it needs in its own L2.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 

@@ -13,9 +13,12 @@ Protocol": 128 sequences of 2048 tokens), which are not available: heavy-tailed
 Student-t weights with outlier input channels, Gaussian or SiLU-gated Gaussian
 activations, at the shapes of 7B / 70B attention and MLP projections.
 
-Random streams: numpy ``Generator(PCG64(SeedSequence([seed, tag])))`` with a
-fixed integer tag per tensor, so every tensor is reproducible on its own.
-Seeds 0, 1, 2 follow the paper's evaluation protocol.
+Random streams: numpy ``Generator(PCG64(SeedSequence([seed, tag, sub, i])))``
+with a fixed integer tag (and sub-tag) per tensor and i the index of a fixed
+chunk of 2^22 elements, so every tensor is reproducible on its own and chunks
+can be drawn in parallel.  Student-t(nu) samples are Z / sqrt(V / nu) with
+Z ~ N(0, 1) and V ~ chi-square(nu) drawn as 2 Gamma(nu / 2).  Seeds 0, 1, 2
+follow the paper's evaluation protocol.
 """
 from __future__ import annotations
 
@@ -105,14 +108,65 @@ def _name_tag(name: str) -> int:
     return zlib.crc32(name.encode())
 
 
+# Large tensors are drawn in fixed chunks of CHUNK elements (row-major order),
+# chunk i from its own stream rng(seed, tag, sub, i), so a tensor is the same
+# whatever the number of threads that fill it.
+CHUNK = 1 << 22
+_POOL = None
+
+
+def _pool():
+    global _POOL
+    if _POOL is None:
+        import os
+        from concurrent.futures import ThreadPoolExecutor
+        n = max(1, min(16, len(os.sched_getaffinity(0))))
+        _POOL = ThreadPoolExecutor(n)
+    return _POOL
+
+
+def _fill(shape, seed: int, tag: int, sub: int, draw) -> np.ndarray:
+    """float32 array of `shape`; draw(generator, out) fills one flat chunk."""
+    out = np.empty(shape, np.float32)
+    flat = out.reshape(-1)
+    n = flat.size
+    starts = range(0, n, CHUNK)
+
+    def one(i0):
+        draw(np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, tag, sub, i0 // CHUNK]))),
+             flat[i0:min(n, i0 + CHUNK)])
+
+    list(_pool().map(one, starts))
+    return out
+
+
+def _student_t(nu: float, scale: float):
+    """Student-t(nu) times scale: Z / sqrt(V / nu) with Z ~ N(0, 1) and
+    V = 2 Gamma(nu / 2) ~ chi-square(nu), drawn in float64 and stored fp32."""
+    def draw(g, out):
+        z = g.standard_normal(out.size)
+        v = g.standard_gamma(nu / 2.0, out.size) * (2.0 / nu)
+        np.multiply(z / np.sqrt(v), scale, out=out, casting="same_kind")
+    return draw
+
+
+def _normal(scale: float = 1.0, shift: float = 0.0):
+    def draw(g, out):
+        g.standard_normal(out=out, dtype=np.float32)
+        if scale != 1.0:
+            out *= np.float32(scale)
+        if shift != 0.0:
+            out += np.float32(shift)
+    return draw
+
+
 def _weights(spec: MatrixSpec, seed: int, cols: np.ndarray) -> np.ndarray:
-    g = rng(seed, TAG_W, _name_tag(spec.name))
+    sub = _name_tag(spec.name)
     if spec.w_dist == "normal":
-        w = g.standard_normal((spec.R, spec.C), dtype=np.float32) * np.float32(spec.w_std)
+        w = _fill((spec.R, spec.C), seed, TAG_W, sub, _normal(spec.w_std))
     else:
         nu = spec.w_nu
-        scale = spec.w_std / np.sqrt(nu / (nu - 2.0))
-        w = (g.standard_t(nu, size=(spec.R, spec.C)) * scale).astype(np.float32)
+        w = _fill((spec.R, spec.C), seed, TAG_W, sub, _student_t(nu, spec.w_std / np.sqrt(nu / (nu - 2.0))))
     if cols.size and spec.w_outlier_mult != 1.0:
         w[:, cols] *= np.float32(spec.w_outlier_mult)
     return w
@@ -120,13 +174,25 @@ def _weights(spec: MatrixSpec, seed: int, cols: np.ndarray) -> np.ndarray:
 
 def _inputs(spec: MatrixSpec, seed: int, cols: np.ndarray) -> np.ndarray:
     if spec.x_dist == "normal":
-        x = rng(seed, TAG_X, spec.x_stream).standard_normal((spec.T, spec.C), dtype=np.float32)
+        x = _fill((spec.T, spec.C), seed, TAG_X, spec.x_stream, _normal())
     else:
-        a = rng(seed, TAG_SILU_A, spec.x_stream).standard_normal((spec.T, spec.C), dtype=np.float32)
-        b = rng(seed, TAG_SILU_B, spec.x_stream).standard_normal((spec.T, spec.C), dtype=np.float32)
+        a = _fill((spec.T, spec.C), seed, TAG_SILU_A, spec.x_stream, _normal())
+        b = _fill((spec.T, spec.C), seed, TAG_SILU_B, spec.x_stream, _normal())
         x = (a / (np.float32(1.0) + np.exp(-a)) * b).astype(np.float32)
     if cols.size and spec.x_outlier_mult != 1.0:
         x[:, cols] *= np.float32(spec.x_outlier_mult)
+    return x
+
+
+def _round_bf16_inplace(x: np.ndarray) -> np.ndarray:
+    """round_to_bf16 applied chunk by chunk in the thread pool."""
+    flat = x.reshape(-1)
+
+    def one(i0):
+        c = flat[i0:i0 + CHUNK]
+        c[...] = round_to_bf16(c)
+
+    list(_pool().map(one, range(0, flat.size, CHUNK)))
     return x
 
 
@@ -137,13 +203,12 @@ def make_matrix(spec: MatrixSpec, seed: int = 0) -> Matrix:
     w = _weights(spec, seed, cols if spec.w_outlier_frac > 0 else np.zeros(0, np.int64))
     x = _inputs(spec, seed, cols if spec.x_outlier_frac > 0 else np.zeros(0, np.int64))
     if spec.s_std > 0:
-        s = (np.float32(1.0) + rng(seed, TAG_S, _name_tag(spec.name))
-             .standard_normal((spec.R, spec.C), dtype=np.float32) * np.float32(spec.s_std)).astype(np.float32)
+        s = _fill((spec.R, spec.C), seed, TAG_S, _name_tag(spec.name), _normal(spec.s_std, 1.0))
     else:
         s = np.ones((spec.R, spec.C), np.float32)
     if spec.dtype == "bf16":
-        w = round_to_bf16(w)
-        x = round_to_bf16(x)
+        w = _round_bf16_inplace(w)
+        x = _round_bf16_inplace(x)
     return Matrix(spec.name, spec.R, spec.C, spec.T, spec.dtype, w, x, s, cols)
 
 

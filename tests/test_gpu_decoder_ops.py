@@ -218,6 +218,58 @@ def test_gemm_nt_batched_causal(L, N, batch):
         assert np.array_equal(host(O1), host(O0)), mode
 
 
+def _bf16_dev(rs, shape, tri=None):
+    a = bfr(rs.standard_normal(shape))
+    if tri is not None:
+        a = tri(a)
+    return a, torch.from_numpy(a.astype(F32)).to("cuda").to(torch.bfloat16)
+
+
+def test_gemm_pp_scores_causal_vs_fp64():
+    """The attention's score products at the 7B block's sequence length on
+    the shapes that select the ping-pong kernel (256 x 256 tiles: L = 2048,
+    4 batches): mode 0 against an fp64 product for every batch, mode 1 against
+    the same reference on every entry j <= i."""
+    L, d, batch = 2048, 128, 4
+    rs = np.random.default_rng(2048 + 4)
+    Q, dQ = _bf16_dev(rs, (batch, L, d))
+    Kk, dK = _bf16_dev(rs, (batch, L, d))
+    S0 = torch.zeros(batch, L, L, device="cuda")
+    S1 = torch.full((batch, L, L), 7.0, device="cuda")
+    uq.uniquan_gemm_nt_batched(L, L, d, batch, dQ, L * d, dK, L * d, S0, L * L, 0.125, 0)
+    uq.uniquan_gemm_nt_batched(L, L, d, batch, dQ, L * d, dK, L * d, S1, L * L, 0.125, 1)
+    torch.cuda.synchronize()
+    g0, g1 = host(S0), host(S1)
+    low = np.tril(np.ones((L, L), dtype=bool))
+    for b in range(batch):
+        ref = 0.125 * Q[b] @ Kk[b].T
+        mag = 0.125 * np.abs(Q[b]) @ np.abs(Kk[b]).T
+        assert np.all(np.abs(g0[b] - ref) <= 1e-5 * mag), b
+        assert np.all(np.abs(g1[b][low] - ref[low]) <= 1e-5 * mag[low]), b
+
+
+@pytest.mark.parametrize("mode,tri", [(2, np.tril), (3, np.triu)])
+def test_gemm_pp_triangular_vs_fp64(mode, tri):
+    """P V and its transposed counterpart at L = 2048, d = 128 with 32 batches
+    (256 x 128 tiles, 64-deep stages of the ping-pong kernel): modes 0 and 2 / 3
+    against an fp64 product for every batch."""
+    L, N, batch = 2048, 128, 32
+    rs = np.random.default_rng(2048 + mode)
+    A, dA = _bf16_dev(rs, (batch, L, L), tri)
+    B, dB = _bf16_dev(rs, (batch, N, L))
+    O0 = torch.zeros(batch, L, N, device="cuda")
+    O1 = torch.full((batch, L, N), 7.0, device="cuda")
+    uq.uniquan_gemm_nt_batched(L, N, L, batch, dA, L * L, dB, N * L, O0, L * N, 1.0, 0)
+    uq.uniquan_gemm_nt_batched(L, N, L, batch, dA, L * L, dB, N * L, O1, L * N, 1.0, mode)
+    torch.cuda.synchronize()
+    g0, g1 = host(O0), host(O1)
+    for b in range(batch):
+        ref = A[b] @ B[b].T
+        mag = np.abs(A[b]) @ np.abs(B[b]).T
+        assert np.all(np.abs(g0[b] - ref) <= 1e-5 * mag + 1e-30), (mode, b)
+        assert np.all(np.abs(g1[b] - ref) <= 1e-5 * mag + 1e-30), (mode, b)
+
+
 @pytest.mark.parametrize("n_seq,L,H,G,nsum", [(2, 8, 4, 2, 2), (2, 64, 8, 4, 4)])
 def test_rope_grouped_slots_and_partial_sums(n_seq, L, H, G, nsum):
     """Grouped slot order (head h at (h mod G) (H / G) + h / G) and the merge

@@ -142,10 +142,30 @@ def test_fwd_local_and_frozen(k):
     check_fwd(m.W, s1, p1, k, g, uq.MAP_LOCAL, prev)
 
 
+@pytest.mark.parametrize("g", [8, 16, 32, 64, 256, 512])
+@pytest.mark.parametrize("k", [1, 2, 5, 6, 7])
+def test_fwd_local_frozen_group_sizes(g, k):
+    """LOCAL and FROZEN over every supported group size and the bit widths the
+    other tests leave out.  g = 8, k = 7 is the one shape whose neighbour table
+    does not fit (64 groups x 128 levels per wavefront), so LOCAL runs the
+    search variant there."""
+    m = small_matrix(9, 1536, 30 + g + k)
+    p = params(m.W, m.s, k, g, "B")
+    f0 = O.fq_fwd(m.W, m.s, p["alpha"], p["z_b"], k, g, p["s_r"], p["delta"], p["z_u"])
+    p1 = dict(p)
+    p1["alpha"] = synth.perturb(p["alpha"], 0.05, g, 5)
+    s1 = synth.perturb(m.s, 0.05, k, 6)
+    for mode in (uq.MAP_LOCAL, uq.MAP_FROZEN):
+        check_fwd(m.W, s1, p1, k, g, mode, f0["codes"])
+    prev = synth.random_codes(9, 1536, k, g + k)
+    check_fwd(m.W, s1, p1, k, g, uq.MAP_LOCAL, prev)
+    check_fwd(m.W, s1, p1, k, g, uq.MAP_FROZEN, prev)
+
+
 @pytest.mark.parametrize("k", [3, 4])
-def test_fwd_four_chunks_ragged(k):
-    """>= 4M weights: four 8-weight chunks per lane, 8192-weight tiles, the
-    last tile holding a single row."""
+def test_fwd_multi_workgroup_ragged(k):
+    """1031 x 4096 weights: 8249 wavefronts of 512 weights over 2063
+    workgroups of four, the last workgroup holding a single wavefront."""
     m = small_matrix(1031, 4096, 10)
     g = 128
     p = params(m.W, m.s, k, g, "A")
@@ -178,6 +198,44 @@ def test_fwd_adversarial():
     ref, codes = check_fwd(W, s, p, k, g, wdt=torch.float32)
     # midpoints of the integer grid go to the lower level (code = level value)
     assert np.array_equal(codes[2, :8] & 0x7F, np.arange(8))
+    # LOCAL and FROZEN on the same values, the previous code of weight j of a
+    # group being the level at sorted position j mod 2^k: every position of
+    # every group (ends, duplicates, zero scales) is a starting point
+    _, code_of, _ = O.sort_levels(O.levels_f32(alpha, z_b))
+    L = 1 << k
+    prev = code_of[:, np.arange(g) % L].astype(np.uint8).reshape(R, C)
+    for mode in (uq.MAP_LOCAL, uq.MAP_FROZEN):
+        check_fwd(W, s, p, k, g, mode, prev, wdt=torch.float32)
+    # and with the positions reversed (each weight starts from the far end)
+    prev_r = code_of[:, (L - 1 - np.arange(g) % L)].astype(np.uint8).reshape(R, C)
+    check_fwd(W, s, p, k, g, uq.MAP_LOCAL, prev_r, wdt=torch.float32)
+
+
+@pytest.mark.parametrize("k,g", [(3, 8), (7, 8), (4, 16)])
+def test_fwd_local_two_level_jump(k, g):
+    """A weight that moved two or more sorted positions since the last full
+    mapping: LOCAL stops one level short of it, FULL reaches it (the local
+    mapping's defining limit), on the uniform level grid 0 .. 2^k - 1."""
+    L = 1 << k
+    R, C = 4, 64
+    Gn = R * C // g
+    alpha = np.tile((2.0 ** (np.arange(k) - 1)).astype(F32), (Gn, 1))
+    z_b = np.full(Gn, (L - 1) / 2, F32)
+    rs = np.random.default_rng(k * g)
+    prev_level = rs.integers(0, L, (R, C))
+    jump = rs.choice(np.array([-3, -2, 2, 3]), (R, C))
+    target = np.clip(prev_level + jump, 0, L - 1)
+    W = (target + rs.uniform(-0.3, 0.3, (R, C))).astype(F32)
+    s = np.ones((R, C), F32)
+    p = dict(alpha=alpha, z_b=z_b, s_r=np.ones(R, F32), delta=np.ones(Gn, F32), z_u=np.zeros(Gn, F32))
+    prev = prev_level.astype(np.uint8)  # level b has code b on this grid
+    _, loc = check_fwd(W, s, p, k, g, uq.MAP_LOCAL, prev, wdt=torch.float32)
+    _, full = check_fwd(W, s, p, k, g, uq.MAP_FULL, None, wdt=torch.float32)
+    step = np.sign(target - prev_level)
+    moved = target != prev_level
+    assert np.array_equal((loc & 0x7F)[moved], (prev_level + step)[moved])
+    assert np.array_equal(full & 0x7F, target.astype(np.uint8))
+    assert (np.abs(target - prev_level) >= 2).sum() > R * C // 2
 
 
 def test_fwd_uq_special_case_equals_rounding():
