@@ -244,6 +244,27 @@ uq_status uniquan_layer_recon(int64_t T, int64_t R, int64_t C,
                               void* stream);
 
 /*
+ * uniquan_layer_recon_noalloc -- uniquan_layer_recon for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): no partials workspace argument; the
+ * loss partials live in a fixed array of the library's device memory, one
+ * per GPU, held until the process ends.  Nothing is allocated or freed by
+ * the call.  Same arguments (minus partials_ws, partials_len), kernels,
+ * results and errors as uniquan_layer_recon, plus UQ_EUNSUPPORTED when the
+ * shape needs more than uniquan_recon_noalloc_max_partials() partials
+ * (uniquan_recon_ws(T, R, C) > 65536, i.e. R * T beyond about 2^30).
+ * Calls that overlap on one GPU (concurrent streams or threads) share the
+ * array and race; calls ordered on one stream do not.
+ */
+uq_status uniquan_layer_recon_noalloc(int64_t T, int64_t R, int64_t C,
+                                      const uint16_t* X, const uint16_t* Xt,
+                                      const uint16_t* W_hat, const float* Yt,
+                                      float* loss, uint16_t* Et,
+                                      void* grad_W_hat, int grad_dtype,
+                                      void* stream);
+size_t uniquan_recon_noalloc_max_partials(void);
+
+/*
  * uniquan_layer_grad -- the weight-gradient half of uniquan_layer_recon on
  * its own: grad_W_hat = 2 Et Xt^T, grad[r, c] = 2 sum_t Et[r, t] X[t, c]
  * (bf16 MFMA, fp32 accumulation).  For callers that run the forward with

@@ -187,6 +187,35 @@ uq_status uniquan_layer_recon(int64_t T, int64_t R, int64_t C, const uint16_t* X
   return hip_status(fn, uq::launch_gemm(b, st));
 }
 
+uq_status uniquan_layer_recon_noalloc(int64_t T, int64_t R, int64_t C, const uint16_t* X, const uint16_t* Xt,
+                                      const uint16_t* W_hat, const float* Yt, float* loss, uint16_t* Et,
+                                      void* grad_W_hat, int grad_dtype, void* stream) {
+  const char* fn = "uniquan_layer_recon_noalloc";
+  if (uq_status st = check_gemm_dims(fn, T, R, C)) return st;
+  REQ_PTR(X, 16); REQ_PTR(W_hat, 16); OPT_PTR(Yt, 16); REQ_PTR(loss, 4); REQ_PTR(Et, 16);
+  if (grad_W_hat != nullptr) {
+    REQ_PTR(Xt, 16);
+    REQ_PTR(grad_W_hat, 16);
+    if (!is_dtype(grad_dtype)) return fail(UQ_EINVAL, "%s: bad dtype", fn);
+  }
+  const size_t need = uniquan_recon_ws(T, R, C);
+  if (need > uq::kNoallocPartials)
+    return fail(UQ_EUNSUPPORTED, "%s: T=%lld, R=%lld need %zu loss partials; the fixed scratch holds %zu", fn,
+                (long long)T, (long long)R, need, uq::kNoallocPartials);
+  float* partials = nullptr;
+  if (uq_status s = hip_status(fn, uq::noalloc_scratch(&partials))) return s;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  uq::GemmLaunch f{W_hat, X, R, T, C, uq::EPI_LOSS, Yt, Et, partials, 1.0f};
+  if (uq_status s = hip_status(fn, uq::launch_gemm(f, st))) return s;
+  if (uq_status s = hip_status(fn, uq::launch_reduce_loss(partials, int64_t(need), loss, st))) return s;
+  if (grad_W_hat == nullptr) return UQ_OK;
+  uq::GemmLaunch b{Et, Xt, R, C, T, grad_dtype == UQ_BF16 ? uq::EPI_GRAD_BF16 : uq::EPI_GRAD_F32,
+                   nullptr, grad_W_hat, nullptr, 2.0f};
+  return hip_status(fn, uq::launch_gemm(b, st));
+}
+
+size_t uniquan_recon_noalloc_max_partials(void) { return uq::kNoallocPartials; }
+
 uq_status uniquan_layer_grad(int64_t T, int64_t R, int64_t C, const uint16_t* Et, const uint16_t* Xt,
                              void* grad_W_hat, int grad_dtype, void* stream) {
   const char* fn = "uniquan_layer_grad";

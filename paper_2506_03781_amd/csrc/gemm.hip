@@ -27,6 +27,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "uq_launch.h"
 
 namespace uq {
@@ -909,6 +911,35 @@ __global__ __launch_bounds__(256) void reduce_loss_kernel(const float* __restric
 hipError_t launch_reduce_loss(const float* partials, int64_t n, float* loss, hipStream_t st) {
   hipLaunchKernelGGL(reduce_loss_kernel, dim3(1), dim3(256), 0, st, partials, n, loss);
   return hipGetLastError();
+}
+
+// Loss partials of uniquan_layer_recon_noalloc: a fixed array in device
+// memory (one copy per GPU, for the life of the process) instead of a
+// caller-provided workspace.  Host code never passes `scratch` itself to a
+// kernel: its device address on the current GPU is looked up once per device
+// with hipGetSymbolAddress and kept.  Every workgroup of the loss GEMM writes
+// its own partial and the reduction reads exactly those, so nothing needs
+// clearing between calls; calls that overlap on one GPU share the array and
+// race.
+static __device__ __align__(256) float scratch[kNoallocPartials];
+
+hipError_t noalloc_scratch(float** out) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static float* ptrs[kMaxDevices] = {};
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (ptrs[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    ptrs[dev] = static_cast<float*>(p);
+  }
+  *out = ptrs[dev];
+  return hipSuccess;
 }
 
 // out[c, r] = in[r, c]; 64 x 64 tiles through LDS (padded against conflicts).

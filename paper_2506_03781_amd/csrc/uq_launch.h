@@ -129,6 +129,10 @@ hipError_t launch_gemm(const GemmLaunch& p, hipStream_t st);
 hipError_t launch_gemm_ste(const GemmLaunch& p, int k, hipStream_t st);
 size_t gemm_workgroups(int64_t M, int64_t N, int epi);
 hipError_t launch_reduce_loss(const float* partials, int64_t n, float* loss, hipStream_t st);
+// Fixed device array (per GPU) of kNoallocPartials loss partials for
+// uniquan_layer_recon_noalloc; *out receives its address on the current GPU.
+constexpr size_t kNoallocPartials = size_t(1) << 16;
+hipError_t noalloc_scratch(float** out);
 hipError_t launch_transpose(int64_t rows, int64_t cols, const uint16_t* in, uint16_t* out, hipStream_t st);
 hipError_t launch_sgd(int64_t n, float* theta, const float* grad, float lr, hipStream_t st);
 hipError_t launch_bcq_pack(const BcqPackLaunch& p, hipStream_t st);

@@ -47,6 +47,8 @@ _SIGS = {
     "uniquan_transpose_bf16": ([_i64, _i64, _vp, _vp, _vp], _i32),
     "uniquan_recon_ws": ([_i64, _i64, _i64], ctypes.c_size_t),
     "uniquan_layer_recon": ([_i64, _i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp, _i32, _vp], _i32),
+    "uniquan_layer_recon_noalloc": ([_i64, _i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp], _i32),
+    "uniquan_recon_noalloc_max_partials": ([], ctypes.c_size_t),
     "uniquan_layer_grad": ([_i64, _i64, _i64, _vp, _vp, _vp, _i32, _vp], _i32),
     "uniquan_layer_grad_ste_sgd": ([_i64, _i64, _i64, _i32, _i32, _vp, _vp, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp,
                                     _vp, _f32, _f32, _vp, _vp, _vp, _vp], _i32),
@@ -285,6 +287,15 @@ def uniquan_layer_recon(T, R, C, X, Xt, W_hat, Yt, loss, Et_ws, partials_ws, gra
         _dt(grad_W_hat) if grad_W_hat is not None else UQ_BF16, _stream(stream)))
 
 
+def uniquan_layer_recon_noalloc(T, R, C, X, Xt, W_hat, Yt, loss, Et, grad_W_hat=None, stream=None):
+    """uniquan_layer_recon with the loss partials in the library's fixed scratch."""
+    _check(lib().uniquan_layer_recon_noalloc(
+        T, R, C, _p(X, T * C, _B, "X"), _p(Xt, T * C, _B, "Xt"), _p(W_hat, R * C, _B, "W_hat"),
+        _p(Yt, R * T, _F, "Yt"), _p(loss, 1, _F, "loss"), _p(Et, R * T, _B, "Et"),
+        _p(grad_W_hat, R * C, _W, "grad_W_hat"),
+        _dt(grad_W_hat) if grad_W_hat is not None else UQ_BF16, _stream(stream)))
+
+
 def uniquan_layer_grad(T, R, C, Et, Xt, grad_W_hat, stream=None):
     _check(lib().uniquan_layer_grad(T, R, C, _p(Et, R * T, _B, "Et"), _p(Xt, T * C, _B, "Xt"),
                                     _p(grad_W_hat, R * C, _W, "grad_W_hat"), _dt(grad_W_hat), _stream(stream)))
@@ -468,3 +479,7 @@ def uniquan_probe_stream(op, n_bytes, src, dst, sink, stream=None):
 
 def uniquan_probe_mfma(iters, sink, stream=None):
     _check(lib().uniquan_probe_mfma(int(iters), _p(sink, uniquan_probe_sink_len(), None, "sink"), _stream(stream)))
+
+
+def uniquan_recon_noalloc_max_partials() -> int:
+    return int(lib().uniquan_recon_noalloc_max_partials())

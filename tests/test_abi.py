@@ -226,7 +226,7 @@ def test_recorder_classifies_launches(L):
     assert "uniquan_fq_fwd" in launches and "uniquan_gemm_nt" in launches and "uniquan_bcq_matmul" in launches
     others = {n for n in uq._SIGS if n not in launches}
     assert others == ({"uniquan_abi_version", "uniquan_last_error", "uniquan_probe_sink_len",
-                       "uniquan_probe_mfma_flops"} | {n for n in uq._SIGS if n.endswith("_ws")})
+                       "uniquan_probe_mfma_flops", "uniquan_recon_noalloc_max_partials"} | {n for n in uq._SIGS if n.endswith("_ws")})
 
 
 def test_replay_raises_on_error_status(L):
