@@ -599,21 +599,22 @@ uq_status uniquan_sgd(int64_t n, float* theta, const float* grad, float lr, void
 /*
  * Measurement probes (not part of the method): the streaming HBM rates and
  * the bf16 MFMA issue rate this GPU reaches, reported next to the nominal
- * peaks.  sink [uniquan_probe_sink_len()] uint32/fp32 receives one word per
- * lane (so that nothing is optimised away); its contents are meaningless.
+ * peaks.  sink: 16 bytes of device memory (16-byte aligned) that a probe
+ * writes only when its result equals a value the data cannot produce, so
+ * that nothing is optimised away; its contents are meaningless.
  *
  * uniquan_probe_stream -- op 0 reads n_bytes of src, op 1 writes n_bytes of
  * dst, op 2 copies n_bytes from src to dst; 16-byte nontemporal accesses in a
- * grid-stride loop.  n_bytes a positive multiple of 16; src, dst 16-byte
- * aligned device memory (the unused one may be NULL).
+ * grid-stride loop over `blocks` workgroups of 256 lanes (1 .. 2^20).
+ * n_bytes a positive multiple of 16; src, dst 16-byte aligned device memory
+ * (the unused one may be NULL).
  * uniquan_probe_mfma -- iters rounds of independent v_mfma_f32_32x32x16_bf16
  * chains on register operands over the whole GPU; the work done is
  * uniquan_probe_mfma_flops(iters) floating-point operations.
  */
-size_t uniquan_probe_sink_len(void);
 double uniquan_probe_mfma_flops(int iters);
 uq_status uniquan_probe_stream(int op, int64_t n_bytes, const void* src, void* dst,
-                               uint32_t* sink, void* stream);
+                               void* sink, int blocks, void* stream);
 uq_status uniquan_probe_mfma(int iters, float* sink, void* stream);
 
 #ifdef __cplusplus

@@ -522,29 +522,27 @@ uq_status uniquan_sgd(int64_t n, float* theta, const float* grad, float lr, void
   return hip_status(fn, uq::launch_sgd(n, theta, grad, lr, static_cast<hipStream_t>(stream)));
 }
 
-size_t uniquan_probe_sink_len(void) {
-  const size_t a = size_t(uq::PROBE_BLOCKS) * 256, b = size_t(uq::PROBE_MFMA_BLOCKS) * 256;
-  return a > b ? a : b;
-}
-
 double uniquan_probe_mfma_flops(int iters) {
   return 2.0 * 32 * 32 * 16 * double(uq::PROBE_MFMA_CHAINS) * double(iters) * (4.0 * uq::PROBE_MFMA_BLOCKS);
 }
 
-uq_status uniquan_probe_stream(int op, int64_t n_bytes, const void* src, void* dst, uint32_t* sink, void* stream) {
+uq_status uniquan_probe_stream(int op, int64_t n_bytes, const void* src, void* dst, void* sink, int blocks,
+                               void* stream) {
   const char* fn = "uniquan_probe_stream";
   if (op < 0 || op > 2) return fail(UQ_EINVAL, "%s: op=%d must be 0 (read), 1 (write) or 2 (copy)", fn, op);
   if (n_bytes < 16 || n_bytes % 16 != 0) return fail(UQ_EINVAL, "%s: n_bytes must be a positive multiple of 16", fn);
+  if (blocks < 1 || blocks > (1 << 20)) return fail(UQ_EINVAL, "%s: blocks=%d must be in [1, 2^20]", fn, blocks);
   if (op != 1) REQ_PTR(src, 16);
   if (op != 0) REQ_PTR(dst, 16);
-  REQ_PTR(sink, 4);
-  return hip_status(fn, uq::launch_probe_stream(op, n_bytes / 16, src, dst, sink, static_cast<hipStream_t>(stream)));
+  REQ_PTR(sink, 16);
+  return hip_status(fn, uq::launch_probe_stream(op, n_bytes / 16, src, dst, sink, blocks,
+                                                static_cast<hipStream_t>(stream)));
 }
 
 uq_status uniquan_probe_mfma(int iters, float* sink, void* stream) {
   const char* fn = "uniquan_probe_mfma";
   if (iters < 1 || iters > (1 << 24)) return fail(UQ_EINVAL, "%s: iters=%d must be in [1, 2^24]", fn, iters);
-  REQ_PTR(sink, 4);
+  REQ_PTR(sink, 16);
   return hip_status(fn, uq::launch_probe_mfma(iters, reinterpret_cast<float*>(sink), static_cast<hipStream_t>(stream)));
 }
 

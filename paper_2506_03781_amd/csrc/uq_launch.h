@@ -158,12 +158,12 @@ hipError_t launch_silu_mul_bwd(int64_t n, const uint16_t* dH, const uint16_t* G,
 hipError_t launch_bcq_matmul(const BcqMatmulLaunch& p, hipStream_t st);
 int64_t bcq_slabs(int64_t R, int64_t C);
 
-// Ceiling probes (probe.hip): PROBE_BLOCKS x 256 lanes stream; the MFMA probe
-// runs PROBE_MFMA_BLOCKS x 4 wavefronts of PROBE_MFMA_CHAINS chains.
-constexpr int PROBE_BLOCKS = 4096;
+// Ceiling probes (probe.hip): the MFMA probe runs PROBE_MFMA_BLOCKS x 4
+// wavefronts of PROBE_MFMA_CHAINS chains.
 constexpr int PROBE_MFMA_BLOCKS = 1024;
 constexpr int PROBE_MFMA_CHAINS = 8;
-hipError_t launch_probe_stream(int op, int64_t n16, const void* src, void* dst, uint32_t* sink, hipStream_t st);
+hipError_t launch_probe_stream(int op, int64_t n16, const void* src, void* dst, void* sink, int blocks,
+                               hipStream_t st);
 hipError_t launch_probe_mfma(int iters, float* sink, hipStream_t st);
 
 }  // namespace uq

@@ -73,9 +73,8 @@ _SIGS = {
     "uniquan_transpose_bf16_batched": ([_i64, _i64, _i64, _vp, _vp, _vp], _i32),
     "uniquan_block_loss_ws": ([], ctypes.c_size_t),
     "uniquan_block_loss": ([_i64, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp, _vp], _i32),
-    "uniquan_probe_sink_len": ([], ctypes.c_size_t),
     "uniquan_probe_mfma_flops": ([_i32], ctypes.c_double),
-    "uniquan_probe_stream": ([_i32, _i64, _vp, _vp, _vp, _vp], _i32),
+    "uniquan_probe_stream": ([_i32, _i64, _vp, _vp, _vp, _i32, _vp], _i32),
     "uniquan_probe_mfma": ([_i32, _vp, _vp], _i32),
     "uniquan_bcq_matmul_ws": ([_i32, _i64, _i64], ctypes.c_size_t),
     "uniquan_bcq_matmul": ([_i32, _i64, _i64, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp],
@@ -460,25 +459,21 @@ def uniquan_block_loss(n, R, M, Yref, E, partials, loss, stream=None):
                                     _p(loss, 1, _F, "loss"), _stream(stream)))
 
 
-def uniquan_probe_sink_len() -> int:
-    return int(lib().uniquan_probe_sink_len())
-
-
 def uniquan_probe_mfma_flops(iters) -> float:
     return float(lib().uniquan_probe_mfma_flops(int(iters)))
 
 
-def uniquan_probe_stream(op, n_bytes, src, dst, sink, stream=None):
+def uniquan_probe_stream(op, n_bytes, src, dst, sink, blocks=8192, stream=None):
     """Ceiling probe: op 0 reads src, 1 writes dst, 2 copies src -> dst (n_bytes each)."""
     for t, used, name in ((src, op != 1, "src"), (dst, op != 0, "dst")):
         if used and (t is None or t.numel() * t.element_size() < n_bytes):
             raise ValueError(f"{name} must hold {n_bytes} bytes")
     _check(lib().uniquan_probe_stream(int(op), int(n_bytes), _p(src, None, None, "src"), _p(dst, None, None, "dst"),
-                                      _p(sink, uniquan_probe_sink_len(), None, "sink"), _stream(stream)))
+                                      _p(sink, 4, _F, "sink"), int(blocks), _stream(stream)))
 
 
 def uniquan_probe_mfma(iters, sink, stream=None):
-    _check(lib().uniquan_probe_mfma(int(iters), _p(sink, uniquan_probe_sink_len(), None, "sink"), _stream(stream)))
+    _check(lib().uniquan_probe_mfma(int(iters), _p(sink, 4, _F, "sink"), _stream(stream)))
 
 
 def uniquan_recon_noalloc_max_partials() -> int:

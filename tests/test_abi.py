@@ -225,8 +225,7 @@ def test_recorder_classifies_launches(L):
     launches = {n for n in uq._SIGS if uq._is_launch(n)}
     assert "uniquan_fq_fwd" in launches and "uniquan_gemm_nt" in launches and "uniquan_bcq_matmul" in launches
     others = {n for n in uq._SIGS if n not in launches}
-    assert others == ({"uniquan_abi_version", "uniquan_last_error", "uniquan_probe_sink_len",
-                       "uniquan_probe_mfma_flops", "uniquan_recon_noalloc_max_partials"} | {n for n in uq._SIGS if n.endswith("_ws")})
+    assert others == ({"uniquan_abi_version", "uniquan_last_error", "uniquan_probe_mfma_flops", "uniquan_recon_noalloc_max_partials"} | {n for n in uq._SIGS if n.endswith("_ws")})
 
 
 def test_replay_raises_on_error_status(L):
@@ -245,12 +244,12 @@ def test_record_propagates_and_resets(L):
 
 
 def test_probe_entry_validation(L):
-    assert L.uniquan_probe_sink_len() >= 4096 * 256
     assert L.uniquan_probe_mfma_flops(10) == 2.0 * 32 * 32 * 16 * 8 * 10 * 4096
-    assert L.uniquan_probe_stream(3, 64, FAKE, FAKE, FAKE, None) == uq.UQ_EINVAL
-    assert L.uniquan_probe_stream(0, 24, FAKE, None, FAKE, None) == uq.UQ_EINVAL
-    assert L.uniquan_probe_stream(0, 64, None, None, FAKE, None) == uq.UQ_EINVAL
-    assert L.uniquan_probe_stream(1, 64, None, None, FAKE, None) == uq.UQ_EINVAL
+    assert L.uniquan_probe_stream(3, 64, FAKE, FAKE, FAKE, 64, None) == uq.UQ_EINVAL
+    assert L.uniquan_probe_stream(0, 24, FAKE, None, FAKE, 64, None) == uq.UQ_EINVAL
+    assert L.uniquan_probe_stream(0, 64, None, None, FAKE, 64, None) == uq.UQ_EINVAL
+    assert L.uniquan_probe_stream(1, 64, None, None, FAKE, 64, None) == uq.UQ_EINVAL
+    assert L.uniquan_probe_stream(2, 64, FAKE, FAKE, FAKE, 0, None) == uq.UQ_EINVAL
     assert L.uniquan_probe_mfma(0, FAKE, None) == uq.UQ_EINVAL
 
 
