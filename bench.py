@@ -115,7 +115,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--workload", default="mlp70b")
-    ap.add_argument("--sub-workloads", default="attn4096,mlp7b,block7b",
+    ap.add_argument("--sub-workloads", default="attn4096,mlp7b,block7b,mlp7b_rows",
                     help="comma-separated workloads reported as sub-records ('' for none)")
     ap.add_argument("--sub-steps", type=int, default=20, help="timed steps of each sub-record")
     ap.add_argument("--block7b-steps", type=int, default=100,
@@ -358,6 +358,139 @@ def ceilings(n_bytes=1 << 30, reps=3, grids=(2048, 8192, 32768)):
     return out
 
 
+def bcq_inference(layers, batches=(1, 8), target_bytes=512 << 20):
+    """The deployed layer after the timed steps: fold (Theorem 1) -> stored
+    form -> Y = X What^T for a batch of T activation rows.  Copies of the
+    stored form are rotated so that the bytes touched between two reads of one
+    copy exceed the 256 MB last-level cache (cold-cache decode, as one token's
+    pass over a model reads each layer once)."""
+    import torch
+
+    from paper_2506_03781_amd import uniquan as uq
+    res = []
+    for lay in layers:
+        R, C, k, g = lay.R, lay.C, lay.k, lay.g
+        if C % 128 or g % 128 or k > 4:
+            continue
+        a, z, c = lay.fold()
+        Gn = R * C // g
+        per_copy = R * C * k // 8 + 2 * (k + 1) * Gn
+        n_copy = int(min(64, max(2, -(-target_bytes // per_copy))))
+        copies = []
+        for _ in range(n_copy):
+            st = (torch.empty(R * C * k // 32, dtype=torch.int32, device="cuda"),
+                  torch.empty(Gn * k, dtype=torch.float16, device="cuda"),
+                  torch.empty(Gn, dtype=torch.float16, device="cuda"))
+            uq.uniquan_bcq_pack(R, C, k, g, c, a, z, *st)
+            copies.append(st)
+        for T in batches:
+            X = lay.X[:T].contiguous()
+            Y = torch.empty(T, R, device="cuda")
+            ws = torch.empty(max(1, uq.uniquan_bcq_matmul_ws(T, R, C)), device="cuda")
+            for i in range(3):
+                uq.uniquan_bcq_matmul(T, R, C, k, g, X, *copies[i % n_copy], Y, ws)
+            n_it = max(20, 2 * n_copy)
+            e0, e1 = TimingEvent(), TimingEvent()
+            e0.record()
+            for i in range(n_it):
+                uq.uniquan_bcq_matmul(T, R, C, k, g, X, *copies[i % n_copy], Y, ws)
+            e1.record()
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) / n_it * 1e3
+            byt = per_copy + 2 * T * C + 4 * T * R
+            gbs = byt / (us * 1e-6) / 1e9
+            res.append({"R": R, "C": C, "k": k, "g": g, "T": T, "us_per_call": us, "algorithmic_bytes": byt,
+                        "achieved_gbs": gbs, "frac_hbm": gbs / HBM_PEAK_GBS, "copies_rotated": n_copy})
+        del copies
+    return res
+
+
+def block_decoder(seed, k=3, steps=5, warmup=2, n_kv=None):
+    """Block-level reconstruction of a 7B decoder block (Algorithm 1 with f =
+    one rotary causal attention module and one SiLU-gated MLP module): per
+    step the seven fake-quant forwards, the block's forward on What, the
+    loss, backpropagation to all seven matrices and the straight-through
+    backward with the SGD update.  8192 tokens as 4 sequences of 2048,
+    C = 4096 in 32 heads of 128, I = 11008; n_kv key/value heads (32 by
+    default; 8 gives the grouped-query form with k, v of [1024, 4096])."""
+    import numpy as np
+    import torch
+
+    from paper_2506_03781_amd import synth
+    from paper_2506_03781_amd import uniquan as uq
+    from paper_2506_03781_amd.block import DecoderBlock, QuantMatrix
+    wl = synth.WORKLOADS["block7b"]
+    g = wl.group_size
+    n_seq, H = 4, 32
+    n_kv = H if n_kv is None else n_kv
+    mats, X = {}, None
+    for name, spec in zip(DecoderBlock.NAMES, wl.matrices):
+        # only the first matrix's activations are used; the weights do not depend on T
+        sc = synth.scaled(spec, T=8) if X is not None else spec
+        if name in ("k", "v"):
+            sc = synth.scaled(sc, R=spec.R * n_kv // H)
+        m = synth.make_matrix(sc, seed)
+        if X is None:
+            X = m.X
+        q = QuantMatrix(m.W, m.s, k, g)
+        q.init_unified()
+        mats[name] = q
+        del m
+    rs = np.random.default_rng(seed + 1000)
+    C = mats["q"].C
+    g1 = (1.0 + 0.1 * rs.standard_normal(C)).astype(np.float32)
+    g2 = (1.0 + 0.1 * rs.standard_normal(C)).astype(np.float32)
+    blk = DecoderBlock(mats, g1, g2, X.shape[0], n_seq, H, n_kv=n_kv)
+    blk.prepare(X)
+    blk.set_input(X)
+    # SGD on L / L0 (one step with zero learning rates measures L0)
+    blk.step(uq.MAP_FULL, 0.0, 0.0)
+    l0 = float(blk.loss.item())
+    lr_f, lr_b = 0.005 / l0, 0.0005 / l0
+    rel = []
+    for i in range(warmup):
+        blk.step(uq.MAP_FULL if i == 0 else uq.MAP_LOCAL, lr_f, lr_b)
+        rel.append(float(blk.loss.item()) / l0)
+    step_local = uq.record(blk.step, uq.MAP_LOCAL, lr_f, lr_b)
+    torch.cuda.synchronize()
+    e0, e1 = TimingEvent(), TimingEvent()
+    e0.record()
+    for _ in range(steps):
+        step_local()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    # one instrumented step for the split between phases
+    ev = [TimingEvent() for _ in range(6)]
+    ev[0].record()
+    blk.quantize(uq.MAP_LOCAL)
+    ev[1].record()
+    blk.forward()
+    ev[2].record()
+    blk.compute_loss()
+    ev[3].record()
+    blk.backward()
+    ev[4].record()
+    blk.update(lr_f, lr_b)
+    ev[5].record()
+    torch.cuda.synchronize()
+    phases = dict(zip(("fq_fwd", "forward", "loss", "backward", "ste_sgd"),
+                      (ev[i].elapsed_time(ev[i + 1]) for i in range(5))))
+    flops = blk.flops_per_step()
+    tf = flops / (ms * 1e-3) / 1e12
+    n_w = sum(q.R * q.C for q in mats.values())
+    last = float(blk.loss.item()) / l0
+    return {"T": blk.T, "C": blk.C, "I": blk.I, "heads": H, "kv_heads": n_kv, "seq_len": blk.L, "n_seq": n_seq, "k": k, "g": g,
+            "steps": steps, "ms_per_step": ms, "gweights_per_s": n_w / (ms * 1e-3) / 1e9,
+            "gemm_flops_per_step": flops, "tflops_effective": tf, "frac_mfma": tf / MFMA_BF16_PEAK_TFLOPS,
+            "phase_ms": phases, "loss_init": l0, "rel_loss_warmup": rel, "rel_loss_last": last,
+            "state_finite": bool(math.isfinite(last)),
+            "optimiser": "SGD on L / L_init (learning rates 0.005 / 0.0005 divided by the initial loss)",
+            "note": "whole step over the seven matrices (fake-quant fwd, block forward on What with the "
+                    "quantized input, loss, backpropagation, straight-through backward + SGD); flops count "
+                    "the GEMMs only"}
+
+
 # Kernel-name patterns of the step's four phases in rocprofv3 output.
 PHASE_PATTERNS = {
     "fq_fwd": r"fq_fwd_kernel<1, 1, [23], ",
@@ -472,16 +605,18 @@ def build_layers(wl, args, want_cpu):
     from paper_2506_03781_amd import synth
     from paper_2506_03781_amd import uniquan as uq
     from paper_2506_03781_amd.layer import QuantLayer
-    g = wl.group_size
     layers, host_np, init_ms = [], [], []
     init_np, X_np = None, None
     for spec in wl.matrices:
+        g = wl.group_size or spec.C
         m = synth.make_matrix(spec, args.seed)
         progress(f"{wl.name}: {spec.name} {spec.R}x{spec.C} generated")
         wdt = torch.bfloat16 if spec.dtype == "bf16" else torch.float32
         for k in wl.ks:
             lay = QuantLayer(m.W, m.X, m.s, k, g, w_dtype=wdt, residual=not args.target)
-            if args.init == "unified":
+            # the unified initialisation takes groups of up to 512 weights; larger
+            # (per-row) groups start from the greedy binary coding (Delta = 1, z_U = 0)
+            if args.init == "unified" and g <= 512:
                 if not layers:
                     lay.init_unified(args.init_grid, args.init_rounds, args.init_clip)  # first-launch warm-up
                 e0, e1 = TimingEvent(), TimingEvent()
@@ -642,7 +777,7 @@ def sub_record(name, args, steps, warmup):
     sm = step_summary(layers, res, mode0)
     ks = layer_kernel_stats(layers, res["tot"], mode0)
     rec = {"description": wl.description, "matrices": [[l.R, l.C] for l in layers], "T": layers[0].T,
-           "k": [l.k for l in layers], "g": wl.group_size, "steps": steps, "warmup": warmup,
+           "k": [l.k for l in layers], "g": [l.g for l in layers], "steps": steps, "warmup": warmup,
            "ms_per_step": res["ms_per_step"], "timed_s": res["wall_s"],
            "value": sm["value"], "unit": "Gweights/s", "fq_frac_hbm": sm["fq_frac_hbm"],
            "gemm_tflops": sm["gemm_tflops"], "gemm_frac_mfma": sm["gemm_frac_mfma"],

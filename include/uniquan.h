@@ -33,7 +33,12 @@
  *           mask m (1 = gradient kept).  Bits k..6 are zero on output and
  *           ignored on input.
  * Dtypes.   UQ_F32 = IEEE binary32, UQ_BF16 = bfloat16 (uint16 storage).
- * Sizes.    R, C, T >= 1.  g is a power of two in [8, 512] dividing C.
+ * Sizes.    R, C, T >= 1.  g divides C and is either a power of two in
+ *           [8, 512] or a multiple of 8 above 512 (e.g. the per-row groups
+ *           g = C of the paper's 7B / 8B settings, 4096, 11008 or 14336
+ *           weights; one workgroup per group then).  The unified
+ *           initialisation and the fused gradient-GEMM backward take
+ *           g <= 512 and g <= 128 respectively.
  *           1 <= k <= 7.  T (calibration tokens) is a multiple of 8.
  * Alignment Per-weight arrays, X, Xt, Yt and workspaces: 16 bytes.
  *           Per-group and per-row arrays: 4 bytes.

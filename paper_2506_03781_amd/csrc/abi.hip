@@ -40,8 +40,10 @@ bool is_dtype(int d) { return d == UQ_F32 || d == UQ_BF16; }
 uq_status check_quant_shape(const char* fn, int64_t R, int64_t C, int k, int g) {
   if (R < 1 || C < 1) return fail(UQ_EINVAL, "%s: R=%lld and C=%lld must be >= 1", fn, (long long)R, (long long)C);
   if (k < 1 || k > 7) return fail(UQ_EINVAL, "%s: k=%d must be in [1, 7]", fn, k);
-  if (g < 8 || (g & (g - 1)) != 0) return fail(UQ_EINVAL, "%s: g=%d must be a power of two >= 8", fn, g);
-  if (g > 512) return fail(UQ_EUNSUPPORTED, "%s: g=%d > 512 is not supported", fn, g);
+  if (g < 8 || g % 8 != 0) return fail(UQ_EINVAL, "%s: g=%d must be a positive multiple of 8", fn, g);
+  if (g <= 512 && (g & (g - 1)) != 0)
+    return fail(UQ_EUNSUPPORTED, "%s: g=%d: groups of up to 512 weights must be a power of two", fn, g);
+  if (g > (1 << 24)) return fail(UQ_EUNSUPPORTED, "%s: g=%d > 2^24 is not supported", fn, g);
   if (C % g != 0) return fail(UQ_EINVAL, "%s: g=%d must divide C=%lld", fn, g, (long long)C);
   if (R > (int64_t(1) << 40) / C) return fail(UQ_EUNSUPPORTED, "%s: R*C too large", fn);
   if ((R * C) / g >= (int64_t(1) << 31)) return fail(UQ_EUNSUPPORTED, "%s: more than 2^31 groups", fn);
@@ -296,6 +298,7 @@ uq_status uniquan_init_unified(int64_t R, int64_t C, int k, int g, const void* W
   const char* fn = "uniquan_init_unified";
   if (uq_status st = check_quant_shape(fn, R, C, k, g)) return st;
   if (k > 4) return fail(UQ_EUNSUPPORTED, "%s: k = %d, supported 1..4", fn, k);
+  if (g > 512) return fail(UQ_EUNSUPPORTED, "%s: g = %d, supported up to 512", fn, g);
   if (!is_dtype(w_dtype)) return fail(UQ_EINVAL, "%s: bad dtype", fn);
   if (grid_G < 1 || grid_G > 4096) return fail(UQ_EINVAL, "%s: grid_G = %d, must be in 1..4096", fn, grid_G);
   if (alt_T < 0 || alt_T > 10000) return fail(UQ_EINVAL, "%s: alt_T = %d, must be in 0..10000", fn, alt_T);

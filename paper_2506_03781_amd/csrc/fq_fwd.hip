@@ -476,6 +476,322 @@ __global__ __launch_bounds__(kThreads) void greedy_kernel(GreedyArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Groups larger than 512 weights: the paper's per-row groups for 7B / 8B
+// models (g = C, e.g. 4096, 11008 or 14336 weights), or any multiple of 8
+// that divides C.  One workgroup of 256 lanes per group reads the group's
+// parameters once, builds its sorted level table (at most 128 levels) in
+// LDS, and streams the group's weights 8 per lane, two chunks per lane in
+// flight.  The per-weight arithmetic is that of fq_fwd_kernel and the fold,
+// so codes and What are the same bit for bit.
+// ---------------------------------------------------------------------------
+constexpr int kBigThreads = 256;
+
+struct BigArgs {
+  int64_t Gn;
+  int g, gpr, k;
+  const void* W;
+  const float* s;
+  const float* s_r;
+  const float* delta;
+  const float* z_u;
+  const float* alpha;
+  const float* z_b;
+  uint8_t* codes;
+  void* W_hat;
+  int resid;
+  // fold
+  float* alpha_star;
+  float* z_star;
+  int code_src;
+};
+
+// Sorted table of one group from its L raw levels (raw[b] already written by
+// the caller and made visible by a barrier): qs[pos], code_of[pos],
+// pos_of[b], sort key (value, code); with NB also the neighbour entries of
+// the local mapping.  Ends with a barrier.
+template <int LOGL, bool NB>
+__device__ __forceinline__ void big_sort(const float* raw, float* qs, uint8_t* code_of, uint8_t* pos_of, float4* nb) {
+  constexpr int L = 1 << LOGL;
+  const int t = threadIdx.x;
+  if (t < L) {
+    const uint64_t kb = level_key(raw[t], t);
+    int rank = 0;
+    for (int b2 = 0; b2 < L; ++b2) rank += level_key(raw[b2], b2) < kb;
+    qs[rank] = raw[t];
+    code_of[rank] = uint8_t(t);
+    pos_of[t] = uint8_t(rank);
+  }
+  __syncthreads();
+  if constexpr (NB) {
+    if (t < L) {
+      const int d = pos_of[t];
+      const int l = d > 0 ? d - 1 : 0;
+      const int r = d < L - 1 ? d + 1 : L - 1;
+      const uint32_t cs = uint32_t(code_of[l]) | (uint32_t(code_of[d]) << 8) | (uint32_t(code_of[r]) << 16);
+      nb[t] = make_float4(qs[l], qs[d], qs[r], __uint_as_float(cs));
+    }
+    __syncthreads();
+  }
+}
+
+// MODE: 0 FULL, 2 FROZEN, 3 LOCAL (neighbour entries).
+template <int WDT, int ODT, int MODE, int LOGL>
+__global__ __launch_bounds__(kBigThreads) void fq_fwd_big_kernel(BigArgs a) {
+  constexpr int L = 1 << LOGL;
+  __shared__ float raw[L], qs[L];
+  __shared__ uint8_t code_of[L], pos_of[L];
+  __shared__ float4 nb[MODE == 3 ? L : 1];
+  const int64_t gid = blockIdx.x;
+  const float* alpha_g = a.alpha + gid * LOGL;
+  if (threadIdx.x < L) raw[threadIdx.x] = level_value_k<LOGL>(alpha_g, a.z_b[gid], threadIdx.x);
+  __syncthreads();
+  if constexpr (MODE != 2) big_sort<LOGL, MODE == 3>(raw, qs, code_of, pos_of, nb);
+  const float dl = a.delta ? a.delta[gid] : 1.0f;
+  const float sr = a.s_r ? a.s_r[gid / a.gpr] : 1.0f;
+  const float zu = a.z_u ? a.z_u[gid] : 0.0f;
+  const float ds = dl * sr;
+  const float tau = tau_k<LOGL>(alpha_g);
+  const int nch = a.g >> 3;
+  const int64_t base = gid * a.g;
+  for (int c0 = threadIdx.x; c0 < nch; c0 += 2 * kBigThreads) {
+    Raw8<WDT> w[2];
+    float4 s0[2], s1[2];
+    uint2 prev[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int c = c0 + h * kBigThreads;
+      s0[h] = s1[h] = make_float4(0, 0, 0, 0);
+      prev[h] = make_uint2(0u, 0u);
+      if (c < nch) {
+        const int64_t off = base + int64_t(c) * kVec;
+        w[h].load(a.W, off);
+        const float4* sp = reinterpret_cast<const float4*>(a.s + off);
+        s0[h] = sp[0];
+        s1[h] = sp[1];
+        if constexpr (MODE != 0) prev[h] = load8u8(a.codes, off);
+      }
+    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int c = c0 + h * kBigThreads;
+      if (c >= nch) break;
+      const int64_t off = base + int64_t(c) * kVec;
+      const float sv[8] = {s0[h].x, s0[h].y, s0[h].z, s0[h].w, s1[h].x, s1[h].y, s1[h].z, s1[h].w};
+      float out[8];
+      uint32_t cw[2] = {0u, 0u};
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float den = ds * sv[i];
+        const float wb = w[h].get(i) / den + zu;
+        float d, wt;
+        uint32_t code;
+        if constexpr (MODE == 0) {
+          const int jj = nearest_full_k<LOGL>(qs, wb, d);
+          wt = qs[jj];
+          code = code_of[jj];
+        } else if constexpr (MODE == 2) {
+          code = byte_of(prev[h], i) & uint32_t(L - 1);
+          wt = raw[code];
+          d = fabsf(wb - wt);
+        } else {
+          const float4 e4 = nb[byte_of(prev[h], i) & uint32_t(L - 1)];
+          const uint32_t cs = __float_as_uint(e4.w);
+          float bd = fabsf(wb - e4.x);
+          wt = e4.x;
+          uint32_t sh = 0;
+          const float dm = fabsf(wb - e4.y);
+          if (dm < bd) { bd = dm; wt = e4.y; sh = 8; }
+          const float dr = fabsf(wb - e4.z);
+          if (dr < bd) { bd = dr; wt = e4.z; sh = 16; }
+          d = bd;
+          code = (cs >> sh) & 0xFFu;
+        }
+        const uint32_t byte = code | (d > tau ? 0u : 0x80u);
+        cw[i >> 2] |= byte << (8 * (i & 3));
+        out[i] = dl * (wt - zu);
+        if (a.resid) out[i] = out[i] - w[h].get(i);
+      }
+      store8<ODT>(a.W_hat, off, out);
+      store8u8(a.codes, off, make_uint2(cw[0], cw[1]));
+    }
+  }
+}
+
+// Fold of one large group: alpha* = Delta alpha, z* = Delta (z_B - z_U), and
+// the codes of the FULL mapping of wbar (code_src 0) or of the raw w against
+// the folded levels (code_src 1), as fold_kernel computes them.
+template <int WDT, int LOGL>
+__global__ __launch_bounds__(kBigThreads) void fold_big_kernel(BigArgs a) {
+  constexpr int L = 1 << LOGL;
+  __shared__ float raw[L], qs[L], s_alpha[LOGL];
+  __shared__ uint8_t code_of[L], pos_of[L];
+  const int64_t gid = blockIdx.x;
+  const float dl = a.delta ? a.delta[gid] : 1.0f;
+  const float zu = a.z_u ? a.z_u[gid] : 0.0f;
+  const float sr = a.s_r ? a.s_r[gid / a.gpr] : 1.0f;
+  const float zst = dl * (a.z_b[gid] - zu);
+  if (threadIdx.x < LOGL) {
+    const float as = dl * a.alpha[gid * LOGL + threadIdx.x];
+    a.alpha_star[gid * LOGL + threadIdx.x] = as;
+    s_alpha[threadIdx.x] = as;
+  }
+  if (threadIdx.x == 0) a.z_star[gid] = zst;
+  if (a.codes == nullptr) return;  // uniform across the grid
+  __syncthreads();
+  if (threadIdx.x < L) {
+    raw[threadIdx.x] = a.code_src == 0 ? level_value_k<LOGL>(a.alpha + gid * LOGL, a.z_b[gid], threadIdx.x)
+                                       : level_value_k<LOGL>(s_alpha, zst, threadIdx.x);
+  }
+  __syncthreads();
+  big_sort<LOGL, false>(raw, qs, code_of, pos_of, nullptr);
+  const float ds = dl * sr;
+  const int nch = a.g >> 3;
+  const int64_t base = gid * a.g;
+  for (int c = threadIdx.x; c < nch; c += kBigThreads) {
+    const int64_t off = base + int64_t(c) * kVec;
+    float w[8], sv[8];
+    load8<WDT>(a.W, off, w);
+    if (a.code_src == 0) load8f(a.s, off, sv);
+    uint32_t cw[2] = {0u, 0u};
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      float x = w[i];
+      if (a.code_src == 0) {
+        const float den = ds * sv[i];
+        x = x / den + zu;
+      }
+      float d;
+      const int j = nearest_full_k<LOGL>(qs, x, d);
+      cw[i >> 2] |= uint32_t(code_of[j]) << (8 * (i & 3));
+    }
+    store8u8(a.codes, off, make_uint2(cw[0], cw[1]));
+  }
+}
+
+// Dequantization of one large group: W_out[j] = q(code_j).
+template <int ODT>
+__global__ __launch_bounds__(kBigThreads) void dequant_big_kernel(BigArgs a) {
+  __shared__ float raw[128];
+  const int64_t gid = blockIdx.x;
+  const int L = 1 << a.k;
+  if (int(threadIdx.x) < L) raw[threadIdx.x] = level_value(a.alpha + gid * a.k, a.z_b[gid], a.k, threadIdx.x);
+  __syncthreads();
+  const int nch = a.g >> 3;
+  const int64_t base = gid * a.g;
+  for (int c = threadIdx.x; c < nch; c += kBigThreads) {
+    const int64_t off = base + int64_t(c) * kVec;
+    const uint2 cb = load8u8(a.codes, off);
+    float out[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) out[i] = raw[byte_of(cb, i) & uint32_t(L - 1)];
+    store8<ODT>(a.W_hat, off, out);
+  }
+}
+
+// Sum of v over the workgroup's 256 lanes in a fixed order: xor butterfly in
+// each wavefront, then the four wavefront sums pairwise.  Every lane gets the
+// result.
+__device__ __forceinline__ float big_block_sum(float v, float* red) {
+  for (int msk = 32; msk >= 1; msk >>= 1) v += __shfl_xor(v, msk, 64);
+  __syncthreads();  // red is free (earlier readers are done)
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  return (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+// Greedy start on one large group: per bit, alpha = (sum of |r|) / g with the
+// workgroup sum above, r recomputed from w and s for every bit (set-up only,
+// so the group need not stay in registers).
+template <int WDT>
+__global__ __launch_bounds__(kBigThreads) void greedy_big_kernel(BigArgs a) {
+  __shared__ float red[4];
+  __shared__ float s_al[8];
+  const int64_t gid = blockIdx.x;
+  const float dl = a.delta ? a.delta[gid] : 1.0f;
+  const float sr = a.s_r ? a.s_r[gid / a.gpr] : 1.0f;
+  const float zu = a.z_u ? a.z_u[gid] : 0.0f;
+  const float zb = a.z_b[gid];
+  const float ds = dl * sr;
+  const int nch = a.g >> 3;
+  const int64_t base = gid * a.g;
+  for (int b = 0; b < a.k; ++b) {
+    float acc = 0.0f;
+    for (int c = threadIdx.x; c < nch; c += kBigThreads) {
+      const int64_t off = base + int64_t(c) * kVec;
+      float w[8], sv[8];
+      load8<WDT>(a.W, off, w);
+      load8f(a.s, off, sv);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        float r = (w[i] / (ds * sv[i]) + zu) - zb;
+        for (int j = 0; j < b; ++j) r = r >= 0.0f ? r - s_al[j] : r + s_al[j];
+        acc += fabsf(r);
+      }
+    }
+    const float al = big_block_sum(acc, red) / float(a.g);
+    if (threadIdx.x == 0) {
+      s_al[b] = al;
+      a.alpha_star[gid * a.k + b] = al;  // the greedy alpha (the launcher passes its output here)
+    }
+    __syncthreads();
+  }
+}
+
+static BigArgs big_args(int64_t R, int64_t C, int k, int g) {
+  BigArgs b{};
+  b.Gn = R * C / g;
+  b.g = g;
+  b.gpr = int(C / g);
+  b.k = k;
+  return b;
+}
+
+template <int WD, int OD, int MD>
+static hipError_t launch_fwd_big(const BigArgs& a, hipStream_t st) {
+  const dim3 grid(unsigned(a.Gn)), block(kBigThreads);
+  switch (a.k) {
+    case 1: hipLaunchKernelGGL((fq_fwd_big_kernel<WD, OD, MD, 1>), grid, block, 0, st, a); break;
+    case 2: hipLaunchKernelGGL((fq_fwd_big_kernel<WD, OD, MD, 2>), grid, block, 0, st, a); break;
+    case 3: hipLaunchKernelGGL((fq_fwd_big_kernel<WD, OD, MD, 3>), grid, block, 0, st, a); break;
+    case 4: hipLaunchKernelGGL((fq_fwd_big_kernel<WD, OD, MD, 4>), grid, block, 0, st, a); break;
+    case 5: hipLaunchKernelGGL((fq_fwd_big_kernel<WD, OD, MD, 5>), grid, block, 0, st, a); break;
+    case 6: hipLaunchKernelGGL((fq_fwd_big_kernel<WD, OD, MD, 6>), grid, block, 0, st, a); break;
+    default: hipLaunchKernelGGL((fq_fwd_big_kernel<WD, OD, MD, 7>), grid, block, 0, st, a); break;
+  }
+  return hipGetLastError();
+}
+
+static hipError_t launch_fq_fwd_big(const FqFwdLaunch& p, hipStream_t st) {
+  BigArgs a = big_args(p.R, p.C, p.k, p.g);
+  a.W = p.W; a.s = p.s; a.s_r = p.s_r; a.delta = p.delta; a.z_u = p.z_u;
+  a.alpha = p.alpha; a.z_b = p.z_b; a.codes = p.codes; a.W_hat = p.W_hat;
+  a.resid = p.resid;
+#define UQ_FWDB(WD, OD, MD, MK) \
+  if (p.w_dtype == WD && p.w_hat_dtype == OD && p.mode == MD) return launch_fwd_big<WD, OD, MK>(a, st);
+  UQ_FWDB(BF16, BF16, 0, 0) UQ_FWDB(BF16, BF16, 1, 3) UQ_FWDB(BF16, BF16, 2, 2)
+  UQ_FWDB(BF16, F32, 0, 0) UQ_FWDB(BF16, F32, 1, 3) UQ_FWDB(BF16, F32, 2, 2)
+  UQ_FWDB(F32, BF16, 0, 0) UQ_FWDB(F32, BF16, 1, 3) UQ_FWDB(F32, BF16, 2, 2)
+  UQ_FWDB(F32, F32, 0, 0) UQ_FWDB(F32, F32, 1, 3) UQ_FWDB(F32, F32, 2, 2)
+#undef UQ_FWDB
+  return hipErrorInvalidValue;
+}
+
+template <int WD>
+static hipError_t launch_fold_big(const BigArgs& a, hipStream_t st) {
+  const dim3 grid(unsigned(a.Gn)), block(kBigThreads);
+  switch (a.k) {
+    case 1: hipLaunchKernelGGL((fold_big_kernel<WD, 1>), grid, block, 0, st, a); break;
+    case 2: hipLaunchKernelGGL((fold_big_kernel<WD, 2>), grid, block, 0, st, a); break;
+    case 3: hipLaunchKernelGGL((fold_big_kernel<WD, 3>), grid, block, 0, st, a); break;
+    case 4: hipLaunchKernelGGL((fold_big_kernel<WD, 4>), grid, block, 0, st, a); break;
+    case 5: hipLaunchKernelGGL((fold_big_kernel<WD, 5>), grid, block, 0, st, a); break;
+    case 6: hipLaunchKernelGGL((fold_big_kernel<WD, 6>), grid, block, 0, st, a); break;
+    default: hipLaunchKernelGGL((fold_big_kernel<WD, 7>), grid, block, 0, st, a); break;
+  }
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // Launchers
 // ---------------------------------------------------------------------------
 // Tile of `chunks` x 2048 weights, capped so the level tables stay within
@@ -556,6 +872,7 @@ static hipError_t launch_fwd_k(const FwdArgs& a, int k, hipStream_t st) {
 }
 
 hipError_t launch_fq_fwd(const FqFwdLaunch& p, hipStream_t st) {
+  if (p.g > 512) return launch_fq_fwd_big(p, st);
   FwdArgs a;
   a.t = make_geom(p.R, p.C, p.k, p.g, 1);
   a.W = p.W; a.s = p.s; a.s_r = p.s_r; a.delta = p.delta; a.z_u = p.z_u;
@@ -572,6 +889,13 @@ hipError_t launch_fq_fwd(const FqFwdLaunch& p, hipStream_t st) {
 }
 
 hipError_t launch_fold(const FoldLaunch& p, hipStream_t st) {
+  if (p.g > 512) {
+    BigArgs b = big_args(p.R, p.C, p.k, p.g);
+    b.W = p.W; b.s = p.s; b.s_r = p.s_r; b.delta = p.delta; b.z_u = p.z_u;
+    b.alpha = p.alpha; b.z_b = p.z_b; b.alpha_star = p.alpha_star; b.z_star = p.z_star;
+    b.codes = p.codes; b.code_src = p.code_src;
+    return p.w_dtype == BF16 ? launch_fold_big<BF16>(b, st) : launch_fold_big<F32>(b, st);
+  }
   FoldArgs a;
   a.t = make_geom(p.R, p.C, p.k, p.g, 1);
   a.W = p.W; a.s = p.s; a.s_r = p.s_r; a.delta = p.delta; a.z_u = p.z_u;
@@ -585,6 +909,14 @@ hipError_t launch_fold(const FoldLaunch& p, hipStream_t st) {
 }
 
 hipError_t launch_dequant(const DequantLaunch& p, hipStream_t st) {
+  if (p.g > 512) {
+    BigArgs b = big_args(p.R, p.C, p.k, p.g);
+    b.codes = const_cast<uint8_t*>(p.codes); b.alpha = p.alpha; b.z_b = p.z_b; b.W_hat = p.W_out;
+    const dim3 grid(unsigned(b.Gn)), block(kBigThreads);
+    if (p.out_dtype == BF16) hipLaunchKernelGGL((dequant_big_kernel<BF16>), grid, block, 0, st, b);
+    else hipLaunchKernelGGL((dequant_big_kernel<F32>), grid, block, 0, st, b);
+    return hipGetLastError();
+  }
   DequantArgs a;
   a.t = make_geom(p.R, p.C, p.k, p.g, 1);
   a.codes = p.codes; a.alpha = p.alpha; a.z_b = p.z_b; a.W_out = p.W_out;
@@ -596,6 +928,15 @@ hipError_t launch_dequant(const DequantLaunch& p, hipStream_t st) {
 }
 
 hipError_t launch_greedy(const GreedyLaunch& p, hipStream_t st) {
+  if (p.g > 512) {
+    BigArgs b = big_args(p.R, p.C, p.k, p.g);
+    b.W = p.W; b.s = p.s; b.s_r = p.s_r; b.delta = p.delta; b.z_u = p.z_u; b.z_b = p.z_b;
+    b.alpha_star = p.alpha;  // output: alpha
+    const dim3 grid(unsigned(b.Gn)), block(kBigThreads);
+    if (p.w_dtype == BF16) hipLaunchKernelGGL((greedy_big_kernel<BF16>), grid, block, 0, st, b);
+    else hipLaunchKernelGGL((greedy_big_kernel<F32>), grid, block, 0, st, b);
+    return hipGetLastError();
+  }
   GreedyArgs a;
   a.t = make_geom(p.R, p.C, p.k, p.g, 1);
   a.W = p.W; a.s = p.s; a.s_r = p.s_r; a.delta = p.delta; a.z_u = p.z_u;

@@ -100,7 +100,7 @@ class Workload:
     name: str
     description: str
     ks: tuple
-    group_size: int
+    group_size: int     # 0: one group per row (g = C of each matrix)
     matrices: list
 
 
@@ -244,6 +244,12 @@ WORKLOADS = {
          _spec7b("v_proj", 4096, 4096, 8192), _spec7b("o_proj", 4096, 4096, 8192, x_stream=2),
          _spec7b("gate_proj", 11008, 4096, 8192), _spec7b("up_proj", 11008, 4096, 8192),
          _spec7b("down_proj", 4096, 11008, 8192, "silu_gated", 1)]),
+    "mlp7b_rows": Workload(
+        "mlp7b_rows", "7B MLP gate/up 11008x4096, down 4096x11008, X 4096 tokens, k=3, one group per row "
+        "(g = C: 4096 and 11008)",
+        (3,), 0,
+        [_spec7b("gate_proj", 11008, 4096, 4096), _spec7b("up_proj", 11008, 4096, 4096),
+         _spec7b("down_proj", 4096, 11008, 4096, "silu_gated", 1)]),
     "mlp70b": Workload(
         "mlp70b", "70B MLP slice gate/up 28672x8192, down 8192x28672, X 4096 tokens, k in {2,3}, g=128",
         (2, 3), 128,

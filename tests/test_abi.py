@@ -55,9 +55,10 @@ def fwd(L, R=4, C=256, k=3, g=128, W=FAKE, wdt=uq.UQ_BF16, s=FAKE, alpha=FAKE, z
 @pytest.mark.parametrize("kw,status,text", [
     (dict(k=0), uq.UQ_EINVAL, "k=0"),
     (dict(k=8), uq.UQ_EINVAL, "k=8"),
-    (dict(g=96), uq.UQ_EINVAL, "power of two"),
-    (dict(g=4), uq.UQ_EINVAL, "power of two"),
-    (dict(g=1024, C=2048), uq.UQ_EUNSUPPORTED, "g=1024"),
+    (dict(g=96), uq.UQ_EUNSUPPORTED, "power of two"),
+    (dict(g=4), uq.UQ_EINVAL, "multiple of 8"),
+    (dict(g=1028, C=2056), uq.UQ_EINVAL, "multiple of 8"),
+    (dict(g=1032, C=2048), uq.UQ_EINVAL, "divide"),
     (dict(C=192), uq.UQ_EINVAL, "divide"),
     (dict(R=0), uq.UQ_EINVAL, "R=0"),
     (dict(W=None), uq.UQ_EINVAL, "W must not be NULL"),
@@ -70,6 +71,17 @@ def fwd(L, R=4, C=256, k=3, g=128, W=FAKE, wdt=uq.UQ_BF16, s=FAKE, alpha=FAKE, z
 def test_fq_fwd_validation(L, kw, status, text):
     assert fwd(L, **kw) == status
     assert text in uq.last_error()
+
+
+def test_large_groups_accepted_where_supported(L):
+    """Groups of more than 512 weights (any multiple of 8 dividing C, e.g. one
+    row of 11008): the quantizer entry points take them, the unified
+    initialisation and the fused gradient-GEMM backward do not."""
+    assert L.uniquan_init_unified(4, 11008, 3, 11008, FAKE, 1, 30, 15, 0, FAKE, FAKE, FAKE, FAKE, None, None,
+                                  None, None, None) == uq.UQ_EUNSUPPORTED
+    assert "up to 512" in uq.last_error()
+    assert L.uniquan_layer_grad_ste_sgd(64, 4, 4096, 3, 4096, FAKE, FAKE, FAKE, 1, FAKE, None, None, None, FAKE,
+                                        FAKE, FAKE, 0.1, 0.1, None, None, None, None) == uq.UQ_EUNSUPPORTED
 
 
 def test_fq_bwd_validation(L):
