@@ -121,6 +121,9 @@ def parse():
     ap.add_argument("--block7b-steps", type=int, default=100,
                     help="timed steps of the 7B block's seven matrices (the configuration times 100)")
     ap.add_argument("--no-ceilings", action="store_true", help="skip the streaming and MFMA ceiling probes")
+    ap.add_argument("--unfused", action="store_true",
+                    help="time the step as four passes (fq_fwd, loss GEMM, gradient GEMM, fq_bwd with SGD) instead "
+                         "of two GEMMs and the fused backward + SGD + next forward pass")
     ap.add_argument("--summarize-profiles", default=None, metavar="WORKLOAD",
                     help="(no GPU) write profiles/ summaries from the rocprofv3 CSVs under gpurun_out/")
     ap.add_argument("--mode", default="paper", choices=["paper", "full", "local", "frozen"])
@@ -161,6 +164,18 @@ def fq_bytes_per_weight(k, g, mode, w_bytes=2, what_bytes=2, grad_bytes=2):
     # dL/dWhat, W, s, code in; s out; per group Delta, z_U in, alpha, z_B in and out
     bwd = grad_bytes + w_bytes + 4 + 1 + 4 + (8 + 2 * (4 * k + 4)) / g
     return fwd, bwd
+
+
+def fq_step_bytes_per_weight(k, g, w_bytes=2, what_bytes=2, grad_bytes=2):
+    """Algorithmic bytes per weight of uniquan_fq_step (backward + SGD of one
+    step, forward of the next), as (read, written).  One pass for g <= 512:
+    dL/dWhat, W, s, code in; s, What, code out; per group Delta, z_U, s_r,
+    alpha, z_B in and alpha, z_B out.  Larger groups run the two passes."""
+    if g > 512:
+        return fq_read_write_bytes(k, g, "local", w_bytes, what_bytes, grad_bytes)
+    rd = grad_bytes + w_bytes + 4 + 1 + (4 * k + 12) / g
+    wr = 4 + what_bytes + 1 + (4 * k + 4) / g
+    return rd, wr
 
 
 def fq_read_write_bytes(k, g, mode, w_bytes=2, what_bytes=2, grad_bytes=2):
@@ -497,10 +512,11 @@ PHASE_PATTERNS = {
     "gemm_fwd": r"gemm_pp_kernel<256, \d+, [14], ",
     "gemm_bwd": r"gemm_pp_kernel<256, 256, 2, ",
     "fq_bwd": r"fq_bwd_kernel<1, 1, ",
+    "fq_step": r"fq_step_kernel<1, 1, 1, [023], ",
 }
 
 
-def summarize_profiles(workload, steps, warmup, out_dir=PROFILES, run_dir=os.path.join(ROOT, "gpurun_out")):
+def summarize_profiles(workload, steps, warmup, fused=True, out_dir=PROFILES, run_dir=os.path.join(ROOT, "gpurun_out")):
     """Write profiles/uniquan_kernels_<workload>.md and pmc_<workload>.json from
     the CSVs of three rocprofv3 runs of this script (commands in the summary):
     a kernel trace with statistics, then FETCH_SIZE and WRITE_SIZE counter
@@ -534,14 +550,16 @@ def summarize_profiles(workload, steps, warmup, out_dir=PROFILES, run_dir=os.pat
         vals = [v for k, vs in d.items() if re.search(pat, k) for v in vs]
         return sum(vals) / len(vals), len(vals)
 
+    phases = FUSED_PHASES if fused else PHASES
+    patterns = {ph: PHASE_PATTERNS[ph] for ph in phases}
     kern = {}
-    for ph, pat in PHASE_PATTERNS.items():
+    for ph, pat in patterns.items():
         f, nf = mean_kib(fetch, pat)
         w, nw = mean_kib(write, pat)
         kern[ph] = {"pattern": pat, "fetch_kib_raw": f, "write_kib_raw": w, "dispatches": [nf, nw],
                     "hbm_bytes_per_launch": (f * fscale + w * wscale) * 1024}
     win = {}
-    for ph, pat in list(PHASE_PATTERNS.items()) + [("loss_reduce", r"reduce_loss_kernel")]:
+    for ph, pat in list(patterns.items()) + [("loss_reduce", r"reduce_loss_kernel")]:
         d = sorted((int(r["Start_Timestamp"]), int(r["End_Timestamp"])) for r in trace
                    if re.search(pat, r["Kernel_Name"]))
         sel = d[warmup * n_layers:(warmup + steps) * n_layers]
@@ -551,10 +569,13 @@ def summarize_profiles(workload, steps, warmup, out_dir=PROFILES, run_dir=os.pat
                          "WRITE_SIZE scaled so that it reads and writes 262144 KiB",
           "kernels": kern, "trace_timed_avg_us": {ph: v[1] for ph, v in win.items()}}
     json.dump(js, open(os.path.join(out_dir, f"pmc_{workload}.json"), "w"), indent=1)
-    cmd_common = f"--workload {workload} --no-cpu-baseline --no-block --no-ceilings --sub-workloads ''"
+    cmd_common = (f"--workload {workload} --no-cpu-baseline --no-block --no-ceilings --sub-workloads ''"
+                  + ("" if fused else " --unfused"))
     lines = [f"# rocprofv3 summary: UniQuan_F step kernels, workload `{workload}`", "",
              f"Workload: {wl.description}; bench.py step (unified initialisation G = 30, T = 15 at set-up, "
-             "residual loss form, LOCAL/FROZEN mapping alternating); MI355X.", "",
+             "residual loss form, LOCAL/FROZEN mapping alternating, " + (
+                 "two GEMMs and the fused backward + SGD + next forward pass" if fused else
+                 "four passes") + "); MI355X.", "",
              "Commands (run from the repository root on the GPU box; the summary is then written on the CPU "
              f"with `python bench.py --summarize-profiles {workload} --steps {steps} --warmup {warmup}`):", "",
              "```",
@@ -571,7 +592,7 @@ def summarize_profiles(workload, steps, warmup, out_dir=PROFILES, run_dir=os.pat
              "is the loss GEMM plus its loss reduction.", "",
              "| Phase | Kernel pattern | Dispatches | Average (us) |", "|---|---|---|---|"]
     for ph, (n, avg) in win.items():
-        lines.append(f"| {ph} | `{PHASE_PATTERNS.get(ph, 'reduce_loss_kernel')}` | {n} | {avg:.1f} |")
+        lines.append(f"| {ph} | `{patterns.get(ph, 'reduce_loss_kernel')}` | {n} | {avg:.1f} |")
     lines += ["", "## HBM traffic per launch (`--pmc FETCH_SIZE`, `--pmc WRITE_SIZE`)", "",
               f"Calibration on a plain 256 MiB device copy: FETCH_SIZE x {fscale:.3f}, WRITE_SIZE x {wscale:.3f}.",
               "", "| Phase | Kernel pattern | FETCH_SIZE raw (KiB) | WRITE_SIZE (KiB) | HBM bytes / launch (scaled) |",
@@ -649,6 +670,7 @@ def build_layers(wl, args, want_cpu):
 
 
 PHASES = ["fq_fwd", "gemm_fwd", "gemm_bwd", "fq_bwd"]
+FUSED_PHASES = ["gemm_fwd", "gemm_bwd", "fq_step"]
 
 
 class StepRunner:
@@ -656,10 +678,17 @@ class StepRunner:
     recorded through the checked wrappers the first time it runs (a warm-up
     step) and replayed afterwards, so the host enqueues a phase in a few
     microseconds and the stream stays ahead of the GPU; the timing events are
-    created before the timed steps."""
+    created before the timed steps.
 
-    def __init__(self, layers, mode):
-        self.layers, self.mode = layers, mode
+    fused = False: fq_fwd -> loss GEMM -> weight-gradient GEMM -> fq_bwd with
+    SGD.  fused = True: loss GEMM -> weight-gradient GEMM -> fq_step (the
+    backward with SGD and the next step's forward in one pass); the first
+    step's forward is the initial mapping done at set-up, so every step still
+    runs the whole hot path once."""
+
+    def __init__(self, layers, mode, fused=False):
+        self.layers, self.mode, self.fused = layers, mode, fused
+        self.phases = FUSED_PHASES if fused else PHASES
         self.launches = {}
 
     def phase(self, li, name, mode, fn, *a):
@@ -673,48 +702,49 @@ class StepRunner:
     def step(self, step, evs=None):
         from paper_2506_03781_amd import uniquan as uq
         mode = schedule(self.mode, step)
+        nxt = schedule(self.mode, step + 1)
         for li, lay in enumerate(self.layers):
             es = evs[li] if evs is not None else None
+            calls = ([] if self.fused else [("fq_fwd", mode, lay.fq_fwd, (mode,))]) + [
+                ("gemm_fwd", 0, lay.recon, (False,)),
+                ("gemm_bwd", 0, uq.uniquan_layer_grad, (lay.T, lay.R, lay.C, lay.Et, lay.Xt, lay.G))]
+            if self.fused:
+                calls.append(("fq_step", nxt, lay.fq_step, (*lay.lr, nxt)))
+            else:
+                calls.append(("fq_bwd", 0, lay.fq_bwd_sgd, lay.lr))
+            for i, (name, md, fn, a) in enumerate(calls):
+                if es:
+                    es[i].record()
+                self.phase(li, name, md, fn, *a)
             if es:
-                es[0].record()
-            self.phase(li, "fq_fwd", mode, lay.fq_fwd, mode)
-            if es:
-                es[1].record()
-            self.phase(li, "gemm_fwd", 0, lay.recon, False)
-            if es:
-                es[2].record()
-            self.phase(li, "gemm_bwd", 0, uq.uniquan_layer_grad, lay.T, lay.R, lay.C, lay.Et, lay.Xt, lay.G)
-            if es:
-                es[3].record()
-            self.phase(li, "fq_bwd", 0, lay.fq_bwd_sgd, *lay.lr)
-            if es:
-                es[4].record()
+                es[len(calls)].record()
 
-    def run(self, steps, warmup):
+    def run(self, steps, warmup, first_step=0):
         """warmup untimed steps, then `steps` timed ones; per-phase HIP events."""
         import torch
-        pool = [[[TimingEvent() for _ in range(5)] for _ in self.layers] for _ in range(steps)]
+        nph = len(self.phases)
+        pool = [[[TimingEvent() for _ in range(nph + 1)] for _ in self.layers] for _ in range(steps)]
         for s_ in range(warmup):
-            self.step(s_)
+            self.step(first_step + s_)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for s_ in range(steps):
-            self.step(warmup + s_, pool[s_])
+            self.step(first_step + warmup + s_, pool[s_])
         torch.cuda.synchronize()
         t1 = time.perf_counter()
-        tot = {p: 0.0 for p in PHASES}
+        tot = {p: 0.0 for p in self.phases}
         per_layer = []
         for li in range(len(self.layers)):
-            d = {p: 0.0 for p in PHASES}
+            d = {p: 0.0 for p in self.phases}
             for es_step in pool:
                 es = es_step[li]
-                for i, p in enumerate(PHASES):
+                for i, p in enumerate(self.phases):
                     d[p] += es[i].elapsed_time(es[i + 1])
-            for p in PHASES:
+            for p in self.phases:
                 d[p] /= steps
                 tot[p] += d[p]
             per_layer.append(d)
-        self.next_step = warmup + steps
+        self.next_step = first_step + warmup + steps
         return {"ms_per_step": (t1 - t0) * 1e3 / steps, "wall_s": t1 - t0, "tot": tot, "per_layer": per_layer}
 
 
@@ -723,7 +753,7 @@ def layer_kernel_stats(layers, tot, mode0):
     import torch
     n = len(layers)
     out = {}
-    for ph in PHASES:
+    for ph in tot:
         dur_ms = tot[ph] / n
         if ph in ("gemm_fwd", "gemm_bwd"):
             work = sum(2.0 * l.T * l.R * l.C for l in layers) / n
@@ -734,8 +764,11 @@ def layer_kernel_stats(layers, tot, mode0):
         byt = 0.0
         for l in layers:
             wb = 2 if l.W.dtype == torch.bfloat16 else 4
-            f, b = fq_bytes_per_weight(l.k, l.g, mode0, wb)
-            byt += (f if ph == "fq_fwd" else b) * l.R * l.C
+            if ph == "fq_step":
+                byt += sum(fq_step_bytes_per_weight(l.k, l.g, wb)) * l.R * l.C
+            else:
+                f, b = fq_bytes_per_weight(l.k, l.g, mode0, wb)
+                byt += (f if ph == "fq_fwd" else b) * l.R * l.C
         byt /= n
         ach = byt / (dur_ms * 1e-3) / 1e9
         out[ph] = dict(bound="hbm", achieved=ach, peak=HBM_PEAK_GBS, unit="GB/s", frac=ach / HBM_PEAK_GBS,
@@ -748,13 +781,17 @@ def step_summary(layers, res, mode0):
     tot = res["tot"]
     weights = sum(l.R * l.C for l in layers)
     flops = sum(4.0 * l.T * l.R * l.C for l in layers)
-    fq_ms = tot["fq_fwd"] + tot["fq_bwd"]
+    fused = "fq_step" in tot
+    fq_ms = tot["fq_step"] if fused else tot["fq_fwd"] + tot["fq_bwd"]
     gemm_ms = tot["gemm_fwd"] + tot["gemm_bwd"]
     fq_bytes = 0.0
     for l in layers:
         wb = 2 if l.W.dtype == torch.bfloat16 else 4
-        f, b = fq_bytes_per_weight(l.k, l.g, mode0, wb)
-        fq_bytes += (f + b) * l.R * l.C
+        if fused:
+            fq_bytes += sum(fq_step_bytes_per_weight(l.k, l.g, wb)) * l.R * l.C
+        else:
+            f, b = fq_bytes_per_weight(l.k, l.g, mode0, wb)
+            fq_bytes += (f + b) * l.R * l.C
     fq_gbs = fq_bytes / (fq_ms * 1e-3) / 1e9
     gemm_tflops = flops / (gemm_ms * 1e-3) / 1e12
     rel = [float(l.loss.item()) / l.l0 for l in layers]
@@ -773,7 +810,7 @@ def sub_record(name, args, steps, warmup):
     wl = synth.WORKLOADS[name]
     layers, init_ms, _, _, _ = build_layers(wl, args, False)
     mode0 = "local" if args.mode == "paper" else args.mode
-    res = StepRunner(layers, args.mode).run(steps, warmup)
+    res = StepRunner(layers, args.mode, fused=not args.unfused).run(steps, warmup)
     sm = step_summary(layers, res, mode0)
     ks = layer_kernel_stats(layers, res["tot"], mode0)
     rec = {"description": wl.description, "matrices": [[l.R, l.C] for l in layers], "T": layers[0].T,
@@ -795,7 +832,7 @@ def sub_record(name, args, steps, warmup):
 def main():
     args = parse()
     if args.summarize_profiles:
-        summarize_profiles(args.summarize_profiles, args.steps, args.warmup)
+        summarize_profiles(args.summarize_profiles, args.steps, args.warmup, fused=not args.unfused)
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); this build has no multi-GPU path.",
@@ -815,7 +852,7 @@ def main():
     layers, init_ms, host_np, init_np, X_np = build_layers(wl, args, want_cpu)
     mode0 = "local" if args.mode == "paper" else args.mode
 
-    runner = StepRunner(layers, args.mode)
+    runner = StepRunner(layers, args.mode, fused=not args.unfused)
     if args.calib_copy:
         src = torch.empty(64 << 20, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)
@@ -871,10 +908,20 @@ def main():
                 fev.append(e)
         torch.cuda.synchronize()
         fused_ms = sum(a.elapsed_time(b) for a, b in fev) / len(fev)
-        fused = {"ms_per_step": fused_ms, "unfused_ms_per_step_events": sum(tot.values()), "steps": nfs,
+        fused = {"ms_per_step": fused_ms, "headline_ms_per_step_events": sum(tot.values()), "steps": nfs,
                  "note": "fq_fwd -> loss GEMM -> weight-gradient GEMM with the straight-through backward "
                          "and SGD update in its epilogue (dL/dWhat never written)"}
 
+    # the other form of the step (four passes, or the fused one), for comparison
+    alt_runner = StepRunner(layers, args.mode, fused=args.unfused)
+    alt = alt_runner.run(min(args.steps, 10), 2, first_step=runner.next_step)
+    alt_sm = step_summary(layers, alt, mode0)
+    alt_rec = {"fused": bool(args.unfused), "ms_per_step": alt["ms_per_step"], "phase_ms_per_step": alt["tot"],
+               "value": alt_sm["value"], "fq_frac_hbm": alt_sm["fq_frac_hbm"], "gemm_tflops": alt_sm["gemm_tflops"],
+               "steps": min(args.steps, 10),
+               "note": ("fq_fwd -> loss GEMM -> weight-gradient GEMM -> fq_bwd with SGD, four passes"
+                        if not args.unfused else "loss GEMM -> weight-gradient GEMM -> fq_step (backward + SGD "
+                        "+ next forward in one pass)")}
     bcq = bcq_inference(layers)
     progress("per-mode, fused and deployment legs done")
     rel_loss, finite = sm["rel_loss"], sm["finite"]
@@ -905,6 +952,10 @@ def main():
         "fq_fwd_us_by_mode": by_mode,
         "roofline": roof,
         "fused_bwd_step": fused,
+        "step_form": ("two GEMMs + fq_step (straight-through backward with SGD fused with the next step's "
+                      "forward; the first forward is the initial mapping at set-up)") if not args.unfused else
+                     "four passes: fq_fwd, loss GEMM, weight-gradient GEMM, fq_bwd with SGD",
+        "other_step_form": alt_rec,
         "optimiser": {"rule": "SGD on L / L_init per layer (learning rates 0.005 for s, 0.0005 for alpha and z_B, "
                               "divided by the layer's initial loss)",
                       "rel_loss_after_timed_steps": rel_loss, "state_finite": finite},
@@ -929,7 +980,7 @@ def main():
     fq_mix = [0.0, 0.0]
     for l in layers:
         wb = 2 if l.W.dtype == torch.bfloat16 else 4
-        r_, w_ = fq_read_write_bytes(l.k, l.g, mode0, wb)
+        r_, w_ = fq_read_write_bytes(l.k, l.g, mode0, wb) if args.unfused else fq_step_bytes_per_weight(l.k, l.g, wb)
         fq_mix[0] += r_ * l.R * l.C
         fq_mix[1] += w_ * l.R * l.C
     del layers, runner

@@ -197,6 +197,31 @@ uq_status uniquan_fq_bwd_sgd(int64_t R, int64_t C, int k, int g,
                              void* stream);
 
 /*
+ * uniquan_fq_step -- the end of one optimisation step and the start of the
+ * next in one pass over the weights (Algorithm 1's update line, then its
+ * quantization line for the next step): uniquan_fq_bwd_sgd with the codes'
+ * mask bits and dL/dWhat of step t (s, alpha, z_b updated in place), then
+ * uniquan_fq_fwd (residual == 0) or uniquan_fq_fwd_residual (residual == 1)
+ * with next_mode on the updated parameters, writing W_hat and the new code
+ * bytes.  The results equal those two calls bit for bit.  Per weight it reads
+ * dL/dWhat, W, s and the code byte once (9 B with bf16 W and dL/dWhat) and
+ * writes s, W_hat and the code byte (7 B), against 23 B for the two passes.
+ * Runs as one kernel for g <= 512 (LOCAL mapping: where the neighbour table
+ * fits, i.e. (512 / g) 2^k <= 4096); otherwise as the two calls.  Arguments
+ * and errors as for those calls; the gradient outputs are not stored.
+ */
+uq_status uniquan_fq_step(int64_t R, int64_t C, int k, int g,
+                          const void* W, int w_dtype,
+                          float* s, const float* s_r,
+                          const float* delta, const float* z_u,
+                          float* alpha, float* z_b,
+                          uint8_t* codes,
+                          const void* grad_W_hat, int grad_dtype,
+                          float lr_f, float lr_b,
+                          int next_mode, void* W_hat, int w_hat_dtype, int residual,
+                          void* stream);
+
+/*
  * uniquan_layer_target -- the fixed reconstruction target of one linear
  * layer, Y = X W^T (Algorithm 1, output of the unquantized layer), stored
  * transposed: Yt[r, t] = sum_c W[r, c] X[t, c], fp32 accumulation on bf16

@@ -138,6 +138,24 @@ uq_status uniquan_fq_bwd_sgd(int64_t R, int64_t C, int k, int g, const void* W, 
   return hip_status(fn, uq::launch_fq_bwd(p, static_cast<hipStream_t>(stream)));
 }
 
+uq_status uniquan_fq_step(int64_t R, int64_t C, int k, int g, const void* W, int w_dtype, float* s,
+                          const float* s_r, const float* delta, const float* z_u, float* alpha, float* z_b,
+                          uint8_t* codes, const void* grad_W_hat, int grad_dtype, float lr_f, float lr_b,
+                          int next_mode, void* W_hat, int w_hat_dtype, int residual, void* stream) {
+  const char* fn = "uniquan_fq_step";
+  if (uq_status st = check_quant_shape(fn, R, C, k, g)) return st;
+  if (!is_dtype(w_dtype) || !is_dtype(grad_dtype) || !is_dtype(w_hat_dtype)) return fail(UQ_EINVAL, "%s: bad dtype", fn);
+  if (next_mode < UQ_MAP_FULL || next_mode > UQ_MAP_FROZEN)
+    return fail(UQ_EINVAL, "%s: bad mapping mode %d", fn, next_mode);
+  if (residual != 0 && residual != 1) return fail(UQ_EINVAL, "%s: residual must be 0 or 1", fn);
+  REQ_PTR(W, 16); REQ_PTR(s, 16); REQ_PTR(alpha, 4); REQ_PTR(z_b, 4); REQ_PTR(codes, 16);
+  REQ_PTR(grad_W_hat, 16); REQ_PTR(W_hat, 16);
+  OPT_PTR(s_r, 4); OPT_PTR(delta, 4); OPT_PTR(z_u, 4);
+  uq::FqStepLaunch p{R, C, k, g, W, w_dtype, s, s_r, delta, z_u, alpha, z_b, codes, grad_W_hat, grad_dtype,
+                     lr_f, lr_b, next_mode, W_hat, w_hat_dtype, residual};
+  return hip_status(fn, uq::launch_fq_step(p, static_cast<hipStream_t>(stream)));
+}
+
 uq_status uniquan_layer_target(int64_t T, int64_t R, int64_t C, const uint16_t* X, const uint16_t* W, float* Yt,
                                void* stream) {
   const char* fn = "uniquan_layer_target";

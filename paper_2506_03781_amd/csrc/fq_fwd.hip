@@ -296,6 +296,219 @@ __global__ __launch_bounds__(kThreads) void fq_fwd_kernel(FwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// One pass per step over the weights: the straight-through backward of step
+// t with its SGD update (the arithmetic of fq_bwd_kernel with update = 1,
+// bit for bit), then the forward of step t + 1 with the updated s, alpha, z_B
+// (the arithmetic of fq_fwd_kernel, bit for bit).  Each wavefront owns 512
+// consecutive weights as in the forward: it loads dL/dWhat, W, s and the
+// code bytes once, reduces the group sums with the backward's xor
+// butterfly, writes the updated alpha and z_B of its groups to global memory
+// and to its LDS region, builds the level tables from them, maps its weights
+// and stores s, What (or the residual) and the new code bytes.  Per weight:
+// 9 B read and 7 B written, against 10 + 13 for the two passes.
+// ---------------------------------------------------------------------------
+struct StepArgs {
+  FwdArgs f;          // W, s (read), s_r, delta, z_u, alpha, z_b (read), codes, W_hat, resid
+  float* s_out;       // = s (updated in place)
+  float* alpha_out;   // = alpha
+  float* z_b_out;     // = z_b
+  const void* G;
+  float lr_f, lr_b;
+};
+
+// Per-wave LDS of the fused pass: the forward's, plus alpha' and z_B' of each group.
+__host__ __device__ inline size_t wave_step_lds_bytes(int logg, int k, bool nbt) {
+  const size_t groups = size_t(512) >> logg;
+  return wave_lds_bytes(logg, k, nbt, 1) + ((groups * (k + 1) * 4 + 15) & ~size_t(15));
+}
+
+template <int WDT, int GDT, int ODT, int MODE, int LOGL>
+__global__ __launch_bounds__(kThreads) void fq_step_kernel(StepArgs sa) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const FwdArgs& a = sa.f;
+  constexpr int L = 1 << LOGL;
+  constexpr int K = LOGL;
+  constexpr bool has_nb = MODE == 3;
+  constexpr bool keyed = LOGL <= 4;
+  const TileGeom& g = a.t;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int gw = 512 >> g.logg;
+  const int ew = gw << LOGL;
+  char* mine = smem + size_t(wave) * wave_step_lds_bytes(g.logg, LOGL, has_nb);
+  LevelTables tab;
+  char* p = carve_tables(tab, mine, ew);
+  float4* nb = reinterpret_cast<float4*>(p);
+  if (has_nb) p += 16 * size_t(ew);
+  float* s_tau = reinterpret_cast<float*>(p) + 3 * gw;  // the forward's per-group slots; only tau is used
+  uint64_t* keys = reinterpret_cast<uint64_t*>(s_tau + gw);
+  float* s_par = reinterpret_cast<float*>(mine + wave_lds_bytes(g.logg, LOGL, has_nb, 1));  // [gw][K + 1]
+  const int64_t wbase = (int64_t(blockIdx.x) * (blockDim.x >> 6) + wave) * 512;
+  if (wbase >= g.N) return;
+  const int nvalid = int(min<int64_t>(512, g.N - wbase));
+  const int gv = nvalid >> g.logg;
+  const int ev = gv << LOGL;
+  const int64_t gid0 = wbase >> g.logg;
+  const int lpg = 1 << (g.logg - 3);              // lanes per group
+  const int lo = lane * kVec;
+  const bool active = lo < nvalid;
+  const int64_t off = wbase + lo;
+  const int gl = active ? (lo >> g.logg) : 0;
+  const int64_t gid = gid0 + gl;
+
+  // loads: the chunk, then this lane's group parameters
+  Raw8<WDT> w;
+  float sv[8], G[8];
+  uint2 cb = make_uint2(0u, 0u);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) sv[i] = G[i] = 0.0f;
+  float dl = 1.0f, sr = 1.0f, zu = 0.0f, zb = 0.0f, al[K];
+#pragma unroll
+  for (int b = 0; b < K; ++b) al[b] = 0.0f;
+  if (active) {
+    w.load(a.W, off);
+    load8f(a.s, off, sv);
+    load8<GDT>(sa.G, off, G);
+    cb = load8u8(a.codes, off);
+    dl = a.delta ? a.delta[gid] : 1.0f;
+    sr = a.s_r ? a.s_r[uint32_t(gid) / uint32_t(g.gpr)] : 1.0f;
+    zu = a.z_u ? a.z_u[gid] : 0.0f;
+    zb = a.z_b[gid];
+#pragma unroll
+    for (int b = 0; b < K; ++b) al[b] = a.alpha[gid * K + b];
+  }
+  const float ds = dl * sr;
+
+  // straight-through backward and the SGD update of s (fq_bwd_kernel's order)
+  float S = 0.0f, Sa[K];
+#pragma unroll
+  for (int b = 0; b < K; ++b) Sa[b] = 0.0f;
+  float sn[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const uint32_t byte = byte_of(cb, i);
+    const bool m = (byte & 0x80u) != 0u;
+    const float gg = G[i];
+    S += gg;
+#pragma unroll
+    for (int b = 0; b < K; ++b) Sa[b] += ((byte >> b) & 1u) ? gg : -gg;
+    const float x = w.get(i) * __builtin_amdgcn_rcpf(ds * sv[i]);
+    const float gs = m ? -(dl * gg) * x * __builtin_amdgcn_rcpf(sv[i]) : 0.0f;
+    sn[i] = sv[i] - sa.lr_f * gs;
+  }
+  for (int msk = lpg >> 1; msk >= 1; msk >>= 1) {
+    S += __shfl_xor(S, msk, 64);
+#pragma unroll
+    for (int b = 0; b < K; ++b) Sa[b] += __shfl_xor(Sa[b], msk, 64);
+  }
+  // updated alpha', z_B' (every lane of a group holds the same sums); the
+  // group's first lane publishes them
+  if (active && (lane & (lpg - 1)) == 0) {
+    float* par = s_par + gl * (K + 1);
+#pragma unroll
+    for (int b = 0; b < K; ++b) {
+      const float an = al[b] - sa.lr_b * (dl * Sa[b]);
+      sa.alpha_out[gid * K + b] = an;
+      par[b] = an;
+    }
+    const float zn = zb - sa.lr_b * (dl * S);
+    sa.z_b_out[gid] = zn;
+    par[K] = zn;
+  }
+  wave_lds_sync();
+  // level tables of the wave's groups from alpha', z_B' (fq_fwd_kernel's order)
+  for (int e = lane; e < ev; e += 64) {
+    const int gg = e >> LOGL;
+    const float* par = s_par + gg * (K + 1);
+    const float q = level_value_k<LOGL>(par, par[K], e & (L - 1));
+    tab.raw[e] = q;
+    if constexpr (keyed && MODE != 2) keys[e] = level_key(q, e & (L - 1));
+  }
+  for (int gg = lane; gg < gv; gg += 64) s_tau[gg] = tau_k<LOGL>(s_par + gg * (K + 1));
+  wave_lds_sync();
+  if constexpr (MODE != 2) {
+    for (int e = lane; e < ev; e += 64) {
+      const int gg = e >> LOGL;
+      const int b = e & (L - 1);
+      const float* row = tab.raw + (gg << LOGL);
+      const float q = row[b];
+      int rank = 0;
+      if constexpr (keyed) {
+        const uint64_t* krow = keys + (gg << LOGL);
+        const uint64_t kb = krow[b];
+#pragma unroll
+        for (int b2 = 0; b2 < L; ++b2) rank += krow[b2] < kb;
+      } else {
+#pragma unroll
+        for (int b2 = 0; b2 < L; ++b2) {
+          const float q2 = row[b2];
+          rank += (q2 < q) | ((q2 == q) & (b2 < b));
+        }
+      }
+      tab.qs[(gg << LOGL) + rank] = q;
+      tab.code_of[(gg << LOGL) + rank] = uint8_t(b);
+      tab.pos_of[(gg << LOGL) + b] = uint8_t(rank);
+    }
+    wave_lds_sync();
+  }
+  if (has_nb) {
+    for (int e = lane; e < ev; e += 64) {
+      const int base = e & ~(L - 1);
+      const int d = tab.pos_of[e];
+      const int l = d > 0 ? d - 1 : 0;
+      const int r = d < L - 1 ? d + 1 : L - 1;
+      const uint32_t codes = uint32_t(tab.code_of[base + l]) | (uint32_t(tab.code_of[base + d]) << 8) |
+                             (uint32_t(tab.code_of[base + r]) << 16);
+      nb[e] = make_float4(tab.qs[base + l], tab.qs[base + d], tab.qs[base + r], __uint_as_float(codes));
+    }
+    wave_lds_sync();
+  }
+  if (!active) return;
+  store8f(sa.s_out, off, sn);
+  // the next step's forward on the updated parameters
+  const float tau = s_tau[gl];
+  const float* q = tab.qs + (gl << LOGL);
+  const float* qraw = tab.raw + (gl << LOGL);
+  const float4* nbg = nb + (gl << LOGL);
+  const uint8_t* code_of = tab.code_of + (gl << LOGL);
+  float out[8];
+  uint32_t cw[2] = {0u, 0u};
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const float den = ds * sn[i];
+    const float wb = w.get(i) / den + zu;
+    float d, wt;
+    uint32_t code;
+    if constexpr (MODE == 0) {
+      const int jj = nearest_full_k<LOGL>(q, wb, d);
+      wt = q[jj];
+      code = code_of[jj];
+    } else if constexpr (MODE == 2) {
+      code = byte_of(cb, i) & uint32_t(L - 1);
+      wt = qraw[code];
+      d = fabsf(wb - wt);
+    } else {
+      const float4 e4 = nbg[byte_of(cb, i) & uint32_t(L - 1)];
+      const uint32_t cs = __float_as_uint(e4.w);
+      float bd = fabsf(wb - e4.x);
+      wt = e4.x;
+      uint32_t sh = 0;
+      const float dm = fabsf(wb - e4.y);
+      if (dm < bd) { bd = dm; wt = e4.y; sh = 8; }
+      const float dr = fabsf(wb - e4.z);
+      if (dr < bd) { bd = dr; wt = e4.z; sh = 16; }
+      d = bd;
+      code = (cs >> sh) & 0xFFu;
+    }
+    const uint32_t byte = code | (d > tau ? 0u : 0x80u);
+    cw[i >> 2] |= byte << (8 * (i & 3));
+    out[i] = dl * (wt - zu);
+    if (a.resid) out[i] = out[i] - w.get(i);
+  }
+  store8<ODT>(a.W_hat, off, out);
+  store8u8(a.codes, off, make_uint2(cw[0], cw[1]));
+}
+
+// ---------------------------------------------------------------------------
 // Fold (Theorem 1): alpha* = Delta alpha, z* = Delta (z_B - z_U); codes by
 // FULL mapping of wbar (code_src 0) or of the raw w against the folded
 // levels (code_src 1, Eq. (4) as printed).
@@ -886,6 +1099,71 @@ hipError_t launch_fq_fwd(const FqFwdLaunch& p, hipStream_t st) {
   UQ_FWD(F32, F32, 0) UQ_FWD(F32, F32, 1) UQ_FWD(F32, F32, 2)
 #undef UQ_FWD
   return hipErrorInvalidValue;
+}
+
+template <int WD, int GD, int OD, int MD, int LOGL>
+static hipError_t launch_step_l(const StepArgs& a, hipStream_t st) {
+  auto kern = fq_step_kernel<WD, GD, OD, MD, LOGL>;
+  const size_t wave_bytes = wave_step_lds_bytes(a.f.t.logg, LOGL, MD == 3);
+  const int wpb = fwd_waves_per_block(wave_bytes);
+  const size_t lds = size_t(wpb) * wave_bytes;
+  if (lds > 65536) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+    if (e != hipSuccess) return e;
+  }
+  const int64_t waves = (a.f.t.N + 511) / 512;
+  hipLaunchKernelGGL(kern, dim3(unsigned((waves + wpb - 1) / wpb)), dim3(64 * wpb), lds, st, a);
+  return hipGetLastError();
+}
+
+template <int WD, int GD, int OD, int MD>
+static hipError_t launch_step_m(const StepArgs& a, int k, hipStream_t st) {
+  switch (k) {
+    case 1: return launch_step_l<WD, GD, OD, MD, 1>(a, st);
+    case 2: return launch_step_l<WD, GD, OD, MD, 2>(a, st);
+    case 3: return launch_step_l<WD, GD, OD, MD, 3>(a, st);
+    case 4: return launch_step_l<WD, GD, OD, MD, 4>(a, st);
+    case 5: return launch_step_l<WD, GD, OD, MD, 5>(a, st);
+    case 6: return launch_step_l<WD, GD, OD, MD, 6>(a, st);
+    default: return launch_step_l<WD, GD, OD, MD, 7>(a, st);
+  }
+}
+
+template <int WD, int GD, int OD>
+static hipError_t launch_step_d(const StepArgs& a, int k, int mode, hipStream_t st) {
+  if (mode == 0) return launch_step_m<WD, GD, OD, 0>(a, k, st);
+  if (mode == 2) return launch_step_m<WD, GD, OD, 2>(a, k, st);
+  if (use_neighbour_table(a.f.t.logg, k)) return launch_step_m<WD, GD, OD, 3>(a, k, st);
+  return hipErrorNotSupported;  // LOCAL without a neighbour table: the caller runs the two passes
+}
+
+// Fused pass for g <= 512 (whose neighbour tables fit when the next mapping is
+// LOCAL); otherwise the backward with the update, then the forward.
+hipError_t launch_fq_step(const FqStepLaunch& p, hipStream_t st) {
+  const bool fused = p.g <= 512 && !(p.mode == 1 && !use_neighbour_table(__builtin_ctz(unsigned(p.g)), p.k));
+  if (fused) {
+    StepArgs a;
+    a.f.t = make_geom(p.R, p.C, p.k, p.g, 1);
+    a.f.W = p.W; a.f.s = p.s; a.f.s_r = p.s_r; a.f.delta = p.delta; a.f.z_u = p.z_u;
+    a.f.alpha = p.alpha; a.f.z_b = p.z_b; a.f.codes = p.codes; a.f.W_hat = p.W_hat; a.f.resid = p.resid;
+    a.s_out = p.s; a.alpha_out = p.alpha; a.z_b_out = p.z_b;
+    a.G = p.grad_W_hat; a.lr_f = p.lr_f; a.lr_b = p.lr_b;
+#define UQ_STEP(WD, GD, OD) \
+    if (p.w_dtype == WD && p.grad_dtype == GD && p.w_hat_dtype == OD) return launch_step_d<WD, GD, OD>(a, p.k, p.mode, st);
+    UQ_STEP(BF16, BF16, BF16) UQ_STEP(BF16, BF16, F32) UQ_STEP(BF16, F32, BF16) UQ_STEP(BF16, F32, F32)
+    UQ_STEP(F32, BF16, BF16) UQ_STEP(F32, BF16, F32) UQ_STEP(F32, F32, BF16) UQ_STEP(F32, F32, F32)
+#undef UQ_STEP
+    return hipErrorInvalidValue;
+  }
+  FqBwdLaunch b{p.R, p.C, p.k, p.g, p.W, p.w_dtype, p.s, p.s_r, p.delta, p.z_u, p.alpha, p.z_b, p.codes,
+                p.grad_W_hat, p.grad_dtype, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
+                1, p.lr_f, p.lr_b};
+  hipError_t e = launch_fq_bwd(b, st);
+  if (e != hipSuccess) return e;
+  FqFwdLaunch f{p.R, p.C, p.k, p.g, p.W, p.w_dtype, p.s, p.s_r, p.delta, p.z_u, p.alpha, p.z_b, p.mode, p.codes,
+                p.W_hat, p.w_hat_dtype, p.resid};
+  return launch_fq_fwd(f, st);
 }
 
 hipError_t launch_fold(const FoldLaunch& p, hipStream_t st) {

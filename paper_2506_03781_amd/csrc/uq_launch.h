@@ -34,6 +34,22 @@ struct FqBwdLaunch {
   float lr_f, lr_b;
 };
 
+// Straight-through backward + SGD of one step fused with the next step's
+// forward (uniquan_fq_step).
+struct FqStepLaunch {
+  int64_t R, C;
+  int k, g;
+  const void* W; int w_dtype;
+  float* s; const float* s_r; const float* delta; const float* z_u;
+  float* alpha; float* z_b;
+  uint8_t* codes;
+  const void* grad_W_hat; int grad_dtype;
+  float lr_f, lr_b;
+  int mode;
+  void* W_hat; int w_hat_dtype;
+  int resid;
+};
+
 struct FoldLaunch {
   int64_t R, C;
   int k, g;
@@ -121,6 +137,7 @@ struct BcqMatmulLaunch {
 
 hipError_t launch_fq_fwd(const FqFwdLaunch& p, hipStream_t st);
 hipError_t launch_fq_bwd(const FqBwdLaunch& p, hipStream_t st);
+hipError_t launch_fq_step(const FqStepLaunch& p, hipStream_t st);
 hipError_t launch_fold(const FoldLaunch& p, hipStream_t st);
 hipError_t launch_dequant(const DequantLaunch& p, hipStream_t st);
 hipError_t launch_greedy(const GreedyLaunch& p, hipStream_t st);

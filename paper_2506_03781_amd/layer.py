@@ -102,6 +102,14 @@ class QuantLayer:
         uq.uniquan_fq_bwd_sgd(self.R, self.C, self.k, self.g, self.W, self.s, self.s_r, self.delta,
                               self.z_u, self.alpha, self.z_b, self.codes, self.G, gs, ga, gz, lr_f, lr_b)
 
+    def fq_step(self, lr_f=0.005, lr_b=0.0005, next_mode=uq.MAP_LOCAL):
+        """End of this step and start of the next in one pass: the backward with
+        the SGD update (dL/dWhat in G, mask bits in codes), then the forward with
+        next_mode on the updated parameters (W_hat and codes for the next step)."""
+        uq.uniquan_fq_step(self.R, self.C, self.k, self.g, self.W, self.s, self.s_r, self.delta, self.z_u,
+                           self.alpha, self.z_b, self.codes, self.G, lr_f, lr_b, next_mode, self.W_hat,
+                           residual=self.residual)
+
     def sgd(self, lr_f=0.005, lr_b=0.0005):
         """Plain SGD with the paper's learning rates (Theta_F: s; Theta_B: alpha, z_B)."""
         uq.uniquan_sgd(self.s, self.grad_s, lr_f)

@@ -43,6 +43,8 @@ _SIGS = {
                         _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp], _i32),
     "uniquan_fq_bwd_sgd": ([_i64, _i64, _i32, _i32, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32,
                             _vp, _vp, _vp, _f32, _f32, _vp], _i32),
+    "uniquan_fq_step": ([_i64, _i64, _i32, _i32, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _f32, _f32,
+                         _i32, _vp, _i32, _i32, _vp], _i32),
     "uniquan_layer_target": ([_i64, _i64, _i64, _vp, _vp, _vp, _vp], _i32),
     "uniquan_transpose_bf16": ([_i64, _i64, _vp, _vp, _vp], _i32),
     "uniquan_recon_ws": ([_i64, _i64, _i64], ctypes.c_size_t),
@@ -260,6 +262,18 @@ def uniquan_fq_bwd_sgd(R, C, k, g, W, s, s_r, delta, z_u, alpha, z_b, codes, gra
         _p(z_b, Gn, _F, "z_b"), _p(codes, N, _U8, "codes"), _p(grad_W_hat, N, _W, "grad_W_hat"),
         _dt(grad_W_hat), _p(grad_s, N, _F, "grad_s"), _p(grad_alpha, Gn * k, _F, "grad_alpha"),
         _p(grad_z_b, Gn, _F, "grad_z_b"), float(lr_f), float(lr_b), _stream(stream)))
+
+
+def uniquan_fq_step(R, C, k, g, W, s, s_r, delta, z_u, alpha, z_b, codes, grad_W_hat, lr_f, lr_b, next_mode,
+                    W_hat, residual=False, stream=None):
+    """Backward + SGD of this step fused with the next step's forward (next_mode)."""
+    N, Gn = R * C, R * C // g
+    _check(lib().uniquan_fq_step(
+        R, C, k, g, _p(W, N, _W, "W"), _dt(W), _p(s, N, _F, "s"), _p(s_r, R, _F, "s_r"),
+        _p(delta, Gn, _F, "delta"), _p(z_u, Gn, _F, "z_u"), _p(alpha, Gn * k, _F, "alpha"),
+        _p(z_b, Gn, _F, "z_b"), _p(codes, N, _U8, "codes"), _p(grad_W_hat, N, _W, "grad_W_hat"),
+        _dt(grad_W_hat), float(lr_f), float(lr_b), int(next_mode), _p(W_hat, N, _W, "W_hat"), _dt(W_hat),
+        int(bool(residual)), _stream(stream)))
 
 
 def uniquan_layer_target(T, R, C, X, W, Yt, stream=None):
