@@ -162,7 +162,11 @@ def decoder_step(Xhat, Y_ref, W, g1, g2, n_seq, H, store=_ident, n_kv=None):
     go = dA.T @ f["O"]
     dOh = split_heads(store(dA @ Wf["o"]), n_seq, H)
     dP = dOh @ np.swapaxes(f["Vx"], -1, -2)
-    dS = store(f["P"] * (dP - np.sum(dP * f["P"], axis=-1, keepdims=True)))
+    # softmax backward: dS = P (dP - delta) with the row term delta_i =
+    # sum_j P_ij dP_ij written as dO_i . O_i (the same value in exact
+    # arithmetic, O = P V), evaluated from the stored O
+    delta = np.sum(dOh * split_heads(f["O"], n_seq, H), axis=-1, keepdims=True)
+    dS = store(f["P"] * (dP - delta))
     dQh = dS @ f["Kx"] / np.sqrt(d)
 
     def group_sum(x):  # per query head -> per key/value head

@@ -152,6 +152,7 @@ class DecoderBlock:
         C, I = q.C, gm.R
         n_kv = H if n_kv is None else n_kv
         assert C % H == 0 and T % n_seq == 0 and H % n_kv == 0
+        assert C // H == 128 and (T // n_seq) % 32 == 0, "the fused attention takes d = 128 and L % 32 == 0"
         self.mats, self.T, self.C, self.I, self.H, self.n_seq = mats, T, C, I, H, n_seq
         self.d, self.L = C // H, T // n_seq
         self.Hkv, self.grp = n_kv, H // n_kv
@@ -178,10 +179,11 @@ class DecoderBlock:
         self.Kh, self.Vh = e(Bkv, L, d, **b16), e(Bkv, L, d, **b16)
         self.Qt, self.dOt = e(B, d, L, **b16), e(B, d, L, **b16)
         self.Kt, self.Vt = e(Bkv, d, L, **b16), e(Bkv, d, L, **b16)
-        # dQ per query head; dK, dV per query head = grp stacked partials per key/value head
-        self.dQr, self.dKp, self.dVp = (e(B, L, d, **f32) for _ in range(3))
-        self.S, self.dP = e(B, L, L, **f32), e(B, L, L, **f32)
-        self.P, self.Pt, self.dS, self.dSt = (e(B, L, L, **b16) for _ in range(4))
+        # attention rows: max and exp-sum of the scores, the softmax backward's row term
+        self.m_att, self.l_att, self.delta = (e(B, L, **f32) for _ in range(3))
+        # dQ per query head; dK, dV per key/value head (summed over its query heads)
+        self.dQr = e(B, L, d, **f32)
+        self.dKp, self.dVp = e(Bkv, L, d, **f32), e(Bkv, L, d, **f32)
         self.Gt, self.Ut, self.Ht, self.dHt, self.dGt, self.dUt = (e(I, T, **b16) for _ in range(6))
         self.Hm, self.dG, self.dU = (e(T, I, **b16) for _ in range(3))
         self.WdT = e(I, C, **b16)
@@ -205,13 +207,8 @@ class DecoderBlock:
         uq.uniquan_rope_split(T, Hkv, d, L, self.Kf, self.Kh, rotate=True)
         uq.uniquan_rope_split(T, Hkv, d, L, self.Vb, self.Vh, rotate=False)
         uq.uniquan_transpose_bf16_batched(Bkv, L, d, self.Vh, self.Vt)
-        for g in range(grp):   # query heads at group position g against every key/value head
-            uq.uniquan_gemm_nt_batched(L, L, d, Bkv, self._q(self.Qh, g, L * d), L * d, self.Kh, L * d,
-                                       self._q(self.S, g, L * L), L * L, sc, causal=1)
-        uq.uniquan_softmax_causal(B * L, L, self.S, self.P)
-        for g in range(grp):
-            uq.uniquan_gemm_nt_batched(L, d, L, Bkv, self._q(self.P, g, L * L), L * L, self.Vt, d * L,
-                                       self._q(self.Oh, g, L * d), L * d, causal=2)
+        # causal attention with the score tiles on chip (query batch g Bkv + c uses key/value batch c)
+        uq.uniquan_attn_fwd(B, Bkv, L, d, self.Qh, self.Kh, self.Vt, sc, self.Oh, self.m_att, self.l_att)
         uq.uniquan_rope_merge(T, H, d, L, self.Oh, self.O, rotate=False, group=grp)
         uq.uniquan_gemm_nt(T, C, C, self.O, W["o"], self.A32)
         uq.uniquan_add_rmsnorm(T, C, X, self.A32, self.g2, self.R, self.Z2, self.r2)
@@ -220,11 +217,6 @@ class DecoderBlock:
         uq.uniquan_silu_mul_fwd(self.Gt, self.Ut, self.Ht)
         uq.uniquan_transpose_bf16(I, T, self.Ht, self.Hm)
         uq.uniquan_gemm_nt(T, C, I, self.Hm, W["d"], self.M32)
-
-    def _q(self, x, g, per):
-        """Batches of group position g of a query-head buffer (grp blocks of Bkv batches of `per` elements)."""
-        n = self.Bkv * per
-        return x.view(-1)[g * n:(g + 1) * n]
 
     def _sum_out(self, out):
         """out = R + M (fp32), through the residual-add path of the norm kernel."""
@@ -289,28 +281,15 @@ class DecoderBlock:
         uq.uniquan_transpose_bf16(C, C, Wh["o"], self.WoT)
         uq.uniquan_gemm_nt(T, C, C, self.dA, self.WoT, self.dO)
         Hkv, Ckv, Bkv, grp = self.Hkv, self.Ckv, self.Bkv, self.grp
-        q = self._q
         uq.uniquan_rope_split(T, H, d, L, self.dO, self.dOh, rotate=False, group=grp)
-        for g in range(grp):
-            uq.uniquan_gemm_nt_batched(L, L, d, Bkv, q(self.dOh, g, L * d), L * d, self.Vh, L * d,
-                                       q(self.dP, g, L * L), L * L, causal=1)
-        uq.uniquan_softmax_causal_bwd(B * L, L, self.dP, self.P, self.dS)
         uq.uniquan_transpose_bf16_batched(Bkv, L, d, self.Kh, self.Kt)
-        uq.uniquan_transpose_bf16_batched(B, L, L, self.dS, self.dSt)
         uq.uniquan_transpose_bf16_batched(B, L, d, self.Qh, self.Qt)
-        uq.uniquan_transpose_bf16_batched(B, L, L, self.P, self.Pt)
         uq.uniquan_transpose_bf16_batched(B, L, d, self.dOh, self.dOt)
-        for g in range(grp):
-            uq.uniquan_gemm_nt_batched(L, d, L, Bkv, q(self.dS, g, L * L), L * L, self.Kt, d * L,
-                                       q(self.dQr, g, L * d), L * d, sc, causal=2)
-            # partial g of each shared key/value head's gradient
-            uq.uniquan_gemm_nt_batched(L, d, L, Bkv, q(self.dSt, g, L * L), L * L, q(self.Qt, g, d * L), d * L,
-                                       q(self.dKp, g, L * d), L * d, sc, causal=3)
-            uq.uniquan_gemm_nt_batched(L, d, L, Bkv, q(self.Pt, g, L * L), L * L, q(self.dOt, g, d * L), d * L,
-                                       q(self.dVp, g, L * d), L * d, causal=3)
+        uq.uniquan_attn_bwd(B, Bkv, L, d, self.Qh, self.Qt, self.Kh, self.Kt, self.Vh, self.Oh, self.dOh, self.dOt,
+                            self.m_att, self.l_att, sc, self.delta, self.dQr, self.dKp, self.dVp)
         uq.uniquan_rope_merge(T, H, d, L, self.dQr, self.dQ, rotate=True, group=grp)
-        uq.uniquan_rope_merge(T, Hkv, d, L, self.dKp, self.dK, rotate=True, nsum=grp)
-        uq.uniquan_rope_merge(T, Hkv, d, L, self.dVp, self.dV, rotate=False, nsum=grp)
+        uq.uniquan_rope_merge(T, Hkv, d, L, self.dKp, self.dK, rotate=True)
+        uq.uniquan_rope_merge(T, Hkv, d, L, self.dVp, self.dV, rotate=False)
         uq.uniquan_transpose_bf16(T, C, self.Z1, self.Z1t)
         uq.uniquan_transpose_bf16(T, C, self.dQ, self.dQt)
         uq.uniquan_gemm_nt(C, C, T, self.dQt, self.Z1t, m["q"].G)

@@ -20,7 +20,7 @@ CSRC = os.path.join(HERE, "csrc")
 OBJ = os.path.join(os.path.dirname(HERE), "_build")
 LIB = os.path.join(HERE, "libuniquan.so")
 SOURCES = ["abi.hip", "fq_fwd.hip", "fq_bwd.hip", "gemm.hip", "init_unified.hip", "bcq_deploy.hip", "block_mlp.hip",
-           "block_attn.hip", "probe.hip"]
+           "block_attn.hip", "attn_fused.hip", "probe.hip"]
 
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -543,6 +543,46 @@ uq_status uniquan_sgd(int64_t n, float* theta, const float* grad, float lr, void
   return hip_status(fn, uq::launch_sgd(n, theta, grad, lr, static_cast<hipStream_t>(stream)));
 }
 
+static uq_status check_attn(const char* fn, int64_t batch, int64_t kv_batch, int L, int d) {
+  if (batch < 1 || kv_batch < 1 || batch % kv_batch != 0)
+    return fail(UQ_EINVAL, "%s: batch=%lld must be a positive multiple of kv_batch=%lld", fn, (long long)batch,
+                (long long)kv_batch);
+  if (batch > 65535) return fail(UQ_EUNSUPPORTED, "%s: batch=%lld > 65535", fn, (long long)batch);
+  if (d != 128) return fail(UQ_EUNSUPPORTED, "%s: d=%d, supported 128", fn, d);
+  if (L < 32 || L % 32 != 0) return fail(UQ_EUNSUPPORTED, "%s: L=%d must be a positive multiple of 32", fn, L);
+  if (int64_t(L) * L >= (int64_t(1) << 31)) return fail(UQ_EUNSUPPORTED, "%s: L=%d too large", fn, L);
+  return UQ_OK;
+}
+
+uq_status uniquan_attn_fwd(int64_t batch, int64_t kv_batch, int L, int d, const uint16_t* Q, const uint16_t* K,
+                           const uint16_t* Vt, float scale, uint16_t* O, float* row_max, float* row_sum,
+                           void* stream) {
+  const char* fn = "uniquan_attn_fwd";
+  if (uq_status st = check_attn(fn, batch, kv_batch, L, d)) return st;
+  REQ_PTR(Q, 16); REQ_PTR(K, 16); REQ_PTR(Vt, 16); REQ_PTR(O, 16); REQ_PTR(row_max, 4); REQ_PTR(row_sum, 4);
+  uq::AttnLaunch q{};
+  q.batch = batch; q.kv_batch = kv_batch; q.L = L; q.scale = scale;
+  q.Q = Q; q.K = K; q.Vt = Vt; q.O_out = O; q.m = row_max; q.l = row_sum;
+  return hip_status(fn, uq::launch_attn_fwd(q, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uniquan_attn_bwd(int64_t batch, int64_t kv_batch, int L, int d, const uint16_t* Q, const uint16_t* Qt,
+                           const uint16_t* K, const uint16_t* Kt, const uint16_t* V, const uint16_t* O,
+                           const uint16_t* dO, const uint16_t* dOt, const float* row_max, const float* row_sum,
+                           float scale, float* delta, float* dQ, float* dK, float* dV, void* stream) {
+  const char* fn = "uniquan_attn_bwd";
+  if (uq_status st = check_attn(fn, batch, kv_batch, L, d)) return st;
+  REQ_PTR(Q, 16); REQ_PTR(Qt, 16); REQ_PTR(K, 16); REQ_PTR(Kt, 16); REQ_PTR(V, 16); REQ_PTR(O, 16);
+  REQ_PTR(dO, 16); REQ_PTR(dOt, 16); REQ_PTR(row_max, 4); REQ_PTR(row_sum, 4); REQ_PTR(delta, 4);
+  REQ_PTR(dQ, 16); REQ_PTR(dK, 16); REQ_PTR(dV, 16);
+  uq::AttnLaunch q{};
+  q.batch = batch; q.kv_batch = kv_batch; q.L = L; q.scale = scale;
+  q.Q = Q; q.Qt = Qt; q.K = K; q.Kt = Kt; q.V = V; q.O = O; q.dO = dO; q.dOt = dOt;
+  q.m = const_cast<float*>(row_max); q.l = const_cast<float*>(row_sum); q.delta = delta;
+  q.dQ = dQ; q.dK = dK; q.dV = dV;
+  return hip_status(fn, uq::launch_attn_bwd(q, static_cast<hipStream_t>(stream)));
+}
+
 double uniquan_probe_mfma_flops(int iters) {
   return 2.0 * 32 * 32 * 16 * double(uq::PROBE_MFMA_CHAINS) * double(iters) * (4.0 * uq::PROBE_MFMA_BLOCKS);
 }

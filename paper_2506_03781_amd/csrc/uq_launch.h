@@ -120,6 +120,18 @@ struct GemmLaunch {
   int causal;  // 0, or the causal mode of square attention products (see gemm.hip)
 };
 
+// Causal attention with the score tiles on chip (attn_fused.hip), d = 128.
+struct AttnLaunch {
+  int64_t batch, kv_batch;
+  int L;
+  float scale;
+  const uint16_t* Q; const uint16_t* Qt; const uint16_t* K; const uint16_t* Kt;
+  const uint16_t* V; const uint16_t* Vt; const uint16_t* O; const uint16_t* dO; const uint16_t* dOt;
+  uint16_t* O_out; float* m; float* l; float* delta; float* dQ; float* dK; float* dV;
+};
+hipError_t launch_attn_fwd(const AttnLaunch& p, hipStream_t st);
+hipError_t launch_attn_bwd(const AttnLaunch& p, hipStream_t st);
+
 // Deployment form (bit-planes + binary16 Theta*_B) and its product.
 struct BcqPackLaunch {
   int64_t R, C;

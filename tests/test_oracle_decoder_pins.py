@@ -212,8 +212,32 @@ def pin_grouped_heads():
     assert np.allclose(D.decoder_forward(X, Wm, g1, g2, n_seq, H, n_kv=4)["Y"], b)
 
 
+def pin_softmax_row_term():
+    """DB10: the softmax backward's row term.  Without storage rounding the
+    step's delta_i = dO_i . O_i equals sum_j P_ij dP_ij (O = P V), and dS has
+    zero row sums (the softmax Jacobian annihilates constants); with the bf16
+    storage hook the two row terms differ only by the rounding of O."""
+    rs = np.random.default_rng(21)
+    n_seq, H, C, I = 2, 2, 16, 12
+    T = 2 * 5
+    X = rs.standard_normal((T, C))
+    W = {n: 0.3 * rs.standard_normal(sh) for n, sh in
+         (("q", (C, C)), ("k", (C, C)), ("v", (C, C)), ("o", (C, C)), ("g", (I, C)), ("u", (I, C)), ("d", (C, I)))}
+    g1, g2 = 1 + 0.1 * rs.standard_normal(C), 1 + 0.1 * rs.standard_normal(C)
+    Y_ref = rs.standard_normal((T, C))
+    st = D.decoder_step(X, Y_ref, W, g1, g2, n_seq, H)
+    dOh = D.split_heads(st["dR"] @ W["o"], n_seq, H)
+    dP = dOh @ np.swapaxes(st["Vx"], -1, -2)
+    delta_p = np.sum(st["P"] * dP, axis=-1)
+    delta_o = np.sum(dOh * D.split_heads(st["O"], n_seq, H), axis=-1)
+    assert np.allclose(delta_o, delta_p, rtol=1e-12, atol=1e-12)
+    assert np.allclose(st["dS"].sum(-1), 0.0, atol=1e-12)
+    # the step's dS is P (dP - delta) with that row term
+    assert np.allclose(st["dS"], st["P"] * (dP - delta_p[..., None]), rtol=1e-12, atol=1e-12)
+
+
 PINS = [pin_rmsnorm, pin_rope, pin_causal_softmax, pin_forward_loops, pin_gradients_finite_differences,
-        pin_zero_loss, pin_store_hook, pin_reduces_to_mlp, pin_grouped_heads]
+        pin_zero_loss, pin_store_hook, pin_reduces_to_mlp, pin_grouped_heads, pin_softmax_row_term]
 
 
 @pytest.mark.parametrize("pin", PINS, ids=[p.__name__ for p in PINS])
