@@ -504,37 +504,39 @@ uq_status uniquan_softmax_causal_bwd(int64_t rows, int L, const float* dP,
 
 /*
  * uniquan_attn_fwd / uniquan_attn_bwd -- the block's causal attention with
- * the [L, L] score tiles kept on chip (none is written to memory).  Per
- * sequence and query head b < batch, with key/value head b mod kv_batch
- * (the grouped slot order of uniquan_rope_split: query batch
- * g kv_batch + c pairs with key/value batch c), head dimension d = 128:
- *   S = Q K^T scale, P = bf16(causal row softmax of S) (rows i over j <= i),
- *   O = bf16(P V);
- * the forward also writes each row's maximum m of S and sum l of exp(S - m),
- * so that the backward recomputes the same P.  Backward:
- *   dP = dO V^T (fp32), delta_i = dO_i . O_i (fp32; equal to
- *   sum_j P_ij dP_ij in exact arithmetic), dS = bf16(P (dP - delta)),
- *   dQ = dS K scale, dK = dS^T Q scale, dV = P^T dO  (fp32 out),
- * dK and dV summed over the query heads sharing a key/value head in head
- * order.  The rounding points are those of the unfused path (P and dS in
- * bf16, S and dP in fp32).
- * Layouts (bf16 unless stated): Q, O, dO [batch, L, d]; Qt, dOt
- * [batch, d, L]; K, V [kv_batch, L, d]; Kt, Vt [kv_batch, d, L] (the
- * transposes, e.g. from uniquan_transpose_bf16_batched); row_max, row_sum,
- * delta [batch, L] fp32 (delta written by uniquan_attn_bwd); dQ [batch, L, d],
- * dK, dV [kv_batch, L, d] fp32 out.  d = 128 and L a multiple of 32
- * (UQ_EUNSUPPORTED otherwise); batch a multiple of kv_batch, at most 65535.
+ * the [L, L] score tiles kept on chip (none is written to memory); the
+ * attention of the Transformer block that Algorithm 1 reconstructs (appendix
+ * "Units in LLMs").  Per sequence and query head b < batch, with key/value
+ * head b mod kv_batch (the grouped slot order of uniquan_rope_split: query
+ * batch g kv_batch + c pairs with key/value batch c), head dimension d = 128
+ * and c = scale log2(e):
+ *   S = Q K^T, row_lse_i = log2 sum_{j <= i} 2^(c S_ij) (the base-2
+ *   log-sum-exp of the scaled scores), P = bf16(2^(c S - row_lse)) (the causal
+ *   row softmax of S scale), O = bf16(P V).
+ * Backward, recomputing the same P from row_lse:
+ *   dP = dO V^T (fp32), delta_i = dO_i . O_i (fp32; equal to sum_j P_ij dP_ij
+ *   in exact arithmetic), dS = bf16(P (dP - delta)), dQ = dS K scale, and per
+ *   query head b the contributions dK_b = dS^T Q scale, dV_b = P^T dO (fp32
+ *   out); the gradient of a key/value head shared by several query heads is
+ *   the sum of their contributions (uniquan_rope_merge with nsum sums them).
+ * The rounding points are those of the unfused path (P and dS in bf16, S and
+ * dP in fp32).
+ * Layouts (bf16 unless stated): Q, O, dO [batch, L, d]; Qt, dOt [batch, d, L];
+ * K, V [kv_batch, L, d]; Kt, Vt [kv_batch, d, L] (the transposes, e.g. from
+ * uniquan_transpose_bf16_batched); row_lse, delta [batch, L] fp32 (delta
+ * written by uniquan_attn_bwd); dQ, dK, dV [batch, L, d] fp32 out.  d = 128
+ * and L a multiple of 32 (UQ_EUNSUPPORTED otherwise); batch a positive
+ * multiple of kv_batch, at most 65535; every pointer 16-byte aligned.
  */
 uq_status uniquan_attn_fwd(int64_t batch, int64_t kv_batch, int L, int d,
                            const uint16_t* Q, const uint16_t* K, const uint16_t* Vt,
-                           float scale, uint16_t* O, float* row_max, float* row_sum,
-                           void* stream);
+                           float scale, uint16_t* O, float* row_lse, void* stream);
 uq_status uniquan_attn_bwd(int64_t batch, int64_t kv_batch, int L, int d,
                            const uint16_t* Q, const uint16_t* Qt, const uint16_t* K,
                            const uint16_t* Kt, const uint16_t* V, const uint16_t* O,
-                           const uint16_t* dO, const uint16_t* dOt,
-                           const float* row_max, const float* row_sum, float scale,
-                           float* delta, float* dQ, float* dK, float* dV, void* stream);
+                           const uint16_t* dO, const uint16_t* dOt, const float* row_lse,
+                           float scale, float* delta, float* dQ, float* dK, float* dV,
+                           void* stream);
 
 /*
  * uniquan_transpose_bf16_batched -- out_b = in_b^T for batch matrices

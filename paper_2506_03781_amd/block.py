@@ -179,11 +179,10 @@ class DecoderBlock:
         self.Kh, self.Vh = e(Bkv, L, d, **b16), e(Bkv, L, d, **b16)
         self.Qt, self.dOt = e(B, d, L, **b16), e(B, d, L, **b16)
         self.Kt, self.Vt = e(Bkv, d, L, **b16), e(Bkv, d, L, **b16)
-        # attention rows: max and exp-sum of the scores, the softmax backward's row term
-        self.m_att, self.l_att, self.delta = (e(B, L, **f32) for _ in range(3))
-        # dQ per query head; dK, dV per key/value head (summed over its query heads)
-        self.dQr = e(B, L, d, **f32)
-        self.dKp, self.dVp = e(Bkv, L, d, **f32), e(Bkv, L, d, **f32)
+        # attention rows: base-2 log-sum-exp of the scores, the softmax backward's row term
+        self.lse, self.delta = e(B, L, **f32), e(B, L, **f32)
+        # dQ per query head; dK, dV contributions per query head (summed per key/value head)
+        self.dQr, self.dKp, self.dVp = (e(B, L, d, **f32) for _ in range(3))
         self.Gt, self.Ut, self.Ht, self.dHt, self.dGt, self.dUt = (e(I, T, **b16) for _ in range(6))
         self.Hm, self.dG, self.dU = (e(T, I, **b16) for _ in range(3))
         self.WdT = e(I, C, **b16)
@@ -208,7 +207,7 @@ class DecoderBlock:
         uq.uniquan_rope_split(T, Hkv, d, L, self.Vb, self.Vh, rotate=False)
         uq.uniquan_transpose_bf16_batched(Bkv, L, d, self.Vh, self.Vt)
         # causal attention with the score tiles on chip (query batch g Bkv + c uses key/value batch c)
-        uq.uniquan_attn_fwd(B, Bkv, L, d, self.Qh, self.Kh, self.Vt, sc, self.Oh, self.m_att, self.l_att)
+        uq.uniquan_attn_fwd(B, Bkv, L, d, self.Qh, self.Kh, self.Vt, sc, self.Oh, self.lse)
         uq.uniquan_rope_merge(T, H, d, L, self.Oh, self.O, rotate=False, group=grp)
         uq.uniquan_gemm_nt(T, C, C, self.O, W["o"], self.A32)
         uq.uniquan_add_rmsnorm(T, C, X, self.A32, self.g2, self.R, self.Z2, self.r2)
@@ -286,10 +285,10 @@ class DecoderBlock:
         uq.uniquan_transpose_bf16_batched(B, L, d, self.Qh, self.Qt)
         uq.uniquan_transpose_bf16_batched(B, L, d, self.dOh, self.dOt)
         uq.uniquan_attn_bwd(B, Bkv, L, d, self.Qh, self.Qt, self.Kh, self.Kt, self.Vh, self.Oh, self.dOh, self.dOt,
-                            self.m_att, self.l_att, sc, self.delta, self.dQr, self.dKp, self.dVp)
+                            self.lse, sc, self.delta, self.dQr, self.dKp, self.dVp)
         uq.uniquan_rope_merge(T, H, d, L, self.dQr, self.dQ, rotate=True, group=grp)
-        uq.uniquan_rope_merge(T, Hkv, d, L, self.dKp, self.dK, rotate=True)
-        uq.uniquan_rope_merge(T, Hkv, d, L, self.dVp, self.dV, rotate=False)
+        uq.uniquan_rope_merge(T, Hkv, d, L, self.dKp, self.dK, rotate=True, nsum=grp)
+        uq.uniquan_rope_merge(T, Hkv, d, L, self.dVp, self.dV, rotate=False, nsum=grp)
         uq.uniquan_transpose_bf16(T, C, self.Z1, self.Z1t)
         uq.uniquan_transpose_bf16(T, C, self.dQ, self.dQt)
         uq.uniquan_gemm_nt(C, C, T, self.dQt, self.Z1t, m["q"].G)

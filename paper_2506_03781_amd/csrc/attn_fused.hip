@@ -2,29 +2,38 @@
 // Transformer block; appendix "Units in LLMs") with the score tiles kept on
 // chip: no [L, L] score, probability or gradient array is written.
 //
-// Per sequence and query head b (key/value head b mod kv_batch), d = 128:
-//   S = Q K^T * scale (fp32), P = bf16(softmax over keys j <= i of S),
+// Per sequence and query head b (key/value head b mod kv_batch), d = 128,
+// with c = scale * log2(e):
+//   S = Q K^T (fp32), lse_i = log2 sum_{j <= i} 2^(c S_ij) (base-2 log-sum-exp
+//   of the scaled scores), P = bf16(2^(c S - lse)) (the causal row softmax),
 //   O = bf16(P V) (fp32 accumulation);
 //   backward with dP = dO V^T (fp32), delta_i = dO_i . O_i (fp32, from the
 //   stored bf16 O and dO; equal to sum_j P_ij dP_ij in exact arithmetic),
-//   dS = bf16(P (dP - delta)), dQ = dS K * scale, dK = dS^T Q * scale,
-//   dV = P^T dO (fp32 out; the key/value gradients summed over the query heads
-//   that share the head, in head order).
+//   dS = bf16(P (dP - delta)), dQ = dS K * scale, and per query head the
+//   contributions dK_b = dS^T Q * scale, dV_b = P^T dO (fp32 out; the
+//   gradient of a shared key/value head is the sum of its query heads').
 // These are the rounding points of the unfused path (P and dS stored in
 // bf16, S and dP in fp32).  The forward runs two passes over the keys: the
-// first finds each row's maximum m and sum l of exp(S - m), the second forms
-// P = exp(S - m) / l exactly as the row softmax does and accumulates P V; m
-// and l are kept so that the backward recomputes the same P bit for bit.
+// first finds each row's maximum and exp-sum (online, per lane, then the two
+// half-waves of a query combined) and so lse; the second forms P from lse and
+// accumulates P V.  The backward recomputes the same P from the stored lse.
 //
 // MFMA layout (v_mfma_f32_32x32x16_bf16, C[m][n] += A[m][k] B[n][k]): lane l
 // supplies row l % 32 of A and of B with k = 8 (l / 32) .. + 8, and holds
 // C rows 8 (r / 4) + 4 (l / 32) + r % 4, r < 16, of column l % 32.  A score
-// tile is computed transposed (keys as rows) where its columns must be
-// queries, so a lane's 16 accumulator values are one query's scores for 16
-// keys; those values then serve directly as the B operand of the next
-// product, with the keys (its k dimension) in the permuted order
-// kperm(i) = {0, 1, 2, 3, 8, 9, 10, 11}[i] (+4 in the upper half-wave), and
-// the A operand of that product is read with the same permutation.
+// tile is computed with the 32 rows of its key (or query) tile as M, read
+// from LDS in the order perm32 (bits 2 and 3 of the row index swapped): then
+// accumulator slot r of lane l belongs to tile row 16 (r / 8) + 8 (l / 32) +
+// r % 8, so the 8 values of each half (slots 8 h .. 8 h + 7) are 8
+// consecutive rows and serve directly as the B operand of the next product
+// (contraction over those rows), whose A operand is one 16-byte LDS read of
+// a transposed tile.
+//
+// Tiles (32 rows of 128 bf16, or 128 rows of 32 bf16 for the transposed
+// ones) go straight from global memory into a ring of S LDS stages
+// (global_load_lds, 16 bytes per lane, S - 1 tiles ahead); each wave waits
+// for its own copies with an exact vmcnt before the workgroup barrier that
+// precedes the reads, and the barrier also orders the reuse of a stage.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -38,83 +47,91 @@ typedef __bf16 bf16x8a __attribute__((ext_vector_type(8)));
 typedef float f32x16a __attribute__((ext_vector_type(16)));
 typedef unsigned int u32x4a __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2a __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) void lds_void_a;
+typedef const __attribute__((address_space(1))) void glb_void_a;
 
-constexpr int D = 128;      // head dimension
-constexpr int NB = 32;      // keys (or queries) per tile
+constexpr int D = 128;                       // head dimension
+constexpr int NB = 32;                       // rows (keys or queries) per tile
+constexpr int TILE16 = NB * D * 2 / 16;      // 16-byte slots of a tile (512)
+constexpr float LOG2E = 1.44269504088896341f;
 
 __device__ __forceinline__ f32x16a mfma(const bf16x8a& a, const bf16x8a& b, const f32x16a& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
-__device__ __forceinline__ uint32_t bf16_bits(float x) {  // round to nearest even
-  const uint32_t u = __float_as_uint(x);
-  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+__device__ __forceinline__ float exp2a(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// bf16 value nearest to x (ties to even), as fp32.
+__device__ __forceinline__ float bf16_round(float x) { return float(__bf16(x)); }
+
+// Tile row held by accumulator slot r of this lane (rows read in perm32 order).
+__device__ __forceinline__ int slot_row(int r, int lane) { return 16 * (r >> 3) + 8 * (lane >> 5) + (r & 7); }
+
+// Swap bits 2 and 3 of a row index below 32 (an involution).
+__device__ __forceinline__ int perm32(int r) { return (r & 19) | ((r & 4) << 1) | ((r >> 1) & 4); }
+
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  // s_waitcnt fields: vmcnt[3:0] and [15:14], expcnt[6:4], lgkmcnt[11:8]
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
-__device__ __forceinline__ float bf16_round(float x) { return __uint_as_float(bf16_bits(x) << 16); }
+// Wait until at most `ahead` (0..2) later tiles of PW copies each are in flight.
+template <int PW>
+__device__ __forceinline__ void wait_tiles(int ahead) {
+  if (ahead >= 2) vm_wait<2 * PW>();
+  else if (ahead == 1) vm_wait<PW>();
+  else vm_wait<0>();
+}
 
-// Row of the accumulator held in slot r by lane l.
-__device__ __forceinline__ int acc_row(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
+__device__ __forceinline__ void lds_wait_barrier() {
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's LDS reads are done
+  __builtin_amdgcn_s_barrier();
+}
 
-// Row-major tile [32 rows][128] bf16 in LDS: 16-byte chunk c of row r at
-// r * 16 + (c ^ (r & 15)), so the 32 rows a fragment read touches at one
-// chunk fall in distinct bank groups.
-struct RowTile {
-  u32x4a* p;
-  __device__ __forceinline__ void load(const uint16_t* __restrict__ src, int64_t ld, int row0, int rows_valid) {
-    // 512 chunks: two per lane of the workgroup
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int t = threadIdx.x + h * 256;
-      const int r = t >> 4, c = t & 15;
-      u32x4a v = {0u, 0u, 0u, 0u};
-      if (r < rows_valid) v = *reinterpret_cast<const u32x4a*>(src + int64_t(row0 + r) * ld + c * 8);
-      p[r * 16 + (c ^ (r & 15))] = v;
-    }
-  }
-  // A or B fragment of k-step j for this lane: row (lane % 32), d = 16 j + 8 (lane / 32)
-  __device__ __forceinline__ bf16x8a frag(int j, int lane) const {
-    const int r = lane & 31, c = 2 * j + (lane >> 5);
-    return __builtin_bit_cast(bf16x8a, p[r * 16 + (c ^ (r & 15))]);
-  }
-};
+// Row tile (32 rows of 128 bf16 = 512 slots of 16 bytes): slot s holds chunk
+// (s % 16) ^ (rho % 16) of tile row rho = s / 16, and tile row rho holds
+// source row perm32(rho) of the tile.  Copy block blk fills slots 64 blk ..
+// + 64; row_off is this lane's byte offset in the source tile for block blk.
+__device__ __forceinline__ uint32_t row_off(int blk, int lane) {
+  const int s = blk * 64 + lane;
+  const int rho = s >> 4, c = (s & 15) ^ (rho & 15);
+  return uint32_t(perm32(rho) * D * 2 + c * 16);
+}
 
-// Transposed tile [128 rows (d)][32 columns] bf16 in LDS from a [d][L]
-// source: 8-byte unit u of row d at d * 8 + (u ^ ((d >> 2) & 7)).
-struct ColTile {
-  u32x2a* p;
-  __device__ __forceinline__ void load(const uint16_t* __restrict__ src, int64_t ld, int col0) {
-    // 128 rows x 4 pieces of 16 B: two per lane
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int t = threadIdx.x + h * 256;
-      const int d = t >> 2, q = t & 3;
-      const u32x4a v = *reinterpret_cast<const u32x4a*>(src + int64_t(d) * ld + col0 + q * 8);
-      const int sw = (d >> 2) & 7;
-      p[d * 8 + ((2 * q) ^ sw)] = u32x2a{v.x, v.y};
-      p[d * 8 + ((2 * q + 1) ^ sw)] = u32x2a{v.z, v.w};
-    }
-  }
-  // A fragment for the product over the tile's 32 columns, half h (16
-  // columns), rows 32 db .. + 32: lane supplies row 32 db + lane % 32 and the
-  // columns kperm: 16 h + 4 (lane / 32) + {0..3} and + 8 + {0..3}.
-  __device__ __forceinline__ bf16x8a frag(int db, int h, int lane) const {
-    const int d = 32 * db + (lane & 31);
-    const int sw = (d >> 2) & 7;
-    const int u1 = 4 * h + (lane >> 5), u2 = u1 + 2;
-    const u32x2a a = p[d * 8 + (u1 ^ sw)], b = p[d * 8 + (u2 ^ sw)];
-    return __builtin_bit_cast(bf16x8a, u32x4a{a.x, a.y, b.x, b.y});
-  }
-};
+// A copy of 64 slots: lane l's 16 bytes at base + off land in slot l of dst.
+__device__ __forceinline__ void copy16(const void* base, uint32_t off, u32x4a* dst) {
+  __builtin_amdgcn_global_load_lds((glb_void_a*)(static_cast<const char*>(base) + off), (lds_void_a*)dst, 16, 0, 0);
+}
 
-// The 8 accumulator values of half h (slots 8 h .. 8 h + 7) as a bf16 B
-// operand (values already rounded or to be rounded here).
+// A or B fragment of k-step j (d = 16 j + 8 (lane / 32) .. + 8) of tile row lane % 32.
+__device__ __forceinline__ bf16x8a row_frag(const u32x4a* tile, int j, int lane) {
+  const int rho = lane & 31, c = 2 * j + (lane >> 5);
+  return __builtin_bit_cast(bf16x8a, tile[rho * 16 + (c ^ (rho & 15))]);
+}
+
+// Transposed tile (128 rows d of 32 bf16 columns from a [D][ld] source, 4
+// pieces of 8 columns per row): slot s holds piece (s % 4) ^ ((d / 2) % 4) of
+// row d = s / 4; col_off is this lane's byte offset for copy block blk.
+__device__ __forceinline__ uint32_t col_off(int blk, int lane, int ld) {
+  const int s = blk * 64 + lane;
+  const int d = s >> 2, p = (s & 3) ^ ((d >> 1) & 3);
+  return uint32_t(d) * uint32_t(ld) * 2u + uint32_t(p * 16);
+}
+
+// A fragment of rows 32 db .. + 32 over the 16 columns of half h: lane
+// supplies row 32 db + lane % 32 and columns 16 h + 8 (lane / 32) .. + 8.
+__device__ __forceinline__ bf16x8a col_frag(const u32x4a* tile, int db, int h, int lane) {
+  const int d = 32 * db + (lane & 31), p = 2 * h + (lane >> 5);
+  return __builtin_bit_cast(bf16x8a, tile[d * 4 + (p ^ ((d >> 1) & 3))]);
+}
+
+// Slots 8 h .. 8 h + 7 as a bf16 B operand.
 __device__ __forceinline__ bf16x8a pack_half(const float (&v)[16], int h) {
-  u32x4a w;
+  bf16x8a w;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-    w[i] = bf16_bits(v[8 * h + 2 * i]) | (bf16_bits(v[8 * h + 2 * i + 1]) << 16);
-  return __builtin_bit_cast(bf16x8a, w);
+  for (int i = 0; i < 8; ++i) w[i] = __bf16(v[8 * h + i]);
+  return w;
 }
 
 __device__ __forceinline__ f32x16a zero16() {
@@ -122,6 +139,35 @@ __device__ __forceinline__ f32x16a zero16() {
 #pragma unroll
   for (int r = 0; r < 16; ++r) z[r] = 0.0f;
   return z;
+}
+
+// 16 fp32 accumulator values of 32 rows db (4 per row group) at this lane's
+// column: store rows 32 db + 8 g4 + 4 (lane / 32) .. + 4 of column `row`.
+__device__ __forceinline__ void store_f32_rows(float* out, const f32x16a (&acc)[4], float mul, int lane) {
+#pragma unroll
+  for (int db = 0; db < 4; ++db)
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4) {
+      const int d0 = 32 * db + 8 * g4 + 4 * (lane >> 5);
+      *reinterpret_cast<float4*>(out + d0) = make_float4(acc[db][4 * g4] * mul, acc[db][4 * g4 + 1] * mul,
+                                                         acc[db][4 * g4 + 2] * mul, acc[db][4 * g4 + 3] * mul);
+    }
+}
+
+// Workgroup -> (row block, batch).  When the batch count is a multiple of 8
+// the row blocks of one batch go to one XCD (workgroups are dealt to the 8
+// XCDs round-robin), so its keys and values stay in that XCD's L2; within a
+// batch the blocks with the most work come first.
+__device__ __forceinline__ void block_of(int nblk, int64_t batch, int& blk, int64_t& b) {
+  const int64_t w = blockIdx.x;
+  if ((batch & 7) == 0) {
+    const int64_t y = w >> 3;
+    b = (w & 7) + 8 * (y / nblk);
+    blk = nblk - 1 - int(y % nblk);
+  } else {
+    b = w / nblk;
+    blk = nblk - 1 - int(w % nblk);
+  }
 }
 
 }  // namespace
@@ -140,138 +186,195 @@ struct AttnArgs {
   const uint16_t* dO;   // [batch, L, D]
   const uint16_t* dOt;  // [batch, D, L]
   uint16_t* O_out;      // [batch, L, D]
-  float* m;             // [batch, L] row maximum of S
-  float* l;             // [batch, L] row sum of exp(S - m)
+  float* lse;           // [batch, L] base-2 log-sum-exp of the scaled scores
   float* delta;         // [batch, L]
   float* dQ;            // [batch, L, D]
-  float* dK;            // [kv_batch, L, D]
-  float* dV;            // [kv_batch, L, D]
+  float* dK;            // [batch, L, D] per query head
+  float* dV;            // [batch, L, D] per query head
 };
 
-// Forward: one workgroup per (128 queries, query batch); wave w owns queries
-// q0 = 128 blockIdx.x + 32 w .. + 32 and loops over the key tiles up to its
-// diagonal (the workgroup's tiles are loaded cooperatively).
-__global__ __launch_bounds__(256) void attn_fwd_kernel(AttnArgs a) {
-  __shared__ u32x4a sK[NB * 16];
-  __shared__ u32x2a sVt[D * 8];
-  RowTile tK{sK};
-  ColTile tV{sVt};
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int64_t b = blockIdx.y, bk = b % a.kv_batch;
+// Copies of one tile: PW blocks of 64 slots per wave (blocks wave PW .. + PW).
+template <int PW>
+__device__ __forceinline__ void copy_tile(const uint16_t* base, const uint32_t (&off)[PW], u32x4a* tile, int wave) {
+#pragma unroll
+  for (int q = 0; q < PW; ++q) copy16(base, off[q], tile + (wave * PW + q) * 64);
+}
+
+// Forward: one workgroup of NW waves per (NW * 32 queries, query batch); wave
+// w owns 32 queries and multiplies the key tiles up to its diagonal (the
+// workgroup copies the tiles up to its last diagonal).
+template <int NW, int S>
+__global__ __launch_bounds__(NW * 64) void attn_fwd_kernel(AttnArgs a) {
+  constexpr int QB = NW * NB;
+  constexpr int PW = 8 / NW;  // copy blocks per wave and tile
+  constexpr int STAGE = 2 * TILE16;  // key tile, transposed value tile
+  __shared__ u32x4a smem[S * STAGE];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
   const int L = a.L;
-  const int q0 = blockIdx.x * 128 + wave * NB;
+  int qb;
+  int64_t b;
+  block_of((L + QB - 1) / QB, a.batch, qb, b);
+  const int64_t bk = b % a.kv_batch;
+  const int q0 = qb * QB + wave * NB;
   const bool active = q0 < L;
   const int qi = q0 + (lane & 31);  // this lane's query
-  const int n_tiles = min(L, int(blockIdx.x) * 128 + 128) / NB;  // key tiles the workgroup needs
+  const int n_tiles = min(L, qb * QB + QB) / NB;
   const int my_tiles = active ? q0 / NB + 1 : 0;
   const uint16_t* Kb = a.K + bk * int64_t(L) * D;
   const uint16_t* Vtb = a.Vt + bk * int64_t(D) * L;
-  // this lane's query row as B fragments
+  const float c = a.scale * LOG2E;
+  uint32_t ro[PW], co[PW];
+#pragma unroll
+  for (int q = 0; q < PW; ++q) {
+    ro[q] = row_off(wave * PW + q, lane);
+    co[q] = col_off(wave * PW + q, lane, L);
+  }
   bf16x8a qf[8];
   {
     const uint16_t* qrow = a.Q + (b * L + min(qi, L - 1)) * int64_t(D) + 8 * (lane >> 5);
 #pragma unroll
     for (int j = 0; j < 8; ++j) qf[j] = __builtin_bit_cast(bf16x8a, *reinterpret_cast<const u32x4a*>(qrow + 16 * j));
   }
-  // pass 1: row maximum and sum (per half-wave: 16 of each tile's 32 keys)
+  // pass 1: running maximum m (of c S) and sum l of 2^(c S - m) over this lane's keys
   float m = -INFINITY, l = 0.0f;
+#pragma unroll
+  for (int t = 0; t < S - 1; ++t)
+    if (t < n_tiles) copy_tile<PW>(Kb + int64_t(t) * NB * D, ro, smem + (t % S) * STAGE, wave);
   for (int t = 0; t < n_tiles; ++t) {
-    __syncthreads();
-    tK.load(Kb, D, t * NB, NB);
-    __syncthreads();
+    wait_tiles<PW>(min(S - 2, n_tiles - 1 - t));
+    lds_wait_barrier();
+    if (t + S - 1 < n_tiles) {
+      const int u = t + S - 1;
+      copy_tile<PW>(Kb + int64_t(u) * NB * D, ro, smem + (u % S) * STAGE, wave);
+    }
     if (t >= my_tiles) continue;
+    const u32x4a* tk = smem + (t % S) * STAGE;
+    bf16x8a kf[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) kf[j] = row_frag(tk, j, lane);
     f32x16a s = zero16();
 #pragma unroll
-    for (int j = 0; j < 8; ++j) s = mfma(tK.frag(j, lane), qf[j], s);
-    float mt = m;
+    for (int j = 0; j < 8; ++j) s = mfma(kf[j], qf[j], s);
+    if (t == my_tiles - 1) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int key = t * NB + acc_row(r, lane);
-      if (key <= qi) mt = fmaxf(mt, s[r] * a.scale);
+      for (int r = 0; r < 16; ++r)
+        if (t * NB + slot_row(r, lane) > qi) s[r] = -INFINITY;
     }
+    float mx = s[0];
+#pragma unroll
+    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s[r]);
+    const float mt = fmaxf(m, mx * c);
+    const float ms = mt == -INFINITY ? 0.0f : mt;
     float sum = 0.0f;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int key = t * NB + acc_row(r, lane);
-      if (key <= qi) sum += expf(s[r] * a.scale - mt);
-    }
-    l = (m == -INFINITY ? 0.0f : l * expf(m - mt)) + sum;
+    for (int r = 0; r < 16; ++r) sum += exp2a(fmaf(s[r], c, -ms));
+    l = l * exp2a(m - ms) + sum;
     m = mt;
   }
-  // combine the two half-waves of each query (fixed order: lower half first)
+  // the two half-waves of a query (lower half first) -> lse
+  float lse;
   {
     const float m2 = __shfl_xor(m, 32, 64), l2 = __shfl_xor(l, 32, 64);
     const float mlo = (lane < 32) ? m : m2, llo = (lane < 32) ? l : l2;
     const float mhi = (lane < 32) ? m2 : m, lhi = (lane < 32) ? l2 : l;
     const float mm = fmaxf(mlo, mhi);
-    const float a0 = mlo == -INFINITY ? 0.0f : llo * expf(mlo - mm);
-    const float a1 = mhi == -INFINITY ? 0.0f : lhi * expf(mhi - mm);
-    m = mm;
-    l = a0 + a1;
+    const float ms = mm == -INFINITY ? 0.0f : mm;
+    const float lt = llo * exp2a(mlo - ms) + lhi * exp2a(mhi - ms);
+    lse = mm + __builtin_amdgcn_logf(lt);  // log2
   }
-  const float inv = 1.0f / l;
-  // pass 2: P = bf16(exp(S - m) / l), O += P V
+  lds_wait_barrier();  // every wave is past pass 1's reads before the stages are refilled
+  // pass 2: P = bf16(2^(c S - lse)), O += P V
   f32x16a o[4] = {zero16(), zero16(), zero16(), zero16()};
+#pragma unroll
+  for (int t = 0; t < S - 1; ++t)
+    if (t < n_tiles) {
+      copy_tile<PW>(Kb + int64_t(t) * NB * D, ro, smem + (t % S) * STAGE, wave);
+      copy_tile<PW>(Vtb + int64_t(t) * NB, co, smem + (t % S) * STAGE + TILE16, wave);
+    }
   for (int t = 0; t < n_tiles; ++t) {
-    __syncthreads();
-    tK.load(Kb, D, t * NB, NB);
-    tV.load(Vtb, L, t * NB);
-    __syncthreads();
+    wait_tiles<2 * PW>(min(S - 2, n_tiles - 1 - t));
+    lds_wait_barrier();
+    if (t + S - 1 < n_tiles) {
+      const int u = t + S - 1;
+      copy_tile<PW>(Kb + int64_t(u) * NB * D, ro, smem + (u % S) * STAGE, wave);
+      copy_tile<PW>(Vtb + int64_t(u) * NB, co, smem + (u % S) * STAGE + TILE16, wave);
+    }
     if (t >= my_tiles) continue;
+    const u32x4a* tk = smem + (t % S) * STAGE;
+    const u32x4a* tv = tk + TILE16;
+    bf16x8a kf[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) kf[j] = row_frag(tk, j, lane);
     f32x16a s = zero16();
 #pragma unroll
-    for (int j = 0; j < 8; ++j) s = mfma(tK.frag(j, lane), qf[j], s);
+    for (int j = 0; j < 8; ++j) s = mfma(kf[j], qf[j], s);
+    bf16x8a vf[8];  // read while P is formed
+#pragma unroll
+    for (int i = 0; i < 8; ++i) vf[i] = col_frag(tv, i & 3, i >> 2, lane);
     float p[16];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int key = t * NB + acc_row(r, lane);
-      p[r] = key <= qi ? expf(s[r] * a.scale - m) * inv : 0.0f;
+    for (int r = 0; r < 16; ++r) p[r] = exp2a(fmaf(s[r], c, -lse));
+    if (t == my_tiles - 1) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        if (t * NB + slot_row(r, lane) > qi) p[r] = 0.0f;
     }
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const bf16x8a pb = pack_half(p, h);
 #pragma unroll
-      for (int db = 0; db < 4; ++db) o[db] = mfma(tV.frag(db, h, lane), pb, o[db]);
+      for (int db = 0; db < 4; ++db) o[db] = mfma(vf[4 * h + db], pb, o[db]);
     }
   }
-  if (!active || qi >= L) return;
+  if (!active) return;
   uint16_t* orow = a.O_out + (b * L + qi) * int64_t(D);
 #pragma unroll
   for (int db = 0; db < 4; ++db)
 #pragma unroll
     for (int g4 = 0; g4 < 4; ++g4) {
       const int d0 = 32 * db + 8 * g4 + 4 * (lane >> 5);
-      const uint32_t w0 = bf16_bits(o[db][4 * g4]) | (bf16_bits(o[db][4 * g4 + 1]) << 16);
-      const uint32_t w1 = bf16_bits(o[db][4 * g4 + 2]) | (bf16_bits(o[db][4 * g4 + 3]) << 16);
-      *reinterpret_cast<u32x2a*>(orow + d0) = u32x2a{w0, w1};
+      bf16x8a w;  // only the first four are stored
+#pragma unroll
+      for (int i = 0; i < 8; ++i) w[i] = __bf16(o[db][4 * g4 + (i & 3)]);
+      const u32x4a u = __builtin_bit_cast(u32x4a, w);
+      *reinterpret_cast<u32x2a*>(orow + d0) = u32x2a{u.x, u.y};
     }
-  if (lane < 32) {
-    a.m[b * L + qi] = m;
-    a.l[b * L + qi] = l;
-  }
+  if (lane < 32) a.lse[b * L + qi] = lse;
 }
 
-// Backward for the queries: delta = dO . O per row (written for the key
-// kernel), then per key tile S -> P (the forward's m, l), dP = dO V^T,
-// dS = bf16(P (dP - delta)), dQ += dS K; dQ * scale stored in fp32.
-__global__ __launch_bounds__(256) void attn_bwd_dq_kernel(AttnArgs a) {
-  __shared__ u32x4a sK[NB * 16];
-  __shared__ u32x4a sV[NB * 16];
-  __shared__ u32x2a sKt[D * 8];
-  RowTile tK{sK}, tV{sV};
-  ColTile tKt{sKt};
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int64_t b = blockIdx.y, bk = b % a.kv_batch;
+// Backward for the queries: delta = dO . O per row, then per key tile
+// S -> P (from lse), dP = dO V^T, dS = bf16(P (dP - delta)), dQ += dS K;
+// dQ * scale stored in fp32, delta stored for the key kernel.
+template <int NW, int S>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_bwd_dq_kernel(AttnArgs a) {
+  constexpr int QB = NW * NB;
+  constexpr int PW = 8 / NW;
+  constexpr int STAGE = 3 * TILE16;  // key tile, value tile, transposed key tile
+  __shared__ u32x4a smem[S * STAGE];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
   const int L = a.L;
-  const int q0 = blockIdx.x * 128 + wave * NB;
+  int qb;
+  int64_t b;
+  block_of((L + QB - 1) / QB, a.batch, qb, b);
+  const int64_t bk = b % a.kv_batch;
+  const int q0 = qb * QB + wave * NB;
   const bool active = q0 < L;
   const int qi = q0 + (lane & 31);
   const int qc = min(qi, L - 1);
-  const int n_tiles = min(L, int(blockIdx.x) * 128 + 128) / NB;
+  const int n_tiles = min(L, qb * QB + QB) / NB;
   const int my_tiles = active ? q0 / NB + 1 : 0;
   const uint16_t* Kb = a.K + bk * int64_t(L) * D;
   const uint16_t* Vb = a.V + bk * int64_t(L) * D;
   const uint16_t* Ktb = a.Kt + bk * int64_t(D) * L;
+  const float c = a.scale * LOG2E;
+  uint32_t ro[PW], co[PW];
+#pragma unroll
+  for (int q = 0; q < PW; ++q) {
+    ro[q] = row_off(wave * PW + q, lane);
+    co[q] = col_off(wave * PW + q, lane, L);
+  }
   bf16x8a qf[8], df[8];
   float dl = 0.0f;
   {
@@ -285,156 +388,216 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_kernel(AttnArgs a) {
       for (int i = 0; i < 8; ++i) dl += float(df[j][i]) * float(ov[i]);
     }
   }
-  // delta: this lane's 64 d values, then the other half-wave's (lower half first)
-  {
+  {  // delta: this lane's 64 d values plus the other half-wave's (lower half first)
     const float d2 = __shfl_xor(dl, 32, 64);
     dl = lane < 32 ? dl + d2 : d2 + dl;
   }
-  const float mq = a.m[b * L + qc];
-  const float inv = 1.0f / a.l[b * L + qc];
-  if (active && lane < 32 && qi < L) a.delta[b * L + qi] = dl;
+  const float lse = a.lse[b * L + qc];
   f32x16a dq[4] = {zero16(), zero16(), zero16(), zero16()};
+#pragma unroll
+  for (int t = 0; t < S - 1; ++t)
+    if (t < n_tiles) {
+      u32x4a* st = smem + (t % S) * STAGE;
+      copy_tile<PW>(Kb + int64_t(t) * NB * D, ro, st, wave);
+      copy_tile<PW>(Vb + int64_t(t) * NB * D, ro, st + TILE16, wave);
+      copy_tile<PW>(Ktb + int64_t(t) * NB, co, st + 2 * TILE16, wave);
+    }
   for (int t = 0; t < n_tiles; ++t) {
-    __syncthreads();
-    tK.load(Kb, D, t * NB, NB);
-    tV.load(Vb, D, t * NB, NB);
-    tKt.load(Ktb, L, t * NB);
-    __syncthreads();
+    wait_tiles<3 * PW>(min(S - 2, n_tiles - 1 - t));
+    lds_wait_barrier();
+    if (t + S - 1 < n_tiles) {
+      const int u = t + S - 1;
+      u32x4a* st = smem + (u % S) * STAGE;
+      copy_tile<PW>(Kb + int64_t(u) * NB * D, ro, st, wave);
+      copy_tile<PW>(Vb + int64_t(u) * NB * D, ro, st + TILE16, wave);
+      copy_tile<PW>(Ktb + int64_t(u) * NB, co, st + 2 * TILE16, wave);
+    }
     if (t >= my_tiles) continue;
+    const u32x4a* tk = smem + (t % S) * STAGE;
+    bf16x8a f[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) f[j] = row_frag(tk, j, lane);
     f32x16a s = zero16(), dp = zero16();
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      s = mfma(tK.frag(j, lane), qf[j], s);
-      dp = mfma(tV.frag(j, lane), df[j], dp);
-    }
-    float ds[16];
+    for (int j = 0; j < 8; ++j) s = mfma(f[j], qf[j], s);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int key = t * NB + acc_row(r, lane);
-      const float p = key <= qi ? bf16_round(expf(s[r] * a.scale - mq) * inv) : 0.0f;
-      ds[r] = p * (dp[r] - dl);
+    for (int j = 0; j < 8; ++j) f[j] = row_frag(tk + TILE16, j, lane);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) dp = mfma(f[j], df[j], dp);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) f[i] = col_frag(tk + 2 * TILE16, i & 3, i >> 2, lane);
+    // dS in place of dP
+#pragma unroll
+    for (int r = 0; r < 16; ++r) dp[r] = bf16_round(exp2a(fmaf(s[r], c, -lse))) * (dp[r] - dl);
+    if (t == my_tiles - 1) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        if (t * NB + slot_row(r, lane) > qi) dp[r] = 0.0f;
     }
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      const bf16x8a sb = pack_half(ds, h);
+      bf16x8a sb;
 #pragma unroll
-      for (int db = 0; db < 4; ++db) dq[db] = mfma(tKt.frag(db, h, lane), sb, dq[db]);
+      for (int i = 0; i < 8; ++i) sb[i] = __bf16(dp[8 * h + i]);
+#pragma unroll
+      for (int db = 0; db < 4; ++db) dq[db] = mfma(f[4 * h + db], sb, dq[db]);
     }
   }
-  if (!active || qi >= L) return;
-  float* out = a.dQ + (b * L + qi) * int64_t(D);
-#pragma unroll
-  for (int db = 0; db < 4; ++db)
-#pragma unroll
-    for (int g4 = 0; g4 < 4; ++g4) {
-      const int d0 = 32 * db + 8 * g4 + 4 * (lane >> 5);
-      *reinterpret_cast<float4*>(out + d0) = make_float4(dq[db][4 * g4] * a.scale, dq[db][4 * g4 + 1] * a.scale,
-                                                         dq[db][4 * g4 + 2] * a.scale, dq[db][4 * g4 + 3] * a.scale);
-    }
+  if (!active) return;
+  if (lane < 32) a.delta[b * L + qi] = dl;
+  store_f32_rows(a.dQ + (b * L + qi) * int64_t(D), dq, a.scale, lane);
 }
 
-// Backward for the keys and values: one workgroup per (128 keys, key/value
-// batch); wave w owns keys k0 = 128 blockIdx.x + 32 w .. + 32 and loops over
-// the query heads that share the key/value head (in head order) and over the
-// query tiles from its diagonal on.  S = Q K^T and dP = dO V^T have queries
-// as rows and this lane's key as column, so P and dS feed dV += P^T dO and
-// dK += dS^T Q directly.
-__global__ __launch_bounds__(256) void attn_bwd_dkv_kernel(AttnArgs a) {
-  __shared__ u32x4a sQ[NB * 16];
-  __shared__ u32x4a sdO[NB * 16];
-  __shared__ u32x2a sQt[D * 8];
-  __shared__ u32x2a sdOt[D * 8];
-  __shared__ float sm[NB], sinv[NB], sdl[NB];
-  RowTile tQ{sQ}, tdO{sdO};
-  ColTile tQt{sQt}, tdOt{sdOt};
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int64_t bk = blockIdx.y;
+// Backward for the keys and values of one query head: one workgroup of NW
+// waves per (NW * 32 keys, query batch b); wave w owns 32 keys (K, V rows in
+// registers) and multiplies the query tiles from its diagonal on.  S = Q K^T
+// and dP = dO V^T have the query tile as M and this lane's key as column, so
+// P and dS feed dV_b += P^T dO and dK_b += dS^T Q directly.  The row terms
+// (lse, delta) of a query tile come through LDS: wave 0 copies them into a
+// 1 KB slot of the stage (lanes 0-7 lse, 8-15 delta, the rest repeat them).
+// To hold two workgroups of 256 registers per lane on a SIMD, the last NPARK
+// of the wave's V fragments are kept in LDS and read back for each tile.
+template <int NW, int S>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_bwd_dkv_kernel(AttnArgs a) {
+  constexpr int KB = NW * NB;
+  constexpr int PW = 8 / NW;
+  constexpr int STAGE = 4 * TILE16 + 64;  // Q, dO, Qt, dOt tiles, row terms
+  constexpr int NPARK = 3;
+  __shared__ u32x4a smem[S * STAGE + NW * NPARK * 64];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
   const int L = a.L;
-  const int k0 = blockIdx.x * 128 + wave * NB;
+  int kb;
+  int64_t b;
+  block_of((L + KB - 1) / KB, a.batch, kb, b);
+  const int64_t bk = b % a.kv_batch;
+  const int k0 = kb * KB + wave * NB;
   const bool active = k0 < L;
   const int kj = k0 + (lane & 31);  // this lane's key
   const int kc = min(kj, L - 1);
-  const int first_tile = int(blockIdx.x) * 128 / NB;  // query tiles the workgroup needs
-  const int my_first = active ? k0 / NB : L / NB;
-  const int groups = int(a.batch / a.kv_batch);
-  bf16x8a kf[8], vf[8];
+  const int first = kb * KB / NB;   // first query tile of the workgroup
+  const int n_tiles = L / NB;
+  const int my_first = active ? k0 / NB : n_tiles;
+  const float c = a.scale * LOG2E;
+  const uint16_t* Qb = a.Q + b * int64_t(L) * D;
+  const uint16_t* dOb = a.dO + b * int64_t(L) * D;
+  const uint16_t* Qtb = a.Qt + b * int64_t(D) * L;
+  const uint16_t* dOtb = a.dOt + b * int64_t(D) * L;
+  // row terms: lane (l % 16) copies 4 floats of lse (l % 16 < 8) or delta
+  const float* rt_src = ((lane & 15) < 8 ? a.lse : a.delta) + b * L + 4 * (lane & 7);
+  uint32_t ro[PW], co[PW];
+#pragma unroll
+  for (int q = 0; q < PW; ++q) {
+    ro[q] = row_off(wave * PW + q, lane);
+    co[q] = col_off(wave * PW + q, lane, L);
+  }
+  bf16x8a kf[8], vf[8 - NPARK];
+  u32x4a* park = smem + S * STAGE + wave * NPARK * 64;
   {
     const int64_t row = (bk * L + kc) * int64_t(D) + 8 * (lane >> 5);
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       kf[j] = __builtin_bit_cast(bf16x8a, *reinterpret_cast<const u32x4a*>(a.K + row + 16 * j));
-      vf[j] = __builtin_bit_cast(bf16x8a, *reinterpret_cast<const u32x4a*>(a.V + row + 16 * j));
+      const u32x4a v = *reinterpret_cast<const u32x4a*>(a.V + row + 16 * j);
+      if (j < 8 - NPARK) vf[j] = __builtin_bit_cast(bf16x8a, v);
+      else park[(j - 8 + NPARK) * 64 + lane] = v;
     }
   }
   f32x16a dk[4] = {zero16(), zero16(), zero16(), zero16()};
   f32x16a dv[4] = {zero16(), zero16(), zero16(), zero16()};
-  for (int g = 0; g < groups; ++g) {
-    const int64_t b = int64_t(g) * a.kv_batch + bk;  // query batch of head position g
-    const uint16_t* Qb = a.Q + b * int64_t(L) * D;
-    const uint16_t* dOb = a.dO + b * int64_t(L) * D;
-    const uint16_t* Qtb = a.Qt + b * int64_t(D) * L;
-    const uint16_t* dOtb = a.dOt + b * int64_t(D) * L;
-    for (int t = first_tile; t < L / NB; ++t) {
-      __syncthreads();
-      tQ.load(Qb, D, t * NB, NB);
-      tdO.load(dOb, D, t * NB, NB);
-      tQt.load(Qtb, L, t * NB);
-      tdOt.load(dOtb, L, t * NB);
-      if (threadIdx.x < NB) {
-        const int64_t i = b * L + t * NB + threadIdx.x;
-        sm[threadIdx.x] = a.m[i];
-        sinv[threadIdx.x] = 1.0f / a.l[i];
-        sdl[threadIdx.x] = a.delta[i];
+  const int nt = n_tiles - first;  // tiles the workgroup walks
+#pragma unroll
+  for (int i = 0; i < S - 1; ++i)
+    if (i < nt) {
+      const int t = first + i;
+      u32x4a* st = smem + (i % S) * STAGE;
+      copy_tile<PW>(Qb + int64_t(t) * NB * D, ro, st, wave);
+      copy_tile<PW>(dOb + int64_t(t) * NB * D, ro, st + TILE16, wave);
+      copy_tile<PW>(Qtb + int64_t(t) * NB, co, st + 2 * TILE16, wave);
+      copy_tile<PW>(dOtb + int64_t(t) * NB, co, st + 3 * TILE16, wave);
+      if (wave == 0) copy16(rt_src + t * NB, 0, st + 4 * TILE16);
+    }
+  for (int i = 0; i < nt; ++i) {
+    if (wave == 0) wait_tiles<4 * PW + 1>(min(S - 2, nt - 1 - i));
+    else wait_tiles<4 * PW>(min(S - 2, nt - 1 - i));
+    lds_wait_barrier();
+    if (i + S - 1 < nt) {
+      const int u = i + S - 1, t = first + u;
+      u32x4a* st = smem + (u % S) * STAGE;
+      copy_tile<PW>(Qb + int64_t(t) * NB * D, ro, st, wave);
+      copy_tile<PW>(dOb + int64_t(t) * NB * D, ro, st + TILE16, wave);
+      copy_tile<PW>(Qtb + int64_t(t) * NB, co, st + 2 * TILE16, wave);
+      copy_tile<PW>(dOtb + int64_t(t) * NB, co, st + 3 * TILE16, wave);
+      if (wave == 0) copy16(rt_src + t * NB, 0, st + 4 * TILE16);
+    }
+    const int t = first + i;
+    if (t < my_first) continue;
+    const u32x4a* st = smem + (i % S) * STAGE;
+    const float* rt = reinterpret_cast<const float*>(st + 4 * TILE16);  // lse[32], delta[32]
+    f32x16a s = zero16(), dp = zero16();
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      s = mfma(row_frag(st, j, lane), kf[j], s);
+      const bf16x8a vj = j < 8 - NPARK ? vf[j] : __builtin_bit_cast(bf16x8a, park[(j - 8 + NPARK) * 64 + lane]);
+      dp = mfma(row_frag(st + TILE16, j, lane), vj, dp);
+    }
+    // P and dS in place of S and dP
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int q8 = 16 * h + 8 * (lane >> 5);  // the 8 query rows of slots 8 h .. + 8
+      const float4 l0 = *reinterpret_cast<const float4*>(rt + q8), l1 = *reinterpret_cast<const float4*>(rt + q8 + 4);
+      const float4 e0 = *reinterpret_cast<const float4*>(rt + 32 + q8),
+                   e1 = *reinterpret_cast<const float4*>(rt + 32 + q8 + 4);
+      const float ls[8] = {l0.x, l0.y, l0.z, l0.w, l1.x, l1.y, l1.z, l1.w};
+      const float de[8] = {e0.x, e0.y, e0.z, e0.w, e1.x, e1.y, e1.z, e1.w};
+#pragma unroll
+      for (int i8 = 0; i8 < 8; ++i8) {
+        const int r = 8 * h + i8;
+        const float pv = bf16_round(exp2a(fmaf(s[r], c, -ls[i8])));
+        s[r] = pv;
+        dp[r] = pv * (dp[r] - de[i8]);
       }
-      __syncthreads();
-      if (t < my_first) continue;
-      f32x16a s = zero16(), dp = zero16();
+    }
+    if (t == my_first) {
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        s = mfma(tQ.frag(j, lane), kf[j], s);
-        dp = mfma(tdO.frag(j, lane), vf[j], dp);
-      }
-      float p[16], ds[16];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int qr = acc_row(r, lane);
-        const int qi = t * NB + qr;
-        const float pv = kj <= qi ? bf16_round(expf(s[r] * a.scale - sm[qr]) * sinv[qr]) : 0.0f;
-        p[r] = pv;
-        ds[r] = pv * (dp[r] - sdl[qr]);
-      }
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const bf16x8a pb = pack_half(p, h), sb = pack_half(ds, h);
-#pragma unroll
-        for (int db = 0; db < 4; ++db) {
-          dv[db] = mfma(tdOt.frag(db, h, lane), pb, dv[db]);
-          dk[db] = mfma(tQt.frag(db, h, lane), sb, dk[db]);
+      for (int r = 0; r < 16; ++r)
+        if (kj > t * NB + slot_row(r, lane)) {
+          s[r] = 0.0f;
+          dp[r] = 0.0f;
         }
+    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      bf16x8a pb, sb;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        pb[i] = __bf16(s[8 * h + i]);
+        sb[i] = __bf16(dp[8 * h + i]);
+      }
+#pragma unroll
+      for (int db = 0; db < 4; ++db) {
+        dv[db] = mfma(col_frag(st + 3 * TILE16, db, h, lane), pb, dv[db]);
+        dk[db] = mfma(col_frag(st + 2 * TILE16, db, h, lane), sb, dk[db]);
       }
     }
   }
-  if (!active || kj >= L) return;
-  float* ko = a.dK + (bk * L + kj) * int64_t(D);
-  float* vo = a.dV + (bk * L + kj) * int64_t(D);
-#pragma unroll
-  for (int db = 0; db < 4; ++db)
-#pragma unroll
-    for (int g4 = 0; g4 < 4; ++g4) {
-      const int d0 = 32 * db + 8 * g4 + 4 * (lane >> 5);
-      *reinterpret_cast<float4*>(ko + d0) = make_float4(dk[db][4 * g4] * a.scale, dk[db][4 * g4 + 1] * a.scale,
-                                                        dk[db][4 * g4 + 2] * a.scale, dk[db][4 * g4 + 3] * a.scale);
-      *reinterpret_cast<float4*>(vo + d0) =
-          make_float4(dv[db][4 * g4], dv[db][4 * g4 + 1], dv[db][4 * g4 + 2], dv[db][4 * g4 + 3]);
-    }
+  if (!active) return;
+  store_f32_rows(a.dK + (b * L + kj) * int64_t(D), dk, a.scale, lane);
+  store_f32_rows(a.dV + (b * L + kj) * int64_t(D), dv, 1.0f, lane);
 }
+
+namespace {
+constexpr int FWD_NW = 8, FWD_S = 2;
+constexpr int DQ_NW = 4, DQ_S = 2;
+constexpr int DKV_NW = 8, DKV_S = 2;
+}  // namespace
 
 hipError_t launch_attn_fwd(const AttnLaunch& q, hipStream_t st) {
   AttnArgs a{};
   a.batch = q.batch; a.kv_batch = q.kv_batch; a.L = q.L; a.scale = q.scale;
-  a.Q = q.Q; a.K = q.K; a.Vt = q.Vt; a.O_out = q.O_out; a.m = q.m; a.l = q.l;
-  const dim3 grid(unsigned((q.L + 127) / 128), unsigned(q.batch));
-  hipLaunchKernelGGL(attn_fwd_kernel, grid, dim3(256), 0, st, a);
+  a.Q = q.Q; a.K = q.K; a.Vt = q.Vt; a.O_out = q.O_out; a.lse = q.lse;
+  const int64_t nblk = (q.L + FWD_NW * NB - 1) / (FWD_NW * NB);
+  hipLaunchKernelGGL((attn_fwd_kernel<FWD_NW, FWD_S>), dim3(unsigned(nblk * q.batch)), dim3(FWD_NW * 64), 0, st, a);
   return hipGetLastError();
 }
 
@@ -442,13 +605,14 @@ hipError_t launch_attn_bwd(const AttnLaunch& q, hipStream_t st) {
   AttnArgs a{};
   a.batch = q.batch; a.kv_batch = q.kv_batch; a.L = q.L; a.scale = q.scale;
   a.Q = q.Q; a.Qt = q.Qt; a.K = q.K; a.Kt = q.Kt; a.V = q.V; a.O = q.O; a.dO = q.dO; a.dOt = q.dOt;
-  a.m = q.m; a.l = q.l; a.delta = q.delta; a.dQ = q.dQ; a.dK = q.dK; a.dV = q.dV;
-  const dim3 gq(unsigned((q.L + 127) / 128), unsigned(q.batch));
-  hipLaunchKernelGGL(attn_bwd_dq_kernel, gq, dim3(256), 0, st, a);
+  a.lse = q.lse; a.delta = q.delta; a.dQ = q.dQ; a.dK = q.dK; a.dV = q.dV;
+  const int64_t nq = (q.L + DQ_NW * NB - 1) / (DQ_NW * NB);
+  hipLaunchKernelGGL((attn_bwd_dq_kernel<DQ_NW, DQ_S>), dim3(unsigned(nq * q.batch)), dim3(DQ_NW * 64), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const dim3 gk(unsigned((q.L + 127) / 128), unsigned(q.kv_batch));
-  hipLaunchKernelGGL(attn_bwd_dkv_kernel, gk, dim3(256), 0, st, a);
+  const int64_t nk = (q.L + DKV_NW * NB - 1) / (DKV_NW * NB);
+  hipLaunchKernelGGL((attn_bwd_dkv_kernel<DKV_NW, DKV_S>), dim3(unsigned(nk * q.batch)), dim3(DKV_NW * 64), 0, st,
+                     a);
   return hipGetLastError();
 }
 

@@ -188,6 +188,127 @@ __global__ __launch_bounds__(256) void rope_split_kernel(int64_t T, int H, int d
   out[dst + hd] = to_bf(y2);
 }
 
+// The same two layout changes for d a multiple of 16 (up to 512) and 16-byte
+// aligned buffers: a workgroup takes RT consecutive tokens, computes the cos
+// and sin of their d/2 angles once into LDS (the same angle and sincosf as
+// the one-pair kernels, so the results are bit-identical), and moves chunks
+// of 8 pairs with 16-byte accesses.
+constexpr int RT = 4;           // tokens per workgroup
+constexpr int RT_MAX_HD = 256;  // d / 2 limit of the LDS angle table
+
+__device__ __forceinline__ void load8(const void* in, bool f32, int64_t off, float (&x)[8]) {
+  if (f32) {
+    const float4 a = *reinterpret_cast<const float4*>(static_cast<const float*>(in) + off);
+    const float4 b = *reinterpret_cast<const float4*>(static_cast<const float*>(in) + off + 4);
+    x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w; x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+  } else {
+    const uint4 v = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(in) + off);
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      x[2 * j] = __uint_as_float(w[j] << 16);
+      x[2 * j + 1] = __uint_as_float(w[j] & 0xFFFF0000u);
+    }
+  }
+}
+
+__device__ __forceinline__ void store8(uint16_t* out, const float (&y)[8]) {
+  uint32_t w[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) w[j] = uint32_t(to_bf(y[2 * j])) | (uint32_t(to_bf(y[2 * j + 1])) << 16);
+  *reinterpret_cast<uint4*>(out) = make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+// cos and sin of the RT tokens' angles: cs[tt * hd + i] for token t0 + tt.
+template <bool ROT>
+__device__ __forceinline__ void rope_table(float2* cs, int64_t t0, int64_t T, int L, int d) {
+  if (!ROT) return;
+  const int hd = d >> 1;
+  for (int k = threadIdx.x; k < RT * hd; k += 256) {
+    const int tt = k / hd, i = k % hd;
+    float sn = 0.0f, cn = 1.0f;
+    if (t0 + tt < T) sincosf(rope_angle(int((t0 + tt) % L), i, d), &sn, &cn);
+    cs[k] = make_float2(cn, sn);
+  }
+  __syncthreads();
+}
+
+template <bool IN_F32, bool ROT>
+__global__ __launch_bounds__(256) void rope_split_vec_kernel(int64_t T, int H, int d, int L, int perm,
+                                                             const void* __restrict__ in, uint16_t* __restrict__ out) {
+  __shared__ float2 cs[RT * RT_MAX_HD];
+  const int hd = d >> 1, cph = hd / 8, cpt = H * cph;  // chunks per head, per token
+  const int64_t t0 = int64_t(blockIdx.x) * RT;
+  rope_table<ROT>(cs, t0, T, L, d);
+  for (int k = threadIdx.x; k < RT * cpt; k += 256) {
+    const int tt = k / cpt, r = k % cpt;
+    const int64_t t = t0 + tt;
+    if (t >= T) break;
+    const int h = r / cph, i = (r % cph) * 8;
+    const int64_t src = t * (int64_t(H) * d) + int64_t(h) * d + i;
+    float x1[8], x2[8], y1[8], y2[8];
+    load8(in, IN_F32, src, x1);
+    load8(in, IN_F32, src + hd, x2);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      if (ROT) {
+        const float2 a = cs[tt * hd + i + e];
+        y1[e] = x1[e] * a.x - x2[e] * a.y;
+        y2[e] = x2[e] * a.x + x1[e] * a.y;
+      } else {
+        y1[e] = x1[e];
+        y2[e] = x2[e];
+      }
+    }
+    const int64_t dst = (int64_t(head_slot(h, H, perm)) * T + t) * d + i;
+    store8(out + dst, y1);
+    store8(out + dst + hd, y2);
+  }
+}
+
+template <bool IN_F32, bool ROT>
+__global__ __launch_bounds__(256) void rope_merge_vec_kernel(int64_t T, int H, int d, int L, int perm, int nsum,
+                                                             const void* __restrict__ in, uint16_t* __restrict__ out) {
+  __shared__ float2 cs[RT * RT_MAX_HD];
+  const int hd = d >> 1, cph = hd / 8, cpt = H * cph;
+  const int64_t t0 = int64_t(blockIdx.x) * RT;
+  const int64_t pstride = int64_t(H) * T * d;
+  rope_table<ROT>(cs, t0, T, L, d);
+  for (int k = threadIdx.x; k < RT * cpt; k += 256) {
+    const int tt = k / cpt, r = k % cpt;
+    const int64_t t = t0 + tt;
+    if (t >= T) break;
+    const int h = r / cph, i = (r % cph) * 8;
+    const int64_t src0 = (int64_t(head_slot(h, H, perm)) * T + t) * d + i;
+    float x1[8] = {0, 0, 0, 0, 0, 0, 0, 0}, x2[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (int q = 0; q < nsum; ++q) {
+      float v1[8], v2[8];
+      load8(in, IN_F32, src0 + q * pstride, v1);
+      load8(in, IN_F32, src0 + q * pstride + hd, v2);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        x1[e] += v1[e];
+        x2[e] += v2[e];
+      }
+    }
+    float y1[8], y2[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      if (ROT) {
+        const float2 a = cs[tt * hd + i + e];
+        y1[e] = x1[e] * a.x + x2[e] * a.y;
+        y2[e] = x2[e] * a.x - x1[e] * a.y;
+      } else {
+        y1[e] = x1[e];
+        y2[e] = x2[e];
+      }
+    }
+    const int64_t dst = t * (int64_t(H) * d) + int64_t(h) * d + i;
+    store8(out + dst, y1);
+    store8(out + dst + hd, y2);
+  }
+}
+
 // Head-major [nsum, H, T, d] (fp32 or bf16; head h at head_slot(h)) ->
 // token-major bf16 [T, C]: the nsum stacked partials are summed (the
 // gradient of a key/value head shared by a group), then rotated by minus
@@ -395,8 +516,24 @@ hipError_t launch_rmsnorm_bwd(int64_t T, int64_t C, const float* dZa, const floa
   return hipGetLastError();
 }
 
+static bool rope_vec_ok(int d, const void* in, const void* out) {
+  return d % 16 == 0 && d / 2 <= RT_MAX_HD && (reinterpret_cast<uintptr_t>(in) & 15) == 0 &&
+         (reinterpret_cast<uintptr_t>(out) & 15) == 0;
+}
+
 hipError_t launch_rope_split(int64_t T, int H, int d, int L, int perm, const void* in, int in_f32, int rotate,
                              uint16_t* out, hipStream_t st) {
+  if (rope_vec_ok(d, in, out)) {
+    const dim3 grid(unsigned((T + RT - 1) / RT));
+    if (in_f32 && rotate)
+      hipLaunchKernelGGL((rope_split_vec_kernel<true, true>), grid, dim3(256), 0, st, T, H, d, L, perm, in, out);
+    else if (in_f32)
+      hipLaunchKernelGGL((rope_split_vec_kernel<true, false>), grid, dim3(256), 0, st, T, H, d, L, perm, in, out);
+    else if (rotate)
+      hipLaunchKernelGGL((rope_split_vec_kernel<false, true>), grid, dim3(256), 0, st, T, H, d, L, perm, in, out);
+    else hipLaunchKernelGGL((rope_split_vec_kernel<false, false>), grid, dim3(256), 0, st, T, H, d, L, perm, in, out);
+    return hipGetLastError();
+  }
   const dim3 grid(unsigned((T * H * (d / 2) + 255) / 256));
   if (in_f32 && rotate)
     hipLaunchKernelGGL((rope_split_kernel<true, true>), grid, dim3(256), 0, st, T, H, d, L, perm, in, out);
@@ -410,6 +547,21 @@ hipError_t launch_rope_split(int64_t T, int H, int d, int L, int perm, const voi
 
 hipError_t launch_rope_merge(int64_t T, int H, int d, int L, int perm, int nsum, const void* in, int in_f32,
                              int rotate, uint16_t* out, hipStream_t st) {
+  if (rope_vec_ok(d, in, out)) {
+    const dim3 grid(unsigned((T + RT - 1) / RT));
+    if (in_f32 && rotate)
+      hipLaunchKernelGGL((rope_merge_vec_kernel<true, true>), grid, dim3(256), 0, st, T, H, d, L, perm, nsum, in, out);
+    else if (in_f32)
+      hipLaunchKernelGGL((rope_merge_vec_kernel<true, false>), grid, dim3(256), 0, st, T, H, d, L, perm, nsum, in,
+                         out);
+    else if (rotate)
+      hipLaunchKernelGGL((rope_merge_vec_kernel<false, true>), grid, dim3(256), 0, st, T, H, d, L, perm, nsum, in,
+                         out);
+    else
+      hipLaunchKernelGGL((rope_merge_vec_kernel<false, false>), grid, dim3(256), 0, st, T, H, d, L, perm, nsum, in,
+                         out);
+    return hipGetLastError();
+  }
   const dim3 grid(unsigned((T * H * (d / 2) + 255) / 256));
   if (in_f32 && rotate)
     hipLaunchKernelGGL((rope_merge_kernel<true, true>), grid, dim3(256), 0, st, T, H, d, L, perm, nsum, in, out);

@@ -942,20 +942,34 @@ hipError_t noalloc_scratch(float** out) {
   return hipSuccess;
 }
 
-// out[c, r] = in[r, c]; 64 x 64 tiles through LDS (padded against conflicts).
+// out[c, r] = in[r, c] for rows and cols multiples of 8: 64 x 64 tiles
+// through LDS with 16-byte global accesses (8 bf16 per lane).  A load chunk
+// is 8 consecutive columns of one input row; a store chunk is 8 consecutive
+// input rows of one column, and the 8 lanes of an output row write its 128
+// bytes together.  Chunks past the edge of the matrix are skipped whole.
 __global__ __launch_bounds__(256) void transpose_kernel(const uint16_t* __restrict__ in, uint16_t* __restrict__ out,
                                                         int64_t rows, int64_t cols) {
-  __shared__ uint16_t t[64][66];
+  __shared__ __align__(16) uint16_t t[64][72];  // 144-byte rows keep 16-byte chunks aligned
   const int64_t r0 = int64_t(blockIdx.y) * 64, c0 = int64_t(blockIdx.x) * 64;
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-  for (int i = ty; i < 64; i += 4) {
-    const int64_t r = r0 + i, c = c0 + tx;
-    t[i][tx] = (r < rows && c < cols) ? in[r * cols + c] : uint16_t(0);
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int k = threadIdx.x + 256 * h;
+    const int r = k >> 3, c8 = (k & 7) * 8;
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    if (r0 + r < rows && c0 + c8 < cols) v = *reinterpret_cast<const uint4*>(in + (r0 + r) * cols + c0 + c8);
+    *reinterpret_cast<uint4*>(&t[r][c8]) = v;
   }
   __syncthreads();
-  for (int i = ty; i < 64; i += 4) {
-    const int64_t c = c0 + i, r = r0 + tx;
-    if (c < cols && r < rows) out[c * rows + r] = t[tx][i];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int k = threadIdx.x + 256 * h;
+    const int c = k >> 3, r8 = (k & 7) * 8;  // output row c0 + c, columns r0 + r8 .. + 8
+    if (c0 + c < cols && r0 + r8 < rows) {
+      uint32_t w[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) w[j] = uint32_t(t[r8 + 2 * j][c]) | (uint32_t(t[r8 + 2 * j + 1][c]) << 16);
+      *reinterpret_cast<uint4*>(out + (c0 + c) * rows + r0 + r8) = make_uint4(w[0], w[1], w[2], w[3]);
+    }
   }
 }
 

@@ -140,6 +140,49 @@ def test_rope_split_merge(n_seq, L, H, d):
     assert np.array_equal(host(tm), xb)
 
 
+@pytest.mark.parametrize("n_seq,L,H,d,G,nsum", [(3, 43, 5, 128, 1, 1), (2, 40, 6, 16, 3, 2), (1, 9, 2, 512, 2, 2),
+                                                 (2, 21, 4, 64, 2, 3)])
+def test_rope_vector_path_matches_pair_path(n_seq, L, H, d, G, nsum):
+    """The 16-byte chunk kernels (d a multiple of 16, 16-byte aligned buffers)
+    against the one-pair kernels, reached through buffers offset by one
+    element: bit-identical outputs for every input type and rotation, on
+    token counts that leave a partial workgroup."""
+    T, C = n_seq * L, H * d
+    rs = np.random.default_rng(T + H + d)
+
+    def run(fn, x, n_out, **kw):
+        outs = []
+        for shift in (0, 1):   # 0: aligned (chunk kernel); 1: offset by one element (pair kernel)
+            xin = torch.empty(x.numel() + 8, dtype=x.dtype, device="cuda")
+            xin[shift:shift + x.numel()] = x.reshape(-1)
+            o = torch.empty(n_out + 8, dtype=torch.bfloat16, device="cuda")
+            fn(T, H, d, L, xin[shift:shift + x.numel()], o[shift:shift + n_out], **kw)
+            torch.cuda.synchronize()
+            outs.append(o[shift:shift + n_out].clone())
+        assert torch.equal(outs[0], outs[1]), (fn.__name__, kw)
+
+    x32 = dev(rs.standard_normal((T, C)).astype(F32), torch.float32)
+    xb = dev(bfr(rs.standard_normal((T, C))), torch.bfloat16)
+    for x in (x32, xb):
+        for rot in (True, False):
+            run(uq.uniquan_rope_split, x, T * C, rotate=rot, group=G)
+    y32 = dev(rs.standard_normal((nsum, H, T, d)).astype(F32), torch.float32)
+    yb = dev(bfr(rs.standard_normal((nsum, H, T, d))), torch.bfloat16)
+    for y in (y32, yb):
+        for rot in (True, False):
+            run(uq.uniquan_rope_merge, y, T * C, rotate=rot, group=G, nsum=nsum)
+
+
+@pytest.mark.parametrize("R,C", [(8, 8), (72, 200), (2048, 136), (136, 4096)])
+def test_transpose_2d_edges(R, C):
+    """uniquan_transpose_bf16 on shapes with partial 64 x 64 tiles: bit-exact."""
+    x = bfr(np.random.default_rng(R + C).standard_normal((R, C)))
+    out = torch.empty(C, R, dtype=torch.bfloat16, device="cuda")
+    uq.uniquan_transpose_bf16(R, C, dev(x, torch.bfloat16), out)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(out), x.T)
+
+
 @pytest.mark.parametrize("B,L", [(3, 7), (4, 130), (2, 2048), (1, 2100)])   # 2100: rows past the register path
 def test_softmax_causal(B, L):
     rs = np.random.default_rng(B * L)
