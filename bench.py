@@ -474,6 +474,17 @@ def block_decoder(seed, k=3, steps=5, warmup=2, n_kv=None):
         step_local()
     e1.record()
     torch.cuda.synchronize()
+    ms_unfused = e0.elapsed_time(e1) / steps
+    # the fused step form: the straight-through backward + SGD of each matrix
+    # fused with its next fake-quant forward (What left by the last quantize)
+    blk.quantize(uq.MAP_LOCAL)
+    step_fused = uq.record(blk.step_fused, uq.MAP_LOCAL, lr_f, lr_b)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(steps):
+        step_fused()
+    e1.record()
+    torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / steps
     # one instrumented step for the split between phases
     ev = [TimingEvent() for _ in range(6)]
@@ -496,14 +507,17 @@ def block_decoder(seed, k=3, steps=5, warmup=2, n_kv=None):
     n_w = sum(q.R * q.C for q in mats.values())
     last = float(blk.loss.item()) / l0
     return {"T": blk.T, "C": blk.C, "I": blk.I, "heads": H, "kv_heads": n_kv, "seq_len": blk.L, "n_seq": n_seq, "k": k, "g": g,
-            "steps": steps, "ms_per_step": ms, "gweights_per_s": n_w / (ms * 1e-3) / 1e9,
+            "steps": steps, "ms_per_step": ms, "ms_per_step_unfused": ms_unfused,
+            "gweights_per_s": n_w / (ms * 1e-3) / 1e9,
             "gemm_flops_per_step": flops, "tflops_effective": tf, "frac_mfma": tf / MFMA_BF16_PEAK_TFLOPS,
             "phase_ms": phases, "loss_init": l0, "rel_loss_warmup": rel, "rel_loss_last": last,
             "state_finite": bool(math.isfinite(last)),
             "optimiser": "SGD on L / L_init (learning rates 0.005 / 0.0005 divided by the initial loss)",
-            "note": "whole step over the seven matrices (fake-quant fwd, block forward on What with the "
-                    "quantized input, loss, backpropagation, straight-through backward + SGD); flops count "
-                    "the GEMMs only"}
+            "note": "whole step over the seven matrices in the fused form (block forward on What with the "
+                    "quantized input, loss, backpropagation, then per matrix the straight-through backward + "
+                    "SGD fused with the next fake-quant forward); ms_per_step_unfused: the same step with the "
+                    "fake-quant forward and the backward + SGD as separate passes; phase_ms splits an unfused "
+                    "step; flops count the GEMMs only"}
 
 
 # Kernel-name patterns of the step's four phases in rocprofv3 output.

@@ -64,6 +64,13 @@ class QuantMatrix:
         uq.uniquan_fq_bwd_sgd(self.R, self.C, self.k, self.g, self.W, self.s, self.s_r, self.delta, self.z_u,
                               self.alpha, self.z_b, self.codes, self.G, gs, ga, gz, lr_f, lr_b)
 
+    def fq_step(self, lr_f, lr_b, next_mode):
+        """The straight-through backward with the SGD update and the next
+        step's forward (next_mode) in one pass: W_hat and codes for the next
+        step."""
+        uq.uniquan_fq_step(self.R, self.C, self.k, self.g, self.W, self.s, self.s_r, self.delta, self.z_u,
+                           self.alpha, self.z_b, self.codes, self.G, lr_f, lr_b, next_mode, self.W_hat)
+
 
 class MLPBlock:
     """The MLP module of one block: gate/up [I, C], down [C, I], activations
@@ -304,6 +311,19 @@ class DecoderBlock:
     def step(self, mode=uq.MAP_FULL, lr_f=0.005, lr_b=0.0005, keep_grads=False):
         self.forward_backward(mode)
         self.update(lr_f, lr_b, keep_grads)
+
+    def step_fused(self, next_mode=uq.MAP_LOCAL, lr_f=0.005, lr_b=0.0005):
+        """One step in the fused form: the block's forward on the current
+        What (left by quantize() or by the previous fused step), the loss,
+        backpropagation, then per matrix the straight-through backward with
+        SGD fused with the next step's forward (next_mode).  The same
+        sequence of operations as step() across steps; each matrix's What is
+        read once less and written once instead of twice."""
+        self.forward()
+        self.compute_loss()
+        self.backward()
+        for q in self.mats.values():
+            q.fq_step(lr_f, lr_b, next_mode)
 
     def flops_per_step(self):
         """GEMM flops of one step: the seven projections forward and their

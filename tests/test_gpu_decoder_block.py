@@ -67,13 +67,13 @@ def shapes_for(C_, I_, n_kv_d):
             "d": (C_, I_)}
 
 
-def make_block(seed, qk_scale=1.0, shapes=SHAPES):
+def make_block(seed, qk_scale=1.0, shapes=SHAPES, T_=T):
     specs = synth.WORKLOADS["block7b"].matrices
     mats, X = {}, None
     C = shapes["q"][1]
     for name, spec in zip(shapes, specs):
         R_, C_ = shapes[name]
-        m = synth.make_matrix(synth.scaled(spec, R=R_, C=C_, T=T), seed)
+        m = synth.make_matrix(synth.scaled(spec, R=R_, C=C_, T=T_), seed)
         if X is None:
             X = m.X.astype(F32)
         W = m.W
@@ -86,10 +86,10 @@ def make_block(seed, qk_scale=1.0, shapes=SHAPES):
     return X, mats, g1, g2
 
 
-def device_block(mats, g1, g2, H_=H, n_kv=None):
+def device_block(mats, g1, g2, H_=H, n_kv=None, T_=T, n_seq=N_SEQ):
     qs = {n: QuantMatrix(W, s, K, G, p["delta"], p["z_u"], p["s_r"], p["z_b"], p["alpha"])
           for n, (W, s, p) in mats.items()}
-    return DecoderBlock(qs, g1, g2, T, N_SEQ, H_, n_kv=n_kv), qs
+    return DecoderBlock(qs, g1, g2, T_, n_seq, H_, n_kv=n_kv), qs
 
 
 def oracle_what(mats, mode=O.MAP_FULL):
@@ -213,3 +213,62 @@ def test_decoder_block_grouped_query(n_kv, qk_scale):
     assert abs(loss - st["loss"]) <= 1e-2 * st["loss"], (loss, st["loss"])
     for n in mats:
         close(host(qs[n].G), st["grads"][n], elem=0.3, what=f"dL/dWhat_{n}")
+
+
+@pytest.mark.parametrize("n_kv", [2, 1])
+def test_decoder_block_step_long_sequences(n_kv):
+    """Two sequences of 512 tokens (several query and key blocks of the fused
+    attention per head, its pipelined tiles and the diagonal masking over a
+    long causal range): codes bit-exact, loss within 1e-2, dL/dWhat within
+    1e-2 normwise and the per-element bars of the short-sequence tests."""
+    n_seq, Ls = 2, 512
+    Tl = n_seq * Ls
+    Hq, Cq, Iq = 2, 256, 384
+    shapes = shapes_for(Cq, Iq, n_kv * (Cq // Hq))
+    X, mats, g1, g2 = make_block(21 + n_kv, 1.0, shapes, T_=Tl)
+    blk, qs = device_block(mats, g1, g2, Hq, n_kv, T_=Tl, n_seq=n_seq)
+    blk.prepare(X)
+    blk.set_input(X)
+    blk.forward_backward(uq.MAP_FULL)
+    torch.cuda.synchronize()
+
+    f = oracle_what(mats)
+    for n in mats:
+        assert np.array_equal(host(qs[n].codes).reshape(shapes[n]).astype(np.uint8), f[n]["codes"]), f"{n} codes"
+    Y_ref = D.decoder_forward(X, wfp(mats), g1, g2, n_seq, Hq, store=O.bf16_rne, n_kv=n_kv)["Y"]
+    assert np.allclose(host(blk.Yref), Y_ref, rtol=2e-2, atol=2e-2 * np.abs(Y_ref).max())
+    st = D.decoder_step(X, Y_ref, {n: f[n]["what_bf16"] for n in mats}, g1, g2, n_seq, Hq, store=O.bf16_rne,
+                        n_kv=n_kv)
+    loss = float(blk.loss.item())
+    assert abs(loss - st["loss"]) <= 1e-2 * st["loss"], (loss, st["loss"])
+    for n in mats:
+        close(host(qs[n].G), st["grads"][n], elem=0.1 if n_kv == Hq else 0.3, what=f"dL/dWhat_{n}")
+
+
+def test_decoder_block_fused_step_form():
+    """quantize, then step_fused twice equals step twice followed by quantize:
+    every matrix's s, alpha, z_B, codes and What, and the losses, bit for bit."""
+    X, mats, g1, g2 = make_block(31)
+    blocks = []
+    for _ in range(2):
+        blk, qs = device_block(mats, g1, g2)
+        blk.prepare(X)
+        blk.set_input(X)
+        blocks.append((blk, qs))
+    (a, qa), (b, qb) = blocks
+    lr_f, lr_b = 1e-4, 1e-5
+    la, lb = [], []
+    a.quantize(uq.MAP_FULL)
+    for nxt in (uq.MAP_LOCAL, uq.MAP_LOCAL):
+        a.step_fused(nxt, lr_f, lr_b)
+        la.append(a.loss.clone())
+    for mode in (uq.MAP_FULL, uq.MAP_LOCAL):
+        b.step(mode, lr_f, lr_b)
+        lb.append(b.loss.clone())
+    b.quantize(uq.MAP_LOCAL)
+    torch.cuda.synchronize()
+    for x, y in zip(la, lb):
+        assert torch.equal(x, y)
+    for n in qa:
+        for attr in ("s", "alpha", "z_b", "codes", "W_hat"):
+            assert torch.equal(getattr(qa[n], attr), getattr(qb[n], attr)), (n, attr)
