@@ -4,30 +4,37 @@ oracle/block_decoder.py.
 
 Seeded inputs: the seven matrices from the generator's 7B block recipe at a
 small shape (C = 256 in 2 heads of 128, I = 384, two sequences of 64
-tokens), norm weights 1 + 0.1 N(0, 1), quantizer parameters from the
-oracle's fixed-minimum clipping with a greedy start.  The oracle evaluates
-the block in fp64 with the device's bf16 storage points and never sees
-device output.  Bars: codes bit-exact per matrix; the loss within 1e-2;
-dL/dWhat of all seven matrices within 1e-2 normwise.  Per element the bar is
-0.1 of max(|x|, rms): the residual E = Yhat - Y_ref is a small difference of
-large values and each side rounds its bf16 intermediates (and its target)
-independently, so single elements of E, and of the gradients summed from
-them, differ by several percent where the attention is sharp; the
-per-element check still catches a misplaced or transposed gradient.  The
-grouped-query cases use C = 512 in 4 query heads of 128 sharing 2 or 1
-key/value heads (k, v of [n_kv 128, 512]); their per-element bar is 0.3:
-there the oracle's own bf16-storage gradients differ from its exact ones
-by 7% normwise and up to 2-4 rms in single elements of dL/dWhat_q, so one
-rounding decision taken the other way at a storage point moves isolated
-elements by a fifth of rms, while a misplaced row, column or head still
-fails the normwise 1e-2.  The chained test gives the second block the first
-quantized block's output as its input (Algorithm 1 run from the bottom
-block up), each side computing that input itself.
+tokens; grouped-query cases C = 512 in 4 query heads over 2 or 1 key/value
+heads; two sequences of 512 tokens in the long cases), norm weights
+1 + 0.1 N(0, 1), quantizer parameters from the oracle's fixed-minimum
+clipping with a greedy start.  The oracle evaluates the block in fp64 with
+the device's bf16 storage points and never sees device output; the target
+Y_ref is the oracle's (checked against the device's own full-precision
+forward to 2e-2, then given to the device so that both sides share it).
+
+Bars: codes bit-exact per matrix; the loss within 1e-2; dL/dWhat of all
+seven matrices within 1e-2 normwise and, per element, within 8 sigma plus
+the largest single rounding flip of the product's own operands plus one
+bf16 ulp of the value (the device stores dL/dWhat in bf16), where sigma is
+the spread that bf16 rounding decisions taken the other way at the
+storage points propagate to that element (tests/block_bounds.py: a variance
+model in which a stored value whose inputs differ by s rounds to the other
+bf16 neighbour with probability s / ulp).  Calibrated on the oracle against
+itself with fp32-sized perturbations before every rounding, the largest
+observed difference is 3 sigma; sigma is a small fraction of the value for
+most elements and grows only where the result is genuinely sensitive (the
+q and k gradients of rows whose attention has near-ties), so a misplaced,
+transposed or mis-scaled gradient still fails both bars.  The chained test
+gives the second block the first quantized block's output as its input
+(Algorithm 1 run from the bottom block up), each side computing that input
+itself, checked on the loss and normwise; block 2 is then checked per
+element on inputs both sides share.
 """
 import numpy as np
 import pytest
 import torch
 
+import block_bounds as BB
 import oracle.block_decoder as D
 import oracle.uniquan as O
 from paper_2506_03781_amd import synth
@@ -60,6 +67,39 @@ def close(x, ref, tol=1e-2, elem=0.1, what=""):
     rms = np.sqrt(np.mean(ref * ref))
     ratio = np.abs(x - ref) / np.maximum(np.abs(ref), rms)
     assert np.all(ratio <= elem), f"{what}: {(ratio > elem).sum()} of {ratio.size} elements, worst {ratio.max():.3g}"
+
+
+K_SIGMA = 8.0
+
+
+def share_target(blk, Y_ref):
+    """The oracle's target, checked against the device's own and then given
+    to the device (fp32, as it stores it); returns it as the oracle uses it."""
+    Y32 = np.asarray(Y_ref, F32)
+    assert np.allclose(host(blk.Yref), Y32, rtol=2e-2, atol=2e-2 * np.abs(Y32).max())
+    blk.Yref.copy_(torch.from_numpy(Y32).to(blk.Yref.device))
+    return Y32.astype(np.float64)
+
+
+def check_step(blk, qs, Xhat, Y32, what, g1, g2, n_seq, H_, n_kv, what_for=""):
+    """Loss within 1e-2; each dL/dWhat within 1e-2 normwise and, per element,
+    within K_SIGMA sigma plus the largest single rounding flip of its operands
+    plus one bf16 ulp of the value (the device stores dL/dWhat in bf16)."""
+    st, sig, flip = BB.decoder_step_spread(Xhat, Y32, what, g1, g2, n_seq, H_, n_kv=n_kv)
+    loss = float(blk.loss.item())
+    assert abs(loss - st["loss"]) <= 1e-2 * st["loss"], (what_for, loss, st["loss"])
+    for n in what:
+        x, ref = host(qs[n].G), st["grads"][n]
+        nrm = np.linalg.norm(ref)
+        assert np.linalg.norm(x - ref) <= 1e-2 * nrm, f"{what_for} {n}: normwise {np.linalg.norm(x - ref) / nrm}"
+        rms = np.sqrt(np.mean(ref * ref))
+        bar = K_SIGMA * sig[n] + flip[n] + 2.0 ** -8 * np.abs(ref) + 1e-6 * rms  # dL/dWhat is stored in bf16
+        ratio = np.abs(x - ref) / bar
+        rel = bar / np.maximum(np.abs(ref), rms)
+        print(f"{what_for} dL/dWhat_{n}: worst |x - ref| / bar {ratio.max():.3g}; bar / max(|ref|, rms) "
+              f"median {np.median(rel):.2g} max {rel.max():.2g}")
+        assert np.all(ratio <= 1.0), f"{what_for} {n}: {(ratio > 1).sum()} of {ratio.size} elements, worst {ratio.max():.3g}"
+    return st
 
 
 def shapes_for(C_, I_, n_kv_d):
@@ -103,27 +143,29 @@ def wfp(mats):
     return {n: np.asarray(W, np.float64) for n, (W, _, _) in mats.items()}
 
 
-@pytest.mark.parametrize("qk_scale", [1.0, 6.0])
-def test_decoder_block_step(qk_scale):
-    X, mats, g1, g2 = make_block(3, qk_scale)
-    blk, qs = device_block(mats, g1, g2)
+def run_and_check(seed, qk_scale=1.0, shapes=SHAPES, H_=H, n_kv=None, T_=T, n_seq=N_SEQ, what_for=""):
+    """One FULL-mode step of a device block against the oracle on shared
+    inputs and target: codes bit-exact, then check_step."""
+    X, mats, g1, g2 = make_block(seed, qk_scale, shapes, T_=T_)
+    blk, qs = device_block(mats, g1, g2, H_, n_kv, T_=T_, n_seq=n_seq)
+    nk = H_ if n_kv is None else n_kv
     blk.prepare(X)
+    Y_ref = D.decoder_forward(X, wfp(mats), g1, g2, n_seq, H_, store=O.bf16_rne, n_kv=nk)["Y"]
+    Y32 = share_target(blk, Y_ref)
     blk.set_input(X)
     blk.forward_backward(uq.MAP_FULL)
     torch.cuda.synchronize()
-
     f = oracle_what(mats)
     for n in mats:
-        assert np.array_equal(host(qs[n].codes).reshape(SHAPES[n]).astype(np.uint8), f[n]["codes"]), f"{n} codes"
-    Y_ref = D.decoder_forward(X, wfp(mats), g1, g2, N_SEQ, H, store=O.bf16_rne)["Y"]
-    assert np.allclose(host(blk.Yref), Y_ref, rtol=2e-2, atol=2e-2 * np.abs(Y_ref).max())
-    st = D.decoder_step(X, Y_ref, {n: f[n]["what_bf16"] for n in mats}, g1, g2, N_SEQ, H, store=O.bf16_rne)
+        assert np.array_equal(host(qs[n].codes).reshape(shapes[n]).astype(np.uint8), f[n]["codes"]), f"{n} codes"
+    return check_step(blk, qs, X, Y32, {n: f[n]["what_bf16"] for n in mats}, g1, g2, n_seq, H_, nk, what_for)
+
+
+@pytest.mark.parametrize("qk_scale", [1.0, 6.0])
+def test_decoder_block_step(qk_scale):
+    st = run_and_check(3, qk_scale, what_for=f"qk {qk_scale}")
     if qk_scale > 1.0:   # the attention is far from uniform
         assert np.mean(np.max(st["P"][..., 8:, :], axis=-1)) > 0.3
-    loss = float(blk.loss.item())
-    assert abs(loss - st["loss"]) <= 1e-2 * st["loss"], (loss, st["loss"])
-    for n in mats:
-        close(host(qs[n].G), st["grads"][n], what=f"dL/dWhat_{n}")
 
 
 def test_decoder_blocks_chained():
@@ -161,14 +203,13 @@ def test_decoder_blocks_chained():
     assert abs(float(b2.loss.item()) - st["loss"]) <= 1e-2 * st["loss"]
     for n in m2:
         close(host(q2[n].G), st["grads"][n], elem=np.inf, what=f"chained block 2 dL/dWhat_{n}")
-    # block 2 on the oracle's block-1 outputs
+    # block 2 on the oracle's block-1 outputs and target
     b2.prepare(x2_o)
+    Y2_32 = share_target(b2, Y2_ref)
     b2.set_input(xhat2_o)
     b2.forward_backward(uq.MAP_FULL)
     torch.cuda.synchronize()
-    assert abs(float(b2.loss.item()) - st["loss"]) <= 1e-2 * st["loss"]
-    for n in m2:
-        close(host(q2[n].G), st["grads"][n], what=f"block 2 dL/dWhat_{n}")
+    check_step(b2, q2, xhat2_o, Y2_32, what2, g1b, g2b, N_SEQ, H, H, "block 2")
 
 
 def test_decoder_block_step_updates():
@@ -194,55 +235,18 @@ def test_decoder_block_grouped_query(n_kv, qk_scale):
     """Grouped-query attention: 4 query heads over n_kv key/value heads; the
     gradients of the shared k and v matrices sum over each group."""
     Hq, Cq, Iq = 4, 512, 384
-    shapes = shapes_for(Cq, Iq, n_kv * (Cq // Hq))
-    X, mats, g1, g2 = make_block(11 + n_kv, qk_scale, shapes)
-    blk, qs = device_block(mats, g1, g2, Hq, n_kv)
-    blk.prepare(X)
-    blk.set_input(X)
-    blk.forward_backward(uq.MAP_FULL)
-    torch.cuda.synchronize()
-
-    f = oracle_what(mats)
-    for n in mats:
-        assert np.array_equal(host(qs[n].codes).reshape(shapes[n]).astype(np.uint8), f[n]["codes"]), f"{n} codes"
-    Y_ref = D.decoder_forward(X, wfp(mats), g1, g2, N_SEQ, Hq, store=O.bf16_rne, n_kv=n_kv)["Y"]
-    assert np.allclose(host(blk.Yref), Y_ref, rtol=2e-2, atol=2e-2 * np.abs(Y_ref).max())
-    st = D.decoder_step(X, Y_ref, {n: f[n]["what_bf16"] for n in mats}, g1, g2, N_SEQ, Hq, store=O.bf16_rne,
-                        n_kv=n_kv)
-    loss = float(blk.loss.item())
-    assert abs(loss - st["loss"]) <= 1e-2 * st["loss"], (loss, st["loss"])
-    for n in mats:
-        close(host(qs[n].G), st["grads"][n], elem=0.3, what=f"dL/dWhat_{n}")
+    run_and_check(11 + n_kv, qk_scale, shapes_for(Cq, Iq, n_kv * (Cq // Hq)), Hq, n_kv,
+                  what_for=f"n_kv {n_kv} qk {qk_scale}")
 
 
 @pytest.mark.parametrize("n_kv", [2, 1])
 def test_decoder_block_step_long_sequences(n_kv):
     """Two sequences of 512 tokens (several query and key blocks of the fused
     attention per head, its pipelined tiles and the diagonal masking over a
-    long causal range): codes bit-exact, loss within 1e-2, dL/dWhat within
-    1e-2 normwise and the per-element bars of the short-sequence tests."""
-    n_seq, Ls = 2, 512
-    Tl = n_seq * Ls
+    long causal range), multi-head and grouped-query."""
     Hq, Cq, Iq = 2, 256, 384
-    shapes = shapes_for(Cq, Iq, n_kv * (Cq // Hq))
-    X, mats, g1, g2 = make_block(21 + n_kv, 1.0, shapes, T_=Tl)
-    blk, qs = device_block(mats, g1, g2, Hq, n_kv, T_=Tl, n_seq=n_seq)
-    blk.prepare(X)
-    blk.set_input(X)
-    blk.forward_backward(uq.MAP_FULL)
-    torch.cuda.synchronize()
-
-    f = oracle_what(mats)
-    for n in mats:
-        assert np.array_equal(host(qs[n].codes).reshape(shapes[n]).astype(np.uint8), f[n]["codes"]), f"{n} codes"
-    Y_ref = D.decoder_forward(X, wfp(mats), g1, g2, n_seq, Hq, store=O.bf16_rne, n_kv=n_kv)["Y"]
-    assert np.allclose(host(blk.Yref), Y_ref, rtol=2e-2, atol=2e-2 * np.abs(Y_ref).max())
-    st = D.decoder_step(X, Y_ref, {n: f[n]["what_bf16"] for n in mats}, g1, g2, n_seq, Hq, store=O.bf16_rne,
-                        n_kv=n_kv)
-    loss = float(blk.loss.item())
-    assert abs(loss - st["loss"]) <= 1e-2 * st["loss"], (loss, st["loss"])
-    for n in mats:
-        close(host(qs[n].G), st["grads"][n], elem=0.1 if n_kv == Hq else 0.3, what=f"dL/dWhat_{n}")
+    run_and_check(21 + n_kv, 1.0, shapes_for(Cq, Iq, n_kv * (Cq // Hq)), Hq, n_kv, T_=2 * 512, n_seq=2,
+                  what_for=f"L 512 n_kv {n_kv}")
 
 
 def test_decoder_block_fused_step_form():
