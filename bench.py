@@ -151,9 +151,15 @@ STEP_SOURCES = ("fq_fwd.hip", "fq_bwd.hip", "gemm.hip", "uq_device.h", "uq_launc
 
 
 def src_hash() -> str:
+    """Hash of the step kernels' sources with comments and blank space taken
+    out, so that an edit of a comment keeps the counters that were taken."""
+    import re
     h = hashlib.sha256()
     for f in STEP_SOURCES:
-        h.update(open(os.path.join(CSRC, f), "rb").read())
+        text = open(os.path.join(CSRC, f)).read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 

@@ -2,16 +2,21 @@
 // (Theorem 1, Eq. (4)), binary-coding dequantization (Sec. 2.3) and the
 // greedy binary-coding start (appendix "General alternating update").
 //
-// Work split of the forward: each wavefront owns 512 consecutive weights
-// (8 per lane, 16-byte bf16 / 2 x 16-byte fp32 loads; g divides 512, so a
-// group never straddles wavefronts and a 128-weight group is 16 lanes) and
-// builds the sorted level tables of its own groups in a private LDS region,
-// with wave-local ordering only; every lane then maps its 8 weights by an LDS
-// binary search (FULL), a neighbour-table lookup (LOCAL) or the stored code
-// (FROZEN).  The fold, dequantization and greedy kernels work on tiles of
-// whole groups per workgroup with workgroup-wide tables.  HBM-bound: per
-// weight the forward reads W (2 B) and s (4 B) and writes What (2 B) and the
-// code byte (1 B).
+// Work split of the forward for groups of up to 512 weights (a power of two,
+// so a group never straddles wavefronts): each wavefront owns 512
+// consecutive weights (8 per lane, 16-byte bf16 / 2 x 16-byte fp32 loads; a
+// 128-weight group is 16 lanes) and builds the sorted level tables of its own
+// groups in a private LDS region, with wave-local ordering only; every lane
+// then maps its 8 weights by an LDS binary search (FULL), a neighbour-table
+// lookup (LOCAL) or the stored code (FROZEN).  fq_step_kernel is the same
+// forward preceded, in the same pass, by the straight-through backward and
+// the SGD update of the group's parameters (the previous step's end).  The
+// fold, dequantization and greedy kernels work on tiles of whole groups per
+// workgroup with workgroup-wide tables.  Groups of more than 512 weights (a
+// whole row per group) take the *_big kernels: one workgroup of 256 lanes per
+// group, its tables built once in LDS and its sums reduced across the
+// wavefronts in a fixed order.  HBM-bound: per weight the forward reads W
+// (2 B) and s (4 B) and writes What (2 B) and the code byte (1 B).
 #include "uq_device.h"
 #include "uq_launch.h"
 
