@@ -655,9 +655,7 @@ def build_layers(wl, args, want_cpu):
         wdt = torch.bfloat16 if spec.dtype == "bf16" else torch.float32
         for k in wl.ks:
             lay = QuantLayer(m.W, m.X, m.s, k, g, w_dtype=wdt, residual=not args.target)
-            # the unified initialisation takes groups of up to 512 weights; larger
-            # (per-row) groups start from the greedy binary coding (Delta = 1, z_U = 0)
-            if args.init == "unified" and g <= 512:
+            if args.init == "unified":
                 if not layers:
                     lay.init_unified(args.init_grid, args.init_rounds, args.init_clip)  # first-launch warm-up
                 e0, e1 = TimingEvent(), TimingEvent()

@@ -37,8 +37,8 @@
  *           [8, 512] or a multiple of 8 above 512 (e.g. the per-row groups
  *           g = C of the paper's 7B / 8B settings, 4096, 11008 or 14336
  *           weights; one workgroup per group then).  The unified
- *           initialisation and the fused gradient-GEMM backward take
- *           g <= 512 and g <= 128 respectively.
+ *           initialisation takes g <= 16384, the fused gradient-GEMM
+ *           backward g <= 128.
  *           1 <= k <= 7.  T (calibration tokens) is a multiple of 8.
  * Alignment Per-weight arrays, X, Xt, Yt and workspaces: 16 bytes.
  *           Per-group and per-row arrays: 4 bytes.
@@ -635,17 +635,21 @@ uq_status uniquan_init_greedy(int64_t R, int64_t C, int k, int g,
  *                      z_B <- mean(wbar - C alpha) when grid_G == 1;
  *     e' = ||w - what||^2, what = the fp32 output of uniquan_fq_fwd (FULL);
  *   keep the first candidate, then any with strictly smaller e'.
- * Fixed fp32 evaluation order: group sums are pairwise with adjacent pairing;
- * the inverse of C^T C is exact (integer adjugate over the determinant), its
- * product with C^T (wbar - z_B) formed in fp64 and rounded to fp32; a singular
- * C^T C keeps the previous alpha.  Results are bit-reproducible.
+ * Fixed fp32 evaluation order: group sums are pairwise with adjacent pairing
+ * over the group zero-padded to a power of two; means are those sums divided
+ * by g; the inverse of C^T C is taken through its exact integer adjugate and
+ * determinant, its product with C^T (wbar - z_B) formed in fp64 (each product
+ * rounded, added in ascending order; exact for g <= 512) and divided by the
+ * determinant, then rounded to fp32; a singular C^T C keeps the previous
+ * alpha.  Results are bit-reproducible.  Groups above 512 weights (per-row
+ * groups) run one workgroup per group.
  *
  * W [R*C] w_dtype (16-byte aligned).  Out (fp32, caller-owned): delta, z_u,
  * z_b [Gn], alpha [Gn*k].  Optional out (NULL = skipped): codes [R*C] uint8,
  * the kept candidate's FULL-mapping codes (bit 7 clear; 8-byte aligned);
  * err [Gn], its e'; s [R*C] and s_r [R] filled with 1.
- * Limits: 1 <= k <= 4 (UQ_EUNSUPPORTED above), g a power of two in 8..512,
- * 1 <= grid_G <= 4096, 0 <= alt_T <= 10000, clip in {0, 1, 2} (UQ_EINVAL).
+ * Limits: 1 <= k <= 4 (UQ_EUNSUPPORTED above), g as for the quantizer and at
+ * most 16384 (UQ_EUNSUPPORTED above), 1 <= grid_G <= 4096, 0 <= alt_T <= 10000, clip in {0, 1, 2} (UQ_EINVAL).
  * Preconditions (not checked): finite weights whose squares are finite.
  */
 uq_status uniquan_init_unified(int64_t R, int64_t C, int k, int g,

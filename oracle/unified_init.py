@@ -28,13 +28,17 @@ whole initialisation is evaluated as a float32 decision mirror with a fixed,
 stated order of operations that the GPU follows too:
 
 * every sum over a group uses pairwise summation with adjacent pairing
-  (level by level, element j of the next level is fl(x[2j] + x[2j+1]));
-  g is a power of two;
+  (level by level, element j of the next level is fl(x[2j] + x[2j+1])),
+  over the group zero-padded to the next power of two (a whole row of 4096,
+  11008 or 14336 weights is one group in the per-row setting);
 * C^T C is a matrix of integers, and its inverse is taken exactly: the
   adjugate and determinant are exact integers (cofactor expansion), so
-  alpha_a = fl32( fl64(sum_b adj_ab v_b) / det ) with v = C^T (wbar - z_B 1)
-  from the pairwise sums, the products adj_ab v_b exact in float64 and added
-  in ascending b; a singular C^T C (det = 0) leaves alpha unchanged;
+  alpha_a = fl32( fl64(sum_b adj_ab v_b) / fl64(det) ) with v = C^T (wbar - z_B 1)
+  from the pairwise sums, each product adj_ab v_b rounded to float64 and the
+  products added in ascending b (for g <= 512 the adjugate stays below 2^27
+  and every product is exact; above, |adj| <= g^3 < 2^53 is still exact and
+  only the products and sums round); a singular C^T C (det = 0) leaves
+  alpha unchanged;
 * the nearest level is the fp32 argmin of |fl(wbar - q)| over the ascending
   level table, ties to the lower level (the same rule as the forward);
 * a constant group (w_M = w_m) takes Delta' = 1;
@@ -42,8 +46,9 @@ stated order of operations that the GPU follows too:
   strictly smaller (the paper starts the running minimum at the largest
   number, which is the same whenever the errors are finite).
 
-Restricted to 1 <= k <= 4 (the paper's bit widths) and g a power of two <= 512,
-which keeps the adjugate below 2^27 and every product adj_ab v_b exact.
+Restricted to 1 <= k <= 4 (the paper's bit widths); any g (the library takes
+multiples of 8 that divide C: powers of two up to 512 and per-row groups up
+to 16384).
 """
 from __future__ import annotations
 
@@ -61,11 +66,16 @@ CLIP_BALANCED = 2
 # Sums over a group.
 # ----------------------------------------------------------------------------
 def tree_sum_f32(x: np.ndarray) -> np.ndarray:
-    """Pairwise sum over the last axis (length a power of two), fp32:
-    ((x0 + x1) + (x2 + x3)) + ((x4 + x5) + (x6 + x7)) + ..."""
+    """Pairwise sum over the last axis, fp32:
+    ((x0 + x1) + (x2 + x3)) + ((x4 + x5) + (x6 + x7)) + ...,
+    the axis zero-padded to the next power of two."""
     x = np.asarray(x, F32)
     n = x.shape[-1]
-    assert n >= 1 and n & (n - 1) == 0, "group size must be a power of two"
+    assert n >= 1
+    p2 = 1 << (n - 1).bit_length()
+    if p2 != n:
+        pad = np.zeros(x.shape[:-1] + (p2 - n,), F32)
+        x = np.concatenate([x, pad], axis=-1)
     while x.shape[-1] > 1:
         x = (x[..., 0::2] + x[..., 1::2]).astype(F32)
     return x[..., 0]

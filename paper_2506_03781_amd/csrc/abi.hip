@@ -316,7 +316,7 @@ uq_status uniquan_init_unified(int64_t R, int64_t C, int k, int g, const void* W
   const char* fn = "uniquan_init_unified";
   if (uq_status st = check_quant_shape(fn, R, C, k, g)) return st;
   if (k > 4) return fail(UQ_EUNSUPPORTED, "%s: k = %d, supported 1..4", fn, k);
-  if (g > 512) return fail(UQ_EUNSUPPORTED, "%s: g = %d, supported up to 512", fn, g);
+  if (g > 16384) return fail(UQ_EUNSUPPORTED, "%s: g = %d, supported up to 16384", fn, g);
   if (!is_dtype(w_dtype)) return fail(UQ_EINVAL, "%s: bad dtype", fn);
   if (grid_G < 1 || grid_G > 4096) return fail(UQ_EINVAL, "%s: grid_G = %d, must be in 1..4096", fn, grid_G);
   if (alt_T < 0 || alt_T > 10000) return fail(UQ_EINVAL, "%s: alt_T = %d, must be in 0..10000", fn, alt_T);

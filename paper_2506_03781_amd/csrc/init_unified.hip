@@ -395,6 +395,403 @@ __global__ __launch_bounds__(kThreads) void init_unified_kernel(InitArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Groups of more than 512 weights (a whole row per group, up to 16384): one
+// workgroup per group, NW wavefronts, lane l holding the E consecutive
+// elements l E .. l E + E - 1 of the group zero-padded to P = 64 NW E (the
+// next power of two; E >= 8), so the pairwise tree over the padded group is
+// the lane's own pairwise sum of its E values, then the butterfly over the 64
+// lanes of a wavefront, then the wavefronts' sums pairwise in order.  The
+// weights, their transforms and the codes stay in registers; each wavefront
+// keeps its own copy of the level table in LDS.  C^T C entries reach g, so
+// its adjugate (|adj| <= g^3 < 2^42) and determinant are int64, exactly
+// converted (the determinant rounded) to fp64, and the products adj_ab v_b
+// round in fp64 and are added in ascending b, as written.
+// ---------------------------------------------------------------------------
+// Pairwise sum of E values produced in index order (adjacent pairing): a
+// stack of partial sums, one per level.
+template <int E>
+struct LaneTree {
+  static constexpr int LG = __builtin_ctz(E);
+  float st[LG + 1];
+  template <int I>
+  __device__ __forceinline__ void push(float v) {
+#pragma unroll
+    for (int l = 0; l < LG; ++l) {
+      if (((I >> l) & 1) == 0) {
+        st[l] = v;
+        return;
+      }
+      v = st[l] + v;
+    }
+    st[LG] = v;
+  }
+};
+
+template <int E, int I = 0, typename F>
+__device__ __forceinline__ void tree_push_all(LaneTree<E>& t, const F& f) {
+  if constexpr (I < E) {
+    t.template push<I>(f(I));
+    tree_push_all<E, I + 1>(t, f);
+  }
+}
+
+// Workgroup-wide pairwise sums of NV lane values (each lane already holds its
+// own subtree's sum), left in every lane.
+template <int NW, int NV>
+__device__ __forceinline__ void block_tree(float (&t)[NV], float* red, int lane, int wave) {
+#pragma unroll
+  for (int v = 0; v < NV; ++v) t[v] = group_reduce<64>(t[v], AddF());
+  if (lane == 0) {
+#pragma unroll
+    for (int v = 0; v < NV; ++v) red[v * NW + wave] = t[v];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int v = 0; v < NV; ++v) {
+    if constexpr (NW == 2) t[v] = red[v * NW] + red[v * NW + 1];
+    else t[v] = (red[v * NW] + red[v * NW + 1]) + (red[v * NW + 2] + red[v * NW + 3]);
+  }
+  __syncthreads();
+}
+
+template <int NW, int NV>
+__device__ __forceinline__ void block_isum(int (&t)[NV], int* red, int lane, int wave) {
+#pragma unroll
+  for (int v = 0; v < NV; ++v) t[v] = group_reduce<64>(t[v], AddI());
+  if (lane == 0) {
+#pragma unroll
+    for (int v = 0; v < NV; ++v) red[v * NW + wave] = t[v];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int v = 0; v < NV; ++v) {
+    int s = 0;
+#pragma unroll
+    for (int q = 0; q < NW; ++q) s += red[v * NW + q];
+    t[v] = s;
+  }
+  __syncthreads();
+}
+
+// Cofactor of the symmetric integer matrix M (int64: entries up to 2^14).
+template <int K>
+__device__ __forceinline__ int64_t cofactor64(const int (&M)[K][K], int r, int c) {
+  int64_t S[3][3];
+#pragma unroll
+  for (int i = 0, ii = 0; i < K; ++i) {
+    if (i == r) continue;
+#pragma unroll
+    for (int j = 0, jj = 0; j < K; ++j) {
+      if (j == c) continue;
+      S[ii][jj] = M[i][j];
+      ++jj;
+    }
+    ++ii;
+  }
+  int64_t d;
+  if constexpr (K == 2) {
+    d = S[0][0];
+  } else if constexpr (K == 3) {
+    d = S[0][0] * S[1][1] - S[0][1] * S[1][0];
+  } else {
+    d = S[0][0] * (S[1][1] * S[2][2] - S[1][2] * S[2][1]) - S[0][1] * (S[1][0] * S[2][2] - S[1][2] * S[2][0]) +
+        S[0][2] * (S[1][0] * S[2][1] - S[1][1] * S[2][0]);
+  }
+  return ((r + c) & 1) ? -d : d;
+}
+
+template <int K>
+__device__ __forceinline__ void solve_alpha64(const int (&M)[K][K], const float (&v)[K], float (&al)[K]) {
+  int64_t adj[K][K];
+  if constexpr (K == 1) {
+    adj[0][0] = 1;
+  } else {
+#pragma unroll
+    for (int a = 0; a < K; ++a)
+#pragma unroll
+      for (int b = a; b < K; ++b) {
+        adj[a][b] = cofactor64<K>(M, b, a);
+        adj[b][a] = adj[a][b];
+      }
+  }
+  int64_t det = 0;
+#pragma unroll
+  for (int b = 0; b < K; ++b) det += int64_t(M[0][b]) * adj[b][0];
+  if (det == 0) return;
+  const double dd = double(det);
+#pragma unroll
+  for (int a = 0; a < K; ++a) {
+    double S = double(adj[a][0]) * double(v[0]);
+#pragma unroll
+    for (int b = 1; b < K; ++b) {
+      const double pr = double(adj[a][b]) * double(v[b]);
+      S = S + pr;
+    }
+    al[a] = float(S / dd);
+  }
+}
+
+template <int WDT, int K, int NW, int E>
+__global__ __launch_bounds__(NW * 64) void init_unified_big_kernel(InitArgs a, int g) {
+  constexpr int L = 1 << K;
+  constexpr int NP = E / 4;  // packed code words per lane
+  __shared__ float tab_raw[NW][L], tab_qs[NW][L];
+  __shared__ uint8_t tab_cof[NW][L];
+  __shared__ float red[8 * NW];
+  __shared__ int redi[8 * NW];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t gid = blockIdx.x;
+  const int64_t goff = gid * int64_t(g);
+  const int e0 = int(threadIdx.x) * E;  // first padded element of this lane
+  float* raw = tab_raw[wave];
+  float* qs = tab_qs[wave];
+  uint8_t* cof = tab_cof[wave];
+
+  float w[E];
+#pragma unroll
+  for (int c = 0; c < E; c += 8) {
+    float v[8];
+    if (e0 + c < g) {
+      load8<WDT>(a.W, goff + e0 + c, v);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = 0.0f;
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) w[c + i] = v[i];
+  }
+  // validity: g is a multiple of 8, so chunks of 8 are whole
+  uint32_t valid8 = 0;  // bit c/8: chunk c .. c+7 real
+#pragma unroll
+  for (int c = 0; c < E; c += 8)
+    if (e0 + c < g) valid8 |= 1u << (c / 8);
+#define UQ_VALID(i) (((valid8 >> ((i) / 8)) & 1u) != 0u)
+
+  float mm[2] = {INFINITY, -INFINITY};
+#pragma unroll
+  for (int i = 0; i < E; ++i)
+    if (UQ_VALID(i)) {
+      mm[0] = fminf(mm[0], w[i]);
+      mm[1] = fmaxf(mm[1], w[i]);
+    }
+  mm[0] = group_reduce<64>(mm[0], MinF());
+  mm[1] = group_reduce<64>(mm[1], MaxF());
+  if (lane == 0) {
+    red[wave] = mm[0];
+    red[NW + wave] = mm[1];
+  }
+  __syncthreads();
+  float wm = red[0], wM = red[NW];
+#pragma unroll
+  for (int q = 1; q < NW; ++q) {
+    wm = fminf(wm, red[q]);
+    wM = fmaxf(wM, red[NW + q]);
+  }
+  __syncthreads();
+
+  const float L1 = float(L - 1);
+  const float zb0 = L1 * 0.5f;
+  const float gf = float(g);
+  float best_d = 1.0f, best_zu = 0.0f, best_zb = zb0, best_e = 0.0f, best_al[K];
+  uint32_t best_cw[NP];
+#pragma unroll
+  for (int b = 0; b < K; ++b) best_al[b] = 0.0f;
+#pragma unroll
+  for (int q = 0; q < NP; ++q) best_cw[q] = 0u;
+
+  for (int j = 1; j <= a.G; ++j) {
+    const float gamma = float(j) / float(a.G);
+    float dl = (gamma * (wM - wm)) / L1;
+    if (!(dl > 0.0f)) dl = 1.0f;
+    float zu;
+    if (a.clip == 0) zu = -(wm / dl);
+    else if (a.clip == 1) zu = L1 - (wM / dl);
+    else zu = -((gamma * wm) / dl);
+    float wbar[E];
+#pragma unroll
+    for (int i = 0; i < E; ++i) wbar[i] = (w[i] / dl) + zu;
+    float zb = zb0;
+
+    // greedy start, one bit at a time (r recomputed from x and the bits so far)
+    float al[K];
+    uint32_t cw[NP];
+#pragma unroll
+    for (int q = 0; q < NP; ++q) cw[q] = 0u;
+#pragma unroll
+    for (int b = 0; b < K; ++b) {
+      LaneTree<E> tr;
+      tree_push_all<E>(tr, [&](int i) {
+        float r = wbar[i] - zb;
+        for (int bb = 0; bb < b; ++bb) r = ((cw[i / 4] >> (8 * (i & 3) + bb)) & 1u) ? r - al[bb] : r + al[bb];
+        return UQ_VALID(i) ? fabsf(r) : 0.0f;
+      });
+      float t[1] = {tr.st[LaneTree<E>::LG]};
+      block_tree<NW, 1>(t, red, lane, wave);
+      const float ai = t[0] / gf;
+#pragma unroll
+      for (int i = 0; i < E; ++i) {
+        float r = wbar[i] - zb;
+        for (int bb = 0; bb < b; ++bb) r = ((cw[i / 4] >> (8 * (i & 3) + bb)) & 1u) ? r - al[bb] : r + al[bb];
+        if (UQ_VALID(i) && r >= 0.0f) cw[i / 4] |= 1u << (8 * (i & 3) + b);
+      }
+      al[b] = ai;
+    }
+
+    for (int t = 0; t < a.T; ++t) {
+      // alpha <- (C^T C)^{-1} C^T (wbar - z_B)
+      float v[K];
+#pragma unroll
+      for (int b = 0; b < K; ++b) {
+        LaneTree<E> tr;
+        tree_push_all<E>(tr, [&](int i) {
+          const float x = wbar[i] - zb;
+          const bool bit = (cw[i / 4] >> (8 * (i & 3) + b)) & 1u;
+          return UQ_VALID(i) ? (bit ? x : -x) : 0.0f;
+        });
+        v[b] = tr.st[LaneTree<E>::LG];
+      }
+      block_tree<NW, K>(v, red, lane, wave);
+      int M[K][K];
+      {
+        int dis[K * K];
+#pragma unroll
+        for (int p = 0; p < K * K; ++p) dis[p] = 0;
+#pragma unroll
+        for (int p = 0; p < K; ++p)
+#pragma unroll
+          for (int q = p + 1; q < K; ++q) {
+            int c = 0;
+#pragma unroll
+            for (int w4 = 0; w4 < NP; ++w4)
+              c += __builtin_popcount(((cw[w4] >> p) ^ (cw[w4] >> q)) & 0x01010101u);
+            dis[p * K + q] = c;
+          }
+        block_isum<NW, K * K>(dis, redi, lane, wave);
+#pragma unroll
+        for (int p = 0; p < K; ++p) {
+          M[p][p] = g;
+#pragma unroll
+          for (int q = p + 1; q < K; ++q) {
+            M[p][q] = g - 2 * dis[p * K + q];
+            M[q][p] = M[p][q];
+          }
+        }
+      }
+      solve_alpha64<K>(M, v, al);
+
+      // C <- nearest level's code (padding keeps code 0)
+      build_table<K>(raw, qs, cof, al, zb, lane, 64);
+      uint32_t nw[NP];
+#pragma unroll
+      for (int q = 0; q < NP; ++q) nw[q] = 0u;
+#pragma unroll
+      for (int i = 0; i < E; ++i) {
+        if (UQ_VALID(i)) {
+          float dist;
+          nw[i / 4] |= uint32_t(cof[nearest_full_k<K>(qs, wbar[i], dist)]) << (8 * (i & 3));
+        }
+      }
+      const float zb_prev = zb;
+      if (a.G == 1) {
+        LaneTree<E> tr;
+        tree_push_all<E>(tr, [&](int i) {
+          const uint32_t code = (nw[i / 4] >> (8 * (i & 3))) & 0xFFu;
+          float ca = 0.0f;
+          for (int b = 0; b < K; ++b) ca = ((code >> b) & 1u) ? ca + al[b] : ca - al[b];
+          return UQ_VALID(i) ? wbar[i] - ca : 0.0f;
+        });
+        float tz[1] = {tr.st[LaneTree<E>::LG]};
+        block_tree<NW, 1>(tz, red, lane, wave);
+        zb = tz[0] / gf;
+      }
+      int same = 1;
+#pragma unroll
+      for (int q = 0; q < NP; ++q) same &= int(nw[q] == cw[q]);
+      same &= int(zb == zb_prev);
+#pragma unroll
+      for (int q = 0; q < NP; ++q) cw[q] = nw[q];
+      int st1[1] = {same};
+      block_isum<NW, 1>(st1, redi, lane, wave);
+      if (st1[0] == NW * 64) break;  // every lane at a fixed point (uniform)
+    }
+
+    // candidate error ||w - Q*(w)||^2 with the forward's FULL mapping
+    build_table<K>(raw, qs, cof, al, zb, lane, 64);
+    uint32_t cc[NP];
+#pragma unroll
+    for (int q = 0; q < NP; ++q) cc[q] = 0u;
+    LaneTree<E> tr;
+    tree_push_all<E>(tr, [&](int i) {
+      if (!UQ_VALID(i)) return 0.0f;
+      float dist;
+      const int pos = nearest_full_k<K>(qs, wbar[i], dist);
+      cc[i / 4] |= uint32_t(cof[pos]) << (8 * (i & 3));
+      const float what = dl * (qs[pos] - zu);
+      const float d = w[i] - what;
+      return d * d;
+    });
+    float te[1] = {tr.st[LaneTree<E>::LG]};
+    block_tree<NW, 1>(te, red, lane, wave);
+    const float e = te[0];
+    if (j == 1 || e < best_e) {
+      best_e = e;
+      best_d = dl;
+      best_zu = zu;
+      best_zb = zb;
+#pragma unroll
+      for (int b = 0; b < K; ++b) best_al[b] = al[b];
+#pragma unroll
+      for (int q = 0; q < NP; ++q) best_cw[q] = cc[q];
+    }
+  }
+
+#pragma unroll
+  for (int c = 0; c < E; c += 8) {
+    if (e0 + c >= g) continue;
+    if (a.codes) store8u8(a.codes, goff + e0 + c, make_uint2(best_cw[c / 4], best_cw[c / 4 + 1]));
+    if (a.s) {
+      const float one[8] = {1.0f, 1.0f, 1.0f, 1.0f, 1.0f, 1.0f, 1.0f, 1.0f};
+      store8f(a.s, goff + e0 + c, one);
+    }
+  }
+#undef UQ_VALID
+  if (threadIdx.x == 0) {
+    a.delta[gid] = best_d;
+    a.z_u[gid] = best_zu;
+    a.z_b[gid] = best_zb;
+#pragma unroll
+    for (int b = 0; b < K; ++b) a.alpha[gid * K + b] = best_al[b];
+    if (a.err) a.err[gid] = best_e;
+    if (a.s_r && (gid % a.gpr) == 0) a.s_r[gid / a.gpr] = 1.0f;
+  }
+}
+
+template <int WDT, int K>
+static void launch_init_big(const InitArgs& a, int g, int64_t groups, hipStream_t st) {
+  int p2 = 1024;
+  while (p2 < g) p2 <<= 1;
+  const dim3 grid(static_cast<unsigned>(groups));
+  switch (p2) {
+    case 1024: hipLaunchKernelGGL((init_unified_big_kernel<WDT, K, 2, 8>), grid, dim3(128), 0, st, a, g); break;
+    case 2048: hipLaunchKernelGGL((init_unified_big_kernel<WDT, K, 4, 8>), grid, dim3(256), 0, st, a, g); break;
+    case 4096: hipLaunchKernelGGL((init_unified_big_kernel<WDT, K, 4, 16>), grid, dim3(256), 0, st, a, g); break;
+    case 8192: hipLaunchKernelGGL((init_unified_big_kernel<WDT, K, 4, 32>), grid, dim3(256), 0, st, a, g); break;
+    default: hipLaunchKernelGGL((init_unified_big_kernel<WDT, K, 4, 64>), grid, dim3(256), 0, st, a, g); break;
+  }
+}
+
+template <int WDT>
+static hipError_t launch_init_big_k(const InitArgs& a, int k, int g, int64_t groups, hipStream_t st) {
+  switch (k) {
+    case 1: launch_init_big<WDT, 1>(a, g, groups, st); break;
+    case 2: launch_init_big<WDT, 2>(a, g, groups, st); break;
+    case 3: launch_init_big<WDT, 3>(a, g, groups, st); break;
+    default: launch_init_big<WDT, 4>(a, g, groups, st); break;
+  }
+  return hipGetLastError();
+}
+
 template <int WDT, int K>
 static void launch_init_g(const InitArgs& a, dim3 grid, size_t lds, hipStream_t st) {
   switch (a.logg) {
@@ -422,7 +819,7 @@ static hipError_t launch_init_k(const InitArgs& a, int k, dim3 grid, size_t lds,
 hipError_t launch_init_unified(const InitUnifiedLaunch& p, hipStream_t st) {
   InitArgs a;
   a.N = p.R * p.C;
-  a.logg = __builtin_ctz(unsigned(p.g));
+  a.logg = p.g > 512 ? 0 : __builtin_ctz(unsigned(p.g));
   a.gpr = int(p.C / p.g);
   a.G = p.grid_G;
   a.T = p.alt_T;
@@ -430,6 +827,11 @@ hipError_t launch_init_unified(const InitUnifiedLaunch& p, hipStream_t st) {
   a.W = p.W;
   a.delta = p.delta; a.z_u = p.z_u; a.alpha = p.alpha; a.z_b = p.z_b;
   a.codes = p.codes; a.err = p.err; a.s = p.s; a.s_r = p.s_r;
+  if (p.g > 512) {
+    const int64_t groups = a.N / p.g;
+    if (p.w_dtype == BF16) return launch_init_big_k<BF16>(a, p.k, p.g, groups, st);
+    return launch_init_big_k<F32>(a, p.k, p.g, groups, st);
+  }
   const int64_t waves = (a.N + 511) / 512;
   const dim3 grid(unsigned((waves + 3) / 4));
   const size_t lds = 4 * init_wave_lds_bytes(a.logg, p.k);

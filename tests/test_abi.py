@@ -76,10 +76,11 @@ def test_fq_fwd_validation(L, kw, status, text):
 def test_large_groups_accepted_where_supported(L):
     """Groups of more than 512 weights (any multiple of 8 dividing C, e.g. one
     row of 11008): the quantizer entry points take them, the unified
-    initialisation and the fused gradient-GEMM backward do not."""
-    assert L.uniquan_init_unified(4, 11008, 3, 11008, FAKE, 1, 30, 15, 0, FAKE, FAKE, FAKE, FAKE, None, None,
+    initialisation up to 16384 weights per group, the fused gradient-GEMM
+    backward not at all."""
+    assert L.uniquan_init_unified(4, 16392, 3, 16392, FAKE, 1, 30, 15, 0, FAKE, FAKE, FAKE, FAKE, None, None,
                                   None, None, None) == uq.UQ_EUNSUPPORTED
-    assert "up to 512" in uq.last_error()
+    assert "up to 16384" in uq.last_error()
     assert L.uniquan_layer_grad_ste_sgd(64, 4, 4096, 3, 4096, FAKE, FAKE, FAKE, 1, FAKE, None, None, None, FAKE,
                                         FAKE, FAKE, 0.1, 0.1, None, None, None, None) == uq.UQ_EUNSUPPORTED
 

@@ -136,6 +136,33 @@ def test_init_optional_outputs_and_determinism():
         assert np.array_equal(again[name], ref[name])
 
 
+# ---------------------------------------------------------------------------
+# Per-row groups (g = C, above 512): one workgroup per group, the pairwise
+# tree over the row zero-padded to a power of two, the int64 adjugate.
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("R,C,k,G,T,clip", [
+    (5, 1000, 3, 3, 4, 0),     # not a power of two: 128 lanes of 8, padded to 1024
+    (4, 1024, 2, 1, 6, 2),     # 128 lanes of 8, G = 1 (z_B updated)
+    (3, 4096, 4, 3, 3, 1),     # 256 lanes of 16
+    (2, 11008, 3, 2, 4, 0),    # the 7B down projection's row: lanes of 64, padded to 16384
+    (2, 14336, 2, 2, 3, 2),    # the 8B down projection's row
+    (2, 6152, 4, 1, 5, 0),     # lanes of 32 with a partly padded lane
+])
+def test_init_per_row_groups(R, C, k, G, T, clip):
+    W = weights(R, C, 40 + k)
+    check(W, k, C, G, T, clip)
+
+
+def test_init_per_row_fp32_degenerate():
+    rs = np.random.default_rng(12)
+    W = (rs.standard_normal((4, 2048)) * 0.05).astype(F32)
+    W[0] = 0.125               # constant row: Delta' = 1
+    W[1] = 0.0                 # all-zero row
+    W[2] = np.where(np.arange(2048) % 2 == 0, -0.5, 0.5)   # two values
+    check(W, 3, 2048, 2, 4, 0, wdt=torch.float32)
+    check(W, 4, 2048, 1, 3, 2, wdt=torch.float32)
+
+
 def test_init_rejects_bad_arguments():
     W = torch.zeros(4 * 128, device=DEV, dtype=torch.bfloat16)
     o = [torch.empty(4 * 8, device=DEV) for _ in range(4)]

@@ -47,6 +47,17 @@ def pin_tree_sum():
         bound = 9 * 2.0 ** -24 * float(np.abs(v[i].astype(F64)).sum())
         assert abs(got[i] - exact) <= bound
     assert UI.tree_sum_f32(np.array([[3.5]], F32))[0] == F32(3.5)
+    # Lengths that are not powers of two (per-row groups): the same pairing
+    # over the zero-padded vector; exact on small integers, and within the
+    # pairwise bound of the next power of two at a 7B down-projection row.
+    assert UI.tree_sum_f32(np.array([[1e8, 1.0, -1e8, 1.0, 5.0]], F32))[0] == 5.0
+    ints = rs.integers(-1000, 1000, size=(3, 1000)).astype(F32)
+    assert np.array_equal(UI.tree_sum_f32(ints), ints.astype(F64).sum(axis=1).astype(F32))
+    v = rs.standard_normal((2, 11008)).astype(F32)
+    got = UI.tree_sum_f32(v).astype(F64)
+    for i in range(2):
+        exact = math.fsum(float(t) for t in v[i])
+        assert abs(got[i] - exact) <= 14 * 2.0 ** -24 * float(np.abs(v[i].astype(F64)).sum())
 
 
 def test_i1_tree_sum():
@@ -348,6 +359,15 @@ def pin_against_f64():
         rel = np.abs(got - want) / want
         assert np.median(rel) < 1e-4
         assert np.all(rel < 2e-2)
+    # per-row groups: a power of two above 512 and a row length that is not one
+    for C, k, G, T, clip in ((1024, 3, 3, 4, UI.CLIP_FIXED_MIN), (1000, 2, 1, 6, UI.CLIP_BALANCED),
+                             (1000, 4, 2, 3, UI.CLIP_FIXED_MAX)):
+        W = _weights(rs, 4, C)
+        got = UI.unified_init(W, k, C, G=G, T=T, clip=clip)["err"].astype(F64)
+        want = _unified_init_f64(W, k, C, G, T, clip)
+        rel = np.abs(got - want) / want
+        assert np.all(rel < 2e-2), (C, k, rel)
+        assert np.median(rel) < 1e-3, (C, k, rel)
 
 
 def test_i9_against_f64():
