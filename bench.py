@@ -124,6 +124,8 @@ def parse():
     ap.add_argument("--unfused", action="store_true",
                     help="time the step as four passes (fq_fwd, loss GEMM, gradient GEMM, fq_bwd with SGD) instead "
                          "of two GEMMs and the fused backward + SGD + next forward pass")
+    ap.add_argument("--summarize-block-profile", action="store_true",
+                    help="write profiles/decoder_block7b.md from gpurun_out/prof_block7b (no GPU needed)")
     ap.add_argument("--summarize-profiles", default=None, metavar="WORKLOAD",
                     help="(no GPU) write profiles/ summaries from the rocprofv3 CSVs under gpurun_out/")
     ap.add_argument("--mode", default="paper", choices=["paper", "full", "local", "frozen"])
@@ -633,6 +635,64 @@ def summarize_profiles(workload, steps, warmup, fused=True, out_dir=PROFILES, ru
     print("\n".join(lines))
 
 
+def summarize_block_profile(out_dir=PROFILES, run_dir=os.path.join(ROOT, "gpurun_out")):
+    """Write profiles/decoder_block7b.md from a kernel trace of the bench's two
+    decoder-block legs (command in the summary): per step (the kernels from
+    one attention forward to the next), the median fused-form step of the
+    multi-head leg and of the grouped-query leg (they run in that order), by
+    kernel, with the attention kernels' rates."""
+    import collections
+    import csv
+    import re
+    pdir = os.path.join(run_dir, "prof_block7b")
+    rows = sorted(csv.DictReader(open(os.path.join(pdir, "trace_kernel_trace.csv"))),
+                  key=lambda r: int(r["Start_Timestamp"]))
+    marks = [i for i, r in enumerate(rows) if "attn_fwd_kernel" in r["Kernel_Name"]]
+    cycles = []
+    for i0, i1 in zip(marks, marks[1:]):
+        ks = rows[i0:i1]
+        if not any("fq_step_kernel" in r["Kernel_Name"] for r in ks):
+            continue
+        agg, cnt = collections.defaultdict(float), collections.Counter()
+        for r in ks:
+            n = re.sub(r"\(.*", "", r["Kernel_Name"]).replace("void ", "")
+            agg[n] += (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+            cnt[n] += 1
+        wall = (int(rows[i1]["Start_Timestamp"]) - int(rows[i0]["Start_Timestamp"])) / 1e3
+        cycles.append((wall, agg, cnt))
+    half = len(cycles) // 2
+    legs = {"multi-head (32 key/value heads)": cycles[:half], "grouped-query (8 key/value heads)": cycles[half:]}
+    B, L, d = 128, 2048, 128
+    per_product = 2.0 * B * (L * (L + 32) / 2) * d        # causal, diagonal tiles whole
+    flops = {"attn_fwd_kernel": 3 * per_product, "attn_bwd_dq_kernel": 3 * per_product,
+             "attn_bwd_dkv_kernel": 4 * per_product}
+    cmd = ("rocprofv3 --kernel-trace --stats -f csv -d gpurun_out/prof_block7b -o trace -- python3 bench.py "
+           "--steps 3 --warmup 1 --workload mlp7b --no-cpu-baseline --no-ceilings --sub-workloads ''")
+    lines = ["# rocprofv3 summary: the 7B decoder block step, kernel by kernel", "",
+             "Workload: one 7B decoder block (C = 4096 in 32 heads of 128, I = 11008), 8192 tokens as 4 "
+             "sequences of 2048, k = 3, g = 128, all seven matrices quantized, the fused step form (block "
+             "forward, loss, backpropagation, one fused backward + SGD + next forward per matrix); the bench's "
+             "block legs (`block_decoder`, `block_decoder_gqa`).  MI355X.", "",
+             "Command (run from the repository root on the GPU box; the summary is then written on the CPU "
+             "with `python bench.py --summarize-block-profile`):", "", "```", cmd, "```", ""]
+    for leg, cyc in legs.items():
+        if not cyc:
+            continue
+        cyc = sorted(cyc, key=lambda c: c[0])
+        wall, agg, cnt = cyc[len(cyc) // 2]
+        tot = sum(agg.values())
+        lines += [f"## {leg}: median of {len(cyc)} fused steps", "",
+                  f"Step {wall / 1e3:.2f} ms from one attention forward to the next, {tot / 1e3:.2f} ms of kernel "
+                  "time.", "", "| Kernel | Calls | Time (us) | Share | Rate |", "|---|---|---|---|---|"]
+        for n, v in sorted(agg.items(), key=lambda x: -x[1]):
+            base = re.sub(r"<.*", "", n).replace("uq::", "")
+            rate = f"{flops[base] / (v / cnt[n] * 1e-6) / 1e12:.0f} TFLOP/s" if base in flops else ""
+            lines.append(f"| `{n[:80]}` | {cnt[n]} | {v:.1f} | {100 * v / tot:.1f}% | {rate} |")
+        lines.append("")
+    open(os.path.join(out_dir, "decoder_block7b.md"), "w").write("\n".join(lines))
+    print("\n".join(lines))
+
+
 def progress(msg):
     """One progress line on stderr (stdout carries only the JSON line)."""
     print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
@@ -851,6 +911,9 @@ def main():
     args = parse()
     if args.summarize_profiles:
         summarize_profiles(args.summarize_profiles, args.steps, args.warmup, fused=not args.unfused)
+        return
+    if args.summarize_block_profile:
+        summarize_block_profile()
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); this build has no multi-GPU path.",
