@@ -19,7 +19,10 @@
 //     fp32( fp64(sum_b adj_ab v_b) / det ) with the integer adjugate, where
 //     every product adj_ab v_b is exact in fp64 (C^T C and its adjugate are
 //     positive semidefinite, so |adj_ab| <= g^3 <= 2^27, and v is fp32);
-//     det = 0 keeps the previous alpha;
+//     det = 0 keeps the previous alpha; where a group has at least
+//     k (k + 1) / 2 lanes, each of its lanes computes one distinct adjugate
+//     entry and lane a forms alpha_a (shuffles gather the operands), instead
+//     of every lane solving the whole system;
 //   * nearest level: first minimum of |fl(wbar - q)| over the ascending table
 //     (the forward's rule), a constant group takes Delta' = 1.
 // ALU-bound: the weights are read once and stay in registers for all G * T
@@ -155,6 +158,90 @@ __device__ __forceinline__ void solve_alpha(const int (&M)[K][K], const float (&
     for (int b = 1; b < K; ++b) S = __builtin_fma(double(adj[a][b]), double(v[b]), S);
     al[a] = float(S / det);
   }
+}
+
+// The same solve spread over the LPG lanes of a group (LPG >= K (K + 1) / 2):
+// lane j < K (K + 1) / 2 computes the j-th of the adjugate's distinct entries
+// adj_ab, a <= b in row-major order (the cofactor of M without row b and
+// column a, its rows and columns chosen by per-lane selects), lane a < K
+// gathers row a of the adjugate and forms alpha_a with the arithmetic of
+// solve_alpha, and every lane gathers the K results.  The determinant is the
+// same row-0 expansion, so the results are those of solve_alpha.
+template <int K>
+__device__ __forceinline__ int pair_index(int a, int b) {  // a <= b
+  return a * K - (a * (a - 1)) / 2 + (b - a);
+}
+
+// The minor of M for adjugate entry jl (its rows and columns picked by
+// per-lane selects) and the parity of its cofactor's sign.
+template <int K>
+__device__ __forceinline__ int lane_minor(const int (&M)[K][K], int jl, int (&S)[3][3]) {
+  // (a, b) of pair jl, 2 bits each, 4 bits per pair
+  uint64_t tab = 0;
+#pragma unroll
+  for (int a = 0; a < K; ++a)
+#pragma unroll
+    for (int b = a; b < K; ++b) tab |= uint64_t(a | (b << 2)) << (4 * pair_index<K>(a, b));
+  const int jc = jl < K * (K + 1) / 2 ? jl : 0;
+  const int e = int(tab >> (4 * jc)) & 15;
+  const int c = e & 3, r = e >> 2;  // the minor without row r = b and column c = a
+  int R[3][K];
+#pragma unroll
+  for (int i = 0; i < K - 1; ++i)
+#pragma unroll
+    for (int j = 0; j < K; ++j) R[i][j] = i >= r ? M[i + 1][j] : M[i][j];
+#pragma unroll
+  for (int i = 0; i < K - 1; ++i)
+#pragma unroll
+    for (int j = 0; j < K - 1; ++j) S[i][j] = j >= c ? R[i][j + 1] : R[i][j];
+  return (r + c) & 1;
+}
+
+template <int K>
+__device__ __forceinline__ int lane_cofactor(const int (&M)[K][K], int jl) {
+  if constexpr (K == 1) {
+    return 1;
+  } else {
+    int S[3][3];
+    const int odd = lane_minor<K>(M, jl, S);
+    int d;
+    if constexpr (K == 2) {
+      d = S[0][0];
+    } else if constexpr (K == 3) {
+      d = det2(S[0][0], S[0][1], S[1][0], S[1][1]);
+    } else {
+      d = __mul24(S[0][0], det2(S[1][1], S[1][2], S[2][1], S[2][2])) -
+          __mul24(S[0][1], det2(S[1][0], S[1][2], S[2][0], S[2][2])) +
+          __mul24(S[0][2], det2(S[1][0], S[1][1], S[2][0], S[2][1]));
+    }
+    return odd ? -d : d;
+  }
+}
+
+template <int K, int LPG>
+__device__ __forceinline__ void solve_alpha_dist(const int (&M)[K][K], const float (&v)[K], float (&al)[K], int jl,
+                                                 int lane) {
+  static_assert(LPG >= K * (K + 1) / 2, "one adjugate entry per lane");
+  const int mine = lane_cofactor<K>(M, jl);
+  const int base = lane - jl;
+  // column 0 of the adjugate, the same in every lane of the group
+  double det = 0.0;
+#pragma unroll
+  for (int b = 0; b < K; ++b)
+    det = __builtin_fma(double(M[0][b]), double(__shfl(mine, base + pair_index<K>(0, b), 64)), det);
+  if (det == 0.0) return;
+  // row jl of the adjugate (lanes jl >= K take row K - 1 and discard it)
+  const int ar = jl < K ? jl : K - 1;
+  double S = 0.0;
+#pragma unroll
+  for (int b = 0; b < K; ++b) {
+    const int idx = ar <= b ? pair_index<K>(ar, b) : pair_index<K>(b, ar);
+    const double t = double(__shfl(mine, base + idx, 64));
+    S = b == 0 ? t * double(v[0]) : __builtin_fma(t, double(v[b]), S);
+  }
+  const float out = float(S / det);
+#pragma unroll
+  for (int a = 0; a < K; ++a) al[a] = __shfl(out, base + a, 64);
 }
 
 // Ascending level table of the lane's group in LDS (raw, sorted, code_of).
@@ -313,7 +400,8 @@ __global__ __launch_bounds__(kThreads) void init_unified_kernel(InitArgs a) {
           }
         }
       }
-      solve_alpha<K>(M, v, al);
+      if constexpr (lpg >= K * (K + 1) / 2) solve_alpha_dist<K, lpg>(M, v, al, jl, lane);
+      else solve_alpha<K>(M, v, al);
 
       // C <- nearest level's code
       build_table<K>(raw, qs, cof, al, zb, jl, lpg);
@@ -436,10 +524,18 @@ __device__ __forceinline__ void tree_push_all(LaneTree<E>& t, const F& f) {
   }
 }
 
+// Pairwise sum of the N (a power of two) values r[0 .. N-1] in order.
+template <int N>
+__device__ __forceinline__ float pairwise_lds(const float* r) {
+  if constexpr (N == 1) return r[0];
+  else return pairwise_lds<N / 2>(r) + pairwise_lds<N / 2>(r + N / 2);
+}
+
 // Workgroup-wide pairwise sums of NV lane values (each lane already holds its
-// own subtree's sum), left in every lane.
-template <int NW, int NV>
-__device__ __forceinline__ void block_tree(float (&t)[NV], float* red, int lane, int wave) {
+// own subtree's sum), left in every lane; red holds NV values per wavefront.
+template <int NW, int NV, int CAP>
+__device__ __forceinline__ void block_tree(float (&t)[NV], float (&red)[CAP], int lane, int wave) {
+  static_assert(NV * NW <= CAP, "reduction buffer too small");
 #pragma unroll
   for (int v = 0; v < NV; ++v) t[v] = group_reduce<64>(t[v], AddF());
   if (lane == 0) {
@@ -448,15 +544,13 @@ __device__ __forceinline__ void block_tree(float (&t)[NV], float* red, int lane,
   }
   __syncthreads();
 #pragma unroll
-  for (int v = 0; v < NV; ++v) {
-    if constexpr (NW == 2) t[v] = red[v * NW] + red[v * NW + 1];
-    else t[v] = (red[v * NW] + red[v * NW + 1]) + (red[v * NW + 2] + red[v * NW + 3]);
-  }
+  for (int v = 0; v < NV; ++v) t[v] = pairwise_lds<NW>(red + v * NW);
   __syncthreads();
 }
 
-template <int NW, int NV>
-__device__ __forceinline__ void block_isum(int (&t)[NV], int* red, int lane, int wave) {
+template <int NW, int NV, int CAP>
+__device__ __forceinline__ void block_isum(int (&t)[NV], int (&red)[CAP], int lane, int wave) {
+  static_assert(NV * NW <= CAP, "reduction buffer too small");
 #pragma unroll
   for (int v = 0; v < NV; ++v) t[v] = group_reduce<64>(t[v], AddI());
   if (lane == 0) {
@@ -474,62 +568,57 @@ __device__ __forceinline__ void block_isum(int (&t)[NV], int* red, int lane, int
   __syncthreads();
 }
 
-// Cofactor of the symmetric integer matrix M (int64: entries up to 2^14).
-template <int K>
-__device__ __forceinline__ int64_t cofactor64(const int (&M)[K][K], int r, int c) {
-  int64_t S[3][3];
-#pragma unroll
-  for (int i = 0, ii = 0; i < K; ++i) {
-    if (i == r) continue;
-#pragma unroll
-    for (int j = 0, jj = 0; j < K; ++j) {
-      if (j == c) continue;
-      S[ii][jj] = M[i][j];
-      ++jj;
-    }
-    ++ii;
-  }
-  int64_t d;
-  if constexpr (K == 2) {
-    d = S[0][0];
-  } else if constexpr (K == 3) {
-    d = S[0][0] * S[1][1] - S[0][1] * S[1][0];
-  } else {
-    d = S[0][0] * (S[1][1] * S[2][2] - S[1][2] * S[2][1]) - S[0][1] * (S[1][0] * S[2][2] - S[1][2] * S[2][0]) +
-        S[0][2] * (S[1][0] * S[2][1] - S[1][1] * S[2][0]);
-  }
-  return ((r + c) & 1) ? -d : d;
+// alpha = (C^T C)^{-1} v for C^T C entries up to 2^14, spread over the lanes
+// of a wavefront as solve_alpha_dist: lane j < K (K + 1) / 2 computes one
+// distinct adjugate entry in int64 (|adj| <= g^3 < 2^42), lane a < K forms
+// alpha_a = (sum_b adj_ab v_b) / det with the exact int64 determinant (row-0
+// expansion) converted to fp64 and the fp64 products added in ascending b,
+// and every lane gathers the K results.  Unchanged if det = 0.
+__device__ __forceinline__ int64_t shfl64(int64_t x, int src) {
+  const int lo = __shfl(int(uint32_t(uint64_t(x))), src, 64);
+  const int hi = __shfl(int(uint32_t(uint64_t(x) >> 32)), src, 64);
+  return int64_t((uint64_t(uint32_t(hi)) << 32) | uint32_t(lo));
 }
 
 template <int K>
-__device__ __forceinline__ void solve_alpha64(const int (&M)[K][K], const float (&v)[K], float (&al)[K]) {
-  int64_t adj[K][K];
-  if constexpr (K == 1) {
-    adj[0][0] = 1;
-  } else {
+__device__ __forceinline__ void solve_alpha64_dist(const int (&M)[K][K], const float (&v)[K], float (&al)[K],
+                                                   int lane) {
+  int64_t mine = 1;
+  if constexpr (K > 1) {
+    int S0[3][3];
+    const int odd = lane_minor<K>(M, lane, S0);
+    int64_t S[3][3];
 #pragma unroll
-    for (int a = 0; a < K; ++a)
+    for (int i = 0; i < K - 1; ++i)
 #pragma unroll
-      for (int b = a; b < K; ++b) {
-        adj[a][b] = cofactor64<K>(M, b, a);
-        adj[b][a] = adj[a][b];
-      }
+      for (int j = 0; j < K - 1; ++j) S[i][j] = S0[i][j];
+    int64_t d;
+    if constexpr (K == 2) {
+      d = S[0][0];
+    } else if constexpr (K == 3) {
+      d = S[0][0] * S[1][1] - S[0][1] * S[1][0];
+    } else {
+      d = S[0][0] * (S[1][1] * S[2][2] - S[1][2] * S[2][1]) - S[0][1] * (S[1][0] * S[2][2] - S[1][2] * S[2][0]) +
+          S[0][2] * (S[1][0] * S[2][1] - S[1][1] * S[2][0]);
+    }
+    mine = odd ? -d : d;
   }
   int64_t det = 0;
 #pragma unroll
-  for (int b = 0; b < K; ++b) det += int64_t(M[0][b]) * adj[b][0];
+  for (int b = 0; b < K; ++b) det += int64_t(M[0][b]) * shfl64(mine, pair_index<K>(0, b));
   if (det == 0) return;
   const double dd = double(det);
+  const int ar = lane < K ? lane : K - 1;
+  double S = 0.0;
 #pragma unroll
-  for (int a = 0; a < K; ++a) {
-    double S = double(adj[a][0]) * double(v[0]);
-#pragma unroll
-    for (int b = 1; b < K; ++b) {
-      const double pr = double(adj[a][b]) * double(v[b]);
-      S = S + pr;
-    }
-    al[a] = float(S / dd);
+  for (int b = 0; b < K; ++b) {
+    const int idx = ar <= b ? pair_index<K>(ar, b) : pair_index<K>(b, ar);
+    const double pr = double(shfl64(mine, idx)) * double(v[b]);
+    S = b == 0 ? pr : S + pr;
   }
+  const float out = float(S / dd);
+#pragma unroll
+  for (int a = 0; a < K; ++a) al[a] = __shfl(out, a, 64);
 }
 
 template <int WDT, int K, int NW, int E>
@@ -567,6 +656,10 @@ __global__ __launch_bounds__(NW * 64) void init_unified_big_kernel(InitArgs a, i
   for (int c = 0; c < E; c += 8)
     if (e0 + c < g) valid8 |= 1u << (c / 8);
 #define UQ_VALID(i) (((valid8 >> ((i) / 8)) & 1u) != 0u)
+  // A wavefront whose elements are all padding adds exact zeros to every sum
+  // and keeps code 0: it skips the per-element work and only joins the
+  // workgroup reductions.
+  const bool live = __builtin_amdgcn_readfirstlane(wave) * 64 * E < g;
 
   float mm[2] = {INFINITY, -INFINITY};
 #pragma unroll
@@ -620,20 +713,25 @@ __global__ __launch_bounds__(NW * 64) void init_unified_big_kernel(InitArgs a, i
     for (int q = 0; q < NP; ++q) cw[q] = 0u;
 #pragma unroll
     for (int b = 0; b < K; ++b) {
-      LaneTree<E> tr;
-      tree_push_all<E>(tr, [&](int i) {
-        float r = wbar[i] - zb;
-        for (int bb = 0; bb < b; ++bb) r = ((cw[i / 4] >> (8 * (i & 3) + bb)) & 1u) ? r - al[bb] : r + al[bb];
-        return UQ_VALID(i) ? fabsf(r) : 0.0f;
-      });
-      float t[1] = {tr.st[LaneTree<E>::LG]};
+      float t[1] = {0.0f};
+      if (live) {
+        LaneTree<E> tr;
+        tree_push_all<E>(tr, [&](int i) {
+          float r = wbar[i] - zb;
+          for (int bb = 0; bb < b; ++bb) r = ((cw[i / 4] >> (8 * (i & 3) + bb)) & 1u) ? r - al[bb] : r + al[bb];
+          return UQ_VALID(i) ? fabsf(r) : 0.0f;
+        });
+        t[0] = tr.st[LaneTree<E>::LG];
+      }
       block_tree<NW, 1>(t, red, lane, wave);
       const float ai = t[0] / gf;
+      if (live) {
 #pragma unroll
-      for (int i = 0; i < E; ++i) {
-        float r = wbar[i] - zb;
-        for (int bb = 0; bb < b; ++bb) r = ((cw[i / 4] >> (8 * (i & 3) + bb)) & 1u) ? r - al[bb] : r + al[bb];
-        if (UQ_VALID(i) && r >= 0.0f) cw[i / 4] |= 1u << (8 * (i & 3) + b);
+        for (int i = 0; i < E; ++i) {
+          float r = wbar[i] - zb;
+          for (int bb = 0; bb < b; ++bb) r = ((cw[i / 4] >> (8 * (i & 3) + bb)) & 1u) ? r - al[bb] : r + al[bb];
+          if (UQ_VALID(i) && r >= 0.0f) cw[i / 4] |= 1u << (8 * (i & 3) + b);
+        }
       }
       al[b] = ai;
     }
@@ -643,65 +741,74 @@ __global__ __launch_bounds__(NW * 64) void init_unified_big_kernel(InitArgs a, i
       float v[K];
 #pragma unroll
       for (int b = 0; b < K; ++b) {
-        LaneTree<E> tr;
-        tree_push_all<E>(tr, [&](int i) {
-          const float x = wbar[i] - zb;
-          const bool bit = (cw[i / 4] >> (8 * (i & 3) + b)) & 1u;
-          return UQ_VALID(i) ? (bit ? x : -x) : 0.0f;
-        });
-        v[b] = tr.st[LaneTree<E>::LG];
+        v[b] = 0.0f;
+        if (live) {
+          LaneTree<E> tr;
+          tree_push_all<E>(tr, [&](int i) {
+            const float x = wbar[i] - zb;
+            const bool bit = (cw[i / 4] >> (8 * (i & 3) + b)) & 1u;
+            return UQ_VALID(i) ? (bit ? x : -x) : 0.0f;
+          });
+          v[b] = tr.st[LaneTree<E>::LG];
+        }
       }
       block_tree<NW, K>(v, red, lane, wave);
       int M[K][K];
       {
-        int dis[K * K];
+        // disagreement counts of bit pairs p < q, in row-major order
+        constexpr int NPQ = K > 1 ? K * (K - 1) / 2 : 1;
+        int dis[NPQ];
+        dis[0] = 0;
 #pragma unroll
-        for (int p = 0; p < K * K; ++p) dis[p] = 0;
+        for (int p = 0, n = 0; p < K; ++p)
 #pragma unroll
-        for (int p = 0; p < K; ++p)
-#pragma unroll
-          for (int q = p + 1; q < K; ++q) {
+          for (int q = p + 1; q < K; ++q, ++n) {
             int c = 0;
 #pragma unroll
             for (int w4 = 0; w4 < NP; ++w4)
               c += __builtin_popcount(((cw[w4] >> p) ^ (cw[w4] >> q)) & 0x01010101u);
-            dis[p * K + q] = c;
+            dis[n] = c;
           }
-        block_isum<NW, K * K>(dis, redi, lane, wave);
+        block_isum<NW, NPQ>(dis, redi, lane, wave);
 #pragma unroll
-        for (int p = 0; p < K; ++p) {
+        for (int p = 0, n = 0; p < K; ++p) {
           M[p][p] = g;
 #pragma unroll
-          for (int q = p + 1; q < K; ++q) {
-            M[p][q] = g - 2 * dis[p * K + q];
+          for (int q = p + 1; q < K; ++q, ++n) {
+            M[p][q] = g - 2 * dis[n];
             M[q][p] = M[p][q];
           }
         }
       }
-      solve_alpha64<K>(M, v, al);
+      solve_alpha64_dist<K>(M, v, al, lane);
 
       // C <- nearest level's code (padding keeps code 0)
-      build_table<K>(raw, qs, cof, al, zb, lane, 64);
       uint32_t nw[NP];
 #pragma unroll
       for (int q = 0; q < NP; ++q) nw[q] = 0u;
+      if (live) {
+        build_table<K>(raw, qs, cof, al, zb, lane, 64);
 #pragma unroll
-      for (int i = 0; i < E; ++i) {
-        if (UQ_VALID(i)) {
-          float dist;
-          nw[i / 4] |= uint32_t(cof[nearest_full_k<K>(qs, wbar[i], dist)]) << (8 * (i & 3));
+        for (int i = 0; i < E; ++i) {
+          if (UQ_VALID(i)) {
+            float dist;
+            nw[i / 4] |= uint32_t(cof[nearest_full_k<K>(qs, wbar[i], dist)]) << (8 * (i & 3));
+          }
         }
       }
       const float zb_prev = zb;
       if (a.G == 1) {
-        LaneTree<E> tr;
-        tree_push_all<E>(tr, [&](int i) {
-          const uint32_t code = (nw[i / 4] >> (8 * (i & 3))) & 0xFFu;
-          float ca = 0.0f;
-          for (int b = 0; b < K; ++b) ca = ((code >> b) & 1u) ? ca + al[b] : ca - al[b];
-          return UQ_VALID(i) ? wbar[i] - ca : 0.0f;
-        });
-        float tz[1] = {tr.st[LaneTree<E>::LG]};
+        float tz[1] = {0.0f};
+        if (live) {
+          LaneTree<E> tr;
+          tree_push_all<E>(tr, [&](int i) {
+            const uint32_t code = (nw[i / 4] >> (8 * (i & 3))) & 0xFFu;
+            float ca = 0.0f;
+            for (int b = 0; b < K; ++b) ca = ((code >> b) & 1u) ? ca + al[b] : ca - al[b];
+            return UQ_VALID(i) ? wbar[i] - ca : 0.0f;
+          });
+          tz[0] = tr.st[LaneTree<E>::LG];
+        }
         block_tree<NW, 1>(tz, red, lane, wave);
         zb = tz[0] / gf;
       }
@@ -717,21 +824,24 @@ __global__ __launch_bounds__(NW * 64) void init_unified_big_kernel(InitArgs a, i
     }
 
     // candidate error ||w - Q*(w)||^2 with the forward's FULL mapping
-    build_table<K>(raw, qs, cof, al, zb, lane, 64);
     uint32_t cc[NP];
 #pragma unroll
     for (int q = 0; q < NP; ++q) cc[q] = 0u;
-    LaneTree<E> tr;
-    tree_push_all<E>(tr, [&](int i) {
-      if (!UQ_VALID(i)) return 0.0f;
-      float dist;
-      const int pos = nearest_full_k<K>(qs, wbar[i], dist);
-      cc[i / 4] |= uint32_t(cof[pos]) << (8 * (i & 3));
-      const float what = dl * (qs[pos] - zu);
-      const float d = w[i] - what;
-      return d * d;
-    });
-    float te[1] = {tr.st[LaneTree<E>::LG]};
+    float te[1] = {0.0f};
+    if (live) {
+      build_table<K>(raw, qs, cof, al, zb, lane, 64);
+      LaneTree<E> tr;
+      tree_push_all<E>(tr, [&](int i) {
+        if (!UQ_VALID(i)) return 0.0f;
+        float dist;
+        const int pos = nearest_full_k<K>(qs, wbar[i], dist);
+        cc[i / 4] |= uint32_t(cof[pos]) << (8 * (i & 3));
+        const float what = dl * (qs[pos] - zu);
+        const float d = w[i] - what;
+        return d * d;
+      });
+      te[0] = tr.st[LaneTree<E>::LG];
+    }
     block_tree<NW, 1>(te, red, lane, wave);
     const float e = te[0];
     if (j == 1 || e < best_e) {
@@ -776,8 +886,8 @@ static void launch_init_big(const InitArgs& a, int g, int64_t groups, hipStream_
     case 1024: hipLaunchKernelGGL((init_unified_big_kernel<WDT, K, 2, 8>), grid, dim3(128), 0, st, a, g); break;
     case 2048: hipLaunchKernelGGL((init_unified_big_kernel<WDT, K, 4, 8>), grid, dim3(256), 0, st, a, g); break;
     case 4096: hipLaunchKernelGGL((init_unified_big_kernel<WDT, K, 4, 16>), grid, dim3(256), 0, st, a, g); break;
-    case 8192: hipLaunchKernelGGL((init_unified_big_kernel<WDT, K, 4, 32>), grid, dim3(256), 0, st, a, g); break;
-    default: hipLaunchKernelGGL((init_unified_big_kernel<WDT, K, 4, 64>), grid, dim3(256), 0, st, a, g); break;
+    case 8192: hipLaunchKernelGGL((init_unified_big_kernel<WDT, K, 8, 16>), grid, dim3(512), 0, st, a, g); break;
+    default: hipLaunchKernelGGL((init_unified_big_kernel<WDT, K, 16, 16>), grid, dim3(1024), 0, st, a, g); break;
   }
 }
 
