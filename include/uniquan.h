@@ -392,6 +392,24 @@ uq_status uniquan_gemm_nt(int64_t M, int64_t N, int64_t K, const uint16_t* A,
                           float scale, void* stream);
 
 /*
+ * uniquan_gemm -- out[M x N] = scale * sum_k A(m, k) B(n, k) with either
+ * operand stored K-slow, the contractions of the block's backpropagation
+ * (Algorithm 1): the weight gradient dL/dW = dY^T X reads dY [T x out] and
+ * X [T x in] as stored (both K-slow, K = T), the input gradient dX = dY W
+ * reads W [out x in] as stored (B K-slow, K = out).
+ *   A(m, k) = A[m K + k] (a_kslow = 0) or A[k M + m] (a_kslow = 1);
+ *   B(n, k) = B[n K + k] (b_kslow = 0) or B[k N + n] (b_kslow = 1).
+ * bf16 operands (16-byte aligned), fp32 accumulation over k in the same
+ * order as uniquan_gemm_nt (the result equals uniquan_gemm_nt on the
+ * operands transposed to K-contiguous, bit for bit), out bf16 (RNE) or fp32
+ * row-major.  With a K-slow operand: K a multiple of 32, N a multiple of 8,
+ * M a multiple of 8 when A is K-slow; with neither, uniquan_gemm_nt's rules.
+ */
+uq_status uniquan_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* A,
+                       int a_kslow, const uint16_t* B, int b_kslow, void* out,
+                       int out_dtype, float scale, void* stream);
+
+/*
  * uniquan_silu_mul_fwd -- H[i] = silu(G[i]) * U[i], i < n (bf16 in and out,
  * fp32 arithmetic, silu(x) = x / (1 + exp(-x))); n a multiple of 8,
  * pointers 16-byte aligned.

@@ -179,8 +179,6 @@ class DecoderBlock:
         self.r1, self.r2 = e(T, **f32), e(T, **f32)
         (self.Z1, self.O, self.Z2, self.E, self.dA, self.dO, self.dQ) = (e(T, C, **b16) for _ in range(7))
         self.Vb, self.dK, self.dV = (e(T, Ckv, **b16) for _ in range(3))
-        (self.Z1t, self.Ot, self.Z2t, self.Et, self.dAt, self.dQt) = (e(C, T, **b16) for _ in range(6))
-        self.dKt, self.dVt = e(Ckv, T, **b16), e(Ckv, T, **b16)
         # query heads in grouped slot order (see uniquan_rope_split), key/value heads plain
         self.Qh, self.Oh, self.dOh = (e(B, L, d, **b16) for _ in range(3))
         self.Kh, self.Vh = e(Bkv, L, d, **b16), e(Bkv, L, d, **b16)
@@ -190,11 +188,8 @@ class DecoderBlock:
         self.lse, self.delta = e(B, L, **f32), e(B, L, **f32)
         # dQ per query head; dK, dV contributions per query head (summed per key/value head)
         self.dQr, self.dKp, self.dVp = (e(B, L, d, **f32) for _ in range(3))
-        self.Gt, self.Ut, self.Ht, self.dHt, self.dGt, self.dUt = (e(I, T, **b16) for _ in range(6))
-        self.Hm, self.dG, self.dU = (e(T, I, **b16) for _ in range(3))
-        self.WdT = e(I, C, **b16)
-        self.WgT, self.WuT = e(C, I, **b16), e(C, I, **b16)
-        self.WoT = e(C, C, **b16)
+        # MLP activations and their gradients, one row per token
+        self.Gm, self.Um, self.Hm, self.dHm, self.dGm, self.dUm = (e(T, I, **b16) for _ in range(6))
         self.partials = e(uq.uniquan_block_loss_ws(), **f32)
         self.loss = torch.zeros(1, **f32)
         self._rinv_tmp = e(T, **f32)
@@ -218,10 +213,9 @@ class DecoderBlock:
         uq.uniquan_rope_merge(T, H, d, L, self.Oh, self.O, rotate=False, group=grp)
         uq.uniquan_gemm_nt(T, C, C, self.O, W["o"], self.A32)
         uq.uniquan_add_rmsnorm(T, C, X, self.A32, self.g2, self.R, self.Z2, self.r2)
-        uq.uniquan_gemm_nt(I, T, C, W["g"], self.Z2, self.Gt)
-        uq.uniquan_gemm_nt(I, T, C, W["u"], self.Z2, self.Ut)
-        uq.uniquan_silu_mul_fwd(self.Gt, self.Ut, self.Ht)
-        uq.uniquan_transpose_bf16(I, T, self.Ht, self.Hm)
+        uq.uniquan_gemm_nt(T, I, C, self.Z2, W["g"], self.Gm)
+        uq.uniquan_gemm_nt(T, I, C, self.Z2, W["u"], self.Um)
+        uq.uniquan_silu_mul_fwd(self.Gm, self.Um, self.Hm)
         uq.uniquan_gemm_nt(T, C, I, self.Hm, W["d"], self.M32)
 
     def _sum_out(self, out):
@@ -263,29 +257,21 @@ class DecoderBlock:
         sc = 1.0 / float(d) ** 0.5
         m = self.mats
         Wh = {n: q.W_hat for n, q in m.items()}
-        # MLP module (dY = 2 E)
-        uq.uniquan_transpose_bf16(T, C, self.E, self.Et)
-        uq.uniquan_gemm_nt(C, I, T, self.Et, self.Ht, m["d"].G, 2.0)
-        uq.uniquan_transpose_bf16(C, I, Wh["d"], self.WdT)
-        uq.uniquan_gemm_nt(I, T, C, self.WdT, self.E, self.dHt, 2.0)
-        uq.uniquan_silu_mul_bwd(self.dHt, self.Gt, self.Ut, self.dGt, self.dUt)
-        uq.uniquan_transpose_bf16(T, C, self.Z2, self.Z2t)
-        uq.uniquan_gemm_nt(I, C, T, self.dGt, self.Z2t, m["g"].G)
-        uq.uniquan_gemm_nt(I, C, T, self.dUt, self.Z2t, m["u"].G)
-        uq.uniquan_transpose_bf16(I, T, self.dGt, self.dG)
-        uq.uniquan_transpose_bf16(I, T, self.dUt, self.dU)
-        uq.uniquan_transpose_bf16(I, C, Wh["g"], self.WgT)
-        uq.uniquan_transpose_bf16(I, C, Wh["u"], self.WuT)
-        uq.uniquan_gemm_nt(T, C, I, self.dG, self.WgT, self.dZa)
-        uq.uniquan_gemm_nt(T, C, I, self.dU, self.WuT, self.dZb)
+        # MLP module (dY = 2 E).  Weight gradients dY^T X read dY and X as
+        # stored (both K-slow, K = tokens); input gradients dY W read W as
+        # stored (K-slow, K = the matrix's rows).
+        uq.uniquan_gemm(C, I, T, self.E, 1, self.Hm, 1, m["d"].G, 2.0)
+        uq.uniquan_gemm(T, I, C, self.E, 0, Wh["d"], 1, self.dHm, 2.0)
+        uq.uniquan_silu_mul_bwd(self.dHm, self.Gm, self.Um, self.dGm, self.dUm)
+        uq.uniquan_gemm(I, C, T, self.dGm, 1, self.Z2, 1, m["g"].G)
+        uq.uniquan_gemm(I, C, T, self.dUm, 1, self.Z2, 1, m["u"].G)
+        uq.uniquan_gemm(T, C, I, self.dGm, 0, Wh["g"], 1, self.dZa)
+        uq.uniquan_gemm(T, C, I, self.dUm, 0, Wh["u"], 1, self.dZb)
         # second norm and residual: dR = 2 E + RMSNorm backward
         uq.uniquan_rmsnorm_bwd(T, C, self.dZa, self.dZb, self.R, self.g2, self.r2, self.E, 2.0, self.dA)
         # attention module
-        uq.uniquan_transpose_bf16(T, C, self.dA, self.dAt)
-        uq.uniquan_transpose_bf16(T, C, self.O, self.Ot)
-        uq.uniquan_gemm_nt(C, C, T, self.dAt, self.Ot, m["o"].G)
-        uq.uniquan_transpose_bf16(C, C, Wh["o"], self.WoT)
-        uq.uniquan_gemm_nt(T, C, C, self.dA, self.WoT, self.dO)
+        uq.uniquan_gemm(C, C, T, self.dA, 1, self.O, 1, m["o"].G)
+        uq.uniquan_gemm(T, C, C, self.dA, 0, Wh["o"], 1, self.dO)
         Hkv, Ckv, Bkv, grp = self.Hkv, self.Ckv, self.Bkv, self.grp
         uq.uniquan_rope_split(T, H, d, L, self.dO, self.dOh, rotate=False, group=grp)
         uq.uniquan_transpose_bf16_batched(Bkv, L, d, self.Kh, self.Kt)
@@ -296,12 +282,9 @@ class DecoderBlock:
         uq.uniquan_rope_merge(T, H, d, L, self.dQr, self.dQ, rotate=True, group=grp)
         uq.uniquan_rope_merge(T, Hkv, d, L, self.dKp, self.dK, rotate=True, nsum=grp)
         uq.uniquan_rope_merge(T, Hkv, d, L, self.dVp, self.dV, rotate=False, nsum=grp)
-        uq.uniquan_transpose_bf16(T, C, self.Z1, self.Z1t)
-        uq.uniquan_transpose_bf16(T, C, self.dQ, self.dQt)
-        uq.uniquan_gemm_nt(C, C, T, self.dQt, self.Z1t, m["q"].G)
-        for g, src, dst in (("k", self.dK, self.dKt), ("v", self.dV, self.dVt)):
-            uq.uniquan_transpose_bf16(T, Ckv, src, dst)
-            uq.uniquan_gemm_nt(Ckv, C, T, dst, self.Z1t, m[g].G)
+        uq.uniquan_gemm(C, C, T, self.dQ, 1, self.Z1, 1, m["q"].G)
+        uq.uniquan_gemm(Ckv, C, T, self.dK, 1, self.Z1, 1, m["k"].G)
+        uq.uniquan_gemm(Ckv, C, T, self.dV, 1, self.Z1, 1, m["v"].G)
 
     def update(self, lr_f=0.005, lr_b=0.0005, keep_grads=False):
         """Straight-through backward with the SGD update of every matrix."""

@@ -393,6 +393,28 @@ uq_status uniquan_gemm_nt(int64_t M, int64_t N, int64_t K, const uint16_t* A, co
   return hip_status(fn, uq::launch_gemm(g, static_cast<hipStream_t>(stream)));
 }
 
+uq_status uniquan_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* A, int a_kslow, const uint16_t* B, int b_kslow,
+                       void* out, int out_dtype, float scale, void* stream) {
+  const char* fn = "uniquan_gemm";
+  if (M < 1 || N < 1 || K < 1) return fail(UQ_EINVAL, "%s: M, N, K must be >= 1", fn);
+  if ((a_kslow != 0 && a_kslow != 1) || (b_kslow != 0 && b_kslow != 1))
+    return fail(UQ_EINVAL, "%s: a_kslow and b_kslow must be 0 or 1", fn);
+  if (!a_kslow && !b_kslow) return uniquan_gemm_nt(M, N, K, A, B, out, out_dtype, scale, stream);
+  if (N % 8 != 0 || K % 32 != 0 || (a_kslow && M % 8 != 0))
+    return fail(UQ_EINVAL, "%s: N=%lld%s must be a multiple of 8 and K=%lld of 32", fn, (long long)N,
+                a_kslow ? " and M" : "", (long long)K);
+  if (N >= (int64_t(1) << 26) || K >= (int64_t(1) << 31) || M >= (int64_t(1) << 31) ||
+      M * K >= (int64_t(1) << 40) || N * K >= (int64_t(1) << 40) || M * N >= (int64_t(1) << 40))
+    return fail(UQ_EUNSUPPORTED, "%s: shape too large", fn);
+  if (!is_dtype(out_dtype)) return fail(UQ_EINVAL, "%s: bad dtype", fn);
+  REQ_PTR(A, 16); REQ_PTR(B, 16); REQ_PTR(out, 16);
+  uq::GemmLaunch g{A, B, M, N, K, out_dtype == UQ_BF16 ? uq::EPI_GRAD_BF16 : uq::EPI_GRAD_F32, nullptr, out, nullptr,
+                   scale};
+  g.ta = a_kslow;
+  g.tb = b_kslow;
+  return hip_status(fn, uq::launch_gemm(g, static_cast<hipStream_t>(stream)));
+}
+
 uq_status uniquan_silu_mul_fwd(int64_t n, const uint16_t* G, const uint16_t* U, uint16_t* H, void* stream) {
   const char* fn = "uniquan_silu_mul_fwd";
   if (n < 8 || n % 8 != 0) return fail(UQ_EINVAL, "%s: n=%lld must be a positive multiple of 8", fn, (long long)n);

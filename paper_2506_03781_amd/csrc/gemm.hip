@@ -7,7 +7,12 @@
 //            or the straight-through backward + SGD update applied to G in
 //            the epilogue (G never stored)
 // All are C[M x N] = A[M x K] B[N x K]^T with both operands K-contiguous
-// ("NT"), so one kernel template serves them.
+// ("NT"), so one kernel template serves them.  The block's backpropagation
+// also takes operands stored K-slow (A as [K x M], B as [K x N]): the weight
+// gradient dY^T X and the input gradient dY W read the activations and the
+// weights as they are stored, with no transposed copies (ping-pong kernel
+// only; the copies take whole k-rows and the MFMA fragments come from LDS
+// transpose reads).
 //
 // Kernels (all bf16 MFMA v_mfma_f32_32x32x16_bf16, fp32 accumulation):
 //   gemm_pp_kernel    the main one, for K % 32 == 0 on 256 x 256 and 256 x 128
@@ -654,16 +659,50 @@ __device__ __forceinline__ int pp_chunk(int row, int kc) {
   return BK == 64 ? (kc ^ ((row >> 1) & 7)) : (kc ^ ((row >> 2) & 3));
 }
 
-template <int BM, int BN, int EPI, int WAVES_M = (BN == 256 ? 2 : 4), int BK = 32>
+// Operands stored K-slow ([K x M], M contiguous): a 32-deep stage holds 32
+// k-rows of the tile's BM columns, chunk c (8 columns) of k-row r in slot
+// c ^ 4 (r & 3), so the four k-rows a 16-lane group reads sit 64 bytes apart
+// in the bank space.  ds_read_b64_tr_b16 gives lane i of each 16-lane group,
+// in slot j, element i % 4 of the 8 bytes addressed by lane 4 j + i / 4 of
+// the group: with lane 4 q + r addressing k-row k0 + r, columns c0 + 4 q ..
+// c0 + 4 q + 3, lane i receives column c0 + i at k-rows k0 .. k0 + 3, which
+// is half of an MFMA operand fragment (8 consecutive k of one row); two
+// reads, 4 k-rows apart, make the fragment.
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+__device__ __forceinline__ bf16x8 tr_fragment(const char* stage, int off_lo, int off_hi) {
+  const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(stage + off_lo));
+  const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(stage + off_hi));
+  const v4i16 both[2] = {lo, hi};
+  return __builtin_bit_cast(bf16x8, both);
+}
+
+// Byte offset, in a K-slow stage of W columns, of the 8 bytes this lane
+// addresses for the fragment of rows (columns) col0 .. col0 + 31 at substep
+// 0, first half.
+template <int W>
+__device__ __forceinline__ int tr_offset(int col0, int lane) {
+  const int g16 = lane >> 4, s16 = lane & 15;
+  const int kr = 8 * (g16 >> 1) + (s16 >> 2);
+  const int c = col0 + 16 * (g16 & 1) + 4 * (s16 & 3);
+  return kr * W * 2 + (((c >> 3) ^ (4 * (kr & 3))) << 4) + ((c & 7) >> 2) * 8;
+}
+
+template <int BM, int BN, int EPI, int WAVES_M = (BN == 256 ? 2 : 4), int BK = 32, bool TA = false,
+          bool TB = false>
 __global__ __launch_bounds__(512) void gemm_pp_kernel(GemmArgs p) {
   select_batch(p);
+  static_assert(BK == 32 || !(TA || TB), "K-slow operands use 32-deep stages");
   constexpr int S = BK == 64 ? 3 : 4;
   constexpr int CPR = BK / 8;        // 16-byte chunks per stage row
   constexpr int RPB = 64 / CPR;      // stage rows per 1 KB copy
   constexpr int NS = BK / 16;        // MFMA substeps per stage
   constexpr int WAVES_N = 8 / WAVES_M;
   constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N, FM = WM / 32, FN = WN / 32;
-  constexpr int ABLK = BM / RPB, BBLK = BN / RPB, PW = (ABLK + BBLK) / 8;  // 1 KB copies per wave and stage
+  // K-slow operands: chunks per k-row and k-rows per 1 KB copy
+  constexpr int CPKA = BM / 8, KPBA = 64 / CPKA, CPKB = BN / 8, KPBB = 64 / CPKB;
+  constexpr int ABLK = TA ? BK / KPBA : BM / RPB, BBLK = TB ? BK / KPBB : BN / RPB;
+  constexpr int PW = (ABLK + BBLK) / 8;  // 1 KB copies per wave and stage
   static_assert((ABLK + BBLK) % 8 == 0, "stage blocks must split over 8 waves");
 
   __shared__ uint4 smem[S * (BM + BN) * CPR];
@@ -687,29 +726,45 @@ __global__ __launch_bounds__(512) void gemm_pp_kernel(GemmArgs p) {
   const int64_t ke = p.causal == 2 ? min(K, m0 + BM) : K;
 
   // Lane l of a copy fills LDS slot l of a 1 KB block: row RPB blk + l / CPR,
-  // slot l % CPR, which holds chunk pp_chunk(row, l % CPR) of that row.
+  // slot l % CPR, which holds chunk pp_chunk(row, l % CPR) of that row.  A
+  // K-slow operand's block is k-rows KPB blk .. (whole k-rows; slot l % CPK
+  // of k-row r holds chunk (l % CPK) ^ 4 (r & 3)); columns past M or N are
+  // loaded from the last chunk and masked at the store.
   const uint16_t* src[PW];
   int dst_off[PW];
   bool isA[PW];
+  int64_t kstep[PW];  // elements per K stage
 #pragma unroll
   for (int j = 0; j < PW; ++j) {
     const int blk = wave * PW + j;
     const bool a = blk < ABLK;
     const int b = a ? blk : blk - ABLK;
-    const int row = b * RPB + lane / CPR;
-    const int kc = pp_chunk<BK>(row, lane % CPR);
     isA[j] = a;
-    const int64_t gr = a ? min(m0 + row, p.M - 1) : min(n0 + row, p.N - 1);
-    src[j] = (a ? p.A : p.B) + gr * K + kb + kc * 8;
     dst_off[j] = b * 64;
+    if ((a && TA) || (!a && TB)) {
+      const int cpk = a ? CPKA : CPKB, kpb = a ? KPBA : KPBB;
+      const int kr = b * kpb + lane / cpk;
+      const int c = (lane % cpk) ^ (4 * (kr & 3));
+      const int64_t ext = a ? p.M : p.N;
+      const int64_t col = min((a ? m0 : n0) + 8 * c, ext - 8);
+      src[j] = (a ? p.A : p.B) + int64_t(kr) * ext + col;
+      kstep[j] = BK * ext;
+    } else {
+      const int row = b * RPB + lane / CPR;
+      const int kc = pp_chunk<BK>(row, lane % CPR);
+      const int64_t gr = a ? min(m0 + row, p.M - 1) : min(n0 + row, p.N - 1);
+      src[j] = (a ? p.A : p.B) + gr * K + kb + kc * 8;
+      kstep[j] = BK;
+    }
   }
   const int nk = int((ke - kb) / BK);
   auto issue = [&](int stage, int kstage) {
-    const int64_t k0 = int64_t(min(kstage, nk - 1)) * BK;
+    const int64_t ks = int64_t(min(kstage, nk - 1));
 #pragma unroll
     for (int j = 0; j < PW; ++j) {
       uint4* dst = isA[j] ? &sA[stage][dst_off[j]] : &sB[stage][dst_off[j]];
-      __builtin_amdgcn_global_load_lds((glb_void*)(src[j] + k0), (lds_void*)dst, 16, 0, 0);
+      const uint16_t* g = (TA || TB) ? src[j] + ks * kstep[j] : src[j] + ks * BK;
+      __builtin_amdgcn_global_load_lds((glb_void*)g, (lds_void*)dst, 16, 0, 0);
     }
   };
 
@@ -737,14 +792,27 @@ __global__ __launch_bounds__(512) void gemm_pp_kernel(GemmArgs p) {
       offB[s][j] = row * CPR + pp_chunk<BK>(row, kc);
     }
   }
+  int toA[FM], toB[FN];  // K-slow fragments: byte offsets at substep 0, first half
+#pragma unroll
+  for (int i = 0; i < FM; ++i) toA[i] = TA ? tr_offset<BM>(wm * WM + i * 32, lane) : 0;
+#pragma unroll
+  for (int j = 0; j < FN; ++j) toB[j] = TB ? tr_offset<BN>(wn * WN + j * 32, lane) : 0;
   bf16x8 af[NS][FM], bfr[NS][FN];
   auto rd = [&](int st) {
+    const char* stA = reinterpret_cast<const char*>(&sA[st][0]);
+    const char* stB = reinterpret_cast<const char*>(&sB[st][0]);
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
 #pragma unroll
-      for (int i = 0; i < FM; ++i) af[s][i] = __builtin_bit_cast(bf16x8, sA[st][offA[s][i]]);
+      for (int i = 0; i < FM; ++i) {
+        if constexpr (TA) af[s][i] = tr_fragment(stA, toA[i] + 16 * s * BM * 2, toA[i] + (16 * s + 4) * BM * 2);
+        else af[s][i] = __builtin_bit_cast(bf16x8, sA[st][offA[s][i]]);
+      }
 #pragma unroll
-      for (int j = 0; j < FN; ++j) bfr[s][j] = __builtin_bit_cast(bf16x8, sB[st][offB[s][j]]);
+      for (int j = 0; j < FN; ++j) {
+        if constexpr (TB) bfr[s][j] = tr_fragment(stB, toB[j] + 16 * s * BN * 2, toB[j] + (16 * s + 4) * BN * 2);
+        else bfr[s][j] = __builtin_bit_cast(bf16x8, sB[st][offB[s][j]]);
+      }
     }
   };
 
@@ -887,7 +955,41 @@ hipError_t launch_gemm_ste(const GemmLaunch& q, int k, hipStream_t st) {
   return hipGetLastError();
 }
 
+// Products with an operand stored K-slow: the ping-pong kernel with 32-deep
+// stages on 256 x 256 tiles where there are at least 256 of them, on
+// 256 x 128 tiles otherwise.  K % 32 == 0, M % 8 == 0 when A is K-slow.
+template <int BM, int BN, int EPI>
+static void launch_kslow(const GemmArgs& a, int ta, int tb, hipStream_t st) {
+  const dim3 grid(unsigned(a.tiles_m * a.tiles_n));
+  constexpr int WMM = BN == 256 ? 2 : 4;
+  if (ta && tb) hipLaunchKernelGGL((gemm_pp_kernel<BM, BN, EPI, WMM, 32, true, true>), grid, dim3(512), 0, st, a);
+  else if (tb) hipLaunchKernelGGL((gemm_pp_kernel<BM, BN, EPI, WMM, 32, false, true>), grid, dim3(512), 0, st, a);
+  else hipLaunchKernelGGL((gemm_pp_kernel<BM, BN, EPI, WMM, 32, true, false>), grid, dim3(512), 0, st, a);
+}
+
+static hipError_t launch_gemm_kslow(const GemmLaunch& q, hipStream_t st) {
+  GemmArgs a;
+  a.A = q.A; a.B = q.B; a.M = q.M; a.N = q.N; a.K = q.K;
+  a.Yt = nullptr; a.out = q.out; a.partials = nullptr; a.scale = q.scale;
+  a.bsa = a.bsb = a.bso = 0;
+  a.causal = 0;
+  const bool wide = q.M > 128 && q.N > 128 && tiles<256, 256>(q.M, q.N) >= 256;
+  const int BN = wide ? 256 : 128;
+  a.tiles_m = int((q.M + 255) / 256);
+  a.tiles_n = int((q.N + BN - 1) / BN);
+  const bool bf = q.epi == EPI_GRAD_BF16;
+  if (wide) {
+    if (bf) launch_kslow<256, 256, EPI_GRAD_BF16>(a, q.ta, q.tb, st);
+    else launch_kslow<256, 256, EPI_GRAD_F32>(a, q.ta, q.tb, st);
+  } else {
+    if (bf) launch_kslow<256, 128, EPI_GRAD_BF16>(a, q.ta, q.tb, st);
+    else launch_kslow<256, 128, EPI_GRAD_F32>(a, q.ta, q.tb, st);
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_gemm(const GemmLaunch& q, hipStream_t st) {
+  if (q.ta || q.tb) return launch_gemm_kslow(q, st);
   switch (pick(q.M, q.N, q.batch)) {
     case T256x256: return launch_bm<256, 256>(q, st);
     case T256x128: return launch_bm<256, 128>(q, st);

@@ -105,7 +105,8 @@ enum GemmEpi : int {
 };
 
 struct GemmLaunch {
-  // C[M x N] = A[M x K] * B[N x K]^T, bf16 operands with K contiguous.
+  // C[M x N] = A[M x K] * B[N x K]^T, bf16 operands with K contiguous unless
+  // ta / tb say otherwise.
   const uint16_t* A; const uint16_t* B;
   int64_t M, N, K;
   int epi;
@@ -118,6 +119,9 @@ struct GemmLaunch {
   // batch b at A + b bsa, B + b bsb (elements), out + b bso (bytes)
   int64_t batch, bsa, bsb, bso;
   int causal;  // 0, or the causal mode of square attention products (see gemm.hip)
+  // operands stored K-slow (EPI_GRAD_*, no batch, no causal mode): A as
+  // [K x M] (ta = 1), B as [K x N] (tb = 1)
+  int ta, tb;
 };
 
 // Causal attention with the score tiles on chip (attn_fused.hip), d = 128.

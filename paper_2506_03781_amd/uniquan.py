@@ -62,6 +62,7 @@ _SIGS = {
     "uniquan_sgd": ([_i64, _vp, _vp, _f32, _vp], _i32),
     "uniquan_bcq_pack": ([_i64, _i64, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp], _i32),
     "uniquan_gemm_nt": ([_i64, _i64, _i64, _vp, _vp, _vp, _i32, _f32, _vp], _i32),
+    "uniquan_gemm": ([_i64, _i64, _i64, _vp, _i32, _vp, _i32, _vp, _i32, _f32, _vp], _i32),
     "uniquan_silu_mul_fwd": ([_i64, _vp, _vp, _vp, _vp], _i32),
     "uniquan_silu_mul_bwd": ([_i64, _vp, _vp, _vp, _vp, _vp, _vp], _i32),
     "uniquan_gemm_nt_batched": ([_i64, _i64, _i64, _i64, _vp, _i64, _vp, _i64, _vp, _i64, _i32, _f32, _i32, _vp],
@@ -397,6 +398,13 @@ def uniquan_gemm_nt(M, N, K, A, B, out, scale=1.0, stream=None):
     """out [M, N] = scale * A [M, K] B [N, K]^T (bf16 operands; out bf16 or fp32)."""
     _check(lib().uniquan_gemm_nt(M, N, K, _p(A, M * K, _B, "A"), _p(B, N * K, _B, "B"),
                                  _p(out, M * N, _W, "out"), _dt(out), float(scale), _stream(stream)))
+
+
+def uniquan_gemm(M, N, K, A, a_kslow, B, b_kslow, out, scale=1.0, stream=None):
+    """out [M, N] = scale * sum_k A(m, k) B(n, k): A stored [M, K] or, with a_kslow, [K, M];
+    B stored [N, K] or, with b_kslow, [K, N] (bf16 operands; out bf16 or fp32)."""
+    _check(lib().uniquan_gemm(M, N, K, _p(A, M * K, _B, "A"), int(bool(a_kslow)), _p(B, N * K, _B, "B"),
+                              int(bool(b_kslow)), _p(out, M * N, _W, "out"), _dt(out), float(scale), _stream(stream)))
 
 
 def uniquan_silu_mul_fwd(G, U, H, stream=None):

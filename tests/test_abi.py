@@ -196,6 +196,14 @@ def test_block_entry_validation(L):
     assert L.uniquan_gemm_nt(4, 1 << 26, 8, FAKE, FAKE, FAKE, F, 1.0, None) == uq.UQ_EUNSUPPORTED
     assert L.uniquan_gemm_nt(4, 8, 8, ODD, FAKE, FAKE, F, 1.0, None) == uq.UQ_EINVAL
     assert L.uniquan_gemm_nt(4, 8, 8, FAKE, FAKE, FAKE, 7, 1.0, None) == uq.UQ_EINVAL
+    g = L.uniquan_gemm
+    assert g(8, 8, 32, FAKE, 2, FAKE, 0, FAKE, F, 1.0, None) == uq.UQ_EINVAL
+    assert g(8, 8, 48, FAKE, 1, FAKE, 0, FAKE, F, 1.0, None) == uq.UQ_EINVAL   # K-slow needs K % 32 == 0
+    assert "K=48" in uq.last_error()
+    assert g(12, 8, 32, FAKE, 1, FAKE, 1, FAKE, F, 1.0, None) == uq.UQ_EINVAL  # K-slow A needs M % 8 == 0
+    assert g(12, 8, 32, FAKE, 0, ODD, 1, FAKE, F, 1.0, None) == uq.UQ_EINVAL
+    assert g(4, 12, 8, FAKE, 0, FAKE, 0, FAKE, F, 1.0, None) == uq.UQ_EINVAL   # neither: the NT rules
+    assert "uniquan_gemm_nt" in uq.last_error()
     assert L.uniquan_silu_mul_fwd(12, FAKE, FAKE, FAKE, None) == uq.UQ_EINVAL
     assert L.uniquan_silu_mul_fwd(0, FAKE, FAKE, FAKE, None) == uq.UQ_EINVAL
     assert L.uniquan_silu_mul_fwd(16, FAKE, None, FAKE, None) == uq.UQ_EINVAL

@@ -65,6 +65,36 @@ def test_gemm_nt_batched(M, N, K, batch, sa, sb):
         assert np.array_equal(host(single), got[b]), b   # the batch is the same kernel on each slice
 
 
+@pytest.mark.parametrize("M,N,K", [(264, 520, 96), (600, 1032, 160), (4104, 3848, 96)])
+@pytest.mark.parametrize("a_kslow,b_kslow", [(1, 1), (0, 1), (1, 0), (0, 0)])
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
+def test_gemm_kslow_operands(M, N, K, a_kslow, b_kslow, out_dtype):
+    """uniquan_gemm with operands stored K-slow ([K, M] / [K, N]): ragged
+    multi-tile shapes on 256 x 128 tiles (the first two) and 256 x 256 tiles
+    (the third, 17 x 16 tiles), against an fp64 product, and bit for bit
+    against uniquan_gemm_nt on the K-contiguous copies (the same accumulation
+    order over k)."""
+    rs = np.random.default_rng(M * 7 + N * 3 + K + 10 * a_kslow + b_kslow)
+    A = bfr(rs.standard_normal((M, K)))
+    B = bfr(rs.standard_normal((N, K)))
+    dA, dB = dev(A, torch.bfloat16), dev(B, torch.bfloat16)
+    sA = dev(A.T, torch.bfloat16) if a_kslow else dA
+    sB = dev(B.T, torch.bfloat16) if b_kslow else dB
+    out = torch.full((M, N), float("nan"), device="cuda", dtype=out_dtype)
+    nt = torch.full((M, N), float("nan"), device="cuda", dtype=out_dtype)
+    uq.uniquan_gemm(M, N, K, sA, a_kslow, sB, b_kslow, out, 0.5)
+    uq.uniquan_gemm_nt(M, N, K, dA, dB, nt, 0.5)
+    torch.cuda.synchronize()
+    got = host(out)
+    assert np.array_equal(got, host(nt))
+    ref = 0.5 * A @ B.T
+    mag = 0.5 * np.abs(A) @ np.abs(B).T
+    if out_dtype == torch.float32:
+        assert np.all(np.abs(got - ref) <= 1e-5 * mag)
+    else:
+        within_bf16(got, ref, floor=1e-5 * mag, what="bf16 out")
+
+
 @pytest.mark.parametrize("T,C", [(5, 8), (37, 264), (64, 4096)])
 def test_add_rmsnorm(T, C):
     rs = np.random.default_rng(T * C)
