@@ -64,12 +64,13 @@ class QuantMatrix:
         uq.uniquan_fq_bwd_sgd(self.R, self.C, self.k, self.g, self.W, self.s, self.s_r, self.delta, self.z_u,
                               self.alpha, self.z_b, self.codes, self.G, gs, ga, gz, lr_f, lr_b)
 
-    def fq_step(self, lr_f, lr_b, next_mode):
+    def fq_step(self, lr_f, lr_b, next_mode, stream=None):
         """The straight-through backward with the SGD update and the next
         step's forward (next_mode) in one pass: W_hat and codes for the next
         step."""
         uq.uniquan_fq_step(self.R, self.C, self.k, self.g, self.W, self.s, self.s_r, self.delta, self.z_u,
-                           self.alpha, self.z_b, self.codes, self.G, lr_f, lr_b, next_mode, self.W_hat)
+                           self.alpha, self.z_b, self.codes, self.G, lr_f, lr_b, next_mode, self.W_hat,
+                           stream=stream)
 
 
 class MLPBlock:
@@ -251,27 +252,34 @@ class DecoderBlock:
         self.compute_loss()
         self.backward()
 
-    def backward(self):
-        """Backpropagation from E to dL/dWhat of the seven matrices."""
+    def backward(self, done=None):
+        """Backpropagation from E to dL/dWhat of the seven matrices.  done(n),
+        if given, is called as soon as matrix n's gradient is final and its
+        What is read no more in this step."""
         T, C, I, H, d, L, B = self.T, self.C, self.I, self.H, self.d, self.L, self.B
         sc = 1.0 / float(d) ** 0.5
         m = self.mats
         Wh = {n: q.W_hat for n, q in m.items()}
+        done = done or (lambda n: None)
         # MLP module (dY = 2 E).  Weight gradients dY^T X read dY and X as
         # stored (both K-slow, K = tokens); input gradients dY W read W as
         # stored (K-slow, K = the matrix's rows).
         uq.uniquan_gemm(C, I, T, self.E, 1, self.Hm, 1, m["d"].G, 2.0)
         uq.uniquan_gemm(T, I, C, self.E, 0, Wh["d"], 1, self.dHm, 2.0)
+        done("d")
         uq.uniquan_silu_mul_bwd(self.dHm, self.Gm, self.Um, self.dGm, self.dUm)
         uq.uniquan_gemm(I, C, T, self.dGm, 1, self.Z2, 1, m["g"].G)
         uq.uniquan_gemm(I, C, T, self.dUm, 1, self.Z2, 1, m["u"].G)
         uq.uniquan_gemm(T, C, I, self.dGm, 0, Wh["g"], 1, self.dZa)
+        done("g")
         uq.uniquan_gemm(T, C, I, self.dUm, 0, Wh["u"], 1, self.dZb)
+        done("u")
         # second norm and residual: dR = 2 E + RMSNorm backward
         uq.uniquan_rmsnorm_bwd(T, C, self.dZa, self.dZb, self.R, self.g2, self.r2, self.E, 2.0, self.dA)
         # attention module
         uq.uniquan_gemm(C, C, T, self.dA, 1, self.O, 1, m["o"].G)
         uq.uniquan_gemm(T, C, C, self.dA, 0, Wh["o"], 1, self.dO)
+        done("o")
         Hkv, Ckv, Bkv, grp = self.Hkv, self.Ckv, self.Bkv, self.grp
         uq.uniquan_rope_split(T, H, d, L, self.dO, self.dOh, rotate=False, group=grp)
         uq.uniquan_transpose_bf16_batched(Bkv, L, d, self.Kh, self.Kt)
@@ -283,8 +291,11 @@ class DecoderBlock:
         uq.uniquan_rope_merge(T, Hkv, d, L, self.dKp, self.dK, rotate=True, nsum=grp)
         uq.uniquan_rope_merge(T, Hkv, d, L, self.dVp, self.dV, rotate=False, nsum=grp)
         uq.uniquan_gemm(C, C, T, self.dQ, 1, self.Z1, 1, m["q"].G)
+        done("q")
         uq.uniquan_gemm(Ckv, C, T, self.dK, 1, self.Z1, 1, m["k"].G)
+        done("k")
         uq.uniquan_gemm(Ckv, C, T, self.dV, 1, self.Z1, 1, m["v"].G)
+        done("v")
 
     def update(self, lr_f=0.005, lr_b=0.0005, keep_grads=False):
         """Straight-through backward with the SGD update of every matrix."""
@@ -295,18 +306,39 @@ class DecoderBlock:
         self.forward_backward(mode)
         self.update(lr_f, lr_b, keep_grads)
 
-    def step_fused(self, next_mode=uq.MAP_LOCAL, lr_f=0.005, lr_b=0.0005):
+    def step_fused(self, next_mode=uq.MAP_LOCAL, lr_f=0.005, lr_b=0.0005, overlap=False):
         """One step in the fused form: the block's forward on the current
         What (left by quantize() or by the previous fused step), the loss,
         backpropagation, then per matrix the straight-through backward with
         SGD fused with the next step's forward (next_mode).  The same
         sequence of operations as step() across steps; each matrix's What is
-        read once less and written once instead of twice."""
+        read once less and written once instead of twice.
+
+        With overlap, each matrix's fused quantizer pass runs on a second
+        stream as soon as its gradient is final and the backpropagation no
+        longer reads its What; the current stream waits for them before the
+        step returns, so the next step sees every What.  Off by default: on
+        the 7B block the quantizer's workgroups take compute units that the
+        products' next tiles wait for, and the step gets slower (11.9
+        against 10.6 ms with 32 key/value heads, no change with 8)."""
         self.forward()
         self.compute_loss()
-        self.backward()
-        for q in self.mats.values():
-            q.fq_step(lr_f, lr_b, next_mode)
+        if not overlap:
+            self.backward()
+            for q in self.mats.values():
+                q.fq_step(lr_f, lr_b, next_mode)
+            return
+        main = torch.cuda.current_stream()
+        if getattr(self, "_side", None) is None:
+            self._side = torch.cuda.Stream()
+        side = self._side
+
+        def done(n):
+            uq.wait_stream(side, main)
+            self.mats[n].fq_step(lr_f, lr_b, next_mode, stream=side)
+
+        self.backward(done)
+        uq.wait_stream(main, side)
 
     def flops_per_step(self):
         """GEMM flops of one step: the seven projections forward and their

@@ -118,9 +118,19 @@ def _is_launch(name: str) -> bool:
     return sig is not None and sig[1] is _i32 and len(sig[0]) > 0 and sig[0][-1] is _vp
 
 
+def _stream_tag(ptr):
+    """None for the stream current at recording (or the null stream), else
+    the stream's handle."""
+    if not ptr or not torch.cuda.is_available():
+        return None
+    return None if ptr == torch.cuda.current_stream().cuda_stream else ptr
+
+
 class _Recorder:
     """Stands in for the library while ``record`` runs: every launch entry
-    point is called as usual and its marshalled arguments are kept."""
+    point is called as usual and its marshalled arguments are kept, with the
+    stream it was enqueued on (the current one or another) and the waits
+    between streams made through ``wait_stream``."""
 
     def __init__(self, real):
         self.real, self.calls = real, []
@@ -131,28 +141,59 @@ class _Recorder:
             return fn
 
         def call(*args):
-            self.calls.append((fn, args))
+            self.calls.append(("launch", fn, args, _stream_tag(args[-1])))
             return fn(*args)
         return call
 
 
+def wait_stream(waiter, waitee):
+    """waiter.wait_stream(waitee) (torch streams); kept by ``record`` so that
+    a replay orders its streams the same way."""
+    if _recorder is not None:
+        _recorder.calls.append(("wait", _stream_tag(waiter.cuda_stream), _stream_tag(waitee.cuda_stream)))
+    waiter.wait_stream(waitee)
+
+
 class Launches:
     """Entry-point calls recorded once through the checked wrappers and
-    replayed with the same marshalled arguments (pointers, sizes, scalars) on
-    the stream given to the call: the per-tensor checks run once, at
-    recording.  The tensors behind the recorded pointers must stay alive and
-    keep their storage; a status other than UQ_OK still raises."""
+    replayed with the same marshalled arguments (pointers, sizes, scalars):
+    calls made on the stream current at recording go to the stream given to
+    the replay, calls made on other streams to streams of the replay's own
+    (default priority), with the recorded waits between them.  The
+    per-tensor checks run once, at recording.  The tensors behind the
+    recorded pointers must stay alive and keep their storage; a status other
+    than UQ_OK still raises."""
 
     def __init__(self, calls):
         self.calls = calls
+        self._streams = {}
 
     def __len__(self):
-        return len(self.calls)
+        return sum(1 for c in self.calls if c[0] == "launch")
+
+    def _side(self, tag):
+        if tag not in self._streams:
+            self._streams[tag] = torch.cuda.Stream()
+        return self._streams[tag]
 
     def __call__(self, stream=None):
-        st = _stream(stream)
-        for fn, args in self.calls:
-            status = fn(*args[:-1], st)
+        main_ptr = _stream(stream)
+        main = []  # the replay's stream as a torch stream, made only for waits
+
+        def obj(tag):
+            if tag is not None:
+                return self._side(tag)
+            if not main:
+                main.append(stream if isinstance(stream, torch.cuda.Stream) else
+                            torch.cuda.current_stream() if stream is None else torch.cuda.ExternalStream(main_ptr))
+            return main[0]
+
+        for c in self.calls:
+            if c[0] == "wait":
+                obj(c[1]).wait_stream(obj(c[2]))
+                continue
+            _, fn, args, tag = c
+            status = fn(*args[:-1], main_ptr if tag is None else obj(tag).cuda_stream)
             if status != UQ_OK:
                 raise UniquanError(status, last_error())
 

@@ -250,7 +250,7 @@ def test_recorder_classifies_launches(L):
 
 
 def test_replay_raises_on_error_status(L):
-    bad = uq.Launches([(L.uniquan_sgd, (0, FAKE, FAKE, 0.1, None))])
+    bad = uq.Launches([("launch", L.uniquan_sgd, (0, FAKE, FAKE, 0.1, None), None)])
     assert len(bad) == 1
     with pytest.raises(uq.UniquanError, match="n must be"):
         bad(stream=0)

@@ -249,9 +249,13 @@ def test_decoder_block_step_long_sequences(n_kv):
                   what_for=f"L 512 n_kv {n_kv}")
 
 
-def test_decoder_block_fused_step_form():
+@pytest.mark.parametrize("form", ["overlap", "sequential", "replay"])
+def test_decoder_block_fused_step_form(form):
     """quantize, then step_fused twice equals step twice followed by quantize:
-    every matrix's s, alpha, z_B, codes and What, and the losses, bit for bit."""
+    every matrix's s, alpha, z_B, codes and What, and the losses, bit for bit;
+    with the quantizer passes on a second stream (overlap), on one stream
+    (sequential), and replayed from a recording of the first fused step (its
+    second stream and waits included)."""
     X, mats, g1, g2 = make_block(31)
     blocks = []
     for _ in range(2):
@@ -263,8 +267,14 @@ def test_decoder_block_fused_step_form():
     lr_f, lr_b = 1e-4, 1e-5
     la, lb = [], []
     a.quantize(uq.MAP_FULL)
+    rec = None
     for nxt in (uq.MAP_LOCAL, uq.MAP_LOCAL):
-        a.step_fused(nxt, lr_f, lr_b)
+        if form == "replay" and rec is not None:
+            rec()
+        elif form == "replay":
+            rec = uq.record(a.step_fused, nxt, lr_f, lr_b)
+        else:
+            a.step_fused(nxt, lr_f, lr_b, overlap=form == "overlap")
         la.append(a.loss.clone())
     for mode in (uq.MAP_FULL, uq.MAP_LOCAL):
         b.step(mode, lr_f, lr_b)
