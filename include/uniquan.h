@@ -539,20 +539,20 @@ uq_status uniquan_softmax_causal_bwd(int64_t rows, int L, const float* dP,
  *   the sum of their contributions (uniquan_rope_merge with nsum sums them).
  * The rounding points are those of the unfused path (P and dS in bf16, S and
  * dP in fp32).
- * Layouts (bf16 unless stated): Q, O, dO [batch, L, d]; Qt, dOt [batch, d, L];
- * K, V [kv_batch, L, d]; Kt, Vt [kv_batch, d, L] (the transposes, e.g. from
- * uniquan_transpose_bf16_batched); row_lse, delta [batch, L] fp32 (delta
- * written by uniquan_attn_bwd); dQ, dK, dV [batch, L, d] fp32 out.  d = 128
+ * Layouts (bf16 unless stated): Q, O, dO [batch, L, d]; K, V [kv_batch, L,
+ * d] (the products that contract over the rows of a tile read it through
+ * LDS transpose reads, so no transposed copies are taken); row_lse, delta
+ * [batch, L] fp32 (delta written by uniquan_attn_bwd); dQ, dK, dV
+ * [batch, L, d] fp32 out.  d = 128
  * and L a multiple of 32 (UQ_EUNSUPPORTED otherwise); batch a positive
  * multiple of kv_batch, at most 65535; every pointer 16-byte aligned.
  */
 uq_status uniquan_attn_fwd(int64_t batch, int64_t kv_batch, int L, int d,
-                           const uint16_t* Q, const uint16_t* K, const uint16_t* Vt,
+                           const uint16_t* Q, const uint16_t* K, const uint16_t* V,
                            float scale, uint16_t* O, float* row_lse, void* stream);
 uq_status uniquan_attn_bwd(int64_t batch, int64_t kv_batch, int L, int d,
-                           const uint16_t* Q, const uint16_t* Qt, const uint16_t* K,
-                           const uint16_t* Kt, const uint16_t* V, const uint16_t* O,
-                           const uint16_t* dO, const uint16_t* dOt, const float* row_lse,
+                           const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                           const uint16_t* O, const uint16_t* dO, const float* row_lse,
                            float scale, float* delta, float* dQ, float* dK, float* dV,
                            void* stream);
 

@@ -183,8 +183,6 @@ class DecoderBlock:
         # query heads in grouped slot order (see uniquan_rope_split), key/value heads plain
         self.Qh, self.Oh, self.dOh = (e(B, L, d, **b16) for _ in range(3))
         self.Kh, self.Vh = e(Bkv, L, d, **b16), e(Bkv, L, d, **b16)
-        self.Qt, self.dOt = e(B, d, L, **b16), e(B, d, L, **b16)
-        self.Kt, self.Vt = e(Bkv, d, L, **b16), e(Bkv, d, L, **b16)
         # attention rows: base-2 log-sum-exp of the scores, the softmax backward's row term
         self.lse, self.delta = e(B, L, **f32), e(B, L, **f32)
         # dQ per query head; dK, dV contributions per query head (summed per key/value head)
@@ -208,9 +206,8 @@ class DecoderBlock:
         uq.uniquan_rope_split(T, H, d, L, self.Qf, self.Qh, rotate=True, group=grp)
         uq.uniquan_rope_split(T, Hkv, d, L, self.Kf, self.Kh, rotate=True)
         uq.uniquan_rope_split(T, Hkv, d, L, self.Vb, self.Vh, rotate=False)
-        uq.uniquan_transpose_bf16_batched(Bkv, L, d, self.Vh, self.Vt)
         # causal attention with the score tiles on chip (query batch g Bkv + c uses key/value batch c)
-        uq.uniquan_attn_fwd(B, Bkv, L, d, self.Qh, self.Kh, self.Vt, sc, self.Oh, self.lse)
+        uq.uniquan_attn_fwd(B, Bkv, L, d, self.Qh, self.Kh, self.Vh, sc, self.Oh, self.lse)
         uq.uniquan_rope_merge(T, H, d, L, self.Oh, self.O, rotate=False, group=grp)
         uq.uniquan_gemm_nt(T, C, C, self.O, W["o"], self.A32)
         uq.uniquan_add_rmsnorm(T, C, X, self.A32, self.g2, self.R, self.Z2, self.r2)
@@ -282,10 +279,7 @@ class DecoderBlock:
         done("o")
         Hkv, Ckv, Bkv, grp = self.Hkv, self.Ckv, self.Bkv, self.grp
         uq.uniquan_rope_split(T, H, d, L, self.dO, self.dOh, rotate=False, group=grp)
-        uq.uniquan_transpose_bf16_batched(Bkv, L, d, self.Kh, self.Kt)
-        uq.uniquan_transpose_bf16_batched(B, L, d, self.Qh, self.Qt)
-        uq.uniquan_transpose_bf16_batched(B, L, d, self.dOh, self.dOt)
-        uq.uniquan_attn_bwd(B, Bkv, L, d, self.Qh, self.Qt, self.Kh, self.Kt, self.Vh, self.Oh, self.dOh, self.dOt,
+        uq.uniquan_attn_bwd(B, Bkv, L, d, self.Qh, self.Kh, self.Vh, self.Oh, self.dOh,
                             self.lse, sc, self.delta, self.dQr, self.dKp, self.dVp)
         uq.uniquan_rope_merge(T, H, d, L, self.dQr, self.dQ, rotate=True, group=grp)
         uq.uniquan_rope_merge(T, Hkv, d, L, self.dKp, self.dK, rotate=True, nsum=grp)

@@ -577,28 +577,27 @@ static uq_status check_attn(const char* fn, int64_t batch, int64_t kv_batch, int
 }
 
 uq_status uniquan_attn_fwd(int64_t batch, int64_t kv_batch, int L, int d, const uint16_t* Q, const uint16_t* K,
-                           const uint16_t* Vt, float scale, uint16_t* O, float* row_lse, void* stream) {
+                           const uint16_t* V, float scale, uint16_t* O, float* row_lse, void* stream) {
   const char* fn = "uniquan_attn_fwd";
   if (uq_status st = check_attn(fn, batch, kv_batch, L, d)) return st;
-  REQ_PTR(Q, 16); REQ_PTR(K, 16); REQ_PTR(Vt, 16); REQ_PTR(O, 16); REQ_PTR(row_lse, 16);
+  REQ_PTR(Q, 16); REQ_PTR(K, 16); REQ_PTR(V, 16); REQ_PTR(O, 16); REQ_PTR(row_lse, 16);
   uq::AttnLaunch q{};
   q.batch = batch; q.kv_batch = kv_batch; q.L = L; q.scale = scale;
-  q.Q = Q; q.K = K; q.Vt = Vt; q.O_out = O; q.lse = row_lse;
+  q.Q = Q; q.K = K; q.V = V; q.O_out = O; q.lse = row_lse;
   return hip_status(fn, uq::launch_attn_fwd(q, static_cast<hipStream_t>(stream)));
 }
 
-uq_status uniquan_attn_bwd(int64_t batch, int64_t kv_batch, int L, int d, const uint16_t* Q, const uint16_t* Qt,
-                           const uint16_t* K, const uint16_t* Kt, const uint16_t* V, const uint16_t* O,
-                           const uint16_t* dO, const uint16_t* dOt, const float* row_lse, float scale, float* delta,
-                           float* dQ, float* dK, float* dV, void* stream) {
+uq_status uniquan_attn_bwd(int64_t batch, int64_t kv_batch, int L, int d, const uint16_t* Q, const uint16_t* K,
+                           const uint16_t* V, const uint16_t* O, const uint16_t* dO, const float* row_lse, float scale,
+                           float* delta, float* dQ, float* dK, float* dV, void* stream) {
   const char* fn = "uniquan_attn_bwd";
   if (uq_status st = check_attn(fn, batch, kv_batch, L, d)) return st;
-  REQ_PTR(Q, 16); REQ_PTR(Qt, 16); REQ_PTR(K, 16); REQ_PTR(Kt, 16); REQ_PTR(V, 16); REQ_PTR(O, 16);
-  REQ_PTR(dO, 16); REQ_PTR(dOt, 16); REQ_PTR(row_lse, 16); REQ_PTR(delta, 16);
+  REQ_PTR(Q, 16); REQ_PTR(K, 16); REQ_PTR(V, 16); REQ_PTR(O, 16);
+  REQ_PTR(dO, 16); REQ_PTR(row_lse, 16); REQ_PTR(delta, 16);
   REQ_PTR(dQ, 16); REQ_PTR(dK, 16); REQ_PTR(dV, 16);
   uq::AttnLaunch q{};
   q.batch = batch; q.kv_batch = kv_batch; q.L = L; q.scale = scale;
-  q.Q = Q; q.Qt = Qt; q.K = K; q.Kt = Kt; q.V = V; q.O = O; q.dO = dO; q.dOt = dOt;
+  q.Q = Q; q.K = K; q.V = V; q.O = O; q.dO = dO;
   q.lse = const_cast<float*>(row_lse); q.delta = delta;
   q.dQ = dQ; q.dK = dK; q.dV = dV;
   return hip_status(fn, uq::launch_attn_bwd(q, static_cast<hipStream_t>(stream)));

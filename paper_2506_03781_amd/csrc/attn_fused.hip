@@ -26,14 +26,14 @@
 // accumulator slot r of lane l belongs to tile row 16 (r / 8) + 8 (l / 32) +
 // r % 8, so the 8 values of each half (slots 8 h .. 8 h + 7) are 8
 // consecutive rows and serve directly as the B operand of the next product
-// (contraction over those rows), whose A operand is one 16-byte LDS read of
-// a transposed tile.
+// (contraction over those rows), whose A operand (d rows, the tile's rows as
+// k) comes from the same row tile through two LDS transpose reads.
 //
-// Tiles (32 rows of 128 bf16, or 128 rows of 32 bf16 for the transposed
-// ones) go straight from global memory into a ring of S LDS stages
-// (global_load_lds, 16 bytes per lane, S - 1 tiles ahead); each wave waits
-// for its own copies with an exact vmcnt before the workgroup barrier that
-// precedes the reads, and the barrier also orders the reuse of a stage.
+// Tiles (32 rows of 128 bf16, as stored: Q, K, V, dO) go straight from
+// global memory into a ring of S LDS stages (global_load_lds, 16 bytes per
+// lane, S - 1 tiles ahead); each wave waits for its own copies with an exact
+// vmcnt before the workgroup barrier that precedes the reads, and the barrier
+// also orders the reuse of a stage.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -89,13 +89,20 @@ __device__ __forceinline__ void lds_wait_barrier() {
   __builtin_amdgcn_s_barrier();
 }
 
+// Chunk swizzle of tile row rho: the two 2-bit fields of rho % 16 swapped.
+// It is a bijection on rho % 16, so the 16 rows a quarter-wavefront reads at
+// one chunk fall in 16 distinct slots, and four consecutive rows differ in
+// bits 2-3, so the two adjacent chunks of four consecutive rows that a
+// transpose read takes also fall in 8 distinct slots.
+__device__ __forceinline__ int swz(int rho) { return ((rho & 3) << 2) | ((rho >> 2) & 3); }
+
 // Row tile (32 rows of 128 bf16 = 512 slots of 16 bytes): slot s holds chunk
-// (s % 16) ^ (rho % 16) of tile row rho = s / 16, and tile row rho holds
+// (s % 16) ^ swz(rho) of tile row rho = s / 16, and tile row rho holds
 // source row perm32(rho) of the tile.  Copy block blk fills slots 64 blk ..
 // + 64; row_off is this lane's byte offset in the source tile for block blk.
 __device__ __forceinline__ uint32_t row_off(int blk, int lane) {
   const int s = blk * 64 + lane;
-  const int rho = s >> 4, c = (s & 15) ^ (rho & 15);
+  const int rho = s >> 4, c = (s & 15) ^ swz(rho);
   return uint32_t(perm32(rho) * D * 2 + c * 16);
 }
 
@@ -107,23 +114,31 @@ __device__ __forceinline__ void copy16(const void* base, uint32_t off, u32x4a* d
 // A or B fragment of k-step j (d = 16 j + 8 (lane / 32) .. + 8) of tile row lane % 32.
 __device__ __forceinline__ bf16x8a row_frag(const u32x4a* tile, int j, int lane) {
   const int rho = lane & 31, c = 2 * j + (lane >> 5);
-  return __builtin_bit_cast(bf16x8a, tile[rho * 16 + (c ^ (rho & 15))]);
+  return __builtin_bit_cast(bf16x8a, tile[rho * 16 + (c ^ swz(rho))]);
 }
 
-// Transposed tile (128 rows d of 32 bf16 columns from a [D][ld] source, 4
-// pieces of 8 columns per row): slot s holds piece (s % 4) ^ ((d / 2) % 4) of
-// row d = s / 4; col_off is this lane's byte offset for copy block blk.
-__device__ __forceinline__ uint32_t col_off(int blk, int lane, int ld) {
-  const int s = blk * 64 + lane;
-  const int d = s >> 2, p = (s & 3) ^ ((d >> 1) & 3);
-  return uint32_t(d) * uint32_t(ld) * 2u + uint32_t(p * 16);
-}
+typedef short v4i16a __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16a lds_v4i16a;
 
-// A fragment of rows 32 db .. + 32 over the 16 columns of half h: lane
-// supplies row 32 db + lane % 32 and columns 16 h + 8 (lane / 32) .. + 8.
+// A fragment of the transposed row tile: rows d = 32 db .. + 32 over the 16
+// tile rows (keys or queries, in source order) of half h; lane supplies
+// d = 32 db + lane % 32 and source rows 16 h + 8 (lane / 32) .. + 8.
+// ds_read_b64_tr_b16 gives lane i of each 16-lane group, in slot j, element
+// i % 4 of the 8 bytes addressed by lane 4 j + i / 4 of the group; lane
+// 4 j + q addresses source row r0 + j, columns d0 + 4 q .. + 3, so lane i
+// receives column d0 + i of rows r0 .. r0 + 3: half the fragment.
 __device__ __forceinline__ bf16x8a col_frag(const u32x4a* tile, int db, int h, int lane) {
-  const int d = 32 * db + (lane & 31), p = 2 * h + (lane >> 5);
-  return __builtin_bit_cast(bf16x8a, tile[d * 4 + (p ^ ((d >> 1) & 3))]);
+  const int g = lane >> 4, i = lane & 15;
+  const int d = 32 * db + 16 * (g & 1) + 4 * (i & 3);
+  const char* base = reinterpret_cast<const char*>(tile);
+  v4i16a part[2];
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh) {
+    const int rho = perm32(16 * h + 8 * (g >> 1) + 4 * hh + (i >> 2));
+    const int off = rho * D * 2 + (((d >> 3) ^ swz(rho)) << 4) + ((d & 7) >> 2) * 8;
+    part[hh] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16a*)(base + off));
+  }
+  return __builtin_bit_cast(bf16x8a, part);
 }
 
 // Slots 8 h .. 8 h + 7 as a bf16 B operand.
@@ -177,14 +192,10 @@ struct AttnArgs {
   int L;
   float scale;
   const uint16_t* Q;    // [batch, L, D]
-  const uint16_t* Qt;   // [batch, D, L]
   const uint16_t* K;    // [kv_batch, L, D]
-  const uint16_t* Kt;   // [kv_batch, D, L]
   const uint16_t* V;    // [kv_batch, L, D]
-  const uint16_t* Vt;   // [kv_batch, D, L]
   const uint16_t* O;    // [batch, L, D]
   const uint16_t* dO;   // [batch, L, D]
-  const uint16_t* dOt;  // [batch, D, L]
   uint16_t* O_out;      // [batch, L, D]
   float* lse;           // [batch, L] base-2 log-sum-exp of the scaled scores
   float* delta;         // [batch, L]
@@ -207,7 +218,7 @@ template <int NW, int S>
 __global__ __launch_bounds__(NW * 64) void attn_fwd_kernel(AttnArgs a) {
   constexpr int QB = NW * NB;
   constexpr int PW = 8 / NW;  // copy blocks per wave and tile
-  constexpr int STAGE = 2 * TILE16;  // key tile, transposed value tile
+  constexpr int STAGE = 2 * TILE16;  // key tile, value tile
   __shared__ u32x4a smem[S * STAGE];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
@@ -222,14 +233,11 @@ __global__ __launch_bounds__(NW * 64) void attn_fwd_kernel(AttnArgs a) {
   const int n_tiles = min(L, qb * QB + QB) / NB;
   const int my_tiles = active ? q0 / NB + 1 : 0;
   const uint16_t* Kb = a.K + bk * int64_t(L) * D;
-  const uint16_t* Vtb = a.Vt + bk * int64_t(D) * L;
+  const uint16_t* Vb = a.V + bk * int64_t(L) * D;
   const float c = a.scale * LOG2E;
-  uint32_t ro[PW], co[PW];
+  uint32_t ro[PW];
 #pragma unroll
-  for (int q = 0; q < PW; ++q) {
-    ro[q] = row_off(wave * PW + q, lane);
-    co[q] = col_off(wave * PW + q, lane, L);
-  }
+  for (int q = 0; q < PW; ++q) ro[q] = row_off(wave * PW + q, lane);
   bf16x8a qf[8];
   {
     const uint16_t* qrow = a.Q + (b * L + min(qi, L - 1)) * int64_t(D) + 8 * (lane >> 5);
@@ -290,7 +298,7 @@ __global__ __launch_bounds__(NW * 64) void attn_fwd_kernel(AttnArgs a) {
   for (int t = 0; t < S - 1; ++t)
     if (t < n_tiles) {
       copy_tile<PW>(Kb + int64_t(t) * NB * D, ro, smem + (t % S) * STAGE, wave);
-      copy_tile<PW>(Vtb + int64_t(t) * NB, co, smem + (t % S) * STAGE + TILE16, wave);
+      copy_tile<PW>(Vb + int64_t(t) * NB * D, ro, smem + (t % S) * STAGE + TILE16, wave);
     }
   for (int t = 0; t < n_tiles; ++t) {
     wait_tiles<2 * PW>(min(S - 2, n_tiles - 1 - t));
@@ -298,7 +306,7 @@ __global__ __launch_bounds__(NW * 64) void attn_fwd_kernel(AttnArgs a) {
     if (t + S - 1 < n_tiles) {
       const int u = t + S - 1;
       copy_tile<PW>(Kb + int64_t(u) * NB * D, ro, smem + (u % S) * STAGE, wave);
-      copy_tile<PW>(Vtb + int64_t(u) * NB, co, smem + (u % S) * STAGE + TILE16, wave);
+      copy_tile<PW>(Vb + int64_t(u) * NB * D, ro, smem + (u % S) * STAGE + TILE16, wave);
     }
     if (t >= my_tiles) continue;
     const u32x4a* tk = smem + (t % S) * STAGE;
@@ -350,7 +358,7 @@ template <int NW, int S>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_bwd_dq_kernel(AttnArgs a) {
   constexpr int QB = NW * NB;
   constexpr int PW = 8 / NW;
-  constexpr int STAGE = 3 * TILE16;  // key tile, value tile, transposed key tile
+  constexpr int STAGE = 2 * TILE16;  // key tile, value tile
   __shared__ u32x4a smem[S * STAGE];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
@@ -367,14 +375,10 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
   const int my_tiles = active ? q0 / NB + 1 : 0;
   const uint16_t* Kb = a.K + bk * int64_t(L) * D;
   const uint16_t* Vb = a.V + bk * int64_t(L) * D;
-  const uint16_t* Ktb = a.Kt + bk * int64_t(D) * L;
   const float c = a.scale * LOG2E;
-  uint32_t ro[PW], co[PW];
+  uint32_t ro[PW];
 #pragma unroll
-  for (int q = 0; q < PW; ++q) {
-    ro[q] = row_off(wave * PW + q, lane);
-    co[q] = col_off(wave * PW + q, lane, L);
-  }
+  for (int q = 0; q < PW; ++q) ro[q] = row_off(wave * PW + q, lane);
   bf16x8a qf[8], df[8];
   float dl = 0.0f;
   {
@@ -400,17 +404,15 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
       u32x4a* st = smem + (t % S) * STAGE;
       copy_tile<PW>(Kb + int64_t(t) * NB * D, ro, st, wave);
       copy_tile<PW>(Vb + int64_t(t) * NB * D, ro, st + TILE16, wave);
-      copy_tile<PW>(Ktb + int64_t(t) * NB, co, st + 2 * TILE16, wave);
     }
   for (int t = 0; t < n_tiles; ++t) {
-    wait_tiles<3 * PW>(min(S - 2, n_tiles - 1 - t));
+    wait_tiles<2 * PW>(min(S - 2, n_tiles - 1 - t));
     lds_wait_barrier();
     if (t + S - 1 < n_tiles) {
       const int u = t + S - 1;
       u32x4a* st = smem + (u % S) * STAGE;
       copy_tile<PW>(Kb + int64_t(u) * NB * D, ro, st, wave);
       copy_tile<PW>(Vb + int64_t(u) * NB * D, ro, st + TILE16, wave);
-      copy_tile<PW>(Ktb + int64_t(u) * NB, co, st + 2 * TILE16, wave);
     }
     if (t >= my_tiles) continue;
     const u32x4a* tk = smem + (t % S) * STAGE;
@@ -425,7 +427,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 #pragma unroll
     for (int j = 0; j < 8; ++j) dp = mfma(f[j], df[j], dp);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) f[i] = col_frag(tk + 2 * TILE16, i & 3, i >> 2, lane);
+    for (int i = 0; i < 8; ++i) f[i] = col_frag(tk, i & 3, i >> 2, lane);
     // dS in place of dP
 #pragma unroll
     for (int r = 0; r < 16; ++r) dp[r] = bf16_round(exp2a(fmaf(s[r], c, -lse))) * (dp[r] - dl);
@@ -461,7 +463,7 @@ template <int NW, int S>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_bwd_dkv_kernel(AttnArgs a) {
   constexpr int KB = NW * NB;
   constexpr int PW = 8 / NW;
-  constexpr int STAGE = 4 * TILE16 + 64;  // Q, dO, Qt, dOt tiles, row terms
+  constexpr int STAGE = 2 * TILE16 + 64;  // Q, dO tiles, row terms
   constexpr int NPARK = 3;
   __shared__ u32x4a smem[S * STAGE + NW * NPARK * 64];
   const int lane = threadIdx.x & 63;
@@ -481,16 +483,11 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
   const float c = a.scale * LOG2E;
   const uint16_t* Qb = a.Q + b * int64_t(L) * D;
   const uint16_t* dOb = a.dO + b * int64_t(L) * D;
-  const uint16_t* Qtb = a.Qt + b * int64_t(D) * L;
-  const uint16_t* dOtb = a.dOt + b * int64_t(D) * L;
   // row terms: lane (l % 16) copies 4 floats of lse (l % 16 < 8) or delta
   const float* rt_src = ((lane & 15) < 8 ? a.lse : a.delta) + b * L + 4 * (lane & 7);
-  uint32_t ro[PW], co[PW];
+  uint32_t ro[PW];
 #pragma unroll
-  for (int q = 0; q < PW; ++q) {
-    ro[q] = row_off(wave * PW + q, lane);
-    co[q] = col_off(wave * PW + q, lane, L);
-  }
+  for (int q = 0; q < PW; ++q) ro[q] = row_off(wave * PW + q, lane);
   bf16x8a kf[8], vf[8 - NPARK];
   u32x4a* park = smem + S * STAGE + wave * NPARK * 64;
   {
@@ -513,27 +510,23 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
       u32x4a* st = smem + (i % S) * STAGE;
       copy_tile<PW>(Qb + int64_t(t) * NB * D, ro, st, wave);
       copy_tile<PW>(dOb + int64_t(t) * NB * D, ro, st + TILE16, wave);
-      copy_tile<PW>(Qtb + int64_t(t) * NB, co, st + 2 * TILE16, wave);
-      copy_tile<PW>(dOtb + int64_t(t) * NB, co, st + 3 * TILE16, wave);
-      if (wave == 0) copy16(rt_src + t * NB, 0, st + 4 * TILE16);
+      if (wave == 0) copy16(rt_src + t * NB, 0, st + 2 * TILE16);
     }
   for (int i = 0; i < nt; ++i) {
-    if (wave == 0) wait_tiles<4 * PW + 1>(min(S - 2, nt - 1 - i));
-    else wait_tiles<4 * PW>(min(S - 2, nt - 1 - i));
+    if (wave == 0) wait_tiles<2 * PW + 1>(min(S - 2, nt - 1 - i));
+    else wait_tiles<2 * PW>(min(S - 2, nt - 1 - i));
     lds_wait_barrier();
     if (i + S - 1 < nt) {
       const int u = i + S - 1, t = first + u;
       u32x4a* st = smem + (u % S) * STAGE;
       copy_tile<PW>(Qb + int64_t(t) * NB * D, ro, st, wave);
       copy_tile<PW>(dOb + int64_t(t) * NB * D, ro, st + TILE16, wave);
-      copy_tile<PW>(Qtb + int64_t(t) * NB, co, st + 2 * TILE16, wave);
-      copy_tile<PW>(dOtb + int64_t(t) * NB, co, st + 3 * TILE16, wave);
-      if (wave == 0) copy16(rt_src + t * NB, 0, st + 4 * TILE16);
+      if (wave == 0) copy16(rt_src + t * NB, 0, st + 2 * TILE16);
     }
     const int t = first + i;
     if (t < my_first) continue;
     const u32x4a* st = smem + (i % S) * STAGE;
-    const float* rt = reinterpret_cast<const float*>(st + 4 * TILE16);  // lse[32], delta[32]
+    const float* rt = reinterpret_cast<const float*>(st + 2 * TILE16);  // lse[32], delta[32]
     f32x16a s = zero16(), dp = zero16();
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
@@ -566,6 +559,10 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
           dp[r] = 0.0f;
         }
     }
+    // the transpose-read addresses are recomputed for each tile (an opaque
+    // copy of the lane index keeps them from being held across the loop)
+    int tl = lane;
+    asm volatile("" : "+v"(tl));
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       bf16x8a pb, sb;
@@ -576,8 +573,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
       }
 #pragma unroll
       for (int db = 0; db < 4; ++db) {
-        dv[db] = mfma(col_frag(st + 3 * TILE16, db, h, lane), pb, dv[db]);
-        dk[db] = mfma(col_frag(st + 2 * TILE16, db, h, lane), sb, dk[db]);
+        dv[db] = mfma(col_frag(st + TILE16, db, h, tl), pb, dv[db]);
+        dk[db] = mfma(col_frag(st, db, h, tl), sb, dk[db]);
       }
     }
   }
@@ -587,7 +584,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 }
 
 namespace {
-constexpr int FWD_NW = 8, FWD_S = 2;
+constexpr int FWD_NW = 8, FWD_S = 4;
 constexpr int DQ_NW = 4, DQ_S = 2;
 constexpr int DKV_NW = 8, DKV_S = 2;
 }  // namespace
@@ -595,7 +592,7 @@ constexpr int DKV_NW = 8, DKV_S = 2;
 hipError_t launch_attn_fwd(const AttnLaunch& q, hipStream_t st) {
   AttnArgs a{};
   a.batch = q.batch; a.kv_batch = q.kv_batch; a.L = q.L; a.scale = q.scale;
-  a.Q = q.Q; a.K = q.K; a.Vt = q.Vt; a.O_out = q.O_out; a.lse = q.lse;
+  a.Q = q.Q; a.K = q.K; a.V = q.V; a.O_out = q.O_out; a.lse = q.lse;
   const int64_t nblk = (q.L + FWD_NW * NB - 1) / (FWD_NW * NB);
   hipLaunchKernelGGL((attn_fwd_kernel<FWD_NW, FWD_S>), dim3(unsigned(nblk * q.batch)), dim3(FWD_NW * 64), 0, st, a);
   return hipGetLastError();
@@ -604,7 +601,7 @@ hipError_t launch_attn_fwd(const AttnLaunch& q, hipStream_t st) {
 hipError_t launch_attn_bwd(const AttnLaunch& q, hipStream_t st) {
   AttnArgs a{};
   a.batch = q.batch; a.kv_batch = q.kv_batch; a.L = q.L; a.scale = q.scale;
-  a.Q = q.Q; a.Qt = q.Qt; a.K = q.K; a.Kt = q.Kt; a.V = q.V; a.O = q.O; a.dO = q.dO; a.dOt = q.dOt;
+  a.Q = q.Q; a.K = q.K; a.V = q.V; a.O = q.O; a.dO = q.dO;
   a.lse = q.lse; a.delta = q.delta; a.dQ = q.dQ; a.dK = q.dK; a.dV = q.dV;
   const int64_t nq = (q.L + DQ_NW * NB - 1) / (DQ_NW * NB);
   hipLaunchKernelGGL((attn_bwd_dq_kernel<DQ_NW, DQ_S>), dim3(unsigned(nq * q.batch)), dim3(DQ_NW * 64), 0, st, a);

@@ -129,8 +129,7 @@ struct AttnLaunch {
   int64_t batch, kv_batch;
   int L;
   float scale;
-  const uint16_t* Q; const uint16_t* Qt; const uint16_t* K; const uint16_t* Kt;
-  const uint16_t* V; const uint16_t* Vt; const uint16_t* O; const uint16_t* dO; const uint16_t* dOt;
+  const uint16_t* Q; const uint16_t* K; const uint16_t* V; const uint16_t* O; const uint16_t* dO;
   uint16_t* O_out; float* lse; float* delta; float* dQ; float* dK; float* dV;
 };
 hipError_t launch_attn_fwd(const AttnLaunch& p, hipStream_t st);

@@ -77,8 +77,7 @@ _SIGS = {
     "uniquan_block_loss_ws": ([], ctypes.c_size_t),
     "uniquan_block_loss": ([_i64, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp, _vp], _i32),
     "uniquan_attn_fwd": ([_i64, _i64, _i32, _i32, _vp, _vp, _vp, _f32, _vp, _vp, _vp], _i32),
-    "uniquan_attn_bwd": ([_i64, _i64, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _f32, _vp, _vp, _vp, _vp,
-                          _vp], _i32),
+    "uniquan_attn_bwd": ([_i64, _i64, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _f32, _vp, _vp, _vp, _vp, _vp], _i32),
     "uniquan_probe_mfma_flops": ([_i32], ctypes.c_double),
     "uniquan_probe_stream": ([_i32, _i64, _vp, _vp, _vp, _i32, _vp], _i32),
     "uniquan_probe_mfma": ([_i32, _vp, _vp], _i32),
@@ -509,21 +508,19 @@ def uniquan_softmax_causal_bwd(rows, L, dP, P, dS, stream=None):
                                             _stream(stream)))
 
 
-def uniquan_attn_fwd(batch, kv_batch, L, d, Q, K, Vt, scale, O, row_lse, stream=None):
+def uniquan_attn_fwd(batch, kv_batch, L, d, Q, K, V, scale, O, row_lse, stream=None):
     """Causal attention forward with on-chip score tiles (see the header)."""
     nq, nk = batch * L * d, kv_batch * L * d
-    _check(lib().uniquan_attn_fwd(batch, kv_batch, L, d, _p(Q, nq, _B, "Q"), _p(K, nk, _B, "K"), _p(Vt, nk, _B, "Vt"),
+    _check(lib().uniquan_attn_fwd(batch, kv_batch, L, d, _p(Q, nq, _B, "Q"), _p(K, nk, _B, "K"), _p(V, nk, _B, "V"),
                                   float(scale), _p(O, nq, _B, "O"), _p(row_lse, batch * L, _F, "row_lse"),
                                   _stream(stream)))
 
 
-def uniquan_attn_bwd(batch, kv_batch, L, d, Q, Qt, K, Kt, V, O, dO, dOt, row_lse, scale, delta, dQ, dK, dV,
-                     stream=None):
+def uniquan_attn_bwd(batch, kv_batch, L, d, Q, K, V, O, dO, row_lse, scale, delta, dQ, dK, dV, stream=None):
     """Causal attention backward: dQ and the per-query-head dK, dV (fp32), and the row terms delta."""
     nq, nk, nr = batch * L * d, kv_batch * L * d, batch * L
-    _check(lib().uniquan_attn_bwd(batch, kv_batch, L, d, _p(Q, nq, _B, "Q"), _p(Qt, nq, _B, "Qt"), _p(K, nk, _B, "K"),
-                                  _p(Kt, nk, _B, "Kt"), _p(V, nk, _B, "V"), _p(O, nq, _B, "O"), _p(dO, nq, _B, "dO"),
-                                  _p(dOt, nq, _B, "dOt"), _p(row_lse, nr, _F, "row_lse"), float(scale),
+    _check(lib().uniquan_attn_bwd(batch, kv_batch, L, d, _p(Q, nq, _B, "Q"), _p(K, nk, _B, "K"), _p(V, nk, _B, "V"),
+                                  _p(O, nq, _B, "O"), _p(dO, nq, _B, "dO"), _p(row_lse, nr, _F, "row_lse"), float(scale),
                                   _p(delta, nr, _F, "delta"), _p(dQ, nq, _F, "dQ"), _p(dK, nq, _F, "dK"),
                                   _p(dV, nq, _F, "dV"), _stream(stream)))
 

@@ -74,18 +74,14 @@ def test_attention_fused(L, batch, kv_batch, sharp):
     kv = np.arange(batch) % kv_batch          # query batch g kv_batch + c uses key/value batch c
     # device
     dq, dk, dv, ddo = dev(Q), dev(K), dev(V), dev(dO)
-    Vt = dev(np.swapaxes(V, 1, 2))
-    Kt = dev(np.swapaxes(K, 1, 2))
-    Qt = dev(np.swapaxes(Q, 1, 2))
-    dOt = dev(np.swapaxes(dO, 1, 2))
     Od = torch.empty(batch, L, d, dtype=torch.bfloat16, device="cuda")
     lse = torch.empty(batch, L, device="cuda")
-    uq.uniquan_attn_fwd(batch, kv_batch, L, d, dq, dk, Vt, sc, Od, lse)
+    uq.uniquan_attn_fwd(batch, kv_batch, L, d, dq, dk, dv, sc, Od, lse)
     delta = torch.empty(batch, L, device="cuda")
     gQ = torch.empty(batch, L, d, device="cuda")
     gK = torch.empty(batch, L, d, device="cuda")
     gV = torch.empty(batch, L, d, device="cuda")
-    uq.uniquan_attn_bwd(batch, kv_batch, L, d, dq, Qt, dk, Kt, dv, Od, ddo, dOt, lse, sc, delta, gQ, gK, gV)
+    uq.uniquan_attn_bwd(batch, kv_batch, L, d, dq, dk, dv, Od, ddo, lse, sc, delta, gQ, gK, gV)
     torch.cuda.synchronize()
     # oracle, one query batch at a time
     got = dict(O=host(Od), lse=host(lse), delta=host(delta), dQ=host(gQ), dK=host(gK), dV=host(gV))
