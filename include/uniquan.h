@@ -69,7 +69,7 @@ typedef enum { UQ_OK = 0, UQ_EINVAL = 1, UQ_EUNSUPPORTED = 2, UQ_EHIP = 3 } uq_s
 typedef enum { UQ_F32 = 0, UQ_BF16 = 1 } uq_dtype;
 typedef enum { UQ_MAP_FULL = 0, UQ_MAP_LOCAL = 1, UQ_MAP_FROZEN = 2 } uq_map_mode;
 
-#define UNIQUAN_ABI_VERSION 1
+#define UNIQUAN_ABI_VERSION 2
 
 /* ABI version of the loaded library (UNIQUAN_ABI_VERSION). */
 int uniquan_abi_version(void);
@@ -503,6 +503,26 @@ uq_status uniquan_rmsnorm_bwd(int64_t T, int64_t C, const float* dZa,
 uq_status uniquan_rope_split(int64_t T, int H, int d, int L, int group,
                              const void* in, int in_dtype, int rotate,
                              uint16_t* out, void* stream);
+
+/*
+ * uniquan_rope_table -- cs [L, d/2] pairs (cos, sin) of the rotary angle
+ * (p, i) -> p 1e4^(-2i/d) at every position p < L (fp32, 16-byte aligned),
+ * the values uniquan_rope_split uses.  d even, at most 1024.
+ *
+ * uniquan_gemm_heads -- the block's query / key / value projection with the
+ * head split (and rotation) of uniquan_rope_split folded into the product's
+ * store (Algorithm 1's forward through the attention module):
+ *     Y = A W^T  (A [T x K] bf16, W [H 128 x K] bf16, fp32 accumulation),
+ *     out = uniquan_rope_split(Y) with d = 128, group and rotate as there,
+ * out bf16 head-major [H, T, 128], bit for bit the result of
+ * uniquan_gemm_nt (fp32 out) followed by uniquan_rope_split.  cs from
+ * uniquan_rope_table(L, 128) (read only when rotate != 0).  K a multiple of
+ * 32, L divides T; out 8-byte and cs 32-byte aligned.
+ */
+uq_status uniquan_rope_table(int L, int d, float* cs, void* stream);
+uq_status uniquan_gemm_heads(int64_t T, int H, int64_t K, const uint16_t* A,
+                             const uint16_t* W, int L, int group, int rotate,
+                             const float* cs, uint16_t* out, void* stream);
 uq_status uniquan_rope_merge(int64_t T, int H, int d, int L, int group,
                              int nsum, const void* in, int in_dtype, int rotate,
                              uint16_t* out, void* stream);

@@ -185,6 +185,9 @@ class DecoderBlock:
         self.Kh, self.Vh = e(Bkv, L, d, **b16), e(Bkv, L, d, **b16)
         # attention rows: base-2 log-sum-exp of the scores, the softmax backward's row term
         self.lse, self.delta = e(B, L, **f32), e(B, L, **f32)
+        # cos and sin of every rotary angle of a sequence, for the projections' head split
+        self.rope_cs = e(L, d // 2, 2, **f32)
+        uq.uniquan_rope_table(L, d, self.rope_cs)
         # dQ per query head; dK, dV contributions per query head (summed per key/value head)
         self.dQr, self.dKp, self.dVp = (e(B, L, d, **f32) for _ in range(3))
         # MLP activations and their gradients, one row per token
@@ -200,12 +203,9 @@ class DecoderBlock:
         sc = 1.0 / float(d) ** 0.5
         uq.uniquan_add_rmsnorm(T, C, X, None, self.g1, None, self.Z1, self.r1)
         Hkv, Ckv, Bkv, grp = self.Hkv, self.Ckv, self.Bkv, self.grp
-        uq.uniquan_gemm_nt(T, C, C, self.Z1, W["q"], self.Qf)
-        uq.uniquan_gemm_nt(T, Ckv, C, self.Z1, W["k"], self.Kf)
-        uq.uniquan_gemm_nt(T, Ckv, C, self.Z1, W["v"], self.Vb)
-        uq.uniquan_rope_split(T, H, d, L, self.Qf, self.Qh, rotate=True, group=grp)
-        uq.uniquan_rope_split(T, Hkv, d, L, self.Kf, self.Kh, rotate=True)
-        uq.uniquan_rope_split(T, Hkv, d, L, self.Vb, self.Vh, rotate=False)
+        self._project_heads(W["q"], H, self.Qh, grp, True, self.Qf)
+        self._project_heads(W["k"], Hkv, self.Kh, 1, True, self.Kf)
+        self._project_heads(W["v"], Hkv, self.Vh, 1, False, self.Vb)
         # causal attention with the score tiles on chip (query batch g Bkv + c uses key/value batch c)
         uq.uniquan_attn_fwd(B, Bkv, L, d, self.Qh, self.Kh, self.Vh, sc, self.Oh, self.lse)
         uq.uniquan_rope_merge(T, H, d, L, self.Oh, self.O, rotate=False, group=grp)
@@ -215,6 +215,19 @@ class DecoderBlock:
         uq.uniquan_gemm_nt(T, I, C, self.Z2, W["u"], self.Um)
         uq.uniquan_silu_mul_fwd(self.Gm, self.Um, self.Hm)
         uq.uniquan_gemm_nt(T, C, I, self.Hm, W["d"], self.M32)
+
+    def _project_heads(self, Wm, n_heads, out, group, rotate, tmp):
+        """out [n_heads, T, d] = the head split (rotated when rotate) of Z1 Wm^T:
+        in the product's store where the product fills the GPU with 256 x 256
+        tiles, else a product into tmp followed by the stand-alone split (the
+        same values)."""
+        T, C, d, L = self.T, self.C, self.d, self.L
+        N = n_heads * d
+        if ((T + 255) // 256) * ((N + 255) // 256) >= 256:
+            uq.uniquan_gemm_heads(T, n_heads, C, self.Z1, Wm, L, out, group=group, rotate=rotate, cs=self.rope_cs)
+        else:
+            uq.uniquan_gemm_nt(T, N, C, self.Z1, Wm, tmp)
+            uq.uniquan_rope_split(T, n_heads, d, L, tmp, out, rotate=rotate, group=group)
 
     def _sum_out(self, out):
         """out = R + M (fp32), through the residual-add path of the norm kernel."""

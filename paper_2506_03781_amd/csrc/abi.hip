@@ -505,6 +505,32 @@ uq_status uniquan_rope_split(int64_t T, int H, int d, int L, int group, const vo
                                               static_cast<hipStream_t>(stream)));
 }
 
+uq_status uniquan_rope_table(int L, int d, float* cs, void* stream) {
+  const char* fn = "uniquan_rope_table";
+  if (L < 1 || d < 2 || d % 2 != 0 || d > 1024) return fail(UQ_EINVAL, "%s: L=%d >= 1 and even d=%d <= 1024", fn, L, d);
+  if (int64_t(L) * d >= (int64_t(1) << 31)) return fail(UQ_EUNSUPPORTED, "%s: L=%d too large", fn, L);
+  REQ_PTR(cs, 16);
+  return hip_status(fn, uq::launch_rope_table(L, d, cs, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uniquan_gemm_heads(int64_t T, int H, int64_t K, const uint16_t* A, const uint16_t* W, int L, int group,
+                             int rotate, const float* cs, uint16_t* out, void* stream) {
+  const char* fn = "uniquan_gemm_heads";
+  if (T < 1 || H < 1 || K < 1 || L < 1) return fail(UQ_EINVAL, "%s: T, H, K, L must be >= 1", fn);
+  if (K % 32 != 0) return fail(UQ_EINVAL, "%s: K=%lld must be a multiple of 32", fn, (long long)K);
+  if (T % L != 0) return fail(UQ_EINVAL, "%s: L=%d must divide T=%lld", fn, L, (long long)T);
+  if (group < 1 || H % group != 0) return fail(UQ_EINVAL, "%s: group=%d must divide H=%d", fn, group, H);
+  const int64_t N = int64_t(H) * 128;
+  if (N >= (int64_t(1) << 26) || K >= (int64_t(1) << 31) || T >= (int64_t(1) << 31) ||
+      T * K >= (int64_t(1) << 40) || N * K >= (int64_t(1) << 40) || T * N >= (int64_t(1) << 40))
+    return fail(UQ_EUNSUPPORTED, "%s: shape too large", fn);
+  REQ_PTR(A, 16); REQ_PTR(W, 16); REQ_PTR(out, 8);
+  if (rotate) REQ_PTR(cs, 32);
+  uq::GemmLaunch g{A, W, T, N, K, rotate ? uq::EPI_HEADS_ROT : uq::EPI_HEADS, nullptr, out, nullptr, 1.0f};
+  g.heads = uq::HeadsParams{cs, L, H, group};
+  return hip_status(fn, uq::launch_gemm(g, static_cast<hipStream_t>(stream)));
+}
+
 uq_status uniquan_rope_merge(int64_t T, int H, int d, int L, int group, int nsum, const void* in, int in_dtype,
                              int rotate, uint16_t* out, void* stream) {
   const char* fn = "uniquan_rope_merge";

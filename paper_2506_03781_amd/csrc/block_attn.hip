@@ -233,6 +233,19 @@ __device__ __forceinline__ void rope_table(float2* cs, int64_t t0, int64_t T, in
   __syncthreads();
 }
 
+// cos and sin of every pair at every position of an L-token sequence:
+// cs[(p * (d / 2) + i) * 2 + {0, 1}] = cos, sin of rope_angle(p, i, d), the
+// values the rotary kernels compute in place.
+__global__ __launch_bounds__(256) void rope_table_kernel(int L, int d, float* __restrict__ cs) {
+  const int hd = d >> 1;
+  const int64_t k = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (k >= int64_t(L) * hd) return;
+  float sn, cn;
+  sincosf(rope_angle(int(k / hd), int(k % hd), d), &sn, &cn);
+  cs[2 * k] = cn;
+  cs[2 * k + 1] = sn;
+}
+
 template <bool IN_F32, bool ROT>
 __global__ __launch_bounds__(256) void rope_split_vec_kernel(int64_t T, int H, int d, int L, int perm,
                                                              const void* __restrict__ in, uint16_t* __restrict__ out) {
@@ -519,6 +532,12 @@ hipError_t launch_rmsnorm_bwd(int64_t T, int64_t C, const float* dZa, const floa
 static bool rope_vec_ok(int d, const void* in, const void* out) {
   return d % 16 == 0 && d / 2 <= RT_MAX_HD && (reinterpret_cast<uintptr_t>(in) & 15) == 0 &&
          (reinterpret_cast<uintptr_t>(out) & 15) == 0;
+}
+
+hipError_t launch_rope_table(int L, int d, float* cs, hipStream_t st) {
+  const int64_t n = int64_t(L) * (d / 2);
+  hipLaunchKernelGGL(rope_table_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, st, L, d, cs);
+  return hipGetLastError();
 }
 
 hipError_t launch_rope_split(int64_t T, int H, int d, int L, int perm, const void* in, int in_f32, int rotate,

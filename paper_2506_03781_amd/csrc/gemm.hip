@@ -59,6 +59,7 @@ struct GemmArgs {
   // K loop at the row tile's end (A zero above the diagonal), 3 starts it at
   // the row tile's start (A zero below the diagonal)
   int causal;
+  HeadsParams heads;
 };
 
 // Operands and output of batch blockIdx.y.
@@ -78,6 +79,53 @@ typedef float f32x2 __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   const f32x2 f = {lo, hi};
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2));
+}
+
+// A 32-row strip of one head (128 columns, fp32 in LDS, row stride 128) to
+// the head-major bf16 output: element (row_base + r, h * 128 + j) goes to
+// out[(slot(h) * M + row_base + r) * 128 + j], with the pairs (j, j + 64)
+// rotated by the row's position angle when ROT: y1 = x1 c - x2 s,
+// y2 = x2 c + x1 s (products rounded, then the sum, as the stand-alone
+// rotary split computes them).  Lane l takes 4 consecutive pairs of rows
+// l / 16 + 4 k.
+template <bool ROT>
+__device__ __forceinline__ void heads_strip(const GemmArgs& p, const float* strip, int64_t row_base, int64_t col_base,
+                                            int lane) {
+  const HeadsParams& hp = p.heads;
+  const int h = int(col_base >> 7);
+  const int slot = hp.perm > 1 ? (h % hp.perm) * (hp.H / hp.perm) + h / hp.perm : h;
+  const int i0 = 4 * (lane & 15);
+  uint16_t* out = static_cast<uint16_t*>(p.out) + int64_t(slot) * p.M * 128 + i0;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const int r = (lane >> 4) + 4 * k;
+    const int64_t m = row_base + r;
+    if (m >= p.M) break;
+    const float4 a = *reinterpret_cast<const float4*>(&strip[r * 128 + i0]);
+    const float4 b = *reinterpret_cast<const float4*>(&strip[r * 128 + 64 + i0]);
+    float x1[4] = {p.scale * a.x, p.scale * a.y, p.scale * a.z, p.scale * a.w};
+    float x2[4] = {p.scale * b.x, p.scale * b.y, p.scale * b.z, p.scale * b.w};
+    float y1[4], y2[4];
+    if constexpr (ROT) {
+      const float4* cs = reinterpret_cast<const float4*>(hp.cs + (int64_t(m % hp.L) * 64 + i0) * 2);
+      const float4 c01 = cs[0], c23 = cs[1];  // (cos, sin) of pairs i0 .. i0 + 3
+      const float cn[4] = {c01.x, c01.z, c23.x, c23.z}, sn[4] = {c01.y, c01.w, c23.y, c23.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        y1[e] = x1[e] * cn[e] - x2[e] * sn[e];
+        y2[e] = x2[e] * cn[e] + x1[e] * sn[e];
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        y1[e] = x1[e];
+        y2[e] = x2[e];
+      }
+    }
+    uint16_t* o = out + m * 128;
+    *reinterpret_cast<uint2*>(o) = make_uint2(pack_bf16x2(y1[0], y1[1]), pack_bf16x2(y1[2], y1[3]));
+    *reinterpret_cast<uint2*>(o + 64) = make_uint2(pack_bf16x2(y2[0], y2[1]), pack_bf16x2(y2[2], y2[3]));
+  }
 }
 
 // Map a linear workgroup id to (tile_m, tile_n).  Hardware dispatches
@@ -251,6 +299,13 @@ __device__ __forceinline__ void epilogue(const GemmArgs& p, f32x16 (&acc)[FM][FN
     __builtin_amdgcn_wave_barrier();
     const int64_t row_base = m0 + wm * WM + i * 32;
     const int64_t col_base = n0 + wn * WN;
+    if constexpr (EPI == EPI_HEADS || EPI == EPI_HEADS_ROT) {
+      static_assert(WN == 128, "the head split needs 128-column wave tiles");
+      if (col_base < p.N) heads_strip<EPI == EPI_HEADS_ROT>(p, strip, row_base, col_base, lane);
+      __builtin_amdgcn_s_waitcnt(0xC07F);  // strip reads done before the next strip overwrites it
+      __builtin_amdgcn_wave_barrier();
+      continue;
+    }
     if constexpr (EPI >= EPI_STE) {
       static_assert(WN == 128, "the fused backward needs 128-column wave tiles");
       // row-iterations whose loads are in flight together: 8 with four
@@ -988,7 +1043,28 @@ static hipError_t launch_gemm_kslow(const GemmLaunch& q, hipStream_t st) {
   return hipGetLastError();
 }
 
+// Head-split products (EPI_HEADS*): 256 x 256 tiles on the ping-pong kernel
+// with a 4 x 2 wave grid (64 x 128 wave tiles: a wave holds whole heads).
+// K % 32 == 0, N % 128 == 0.
+static hipError_t launch_gemm_heads(const GemmLaunch& q, hipStream_t st) {
+  GemmArgs a;
+  a.A = q.A; a.B = q.B; a.M = q.M; a.N = q.N; a.K = q.K;
+  a.Yt = nullptr; a.out = q.out; a.partials = nullptr; a.scale = q.scale;
+  a.bsa = a.bsb = a.bso = 0;
+  a.causal = 0;
+  a.heads = q.heads;
+  a.tiles_m = int((q.M + 255) / 256);
+  a.tiles_n = int((q.N + 255) / 256);
+  const dim3 grid(unsigned(a.tiles_m * a.tiles_n));
+  if (q.epi == EPI_HEADS_ROT)
+    hipLaunchKernelGGL((gemm_pp_kernel<256, 256, EPI_HEADS_ROT, 4>), grid, dim3(512), 0, st, a);
+  else
+    hipLaunchKernelGGL((gemm_pp_kernel<256, 256, EPI_HEADS, 4>), grid, dim3(512), 0, st, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_gemm(const GemmLaunch& q, hipStream_t st) {
+  if (q.epi == EPI_HEADS || q.epi == EPI_HEADS_ROT) return launch_gemm_heads(q, st);
   if (q.ta || q.tb) return launch_gemm_kslow(q, st);
   switch (pick(q.M, q.N, q.batch)) {
     case T256x256: return launch_bm<256, 256>(q, st);

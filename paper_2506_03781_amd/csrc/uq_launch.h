@@ -102,6 +102,16 @@ enum GemmEpi : int {
   EPI_STE = 16,       // EPI_STE + k: scale * acc is dL/dWhat; straight-through backward + SGD in place
   EPI_GRAD_F32 = 3,   // out fp32 = scale * acc
   EPI_LOSS_RES = 4,   // EPI_LOSS without a target (A holds What - W); chosen when Yt is NULL
+  EPI_HEADS = 5,      // out bf16 head-major [H, M, 128] = scale * acc (column block h to head slot h)
+  EPI_HEADS_ROT = 6,  // EPI_HEADS with the rotary rotation of each head's pairs (i, i + 64)
+};
+
+// Head-split epilogue (EPI_HEADS*): position of row m is m % L; cos and sin
+// of pair i at position p in cs[p * 64 + i]; head h goes to slot
+// (h % perm) * (H / perm) + h / perm (perm > 1) or h.
+struct HeadsParams {
+  const float* cs;  // [L, 64] (cos, sin) pairs
+  int L, H, perm;
 };
 
 struct GemmLaunch {
@@ -122,6 +132,7 @@ struct GemmLaunch {
   // operands stored K-slow (EPI_GRAD_*, no batch, no causal mode): A as
   // [K x M] (ta = 1), B as [K x N] (tb = 1)
   int ta, tb;
+  HeadsParams heads;   // EPI_HEADS*
 };
 
 // Causal attention with the score tiles on chip (attn_fused.hip), d = 128.
@@ -173,6 +184,7 @@ hipError_t launch_add_rmsnorm(int64_t T, int64_t C, const float* X, const float*
 hipError_t launch_rmsnorm_bwd(int64_t T, int64_t C, const float* dZa, const float* dZb, const float* X,
                               const float* gamma, const float* rinv, const uint16_t* E, float escale, uint16_t* dR,
                               float* dRf, hipStream_t st);
+hipError_t launch_rope_table(int L, int d, float* cs, hipStream_t st);
 hipError_t launch_rope_split(int64_t T, int H, int d, int L, int perm, const void* in, int in_f32, int rotate,
                              uint16_t* out, hipStream_t st);
 hipError_t launch_rope_merge(int64_t T, int H, int d, int L, int perm, int nsum, const void* in, int in_f32,

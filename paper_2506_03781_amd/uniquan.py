@@ -63,6 +63,8 @@ _SIGS = {
     "uniquan_bcq_pack": ([_i64, _i64, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp], _i32),
     "uniquan_gemm_nt": ([_i64, _i64, _i64, _vp, _vp, _vp, _i32, _f32, _vp], _i32),
     "uniquan_gemm": ([_i64, _i64, _i64, _vp, _i32, _vp, _i32, _vp, _i32, _f32, _vp], _i32),
+    "uniquan_rope_table": ([_i32, _i32, _vp, _vp], _i32),
+    "uniquan_gemm_heads": ([_i64, _i32, _i64, _vp, _vp, _i32, _i32, _i32, _vp, _vp, _vp], _i32),
     "uniquan_silu_mul_fwd": ([_i64, _vp, _vp, _vp, _vp], _i32),
     "uniquan_silu_mul_bwd": ([_i64, _vp, _vp, _vp, _vp, _vp, _vp], _i32),
     "uniquan_gemm_nt_batched": ([_i64, _i64, _i64, _i64, _vp, _i64, _vp, _i64, _vp, _i64, _i32, _f32, _i32, _vp],
@@ -445,6 +447,19 @@ def uniquan_gemm(M, N, K, A, a_kslow, B, b_kslow, out, scale=1.0, stream=None):
     B stored [N, K] or, with b_kslow, [K, N] (bf16 operands; out bf16 or fp32)."""
     _check(lib().uniquan_gemm(M, N, K, _p(A, M * K, _B, "A"), int(bool(a_kslow)), _p(B, N * K, _B, "B"),
                               int(bool(b_kslow)), _p(out, M * N, _W, "out"), _dt(out), float(scale), _stream(stream)))
+
+
+def uniquan_rope_table(L, d, cs, stream=None):
+    """cs [L, d/2, 2] fp32: cos and sin of every rotary angle (as uniquan_rope_split uses them)."""
+    _check(lib().uniquan_rope_table(int(L), int(d), _p(cs, L * d, _F, "cs"), _stream(stream)))
+
+
+def uniquan_gemm_heads(T, H, K, A, W, L, out, group=1, rotate=True, cs=None, stream=None):
+    """out [H, T, 128] bf16 = uniquan_rope_split(A [T, K] W [H 128, K]^T) (group, rotate as there)."""
+    N = H * 128
+    _check(lib().uniquan_gemm_heads(T, H, K, _p(A, T * K, _B, "A"), _p(W, N * K, _B, "W"), int(L), int(group),
+                                    int(bool(rotate)), _p(cs, L * 128, _F, "cs") if rotate else None,
+                                    _p(out, T * N, _B, "out"), _stream(stream)))
 
 
 def uniquan_silu_mul_fwd(G, U, H, stream=None):

@@ -196,6 +196,13 @@ def test_block_entry_validation(L):
     assert L.uniquan_gemm_nt(4, 1 << 26, 8, FAKE, FAKE, FAKE, F, 1.0, None) == uq.UQ_EUNSUPPORTED
     assert L.uniquan_gemm_nt(4, 8, 8, ODD, FAKE, FAKE, F, 1.0, None) == uq.UQ_EINVAL
     assert L.uniquan_gemm_nt(4, 8, 8, FAKE, FAKE, FAKE, 7, 1.0, None) == uq.UQ_EINVAL
+    assert L.uniquan_rope_table(0, 128, FAKE, None) == uq.UQ_EINVAL
+    assert L.uniquan_rope_table(16, 7, FAKE, None) == uq.UQ_EINVAL
+    gh = L.uniquan_gemm_heads
+    assert gh(512, 4, 48, FAKE, FAKE, 512, 1, 1, FAKE, FAKE, None) == uq.UQ_EINVAL   # K % 32
+    assert gh(512, 4, 64, FAKE, FAKE, 300, 1, 1, FAKE, FAKE, None) == uq.UQ_EINVAL   # L divides T
+    assert gh(512, 4, 64, FAKE, FAKE, 512, 3, 1, FAKE, FAKE, None) == uq.UQ_EINVAL   # group divides H
+    assert gh(512, 4, 64, FAKE, FAKE, 512, 1, 1, None, FAKE, None) == uq.UQ_EINVAL   # rotation needs the table
     g = L.uniquan_gemm
     assert g(8, 8, 32, FAKE, 2, FAKE, 0, FAKE, F, 1.0, None) == uq.UQ_EINVAL
     assert g(8, 8, 48, FAKE, 1, FAKE, 0, FAKE, F, 1.0, None) == uq.UQ_EINVAL   # K-slow needs K % 32 == 0

@@ -95,6 +95,36 @@ def test_gemm_kslow_operands(M, N, K, a_kslow, b_kslow, out_dtype):
         within_bf16(got, ref, floor=1e-5 * mag, what="bf16 out")
 
 
+@pytest.mark.parametrize("T,H,K,L,group,rotate", [(520, 4, 96, 260, 1, True), (2048, 8, 64, 512, 4, True),
+                                                  (2048, 8, 64, 1024, 1, False), (8192, 32, 128, 2048, 1, True)])
+def test_gemm_heads_matches_product_then_split(T, H, K, L, group, rotate):
+    """The projection with the head split (and rotation) in the product's
+    store equals uniquan_gemm_nt (fp32) followed by uniquan_rope_split, bit for
+    bit: ragged rows (520 = 2 x 256 + 8), grouped slot order, no rotation, and
+    the 7B shape (32 heads, sequences of 2048)."""
+    rs = np.random.default_rng(T + H + K + L + group)
+    d = 128
+    A = dev(bfr(rs.standard_normal((T, K))), torch.bfloat16)
+    W = dev(bfr(rs.standard_normal((H * d, K)) * 0.1), torch.bfloat16)
+    cs = torch.empty(L, d // 2, 2, device="cuda")
+    uq.uniquan_rope_table(L, d, cs)
+    fused = torch.full((H, T, d), float("nan"), device="cuda", dtype=torch.bfloat16)
+    uq.uniquan_gemm_heads(T, H, K, A, W, L, fused, group=group, rotate=rotate, cs=cs)
+    Y = torch.empty(T, H * d, device="cuda")
+    uq.uniquan_gemm_nt(T, H * d, K, A, W, Y)
+    ref = torch.empty(H, T, d, device="cuda", dtype=torch.bfloat16)
+    uq.uniquan_rope_split(T, H, d, L, Y, ref, rotate=rotate, group=group)
+    torch.cuda.synchronize()
+    assert torch.equal(fused.view(torch.int16), ref.view(torch.int16))
+    # the table against the angle's definition (fp64 cos / sin of the fp32 angle within fp32 rounding)
+    c = cs.cpu().numpy().astype(np.float64)
+    p = np.arange(L, dtype=np.float64)[:, None]
+    i = np.arange(d // 2, dtype=np.float64)[None, :]
+    ang = p * 10000.0 ** (-2 * i / d)
+    assert np.all(np.abs(c[..., 0] - np.cos(ang)) <= 1e-6 * (1 + np.abs(ang)))
+    assert np.all(np.abs(c[..., 1] - np.sin(ang)) <= 1e-6 * (1 + np.abs(ang)))
+
+
 @pytest.mark.parametrize("T,C", [(5, 8), (37, 264), (64, 4096)])
 def test_add_rmsnorm(T, C):
     rs = np.random.default_rng(T * C)
