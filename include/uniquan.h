@@ -559,22 +559,33 @@ uq_status uniquan_softmax_causal_bwd(int64_t rows, int L, const float* dP,
  *   the sum of their contributions (uniquan_rope_merge with nsum sums them).
  * The rounding points are those of the unfused path (P and dS in bf16, S and
  * dP in fp32).
- * Layouts (bf16 unless stated): Q, O, dO [batch, L, d]; K, V [kv_batch, L,
- * d] (the products that contract over the rows of a tile read it through
- * LDS transpose reads, so no transposed copies are taken); row_lse, delta
- * [batch, L] fp32 (delta written by uniquan_attn_bwd); dQ, dK, dV
- * [batch, L, d] fp32 out.  d = 128
+ * Layouts (bf16 unless stated): Q [batch, L, d]; K, V [kv_batch, L, d] (the
+ * products that contract over the rows of a tile read it through LDS
+ * transpose reads, so no transposed copies are taken); row_lse, delta
+ * [batch, L] fp32 (delta written by uniquan_attn_bwd).
+ * With tok_seqs = 0: O, dO [batch, L, d]; dQ, dK, dV [batch, L, d] fp32 out.
+ * With tok_seqs = n > 0 (n divides batch and kv_batch; H = batch / n query
+ * heads, group dividing H): O and dO are token-major [n L, H d] bf16 rows,
+ * query batch b = slot n + s holding head (slot mod (H/group)) group +
+ * slot / (H/group) of sequence s (the slot order of uniquan_rope_split), so
+ * O needs no merge and dO no split; dQ is written token-major bf16 after the
+ * inverse rotation of uniquan_rope_merge (cs from uniquan_rope_table(L, 128),
+ * 32-byte aligned), bit for bit what the fp32 dQ and a merge give; dK and dV
+ * likewise (dK inverse-rotated, dV not) when kv_batch = batch, and fp32
+ * per-query-head [batch, L, d] partials as with tok_seqs = 0 otherwise (the
+ * merge sums them over each key/value head's group).  d = 128
  * and L a multiple of 32 (UQ_EUNSUPPORTED otherwise); batch a positive
  * multiple of kv_batch, at most 65535; every pointer 16-byte aligned.
  */
 uq_status uniquan_attn_fwd(int64_t batch, int64_t kv_batch, int L, int d,
                            const uint16_t* Q, const uint16_t* K, const uint16_t* V,
-                           float scale, uint16_t* O, float* row_lse, void* stream);
+                           float scale, uint16_t* O, float* row_lse, int tok_seqs,
+                           int group, void* stream);
 uq_status uniquan_attn_bwd(int64_t batch, int64_t kv_batch, int L, int d,
                            const uint16_t* Q, const uint16_t* K, const uint16_t* V,
                            const uint16_t* O, const uint16_t* dO, const float* row_lse,
-                           float scale, float* delta, float* dQ, float* dK, float* dV,
-                           void* stream);
+                           float scale, float* delta, void* dQ, void* dK, void* dV,
+                           int tok_seqs, int group, const float* cs, void* stream);
 
 /*
  * uniquan_transpose_bf16_batched -- out_b = in_b^T for batch matrices

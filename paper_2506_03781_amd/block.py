@@ -181,15 +181,16 @@ class DecoderBlock:
         (self.Z1, self.O, self.Z2, self.E, self.dA, self.dO, self.dQ) = (e(T, C, **b16) for _ in range(7))
         self.Vb, self.dK, self.dV = (e(T, Ckv, **b16) for _ in range(3))
         # query heads in grouped slot order (see uniquan_rope_split), key/value heads plain
-        self.Qh, self.Oh, self.dOh = (e(B, L, d, **b16) for _ in range(3))
+        self.Qh = e(B, L, d, **b16)
         self.Kh, self.Vh = e(Bkv, L, d, **b16), e(Bkv, L, d, **b16)
         # attention rows: base-2 log-sum-exp of the scores, the softmax backward's row term
         self.lse, self.delta = e(B, L, **f32), e(B, L, **f32)
-        # cos and sin of every rotary angle of a sequence, for the projections' head split
+        # cos and sin of every rotary angle of a sequence, for the projections'
+        # head split and the attention gradients' inverse rotation
         self.rope_cs = e(L, d // 2, 2, **f32)
         uq.uniquan_rope_table(L, d, self.rope_cs)
-        # dQ per query head; dK, dV contributions per query head (summed per key/value head)
-        self.dQr, self.dKp, self.dVp = (e(B, L, d, **f32) for _ in range(3))
+        # grouped-query: dK, dV contributions per query head (summed per key/value head)
+        self.dKp, self.dVp = (e(B, L, d, **f32) for _ in range(2)) if self.grp > 1 else (None, None)
         # MLP activations and their gradients, one row per token
         self.Gm, self.Um, self.Hm, self.dHm, self.dGm, self.dUm = (e(T, I, **b16) for _ in range(6))
         self.partials = e(uq.uniquan_block_loss_ws(), **f32)
@@ -207,8 +208,9 @@ class DecoderBlock:
         self._project_heads(W["k"], Hkv, self.Kh, 1, True, self.Kf)
         self._project_heads(W["v"], Hkv, self.Vh, 1, False, self.Vb)
         # causal attention with the score tiles on chip (query batch g Bkv + c uses key/value batch c)
-        uq.uniquan_attn_fwd(B, Bkv, L, d, self.Qh, self.Kh, self.Vh, sc, self.Oh, self.lse)
-        uq.uniquan_rope_merge(T, H, d, L, self.Oh, self.O, rotate=False, group=grp)
+        # (O written token-major: the merge of the heads is in the kernel's store)
+        uq.uniquan_attn_fwd(B, Bkv, L, d, self.Qh, self.Kh, self.Vh, sc, self.O, self.lse,
+                            tok_seqs=self.n_seq, group=grp)
         uq.uniquan_gemm_nt(T, C, C, self.O, W["o"], self.A32)
         uq.uniquan_add_rmsnorm(T, C, X, self.A32, self.g2, self.R, self.Z2, self.r2)
         uq.uniquan_gemm_nt(T, I, C, self.Z2, W["g"], self.Gm)
@@ -291,12 +293,16 @@ class DecoderBlock:
         uq.uniquan_gemm(T, C, C, self.dA, 0, Wh["o"], 1, self.dO)
         done("o")
         Hkv, Ckv, Bkv, grp = self.Hkv, self.Ckv, self.Bkv, self.grp
-        uq.uniquan_rope_split(T, H, d, L, self.dO, self.dOh, rotate=False, group=grp)
-        uq.uniquan_attn_bwd(B, Bkv, L, d, self.Qh, self.Kh, self.Vh, self.Oh, self.dOh,
-                            self.lse, sc, self.delta, self.dQr, self.dKp, self.dVp)
-        uq.uniquan_rope_merge(T, H, d, L, self.dQr, self.dQ, rotate=True, group=grp)
-        uq.uniquan_rope_merge(T, Hkv, d, L, self.dKp, self.dK, rotate=True, nsum=grp)
-        uq.uniquan_rope_merge(T, Hkv, d, L, self.dVp, self.dV, rotate=False, nsum=grp)
+        # O and dO token-major; dQ (and dK, dV with one query head per key/value
+        # head) written token-major and inverse-rotated by the kernels' stores
+        if grp == 1:
+            uq.uniquan_attn_bwd(B, Bkv, L, d, self.Qh, self.Kh, self.Vh, self.O, self.dO, self.lse, sc, self.delta,
+                                self.dQ, self.dK, self.dV, tok_seqs=self.n_seq, group=grp, cs=self.rope_cs)
+        else:
+            uq.uniquan_attn_bwd(B, Bkv, L, d, self.Qh, self.Kh, self.Vh, self.O, self.dO, self.lse, sc, self.delta,
+                                self.dQ, self.dKp, self.dVp, tok_seqs=self.n_seq, group=grp, cs=self.rope_cs)
+            uq.uniquan_rope_merge(T, Hkv, d, L, self.dKp, self.dK, rotate=True, nsum=grp)
+            uq.uniquan_rope_merge(T, Hkv, d, L, self.dVp, self.dV, rotate=False, nsum=grp)
         uq.uniquan_gemm(C, C, T, self.dQ, 1, self.Z1, 1, m["q"].G)
         done("q")
         uq.uniquan_gemm(Ckv, C, T, self.dK, 1, self.Z1, 1, m["k"].G)

@@ -602,30 +602,57 @@ static uq_status check_attn(const char* fn, int64_t batch, int64_t kv_batch, int
   return UQ_OK;
 }
 
+static uq_status check_tok(const char* fn, int64_t batch, int64_t kv_batch, int tok_seqs, int group) {
+  if (tok_seqs < 0 || (tok_seqs > 0 && (batch % tok_seqs != 0 || kv_batch % tok_seqs != 0)))
+    return fail(UQ_EINVAL, "%s: tok_seqs=%d must be 0 or divide batch and kv_batch", fn, tok_seqs);
+  if (tok_seqs > 0 && (group < 1 || (batch / tok_seqs) % group != 0))
+    return fail(UQ_EINVAL, "%s: group=%d must divide the query heads", fn, group);
+  if (tok_seqs > 0 && kv_batch == batch && group != 1)
+    return fail(UQ_EINVAL, "%s: group=%d with one query head per key/value head (must be 1)", fn, group);
+  return UQ_OK;
+}
+
 uq_status uniquan_attn_fwd(int64_t batch, int64_t kv_batch, int L, int d, const uint16_t* Q, const uint16_t* K,
-                           const uint16_t* V, float scale, uint16_t* O, float* row_lse, void* stream) {
+                           const uint16_t* V, float scale, uint16_t* O, float* row_lse, int tok_seqs, int group,
+                           void* stream) {
   const char* fn = "uniquan_attn_fwd";
   if (uq_status st = check_attn(fn, batch, kv_batch, L, d)) return st;
+  if (uq_status st = check_tok(fn, batch, kv_batch, tok_seqs, group)) return st;
   REQ_PTR(Q, 16); REQ_PTR(K, 16); REQ_PTR(V, 16); REQ_PTR(O, 16); REQ_PTR(row_lse, 16);
   uq::AttnLaunch q{};
   q.batch = batch; q.kv_batch = kv_batch; q.L = L; q.scale = scale;
   q.Q = Q; q.K = K; q.V = V; q.O_out = O; q.lse = row_lse;
+  q.tok_seqs = tok_seqs; q.group = group;
   return hip_status(fn, uq::launch_attn_fwd(q, static_cast<hipStream_t>(stream)));
 }
 
 uq_status uniquan_attn_bwd(int64_t batch, int64_t kv_batch, int L, int d, const uint16_t* Q, const uint16_t* K,
                            const uint16_t* V, const uint16_t* O, const uint16_t* dO, const float* row_lse, float scale,
-                           float* delta, float* dQ, float* dK, float* dV, void* stream) {
+                           float* delta, void* dQ, void* dK, void* dV, int tok_seqs, int group, const float* cs,
+                           void* stream) {
   const char* fn = "uniquan_attn_bwd";
   if (uq_status st = check_attn(fn, batch, kv_batch, L, d)) return st;
+  if (uq_status st = check_tok(fn, batch, kv_batch, tok_seqs, group)) return st;
   REQ_PTR(Q, 16); REQ_PTR(K, 16); REQ_PTR(V, 16); REQ_PTR(O, 16);
   REQ_PTR(dO, 16); REQ_PTR(row_lse, 16); REQ_PTR(delta, 16);
   REQ_PTR(dQ, 16); REQ_PTR(dK, 16); REQ_PTR(dV, 16);
+  if (tok_seqs > 0) REQ_PTR(cs, 32);
   uq::AttnLaunch q{};
   q.batch = batch; q.kv_batch = kv_batch; q.L = L; q.scale = scale;
   q.Q = Q; q.K = K; q.V = V; q.O = O; q.dO = dO;
+  q.tok_seqs = tok_seqs; q.group = group; q.cs = cs;
+  const bool bf_kv = tok_seqs > 0 && kv_batch == batch;  // token-major bf16 dK, dV
+  if (tok_seqs > 0) q.dQ_tok = static_cast<uint16_t*>(dQ);
+  if (bf_kv) {
+    q.dK_tok = static_cast<uint16_t*>(dK);
+    q.dV_tok = static_cast<uint16_t*>(dV);
+  }
   q.lse = const_cast<float*>(row_lse); q.delta = delta;
-  q.dQ = dQ; q.dK = dK; q.dV = dV;
+  if (tok_seqs == 0) q.dQ = static_cast<float*>(dQ);
+  if (!bf_kv) {
+    q.dK = static_cast<float*>(dK);
+    q.dV = static_cast<float*>(dV);
+  }
   return hip_status(fn, uq::launch_attn_bwd(q, static_cast<hipStream_t>(stream)));
 }
 

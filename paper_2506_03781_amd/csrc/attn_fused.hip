@@ -100,10 +100,10 @@ __device__ __forceinline__ int swz(int rho) { return ((rho & 3) << 2) | ((rho >>
 // (s % 16) ^ swz(rho) of tile row rho = s / 16, and tile row rho holds
 // source row perm32(rho) of the tile.  Copy block blk fills slots 64 blk ..
 // + 64; row_off is this lane's byte offset in the source tile for block blk.
-__device__ __forceinline__ uint32_t row_off(int blk, int lane) {
+__device__ __forceinline__ uint32_t row_off(int blk, int lane, int ld = D) {
   const int s = blk * 64 + lane;
   const int rho = s >> 4, c = (s & 15) ^ swz(rho);
-  return uint32_t(perm32(rho) * D * 2 + c * 16);
+  return uint32_t(perm32(rho)) * uint32_t(ld) * 2u + uint32_t(c * 16);
 }
 
 // A copy of 64 slots: lane l's 16 bytes at base + off land in slot l of dst.
@@ -169,6 +169,52 @@ __device__ __forceinline__ void store_f32_rows(float* out, const f32x16a (&acc)[
     }
 }
 
+// 16 accumulator values per d block (rows d = 32 db + 8 g4 + 4 (lane / 32) ..
+// + 4, scaled by mul) of this lane's row stored as one bf16 row of 128: the
+// pairs (j, j + 64) (d blocks db and db + 2 of one lane) rotated by minus the
+// angle of position pos when ROT, y1 = x1 c + x2 s, y2 = x2 c - x1 s, with
+// x = 0 + mul acc (the arithmetic of the stand-alone inverse split, which
+// sums its partials from zero).
+template <bool ROT>
+__device__ __forceinline__ void store_bf16_row(uint16_t* out, const f32x16a (&acc)[4], float mul, const float* cs,
+                                               int pos, int lane) {
+#pragma unroll
+  for (int db = 0; db < 2; ++db)
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4) {
+      const int j0 = 32 * db + 8 * g4 + 4 * (lane >> 5);
+      float y1[4], y2[4];
+      float4 c01 = {}, c23 = {};
+      if constexpr (ROT) {
+        const float4* t = reinterpret_cast<const float4*>(cs + (int64_t(pos) * 64 + j0) * 2);
+        c01 = t[0];
+        c23 = t[1];
+      }
+      const float cn[4] = {c01.x, c01.z, c23.x, c23.z}, sn[4] = {c01.y, c01.w, c23.y, c23.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float x1 = 0.0f + acc[db][4 * g4 + e] * mul;
+        const float x2 = 0.0f + acc[db + 2][4 * g4 + e] * mul;
+        if constexpr (ROT) {
+          y1[e] = x1 * cn[e] + x2 * sn[e];
+          y2[e] = x2 * cn[e] - x1 * sn[e];
+        } else {
+          y1[e] = x1;
+          y2[e] = x2;
+        }
+      }
+      bf16x8a w;  // the first four halves of each store
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        w[e] = __bf16(y1[e]);
+        w[4 + e] = __bf16(y2[e]);
+      }
+      const u32x4a u = __builtin_bit_cast(u32x4a, w);
+      *reinterpret_cast<u32x2a*>(out + j0) = u32x2a{u.x, u.y};
+      *reinterpret_cast<u32x2a*>(out + j0 + 64) = u32x2a{u.z, u.w};
+    }
+}
+
 // Workgroup -> (row block, batch).  When the batch count is a multiple of 8
 // the row blocks of one batch go to one XCD (workgroups are dealt to the 8
 // XCDs round-robin), so its keys and values stay in that XCD's L2; within a
@@ -202,7 +248,24 @@ struct AttnArgs {
   float* dQ;            // [batch, L, D]
   float* dK;            // [batch, L, D] per query head
   float* dV;            // [batch, L, D] per query head
+  // token-major I/O (TOK kernels): O, dO and the bf16 gradients as rows of
+  // [n_seq L, heads D]; query batch b = slot n_seq + s is head h(slot) of
+  // sequence s, h(slot) = (slot % (heads / grp)) grp + slot / (heads / grp)
+  // (the grouped slot order of the projections' head split)
+  int n_seq, heads, grp;
+  const float* cs;      // rotary (cos, sin) [L, 64]: the gradients' inverse rotation
+  uint16_t* dQ_tok;     // bf16 [n_seq L, heads D]
+  uint16_t* dK_tok;     // bf16, when kv_batch == batch (else dK, dV per query head)
+  uint16_t* dV_tok;
 };
+
+// Element offset of row l of query batch b in the token-major layout.
+__device__ __forceinline__ int64_t tok_off(const AttnArgs& a, int64_t b, int l) {
+  const int slot = int(b / a.n_seq), s = int(b % a.n_seq);
+  const int per = a.heads / a.grp;
+  const int h = (slot % per) * a.grp + slot / per;
+  return (int64_t(s) * a.L + l) * (int64_t(a.heads) * D) + int64_t(h) * D;
+}
 
 // Copies of one tile: PW blocks of 64 slots per wave (blocks wave PW .. + PW).
 template <int PW>
@@ -214,7 +277,7 @@ __device__ __forceinline__ void copy_tile(const uint16_t* base, const uint32_t (
 // Forward: one workgroup of NW waves per (NW * 32 queries, query batch); wave
 // w owns 32 queries and multiplies the key tiles up to its diagonal (the
 // workgroup copies the tiles up to its last diagonal).
-template <int NW, int S>
+template <int NW, int S, bool TOK>
 __global__ __launch_bounds__(NW * 64) void attn_fwd_kernel(AttnArgs a) {
   constexpr int QB = NW * NB;
   constexpr int PW = 8 / NW;  // copy blocks per wave and tile
@@ -336,7 +399,7 @@ __global__ __launch_bounds__(NW * 64) void attn_fwd_kernel(AttnArgs a) {
     }
   }
   if (!active) return;
-  uint16_t* orow = a.O_out + (b * L + qi) * int64_t(D);
+  uint16_t* orow = a.O_out + (TOK ? tok_off(a, b, qi) : (b * L + qi) * int64_t(D));
 #pragma unroll
   for (int db = 0; db < 4; ++db)
 #pragma unroll
@@ -344,7 +407,11 @@ __global__ __launch_bounds__(NW * 64) void attn_fwd_kernel(AttnArgs a) {
       const int d0 = 32 * db + 8 * g4 + 4 * (lane >> 5);
       bf16x8a w;  // only the first four are stored
 #pragma unroll
-      for (int i = 0; i < 8; ++i) w[i] = __bf16(o[db][4 * g4 + (i & 3)]);
+      for (int i = 0; i < 8; ++i) {
+        w[i] = __bf16(o[db][4 * g4 + (i & 3)]);
+        // token-major: as the stand-alone merge stores it (0 + x: a -0 becomes +0)
+        if (TOK) w[i] = __bf16(0.0f + float(w[i]));
+      }
       const u32x4a u = __builtin_bit_cast(u32x4a, w);
       *reinterpret_cast<u32x2a*>(orow + d0) = u32x2a{u.x, u.y};
     }
@@ -354,7 +421,7 @@ __global__ __launch_bounds__(NW * 64) void attn_fwd_kernel(AttnArgs a) {
 // Backward for the queries: delta = dO . O per row, then per key tile
 // S -> P (from lse), dP = dO V^T, dS = bf16(P (dP - delta)), dQ += dS K;
 // dQ * scale stored in fp32, delta stored for the key kernel.
-template <int NW, int S>
+template <int NW, int S, bool TOK>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_bwd_dq_kernel(AttnArgs a) {
   constexpr int QB = NW * NB;
   constexpr int PW = 8 / NW;
@@ -383,11 +450,12 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
   float dl = 0.0f;
   {
     const int64_t row = (b * L + qc) * int64_t(D) + 8 * (lane >> 5);
+    const int64_t orow = (TOK ? tok_off(a, b, qc) : (b * L + qc) * int64_t(D)) + 8 * (lane >> 5);
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       qf[j] = __builtin_bit_cast(bf16x8a, *reinterpret_cast<const u32x4a*>(a.Q + row + 16 * j));
-      df[j] = __builtin_bit_cast(bf16x8a, *reinterpret_cast<const u32x4a*>(a.dO + row + 16 * j));
-      const bf16x8a ov = __builtin_bit_cast(bf16x8a, *reinterpret_cast<const u32x4a*>(a.O + row + 16 * j));
+      df[j] = __builtin_bit_cast(bf16x8a, *reinterpret_cast<const u32x4a*>(a.dO + orow + 16 * j));
+      const bf16x8a ov = __builtin_bit_cast(bf16x8a, *reinterpret_cast<const u32x4a*>(a.O + orow + 16 * j));
 #pragma unroll
       for (int i = 0; i < 8; ++i) dl += float(df[j][i]) * float(ov[i]);
     }
@@ -447,7 +515,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
   }
   if (!active) return;
   if (lane < 32) a.delta[b * L + qi] = dl;
-  store_f32_rows(a.dQ + (b * L + qi) * int64_t(D), dq, a.scale, lane);
+  if constexpr (TOK) store_bf16_row<true>(a.dQ_tok + tok_off(a, b, qi), dq, a.scale, a.cs, qi, lane);
+  else store_f32_rows(a.dQ + (b * L + qi) * int64_t(D), dq, a.scale, lane);
 }
 
 // Backward for the keys and values of one query head: one workgroup of NW
@@ -459,7 +528,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 // 1 KB slot of the stage (lanes 0-7 lse, 8-15 delta, the rest repeat them).
 // To hold two workgroups of 256 registers per lane on a SIMD, the last NPARK
 // of the wave's V fragments are kept in LDS and read back for each tile.
-template <int NW, int S>
+template <int NW, int S, bool TOK>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_bwd_dkv_kernel(AttnArgs a) {
   constexpr int KB = NW * NB;
   constexpr int PW = 8 / NW;
@@ -482,12 +551,17 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
   const int my_first = active ? k0 / NB : n_tiles;
   const float c = a.scale * LOG2E;
   const uint16_t* Qb = a.Q + b * int64_t(L) * D;
-  const uint16_t* dOb = a.dO + b * int64_t(L) * D;
+  // dO tile t starts at dOb + t NB ldo (token-major rows: a stride of heads D)
+  const int ldo = TOK ? a.heads * D : D;
+  const uint16_t* dOb = a.dO + (TOK ? tok_off(a, b, 0) : b * int64_t(L) * D);
   // row terms: lane (l % 16) copies 4 floats of lse (l % 16 < 8) or delta
   const float* rt_src = ((lane & 15) < 8 ? a.lse : a.delta) + b * L + 4 * (lane & 7);
-  uint32_t ro[PW];
+  uint32_t ro[PW], rod[PW];
 #pragma unroll
-  for (int q = 0; q < PW; ++q) ro[q] = row_off(wave * PW + q, lane);
+  for (int q = 0; q < PW; ++q) {
+    ro[q] = row_off(wave * PW + q, lane);
+    rod[q] = row_off(wave * PW + q, lane, ldo);
+  }
   bf16x8a kf[8], vf[8 - NPARK];
   u32x4a* park = smem + S * STAGE + wave * NPARK * 64;
   {
@@ -509,7 +583,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
       const int t = first + i;
       u32x4a* st = smem + (i % S) * STAGE;
       copy_tile<PW>(Qb + int64_t(t) * NB * D, ro, st, wave);
-      copy_tile<PW>(dOb + int64_t(t) * NB * D, ro, st + TILE16, wave);
+      copy_tile<PW>(dOb + int64_t(t) * NB * ldo, rod, st + TILE16, wave);
       if (wave == 0) copy16(rt_src + t * NB, 0, st + 2 * TILE16);
     }
   for (int i = 0; i < nt; ++i) {
@@ -520,7 +594,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
       const int u = i + S - 1, t = first + u;
       u32x4a* st = smem + (u % S) * STAGE;
       copy_tile<PW>(Qb + int64_t(t) * NB * D, ro, st, wave);
-      copy_tile<PW>(dOb + int64_t(t) * NB * D, ro, st + TILE16, wave);
+      copy_tile<PW>(dOb + int64_t(t) * NB * ldo, rod, st + TILE16, wave);
       if (wave == 0) copy16(rt_src + t * NB, 0, st + 2 * TILE16);
     }
     const int t = first + i;
@@ -579,6 +653,12 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
     }
   }
   if (!active) return;
+  if (TOK && a.kv_batch == a.batch) {
+    const int64_t o = tok_off(a, b, kj);
+    store_bf16_row<true>(a.dK_tok + o, dk, a.scale, a.cs, kj, lane);
+    store_bf16_row<false>(a.dV_tok + o, dv, 1.0f, a.cs, kj, lane);
+    return;
+  }
   store_f32_rows(a.dK + (b * L + kj) * int64_t(D), dk, a.scale, lane);
   store_f32_rows(a.dV + (b * L + kj) * int64_t(D), dv, 1.0f, lane);
 }
@@ -589,12 +669,23 @@ constexpr int DQ_NW = 4, DQ_S = 2;
 constexpr int DKV_NW = 8, DKV_S = 2;
 }  // namespace
 
+static void set_tok(AttnArgs& a, const AttnLaunch& q) {
+  a.n_seq = q.tok_seqs > 0 ? q.tok_seqs : 1;
+  a.heads = int(q.batch / a.n_seq);
+  a.grp = q.group > 0 ? q.group : 1;
+  a.cs = q.cs;
+  a.dQ_tok = q.dQ_tok; a.dK_tok = q.dK_tok; a.dV_tok = q.dV_tok;
+}
+
 hipError_t launch_attn_fwd(const AttnLaunch& q, hipStream_t st) {
   AttnArgs a{};
   a.batch = q.batch; a.kv_batch = q.kv_batch; a.L = q.L; a.scale = q.scale;
   a.Q = q.Q; a.K = q.K; a.V = q.V; a.O_out = q.O_out; a.lse = q.lse;
+  set_tok(a, q);
   const int64_t nblk = (q.L + FWD_NW * NB - 1) / (FWD_NW * NB);
-  hipLaunchKernelGGL((attn_fwd_kernel<FWD_NW, FWD_S>), dim3(unsigned(nblk * q.batch)), dim3(FWD_NW * 64), 0, st, a);
+  const dim3 grid(unsigned(nblk * q.batch));
+  if (q.tok_seqs > 0) hipLaunchKernelGGL((attn_fwd_kernel<FWD_NW, FWD_S, true>), grid, dim3(FWD_NW * 64), 0, st, a);
+  else hipLaunchKernelGGL((attn_fwd_kernel<FWD_NW, FWD_S, false>), grid, dim3(FWD_NW * 64), 0, st, a);
   return hipGetLastError();
 }
 
@@ -603,13 +694,18 @@ hipError_t launch_attn_bwd(const AttnLaunch& q, hipStream_t st) {
   a.batch = q.batch; a.kv_batch = q.kv_batch; a.L = q.L; a.scale = q.scale;
   a.Q = q.Q; a.K = q.K; a.V = q.V; a.O = q.O; a.dO = q.dO;
   a.lse = q.lse; a.delta = q.delta; a.dQ = q.dQ; a.dK = q.dK; a.dV = q.dV;
+  set_tok(a, q);
+  const bool tok = q.tok_seqs > 0;
   const int64_t nq = (q.L + DQ_NW * NB - 1) / (DQ_NW * NB);
-  hipLaunchKernelGGL((attn_bwd_dq_kernel<DQ_NW, DQ_S>), dim3(unsigned(nq * q.batch)), dim3(DQ_NW * 64), 0, st, a);
+  const dim3 gq(unsigned(nq * q.batch));
+  if (tok) hipLaunchKernelGGL((attn_bwd_dq_kernel<DQ_NW, DQ_S, true>), gq, dim3(DQ_NW * 64), 0, st, a);
+  else hipLaunchKernelGGL((attn_bwd_dq_kernel<DQ_NW, DQ_S, false>), gq, dim3(DQ_NW * 64), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t nk = (q.L + DKV_NW * NB - 1) / (DKV_NW * NB);
-  hipLaunchKernelGGL((attn_bwd_dkv_kernel<DKV_NW, DKV_S>), dim3(unsigned(nk * q.batch)), dim3(DKV_NW * 64), 0, st,
-                     a);
+  const dim3 gk(unsigned(nk * q.batch));
+  if (tok) hipLaunchKernelGGL((attn_bwd_dkv_kernel<DKV_NW, DKV_S, true>), gk, dim3(DKV_NW * 64), 0, st, a);
+  else hipLaunchKernelGGL((attn_bwd_dkv_kernel<DKV_NW, DKV_S, false>), gk, dim3(DKV_NW * 64), 0, st, a);
   return hipGetLastError();
 }
 

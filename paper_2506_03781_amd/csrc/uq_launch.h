@@ -142,6 +142,10 @@ struct AttnLaunch {
   float scale;
   const uint16_t* Q; const uint16_t* K; const uint16_t* V; const uint16_t* O; const uint16_t* dO;
   uint16_t* O_out; float* lse; float* delta; float* dQ; float* dK; float* dV;
+  // token-major O / dO / gradients when tok_seqs > 0 (see uniquan_attn_fwd)
+  int tok_seqs, group;
+  const float* cs;
+  uint16_t* dQ_tok; uint16_t* dK_tok; uint16_t* dV_tok;
 };
 hipError_t launch_attn_fwd(const AttnLaunch& p, hipStream_t st);
 hipError_t launch_attn_bwd(const AttnLaunch& p, hipStream_t st);

@@ -78,8 +78,9 @@ _SIGS = {
     "uniquan_transpose_bf16_batched": ([_i64, _i64, _i64, _vp, _vp, _vp], _i32),
     "uniquan_block_loss_ws": ([], ctypes.c_size_t),
     "uniquan_block_loss": ([_i64, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp, _vp], _i32),
-    "uniquan_attn_fwd": ([_i64, _i64, _i32, _i32, _vp, _vp, _vp, _f32, _vp, _vp, _vp], _i32),
-    "uniquan_attn_bwd": ([_i64, _i64, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _f32, _vp, _vp, _vp, _vp, _vp], _i32),
+    "uniquan_attn_fwd": ([_i64, _i64, _i32, _i32, _vp, _vp, _vp, _f32, _vp, _vp, _i32, _i32, _vp], _i32),
+    "uniquan_attn_bwd": ([_i64, _i64, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _f32, _vp, _vp, _vp, _vp, _i32, _i32,
+                          _vp, _vp], _i32),
     "uniquan_probe_mfma_flops": ([_i32], ctypes.c_double),
     "uniquan_probe_stream": ([_i32, _i64, _vp, _vp, _vp, _i32, _vp], _i32),
     "uniquan_probe_mfma": ([_i32, _vp, _vp], _i32),
@@ -523,21 +524,28 @@ def uniquan_softmax_causal_bwd(rows, L, dP, P, dS, stream=None):
                                             _stream(stream)))
 
 
-def uniquan_attn_fwd(batch, kv_batch, L, d, Q, K, V, scale, O, row_lse, stream=None):
-    """Causal attention forward with on-chip score tiles (see the header)."""
+def uniquan_attn_fwd(batch, kv_batch, L, d, Q, K, V, scale, O, row_lse, tok_seqs=0, group=1, stream=None):
+    """Causal attention forward with on-chip score tiles (see the header); tok_seqs > 0 writes O
+    token-major."""
     nq, nk = batch * L * d, kv_batch * L * d
     _check(lib().uniquan_attn_fwd(batch, kv_batch, L, d, _p(Q, nq, _B, "Q"), _p(K, nk, _B, "K"), _p(V, nk, _B, "V"),
                                   float(scale), _p(O, nq, _B, "O"), _p(row_lse, batch * L, _F, "row_lse"),
-                                  _stream(stream)))
+                                  int(tok_seqs), int(group), _stream(stream)))
 
 
-def uniquan_attn_bwd(batch, kv_batch, L, d, Q, K, V, O, dO, row_lse, scale, delta, dQ, dK, dV, stream=None):
-    """Causal attention backward: dQ and the per-query-head dK, dV (fp32), and the row terms delta."""
+def uniquan_attn_bwd(batch, kv_batch, L, d, Q, K, V, O, dO, row_lse, scale, delta, dQ, dK, dV, tok_seqs=0, group=1,
+                     cs=None, stream=None):
+    """Causal attention backward: dQ and dK, dV, and the row terms delta.  tok_seqs = 0: fp32 head-major
+    gradients per query head; tok_seqs > 0: O, dO token-major, dQ token-major bf16 (inverse-rotated, cs from
+    uniquan_rope_table), dK, dV token-major bf16 when kv_batch == batch, else fp32 per-query-head partials."""
     nq, nk, nr = batch * L * d, kv_batch * L * d, batch * L
+    tq = _B if tok_seqs else _F
+    tkv = _B if tok_seqs and kv_batch == batch else _F
     _check(lib().uniquan_attn_bwd(batch, kv_batch, L, d, _p(Q, nq, _B, "Q"), _p(K, nk, _B, "K"), _p(V, nk, _B, "V"),
                                   _p(O, nq, _B, "O"), _p(dO, nq, _B, "dO"), _p(row_lse, nr, _F, "row_lse"), float(scale),
-                                  _p(delta, nr, _F, "delta"), _p(dQ, nq, _F, "dQ"), _p(dK, nq, _F, "dK"),
-                                  _p(dV, nq, _F, "dV"), _stream(stream)))
+                                  _p(delta, nr, _F, "delta"), _p(dQ, nq, tq, "dQ"), _p(dK, nq, tkv, "dK"),
+                                  _p(dV, nq, tkv, "dV"), int(tok_seqs), int(group),
+                                  _p(cs, L * d, _F, "cs") if tok_seqs else None, _stream(stream)))
 
 
 def uniquan_transpose_bf16_batched(batch, R, C, x, out, stream=None):

@@ -107,3 +107,63 @@ def test_attention_fused(L, batch, kv_batch, sharp):
         check(got["dQ"][b], dS @ Kb * sc, sens @ np.abs(Kb) * sc, f"dQ[{b}]")
         check(got["dK"][b], dS.T @ Q[b] * sc, sens.T @ np.abs(Q[b]) * sc, f"dK[{b}]")
         check(got["dV"][b], P.T @ dO[b], np.abs(P).T @ np.abs(dO[b]), f"dV[{b}]")
+
+
+@pytest.mark.parametrize("n_seq,H,Hkv,L", [(2, 4, 4, 256), (2, 8, 2, 128), (1, 2, 2, 96)])
+def test_attention_token_major_io(n_seq, H, Hkv, L):
+    """tok_seqs > 0 reads O and dO token-major and writes dQ (and dK, dV with
+    one query head per key/value head) token-major bf16 after the inverse
+    rotation: bit for bit the head-major kernels followed by the stand-alone
+    split of dO and merges of O and the gradients (grouped slot order with
+    2 key/value heads for 8 query heads)."""
+    grp = H // Hkv
+    T = n_seq * L
+    B, Bkv = H * n_seq, Hkv * n_seq
+    rs = np.random.default_rng(T + H + Hkv)
+    sc = 1.0 / np.sqrt(d)
+    Q = dev(bfr(rs.standard_normal((B, L, d)) * 2.0))
+    K = dev(bfr(rs.standard_normal((Bkv, L, d)) * 2.0))
+    V = dev(bfr(rs.standard_normal((Bkv, L, d))))
+    dO_tok = dev(bfr(rs.standard_normal((T, H * d))))
+    cs = torch.empty(L, d // 2, 2, device="cuda")
+    uq.uniquan_rope_table(L, d, cs)
+    # head-major reference path
+    dOh = torch.empty(B, L, d, dtype=torch.bfloat16, device="cuda")
+    uq.uniquan_rope_split(T, H, d, L, dO_tok, dOh, rotate=False, group=grp)
+    Oh = torch.empty(B, L, d, dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty(B, L, device="cuda")
+    uq.uniquan_attn_fwd(B, Bkv, L, d, Q, K, V, sc, Oh, lse)
+    O_ref = torch.empty(T, H * d, dtype=torch.bfloat16, device="cuda")
+    uq.uniquan_rope_merge(T, H, d, L, Oh, O_ref, rotate=False, group=grp)
+    delta = torch.empty(B, L, device="cuda")
+    f = lambda: torch.empty(B, L, d, device="cuda")
+    dQr, dKp, dVp = f(), f(), f()
+    uq.uniquan_attn_bwd(B, Bkv, L, d, Q, K, V, Oh, dOh, lse, sc, delta, dQr, dKp, dVp)
+    tokb = lambda n: torch.empty(T, n * d, dtype=torch.bfloat16, device="cuda")
+    dQ_ref, dK_ref, dV_ref = tokb(H), tokb(Hkv), tokb(Hkv)
+    uq.uniquan_rope_merge(T, H, d, L, dQr, dQ_ref, rotate=True, group=grp)
+    uq.uniquan_rope_merge(T, Hkv, d, L, dKp, dK_ref, rotate=True, nsum=grp)
+    uq.uniquan_rope_merge(T, Hkv, d, L, dVp, dV_ref, rotate=False, nsum=grp)
+    # token-major path
+    O_tok = tokb(H)
+    lse2, delta2 = torch.empty(B, L, device="cuda"), torch.empty(B, L, device="cuda")
+    uq.uniquan_attn_fwd(B, Bkv, L, d, Q, K, V, sc, O_tok, lse2, tok_seqs=n_seq, group=grp)
+    dQ_tok = tokb(H)
+    if Hkv == H:
+        dK_tok, dV_tok = tokb(H), tokb(H)
+    else:
+        dK_tok, dV_tok = f(), f()
+    uq.uniquan_attn_bwd(B, Bkv, L, d, Q, K, V, O_tok, dO_tok, lse2, sc, delta2, dQ_tok, dK_tok, dV_tok,
+                        tok_seqs=n_seq, group=grp, cs=cs)
+    if Hkv != H:
+        dKp2, dVp2 = dK_tok, dV_tok
+        dK_tok, dV_tok = tokb(Hkv), tokb(Hkv)
+        uq.uniquan_rope_merge(T, Hkv, d, L, dKp2, dK_tok, rotate=True, nsum=grp)
+        uq.uniquan_rope_merge(T, Hkv, d, L, dVp2, dV_tok, rotate=False, nsum=grp)
+    torch.cuda.synchronize()
+    bits = lambda t: t.view(torch.int16)
+    assert torch.equal(lse2, lse) and torch.equal(delta2, delta)
+    assert torch.equal(bits(O_tok), bits(O_ref)), "O"
+    assert torch.equal(bits(dQ_tok), bits(dQ_ref)), "dQ"
+    assert torch.equal(bits(dK_tok), bits(dK_ref)), "dK"
+    assert torch.equal(bits(dV_tok), bits(dV_ref)), "dV"
