@@ -410,6 +410,20 @@ uq_status uniquan_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* A,
                        int out_dtype, float scale, void* stream);
 
 /*
+ * uniquan_gemm_swiglu -- the MLP module's gate and up products with the SiLU
+ * product (Algorithm 1's forward through the SiLU-gated MLP) in one product:
+ *     G = X W_g^T, U = X W_u^T   (X [T x K], W_g, W_u [I x K] bf16, fp32
+ *                                 accumulation, G and U stored bf16 [T x I]),
+ *     H = silu(G) U              (from the stored bf16 G and U, as
+ *                                 uniquan_silu_mul_fwd computes it),
+ * bit for bit uniquan_gemm_nt twice (bf16 out) and uniquan_silu_mul_fwd.
+ * I and K multiples of 32; X, W 16-byte and G, U, H 8-byte aligned.
+ */
+uq_status uniquan_gemm_swiglu(int64_t T, int64_t I, int64_t K, const uint16_t* X,
+                              const uint16_t* Wg, const uint16_t* Wu, uint16_t* G,
+                              uint16_t* U, uint16_t* H, void* stream);
+
+/*
  * uniquan_silu_mul_fwd -- H[i] = silu(G[i]) * U[i], i < n (bf16 in and out,
  * fp32 arithmetic, silu(x) = x / (1 + exp(-x))); n a multiple of 8,
  * pointers 16-byte aligned.

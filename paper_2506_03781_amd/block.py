@@ -213,9 +213,7 @@ class DecoderBlock:
                             tok_seqs=self.n_seq, group=grp)
         uq.uniquan_gemm_nt(T, C, C, self.O, W["o"], self.A32)
         uq.uniquan_add_rmsnorm(T, C, X, self.A32, self.g2, self.R, self.Z2, self.r2)
-        uq.uniquan_gemm_nt(T, I, C, self.Z2, W["g"], self.Gm)
-        uq.uniquan_gemm_nt(T, I, C, self.Z2, W["u"], self.Um)
-        uq.uniquan_silu_mul_fwd(self.Gm, self.Um, self.Hm)
+        uq.uniquan_gemm_swiglu(T, I, C, self.Z2, W["g"], W["u"], self.Gm, self.Um, self.Hm)
         uq.uniquan_gemm_nt(T, C, I, self.Hm, W["d"], self.M32)
 
     def _project_heads(self, Wm, n_heads, out, group, rotate, tmp):

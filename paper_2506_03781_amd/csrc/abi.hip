@@ -415,6 +415,21 @@ uq_status uniquan_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* A, int a
   return hip_status(fn, uq::launch_gemm(g, static_cast<hipStream_t>(stream)));
 }
 
+uq_status uniquan_gemm_swiglu(int64_t T, int64_t I, int64_t K, const uint16_t* X, const uint16_t* Wg,
+                              const uint16_t* Wu, uint16_t* G, uint16_t* U, uint16_t* H, void* stream) {
+  const char* fn = "uniquan_gemm_swiglu";
+  if (T < 1 || I < 1 || K < 1) return fail(UQ_EINVAL, "%s: T, I, K must be >= 1", fn);
+  if (I % 32 != 0 || K % 32 != 0)
+    return fail(UQ_EINVAL, "%s: I=%lld and K=%lld must be multiples of 32", fn, (long long)I, (long long)K);
+  if (2 * I >= (int64_t(1) << 26) || K >= (int64_t(1) << 31) || T >= (int64_t(1) << 31) ||
+      T * K >= (int64_t(1) << 40) || I * K >= (int64_t(1) << 40) || T * I >= (int64_t(1) << 40))
+    return fail(UQ_EUNSUPPORTED, "%s: shape too large", fn);
+  REQ_PTR(X, 16); REQ_PTR(Wg, 16); REQ_PTR(Wu, 16); REQ_PTR(G, 8); REQ_PTR(U, 8); REQ_PTR(H, 8);
+  uq::GemmLaunch g{X, Wg, T, 2 * I, K, uq::EPI_SWIGLU, nullptr, G, nullptr, 1.0f};
+  g.swiglu = uq::SwigluParams{Wu, U, H, I};
+  return hip_status(fn, uq::launch_gemm(g, static_cast<hipStream_t>(stream)));
+}
+
 uq_status uniquan_silu_mul_fwd(int64_t n, const uint16_t* G, const uint16_t* U, uint16_t* H, void* stream) {
   const char* fn = "uniquan_silu_mul_fwd";
   if (n < 8 || n % 8 != 0) return fail(UQ_EINVAL, "%s: n=%lld must be a positive multiple of 8", fn, (long long)n);

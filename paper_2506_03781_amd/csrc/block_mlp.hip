@@ -24,7 +24,6 @@ __device__ __forceinline__ uint32_t pack2(float lo, float hi) {
   const f32x2_t f = {lo, hi};
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2_t));
 }
-__device__ __forceinline__ float sigmoid(float x) { return 1.0f / (1.0f + expf(-x)); }
 
 __device__ __forceinline__ void unpack8(const uint4 v, float (&f)[8]) {
   const uint32_t w[4] = {v.x, v.y, v.z, v.w};
@@ -48,7 +47,7 @@ __global__ __launch_bounds__(256) void silu_mul_fwd_kernel(int64_t n8, const uin
   unpack8(G[i], g);
   unpack8(U[i], u);
 #pragma unroll
-  for (int j = 0; j < 8; ++j) h[j] = g[j] * sigmoid(g[j]) * u[j];
+  for (int j = 0; j < 8; ++j) h[j] = silu_mul(g[j], u[j]);
   H[i] = pack8(h);
 }
 
@@ -63,7 +62,7 @@ __global__ __launch_bounds__(256) void silu_mul_bwd_kernel(int64_t n8, const uin
   unpack8(U[i], u);
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
-    const float s = sigmoid(g[j]);
+    const float s = 1.0f / (1.0f + expf(-g[j]));
     const float silu = g[j] * s;
     const float dsilu = s * (1.0f + g[j] * (1.0f - s));
     dg[j] = dh[j] * u[j] * dsilu;

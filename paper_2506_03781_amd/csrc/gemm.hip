@@ -60,6 +60,7 @@ struct GemmArgs {
   // the row tile's start (A zero below the diagonal)
   int causal;
   HeadsParams heads;
+  SwigluParams swiglu;
 };
 
 // Operands and output of batch blockIdx.y.
@@ -299,6 +300,34 @@ __device__ __forceinline__ void epilogue(const GemmArgs& p, f32x16 (&acc)[FM][FN
     __builtin_amdgcn_wave_barrier();
     const int64_t row_base = m0 + wm * WM + i * 32;
     const int64_t col_base = n0 + wn * WN;
+    if constexpr (EPI == EPI_SWIGLU) {
+      static_assert(WN == 64, "the SiLU product needs 64-column wave tiles (G and U halves)");
+      // strip columns 0..31: G, 32..63: U of rows I0 .. I0 + 31 of W
+      const int64_t I = p.swiglu.I, i0 = n0 / 2 + wn * 32;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int item = lane + 64 * k, rr = item >> 3, cq = (item & 7) * 4;
+        const int64_t m = row_base + rr;
+        if (m >= p.M || i0 + cq >= I) continue;
+        const float4 g4 = *reinterpret_cast<const float4*>(&strip[rr * 64 + cq]);
+        const float4 u4 = *reinterpret_cast<const float4*>(&strip[rr * 64 + 32 + cq]);
+        const uint32_t g01 = pack_bf16x2(p.scale * g4.x, p.scale * g4.y), g23 = pack_bf16x2(p.scale * g4.z, p.scale * g4.w);
+        const uint32_t u01 = pack_bf16x2(p.scale * u4.x, p.scale * u4.y), u23 = pack_bf16x2(p.scale * u4.z, p.scale * u4.w);
+        const float gf[4] = {__uint_as_float(g01 << 16), __uint_as_float(g01 & 0xFFFF0000u),
+                             __uint_as_float(g23 << 16), __uint_as_float(g23 & 0xFFFF0000u)};
+        const float uf[4] = {__uint_as_float(u01 << 16), __uint_as_float(u01 & 0xFFFF0000u),
+                             __uint_as_float(u23 << 16), __uint_as_float(u23 & 0xFFFF0000u)};
+        const int64_t o = m * I + i0 + cq;
+        *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.out) + o) = make_uint2(g01, g23);
+        *reinterpret_cast<uint2*>(p.swiglu.U + o) = make_uint2(u01, u23);
+        *reinterpret_cast<uint2*>(p.swiglu.H + o) =
+            make_uint2(pack_bf16x2(silu_mul(gf[0], uf[0]), silu_mul(gf[1], uf[1])),
+                       pack_bf16x2(silu_mul(gf[2], uf[2]), silu_mul(gf[3], uf[3])));
+      }
+      __builtin_amdgcn_s_waitcnt(0xC07F);  // strip reads done before the next strip overwrites it
+      __builtin_amdgcn_wave_barrier();
+      continue;
+    }
     if constexpr (EPI == EPI_HEADS || EPI == EPI_HEADS_ROT) {
       static_assert(WN == 128, "the head split needs 128-column wave tiles");
       if (col_base < p.N) heads_strip<EPI == EPI_HEADS_ROT>(p, strip, row_base, col_base, lane);
@@ -804,6 +833,13 @@ __global__ __launch_bounds__(512) void gemm_pp_kernel(GemmArgs p) {
       const int64_t col = min((a ? m0 : n0) + 8 * c, ext - 8);
       src[j] = (a ? p.A : p.B) + int64_t(kr) * ext + col;
       kstep[j] = BK * ext;
+    } else if (EPI == EPI_SWIGLU && !a) {
+      // interleaved columns: 32-row blocks of W_g and W_u rows n0 / 2 + 32 (q / 2) ..
+      const int row = b * RPB + lane / CPR;
+      const int kc = pp_chunk<BK>(row, lane % CPR);
+      const int64_t gr = min(n0 / 2 + 32 * (row >> 6) + (row & 31), p.swiglu.I - 1);
+      src[j] = ((row >> 5) & 1 ? p.swiglu.Wu : p.B) + gr * K + kc * 8;
+      kstep[j] = BK;
     } else {
       const int row = b * RPB + lane / CPR;
       const int kc = pp_chunk<BK>(row, lane % CPR);
@@ -1063,7 +1099,25 @@ static hipError_t launch_gemm_heads(const GemmLaunch& q, hipStream_t st) {
   return hipGetLastError();
 }
 
+// Gate and up products with the SiLU product (EPI_SWIGLU): 256 x 256 tiles
+// of the interleaved columns (128 rows of W each) on the ping-pong kernel
+// with the 2 x 4 wave grid.  K % 32 == 0, I % 32 == 0.
+static hipError_t launch_gemm_swiglu(const GemmLaunch& q, hipStream_t st) {
+  GemmArgs a;
+  a.A = q.A; a.B = q.B; a.M = q.M; a.N = 2 * q.swiglu.I; a.K = q.K;
+  a.Yt = nullptr; a.out = q.out; a.partials = nullptr; a.scale = q.scale;
+  a.bsa = a.bsb = a.bso = 0;
+  a.causal = 0;
+  a.swiglu = q.swiglu;
+  a.tiles_m = int((q.M + 255) / 256);
+  a.tiles_n = int((a.N + 255) / 256);
+  hipLaunchKernelGGL((gemm_pp_kernel<256, 256, EPI_SWIGLU>), dim3(unsigned(a.tiles_m * a.tiles_n)), dim3(512), 0, st,
+                     a);
+  return hipGetLastError();
+}
+
 hipError_t launch_gemm(const GemmLaunch& q, hipStream_t st) {
+  if (q.epi == EPI_SWIGLU) return launch_gemm_swiglu(q, st);
   if (q.epi == EPI_HEADS || q.epi == EPI_HEADS_ROT) return launch_gemm_heads(q, st);
   if (q.ta || q.tb) return launch_gemm_kslow(q, st);
   switch (pick(q.M, q.N, q.batch)) {

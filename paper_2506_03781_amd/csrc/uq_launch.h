@@ -104,6 +104,23 @@ enum GemmEpi : int {
   EPI_LOSS_RES = 4,   // EPI_LOSS without a target (A holds What - W); chosen when Yt is NULL
   EPI_HEADS = 5,      // out bf16 head-major [H, M, 128] = scale * acc (column block h to head slot h)
   EPI_HEADS_ROT = 6,  // EPI_HEADS with the rotary rotation of each head's pairs (i, i + 64)
+  EPI_SWIGLU = 7,     // gate and up products in one: G, U, H = silu(G) U (bf16), see SwigluParams
+};
+
+// silu(g) u of the SiLU-gated MLP on bf16-rounded g and u (fp32 arithmetic:
+// (g sigma(g)) u, sigma(x) = 1 / (1 + exp(-x))); one definition for the
+// stand-alone kernel and the product's epilogue.
+__device__ __forceinline__ float silu_mul(float g, float u) { return g * (1.0f / (1.0f + expf(-g))) * u; }
+
+// EPI_SWIGLU: B is W_g and B2 W_u ([I x K] each); the product's columns
+// interleave 32-row blocks of the two (block 2q of a 256-column tile: W_g
+// rows 128 n + 32 q .., block 2q + 1: the same rows of W_u), so a 64-column
+// wave tile holds G and U of the same 32 rows of W; out = G, U, H [M x I].
+struct SwigluParams {
+  const uint16_t* Wu;
+  uint16_t* U;
+  uint16_t* H;
+  int64_t I;
 };
 
 // Head-split epilogue (EPI_HEADS*): position of row m is m % L; cos and sin
@@ -133,6 +150,7 @@ struct GemmLaunch {
   // [K x M] (ta = 1), B as [K x N] (tb = 1)
   int ta, tb;
   HeadsParams heads;   // EPI_HEADS*
+  SwigluParams swiglu; // EPI_SWIGLU
 };
 
 // Causal attention with the score tiles on chip (attn_fused.hip), d = 128.

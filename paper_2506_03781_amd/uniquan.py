@@ -64,6 +64,7 @@ _SIGS = {
     "uniquan_gemm_nt": ([_i64, _i64, _i64, _vp, _vp, _vp, _i32, _f32, _vp], _i32),
     "uniquan_gemm": ([_i64, _i64, _i64, _vp, _i32, _vp, _i32, _vp, _i32, _f32, _vp], _i32),
     "uniquan_rope_table": ([_i32, _i32, _vp, _vp], _i32),
+    "uniquan_gemm_swiglu": ([_i64, _i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp], _i32),
     "uniquan_gemm_heads": ([_i64, _i32, _i64, _vp, _vp, _i32, _i32, _i32, _vp, _vp, _vp], _i32),
     "uniquan_silu_mul_fwd": ([_i64, _vp, _vp, _vp, _vp], _i32),
     "uniquan_silu_mul_bwd": ([_i64, _vp, _vp, _vp, _vp, _vp, _vp], _i32),
@@ -461,6 +462,13 @@ def uniquan_gemm_heads(T, H, K, A, W, L, out, group=1, rotate=True, cs=None, str
     _check(lib().uniquan_gemm_heads(T, H, K, _p(A, T * K, _B, "A"), _p(W, N * K, _B, "W"), int(L), int(group),
                                     int(bool(rotate)), _p(cs, L * 128, _F, "cs") if rotate else None,
                                     _p(out, T * N, _B, "out"), _stream(stream)))
+
+
+def uniquan_gemm_swiglu(T, I, K, X, Wg, Wu, G, U, H, stream=None):
+    """G = X Wg^T, U = X Wu^T (bf16 [T, I]) and H = silu(G) U in one product."""
+    n = T * I
+    _check(lib().uniquan_gemm_swiglu(T, I, K, _p(X, T * K, _B, "X"), _p(Wg, I * K, _B, "Wg"), _p(Wu, I * K, _B, "Wu"),
+                                     _p(G, n, _B, "G"), _p(U, n, _B, "U"), _p(H, n, _B, "H"), _stream(stream)))
 
 
 def uniquan_silu_mul_fwd(G, U, H, stream=None):

@@ -125,6 +125,28 @@ def test_gemm_heads_matches_product_then_split(T, H, K, L, group, rotate):
     assert np.all(np.abs(c[..., 1] - np.sin(ang)) <= 1e-6 * (1 + np.abs(ang)))
 
 
+@pytest.mark.parametrize("T,I,K", [(264, 352, 96), (600, 1056, 64), (8192, 11008, 128)])
+def test_gemm_swiglu_matches_products_then_silu(T, I, K):
+    """The gate and up products with the SiLU product in one (interleaved
+    32-row blocks of W_g and W_u) equal two uniquan_gemm_nt products (bf16)
+    followed by uniquan_silu_mul_fwd, bit for bit: ragged rows and columns
+    (I = 352 is 2 tiles of 128 + 96), and the 7B width."""
+    rs = np.random.default_rng(T + I + K)
+    X = dev(bfr(rs.standard_normal((T, K))), torch.bfloat16)
+    Wg = dev(bfr(rs.standard_normal((I, K)) * 0.2), torch.bfloat16)
+    Wu = dev(bfr(rs.standard_normal((I, K)) * 0.2), torch.bfloat16)
+    e = lambda: torch.full((T, I), float("nan"), device="cuda", dtype=torch.bfloat16)
+    G, U, H = e(), e(), e()
+    uq.uniquan_gemm_swiglu(T, I, K, X, Wg, Wu, G, U, H)
+    G0, U0, H0 = e(), e(), e()
+    uq.uniquan_gemm_nt(T, I, K, X, Wg, G0)
+    uq.uniquan_gemm_nt(T, I, K, X, Wu, U0)
+    uq.uniquan_silu_mul_fwd(G0, U0, H0)
+    torch.cuda.synchronize()
+    bits = lambda t: t.view(torch.int16)
+    assert torch.equal(bits(G), bits(G0)) and torch.equal(bits(U), bits(U0)) and torch.equal(bits(H), bits(H0))
+
+
 @pytest.mark.parametrize("T,C", [(5, 8), (37, 264), (64, 4096)])
 def test_add_rmsnorm(T, C):
     rs = np.random.default_rng(T * C)
