@@ -424,6 +424,23 @@ uq_status uniquan_gemm_swiglu(int64_t T, int64_t I, int64_t K, const uint16_t* X
                               uint16_t* U, uint16_t* H, void* stream);
 
 /*
+ * uniquan_gemm_silu_bwd -- the MLP module's backward through the down
+ * matrix and the SiLU product (Algorithm 1's backpropagation):
+ *     dH = bf16(scale E W_d)   (E [T x K] bf16 K-contiguous, W_d stored as
+ *                               [K x I] (the down matrix, K = C), fp32
+ *                               accumulation; dH is not written),
+ *     dG, dU = the SiLU product's backward at (dH, G, U) (bf16 [T x I], as
+ *                               uniquan_silu_mul_bwd computes it),
+ * bit for bit uniquan_gemm (b_kslow = 1, bf16 out) followed by
+ * uniquan_silu_mul_bwd.  I a multiple of 8, K of 32; E, W_d 16-byte and
+ * G, U, dG, dU 8-byte aligned.
+ */
+uq_status uniquan_gemm_silu_bwd(int64_t T, int64_t I, int64_t K, const uint16_t* E,
+                                const uint16_t* Wd, float scale, const uint16_t* G,
+                                const uint16_t* U, uint16_t* dG, uint16_t* dU,
+                                void* stream);
+
+/*
  * uniquan_silu_mul_fwd -- H[i] = silu(G[i]) * U[i], i < n (bf16 in and out,
  * fp32 arithmetic, silu(x) = x / (1 + exp(-x))); n a multiple of 8,
  * pointers 16-byte aligned.

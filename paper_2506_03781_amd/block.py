@@ -192,7 +192,7 @@ class DecoderBlock:
         # grouped-query: dK, dV contributions per query head (summed per key/value head)
         self.dKp, self.dVp = (e(B, L, d, **f32) for _ in range(2)) if self.grp > 1 else (None, None)
         # MLP activations and their gradients, one row per token
-        self.Gm, self.Um, self.Hm, self.dHm, self.dGm, self.dUm = (e(T, I, **b16) for _ in range(6))
+        self.Gm, self.Um, self.Hm, self.dGm, self.dUm = (e(T, I, **b16) for _ in range(5))
         self.partials = e(uq.uniquan_block_loss_ws(), **f32)
         self.loss = torch.zeros(1, **f32)
         self._rinv_tmp = e(T, **f32)
@@ -275,9 +275,8 @@ class DecoderBlock:
         # stored (both K-slow, K = tokens); input gradients dY W read W as
         # stored (K-slow, K = the matrix's rows).
         uq.uniquan_gemm(C, I, T, self.E, 1, self.Hm, 1, m["d"].G, 2.0)
-        uq.uniquan_gemm(T, I, C, self.E, 0, Wh["d"], 1, self.dHm, 2.0)
+        uq.uniquan_gemm_silu_bwd(T, I, C, self.E, Wh["d"], 2.0, self.Gm, self.Um, self.dGm, self.dUm)
         done("d")
-        uq.uniquan_silu_mul_bwd(self.dHm, self.Gm, self.Um, self.dGm, self.dUm)
         uq.uniquan_gemm(I, C, T, self.dGm, 1, self.Z2, 1, m["g"].G)
         uq.uniquan_gemm(I, C, T, self.dUm, 1, self.Z2, 1, m["u"].G)
         uq.uniquan_gemm(T, C, I, self.dGm, 0, Wh["g"], 1, self.dZa)

@@ -430,6 +430,24 @@ uq_status uniquan_gemm_swiglu(int64_t T, int64_t I, int64_t K, const uint16_t* X
   return hip_status(fn, uq::launch_gemm(g, static_cast<hipStream_t>(stream)));
 }
 
+uq_status uniquan_gemm_silu_bwd(int64_t T, int64_t I, int64_t K, const uint16_t* E, const uint16_t* Wd, float scale,
+                                const uint16_t* G, const uint16_t* U, uint16_t* dG, uint16_t* dU, void* stream) {
+  const char* fn = "uniquan_gemm_silu_bwd";
+  if (T < 1 || I < 1 || K < 1) return fail(UQ_EINVAL, "%s: T, I, K must be >= 1", fn);
+  if (I % 8 != 0 || K % 32 != 0)
+    return fail(UQ_EINVAL, "%s: I=%lld must be a multiple of 8 and K=%lld of 32", fn, (long long)I, (long long)K);
+  if (I >= (int64_t(1) << 26) || K >= (int64_t(1) << 31) || T >= (int64_t(1) << 31) ||
+      T * K >= (int64_t(1) << 40) || I * K >= (int64_t(1) << 40) || T * I >= (int64_t(1) << 40))
+    return fail(UQ_EUNSUPPORTED, "%s: shape too large", fn);
+  REQ_PTR(E, 16); REQ_PTR(Wd, 16); REQ_PTR(G, 8); REQ_PTR(U, 8); REQ_PTR(dG, 8); REQ_PTR(dU, 8);
+  uq::GemmLaunch g{E, Wd, T, I, K, uq::EPI_SWIGLU_BWD, nullptr, dG, nullptr, scale};
+  g.tb = 1;
+  g.swiglu.G_in = G;
+  g.swiglu.U_in = U;
+  g.swiglu.dU = dU;
+  return hip_status(fn, uq::launch_gemm(g, static_cast<hipStream_t>(stream)));
+}
+
 uq_status uniquan_silu_mul_fwd(int64_t n, const uint16_t* G, const uint16_t* U, uint16_t* H, void* stream) {
   const char* fn = "uniquan_silu_mul_fwd";
   if (n < 8 || n % 8 != 0) return fail(UQ_EINVAL, "%s: n=%lld must be a positive multiple of 8", fn, (long long)n);

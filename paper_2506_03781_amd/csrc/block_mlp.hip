@@ -61,13 +61,7 @@ __global__ __launch_bounds__(256) void silu_mul_bwd_kernel(int64_t n8, const uin
   unpack8(G[i], g);
   unpack8(U[i], u);
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const float s = 1.0f / (1.0f + expf(-g[j]));
-    const float silu = g[j] * s;
-    const float dsilu = s * (1.0f + g[j] * (1.0f - s));
-    dg[j] = dh[j] * u[j] * dsilu;
-    du[j] = dh[j] * silu;
-  }
+  for (int j = 0; j < 8; ++j) silu_mul_grad(dh[j], g[j], u[j], dg[j], du[j]);
   dG[i] = pack8(dg);
   dU[i] = pack8(du);
 }

@@ -328,6 +328,47 @@ __device__ __forceinline__ void epilogue(const GemmArgs& p, f32x16 (&acc)[FM][FN
       __builtin_amdgcn_wave_barrier();
       continue;
     }
+    if constexpr (EPI == EPI_SWIGLU_BWD) {
+      // dH = bf16(scale acc) of the strip, then the SiLU product's backward with
+      // G and U of the same elements; the strip's G, U loads are issued first
+      constexpr int IT = 32 * WN / 4 / 64;  // 4-column items per lane
+      uint2 gq[IT], uq4[IT];
+#pragma unroll
+      for (int k = 0; k < IT; ++k) {
+        const int item = lane + 64 * k, rr = item / (WN / 4), cq = (item % (WN / 4)) * 4;
+        const int64_t m = row_base + rr, n = col_base + cq;
+        const bool ok = m < p.M && n < p.N;
+        const int64_t o = ok ? m * p.N + n : 0;
+        gq[k] = *reinterpret_cast<const uint2*>(p.swiglu.G_in + o);
+        uq4[k] = *reinterpret_cast<const uint2*>(p.swiglu.U_in + o);
+      }
+#pragma unroll
+      for (int k = 0; k < IT; ++k) {
+        const int item = lane + 64 * k, rr = item / (WN / 4), cq = (item % (WN / 4)) * 4;
+        const int64_t m = row_base + rr, n = col_base + cq;
+        if (m >= p.M || n >= p.N) continue;
+        const float4 v = *reinterpret_cast<const float4*>(&strip[rr * WN + cq]);
+        const uint32_t h01 = pack_bf16x2(p.scale * v.x, p.scale * v.y), h23 = pack_bf16x2(p.scale * v.z, p.scale * v.w);
+        const uint32_t hw[2] = {h01, h23}, gw[2] = {gq[k].x, gq[k].y}, uw[2] = {uq4[k].x, uq4[k].y};
+        float dg[4], du[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const uint32_t sh = (e & 1) ? 0u : 16u;
+          const uint32_t mk = 0xFFFF0000u;
+          const float dh = __uint_as_float((hw[e >> 1] << sh) & mk);
+          const float g = __uint_as_float((gw[e >> 1] << sh) & mk);
+          const float u = __uint_as_float((uw[e >> 1] << sh) & mk);
+          silu_mul_grad(dh, g, u, dg[e], du[e]);
+        }
+        const int64_t o = m * p.N + n;
+        *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.out) + o) =
+            make_uint2(pack_bf16x2(dg[0], dg[1]), pack_bf16x2(dg[2], dg[3]));
+        *reinterpret_cast<uint2*>(p.swiglu.dU + o) = make_uint2(pack_bf16x2(du[0], du[1]), pack_bf16x2(du[2], du[3]));
+      }
+      __builtin_amdgcn_s_waitcnt(0xC07F);  // strip reads done before the next strip overwrites it
+      __builtin_amdgcn_wave_barrier();
+      continue;
+    }
     if constexpr (EPI == EPI_HEADS || EPI == EPI_HEADS_ROT) {
       static_assert(WN == 128, "the head split needs 128-column wave tiles");
       if (col_base < p.N) heads_strip<EPI == EPI_HEADS_ROT>(p, strip, row_base, col_base, lane);
@@ -1064,11 +1105,18 @@ static hipError_t launch_gemm_kslow(const GemmLaunch& q, hipStream_t st) {
   a.Yt = nullptr; a.out = q.out; a.partials = nullptr; a.scale = q.scale;
   a.bsa = a.bsb = a.bso = 0;
   a.causal = 0;
+  a.swiglu = q.swiglu;
   const bool wide = q.M > 128 && q.N > 128 && tiles<256, 256>(q.M, q.N) >= 256;
   const int BN = wide ? 256 : 128;
   a.tiles_m = int((q.M + 255) / 256);
   a.tiles_n = int((q.N + BN - 1) / BN);
   const bool bf = q.epi == EPI_GRAD_BF16;
+  if (q.epi == EPI_SWIGLU_BWD) {  // input-gradient product dH = E W_d: B K-slow, 256 x 256 tiles
+    a.tiles_n = int((q.N + 255) / 256);
+    hipLaunchKernelGGL((gemm_pp_kernel<256, 256, EPI_SWIGLU_BWD, 2, 32, false, true>),
+                       dim3(unsigned(a.tiles_m * a.tiles_n)), dim3(512), 0, st, a);
+    return hipGetLastError();
+  }
   if (wide) {
     if (bf) launch_kslow<256, 256, EPI_GRAD_BF16>(a, q.ta, q.tb, st);
     else launch_kslow<256, 256, EPI_GRAD_F32>(a, q.ta, q.tb, st);

@@ -105,6 +105,7 @@ enum GemmEpi : int {
   EPI_HEADS = 5,      // out bf16 head-major [H, M, 128] = scale * acc (column block h to head slot h)
   EPI_HEADS_ROT = 6,  // EPI_HEADS with the rotary rotation of each head's pairs (i, i + 64)
   EPI_SWIGLU = 7,     // gate and up products in one: G, U, H = silu(G) U (bf16), see SwigluParams
+  EPI_SWIGLU_BWD = 8, // dH = bf16(scale acc) [M x N], then dG, dU of the SiLU product (SwigluParams)
 };
 
 // silu(g) u of the SiLU-gated MLP on bf16-rounded g and u (fp32 arithmetic:
@@ -112,15 +113,29 @@ enum GemmEpi : int {
 // stand-alone kernel and the product's epilogue.
 __device__ __forceinline__ float silu_mul(float g, float u) { return g * (1.0f / (1.0f + expf(-g))) * u; }
 
+// Its backward on bf16-rounded dh, g, u: dg = (dh u) silu'(g), du = dh silu(g),
+// silu'(x) = sigma(x) (1 + x (1 - sigma(x))).
+__device__ __forceinline__ void silu_mul_grad(float dh, float g, float u, float& dg, float& du) {
+  const float s = 1.0f / (1.0f + expf(-g));
+  const float silu = g * s;
+  const float dsilu = s * (1.0f + g * (1.0f - s));
+  dg = dh * u * dsilu;
+  du = dh * silu;
+}
+
 // EPI_SWIGLU: B is W_g and B2 W_u ([I x K] each); the product's columns
 // interleave 32-row blocks of the two (block 2q of a 256-column tile: W_g
 // rows 128 n + 32 q .., block 2q + 1: the same rows of W_u), so a 64-column
 // wave tile holds G and U of the same 32 rows of W; out = G, U, H [M x I].
+// EPI_SWIGLU_BWD: G, U in (gate, up), out = dG, dU2 = dU [M x N].
 struct SwigluParams {
   const uint16_t* Wu;
   uint16_t* U;
   uint16_t* H;
   int64_t I;
+  const uint16_t* G_in;
+  const uint16_t* U_in;
+  uint16_t* dU;
 };
 
 // Head-split epilogue (EPI_HEADS*): position of row m is m % L; cos and sin

@@ -65,6 +65,7 @@ _SIGS = {
     "uniquan_gemm": ([_i64, _i64, _i64, _vp, _i32, _vp, _i32, _vp, _i32, _f32, _vp], _i32),
     "uniquan_rope_table": ([_i32, _i32, _vp, _vp], _i32),
     "uniquan_gemm_swiglu": ([_i64, _i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp], _i32),
+    "uniquan_gemm_silu_bwd": ([_i64, _i64, _i64, _vp, _vp, _f32, _vp, _vp, _vp, _vp, _vp], _i32),
     "uniquan_gemm_heads": ([_i64, _i32, _i64, _vp, _vp, _i32, _i32, _i32, _vp, _vp, _vp], _i32),
     "uniquan_silu_mul_fwd": ([_i64, _vp, _vp, _vp, _vp], _i32),
     "uniquan_silu_mul_bwd": ([_i64, _vp, _vp, _vp, _vp, _vp, _vp], _i32),
@@ -469,6 +470,14 @@ def uniquan_gemm_swiglu(T, I, K, X, Wg, Wu, G, U, H, stream=None):
     n = T * I
     _check(lib().uniquan_gemm_swiglu(T, I, K, _p(X, T * K, _B, "X"), _p(Wg, I * K, _B, "Wg"), _p(Wu, I * K, _B, "Wu"),
                                      _p(G, n, _B, "G"), _p(U, n, _B, "U"), _p(H, n, _B, "H"), _stream(stream)))
+
+
+def uniquan_gemm_silu_bwd(T, I, K, E, Wd, scale, G, U, dG, dU, stream=None):
+    """dG, dU of the SiLU product at dH = bf16(scale E Wd) (Wd stored [K, I]); dH is not written."""
+    n = T * I
+    _check(lib().uniquan_gemm_silu_bwd(T, I, K, _p(E, T * K, _B, "E"), _p(Wd, K * I, _B, "Wd"), float(scale),
+                                       _p(G, n, _B, "G"), _p(U, n, _B, "U"), _p(dG, n, _B, "dG"), _p(dU, n, _B, "dU"),
+                                       _stream(stream)))
 
 
 def uniquan_silu_mul_fwd(G, U, H, stream=None):

@@ -147,6 +147,27 @@ def test_gemm_swiglu_matches_products_then_silu(T, I, K):
     assert torch.equal(bits(G), bits(G0)) and torch.equal(bits(U), bits(U0)) and torch.equal(bits(H), bits(H0))
 
 
+@pytest.mark.parametrize("T,I,K", [(264, 360, 96), (600, 1056, 64), (8192, 11008, 128)])
+def test_gemm_silu_bwd_matches_product_then_silu_bwd(T, I, K):
+    """dH = 2 E W_d (W_d stored [K, I]) with the SiLU product's backward in the
+    product's store equals uniquan_gemm (bf16 dH) followed by
+    uniquan_silu_mul_bwd, bit for bit (ragged shapes, the 7B width)."""
+    rs = np.random.default_rng(T * 3 + I + K)
+    E = dev(bfr(rs.standard_normal((T, K))), torch.bfloat16)
+    Wd = dev(bfr(rs.standard_normal((K, I)) * 0.2), torch.bfloat16)
+    G = dev(bfr(rs.standard_normal((T, I)) * 2.0), torch.bfloat16)
+    U = dev(bfr(rs.standard_normal((T, I))), torch.bfloat16)
+    e = lambda: torch.full((T, I), float("nan"), device="cuda", dtype=torch.bfloat16)
+    dG, dU = e(), e()
+    uq.uniquan_gemm_silu_bwd(T, I, K, E, Wd, 2.0, G, U, dG, dU)
+    dH0, dG0, dU0 = e(), e(), e()
+    uq.uniquan_gemm(T, I, K, E, 0, Wd, 1, dH0, 2.0)
+    uq.uniquan_silu_mul_bwd(dH0, G, U, dG0, dU0)
+    torch.cuda.synchronize()
+    bits = lambda t: t.view(torch.int16)
+    assert torch.equal(bits(dG), bits(dG0)) and torch.equal(bits(dU), bits(dU0))
+
+
 @pytest.mark.parametrize("T,C", [(5, 8), (37, 264), (64, 4096)])
 def test_add_rmsnorm(T, C):
     rs = np.random.default_rng(T * C)
