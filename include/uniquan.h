@@ -633,6 +633,25 @@ uq_status uniquan_transpose_bf16_batched(int64_t batch, int64_t R, int64_t C,
  * (partials_len gives its size).
  */
 size_t uniquan_block_loss_ws(void);
+
+/*
+ * uniquan_gemm_block_loss -- the block's output product with the loss in its
+ * store (the loss of Algorithm 1 on the block's output, appendix "Error
+ * Types"): with M = H W_d^T (H [T x K], W_d [C x K] bf16, fp32 accumulation)
+ *     E = bf16((R + M) - Yref)   (R, Yref fp32 [T x C]; M is not written),
+ *     loss[0] = sum of the unrounded e^2: per-workgroup fp32 partials (each
+ *               workgroup's wavefronts in a fixed tree) summed in fp64 in a
+ *               fixed order;
+ * the values of uniquan_gemm_nt (fp32 M) followed by uniquan_block_loss, E bit
+ * for bit, the loss to rounding (its partial sums are grouped by tile).
+ * partials holds uniquan_gemm_block_loss_ws(T, C) floats.  C and K multiples
+ * of 8; H, W_d, R, Yref 16-byte and E 8-byte aligned.
+ */
+size_t uniquan_gemm_block_loss_ws(int64_t T, int64_t C);
+uq_status uniquan_gemm_block_loss(int64_t T, int64_t C, int64_t K, const uint16_t* H,
+                                  const uint16_t* Wd, const float* R, const float* Yref,
+                                  uint16_t* E, float* partials, size_t partials_len,
+                                  float* loss, void* stream);
 uq_status uniquan_block_loss(int64_t n, const float* R, const float* M,
                              const float* Yref, uint16_t* E, float* partials,
                              size_t partials_len, float* loss, void* stream);

@@ -193,13 +193,15 @@ class DecoderBlock:
         self.dKp, self.dVp = (e(B, L, d, **f32) for _ in range(2)) if self.grp > 1 else (None, None)
         # MLP activations and their gradients, one row per token
         self.Gm, self.Um, self.Hm, self.dGm, self.dUm = (e(T, I, **b16) for _ in range(5))
-        self.partials = e(uq.uniquan_block_loss_ws(), **f32)
+        self.partials_out = e(max(1, uq.uniquan_gemm_block_loss_ws(T, C)), **f32)
         self.loss = torch.zeros(1, **f32)
         self._rinv_tmp = e(T, **f32)
         self._z_tmp = e(T, C, **b16)
 
     # ---- forward on weights W (dict of bf16 [R, C] tensors) and fp32 input X
-    def _forward(self, W, X):
+    def _forward(self, W, X, loss=False):
+        """The block on X with weights W; with loss, the output product forms E
+        and the loss against Yref in its store (M is not written)."""
         T, C, I, H, d, L, B = self.T, self.C, self.I, self.H, self.d, self.L, self.B
         sc = 1.0 / float(d) ** 0.5
         uq.uniquan_add_rmsnorm(T, C, X, None, self.g1, None, self.Z1, self.r1)
@@ -214,7 +216,11 @@ class DecoderBlock:
         uq.uniquan_gemm_nt(T, C, C, self.O, W["o"], self.A32)
         uq.uniquan_add_rmsnorm(T, C, X, self.A32, self.g2, self.R, self.Z2, self.r2)
         uq.uniquan_gemm_swiglu(T, I, C, self.Z2, W["g"], W["u"], self.Gm, self.Um, self.Hm)
-        uq.uniquan_gemm_nt(T, C, I, self.Hm, W["d"], self.M32)
+        if loss:
+            uq.uniquan_gemm_block_loss(T, C, I, self.Hm, W["d"], self.R, self.Yref, self.E, self.partials_out,
+                                       self.loss)
+        else:
+            uq.uniquan_gemm_nt(T, C, I, self.Hm, W["d"], self.M32)
 
     def _project_heads(self, Wm, n_heads, out, group, rotate, tmp):
         """out [n_heads, T, d] = the head split (rotated when rotate) of Z1 Wm^T:
@@ -248,11 +254,12 @@ class DecoderBlock:
             q.fq_fwd(mode)
 
     def forward(self):
-        """The quantized block on Xhat with the current What."""
-        self._forward({n: q.W_hat for n, q in self.mats.items()}, self.Xhat)
+        """The quantized block on Xhat with the current What, and the loss: E and
+        L = ||f(Xhat; What) - Yref||^2 come from the output product's store."""
+        self._forward({n: q.W_hat for n, q in self.mats.items()}, self.Xhat, loss=True)
 
     def compute_loss(self):
-        uq.uniquan_block_loss(self.T * self.C, self.R, self.M32, self.Yref, self.E, self.partials, self.loss)
+        """The loss is formed by forward(); kept as a step phase (no work)."""
 
     def forward_backward(self, mode):
         """Quantize, forward, loss and dL/dWhat of all seven matrices (left

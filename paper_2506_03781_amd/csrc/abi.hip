@@ -607,6 +607,32 @@ uq_status uniquan_transpose_bf16_batched(int64_t batch, int64_t R, int64_t C, co
 
 size_t uniquan_block_loss_ws(void) { return uq::block_loss_ws(); }
 
+size_t uniquan_gemm_block_loss_ws(int64_t T, int64_t C) {
+  if (T < 1 || C < 1) return 0;
+  return uq::gemm_workgroups(T, C, uq::EPI_LOSS_BLOCK);
+}
+
+uq_status uniquan_gemm_block_loss(int64_t T, int64_t C, int64_t K, const uint16_t* H, const uint16_t* Wd,
+                                  const float* R, const float* Yref, uint16_t* E, float* partials, size_t partials_len,
+                                  float* loss, void* stream) {
+  const char* fn = "uniquan_gemm_block_loss";
+  if (T < 1 || C < 1 || K < 1) return fail(UQ_EINVAL, "%s: T, C, K must be >= 1", fn);
+  if (C % 8 != 0 || K % 8 != 0)
+    return fail(UQ_EINVAL, "%s: C=%lld and K=%lld must be multiples of 8", fn, (long long)C, (long long)K);
+  if (C >= (int64_t(1) << 26) || K >= (int64_t(1) << 31) || T >= (int64_t(1) << 31) ||
+      T * K >= (int64_t(1) << 40) || C * K >= (int64_t(1) << 40) || T * C >= (int64_t(1) << 40))
+    return fail(UQ_EUNSUPPORTED, "%s: shape too large", fn);
+  const size_t need = uniquan_gemm_block_loss_ws(T, C);
+  if (partials_len < need) return fail(UQ_EINVAL, "%s: partials_len=%zu < %zu", fn, partials_len, need);
+  REQ_PTR(H, 16); REQ_PTR(Wd, 16); REQ_PTR(R, 16); REQ_PTR(Yref, 16); REQ_PTR(E, 8); REQ_PTR(partials, 4);
+  REQ_PTR(loss, 4);
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  uq::GemmLaunch g{H, Wd, T, C, K, uq::EPI_LOSS_BLOCK, Yref, E, partials, 1.0f};
+  g.Rres = R;
+  if (uq_status s = hip_status(fn, uq::launch_gemm(g, st))) return s;
+  return hip_status(fn, uq::launch_reduce_loss(partials, int64_t(need), loss, st));
+}
+
 uq_status uniquan_block_loss(int64_t n, const float* R, const float* M, const float* Yref, uint16_t* E,
                              float* partials, size_t partials_len, float* loss, void* stream) {
   const char* fn = "uniquan_block_loss";

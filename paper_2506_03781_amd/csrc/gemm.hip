@@ -61,6 +61,7 @@ struct GemmArgs {
   int causal;
   HeadsParams heads;
   SwigluParams swiglu;
+  const float* Rres;  // EPI_LOSS_BLOCK: the residual added to the product
 };
 
 // Operands and output of batch blockIdx.y.
@@ -389,13 +390,15 @@ __device__ __forceinline__ void epilogue(const GemmArgs& p, f32x16 (&acc)[FM][FN
     // (N < 2^26 is checked on the host)
     const int64_t base = row_base * p.N + col_base;
     const int ldn = int(p.N);
-    float4 y[ITER];
-    if constexpr (EPI == EPI_LOSS) {  // stored target
+    float4 y[ITER], rq[ITER];
+    if constexpr (EPI == EPI_LOSS || EPI == EPI_LOSS_BLOCK) {  // stored target (and residual)
 #pragma unroll
       for (int it = 0; it < ITER; ++it) {
         const int idx = lane + it * 64, rr = idx / Q, cc = (idx % Q) * 4;
         const bool ok = full || (row_base + rr < p.M && col_base + cc < p.N);  // N % 4 == 0 here
         y[it] = ok ? *reinterpret_cast<const float4*>(Yt + base + rr * ldn + cc) : make_float4(0, 0, 0, 0);
+        if constexpr (EPI == EPI_LOSS_BLOCK)
+          rq[it] = ok ? *reinterpret_cast<const float4*>(p.Rres + base + rr * ldn + cc) : make_float4(0, 0, 0, 0);
       }
     }
     auto put = [&](int it) {
@@ -404,13 +407,18 @@ __device__ __forceinline__ void epilogue(const GemmArgs& p, f32x16 (&acc)[FM][FN
       const int64_t o = base + rr * ldn + cc;
       if constexpr (EPI == EPI_TARGET) {
         *reinterpret_cast<float4*>(static_cast<float*>(p.out) + o) = v;
-      } else if constexpr (EPI == EPI_LOSS || EPI == EPI_LOSS_RES) {
+      } else if constexpr (EPI == EPI_LOSS || EPI == EPI_LOSS_RES || EPI == EPI_LOSS_BLOCK) {
         float e0 = v.x, e1 = v.y, e2 = v.z, e3 = v.w;
         if constexpr (EPI == EPI_LOSS) {
           e0 = v.x - y[it].x;
           e1 = v.y - y[it].y;
           e2 = v.z - y[it].z;
           e3 = v.w - y[it].w;
+        } else if constexpr (EPI == EPI_LOSS_BLOCK) {
+          e0 = (rq[it].x + v.x) - y[it].x;
+          e1 = (rq[it].y + v.y) - y[it].y;
+          e2 = (rq[it].z + v.z) - y[it].z;
+          e3 = (rq[it].w + v.w) - y[it].w;
         }
         lsum += e0 * e0;
         lsum += e1 * e1;
@@ -439,7 +447,7 @@ __device__ __forceinline__ void epilogue(const GemmArgs& p, f32x16 (&acc)[FM][FN
     __builtin_amdgcn_s_waitcnt(0xC07F);  // strip reads done before the next strip overwrites it
     __builtin_amdgcn_wave_barrier();
   }
-  if constexpr (EPI == EPI_LOSS || EPI == EPI_LOSS_RES) {
+  if constexpr (EPI == EPI_LOSS || EPI == EPI_LOSS_RES || EPI == EPI_LOSS_BLOCK) {
     __shared__ float sred[NW];
     for (int msk = 32; msk >= 1; msk >>= 1) lsum += __shfl_xor(lsum, msk, 64);
     if (lane == 0) sred[wave] = lsum;
@@ -1032,6 +1040,7 @@ static hipError_t launch_bm(const GemmLaunch& q, hipStream_t st) {
   GemmArgs a;
   a.A = q.A; a.B = q.B; a.M = q.M; a.N = q.N; a.K = q.K;
   a.Yt = q.Yt; a.out = q.out; a.partials = q.partials; a.scale = q.scale;
+  a.Rres = q.Rres;
   a.bsa = q.bsa; a.bsb = q.bsb; a.bso = q.bso;
   a.causal = q.causal;
   a.tiles_m = int((q.M + BM - 1) / BM);
@@ -1043,6 +1052,7 @@ static hipError_t launch_bm(const GemmLaunch& q, hipStream_t st) {
       if (a.Yt != nullptr) launch_epi<BM, BN, EPI_LOSS>(a, grid, st);
       else launch_epi<BM, BN, EPI_LOSS_RES>(a, grid, st);
       break;
+    case EPI_LOSS_BLOCK: launch_epi<BM, BN, EPI_LOSS_BLOCK>(a, grid, st); break;
     case EPI_GRAD_BF16: launch_epi<BM, BN, EPI_GRAD_BF16>(a, grid, st); break;
     default: launch_epi<BM, BN, EPI_GRAD_F32>(a, grid, st); break;
   }

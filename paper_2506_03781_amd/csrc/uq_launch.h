@@ -106,6 +106,7 @@ enum GemmEpi : int {
   EPI_HEADS_ROT = 6,  // EPI_HEADS with the rotary rotation of each head's pairs (i, i + 64)
   EPI_SWIGLU = 7,     // gate and up products in one: G, U, H = silu(G) U (bf16), see SwigluParams
   EPI_SWIGLU_BWD = 8, // dH = bf16(scale acc) [M x N], then dG, dU of the SiLU product (SwigluParams)
+  EPI_LOSS_BLOCK = 9, // e = (Rres + acc) - Yt (fp32, row-major [M x N]); out bf16 = e; partial sum of e^2
 };
 
 // silu(g) u of the SiLU-gated MLP on bf16-rounded g and u (fp32 arithmetic:
@@ -166,6 +167,7 @@ struct GemmLaunch {
   int ta, tb;
   HeadsParams heads;   // EPI_HEADS*
   SwigluParams swiglu; // EPI_SWIGLU
+  const float* Rres;   // EPI_LOSS_BLOCK
 };
 
 // Causal attention with the score tiles on chip (attn_fused.hip), d = 128.

@@ -65,6 +65,8 @@ _SIGS = {
     "uniquan_gemm": ([_i64, _i64, _i64, _vp, _i32, _vp, _i32, _vp, _i32, _f32, _vp], _i32),
     "uniquan_rope_table": ([_i32, _i32, _vp, _vp], _i32),
     "uniquan_gemm_swiglu": ([_i64, _i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp], _i32),
+    "uniquan_gemm_block_loss_ws": ([_i64, _i64], ctypes.c_size_t),
+    "uniquan_gemm_block_loss": ([_i64, _i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp, _vp], _i32),
     "uniquan_gemm_silu_bwd": ([_i64, _i64, _i64, _vp, _vp, _f32, _vp, _vp, _vp, _vp, _vp], _i32),
     "uniquan_gemm_heads": ([_i64, _i32, _i64, _vp, _vp, _i32, _i32, _i32, _vp, _vp, _vp], _i32),
     "uniquan_silu_mul_fwd": ([_i64, _vp, _vp, _vp, _vp], _i32),
@@ -478,6 +480,19 @@ def uniquan_gemm_silu_bwd(T, I, K, E, Wd, scale, G, U, dG, dU, stream=None):
     _check(lib().uniquan_gemm_silu_bwd(T, I, K, _p(E, T * K, _B, "E"), _p(Wd, K * I, _B, "Wd"), float(scale),
                                        _p(G, n, _B, "G"), _p(U, n, _B, "U"), _p(dG, n, _B, "dG"), _p(dU, n, _B, "dU"),
                                        _stream(stream)))
+
+
+def uniquan_gemm_block_loss_ws(T, C) -> int:
+    return int(lib().uniquan_gemm_block_loss_ws(T, C))
+
+
+def uniquan_gemm_block_loss(T, C, K, H, Wd, R, Yref, E, partials, loss, stream=None):
+    """E = bf16((R + H Wd^T) - Yref) and loss = sum e^2 (partials: uniquan_gemm_block_loss_ws floats)."""
+    n = T * C
+    _check(lib().uniquan_gemm_block_loss(T, C, K, _p(H, T * K, _B, "H"), _p(Wd, C * K, _B, "Wd"), _p(R, n, _F, "R"),
+                                         _p(Yref, n, _F, "Yref"), _p(E, n, _B, "E"),
+                                         _p(partials, uniquan_gemm_block_loss_ws(T, C), _F, "partials"),
+                                         partials.numel(), _p(loss, 1, _F, "loss"), _stream(stream)))
 
 
 def uniquan_silu_mul_fwd(G, U, H, stream=None):

@@ -335,6 +335,35 @@ def test_block_loss(n):
     assert abs(float(loss.item()) - ref) <= 1e-5 * ref
 
 
+@pytest.mark.parametrize("T,C,K", [(264, 520, 96), (600, 1032, 160), (8192, 4096, 256)])
+def test_gemm_block_loss_matches_product_then_loss(T, C, K):
+    """The output product with the block loss in its store: E bit for bit the
+    product (fp32) followed by uniquan_block_loss; the loss (partials grouped
+    by tile) within 1e-6 of it and within 1e-5 of the fp64 sum of the same
+    e^2 (ragged multi-tile shapes, the 7B width)."""
+    rs = np.random.default_rng(T + C + K + 5)
+    Hh = dev(bfr(rs.standard_normal((T, K))), torch.bfloat16)
+    Wd = dev(bfr(rs.standard_normal((C, K)) * 0.1), torch.bfloat16)
+    R = dev(rs.standard_normal((T, C)), torch.float32)
+    Y = dev(rs.standard_normal((T, C)), torch.float32)
+    E = torch.full((T, C), float("nan"), device="cuda", dtype=torch.bfloat16)
+    part = torch.empty(uq.uniquan_gemm_block_loss_ws(T, C), device="cuda")
+    loss = torch.zeros(1, device="cuda")
+    uq.uniquan_gemm_block_loss(T, C, K, Hh, Wd, R, Y, E, part, loss)
+    M = torch.empty(T, C, device="cuda")
+    uq.uniquan_gemm_nt(T, C, K, Hh, Wd, M)
+    E0 = torch.empty(T, C, device="cuda", dtype=torch.bfloat16)
+    part0 = torch.empty(uq.uniquan_block_loss_ws(), device="cuda")
+    loss0 = torch.zeros(1, device="cuda")
+    uq.uniquan_block_loss(T * C, R, M, Y, E0, part0, loss0)
+    torch.cuda.synchronize()
+    assert torch.equal(E.view(torch.int16), E0.view(torch.int16))
+    e = ((R.cpu().numpy() + M.cpu().numpy()) - Y.cpu().numpy()).astype(np.float64)
+    ref = float(np.sum(e * e))
+    assert abs(float(loss.item()) - float(loss0.item())) <= 1e-6 * ref
+    assert abs(float(loss.item()) - ref) <= 1e-5 * ref
+
+
 @pytest.mark.parametrize("L,N,batch", [(96, 64, 3), (256, 128, 2), (2048, 128, 2)])
 def test_gemm_nt_batched_causal(L, N, batch):
     """Causal modes against the full product: mode 1 on j <= i; modes 2 and 3
