@@ -147,6 +147,119 @@ __global__ __launch_bounds__(256) void rmsnorm_bwd_kernel(int64_t T, int64_t C, 
   }
 }
 
+// Row-resident forms of the two kernels above for C = 256 NV (NV <= 16): the
+// row's values stay in registers between the reduction and the output pass,
+// so each input is read once.  Same lane layout (lane l takes float4 l + 64 k)
+// and the same order of every sum and product as the two-pass kernels, so
+// the results are the same bit for bit.
+template <int NV>
+__global__ __launch_bounds__(256) void add_rmsnorm_rows_kernel(int64_t T, int64_t C, const float* __restrict__ X,
+                                                               const float* __restrict__ A,
+                                                               const float* __restrict__ gamma,
+                                                               float* __restrict__ R, uint16_t* __restrict__ Z,
+                                                               float* __restrict__ rinv) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (row >= T) return;
+  const float4* x = reinterpret_cast<const float4*>(X + row * C);
+  const float4* a = A ? reinterpret_cast<const float4*>(A + row * C) : nullptr;
+  float4 v[NV];
+#pragma unroll
+  for (int k = 0; k < NV; ++k) v[k] = x[lane + 64 * k];
+  if (a) {
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+      const float4 w = a[lane + 64 * k];
+      v[k].x += w.x; v[k].y += w.y; v[k].z += w.z; v[k].w += w.w;
+    }
+  }
+  float ss = 0.0f;
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    ss += v[k].x * v[k].x;
+    ss += v[k].y * v[k].y;
+    ss += v[k].z * v[k].z;
+    ss += v[k].w * v[k].w;
+  }
+  ss = wave_sum(ss);
+  const float r = 1.0f / sqrtf(ss / float(C) + 1e-5f);
+  if (lane == 0) rinv[row] = r;
+  const float4* g4 = reinterpret_cast<const float4*>(gamma);
+  float4* R4 = R ? reinterpret_cast<float4*>(R + row * C) : nullptr;
+  uint2* Z2 = reinterpret_cast<uint2*>(Z + row * C);
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    const int64_t c = lane + 64 * k;
+    if (R4) R4[c] = v[k];
+    const float4 g = g4[c];
+    Z2[c] = make_uint2(uint32_t(to_bf((v[k].x * r) * g.x)) | (uint32_t(to_bf((v[k].y * r) * g.y)) << 16),
+                       uint32_t(to_bf((v[k].z * r) * g.z)) | (uint32_t(to_bf((v[k].w * r) * g.w)) << 16));
+  }
+}
+
+template <int NV>
+__global__ __launch_bounds__(256) void rmsnorm_bwd_rows_kernel(int64_t T, int64_t C, const float* __restrict__ dZa,
+                                                               const float* __restrict__ dZb,
+                                                               const float* __restrict__ Xin,
+                                                               const float* __restrict__ gamma,
+                                                               const float* __restrict__ rinv,
+                                                               const uint16_t* __restrict__ E, float escale,
+                                                               uint16_t* __restrict__ dR, float* __restrict__ dRf) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (row >= T) return;
+  const int64_t base = row * C;
+  const float4* za = reinterpret_cast<const float4*>(dZa + base);
+  const float4* zb = dZb ? reinterpret_cast<const float4*>(dZb + base) : nullptr;
+  const float4* x4 = reinterpret_cast<const float4*>(Xin + base);
+  const float4* g4 = reinterpret_cast<const float4*>(gamma);
+  float4 gz[NV], xv[NV];
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    gz[k] = za[lane + 64 * k];
+    xv[k] = x4[lane + 64 * k];
+  }
+  if (zb) {
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+      const float4 w = zb[lane + 64 * k];
+      gz[k].x += w.x; gz[k].y += w.y; gz[k].z += w.z; gz[k].w += w.w;
+    }
+  }
+  float dot = 0.0f;
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    const float4 g = g4[lane + 64 * k];
+    gz[k] = make_float4(g.x * gz[k].x, g.y * gz[k].y, g.z * gz[k].z, g.w * gz[k].w);
+    dot += gz[k].x * xv[k].x;
+    dot += gz[k].y * xv[k].y;
+    dot += gz[k].z * xv[k].z;
+    dot += gz[k].w * xv[k].w;
+  }
+  dot = wave_sum(dot);
+  const float r = rinv[row];
+  const float k3 = (r * r * r) * (dot / float(C));
+  const uint2* e2 = E ? reinterpret_cast<const uint2*>(E + base) : nullptr;
+  uint2* d2 = reinterpret_cast<uint2*>(dR + base);
+  float4* df = dRf ? reinterpret_cast<float4*>(dRf + base) : nullptr;
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    const int64_t c = lane + 64 * k;
+    const float4 g = gz[k], v = xv[k];
+    float o[4] = {r * g.x - v.x * k3, r * g.y - v.y * k3, r * g.z - v.z * k3, r * g.w - v.w * k3};
+    if (e2) {
+      const uint2 e = e2[c];
+      o[0] += escale * bf(uint16_t(e.x & 0xFFFFu));
+      o[1] += escale * bf(uint16_t(e.x >> 16));
+      o[2] += escale * bf(uint16_t(e.y & 0xFFFFu));
+      o[3] += escale * bf(uint16_t(e.y >> 16));
+    }
+    d2[c] = make_uint2(uint32_t(to_bf(o[0])) | (uint32_t(to_bf(o[1])) << 16),
+                       uint32_t(to_bf(o[2])) | (uint32_t(to_bf(o[3])) << 16));
+    if (df) df[c] = make_float4(o[0], o[1], o[2], o[3]);
+  }
+}
+
 // Head h of a grouped layout (perm heads sharing a key/value head) is stored
 // at slot (h mod perm) (H / perm) + h / perm: the heads at one position of
 // their groups are contiguous, in key/value head order.
@@ -517,15 +630,37 @@ constexpr int kLossBlocks = 1024;
 
 hipError_t launch_add_rmsnorm(int64_t T, int64_t C, const float* X, const float* A, const float* gamma, float* R,
                               uint16_t* Z, float* rinv, hipStream_t st) {
-  hipLaunchKernelGGL(add_rmsnorm_kernel, dim3(unsigned((T + 3) / 4)), dim3(256), 0, st, T, C, X, A, gamma, R, Z, rinv);
+  const dim3 g(unsigned((T + 3) / 4));
+  switch (C % 256 == 0 ? C / 256 : 0) {
+    case 16: hipLaunchKernelGGL(add_rmsnorm_rows_kernel<16>, g, dim3(256), 0, st, T, C, X, A, gamma, R, Z, rinv); break;
+    case 8: hipLaunchKernelGGL(add_rmsnorm_rows_kernel<8>, g, dim3(256), 0, st, T, C, X, A, gamma, R, Z, rinv); break;
+    case 4: hipLaunchKernelGGL(add_rmsnorm_rows_kernel<4>, g, dim3(256), 0, st, T, C, X, A, gamma, R, Z, rinv); break;
+    default: hipLaunchKernelGGL(add_rmsnorm_kernel, g, dim3(256), 0, st, T, C, X, A, gamma, R, Z, rinv); break;
+  }
   return hipGetLastError();
 }
 
 hipError_t launch_rmsnorm_bwd(int64_t T, int64_t C, const float* dZa, const float* dZb, const float* X,
                               const float* gamma, const float* rinv, const uint16_t* E, float escale, uint16_t* dR,
                               float* dRf, hipStream_t st) {
-  hipLaunchKernelGGL(rmsnorm_bwd_kernel, dim3(unsigned((T + 3) / 4)), dim3(256), 0, st, T, C, dZa, dZb, X, gamma, rinv,
-                     E, escale, dR, dRf);
+  const dim3 g(unsigned((T + 3) / 4));
+  switch (C % 256 == 0 ? C / 256 : 0) {
+    case 16:
+      hipLaunchKernelGGL(rmsnorm_bwd_rows_kernel<16>, g, dim3(256), 0, st, T, C, dZa, dZb, X, gamma, rinv, E, escale,
+                         dR, dRf);
+      break;
+    case 8:
+      hipLaunchKernelGGL(rmsnorm_bwd_rows_kernel<8>, g, dim3(256), 0, st, T, C, dZa, dZb, X, gamma, rinv, E, escale,
+                         dR, dRf);
+      break;
+    case 4:
+      hipLaunchKernelGGL(rmsnorm_bwd_rows_kernel<4>, g, dim3(256), 0, st, T, C, dZa, dZb, X, gamma, rinv, E, escale,
+                         dR, dRf);
+      break;
+    default:
+      hipLaunchKernelGGL(rmsnorm_bwd_kernel, g, dim3(256), 0, st, T, C, dZa, dZb, X, gamma, rinv, E, escale, dR, dRf);
+      break;
+  }
   return hipGetLastError();
 }
 

@@ -168,7 +168,7 @@ def test_gemm_silu_bwd_matches_product_then_silu_bwd(T, I, K):
     assert torch.equal(bits(dG), bits(dG0)) and torch.equal(bits(dU), bits(dU0))
 
 
-@pytest.mark.parametrize("T,C", [(5, 8), (37, 264), (64, 4096)])
+@pytest.mark.parametrize("T,C", [(5, 8), (37, 264), (33, 1024), (9, 2048), (64, 4096)])
 def test_add_rmsnorm(T, C):
     rs = np.random.default_rng(T * C)
     X = rs.standard_normal((T, C)).astype(F32)
@@ -190,7 +190,7 @@ def test_add_rmsnorm(T, C):
     within_bf16(host(Z2), zref2, 1e-6 * np.abs(zref2).max(), "Z without A")
 
 
-@pytest.mark.parametrize("T,C", [(7, 16), (33, 512)])
+@pytest.mark.parametrize("T,C", [(7, 16), (33, 512), (33, 1024), (9, 2048), (64, 4096)])
 def test_rmsnorm_bwd(T, C):
     rs = np.random.default_rng(T + C)
     X = rs.standard_normal((T, C))
