@@ -664,9 +664,9 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 }
 
 namespace {
-constexpr int FWD_NW = 8, FWD_S = 4;
+constexpr int FWD_NW = 4, FWD_S = 2;
 constexpr int DQ_NW = 4, DQ_S = 2;
-constexpr int DKV_NW = 8, DKV_S = 2;
+constexpr int DKV_NW = 4, DKV_S = 2;
 }  // namespace
 
 static void set_tok(AttnArgs& a, const AttnLaunch& q) {
