@@ -69,7 +69,7 @@ typedef enum { UQ_OK = 0, UQ_EINVAL = 1, UQ_EUNSUPPORTED = 2, UQ_EHIP = 3 } uq_s
 typedef enum { UQ_F32 = 0, UQ_BF16 = 1 } uq_dtype;
 typedef enum { UQ_MAP_FULL = 0, UQ_MAP_LOCAL = 1, UQ_MAP_FROZEN = 2 } uq_map_mode;
 
-#define UNIQUAN_ABI_VERSION 2
+#define UNIQUAN_ABI_VERSION 3
 
 /* ABI version of the loaded library (UNIQUAN_ABI_VERSION). */
 int uniquan_abi_version(void);
@@ -392,6 +392,18 @@ uq_status uniquan_gemm_nt(int64_t M, int64_t N, int64_t K, const uint16_t* A,
                           float scale, void* stream);
 
 /*
+ * uniquan_gemm_nt_residual -- out[M x N] = R + A[M x K] B[N x K]^T (fp32
+ * R and out row-major, 16-byte aligned; out may be R itself): the attention
+ * module's output projection with the block's first residual added in the
+ * product's store (Algorithm 1's forward through a pre-norm block), bit for
+ * bit uniquan_gemm_nt (fp32 out, scale 1) followed by the fp32 sum R + P.
+ * uniquan_gemm_nt's rules on the shape and operands.
+ */
+uq_status uniquan_gemm_nt_residual(int64_t M, int64_t N, int64_t K, const uint16_t* A,
+                                   const uint16_t* B, const float* R, float* out,
+                                   void* stream);
+
+/*
  * uniquan_gemm -- out[M x N] = scale * sum_k A(m, k) B(n, k) with either
  * operand stored K-slow, the contractions of the block's backpropagation
  * (Algorithm 1): the weight gradient dL/dW = dY^T X reads dY [T x out] and
@@ -432,13 +444,17 @@ uq_status uniquan_gemm_swiglu(int64_t T, int64_t I, int64_t K, const uint16_t* X
  *     dG, dU = the SiLU product's backward at (dH, G, U) (bf16 [T x I], as
  *                               uniquan_silu_mul_bwd computes it),
  * bit for bit uniquan_gemm (b_kslow = 1, bf16 out) followed by
- * uniquan_silu_mul_bwd.  I a multiple of 8, K of 32; E, W_d 16-byte and
+ * uniquan_silu_mul_bwd.  G and U are [T x I] row-major; the rows of dG and
+ * of dU are ld_d elements apart (0 means I; ld_d = 2 I with dU = dG + I puts
+ * the two side by side in one [T x 2I] array, the operand of the stacked
+ * products dL/dW_g; dL/dW_u = [dG dU]^T X and dX = [dG dU] [W_g; W_u]).
+ * I a multiple of 8, K of 32, ld_d >= I a multiple of 4; E, W_d 16-byte and
  * G, U, dG, dU 8-byte aligned.
  */
 uq_status uniquan_gemm_silu_bwd(int64_t T, int64_t I, int64_t K, const uint16_t* E,
                                 const uint16_t* Wd, float scale, const uint16_t* G,
                                 const uint16_t* U, uint16_t* dG, uint16_t* dU,
-                                void* stream);
+                                int64_t ld_d, void* stream);
 
 /*
  * uniquan_silu_mul_fwd -- H[i] = silu(G[i]) * U[i], i < n (bf16 in and out,

@@ -178,8 +178,8 @@ class DecoderBlock:
         e = torch.empty
         self.g1 = to_dev(g1, torch.float32, device)
         self.g2 = to_dev(g2, torch.float32, device)
-        self.Xhat, self.Yref, self.A32, self.R, self.M32, self.Yhat = (e(T, C, **f32) for _ in range(6))
-        self.Qf, self.dZa, self.dZb = (e(T, C, **f32) for _ in range(3))
+        self.Xhat, self.Yref, self.R, self.M32, self.Yhat = (e(T, C, **f32) for _ in range(5))
+        self.Qf, self.dZa = (e(T, C, **f32) for _ in range(2))
         self.Kf = e(T, Ckv, **f32)
         self.r1, self.r2 = e(T, **f32), e(T, **f32)
         (self.Z1, self.O, self.Z2, self.E, self.dA, self.dO, self.dQ) = (e(T, C, **b16) for _ in range(7))
@@ -195,12 +195,31 @@ class DecoderBlock:
         uq.uniquan_rope_table(L, d, self.rope_cs)
         # grouped-query: dK, dV contributions per query head (summed per key/value head)
         self.dKp, self.dVp = (e(B, L, d, **f32) for _ in range(2)) if self.grp > 1 else (None, None)
-        # MLP activations and their gradients, one row per token
-        self.Gm, self.Um, self.Hm, self.dGm, self.dUm = (e(T, I, **b16) for _ in range(5))
+        # MLP activations, one row per token; the gradients of G and U side by
+        # side in one [T, 2I] array, and W_g, W_u (their What and dL/dWhat)
+        # stacked in [2I, C] arrays, so that dL/dW_g; dL/dW_u = [dG dU]^T Z2
+        # and dZ2 = [dG dU] [W_g; W_u] are one product each (K = 2I for dZ2)
+        self.Gm, self.Um, self.Hm = (e(T, I, **b16) for _ in range(3))
+        self.dGU = e(T, 2 * I, **b16)
+        self.dGm, self.dUm = self.dGU[:, :I], self.dGU[:, I:]
+        self.What_gu = self._stack(mats["g"], mats["u"], "W_hat")
+        self.G_gu = self._stack(mats["g"], mats["u"], "G")
         self.partials_out = e(max(1, uq.uniquan_gemm_block_loss_ws(T, C)), **f32)
         self.loss = torch.zeros(1, **f32)
         self._rinv_tmp = e(T, **f32)
         self._z_tmp = e(T, C, **b16)
+
+    @staticmethod
+    def _stack(a, b, attr):
+        """One [Ra + Rb, C] array holding a.attr then b.attr (their current
+        values); both matrices' attr become row views of it."""
+        x, y = getattr(a, attr), getattr(b, attr)
+        st = torch.empty(x.shape[0] + y.shape[0], x.shape[1], dtype=x.dtype, device=x.device)
+        st[:x.shape[0]].copy_(x)
+        st[x.shape[0]:].copy_(y)
+        setattr(a, attr, st[:x.shape[0]])
+        setattr(b, attr, st[x.shape[0]:])
+        return st
 
     # ---- forward on weights W (dict of bf16 [R, C] tensors) and fp32 input X
     def _forward(self, W, X, loss=False):
@@ -217,8 +236,9 @@ class DecoderBlock:
         # (O written token-major: the merge of the heads is in the kernel's store)
         uq.uniquan_attn_fwd(B, Bkv, L, d, self.Qh, self.Kh, self.Vh, sc, self.O, self.lse,
                             tok_seqs=self.n_seq, group=grp)
-        uq.uniquan_gemm_nt(T, C, C, self.O, W["o"], self.A32)
-        uq.uniquan_add_rmsnorm(T, C, X, self.A32, self.g2, self.R, self.Z2, self.r2)
+        # R = X + O W_o^T in the product's store, then the second norm of R
+        uq.uniquan_gemm_nt_residual(T, C, C, self.O, W["o"], X, self.R)
+        uq.uniquan_add_rmsnorm(T, C, self.R, None, self.g2, None, self.Z2, self.r2)
         uq.uniquan_gemm_swiglu(T, I, C, self.Z2, W["g"], W["u"], self.Gm, self.Um, self.Hm)
         if loss:
             uq.uniquan_gemm_block_loss(T, C, I, self.Hm, W["d"], self.R, self.Yref, self.E, self.partials_out,
@@ -304,19 +324,21 @@ class DecoderBlock:
         # stored (K-slow, K = the matrix's rows).
         fork()
         uq.uniquan_gemm(C, I, T, self.E, 1, self.Hm, 1, m["d"].G, 2.0)
-        uq.uniquan_gemm_silu_bwd(T, I, C, self.E, Wh["d"], 2.0, self.Gm, self.Um, self.dGm, self.dUm, stream=ps)
+        uq.uniquan_gemm_silu_bwd(T, I, C, self.E, Wh["d"], 2.0, self.Gm, self.Um, self.dGm, self.dUm, stream=ps,
+                                 ld_d=2 * I)
         join()
         done("d")
-        fork()
-        uq.uniquan_gemm(I, C, T, self.dGm, 1, self.Z2, 1, m["g"].G)
-        uq.uniquan_gemm(T, C, I, self.dGm, 0, Wh["g"], 1, self.dZa)
-        uq.uniquan_gemm(I, C, T, self.dUm, 1, self.Z2, 1, m["u"].G, stream=ps)
-        uq.uniquan_gemm(T, C, I, self.dUm, 0, Wh["u"], 1, self.dZb, stream=ps)
-        join()
+        # gate and up together: [dG dU] is [T, 2I], What_g; What_u and their
+        # gradients are stacked [2I, C]
+        for n, off in (("g", 0), ("u", I)):
+            assert m[n].W_hat.data_ptr() == self.What_gu[off].data_ptr() and \
+                m[n].G.data_ptr() == self.G_gu[off].data_ptr(), "What / G of gate and up must stay stacked"
+        uq.uniquan_gemm(2 * I, C, T, self.dGU, 1, self.Z2, 1, self.G_gu)
+        uq.uniquan_gemm(T, C, 2 * I, self.dGU, 0, self.What_gu, 1, self.dZa)
         done("g")
         done("u")
         # second norm and residual: dR = 2 E + RMSNorm backward
-        uq.uniquan_rmsnorm_bwd(T, C, self.dZa, self.dZb, self.R, self.g2, self.r2, self.E, 2.0, self.dA)
+        uq.uniquan_rmsnorm_bwd(T, C, self.dZa, None, self.R, self.g2, self.r2, self.E, 2.0, self.dA)
         # attention module
         fork()
         uq.uniquan_gemm(C, C, T, self.dA, 1, self.O, 1, m["o"].G)

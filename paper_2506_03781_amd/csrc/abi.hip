@@ -393,6 +393,21 @@ uq_status uniquan_gemm_nt(int64_t M, int64_t N, int64_t K, const uint16_t* A, co
   return hip_status(fn, uq::launch_gemm(g, static_cast<hipStream_t>(stream)));
 }
 
+uq_status uniquan_gemm_nt_residual(int64_t M, int64_t N, int64_t K, const uint16_t* A, const uint16_t* B,
+                                   const float* R, float* out, void* stream) {
+  const char* fn = "uniquan_gemm_nt_residual";
+  if (M < 1 || N < 1 || K < 1) return fail(UQ_EINVAL, "%s: M, N, K must be >= 1", fn);
+  if (N % 8 != 0 || K % 8 != 0) return fail(UQ_EINVAL, "%s: N=%lld and K=%lld must be multiples of 8", fn,
+                                            (long long)N, (long long)K);
+  if (N >= (int64_t(1) << 26) || K >= (int64_t(1) << 31) || M >= (int64_t(1) << 31) ||
+      M * K >= (int64_t(1) << 40) || N * K >= (int64_t(1) << 40) || M * N >= (int64_t(1) << 40))
+    return fail(UQ_EUNSUPPORTED, "%s: shape too large", fn);
+  REQ_PTR(A, 16); REQ_PTR(B, 16); REQ_PTR(R, 16); REQ_PTR(out, 16);
+  uq::GemmLaunch g{A, B, M, N, K, uq::EPI_RESID, nullptr, out, nullptr, 1.0f};
+  g.Rres = R;
+  return hip_status(fn, uq::launch_gemm(g, static_cast<hipStream_t>(stream)));
+}
+
 uq_status uniquan_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* A, int a_kslow, const uint16_t* B, int b_kslow,
                        void* out, int out_dtype, float scale, void* stream) {
   const char* fn = "uniquan_gemm";
@@ -431,13 +446,17 @@ uq_status uniquan_gemm_swiglu(int64_t T, int64_t I, int64_t K, const uint16_t* X
 }
 
 uq_status uniquan_gemm_silu_bwd(int64_t T, int64_t I, int64_t K, const uint16_t* E, const uint16_t* Wd, float scale,
-                                const uint16_t* G, const uint16_t* U, uint16_t* dG, uint16_t* dU, void* stream) {
+                                const uint16_t* G, const uint16_t* U, uint16_t* dG, uint16_t* dU, int64_t ld_d,
+                                void* stream) {
   const char* fn = "uniquan_gemm_silu_bwd";
   if (T < 1 || I < 1 || K < 1) return fail(UQ_EINVAL, "%s: T, I, K must be >= 1", fn);
   if (I % 8 != 0 || K % 32 != 0)
     return fail(UQ_EINVAL, "%s: I=%lld must be a multiple of 8 and K=%lld of 32", fn, (long long)I, (long long)K);
+  if (ld_d == 0) ld_d = I;
+  if (ld_d < I || ld_d % 4 != 0)
+    return fail(UQ_EINVAL, "%s: ld_d=%lld must be >= I=%lld and a multiple of 4", fn, (long long)ld_d, (long long)I);
   if (I >= (int64_t(1) << 26) || K >= (int64_t(1) << 31) || T >= (int64_t(1) << 31) ||
-      T * K >= (int64_t(1) << 40) || I * K >= (int64_t(1) << 40) || T * I >= (int64_t(1) << 40))
+      T * K >= (int64_t(1) << 40) || I * K >= (int64_t(1) << 40) || T * ld_d >= (int64_t(1) << 40))
     return fail(UQ_EUNSUPPORTED, "%s: shape too large", fn);
   REQ_PTR(E, 16); REQ_PTR(Wd, 16); REQ_PTR(G, 8); REQ_PTR(U, 8); REQ_PTR(dG, 8); REQ_PTR(dU, 8);
   uq::GemmLaunch g{E, Wd, T, I, K, uq::EPI_SWIGLU_BWD, nullptr, dG, nullptr, scale};
@@ -445,6 +464,7 @@ uq_status uniquan_gemm_silu_bwd(int64_t T, int64_t I, int64_t K, const uint16_t*
   g.swiglu.G_in = G;
   g.swiglu.U_in = U;
   g.swiglu.dU = dU;
+  g.swiglu.ldo = ld_d;
   return hip_status(fn, uq::launch_gemm(g, static_cast<hipStream_t>(stream)));
 }
 

@@ -61,7 +61,7 @@ struct GemmArgs {
   int causal;
   HeadsParams heads;
   SwigluParams swiglu;
-  const float* Rres;  // EPI_LOSS_BLOCK: the residual added to the product
+  const float* Rres;  // EPI_LOSS_BLOCK, EPI_RESID: the residual added to the product
 };
 
 // Operands and output of batch blockIdx.y.
@@ -361,7 +361,7 @@ __device__ __forceinline__ void epilogue(const GemmArgs& p, f32x16 (&acc)[FM][FN
           const float u = __uint_as_float((uw[e >> 1] << sh) & mk);
           silu_mul_grad(dh, g, u, dg[e], du[e]);
         }
-        const int64_t o = m * p.N + n;
+        const int64_t o = m * p.swiglu.ldo + n;
         *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.out) + o) =
             make_uint2(pack_bf16x2(dg[0], dg[1]), pack_bf16x2(dg[2], dg[3]));
         *reinterpret_cast<uint2*>(p.swiglu.dU + o) = make_uint2(pack_bf16x2(du[0], du[1]), pack_bf16x2(du[2], du[3]));
@@ -391,13 +391,14 @@ __device__ __forceinline__ void epilogue(const GemmArgs& p, f32x16 (&acc)[FM][FN
     const int64_t base = row_base * p.N + col_base;
     const int ldn = int(p.N);
     float4 y[ITER], rq[ITER];
-    if constexpr (EPI == EPI_LOSS || EPI == EPI_LOSS_BLOCK) {  // stored target (and residual)
+    if constexpr (EPI == EPI_LOSS || EPI == EPI_LOSS_BLOCK || EPI == EPI_RESID) {  // stored target and/or residual
 #pragma unroll
       for (int it = 0; it < ITER; ++it) {
         const int idx = lane + it * 64, rr = idx / Q, cc = (idx % Q) * 4;
         const bool ok = full || (row_base + rr < p.M && col_base + cc < p.N);  // N % 4 == 0 here
-        y[it] = ok ? *reinterpret_cast<const float4*>(Yt + base + rr * ldn + cc) : make_float4(0, 0, 0, 0);
-        if constexpr (EPI == EPI_LOSS_BLOCK)
+        if constexpr (EPI != EPI_RESID)
+          y[it] = ok ? *reinterpret_cast<const float4*>(Yt + base + rr * ldn + cc) : make_float4(0, 0, 0, 0);
+        if constexpr (EPI == EPI_LOSS_BLOCK || EPI == EPI_RESID)
           rq[it] = ok ? *reinterpret_cast<const float4*>(p.Rres + base + rr * ldn + cc) : make_float4(0, 0, 0, 0);
       }
     }
@@ -432,6 +433,10 @@ __device__ __forceinline__ void epilogue(const GemmArgs& p, f32x16 (&acc)[FM][FN
       } else if constexpr (EPI == EPI_GRAD_F32) {
         *reinterpret_cast<float4*>(static_cast<float*>(p.out) + o) =
             make_float4(p.scale * v.x, p.scale * v.y, p.scale * v.z, p.scale * v.w);
+      } else if constexpr (EPI == EPI_RESID) {
+        *reinterpret_cast<float4*>(static_cast<float*>(p.out) + o) =
+            make_float4(rq[it].x + p.scale * v.x, rq[it].y + p.scale * v.y, rq[it].z + p.scale * v.z,
+                        rq[it].w + p.scale * v.w);
       }
     };
     if (full) {  // uniform: interior tiles store without per-element checks
@@ -1053,6 +1058,7 @@ static hipError_t launch_bm(const GemmLaunch& q, hipStream_t st) {
       else launch_epi<BM, BN, EPI_LOSS_RES>(a, grid, st);
       break;
     case EPI_LOSS_BLOCK: launch_epi<BM, BN, EPI_LOSS_BLOCK>(a, grid, st); break;
+    case EPI_RESID: launch_epi<BM, BN, EPI_RESID>(a, grid, st); break;
     case EPI_GRAD_BF16: launch_epi<BM, BN, EPI_GRAD_BF16>(a, grid, st); break;
     default: launch_epi<BM, BN, EPI_GRAD_F32>(a, grid, st); break;
   }
@@ -1116,6 +1122,7 @@ static hipError_t launch_gemm_kslow(const GemmLaunch& q, hipStream_t st) {
   a.bsa = a.bsb = a.bso = 0;
   a.causal = 0;
   a.swiglu = q.swiglu;
+  if (a.swiglu.ldo == 0) a.swiglu.ldo = q.N;
   const bool wide = q.M > 128 && q.N > 128 && tiles<256, 256>(q.M, q.N) >= 256;
   const int BN = wide ? 256 : 128;
   a.tiles_m = int((q.M + 255) / 256);

@@ -107,6 +107,7 @@ enum GemmEpi : int {
   EPI_SWIGLU = 7,     // gate and up products in one: G, U, H = silu(G) U (bf16), see SwigluParams
   EPI_SWIGLU_BWD = 8, // dH = bf16(scale acc) [M x N], then dG, dU of the SiLU product (SwigluParams)
   EPI_LOSS_BLOCK = 9, // e = (Rres + acc) - Yt (fp32, row-major [M x N]); out bf16 = e; partial sum of e^2
+  EPI_RESID = 10,     // out fp32 = Rres + scale acc (Rres fp32 row-major [M x N]; may alias out)
 };
 
 // silu(g) u of the SiLU-gated MLP on bf16-rounded g and u (fp32 arithmetic:
@@ -128,7 +129,9 @@ __device__ __forceinline__ void silu_mul_grad(float dh, float g, float u, float&
 // interleave 32-row blocks of the two (block 2q of a 256-column tile: W_g
 // rows 128 n + 32 q .., block 2q + 1: the same rows of W_u), so a 64-column
 // wave tile holds G and U of the same 32 rows of W; out = G, U, H [M x I].
-// EPI_SWIGLU_BWD: G, U in (gate, up), out = dG, dU2 = dU [M x N].
+// EPI_SWIGLU_BWD: G, U in (gate, up) [M x N], out = dG, dU = dU, rows ldo
+// elements apart (ldo = 2 N with dU = out + N: the two side by side in one
+// [M x 2N] array, as the stacked products of the backward read them).
 struct SwigluParams {
   const uint16_t* Wu;
   uint16_t* U;
@@ -137,6 +140,7 @@ struct SwigluParams {
   const uint16_t* G_in;
   const uint16_t* U_in;
   uint16_t* dU;
+  int64_t ldo;
 };
 
 // Head-split epilogue (EPI_HEADS*): position of row m is m % L; cos and sin

@@ -67,7 +67,8 @@ _SIGS = {
     "uniquan_gemm_swiglu": ([_i64, _i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp], _i32),
     "uniquan_gemm_block_loss_ws": ([_i64, _i64], ctypes.c_size_t),
     "uniquan_gemm_block_loss": ([_i64, _i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp, _vp], _i32),
-    "uniquan_gemm_silu_bwd": ([_i64, _i64, _i64, _vp, _vp, _f32, _vp, _vp, _vp, _vp, _vp], _i32),
+    "uniquan_gemm_nt_residual": ([_i64, _i64, _i64, _vp, _vp, _vp, _vp, _vp], _i32),
+    "uniquan_gemm_silu_bwd": ([_i64, _i64, _i64, _vp, _vp, _f32, _vp, _vp, _vp, _vp, _i64, _vp], _i32),
     "uniquan_gemm_heads": ([_i64, _i32, _i64, _vp, _vp, _i32, _i32, _i32, _vp, _vp, _vp], _i32),
     "uniquan_silu_mul_fwd": ([_i64, _vp, _vp, _vp, _vp], _i32),
     "uniquan_silu_mul_bwd": ([_i64, _vp, _vp, _vp, _vp, _vp, _vp], _i32),
@@ -474,12 +475,37 @@ def uniquan_gemm_swiglu(T, I, K, X, Wg, Wu, G, U, H, stream=None):
                                      _p(G, n, _B, "G"), _p(U, n, _B, "U"), _p(H, n, _B, "H"), _stream(stream)))
 
 
-def uniquan_gemm_silu_bwd(T, I, K, E, Wd, scale, G, U, dG, dU, stream=None):
-    """dG, dU of the SiLU product at dH = bf16(scale E Wd) (Wd stored [K, I]); dH is not written."""
+def uniquan_gemm_nt_residual(M, N, K, A, B, R, out, stream=None):
+    """out = R + A B^T (fp32 [M, N]; A [M, K], B [N, K] bf16); out may be R."""
+    _check(lib().uniquan_gemm_nt_residual(M, N, K, _p(A, M * K, _B, "A"), _p(B, N * K, _B, "B"),
+                                          _p(R, M * N, _F, "R"), _p(out, M * N, _F, "out"), _stream(stream)))
+
+
+def _p_rows(t, rows, cols, ld, dtypes, name):
+    """Device pointer of a [rows, cols] tensor whose rows are ld elements apart
+    (a contiguous tensor when ld == cols, else a column slice of a wider one)."""
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dtype not in dtypes:
+        raise TypeError(f"{name} has dtype {t.dtype}, expected one of {dtypes}")
+    if tuple(t.shape) != (rows, cols) or (rows > 1 and t.stride(0) != ld) or t.stride(1) != 1:
+        raise ValueError(f"{name} must be [{rows}, {cols}] with rows {ld} elements apart")
+    return t.data_ptr()
+
+
+def uniquan_gemm_silu_bwd(T, I, K, E, Wd, scale, G, U, dG, dU, stream=None, ld_d=0):
+    """dG, dU of the SiLU product at dH = bf16(scale E Wd) (Wd stored [K, I]); dH is not written.
+    With ld_d = 0, dG and dU are contiguous [T, I]; else [T, I] views whose rows
+    are ld_d elements apart (dG = A[:, :I], dU = A[:, I:] of one [T, 2I] array A)."""
     n = T * I
+    if ld_d:
+        pg, pu = _p_rows(dG, T, I, ld_d, _B, "dG"), _p_rows(dU, T, I, ld_d, _B, "dU")
+    else:
+        pg, pu = _p(dG, n, _B, "dG"), _p(dU, n, _B, "dU")
     _check(lib().uniquan_gemm_silu_bwd(T, I, K, _p(E, T * K, _B, "E"), _p(Wd, K * I, _B, "Wd"), float(scale),
-                                       _p(G, n, _B, "G"), _p(U, n, _B, "U"), _p(dG, n, _B, "dG"), _p(dU, n, _B, "dU"),
-                                       _stream(stream)))
+                                       _p(G, n, _B, "G"), _p(U, n, _B, "U"), pg, pu, int(ld_d), _stream(stream)))
 
 
 def uniquan_gemm_block_loss_ws(T, C) -> int:

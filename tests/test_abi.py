@@ -206,6 +206,17 @@ def test_block_entry_validation(L):
     assert uq.uniquan_gemm_block_loss_ws(8192, 4096) == 512
     assert L.uniquan_gemm_block_loss(8, 12, 8, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 64, FAKE, None) == uq.UQ_EINVAL
     assert L.uniquan_gemm_block_loss(8192, 4096, 64, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 10, FAKE, None) == uq.UQ_EINVAL
+    rg = L.uniquan_gemm_nt_residual
+    assert rg(4, 12, 8, FAKE, FAKE, FAKE, FAKE, None) == uq.UQ_EINVAL     # N % 8
+    assert rg(4, 8, 8, FAKE, FAKE, ODD, FAKE, None) == uq.UQ_EINVAL       # R alignment
+    assert rg(4, 8, 8, FAKE, FAKE, FAKE, None, None) == uq.UQ_EINVAL      # out required
+    sb = L.uniquan_gemm_silu_bwd
+    assert sb(64, 36, 64, FAKE, FAKE, 2.0, FAKE, FAKE, FAKE, FAKE, 0, None) == uq.UQ_EINVAL     # I % 8
+    assert sb(64, 64, 48, FAKE, FAKE, 2.0, FAKE, FAKE, FAKE, FAKE, 0, None) == uq.UQ_EINVAL     # K % 32
+    assert sb(64, 64, 64, FAKE, FAKE, 2.0, FAKE, FAKE, FAKE, FAKE, 56, None) == uq.UQ_EINVAL    # ld_d >= I
+    assert "ld_d=56" in uq.last_error()
+    assert sb(64, 64, 64, FAKE, FAKE, 2.0, FAKE, FAKE, FAKE, FAKE, 130, None) == uq.UQ_EINVAL   # ld_d % 4
+    assert sb(64, 64, 64, FAKE, FAKE, 2.0, FAKE, FAKE, FAKE, ODD, 128, None) == uq.UQ_EINVAL    # dU alignment
     g = L.uniquan_gemm
     assert g(8, 8, 32, FAKE, 2, FAKE, 0, FAKE, F, 1.0, None) == uq.UQ_EINVAL
     assert g(8, 8, 48, FAKE, 1, FAKE, 0, FAKE, F, 1.0, None) == uq.UQ_EINVAL   # K-slow needs K % 32 == 0

@@ -147,19 +147,48 @@ def test_gemm_swiglu_matches_products_then_silu(T, I, K):
     assert torch.equal(bits(G), bits(G0)) and torch.equal(bits(U), bits(U0)) and torch.equal(bits(H), bits(H0))
 
 
+@pytest.mark.parametrize("M,N,K", [(264, 360, 96), (600, 1056, 72), (1000, 4096, 512), (8192, 4096, 4096)])
+def test_gemm_nt_residual(M, N, K):
+    """out = R + A B^T (the output projection with the first residual in its
+    store) equals uniquan_gemm_nt (fp32 out) followed by the fp32 sum, bit for
+    bit, on every kernel shape (128-, 256 x 128- and 256 x 256-row tiles, K a
+    multiple of 32 or not); also in place (out = R)."""
+    rs = np.random.default_rng(M + N + K)
+    A = dev(bfr(rs.standard_normal((M, K))), torch.bfloat16)
+    B = dev(bfr(rs.standard_normal((N, K)) * 0.1), torch.bfloat16)
+    R = dev(rs.standard_normal((M, N)) * 3.0, torch.float32)
+    P = torch.full((M, N), float("nan"), device="cuda")
+    uq.uniquan_gemm_nt(M, N, K, A, B, P)
+    out = torch.full((M, N), float("nan"), device="cuda")
+    uq.uniquan_gemm_nt_residual(M, N, K, A, B, R, out)
+    R2 = R.clone()
+    uq.uniquan_gemm_nt_residual(M, N, K, A, B, R2, R2)
+    ref = R + P
+    torch.cuda.synchronize()
+    bits = lambda t: t.view(torch.int32)
+    assert torch.equal(bits(out), bits(ref)) and torch.equal(bits(R2), bits(ref))
+
+
+@pytest.mark.parametrize("stacked", [False, True])
 @pytest.mark.parametrize("T,I,K", [(264, 360, 96), (600, 1056, 64), (8192, 11008, 128)])
-def test_gemm_silu_bwd_matches_product_then_silu_bwd(T, I, K):
+def test_gemm_silu_bwd_matches_product_then_silu_bwd(T, I, K, stacked):
     """dH = 2 E W_d (W_d stored [K, I]) with the SiLU product's backward in the
     product's store equals uniquan_gemm (bf16 dH) followed by
-    uniquan_silu_mul_bwd, bit for bit (ragged shapes, the 7B width)."""
+    uniquan_silu_mul_bwd, bit for bit (ragged shapes, the 7B width); stacked:
+    dG and dU side by side in one [T, 2I] array (rows 2I apart)."""
     rs = np.random.default_rng(T * 3 + I + K)
     E = dev(bfr(rs.standard_normal((T, K))), torch.bfloat16)
     Wd = dev(bfr(rs.standard_normal((K, I)) * 0.2), torch.bfloat16)
     G = dev(bfr(rs.standard_normal((T, I)) * 2.0), torch.bfloat16)
     U = dev(bfr(rs.standard_normal((T, I))), torch.bfloat16)
     e = lambda: torch.full((T, I), float("nan"), device="cuda", dtype=torch.bfloat16)
-    dG, dU = e(), e()
-    uq.uniquan_gemm_silu_bwd(T, I, K, E, Wd, 2.0, G, U, dG, dU)
+    if stacked:
+        dGU = torch.full((T, 2 * I), float("nan"), device="cuda", dtype=torch.bfloat16)
+        dG, dU = dGU[:, :I], dGU[:, I:]
+        uq.uniquan_gemm_silu_bwd(T, I, K, E, Wd, 2.0, G, U, dG, dU, ld_d=2 * I)
+    else:
+        dG, dU = e(), e()
+        uq.uniquan_gemm_silu_bwd(T, I, K, E, Wd, 2.0, G, U, dG, dU)
     dH0, dG0, dU0 = e(), e(), e()
     uq.uniquan_gemm(T, I, K, E, 0, Wd, 1, dH0, 2.0)
     uq.uniquan_silu_mul_bwd(dH0, G, U, dG0, dU0)
@@ -190,19 +219,24 @@ def test_add_rmsnorm(T, C):
     within_bf16(host(Z2), zref2, 1e-6 * np.abs(zref2).max(), "Z without A")
 
 
+@pytest.mark.parametrize("two", [True, False])
 @pytest.mark.parametrize("T,C", [(7, 16), (33, 512), (33, 1024), (9, 2048), (64, 4096)])
-def test_rmsnorm_bwd(T, C):
+def test_rmsnorm_bwd(T, C, two):
+    """two: the gradient of Z given as two summed parts (dZa + dZb); else one (dZb NULL)."""
     rs = np.random.default_rng(T + C)
     X = rs.standard_normal((T, C))
     g = 1.0 + 0.2 * rs.standard_normal(C)
     dZa, dZb = rs.standard_normal((T, C)), rs.standard_normal((T, C))
+    if not two:
+        dZb = np.zeros((T, C))
     E = bfr(rs.standard_normal((T, C)))
     _, rref = D.rmsnorm(X, g)
     r32 = rref[:, 0].astype(F32)
     dR = torch.empty(T, C, dtype=torch.bfloat16, device="cuda")
     dRf = torch.empty(T, C, device="cuda")
-    uq.uniquan_rmsnorm_bwd(T, C, dev(dZa, torch.float32), dev(dZb, torch.float32), dev(X, torch.float32),
-                           dev(g, torch.float32), dev(r32, torch.float32), dev(E, torch.bfloat16), 2.0, dR, dRf)
+    uq.uniquan_rmsnorm_bwd(T, C, dev(dZa, torch.float32), dev(dZb, torch.float32) if two else None,
+                           dev(X, torch.float32), dev(g, torch.float32), dev(r32, torch.float32),
+                           dev(E, torch.bfloat16), 2.0, dR, dRf)
     torch.cuda.synchronize()
     ref = 2.0 * E + D.rmsnorm_bwd(dZa.astype(F32).astype(np.float64) + dZb.astype(F32).astype(np.float64),
                                   X.astype(F32).astype(np.float64), g.astype(F32).astype(np.float64),
