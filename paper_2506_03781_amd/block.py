@@ -141,7 +141,9 @@ class DecoderBlock:
     by H / n_kv query heads; n_kv = H by default), and the SiLU-gated MLP.
     The seven matrices are QuantMatrix objects (q, o [C, C]; k, v
     [n_kv d, C]; g, u [I, C]; d [C, I]); g1, g2 are the norms' weights (not
-    trained).
+    trained).  The block re-seats the W_hat and G arrays of g and u as the
+    two halves of stacked [2I, C] arrays (their values kept), so that the
+    backpropagation reads and writes both in one product each.
 
     ``prepare(X)`` computes the full-precision block's output on the
     full-precision input X (the target); ``set_input(Xhat)`` gives the
