@@ -545,7 +545,10 @@ uq_status uniquan_rmsnorm_bwd(int64_t T, int64_t C, const float* dZa,
  * uniquan_rope_merge -- the inverse layout change (head-major in with the
  * same slot order, token-major bf16 out), rotating by minus the angle when
  * rotate != 0; the input holds nsum stacked [H, T, d] partials that are
- * summed first (the gradient of a shared key/value head, nsum = group size).
+ * summed first (the gradient of a shared key/value head, nsum = group size);
+ * the output rows are ld_out >= H d elements apart (0 means H d: the key and
+ * value gradients of grouped-query attention side by side in one [T, 2 H d]
+ * array, the operand of their stacked weight-gradient product).
  */
 uq_status uniquan_rope_split(int64_t T, int H, int d, int L, int group,
                              const void* in, int in_dtype, int rotate,
@@ -572,7 +575,7 @@ uq_status uniquan_gemm_heads(int64_t T, int H, int64_t K, const uint16_t* A,
                              const float* cs, uint16_t* out, void* stream);
 uq_status uniquan_rope_merge(int64_t T, int H, int d, int L, int group,
                              int nsum, const void* in, int in_dtype, int rotate,
-                             uint16_t* out, void* stream);
+                             uint16_t* out, int64_t ld_out, void* stream);
 
 /*
  * uniquan_softmax_causal -- for each row r < rows of S [rows, L] (fp32, row

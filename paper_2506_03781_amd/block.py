@@ -143,7 +143,8 @@ class DecoderBlock:
     [n_kv d, C]; g, u [I, C]; d [C, I]); g1, g2 are the norms' weights (not
     trained).  The block re-seats the W_hat and G arrays of g and u as the
     two halves of stacked [2I, C] arrays (their values kept), so that the
-    backpropagation reads and writes both in one product each.
+    backpropagation reads and writes both in one product each; with
+    grouped-query attention, the G arrays of k and v likewise.
 
     ``prepare(X)`` computes the full-precision block's output on the
     full-precision input X (the target); ``set_input(Xhat)`` gives the
@@ -185,7 +186,16 @@ class DecoderBlock:
         self.Kf = e(T, Ckv, **f32)
         self.r1, self.r2 = e(T, **f32), e(T, **f32)
         (self.Z1, self.O, self.Z2, self.E, self.dA, self.dO, self.dQ) = (e(T, C, **b16) for _ in range(7))
-        self.Vb, self.dK, self.dV = (e(T, Ckv, **b16) for _ in range(3))
+        self.Vb = e(T, Ckv, **b16)
+        if self.grp > 1:
+            # grouped-query: the key and value gradients side by side in one
+            # [T, 2 Ckv] array and dL/dWhat_k; dL/dWhat_v stacked [2 Ckv, C], so
+            # that their weight gradients are one product that fills the GPU
+            self.dKV = e(T, 2 * Ckv, **b16)
+            self.dK, self.dV = self.dKV[:, :Ckv], self.dKV[:, Ckv:]
+            self.G_kv = self._stack(mats["k"], mats["v"], "G")
+        else:
+            self.dK, self.dV = (e(T, Ckv, **b16) for _ in range(2))
         # query heads in grouped slot order (see uniquan_rope_split), key/value heads plain
         self.Qh = e(B, L, d, **b16)
         self.Kh, self.Vh = e(Bkv, L, d, **b16), e(Bkv, L, d, **b16)
@@ -356,13 +366,18 @@ class DecoderBlock:
         else:
             uq.uniquan_attn_bwd(B, Bkv, L, d, self.Qh, self.Kh, self.Vh, self.O, self.dO, self.lse, sc, self.delta,
                                 self.dQ, self.dKp, self.dVp, tok_seqs=self.n_seq, group=grp, cs=self.rope_cs)
-            uq.uniquan_rope_merge(T, Hkv, d, L, self.dKp, self.dK, rotate=True, nsum=grp)
-            uq.uniquan_rope_merge(T, Hkv, d, L, self.dVp, self.dV, rotate=False, nsum=grp)
+            uq.uniquan_rope_merge(T, Hkv, d, L, self.dKp, self.dK, rotate=True, nsum=grp, ld_out=2 * Ckv)
+            uq.uniquan_rope_merge(T, Hkv, d, L, self.dVp, self.dV, rotate=False, nsum=grp, ld_out=2 * Ckv)
         uq.uniquan_gemm(C, C, T, self.dQ, 1, self.Z1, 1, m["q"].G)
         done("q")
-        uq.uniquan_gemm(Ckv, C, T, self.dK, 1, self.Z1, 1, m["k"].G)
+        if grp > 1:
+            for n, off in (("k", 0), ("v", Ckv)):
+                assert m[n].G.data_ptr() == self.G_kv[off].data_ptr(), "dL/dWhat of k and v must stay stacked"
+            uq.uniquan_gemm(2 * Ckv, C, T, self.dKV, 1, self.Z1, 1, self.G_kv)
+        else:
+            uq.uniquan_gemm(Ckv, C, T, self.dK, 1, self.Z1, 1, m["k"].G)
+            uq.uniquan_gemm(Ckv, C, T, self.dV, 1, self.Z1, 1, m["v"].G)
         done("k")
-        uq.uniquan_gemm(Ckv, C, T, self.dV, 1, self.Z1, 1, m["v"].G)
         done("v")
 
     def update(self, lr_f=0.005, lr_b=0.0005, keep_grads=False):

@@ -585,16 +585,19 @@ uq_status uniquan_gemm_heads(int64_t T, int H, int64_t K, const uint16_t* A, con
 }
 
 uq_status uniquan_rope_merge(int64_t T, int H, int d, int L, int group, int nsum, const void* in, int in_dtype,
-                             int rotate, uint16_t* out, void* stream) {
+                             int rotate, uint16_t* out, int64_t ld_out, void* stream) {
   const char* fn = "uniquan_rope_merge";
   const uq_status c = check_heads(fn, T, H, d, L, in_dtype);
   if (c != UQ_OK) return c;
   if (group < 1 || H % group != 0) return fail(UQ_EINVAL, "%s: group=%d must divide H=%d", fn, group, H);
   if (nsum < 1 || nsum > 256 || nsum * T * H * d >= (int64_t(1) << 40))
     return fail(UQ_EINVAL, "%s: nsum=%d must be in 1..256", fn, nsum);
+  if (ld_out == 0) ld_out = int64_t(H) * d;
+  if (ld_out < int64_t(H) * d || T * ld_out >= (int64_t(1) << 40))
+    return fail(UQ_EINVAL, "%s: ld_out=%lld must be >= H d=%lld", fn, (long long)ld_out, (long long)(int64_t(H) * d));
   REQ_PTR(in, in_dtype == UQ_F32 ? 4 : 2); REQ_PTR(out, 2);
   return hip_status(fn, uq::launch_rope_merge(T, H, d, L, group, nsum, in, in_dtype == UQ_F32, rotate != 0, out,
-                                              static_cast<hipStream_t>(stream)));
+                                              ld_out, static_cast<hipStream_t>(stream)));
 }
 
 uq_status uniquan_softmax_causal(int64_t rows, int L, const float* S, uint16_t* P, void* stream) {

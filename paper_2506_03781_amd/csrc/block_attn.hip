@@ -394,7 +394,8 @@ __global__ __launch_bounds__(256) void rope_split_vec_kernel(int64_t T, int H, i
 
 template <bool IN_F32, bool ROT>
 __global__ __launch_bounds__(256) void rope_merge_vec_kernel(int64_t T, int H, int d, int L, int perm, int nsum,
-                                                             const void* __restrict__ in, uint16_t* __restrict__ out) {
+                                                             const void* __restrict__ in, uint16_t* __restrict__ out,
+                                                             int64_t ldo) {
   __shared__ float2 cs[RT * RT_MAX_HD];
   const int hd = d >> 1, cph = hd / 8, cpt = H * cph;
   const int64_t t0 = int64_t(blockIdx.x) * RT;
@@ -429,19 +430,20 @@ __global__ __launch_bounds__(256) void rope_merge_vec_kernel(int64_t T, int H, i
         y2[e] = x2[e];
       }
     }
-    const int64_t dst = t * (int64_t(H) * d) + int64_t(h) * d + i;
+    const int64_t dst = t * ldo + int64_t(h) * d + i;
     store8(out + dst, y1);
     store8(out + dst + hd, y2);
   }
 }
 
 // Head-major [nsum, H, T, d] (fp32 or bf16; head h at head_slot(h)) ->
-// token-major bf16 [T, C]: the nsum stacked partials are summed (the
-// gradient of a key/value head shared by a group), then rotated by minus
-// the position's angle when ROT (the inverse rotation).
+// token-major bf16 [T, C] with rows ldo elements apart: the nsum stacked
+// partials are summed (the gradient of a key/value head shared by a group),
+// then rotated by minus the position's angle when ROT (the inverse rotation).
 template <bool IN_F32, bool ROT>
 __global__ __launch_bounds__(256) void rope_merge_kernel(int64_t T, int H, int d, int L, int perm, int nsum,
-                                                         const void* __restrict__ in, uint16_t* __restrict__ out) {
+                                                         const void* __restrict__ in, uint16_t* __restrict__ out,
+                                                         int64_t ldo) {
   const int hd = d >> 1;
   const int64_t n = T * H * hd;
   const int64_t idx = int64_t(blockIdx.x) * 256 + threadIdx.x;
@@ -469,7 +471,7 @@ __global__ __launch_bounds__(256) void rope_merge_kernel(int64_t T, int H, int d
     y1 = x1 * c + x2 * s;
     y2 = x2 * c - x1 * s;
   }
-  const int64_t dst = t * (int64_t(H) * d) + int64_t(h) * d + i;
+  const int64_t dst = t * ldo + int64_t(h) * d + i;
   out[dst] = to_bf(y1);
   out[dst + hd] = to_bf(y2);
 }
@@ -700,31 +702,34 @@ hipError_t launch_rope_split(int64_t T, int H, int d, int L, int perm, const voi
 }
 
 hipError_t launch_rope_merge(int64_t T, int H, int d, int L, int perm, int nsum, const void* in, int in_f32,
-                             int rotate, uint16_t* out, hipStream_t st) {
-  if (rope_vec_ok(d, in, out)) {
+                             int rotate, uint16_t* out, int64_t ldo, hipStream_t st) {
+  if (ldo == 0) ldo = int64_t(H) * d;
+  if (rope_vec_ok(d, in, out) && ldo % 8 == 0) {
     const dim3 grid(unsigned((T + RT - 1) / RT));
     if (in_f32 && rotate)
-      hipLaunchKernelGGL((rope_merge_vec_kernel<true, true>), grid, dim3(256), 0, st, T, H, d, L, perm, nsum, in, out);
+      hipLaunchKernelGGL((rope_merge_vec_kernel<true, true>), grid, dim3(256), 0, st, T, H, d, L, perm, nsum, in, out,
+                         ldo);
     else if (in_f32)
       hipLaunchKernelGGL((rope_merge_vec_kernel<true, false>), grid, dim3(256), 0, st, T, H, d, L, perm, nsum, in,
-                         out);
+                         out, ldo);
     else if (rotate)
       hipLaunchKernelGGL((rope_merge_vec_kernel<false, true>), grid, dim3(256), 0, st, T, H, d, L, perm, nsum, in,
-                         out);
+                         out, ldo);
     else
       hipLaunchKernelGGL((rope_merge_vec_kernel<false, false>), grid, dim3(256), 0, st, T, H, d, L, perm, nsum, in,
-                         out);
+                         out, ldo);
     return hipGetLastError();
   }
   const dim3 grid(unsigned((T * H * (d / 2) + 255) / 256));
   if (in_f32 && rotate)
-    hipLaunchKernelGGL((rope_merge_kernel<true, true>), grid, dim3(256), 0, st, T, H, d, L, perm, nsum, in, out);
+    hipLaunchKernelGGL((rope_merge_kernel<true, true>), grid, dim3(256), 0, st, T, H, d, L, perm, nsum, in, out, ldo);
   else if (in_f32)
-    hipLaunchKernelGGL((rope_merge_kernel<true, false>), grid, dim3(256), 0, st, T, H, d, L, perm, nsum, in, out);
+    hipLaunchKernelGGL((rope_merge_kernel<true, false>), grid, dim3(256), 0, st, T, H, d, L, perm, nsum, in, out, ldo);
   else if (rotate)
-    hipLaunchKernelGGL((rope_merge_kernel<false, true>), grid, dim3(256), 0, st, T, H, d, L, perm, nsum, in, out);
+    hipLaunchKernelGGL((rope_merge_kernel<false, true>), grid, dim3(256), 0, st, T, H, d, L, perm, nsum, in, out, ldo);
   else
-    hipLaunchKernelGGL((rope_merge_kernel<false, false>), grid, dim3(256), 0, st, T, H, d, L, perm, nsum, in, out);
+    hipLaunchKernelGGL((rope_merge_kernel<false, false>), grid, dim3(256), 0, st, T, H, d, L, perm, nsum, in, out,
+                       ldo);
   return hipGetLastError();
 }
 

@@ -231,7 +231,7 @@ hipError_t launch_rope_table(int L, int d, float* cs, hipStream_t st);
 hipError_t launch_rope_split(int64_t T, int H, int d, int L, int perm, const void* in, int in_f32, int rotate,
                              uint16_t* out, hipStream_t st);
 hipError_t launch_rope_merge(int64_t T, int H, int d, int L, int perm, int nsum, const void* in, int in_f32,
-                             int rotate, uint16_t* out, hipStream_t st);
+                             int rotate, uint16_t* out, int64_t ldo, hipStream_t st);
 hipError_t launch_softmax_causal(int64_t rows, int L, const float* S, uint16_t* P, hipStream_t st);
 hipError_t launch_softmax_bwd(int64_t rows, int L, const float* dP, const uint16_t* P, uint16_t* dS, hipStream_t st);
 hipError_t launch_transpose_batched(int64_t B, int64_t R, int64_t C, const uint16_t* in, uint16_t* out,

@@ -77,7 +77,7 @@ _SIGS = {
     "uniquan_add_rmsnorm": ([_i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp], _i32),
     "uniquan_rmsnorm_bwd": ([_i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _f32, _vp, _vp, _vp], _i32),
     "uniquan_rope_split": ([_i64, _i32, _i32, _i32, _i32, _vp, _i32, _i32, _vp, _vp], _i32),
-    "uniquan_rope_merge": ([_i64, _i32, _i32, _i32, _i32, _i32, _vp, _i32, _i32, _vp, _vp], _i32),
+    "uniquan_rope_merge": ([_i64, _i32, _i32, _i32, _i32, _i32, _vp, _i32, _i32, _vp, _i64, _vp], _i32),
     "uniquan_softmax_causal": ([_i64, _i32, _vp, _vp, _vp], _i32),
     "uniquan_softmax_causal_bwd": ([_i64, _i32, _vp, _vp, _vp, _vp], _i32),
     "uniquan_transpose_bf16_batched": ([_i64, _i64, _i64, _vp, _vp, _vp], _i32),
@@ -564,11 +564,13 @@ def uniquan_rope_split(T, H, d, L, x, out, rotate=True, group=1, stream=None):
                                     _p(out, n, _B, "out"), _stream(stream)))
 
 
-def uniquan_rope_merge(T, H, d, L, x, out, rotate=True, group=1, nsum=1, stream=None):
-    """Head-major x [nsum, H, T, d] (fp32 or bf16) -> token-major bf16 out [T, H d], partials summed."""
+def uniquan_rope_merge(T, H, d, L, x, out, rotate=True, group=1, nsum=1, stream=None, ld_out=0):
+    """Head-major x [nsum, H, T, d] (fp32 or bf16) -> token-major bf16 out [T, H d], partials summed;
+    with ld_out, out is a [T, H d] view whose rows are ld_out elements apart."""
     n = T * H * d
+    po = _p_rows(out, T, H * d, ld_out, _B, "out") if ld_out else _p(out, n, _B, "out")
     _check(lib().uniquan_rope_merge(T, H, d, L, int(group), int(nsum), _p(x, n * nsum, _W, "in"), _dt(x),
-                                    int(bool(rotate)), _p(out, n, _B, "out"), _stream(stream)))
+                                    int(bool(rotate)), po, int(ld_out), _stream(stream)))
 
 
 def uniquan_softmax_causal(rows, L, S, P, stream=None):

@@ -316,8 +316,10 @@ def test_decoder_entry_validation(L):
     assert L.uniquan_rope_split(6, 2, 4, 4, 1, FAKE, F, 1, FAKE, None) == uq.UQ_EINVAL       # L does not divide T
     assert L.uniquan_rope_split(6, 2, 3, 3, 1, FAKE, F, 1, FAKE, None) == uq.UQ_EINVAL       # odd d
     assert L.uniquan_rope_split(6, 4, 4, 3, 3, FAKE, F, 1, FAKE, None) == uq.UQ_EINVAL       # group does not divide H
-    assert L.uniquan_rope_merge(6, 2, 4, 3, 1, 1, FAKE, 9, 1, FAKE, None) == uq.UQ_EINVAL    # bad dtype
-    assert L.uniquan_rope_merge(6, 2, 4, 3, 1, 0, FAKE, F, 1, FAKE, None) == uq.UQ_EINVAL    # nsum
+    assert L.uniquan_rope_merge(6, 2, 4, 3, 1, 1, FAKE, 9, 1, FAKE, 0, None) == uq.UQ_EINVAL    # bad dtype
+    assert L.uniquan_rope_merge(6, 2, 4, 3, 1, 0, FAKE, F, 1, FAKE, 0, None) == uq.UQ_EINVAL    # nsum
+    assert L.uniquan_rope_merge(6, 2, 4, 3, 1, 1, FAKE, F, 1, FAKE, 6, None) == uq.UQ_EINVAL    # ld_out < H d
+    assert "ld_out=6" in uq.last_error()
     assert L.uniquan_softmax_causal(10, 4, FAKE, FAKE, None) == uq.UQ_EINVAL
     assert L.uniquan_softmax_causal_bwd(8, 4, FAKE, None, FAKE, None) == uq.UQ_EINVAL
     assert L.uniquan_transpose_bf16_batched(0, 4, 4, FAKE, FAKE, None) == uq.UQ_EINVAL

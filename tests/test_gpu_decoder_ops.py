@@ -310,6 +310,28 @@ def test_rope_vector_path_matches_pair_path(n_seq, L, H, d, G, nsum):
             run(uq.uniquan_rope_merge, y, T * C, rotate=rot, group=G, nsum=nsum)
 
 
+@pytest.mark.parametrize("n_seq,L,H,d,nsum", [(2, 64, 8, 128, 4), (1, 40, 3, 16, 2)])
+def test_rope_merge_strided_output(n_seq, L, H, d, nsum):
+    """Two merges writing side by side into one [T, 2 H d] array (rows 2 H d
+    apart: the key and value gradients of grouped-query attention) equal the
+    merges into contiguous [T, H d] arrays, bit for bit, on the chunk kernel
+    (16-byte aligned halves) and the pair kernel (d = 16 with H = 3: odd halves)."""
+    T, C = n_seq * L, H * d
+    rs = np.random.default_rng(T + H + d + nsum)
+    yk = dev(rs.standard_normal((nsum, H, T, d)).astype(F32), torch.float32)
+    yv = dev(rs.standard_normal((nsum, H, T, d)).astype(F32), torch.float32)
+    both = torch.full((T, 2 * C), float("nan"), dtype=torch.bfloat16, device="cuda")
+    uq.uniquan_rope_merge(T, H, d, L, yk, both[:, :C], rotate=True, nsum=nsum, ld_out=2 * C)
+    uq.uniquan_rope_merge(T, H, d, L, yv, both[:, C:], rotate=False, nsum=nsum, ld_out=2 * C)
+    rk = torch.empty(T, C, dtype=torch.bfloat16, device="cuda")
+    rv = torch.empty(T, C, dtype=torch.bfloat16, device="cuda")
+    uq.uniquan_rope_merge(T, H, d, L, yk, rk, rotate=True, nsum=nsum)
+    uq.uniquan_rope_merge(T, H, d, L, yv, rv, rotate=False, nsum=nsum)
+    torch.cuda.synchronize()
+    bits = lambda t: t.contiguous().view(torch.int16)
+    assert torch.equal(bits(both[:, :C]), bits(rk)) and torch.equal(bits(both[:, C:]), bits(rv))
+
+
 @pytest.mark.parametrize("R,C", [(8, 8), (72, 200), (2048, 136), (136, 4096)])
 def test_transpose_2d_edges(R, C):
     """uniquan_transpose_bf16 on shapes with partial 64 x 64 tiles: bit-exact."""
