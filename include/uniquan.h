@@ -563,15 +563,18 @@ uq_status uniquan_rope_split(int64_t T, int H, int d, int L, int group,
  * head split (and rotation) of uniquan_rope_split folded into the product's
  * store (Algorithm 1's forward through the attention module):
  *     Y = A W^T  (A [T x K] bf16, W [H 128 x K] bf16, fp32 accumulation),
- *     out = uniquan_rope_split(Y) with d = 128, group and rotate as there,
+ *     out = uniquan_rope_split(Y) with d = 128 and group as there, the
+ *           heads h < n_rot rotated (n_rot = 0: none, >= H: all; rotating
+ *           only the leading heads, e.g. the keys of a stacked key/value
+ *           product [W_k; W_v], needs group 1),
  * out bf16 head-major [H, T, 128], bit for bit the result of
- * uniquan_gemm_nt (fp32 out) followed by uniquan_rope_split.  cs from
- * uniquan_rope_table(L, 128) (read only when rotate != 0).  K a multiple of
- * 32, L divides T; out 8-byte and cs 32-byte aligned.
+ * uniquan_gemm_nt (fp32 out) followed by uniquan_rope_split of each head
+ * range.  cs from uniquan_rope_table(L, 128) (read only when n_rot > 0).
+ * K a multiple of 32, L divides T; out 8-byte and cs 32-byte aligned.
  */
 uq_status uniquan_rope_table(int L, int d, float* cs, void* stream);
 uq_status uniquan_gemm_heads(int64_t T, int H, int64_t K, const uint16_t* A,
-                             const uint16_t* W, int L, int group, int rotate,
+                             const uint16_t* W, int L, int group, int n_rot,
                              const float* cs, uint16_t* out, void* stream);
 uq_status uniquan_rope_merge(int64_t T, int H, int d, int L, int group,
                              int nsum, const void* in, int in_dtype, int rotate,

@@ -144,7 +144,7 @@ class DecoderBlock:
     trained).  The block re-seats the W_hat and G arrays of g and u as the
     two halves of stacked [2I, C] arrays (their values kept), so that the
     backpropagation reads and writes both in one product each; with
-    grouped-query attention, the G arrays of k and v likewise.
+    grouped-query attention, the W_hat and G arrays of k and v likewise.
 
     ``prepare(X)`` computes the full-precision block's output on the
     full-precision input X (the target); ``set_input(Xhat)`` gives the
@@ -189,16 +189,21 @@ class DecoderBlock:
         self.Vb = e(T, Ckv, **b16)
         if self.grp > 1:
             # grouped-query: the key and value gradients side by side in one
-            # [T, 2 Ckv] array and dL/dWhat_k; dL/dWhat_v stacked [2 Ckv, C], so
-            # that their weight gradients are one product that fills the GPU
+            # [T, 2 Ckv] array and What_k; What_v and dL/dWhat_k; dL/dWhat_v
+            # stacked [2 Ckv, C], so that their projection and their weight
+            # gradients are one product each that fills the GPU
             self.dKV = e(T, 2 * Ckv, **b16)
             self.dK, self.dV = self.dKV[:, :Ckv], self.dKV[:, Ckv:]
+            self.What_kv = self._stack(mats["k"], mats["v"], "W_hat")
             self.G_kv = self._stack(mats["k"], mats["v"], "G")
         else:
             self.dK, self.dV = (e(T, Ckv, **b16) for _ in range(2))
         # query heads in grouped slot order (see uniquan_rope_split), key/value heads plain
         self.Qh = e(B, L, d, **b16)
-        self.Kh, self.Vh = e(Bkv, L, d, **b16), e(Bkv, L, d, **b16)
+        # key heads then value heads in one array: one stacked projection
+        # [W_k; W_v] writes both (keys rotated) where it fills the GPU
+        self.KVh = e(2 * Bkv, L, d, **b16)
+        self.Kh, self.Vh = self.KVh[:Bkv], self.KVh[Bkv:]
         # attention rows: base-2 log-sum-exp of the scores, the softmax backward's row term
         self.lse, self.delta = e(B, L, **f32), e(B, L, **f32)
         # cos and sin of every rotary angle of a sequence, for the projections'
@@ -242,8 +247,12 @@ class DecoderBlock:
         uq.uniquan_add_rmsnorm(T, C, X, None, self.g1, None, self.Z1, self.r1)
         Hkv, Ckv, Bkv, grp = self.Hkv, self.Ckv, self.Bkv, self.grp
         self._project_heads(W["q"], H, self.Qh, grp, True, self.Qf)
-        self._project_heads(W["k"], Hkv, self.Kh, 1, True, self.Kf)
-        self._project_heads(W["v"], Hkv, self.Vh, 1, False, self.Vb)
+        Wkv = self._stacked_kv(W)
+        if Wkv is not None:
+            uq.uniquan_gemm_heads(T, 2 * Hkv, C, self.Z1, Wkv, L, self.KVh, cs=self.rope_cs, n_rot=Hkv)
+        else:
+            self._project_heads(W["k"], Hkv, self.Kh, 1, True, self.Kf)
+            self._project_heads(W["v"], Hkv, self.Vh, 1, False, self.Vb)
         # causal attention with the score tiles on chip (query batch g Bkv + c uses key/value batch c)
         # (O written token-major: the merge of the heads is in the kernel's store)
         uq.uniquan_attn_fwd(B, Bkv, L, d, self.Qh, self.Kh, self.Vh, sc, self.O, self.lse,
@@ -257,6 +266,17 @@ class DecoderBlock:
                                        self.loss)
         else:
             uq.uniquan_gemm_nt(T, C, I, self.Hm, W["d"], self.M32)
+
+    def _stacked_kv(self, W):
+        """[W_k; W_v] as one [2 Ckv, C] array when W's key and value weights are
+        the stacked What (grouped-query) and the stacked product fills the GPU
+        with 256 x 256 tiles, else None (two products)."""
+        if self.grp == 1 or ((self.T + 255) // 256) * ((2 * self.Ckv + 255) // 256) < 256:
+            return None
+        kv = self.What_kv
+        if W["k"].data_ptr() != kv.data_ptr() or W["v"].data_ptr() != kv[self.Ckv].data_ptr():
+            return None
+        return kv
 
     def _project_heads(self, Wm, n_heads, out, group, rotate, tmp):
         """out [n_heads, T, d] = the head split (rotated when rotate) of Z1 Wm^T:

@@ -567,7 +567,7 @@ uq_status uniquan_rope_table(int L, int d, float* cs, void* stream) {
 }
 
 uq_status uniquan_gemm_heads(int64_t T, int H, int64_t K, const uint16_t* A, const uint16_t* W, int L, int group,
-                             int rotate, const float* cs, uint16_t* out, void* stream) {
+                             int n_rot, const float* cs, uint16_t* out, void* stream) {
   const char* fn = "uniquan_gemm_heads";
   if (T < 1 || H < 1 || K < 1 || L < 1) return fail(UQ_EINVAL, "%s: T, H, K, L must be >= 1", fn);
   if (K % 32 != 0) return fail(UQ_EINVAL, "%s: K=%lld must be a multiple of 32", fn, (long long)K);
@@ -577,10 +577,14 @@ uq_status uniquan_gemm_heads(int64_t T, int H, int64_t K, const uint16_t* A, con
   if (N >= (int64_t(1) << 26) || K >= (int64_t(1) << 31) || T >= (int64_t(1) << 31) ||
       T * K >= (int64_t(1) << 40) || N * K >= (int64_t(1) << 40) || T * N >= (int64_t(1) << 40))
     return fail(UQ_EUNSUPPORTED, "%s: shape too large", fn);
+  if (n_rot < 0) return fail(UQ_EINVAL, "%s: n_rot=%d must be >= 0", fn, n_rot);
+  if (n_rot > H) n_rot = H;
+  if (n_rot > 0 && group > 1 && n_rot < H)
+    return fail(UQ_EINVAL, "%s: rotating only some heads needs group 1", fn);
   REQ_PTR(A, 16); REQ_PTR(W, 16); REQ_PTR(out, 8);
-  if (rotate) REQ_PTR(cs, 32);
-  uq::GemmLaunch g{A, W, T, N, K, rotate ? uq::EPI_HEADS_ROT : uq::EPI_HEADS, nullptr, out, nullptr, 1.0f};
-  g.heads = uq::HeadsParams{cs, L, H, group};
+  if (n_rot) REQ_PTR(cs, 32);
+  uq::GemmLaunch g{A, W, T, N, K, n_rot ? uq::EPI_HEADS_ROT : uq::EPI_HEADS, nullptr, out, nullptr, 1.0f};
+  g.heads = uq::HeadsParams{cs, L, H, group, n_rot};
   return hip_status(fn, uq::launch_gemm(g, static_cast<hipStream_t>(stream)));
 }
 

@@ -372,7 +372,12 @@ __device__ __forceinline__ void epilogue(const GemmArgs& p, f32x16 (&acc)[FM][FN
     }
     if constexpr (EPI == EPI_HEADS || EPI == EPI_HEADS_ROT) {
       static_assert(WN == 128, "the head split needs 128-column wave tiles");
-      if (col_base < p.N) heads_strip<EPI == EPI_HEADS_ROT>(p, strip, row_base, col_base, lane);
+      if (col_base < p.N) {
+        if (EPI == EPI_HEADS_ROT && int(col_base >> 7) < p.heads.nrot)
+          heads_strip<true>(p, strip, row_base, col_base, lane);
+        else
+          heads_strip<false>(p, strip, row_base, col_base, lane);
+      }
       __builtin_amdgcn_s_waitcnt(0xC07F);  // strip reads done before the next strip overwrites it
       __builtin_amdgcn_wave_barrier();
       continue;

@@ -145,10 +145,12 @@ struct SwigluParams {
 
 // Head-split epilogue (EPI_HEADS*): position of row m is m % L; cos and sin
 // of pair i at position p in cs[p * 64 + i]; head h goes to slot
-// (h % perm) * (H / perm) + h / perm (perm > 1) or h.
+// (h % perm) * (H / perm) + h / perm (perm > 1) or h; with EPI_HEADS_ROT the
+// heads h < nrot are rotated (the keys of a stacked key/value product).
 struct HeadsParams {
   const float* cs;  // [L, 64] (cos, sin) pairs
   int L, H, perm;
+  int nrot;
 };
 
 struct GemmLaunch {

@@ -460,11 +460,13 @@ def uniquan_rope_table(L, d, cs, stream=None):
     _check(lib().uniquan_rope_table(int(L), int(d), _p(cs, L * d, _F, "cs"), _stream(stream)))
 
 
-def uniquan_gemm_heads(T, H, K, A, W, L, out, group=1, rotate=True, cs=None, stream=None):
-    """out [H, T, 128] bf16 = uniquan_rope_split(A [T, K] W [H 128, K]^T) (group, rotate as there)."""
+def uniquan_gemm_heads(T, H, K, A, W, L, out, group=1, rotate=True, cs=None, stream=None, n_rot=None):
+    """out [H, T, 128] bf16 = uniquan_rope_split(A [T, K] W [H 128, K]^T) (group, rotate as there);
+    n_rot, if given, rotates only the heads h < n_rot."""
     N = H * 128
+    nr = (H if rotate else 0) if n_rot is None else int(n_rot)
     _check(lib().uniquan_gemm_heads(T, H, K, _p(A, T * K, _B, "A"), _p(W, N * K, _B, "W"), int(L), int(group),
-                                    int(bool(rotate)), _p(cs, L * 128, _F, "cs") if rotate else None,
+                                    nr, _p(cs, L * 128, _F, "cs") if nr else None,
                                     _p(out, T * N, _B, "out"), _stream(stream)))
 
 

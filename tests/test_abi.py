@@ -203,6 +203,8 @@ def test_block_entry_validation(L):
     assert gh(512, 4, 64, FAKE, FAKE, 300, 1, 1, FAKE, FAKE, None) == uq.UQ_EINVAL   # L divides T
     assert gh(512, 4, 64, FAKE, FAKE, 512, 3, 1, FAKE, FAKE, None) == uq.UQ_EINVAL   # group divides H
     assert gh(512, 4, 64, FAKE, FAKE, 512, 1, 1, None, FAKE, None) == uq.UQ_EINVAL   # rotation needs the table
+    assert gh(512, 4, 64, FAKE, FAKE, 512, 1, -1, FAKE, FAKE, None) == uq.UQ_EINVAL  # n_rot >= 0
+    assert gh(512, 4, 64, FAKE, FAKE, 512, 2, 2, FAKE, FAKE, None) == uq.UQ_EINVAL   # some heads only: group 1
     assert uq.uniquan_gemm_block_loss_ws(8192, 4096) == 512
     assert L.uniquan_gemm_block_loss(8, 12, 8, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 64, FAKE, None) == uq.UQ_EINVAL
     assert L.uniquan_gemm_block_loss(8192, 4096, 64, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 10, FAKE, None) == uq.UQ_EINVAL

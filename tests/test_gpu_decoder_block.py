@@ -286,3 +286,37 @@ def test_decoder_block_fused_step_form(form):
     for n in qa:
         for attr in ("s", "alpha", "z_b", "codes", "W_hat"):
             assert torch.equal(getattr(qa[n], attr), getattr(qb[n], attr)), (n, attr)
+
+
+def test_decoder_block_stacked_kv_projection():
+    """Grouped-query block at a shape where the stacked key/value projection
+    ([W_k; W_v] in one product, the key heads rotated) fills the GPU (8192
+    tokens, 8 key/value heads of 128): its key/value heads, E and loss equal
+    those of the two separate projections (What_k, What_v as unstacked
+    copies), bit for bit."""
+    T_, n_seq, H_, n_kv, C_, I_ = 8192, 4, 16, 8, 2048, 256
+    rs = np.random.default_rng(11)
+    qs = {}
+    for n, (R_, Cc) in shapes_for(C_, I_, n_kv * 128).items():
+        W = O.bf16_rne((0.02 * rs.standard_normal((R_, Cc))).astype(F32))
+        q = QuantMatrix(W, np.ones((R_, Cc), F32), K, G)
+        q.init_unified(grid_G=4, alt_T=2)
+        qs[n] = q
+    g = np.ones(C_, F32)
+    blk = DecoderBlock(qs, g, g, T_, n_seq, H_, n_kv=n_kv)
+    X = torch.randn(T_, C_, device="cuda")
+    blk.prepare(X)
+    blk.set_input(X)
+    blk.quantize(uq.MAP_FULL)
+    assert blk._stacked_kv({n: q.W_hat for n, q in qs.items()}) is not None
+    blk.forward()
+    kv1, e1, l1 = blk.KVh.clone(), blk.E.clone(), blk.loss.clone()
+    W2 = {n: q.W_hat for n, q in qs.items()}
+    W2["k"], W2["v"] = W2["k"].clone(), W2["v"].clone()
+    assert blk._stacked_kv(W2) is None
+    blk._forward(W2, blk.Xhat, loss=True)
+    torch.cuda.synchronize()
+    bits = lambda t: t.contiguous().view(torch.int16)
+    assert torch.equal(bits(kv1), bits(blk.KVh)), "key/value heads"
+    assert torch.equal(bits(e1), bits(blk.E)), "E"
+    assert torch.equal(l1, blk.loss), "loss"

@@ -125,6 +125,34 @@ def test_gemm_heads_matches_product_then_split(T, H, K, L, group, rotate):
     assert np.all(np.abs(c[..., 1] - np.sin(ang)) <= 1e-6 * (1 + np.abs(ang)))
 
 
+@pytest.mark.parametrize("T,Hk,K,L", [(520, 2, 96, 260), (8192, 8, 128, 2048)])
+def test_gemm_heads_leading_rotated(T, Hk, K, L):
+    """Keys and values in one stacked product ([W_k; W_v], 2 Hk heads, the
+    first Hk rotated): the key heads equal the rotated split of the key
+    product and the value heads the plain split of the value product, bit
+    for bit (ragged rows; the 7B grouped-query shape, 8 key/value heads)."""
+    rs = np.random.default_rng(T + Hk + K + L)
+    d = 128
+    A = dev(bfr(rs.standard_normal((T, K))), torch.bfloat16)
+    Wk = dev(bfr(rs.standard_normal((Hk * d, K)) * 0.1), torch.bfloat16)
+    Wv = dev(bfr(rs.standard_normal((Hk * d, K)) * 0.1), torch.bfloat16)
+    cs = torch.empty(L, d // 2, 2, device="cuda")
+    uq.uniquan_rope_table(L, d, cs)
+    Wkv = torch.cat([Wk, Wv]).contiguous()
+    fused = torch.full((2 * Hk, T, d), float("nan"), device="cuda", dtype=torch.bfloat16)
+    uq.uniquan_gemm_heads(T, 2 * Hk, K, A, Wkv, L, fused, cs=cs, n_rot=Hk)
+    refs = []
+    for W, rot in ((Wk, True), (Wv, False)):
+        Y = torch.empty(T, Hk * d, device="cuda")
+        uq.uniquan_gemm_nt(T, Hk * d, K, A, W, Y)
+        r = torch.empty(Hk, T, d, device="cuda", dtype=torch.bfloat16)
+        uq.uniquan_rope_split(T, Hk, d, L, Y, r, rotate=rot)
+        refs.append(r)
+    torch.cuda.synchronize()
+    bits = lambda t: t.contiguous().view(torch.int16)
+    assert torch.equal(bits(fused[:Hk]), bits(refs[0])) and torch.equal(bits(fused[Hk:]), bits(refs[1]))
+
+
 @pytest.mark.parametrize("T,I,K", [(264, 352, 96), (600, 1056, 64), (8192, 11008, 128)])
 def test_gemm_swiglu_matches_products_then_silu(T, I, K):
     """The gate and up products with the SiLU product in one (interleaved
