@@ -710,7 +710,9 @@ uq_status uniquan_bcq_pack(int64_t R, int64_t C, int k, int g,
  * X [T*C] bf16 (8-byte aligned), Y [T*R] fp32 out.  Per group the kernel
  * uses sum_c sigma_i x_c = 2 P_i - S (S: the group's activation sum, P_i:
  * the sum over columns whose bit i is set), P_i from 16-entry subset-sum
- * tables of 4 activations; fp32 accumulation, deterministic order.
+ * tables of 4 activations for T <= 3 and from bf16 MFMA products of the
+ * activations with the 0/1 planes for T >= 4; fp32 accumulation,
+ * deterministic order.
  * partials_ws [partials_len] fp32 workspace of at least
  * uniquan_bcq_matmul_ws(T, R, C) floats (0: may be NULL).
  */

@@ -252,6 +252,112 @@ __global__ __launch_bounds__(256) void bcq_matmul_kernel(BcqArgs a) {
   for (int t = 0; t < T; ++t) out[int64_t(t) * a.R + r] = acc[t];
 }
 
+// The same product for larger batches on MFMA (v_mfma_f32_32x32x16_bf16):
+// P_i = X B_i^T with B_i the 0 / 1 matrix of plane i (exact in bf16) and S =
+// X 1^T, per 128-column quad, then y += sum_i (2 alpha*_i) P_i + (z* -
+// sum_i alpha*_i) S as in the table kernel.  C[m][n] is token m, row n: lane
+// l supplies token l % 32 (zero past T) and the bits of row l % 32, both at
+// columns 16 s + 8 (l / 32) .. + 8 of k-step s, and holds row l % 32 for
+// tokens 4 (l / 32) + rr in accumulator slots rr < 4 (T <= 8).  Each of the
+// 4 wavefronts takes 32 RT rows (RT 32-row tiles) of the workgroup's 128 RT;
+// with RT = 2 the grid, slabs and partial rows are the table kernel's.  The bits of a
+// fragment (8 columns of one row and plane) come from one LDS read of a
+// 256-entry table, whatever T; the table kernel's lookups grow with T.
+typedef __bf16 bf16x8b __attribute__((ext_vector_type(8)));
+typedef float f32x16b __attribute__((ext_vector_type(16)));
+
+// bits j of b (j < 8) as bf16 0.0 / 1.0 in element j: for each pair t of
+// bits, t * 0x8001 puts bit 0 at position 0 and bit 1 at position 16 (the
+// other partial products land at 1 and 15 and are masked off), and the
+// product with 0x3F80 (bf16 1.0) makes the two halves.
+__device__ __forceinline__ bf16x8b bits_bf16(uint32_t b) {
+  u32x4 d;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) d[j] = (((b >> (2 * j)) & 3u) * 0x8001u & 0x10001u) * 0x3F80u;
+  return __builtin_bit_cast(bf16x8b, d);
+}
+
+template <int K, int QPS, int RT = 2>
+__global__ __launch_bounds__(256) void bcq_mfma_kernel(BcqArgs a, int T) {
+  // the 256 bytes as 8 bf16 each, built once: one LDS read per 8 bits
+  __shared__ u32x4 tbl[256];
+  tbl[threadIdx.x] = __builtin_bit_cast(u32x4, bits_bf16(threadIdx.x));
+  __syncthreads();
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int tok = lane & 31, hk = lane >> 5;
+  const int64_t q0 = int64_t(blockIdx.y) * QPS;
+  const int nqs = int(min<int64_t>(QPS, a.nq - q0));
+  const int64_t R = a.R;
+  const int64_t rbase = int64_t(blockIdx.x) * (128 * RT) + wave * (32 * RT);
+  const int64_t pstride = a.nq * R, astride = a.gpr * R;
+  const uint32_t qpg = uint32_t(a.g) >> 7;
+  bf16x8b ones;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) ones[e] = __bf16(1.0f);
+  float y[RT][4];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) y[rt][rr] = 0.0f;
+  for (int qq = 0; qq < nqs; ++qq) {
+    const int64_t q = q0 + qq;
+    const int64_t j = int64_t(uint32_t(q) / qpg);
+    // this lane's activations for the quad's 8 k-steps (two 8-byte loads each)
+    bf16x8b xa[8];
+    const uint2* xr = reinterpret_cast<const uint2*>(a.X + int64_t(min(tok, T - 1)) * a.C + q * 128 + 8 * hk);
+#pragma unroll
+    for (int st = 0; st < 8; ++st) {
+      const uint2 lo = xr[4 * st], hi = xr[4 * st + 1];
+      const u32x4 v = {tok < T ? lo.x : 0u, tok < T ? lo.y : 0u, tok < T ? hi.x : 0u, tok < T ? hi.y : 0u};
+      xa[st] = __builtin_bit_cast(bf16x8b, v);
+    }
+    f32x16b S = {};
+#pragma unroll
+    for (int st = 0; st < 8; ++st) S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xa[st], ones, S, 0, 0, 0);
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      const int64_t r = rbase + 32 * rt + tok;
+      const int64_t rc = r < R ? r : R - 1;
+      u32x4 w[K];
+      float al[K];
+#pragma unroll
+      for (int i = 0; i < K; ++i) {
+        w[i] = a.planes[(i * a.nq + q) * R + rc];
+        al[i] = f16_to_f32(a.alpha16[i * astride + j * R + rc]);
+      }
+      const float zc0 = f16_to_f32(a.z16[j * R + rc]);
+      float asum = 0.0f;
+#pragma unroll
+      for (int i = 0; i < K; ++i) {
+        asum += al[i];
+        f32x16b P = {};
+#pragma unroll
+        for (int st = 0; st < 8; ++st) {
+          const uint32_t byte = (w[i][st >> 1] >> (16 * (st & 1) + 8 * hk)) & 0xFFu;
+          P = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xa[st], __builtin_bit_cast(bf16x8b, tbl[byte]), P, 0, 0, 0);
+        }
+        const float a2 = 2.0f * al[i];
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) y[rt][rr] += a2 * P[rr];
+      }
+      const float zc = zc0 - asum;
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) y[rt][rr] += zc * S[rr];
+    }
+  }
+  float* out = a.out + int64_t(blockIdx.y) * T * R;
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+    const int64_t r = rbase + 32 * rt + tok;
+    if (r >= R) continue;
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      const int t = 4 * hk + rr;
+      if (t < T) out[int64_t(t) * R + r] = y[rt][rr];
+    }
+  }
+}
+
 // Y[t][r] = sum over slabs of the partial rows, slabs in ascending order.
 __global__ __launch_bounds__(256) void bcq_reduce_kernel(const float* __restrict__ part, float* __restrict__ Y,
                                                          int64_t n, int slabs) {
@@ -310,6 +416,13 @@ static void launch_mm_t(const BcqArgs& a, int T, dim3 grid, hipStream_t st) {
   }
 }
 
+template <int K>
+static void launch_mfma_q(const BcqArgs& a, int T, dim3 grid, hipStream_t st) {
+  if (a.qps == 4) hipLaunchKernelGGL((bcq_mfma_kernel<K, 4>), grid, dim3(256), 0, st, a, T);
+  else if (a.qps == 2) hipLaunchKernelGGL((bcq_mfma_kernel<K, 2>), grid, dim3(256), 0, st, a, T);
+  else hipLaunchKernelGGL((bcq_mfma_kernel<K, 1>), grid, dim3(256), 0, st, a, T);
+}
+
 hipError_t launch_bcq_matmul(const BcqMatmulLaunch& p, hipStream_t st) {
   BcqArgs a;
   a.X = p.X;
@@ -325,11 +438,23 @@ hipError_t launch_bcq_matmul(const BcqMatmulLaunch& p, hipStream_t st) {
   const int64_t slabs = (a.nq + a.qps - 1) / a.qps;
   a.out = slabs == 1 ? p.Y : p.partials;
   const dim3 grid(unsigned((p.R + 255) / 256), unsigned(slabs));
-  switch (p.k) {
-    case 1: launch_mm_t<1>(a, p.T, grid, st); break;
-    case 2: launch_mm_t<2>(a, p.T, grid, st); break;
-    case 3: launch_mm_t<3>(a, p.T, grid, st); break;
-    default: launch_mm_t<4>(a, p.T, grid, st); break;
+  // tables for one to three batch rows, MFMA from four on (measured on the
+  // 70B and 4096 x 4096 layers: equal at four rows with k = 2, the MFMA form
+  // 1.9-2.2x faster at eight)
+  if (p.T >= 4) {
+    switch (p.k) {
+      case 1: launch_mfma_q<1>(a, p.T, grid, st); break;
+      case 2: launch_mfma_q<2>(a, p.T, grid, st); break;
+      case 3: launch_mfma_q<3>(a, p.T, grid, st); break;
+      default: launch_mfma_q<4>(a, p.T, grid, st); break;
+    }
+  } else {
+    switch (p.k) {
+      case 1: launch_mm_t<1>(a, p.T, grid, st); break;
+      case 2: launch_mm_t<2>(a, p.T, grid, st); break;
+      case 3: launch_mm_t<3>(a, p.T, grid, st); break;
+      default: launch_mm_t<4>(a, p.T, grid, st); break;
+    }
   }
   if (slabs > 1) {
     const int64_t n = int64_t(p.T) * p.R;

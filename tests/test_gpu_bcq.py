@@ -91,9 +91,10 @@ def test_pack_bit_exact(R, C, k, g):
 
 
 # shapes: one slab (no partial sums), ragged rows (partial row blocks),
-# groups of 256 and of a whole row, 1 to 8 batch rows
+# groups of 256 and of a whole row, 1 to 8 batch rows (tables up to 3, MFMA from 4)
 @pytest.mark.parametrize("T,R,C,k,g", [(1, 256, 512, 3, 128), (8, 300, 384, 4, 128), (3, 1000, 1280, 2, 256),
-                                       (5, 64, 128, 1, 128), (2, 513, 2560, 4, 2560), (7, 4000, 1152, 3, 128)])
+                                       (5, 64, 128, 1, 128), (2, 513, 2560, 4, 2560), (7, 4000, 1152, 3, 128),
+                                       (4, 1000, 1280, 3, 256), (6, 513, 2560, 2, 2560)])
 def test_matmul(T, R, C, k, g):
     codes, a, z, X = inputs(T, R, C, k, g, T + R + C)
     st = gpu_pack(codes, a, z, k, g)
@@ -115,13 +116,15 @@ def sampled(T, R, C, k, g, seed, n_rows):
 
 
 def test_matmul_wide_tables():
-    """8 batch rows and 4 quads per slab: 65.7 KB of tables per workgroup."""
+    """8 batch rows and 4 quads per slab (the MFMA form)."""
     sampled(8, 8192, 8192, 4, 128, 21, 64)
 
 
-def test_matmul_partial_last_slab():
-    """33 column quads at 2 per slab: the last slab holds one quad."""
-    sampled(3, 8192, 4224, 3, 128, 25, 48)
+@pytest.mark.parametrize("T", [3, 6])
+def test_matmul_partial_last_slab(T):
+    """33 column quads at 2 per slab: the last slab holds one quad (table
+    form at 3 batch rows, MFMA form at 6)."""
+    sampled(T, 8192, 4224, 3, 128, 25, 48)
 
 
 def test_matmul_full_size_attn4096():
