@@ -281,15 +281,27 @@ template <int K, int QPS, int RT = 2>
 __global__ __launch_bounds__(256) void bcq_mfma_kernel(BcqArgs a, int T) {
   // the 256 bytes as 8 bf16 each, built once: one LDS read per 8 bits
   __shared__ u32x4 tbl[256];
+  // the slab's activations, T rows of QPS * 128 bf16 with a 32-byte pad
+  // (the 16 fragments a k-step reads fall in distinct bank groups)
+  constexpr int XLD = QPS * 128 + 16;
+  __shared__ __attribute__((aligned(16))) uint16_t xs[8 * XLD];
   tbl[threadIdx.x] = __builtin_bit_cast(u32x4, bits_bf16(threadIdx.x));
+  const int64_t q0 = int64_t(blockIdx.y) * QPS;
+  const int nqs = int(min<int64_t>(QPS, a.nq - q0));
+  {
+    const int per_row = nqs * 32;  // 8-byte chunks per activation row
+    for (int e = threadIdx.x; e < T * per_row; e += 256) {
+      const int t = e / per_row, c = e - t * per_row;
+      *reinterpret_cast<uint2*>(&xs[t * XLD + 4 * c]) =
+          *reinterpret_cast<const uint2*>(a.X + int64_t(t) * a.C + q0 * 128 + 4 * c);
+    }
+  }
   __syncthreads();
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int tok = lane & 31, hk = lane >> 5;
-  const int64_t q0 = int64_t(blockIdx.y) * QPS;
-  const int nqs = int(min<int64_t>(QPS, a.nq - q0));
   const int64_t R = a.R;
   const int64_t rbase = int64_t(blockIdx.x) * (128 * RT) + wave * (32 * RT);
-  const int64_t pstride = a.nq * R, astride = a.gpr * R;
+  const int64_t astride = a.gpr * R;
   const uint32_t qpg = uint32_t(a.g) >> 7;
   bf16x8b ones;
 #pragma unroll
@@ -302,14 +314,14 @@ __global__ __launch_bounds__(256) void bcq_mfma_kernel(BcqArgs a, int T) {
   for (int qq = 0; qq < nqs; ++qq) {
     const int64_t q = q0 + qq;
     const int64_t j = int64_t(uint32_t(q) / qpg);
-    // this lane's activations for the quad's 8 k-steps (two 8-byte loads each)
+    // this lane's activations for the quad's 8 k-steps (zero past T)
     bf16x8b xa[8];
-    const uint2* xr = reinterpret_cast<const uint2*>(a.X + int64_t(min(tok, T - 1)) * a.C + q * 128 + 8 * hk);
+    const u32x4* xr = reinterpret_cast<const u32x4*>(&xs[min(tok, T - 1) * XLD + qq * 128 + 8 * hk]);
 #pragma unroll
     for (int st = 0; st < 8; ++st) {
-      const uint2 lo = xr[4 * st], hi = xr[4 * st + 1];
-      const u32x4 v = {tok < T ? lo.x : 0u, tok < T ? lo.y : 0u, tok < T ? hi.x : 0u, tok < T ? hi.y : 0u};
-      xa[st] = __builtin_bit_cast(bf16x8b, v);
+      const u32x4 v = xr[2 * st];
+      const u32x4 z4 = {0u, 0u, 0u, 0u};
+      xa[st] = __builtin_bit_cast(bf16x8b, tok < T ? v : z4);
     }
     f32x16b S = {};
 #pragma unroll
