@@ -329,3 +329,14 @@ def test_decoder_entry_validation(L):
     assert ws >= 1
     assert L.uniquan_block_loss(16, FAKE, FAKE, FAKE, FAKE, FAKE, ws - 1, FAKE, None) == uq.UQ_EINVAL
     assert L.uniquan_block_loss(0, FAKE, FAKE, FAKE, FAKE, FAKE, ws, FAKE, None) == uq.UQ_EINVAL
+
+
+def test_bench_refuses_several_gpus():
+    """bench.py measures one GPU: --gpus N > 1 exits (status 2) with a
+    message, before touching a device."""
+    import sys as _sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([_sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120, cwd=root)
+    assert r.returncode == 2
+    assert "one GPU only" in r.stderr and r.stdout == ""
