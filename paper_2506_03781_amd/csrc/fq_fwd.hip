@@ -835,6 +835,143 @@ __global__ __launch_bounds__(kBigThreads) void fq_fwd_big_kernel(BigArgs a) {
   }
 }
 
+// The fused step for one large group (g up to 16384): the straight-through
+// backward with the SGD update (fq_bwd_big_kernel's arithmetic and order:
+// each lane's chunks c = lane, lane + 256, ..., the fixed xor butterfly, the
+// four wavefront sums pairwise), then the forward of the next step with the
+// updated s, alpha, z_B (fq_fwd_big_kernel's, bit for bit).  A lane keeps
+// its chunks' W, updated s and code bytes in registers between the two
+// halves, so each weight's W, s, dL/dWhat and code are read once.
+constexpr int kStepBigChunks = 8;  // chunks per lane: g <= 256 * 8 * 8
+
+template <int WDT, int GDT, int ODT, int MODE, int LOGL>
+__global__ __launch_bounds__(kBigThreads) void fq_step_big_kernel(BigArgs a, const void* __restrict__ G, float lr_f,
+                                                                  float lr_b) {
+  constexpr int L = 1 << LOGL, K = LOGL, CPT = kStepBigChunks;
+  __shared__ float raw[L], qs[L];
+  __shared__ uint8_t code_of[L], pos_of[L];
+  __shared__ float4 nb[MODE == 3 ? L : 1];
+  __shared__ float red[4][K + 1];
+  __shared__ float par[K + 1];  // alpha', z_B'
+  const int64_t gid = blockIdx.x;
+  const float dl = a.delta ? a.delta[gid] : 1.0f;
+  const float sr = a.s_r ? a.s_r[gid / a.gpr] : 1.0f;
+  const float zu = a.z_u ? a.z_u[gid] : 0.0f;
+  const float ds = dl * sr;
+  const int nch = a.g >> 3;
+  const int64_t base = gid * a.g;
+  float* s_io = const_cast<float*>(a.s);
+
+  // backward with the update of s; this lane's group sums
+  Raw8<WDT> w[CPT];
+  float sv[CPT][8];
+  uint2 cb[CPT];
+  float S = 0.0f, Sa[K];
+#pragma unroll
+  for (int b = 0; b < K; ++b) Sa[b] = 0.0f;
+#pragma unroll
+  for (int u = 0; u < CPT; ++u) {
+    const int c = int(threadIdx.x) + u * kBigThreads;
+    cb[u] = make_uint2(0u, 0u);
+    if (c < nch) {
+      const int64_t off = base + int64_t(c) * kVec;
+      w[u].load(a.W, off);
+      load8f(a.s, off, sv[u]);
+      float gv[8];
+      load8<GDT>(G, off, gv);
+      cb[u] = load8u8(a.codes, off);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const uint32_t byte = byte_of(cb[u], i);
+        const bool m = (byte & 0x80u) != 0u;
+        const float gg = gv[i];
+        S += gg;
+#pragma unroll
+        for (int b = 0; b < K; ++b) Sa[b] += ((byte >> b) & 1u) ? gg : -gg;
+        const float x = w[u].get(i) * __builtin_amdgcn_rcpf(ds * sv[u][i]);
+        const float gs = m ? -(dl * gg) * x * __builtin_amdgcn_rcpf(sv[u][i]) : 0.0f;
+        sv[u][i] = sv[u][i] - lr_f * gs;
+      }
+      store8f(s_io, off, sv[u]);
+    }
+  }
+  for (int msk = 32; msk >= 1; msk >>= 1) {
+    S += __shfl_xor(S, msk, 64);
+#pragma unroll
+    for (int b = 0; b < K; ++b) Sa[b] += __shfl_xor(Sa[b], msk, 64);
+  }
+  const int wave = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    red[wave][0] = S;
+#pragma unroll
+    for (int b = 0; b < K; ++b) red[wave][1 + b] = Sa[b];
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    auto sum4 = [&](int j) { return (red[0][j] + red[1][j]) + (red[2][j] + red[3][j]); };
+    float* alpha = const_cast<float*>(a.alpha) + gid * K;
+    float* z_b = const_cast<float*>(a.z_b);
+#pragma unroll
+    for (int b = 0; b < K; ++b) {
+      const float an = alpha[b] - lr_b * (dl * sum4(1 + b));
+      alpha[b] = an;
+      par[b] = an;
+    }
+    const float zn = z_b[gid] - lr_b * (dl * sum4(0));
+    z_b[gid] = zn;
+    par[K] = zn;
+  }
+  __syncthreads();
+
+  // forward of the next step on the updated parameters
+  if (threadIdx.x < L) raw[threadIdx.x] = level_value_k<LOGL>(par, par[K], threadIdx.x);
+  __syncthreads();
+  if constexpr (MODE != 2) big_sort<LOGL, MODE == 3>(raw, qs, code_of, pos_of, nb);
+  const float tau = tau_k<LOGL>(par);
+#pragma unroll
+  for (int u = 0; u < CPT; ++u) {
+    const int c = int(threadIdx.x) + u * kBigThreads;
+    if (c >= nch) break;
+    const int64_t off = base + int64_t(c) * kVec;
+    float out[8];
+    uint32_t cw[2] = {0u, 0u};
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float den = ds * sv[u][i];
+      const float wb = w[u].get(i) / den + zu;
+      float d, wt;
+      uint32_t code;
+      if constexpr (MODE == 0) {
+        const int jj = nearest_full_k<LOGL>(qs, wb, d);
+        wt = qs[jj];
+        code = code_of[jj];
+      } else if constexpr (MODE == 2) {
+        code = byte_of(cb[u], i) & uint32_t(L - 1);
+        wt = raw[code];
+        d = fabsf(wb - wt);
+      } else {
+        const float4 e4 = nb[byte_of(cb[u], i) & uint32_t(L - 1)];
+        const uint32_t cs = __float_as_uint(e4.w);
+        float bd = fabsf(wb - e4.x);
+        wt = e4.x;
+        uint32_t sh = 0;
+        const float dm = fabsf(wb - e4.y);
+        if (dm < bd) { bd = dm; wt = e4.y; sh = 8; }
+        const float dr = fabsf(wb - e4.z);
+        if (dr < bd) { bd = dr; wt = e4.z; sh = 16; }
+        d = bd;
+        code = (cs >> sh) & 0xFFu;
+      }
+      const uint32_t byte = code | (d > tau ? 0u : 0x80u);
+      cw[i >> 2] |= byte << (8 * (i & 3));
+      out[i] = dl * (wt - zu);
+      if (a.resid) out[i] = out[i] - w[u].get(i);
+    }
+    store8<ODT>(a.W_hat, off, out);
+    store8u8(a.codes, off, make_uint2(cw[0], cw[1]));
+  }
+}
+
 // Fold of one large group: alpha* = Delta alpha, z* = Delta (z_B - z_U), and
 // the codes of the FULL mapping of wbar (code_src 0) or of the raw w against
 // the folded levels (code_src 1), as fold_kernel computes them.
@@ -1143,9 +1280,38 @@ static hipError_t launch_step_d(const StepArgs& a, int k, int mode, hipStream_t 
   return hipErrorNotSupported;  // LOCAL without a neighbour table: the caller runs the two passes
 }
 
+template <int ODT, int MD>
+static hipError_t launch_step_big(const BigArgs& a, const void* G, float lr_f, float lr_b, hipStream_t st) {
+  const dim3 grid(unsigned(a.Gn)), block(kBigThreads);
+  switch (a.k) {
+#define UQ_SB(KK) \
+    case KK: hipLaunchKernelGGL((fq_step_big_kernel<BF16, BF16, ODT, MD, KK>), grid, block, 0, st, a, G, lr_f, lr_b); break;
+    UQ_SB(1) UQ_SB(2) UQ_SB(3) UQ_SB(4) UQ_SB(5) UQ_SB(6) UQ_SB(7)
+#undef UQ_SB
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 // Fused pass for g <= 512 (whose neighbour tables fit when the next mapping is
-// LOCAL); otherwise the backward with the update, then the forward.
+// LOCAL) and, with bf16 W and dL/dWhat, for large groups up to 16384 weights
+// (one workgroup per group); otherwise the backward with the update, then
+// the forward.
 hipError_t launch_fq_step(const FqStepLaunch& p, hipStream_t st) {
+  if (p.g > 512 && p.g <= kBigThreads * kVec * kStepBigChunks && p.w_dtype == BF16 && p.grad_dtype == BF16) {
+    BigArgs b = big_args(p.R, p.C, p.k, p.g);
+    b.W = p.W; b.s = p.s; b.s_r = p.s_r; b.delta = p.delta; b.z_u = p.z_u;
+    b.alpha = p.alpha; b.z_b = p.z_b; b.codes = p.codes; b.W_hat = p.W_hat; b.resid = p.resid;
+    const int md = p.mode == 0 ? 0 : p.mode == 2 ? 2 : 3;
+    if (p.w_hat_dtype == BF16) {
+      if (md == 0) return launch_step_big<BF16, 0>(b, p.grad_W_hat, p.lr_f, p.lr_b, st);
+      if (md == 2) return launch_step_big<BF16, 2>(b, p.grad_W_hat, p.lr_f, p.lr_b, st);
+      return launch_step_big<BF16, 3>(b, p.grad_W_hat, p.lr_f, p.lr_b, st);
+    }
+    if (md == 0) return launch_step_big<F32, 0>(b, p.grad_W_hat, p.lr_f, p.lr_b, st);
+    if (md == 2) return launch_step_big<F32, 2>(b, p.grad_W_hat, p.lr_f, p.lr_b, st);
+    return launch_step_big<F32, 3>(b, p.grad_W_hat, p.lr_f, p.lr_b, st);
+  }
   const bool fused = p.g <= 512 && !(p.mode == 1 && !use_neighbour_table(__builtin_ctz(unsigned(p.g)), p.k));
   if (fused) {
     StepArgs a;

@@ -131,3 +131,23 @@ def test_step_full_size_7b_gate(mode):
     G = synth.round_to_bf16((0.01 * np.random.default_rng(6).standard_normal(m.W.shape)).astype(F32))
     a, b = _run_pair(m, p, k, g, prev, G, mode, True, torch.bfloat16, torch.bfloat16, torch.bfloat16)
     _assert_same(a, b, "7B gate")
+
+
+@pytest.mark.parametrize("mode", [uq.MAP_FULL, uq.MAP_LOCAL, uq.MAP_FROZEN])
+@pytest.mark.parametrize("k,R,C,g", [(2, 6, 11008, 11008), (3, 12, 8192, 4096), (4, 10, 2064, 1032),
+                                     (7, 4, 4096, 4096), (3, 3, 16384, 16384)])
+@pytest.mark.parametrize("resid", [False, True])
+def test_step_equals_two_passes_row_groups(mode, k, R, C, g, resid):
+    """Groups of whole rows (one workgroup per group, every lane holding up
+    to 8 chunks between the backward and the forward): the fused pass equals
+    the backward with the update followed by the forward, bit for bit, at
+    the 7B row lengths, a ragged chunk count (1032 = 129 chunks) and the
+    largest group the fused pass takes (16384); fp32 What once."""
+    m = P.small_matrix(R, C, 300 + k + g)
+    p = P.params(m.W, m.s, k, g, "B")
+    p["s_r"] = synth.perturb(p["s_r"], 0.01, k, 29)
+    f0 = O.fq_fwd(m.W, m.s, p["alpha"], p["z_b"], k, g, p["s_r"], p["delta"], p["z_u"])
+    G = synth.round_to_bf16(np.random.default_rng(k + g).standard_normal(m.W.shape).astype(F32))
+    odt = torch.float32 if (k == 3 and g == 4096) else torch.bfloat16
+    a, b = _run_pair(m, p, k, g, f0["codes"], G, mode, resid, torch.bfloat16, torch.bfloat16, odt)
+    _assert_same(a, b, f"k={k} g={g} mode={mode}")
