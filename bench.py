@@ -178,8 +178,10 @@ def fq_step_bytes_per_weight(k, g, w_bytes=2, what_bytes=2, grad_bytes=2):
     """Algorithmic bytes per weight of uniquan_fq_step (backward + SGD of one
     step, forward of the next), as (read, written).  One pass for g <= 512:
     dL/dWhat, W, s, code in; s, What, code out; per group Delta, z_U, s_r,
-    alpha, z_B in and alpha, z_B out.  Larger groups run the two passes."""
-    if g > 512:
+    alpha, z_B in and alpha, z_B out.  Groups of 513 to 16384 bf16 weights
+    (bf16 dL/dWhat) take one pass too, one workgroup per group; other large
+    groups run the two passes."""
+    if g > 512 and (g > 16384 or w_bytes != 2 or grad_bytes != 2):
         return fq_read_write_bytes(k, g, "local", w_bytes, what_bytes, grad_bytes)
     rd = grad_bytes + w_bytes + 4 + 1 + (4 * k + 12) / g
     wr = 4 + what_bytes + 1 + (4 * k + 4) / g
