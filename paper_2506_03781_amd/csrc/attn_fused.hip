@@ -276,9 +276,12 @@ __device__ __forceinline__ void copy_tile(const uint16_t* base, const uint32_t (
 
 // Forward: one workgroup of NW waves per (NW * 32 queries, query batch); wave
 // w owns 32 queries and multiplies the key tiles up to its diagonal (the
-// workgroup copies the tiles up to its last diagonal).
+// workgroup copies the tiles up to its last diagonal).  Key and value
+// fragments go from LDS straight into their MFMAs rather than into arrays
+// held across the tile: 156 registers, so three waves share a SIMD and one
+// wave's exponentials overlap another's products (two waves per SIMD at 243).
 template <int NW, int S, bool TOK>
-__global__ __launch_bounds__(NW * 64) void attn_fwd_kernel(AttnArgs a) {
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(3))) void attn_fwd_kernel(AttnArgs a) {
   constexpr int QB = NW * NB;
   constexpr int PW = 8 / NW;  // copy blocks per wave and tile
   constexpr int STAGE = 2 * TILE16;  // key tile, value tile
@@ -321,12 +324,9 @@ __global__ __launch_bounds__(NW * 64) void attn_fwd_kernel(AttnArgs a) {
     }
     if (t >= my_tiles) continue;
     const u32x4a* tk = smem + (t % S) * STAGE;
-    bf16x8a kf[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) kf[j] = row_frag(tk, j, lane);
     f32x16a s = zero16();
 #pragma unroll
-    for (int j = 0; j < 8; ++j) s = mfma(kf[j], qf[j], s);
+    for (int j = 0; j < 8; ++j) s = mfma(row_frag(tk, j, lane), qf[j], s);
     if (t == my_tiles - 1) {
 #pragma unroll
       for (int r = 0; r < 16; ++r)
@@ -374,15 +374,9 @@ __global__ __launch_bounds__(NW * 64) void attn_fwd_kernel(AttnArgs a) {
     if (t >= my_tiles) continue;
     const u32x4a* tk = smem + (t % S) * STAGE;
     const u32x4a* tv = tk + TILE16;
-    bf16x8a kf[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) kf[j] = row_frag(tk, j, lane);
     f32x16a s = zero16();
 #pragma unroll
-    for (int j = 0; j < 8; ++j) s = mfma(kf[j], qf[j], s);
-    bf16x8a vf[8];  // read while P is formed
-#pragma unroll
-    for (int i = 0; i < 8; ++i) vf[i] = col_frag(tv, i & 3, i >> 2, lane);
+    for (int j = 0; j < 8; ++j) s = mfma(row_frag(tk, j, lane), qf[j], s);
     float p[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) p[r] = exp2a(fmaf(s[r], c, -lse));
@@ -395,7 +389,7 @@ __global__ __launch_bounds__(NW * 64) void attn_fwd_kernel(AttnArgs a) {
     for (int h = 0; h < 2; ++h) {
       const bf16x8a pb = pack_half(p, h);
 #pragma unroll
-      for (int db = 0; db < 4; ++db) o[db] = mfma(vf[4 * h + db], pb, o[db]);
+      for (int db = 0; db < 4; ++db) o[db] = mfma(col_frag(tv, db, h, lane), pb, o[db]);
     }
   }
   if (!active) return;
