@@ -207,7 +207,9 @@ uq_status uniquan_fq_bwd_sgd(int64_t R, int64_t C, int k, int g,
  * dL/dWhat, W, s and the code byte once (9 B with bf16 W and dL/dWhat) and
  * writes s, W_hat and the code byte (7 B), against 23 B for the two passes.
  * Runs as one kernel for g <= 512 (LOCAL mapping: where the neighbour table
- * fits, i.e. (512 / g) 2^k <= 4096); otherwise as the two calls.  Arguments
+ * fits, i.e. (512 / g) 2^k <= 4096) and, with bf16 W and dL/dWhat, for
+ * groups of 513 to 16384 weights (one workgroup per group, every mapping);
+ * otherwise as the two calls.  Arguments
  * and errors as for those calls; the gradient outputs are not stored.
  */
 uq_status uniquan_fq_step(int64_t R, int64_t C, int k, int g,
