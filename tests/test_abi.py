@@ -340,3 +340,21 @@ def test_bench_refuses_several_gpus():
                        text=True, timeout=120, cwd=root)
     assert r.returncode == 2
     assert "one GPU only" in r.stderr and r.stdout == ""
+
+
+def test_bench_step_bytes_follow_the_step_kernels():
+    """The algorithmic bytes bench.py charges uniquan_fq_step: one pass (read
+    dL/dWhat, W, s, code; write s, What, code) for g <= 512 and for bf16
+    groups of 513 to 16384 weights, the two passes' sum otherwise."""
+    import importlib.util
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    spec = importlib.util.spec_from_file_location("bench_mod", os.path.join(root, "bench.py"))
+    b = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(b)
+    k = 3
+    for g in (128, 4096, 11008, 16384):
+        rd, wr = b.fq_step_bytes_per_weight(k, g)
+        assert abs(rd - (2 + 2 + 4 + 1 + (4 * k + 12) / g)) < 1e-12
+        assert abs(wr - (4 + 2 + 1 + (4 * k + 4) / g)) < 1e-12
+    for g, wb in ((16392, 2), (4096, 4)):
+        assert b.fq_step_bytes_per_weight(k, g, wb) == b.fq_read_write_bytes(k, g, "local", wb)
