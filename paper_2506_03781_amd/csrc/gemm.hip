@@ -134,8 +134,9 @@ __device__ __forceinline__ void heads_strip(const GemmArgs& p, const float* stri
 // workgroup i to XCD i % 8; renumber so that each XCD receives a contiguous
 // run of logical tiles, then walk logical tiles in groups of GM row-tiles.
 // An XCD's run of tiles then covers GM row-tiles and (run / GM) column-tiles,
-// whose operand panels it pulls into its L2: GM balances the two panel sizes
-// (BM and BN rows of K), 4 for 256 x 128 tiles, 8 otherwise.
+// whose operand panels it pulls into its L2.  GM = 4 for 256-row tiles: on
+// 256 x 256 tiles it beat 1, 2, 3 (by 1-10%), 8 and 16 (by 5-11%) on the 70B
+// and 7B products and matched 5 and 6; 8 for 128 x 128 tiles.
 template <int GM>
 __device__ __forceinline__ void tile_of(int bid, int nb, int tiles_m, int tiles_n, int& tm, int& tn) {
   int logical = bid;
@@ -493,7 +494,7 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs p) {
   const int wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   int tm, tn;
-  tile_of<(BM == 256 && BN == 128) ? 4 : 8>(blockIdx.x, gridDim.x, p.tiles_m, p.tiles_n, tm, tn);
+  tile_of<(BM == 128 && BN == 128) ? 8 : 4>(blockIdx.x, gridDim.x, p.tiles_m, p.tiles_n, tm, tn);
   const int64_t m0 = int64_t(tm) * BM, n0 = int64_t(tn) * BN;
   const int64_t K = p.K;
 
@@ -636,7 +637,7 @@ __global__ __launch_bounds__(256) void gemm_pipe_kernel(GemmArgs p) {
   const int wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   int tm, tn;
-  tile_of<(BM == 256 && BN == 128) ? 4 : 8>(blockIdx.x, gridDim.x, p.tiles_m, p.tiles_n, tm, tn);
+  tile_of<(BM == 128 && BN == 128) ? 8 : 4>(blockIdx.x, gridDim.x, p.tiles_m, p.tiles_n, tm, tn);
   const int64_t m0 = int64_t(tm) * BM, n0 = int64_t(tn) * BN;
   const int64_t K = p.K;
   if (p.causal == 1 && n0 >= m0 + BM) return;  // whole tile above the diagonal (uniform per workgroup)
@@ -860,7 +861,7 @@ __global__ __launch_bounds__(512) void gemm_pp_kernel(GemmArgs p) {
   const int wm = WAVES_M == 2 ? (qw >> 1) : qw;
   const int wn = WAVES_M == 2 ? ((qw & 1) * 2 + grp) : grp;
   int tm, tn;
-  tile_of<(BM == 256 && BN == 128) ? 4 : 8>(blockIdx.x, gridDim.x, p.tiles_m, p.tiles_n, tm, tn);
+  tile_of<(BM == 128 && BN == 128) ? 8 : 4>(blockIdx.x, gridDim.x, p.tiles_m, p.tiles_n, tm, tn);
   const int64_t m0 = int64_t(tm) * BM, n0 = int64_t(tn) * BN;
   const int64_t K = p.K;
   // causal structure (uniform per workgroup, before any barrier)
